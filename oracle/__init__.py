@@ -1,0 +1,119 @@
+"""CPU oracle of the phrase-memory lookup + gated residual injection.
+
+TEST INFRASTRUCTURE ONLY: the tests, the smoke check and the benchmark's
+CPU-baseline leg may import this package; the product path never does.  The
+arithmetic lives in ``oracle.cpp`` (std::map on token tuples, scalar double
+loops); this file only marshals numpy arrays.  ``lru.py`` is the reference
+model of the HBM cache tier's replacement policy.
+"""
+import ctypes
+import os
+
+import numpy as np
+
+from . import _build
+
+OK, INVALID, DUPLICATE = 0, -1, -2
+GATE_SIGMOID, GATE_CONST = 0, 1
+EPS = 1e-6
+
+_lib = None
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_build.SO):
+            _build.build()
+        L = ctypes.CDLL(_build.SO)
+        vp, i64 = ctypes.c_void_p, ctypes.c_int64
+        L.oracle_table_new.argtypes = [vp, vp, i64, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                                       ctypes.POINTER(ctypes.c_int)]
+        L.oracle_table_new.restype = vp
+        L.oracle_table_free.argtypes = [vp]
+        L.oracle_table_free.restype = None
+        L.oracle_lookup.argtypes = [vp, vp, i64, i64, i64, vp, vp, vp]
+        L.oracle_inject.argtypes = [vp, vp, i64, vp, i64, i64, ctypes.c_int, ctypes.c_int,
+                                    ctypes.c_double, vp]
+        L.oracle_gate.argtypes = [vp, vp, i64, ctypes.c_int, ctypes.c_int, ctypes.c_double]
+        L.oracle_gate.restype = ctypes.c_double
+        L.oracle_round_bf16.argtypes = [ctypes.c_double]
+        L.oracle_round_bf16.restype = ctypes.c_uint16
+        _lib = L
+    return _lib
+
+
+def _p(a):
+    return ctypes.c_void_p(a.ctypes.data)
+
+
+class OracleError(Exception):
+    def __init__(self, status):
+        super().__init__("oracle status %d" % status)
+        self.status = status
+
+
+class Table:
+    """phrase tuple -> row map.  tokens: int32 [P x n_max] (oldest first,
+    padded), lens: uint8 [P]."""
+
+    def __init__(self, tokens, lens, n_min, n_max, vocab):
+        self.tokens = np.ascontiguousarray(tokens, np.int32).reshape(-1, n_max)
+        self.lens = np.ascontiguousarray(lens, np.uint8)
+        st = ctypes.c_int(0)
+        self._h = lib().oracle_table_new(_p(self.tokens), _p(self.lens), self.lens.size, n_min,
+                                         n_max, vocab, ctypes.byref(st))
+        if not self._h:
+            raise OracleError(st.value)
+
+    def __del__(self):
+        if getattr(self, "_h", None):
+            lib().oracle_table_free(self._h)
+            self._h = None
+
+    def lookup(self, tokens, ctx, S):
+        """tokens: int32 [B x (ctx+S)] -> (hit uint8, row int32, len uint8), each [B*S]."""
+        tokens = np.ascontiguousarray(tokens, np.int32)
+        B = tokens.shape[0]
+        assert tokens.shape[1] == ctx + S
+        hit = np.empty(B * S, np.uint8)
+        row = np.empty(B * S, np.int32)
+        ln = np.empty(B * S, np.uint8)
+        st = lib().oracle_lookup(self._h, _p(tokens), B, ctx, S, _p(hit), _p(row), _p(ln))
+        if st != OK:
+            raise OracleError(st)
+        return hit, row, ln
+
+
+def inject(hidden, values, index, dtype, gate=GATE_SIGMOID, lam=1.0):
+    """hidden [T x D] (float32, or uint16 bf16 patterns), values [R x D] of the
+    same type, index int64 [T] (row of `values` or -1) -> out like hidden."""
+    hidden = np.ascontiguousarray(hidden)
+    values = np.ascontiguousarray(values)
+    index = np.ascontiguousarray(index, np.int64)
+    T, D = hidden.shape
+    out = np.empty_like(hidden)
+    R = values.shape[0] if values.ndim == 2 else 0
+    st = lib().oracle_inject(_p(hidden), _p(values) if R else None, R, _p(index), T, D, dtype,
+                             gate, float(lam), _p(out))
+    if st != OK:
+        raise OracleError(st)
+    return out
+
+
+def gate_value(h, m, dtype, gate=GATE_SIGMOID, lam=1.0):
+    h = np.ascontiguousarray(h)
+    m = np.ascontiguousarray(m)
+    return float(lib().oracle_gate(_p(h), _p(m), h.size, dtype, gate, float(lam)))
+
+
+def round_bf16(x):
+    return int(lib().oracle_round_bf16(float(x)))
+
+
+def lookup_inject(table, batch_tokens, ctx, S, hidden, values, dtype, gate=GATE_SIGMOID,
+                  lam=1.0):
+    """Whole path for small inputs where the full value matrix is at hand."""
+    hit, row, ln = table.lookup(batch_tokens, ctx, S)
+    out = inject(hidden, values, row.astype(np.int64), dtype, gate, lam)
+    return hit, row, ln, out

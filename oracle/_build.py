@@ -1,0 +1,19 @@
+"""Build the CPU oracle (plain C++, no OpenMP, no GPU) in-tree."""
+import os
+import subprocess
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+SO = os.path.join(HERE, "liboracle.so")
+
+
+def build():
+    cmd = ["g++", "-O2", "-fPIC", "-shared", "-std=c++17", "-Wall", "-o", SO + ".tmp",
+           os.path.join(HERE, "oracle.cpp")]
+    r = subprocess.run(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True)
+    if r.returncode != 0:
+        raise RuntimeError("oracle build failed:\n" + r.stdout)
+    os.replace(SO + ".tmp", SO)
+
+
+if __name__ == "__main__":
+    build()

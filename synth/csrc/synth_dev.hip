@@ -1,0 +1,40 @@
+// Seeded synthetic workload generator, device part (C ABI).
+//
+// Test and benchmark infrastructure only: fills device tables with the same
+// counter-based normal values that synth_host.cpp draws on the CPU (both
+// include synth_rng.h), so tables of many GiB never have to be drawn on the
+// host and copied.  None of the phrase-memory method lives here.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "synth_rng.h"
+
+// One thread per element of rows [row0, row0 + nrows); out points at row0.
+template <int DT>
+__global__ void k_normal_fill(void* __restrict__ out, int64_t row0, int64_t nrows, int64_t cols,
+                              uint64_t key, float scale) {
+  const int64_t n = nrows * cols;
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) {
+    const uint64_t e = (uint64_t)row0 * (uint64_t)cols + (uint64_t)i;
+    const float x = (float)synth_irwin_hall_n(key, e) * scale;
+    if (DT == 0) ((float*)out)[i] = x;
+    else ((uint16_t*)out)[i] = synth_f32_to_bf16(x);
+  }
+}
+
+extern "C" int synth_normal_fill_dev(void* out, int64_t row0, int64_t nrows, int64_t cols,
+                                     uint64_t key, float scale, int dtype, hipStream_t stream) {
+  if (!out || nrows < 0 || cols <= 0 || (dtype != 0 && dtype != 1)) return -1;
+  if (nrows == 0) return 0;
+  const int64_t n = nrows * cols;
+  int64_t blocks = (n + 255) / 256;
+  if (blocks > 1 << 20) blocks = 1 << 20;
+  if (dtype == 0)
+    hipLaunchKernelGGL(k_normal_fill<0>, dim3((unsigned)blocks), dim3(256), 0, stream, out, row0,
+                       nrows, cols, key, scale);
+  else
+    hipLaunchKernelGGL(k_normal_fill<1>, dim3((unsigned)blocks), dim3(256), 0, stream, out, row0,
+                       nrows, cols, key, scale);
+  return hipGetLastError() == hipSuccess ? 0 : -2;
+}

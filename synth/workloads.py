@@ -1,0 +1,138 @@
+"""The five synthetic workloads (seed of workload i is i - 1).
+
+1  tiny, fp32: one 64-token Zipf(1.1) sequence; a 4096-phrase 2/3-gram table
+   holding about half of the sequence's own distinct windows (each kept with
+   probability 1/2) plus uniformly random 2/3-gram tuples that are not windows
+   of the sequence; values N(0, 0.02) fp32, hidden N(0, 1) fp32.
+2  decode, bf16: 64 rows with a 3-token window (2 history + 1 injected);
+   table = the 2^19 most frequent 2-grams and the 2^19 most frequent 3-grams
+   of a 2^26-token Zipf(1.1) stream; values 2^20 x 1024 bf16 (2 GiB).
+3  prefill, bf16: 8 x 4096 positions; table = 2^21 2-grams, 2^20 3-grams and
+   2^20 4-grams of a 200M-token Zipf(1.1) stream ranked by count after the
+   STOP most frequent n-grams of each length are skipped (a stop-phrase
+   filter), which puts the hit rate in [0.30, 0.40]; values 8 GiB bf16.
+4  large table, decode at batch 256: 2^24 2-grams + 2^24 3-grams of a
+   Zipf(1.05) stream (2^25 phrases, 64 GiB bf16 values); Zipf(1.05) queries.
+5  tiered: 2^25 2-grams + 2^25 3-grams of a Zipf(1.1) stream (2^26 phrases,
+   128 GiB bf16 values in pinned host memory), decode at batch 64.
+"""
+import functools
+
+import numpy as np
+
+from . import (BF16, D, F32, TAG_CAND, TAG_HIDDEN, TAG_QUERY, TAG_STREAM, V, PhraseTable,
+               QueryBatch, ngram_top, stack_tables, zipf_tokens)
+
+__all__ = ["config1", "config2_table", "config3_table", "config4_table", "config5_table",
+           "decode_batch", "prefill_batch", "CONFIG3_STOP", "windows_of"]
+
+# Stop-phrase filter of workload 3: the number of most frequent 2-, 3- and
+# 4-grams skipped before the table's phrases are taken.
+CONFIG3_STOP = (6000, 6000, 6000)
+
+
+def windows_of(seq, n):
+    """Distinct n-gram windows of a 1-D token sequence, in order of first
+    appearance."""
+    seen, out = set(), []
+    for i in range(len(seq) - n + 1):
+        w = tuple(int(x) for x in seq[i:i + n])
+        if w not in seen:
+            seen.add(w)
+            out.append(w)
+    return out
+
+
+@functools.lru_cache(maxsize=None)
+def config1():
+    """Returns (table, batch) of workload 1."""
+    seed, P = 0, 4096
+    seq = zipf_tokens(seed, TAG_QUERY, 64, 1.1)
+    rng = np.random.default_rng([seed, TAG_STREAM])
+    own = {2: windows_of(seq, 2), 3: windows_of(seq, 3)}
+    own_set = set(own[2]) | set(own[3])
+    phrases = []
+    for n in (2, 3):
+        for w in own[n]:
+            if rng.random() < 0.5:
+                phrases.append(w)
+    chosen = set(phrases)
+    while len(phrases) < P:
+        n = int(rng.integers(2, 4))
+        w = tuple(int(x) for x in rng.integers(0, V, n))
+        if w in own_set or w in chosen:
+            continue
+        chosen.add(w)
+        phrases.append(w)
+    perm = rng.permutation(P)
+    toks = np.full((P, 3), -1, np.int32)
+    lens = np.zeros(P, np.uint8)
+    for r, i in enumerate(perm):
+        w = phrases[i]
+        toks[r, :len(w)] = w
+        lens[r] = len(w)
+    table = PhraseTable(toks, lens, 2, 3, F32, seed)
+    batch = QueryBatch(seq.reshape(1, 64).copy(), 0, 64, seed, TAG_HIDDEN, F32)
+    return table, batch
+
+
+def _freq_table(seed, s, stream_len, per_n, stop=None):
+    stream = zipf_tokens(seed, TAG_STREAM, stream_len, s)
+    parts = []
+    for j, (n, want) in enumerate(per_n):
+        skip = 0 if stop is None else stop[j]
+        parts.append(ngram_top(stream, n, want, skip=skip))
+    del stream
+    n_max = max(n for n, _ in per_n)
+    toks, lens, _ = stack_tables(parts, n_max)
+    return toks, lens
+
+
+@functools.lru_cache(maxsize=None)
+def config2_table():
+    toks, lens = _freq_table(1, 1.1, 1 << 26, [(2, 1 << 19), (3, 1 << 19)])
+    return PhraseTable(toks, lens, 2, 3, BF16, 1)
+
+
+@functools.lru_cache(maxsize=None)
+def config3_table():
+    toks, lens = _freq_table(2, 1.1, 200_000_000, [(2, 1 << 21), (3, 1 << 20), (4, 1 << 20)],
+                             stop=CONFIG3_STOP)
+    return PhraseTable(toks, lens, 2, 4, BF16, 2)
+
+
+@functools.lru_cache(maxsize=None)
+def config4_table():
+    toks, lens = _freq_table(3, 1.05, 1 << 28, [(2, 1 << 24), (3, 1 << 24)])
+    return PhraseTable(toks, lens, 2, 3, BF16, 3)
+
+
+@functools.lru_cache(maxsize=None)
+def config5_table():
+    toks, lens = _freq_table(4, 1.1, 3 << 27, [(2, 1 << 25), (3, 1 << 25)])
+    return PhraseTable(toks, lens, 2, 3, BF16, 4)
+
+
+def decode_batch(seed, B, s=1.1, window=3, set_index=0, dtype=BF16):
+    """B decode rows, each a window of `window` Zipf(s) tokens whose last
+    token is the injected position (ctx = window - 1, S = 1)."""
+    tok = zipf_tokens(seed, TAG_QUERY + 16 * set_index, B * window, s).reshape(B, window)
+    return QueryBatch(tok, window - 1, 1, seed, TAG_HIDDEN + 16 * set_index, dtype)
+
+
+def prefill_batch(seed, B, S, s=1.1, set_index=0, dtype=BF16):
+    tok = zipf_tokens(seed, TAG_QUERY + 16 * set_index, B * S, s).reshape(B, S)
+    return QueryBatch(tok, 0, S, seed, TAG_HIDDEN + 16 * set_index, dtype)
+
+
+def candidates(seed, B, K, true_next, s=1.1, p_true=0.7, step=0):
+    """K predicted next-token candidates per row: the true next token sits at
+    a random position with probability p_true, the other entries are Zipf(s)
+    draws (workload 5)."""
+    rng = np.random.default_rng([seed, TAG_CAND, step])
+    c = zipf_tokens(seed, TAG_CAND + 16 * (step + 1), B * K, s).reshape(B, K)
+    put = rng.random(B) < p_true
+    pos = rng.integers(0, K, B)
+    rows = np.flatnonzero(put)
+    c[rows, pos[rows]] = true_next[rows]
+    return c
