@@ -1,0 +1,212 @@
+"""Benchmark of the phrase-memory lookup + inject path on one MI355X.
+
+Default workload (batch-64 decode against the 2^20-phrase bf16 table):
+a step is one tfe_lookup_inject call over R = 256 independent batch-64 decode
+steps stacked into one launch (16384 rows, each with its own 3-token window
+and hidden row), i.e. one pass of key formation, probe, gather and gated
+injection over one batch of synthetic input.  Eight input sets (tokens,
+hidden in, hidden out) rotate so more than 512 MB are touched between reuses
+of a set, which keeps the hidden rows out of the 256 MB last-level cache; the
+2 GiB value table is larger than that cache by itself.
+
+The JSON line also carries the latency mode (one batch-64 step per call), the
+roofline of the kernel (algorithmic bytes per launch over the average launch
+duration, measured with HIP events on the launch stream) and the CPU oracle
+timed on a bounded sample of the same workload.
+
+  python bench.py [--steps K] [--warmup W] [--gpus 1] [--stack R] [--sets N]
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "lookup+inject tokens/sec and achieved HBM GB/s, batch-64 decode, 1 MI355X"
+HBM_PEAK_GBPS = 8000.0
+D = 1024
+ESZ = 2  # bf16
+
+
+def algorithmic_bytes(T, hits, keys, window):
+    """Bytes the method must move for T positions (bf16, out of place):
+    hidden row in and out, one value row and one row id per hit, one 8-byte
+    key slot per formed key, the token window, and hit/slot/len outputs."""
+    return (T * 2 * D * ESZ + hits * (D * ESZ + 4) + keys * 8 + T * window * 4 + T * (1 + 4 + 1))
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=1000)
+    ap.add_argument("--warmup", type=int, default=50)
+    ap.add_argument("--stack", type=int, default=256, help="batch-64 steps per call")
+    ap.add_argument("--sets", type=int, default=8, help="rotating input sets")
+    ap.add_argument("--latency-steps", type=int, default=2000)
+    ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(--gpus %d requested)" % args.gpus, file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import synth
+    from paper_2607_07388_amd import tfe
+    from tests import harness as H
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    t0 = time.time()
+    table = synth.config2_table()
+    gt = H.GpuTable(table)
+    print("# table loaded (%d phrases) in %.1f s" % (table.n_phrases, time.time() - t0),
+          file=sys.stderr, flush=True)
+
+    B = 64 * args.stack
+    window, ctx, S = 3, 2, 1
+    stream = torch.cuda.current_stream()
+    sets = []
+    for k in range(args.sets):
+        batch = synth.decode_batch(1, B, set_index=100 + k)
+        tok = torch.from_numpy(batch.tokens).cuda()
+        hid = torch.empty((B, D), dtype=torch.bfloat16, device="cuda")
+        synth.normal_fill_device(hid.data_ptr(), 0, B, D, batch.seed, batch.hidden_tag, 1.0,
+                                 synth.BF16, stream.cuda_stream)
+        sets.append((batch, tok, hid, H.Outputs(B, D, synth.BF16)))
+    torch.cuda.synchronize()
+
+    def call(k):
+        _, tok, hid, outs = sets[k % len(sets)]
+        tfe.tfe_lookup_inject(gt.handle, tok, B, ctx, S, hid, outs.out, outs.hit, outs.slot,
+                              outs.len, tfe.TFE_GATE_SIGMOID, 1.0, stream.cuda_stream)
+
+    for k in range(args.warmup):
+        call(k)
+    torch.cuda.synchronize()
+    hits = [int(s[3].hit.sum().item()) for s in sets]
+    keys = B * (table.n_max - table.n_min + 1)
+
+    # Timed region: K calls; per-call event pairs give the launch durations.
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    w0 = time.perf_counter()
+    for k in range(args.steps):
+        ev[k][0].record(stream)
+        call(k)
+        ev[k][1].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - w0
+    durs = np.array([a.elapsed_time(b) for a, b in ev]) * 1e-3  # seconds
+    avg_launch = float(durs.mean())
+    bytes_per_call = [algorithmic_bytes(B, h, keys, window) for h in hits]
+    avg_bytes = float(np.mean([bytes_per_call[k % len(sets)] for k in range(args.steps)]))
+    achieved = avg_bytes / avg_launch / 1e9
+    tokens_per_s = B * args.steps / wall
+
+    # Latency mode: one batch-64 decode step per call.
+    lat_sets = []
+    for k in range(args.sets):
+        batch = synth.decode_batch(1, 64, set_index=200 + k)
+        tok = torch.from_numpy(batch.tokens).cuda()
+        hid = H.to_device(batch.hidden(), synth.BF16)
+        lat_sets.append((tok, hid, H.Outputs(64, D, synth.BF16)))
+    torch.cuda.synchronize()
+    lev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(args.latency_steps)]
+    l0 = time.perf_counter()
+    for k in range(args.latency_steps):
+        tok, hid, outs = lat_sets[k % len(lat_sets)]
+        lev[k][0].record(stream)
+        tfe.tfe_lookup_inject(gt.handle, tok, 64, ctx, S, hid, outs.out, outs.hit, outs.slot,
+                              outs.len, tfe.TFE_GATE_SIGMOID, 1.0, stream.cuda_stream)
+        lev[k][1].record(stream)
+    torch.cuda.synchronize()
+    lwall = time.perf_counter() - l0
+    ldur = np.array([a.elapsed_time(b) for a, b in lev]) * 1e-3
+    lhits = float(np.mean([s[2].hit.float().mean().item() for s in lat_sets]))
+
+    result = {
+        "metric": METRIC,
+        "value": tokens_per_s,
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": wall / args.steps * 1e3,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": "batch-64 decode, stacked throughput mode: %d batch-64 steps per call "
+                        "(%d rows, 3-token windows, Zipf(1.1) ids), 2^20-phrase 2/3-gram table, "
+                        "1024-wide bf16 values (2 GiB), sigmoid gate, out of place" % (args.stack, B),
+            "table_phrases": table.n_phrases,
+            "rows_per_call": B,
+            "rotating_sets": args.sets,
+            "hit_rate": float(np.mean(hits) / B),
+        },
+        "hbm_gbps_algorithmic": achieved,
+        "roofline": {
+            "bound": "hbm",
+            "kernel": "k_lookup_inject<bf16, D=1024>",
+            "achieved": achieved,
+            "peak": HBM_PEAK_GBPS,
+            "unit": "GB/s",
+            "frac": achieved / HBM_PEAK_GBPS,
+            "traffic": None,
+            "bytes_per_launch": avg_bytes,
+            "avg_launch_us": avg_launch * 1e6,
+        },
+        "latency_mode": {
+            "rows_per_call": 64,
+            "median_us_per_step": float(np.median(ldur) * 1e6),
+            "mean_us_per_step": float(ldur.mean() * 1e6),
+            "tokens_per_s_wall": 64 * args.latency_steps / lwall,
+            "hit_rate": lhits,
+            "algorithmic_gbps_median": algorithmic_bytes(64, lhits * 64, 128, 3) /
+                                       float(np.median(ldur)) / 1e9,
+        },
+    }
+
+    if not args.no_cpu_baseline:
+        import oracle
+        ot = H.oracle_table(table)
+        batch = sets[0][0]
+        hidden = synth.normal_range(batch.seed, batch.hidden_tag, 0, B, D, 1.0, synth.BF16)
+        hit, row, _ = ot.lookup(batch.tokens, ctx, S)
+        uniq, inv = np.unique(row[row >= 0].astype(np.int64), return_inverse=True)
+        vals = table.value_rows(uniq)
+        idx = np.full(B, -1, np.int64)
+        idx[row >= 0] = inv
+        rows_done, c0 = 0, time.perf_counter()
+        while time.perf_counter() - c0 < args.cpu_seconds:
+            ot.lookup(batch.tokens, ctx, S)
+            oracle.inject(hidden, vals, idx, synth.BF16)
+            rows_done += B
+        csec = time.perf_counter() - c0
+        result["cpu_baseline"] = {
+            "value": rows_done / csec,
+            "unit": "tokens/s",
+            "cores": 1,
+            "kind": "oracle",
+            "sample": "%d passes of std::map lookup + double-precision gate/inject over one "
+                      "%d-row stacked decode set (%.1f s, single thread)"
+                      % (rows_done // B, B, csec),
+        }
+    gt.close()
+    print(json.dumps(result))
+
+
+if __name__ == "__main__":
+    main()

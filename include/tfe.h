@@ -1,0 +1,193 @@
+/*
+ * tfe.h -- C ABI of the TF-Engram phrase-memory lookup + inject library for
+ * AMD MI355X (gfx950).
+ *
+ * The operation (paper: "TF-Engram: A Train-Free Engram with SSD-Backed
+ * Memory for Large Language Models"):
+ *   - the memory is a key -> value table whose keys are token n-grams
+ *     (phrases) and whose values are D-wide vectors in the hidden space
+ *     (Sec. 2.2, Eq. 2); each phrase has its own entry, so two phrases never
+ *     share a slot (Sec. 1, Sec. 4.1, Sec. 4.2);
+ *   - at every position t the n-grams that end at t, n = n_min..n_max, are
+ *     matched exactly against the table (Eq. 3, first index level of Eq. 10)
+ *     and the longest match is selected (Sec. 4.2);
+ *   - the selected value row m is injected as h' = h + g * m (Eq. 5);
+ *   - tables larger than device memory live in pinned host memory behind an
+ *     HBM cache tier (Sec. 4.3, Eq. 12, lookup through the hierarchy), which
+ *     is filled ahead of use from predicted next-token candidates (Sec. 4.4,
+ *     Eq. 14-16).
+ *
+ * Conventions shared by every call:
+ *   - "DEVICE" pointers are HIP device memory of the device that was current
+ *     when the table was loaded; "HOST" pointers are ordinary host memory.
+ *   - Streams are hipStream_t handles passed as void* (NULL = the default
+ *     stream).  Device work is enqueued asynchronously; results are valid once
+ *     the stream has reached the enqueued work.
+ *   - Argument errors are detected on the host before anything is enqueued and
+ *     return a negative status; tfe_last_error() then describes the problem.
+ *     A failed HIP call returns TFE_ERR_HIP.  No C++ exception crosses the ABI.
+ *   - A table handle is not thread-safe: calls on one handle must be issued
+ *     from one host thread at a time.
+ */
+#ifndef TFE_H_
+#define TFE_H_
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct tfe_table tfe_table; /* opaque; owned by the library */
+
+typedef enum {
+  TFE_OK = 0,
+  TFE_ERR_INVALID_ARG = -1,   /* bad size, pointer, length range or token */
+  TFE_ERR_DUPLICATE_KEY = -2, /* the same phrase appears twice */
+  TFE_ERR_OOM = -3,           /* device or pinned host allocation failed */
+  TFE_ERR_HIP = -4,           /* a HIP runtime call or kernel launch failed */
+  TFE_ERR_UNSUPPORTED = -5    /* valid request outside what is implemented */
+} tfe_status;
+
+typedef enum { TFE_F32 = 0, TFE_BF16 = 1 } tfe_dtype;
+
+/* Gate of Eq. 5.  The paper allows a scalar, a vector or a function of h and
+ * m; the method trains nothing, so the library offers two parameter-free
+ * gates:
+ *   TFE_GATE_SIGMOID: g = scale * sigmoid(<h / rms(h), m / rms(m)> / sqrt(D)),
+ *                     rms(x) = sqrt(mean(x^2) + 1e-6), i.e. scale times the
+ *                     logistic function of sqrt(D) * cos(h, m);
+ *   TFE_GATE_CONST:   g = scale.
+ * `scale` is the memory-injection scale of the evaluation (Sec. 5.1). */
+typedef enum { TFE_GATE_SIGMOID = 0, TFE_GATE_CONST = 1 } tfe_gate;
+
+typedef struct {
+  /* Phrases (Sec. 4.2): phrase i is phrase_tokens[i*n_max .. i*n_max+len-1],
+   * oldest token first, len = phrase_len[i]; unused columns are ignored.
+   * HOST memory, read during tfe_table_load only. */
+  int64_t n_phrases;            /* P >= 0; P = 0 gives a table that never matches */
+  int32_t n_min, n_max;         /* 2 <= n_min <= n_max <= 4 */
+  int32_t vocab;                /* token ids are valid in [0, vocab), vocab <= 2^18 */
+  const int32_t *phrase_tokens; /* HOST [P x n_max] */
+  const uint8_t *phrase_len;    /* HOST [P], each in [n_min, n_max] */
+  /* Value rows (Eq. 2): row i belongs to phrase i.  [P x dim], row-major. */
+  const void *values;
+  int32_t dim;                  /* D: bf16 512/1024/2048/4096, f32 256/512/1024/2048 */
+  int32_t dtype;                /* tfe_dtype of values and of hidden states */
+  int32_t values_on_device;     /* 1: `values` is DEVICE memory (copied); 0: HOST */
+  double max_load_factor;       /* index occupancy bound in (0, 0.9]; 0 means 0.5 */
+  /* Tiered mode (Sec. 4.3): hbm_cache_rows > 0 keeps the value rows in pinned
+   * host memory and serves them through an HBM cache of that many rows with
+   * least-recently-used replacement. */
+  int64_t hbm_cache_rows;       /* 0: every value row is resident in HBM */
+  int32_t adopt_host_values;    /* tiered: 1 = use the caller's `values` in place; it
+                                   must come from hipHostMalloc and outlive the table */
+  int64_t prefill_rows;         /* tiered: rows [0, prefill_rows) start cached */
+} tfe_table_desc;
+
+typedef struct {
+  uint64_t calls;            /* tfe_lookup_inject calls */
+  uint64_t positions;        /* injected positions looked up */
+  uint64_t hits;             /* positions with a match (tiered mode; resident: 0) */
+  uint64_t cache_hits;       /* tiered: matched rows found in the HBM cache */
+  uint64_t cache_misses;     /* tiered: matched rows fetched from host memory */
+  uint64_t prefetch_keys;    /* tiered: candidate phrases probed by tfe_prefetch */
+  uint64_t prefetch_found;   /* tiered: candidate phrases present in the table */
+  uint64_t prefetch_filled;  /* tiered: rows copied host -> HBM by tfe_prefetch */
+  uint64_t prefetch_used;    /* tiered: prefetched rows later hit by a lookup */
+  uint64_t host_bytes;       /* tiered: bytes read from host memory (both paths) */
+} tfe_stats;
+
+/* Builds the exact-match phrase index and places the value rows.
+ * Paper: Eq. 2 (table), Eq. 10 (token n-gram -> phrase id -> memory address),
+ * Sec. 4.3 and Eq. 12 (tiers).
+ * Rejects (before any device work) phrases whose length is outside
+ * [n_min, n_max], tokens outside [0, vocab) and repeated phrases
+ * (TFE_ERR_DUPLICATE_KEY).  The library copies the phrases, and copies the
+ * values unless adopt_host_values is set.  `stream` orders the uploads; the
+ * call returns after they completed.  On success *out owns all device and
+ * pinned memory of the table until tfe_table_free. */
+tfe_status tfe_table_load(const tfe_table_desc *desc, void *stream, tfe_table **out);
+
+/* Releases a table (waits for its pending work first).  NULL is accepted. */
+tfe_status tfe_table_free(tfe_table *table);
+
+/* Lookup + inject for B rows of ctx + S tokens.
+ * Paper: Eq. 3 (lookup from recent tokens), Sec. 4.2 (longest match),
+ * Eq. 5 (gated residual injection), Sec. 4.3 (lookup through the hierarchy).
+ *   tokens     DEVICE int32 [B x (ctx + S)], oldest first.  The first ctx
+ *              columns of a row are history: they take part in the windows
+ *              of later columns but are not injected.  Position (b, s) is
+ *              column ctx + s of row b; its n-gram is columns
+ *              ctx+s-n+1 .. ctx+s of the same row and exists only if it starts
+ *              at column >= 0 and all its tokens are in [0, vocab).
+ *   hidden_in  DEVICE [B*S x dim] of the table's dtype, row p = b*S + s.
+ *   hidden_out DEVICE [B*S x dim]; may equal hidden_in (in place: rows
+ *              without a match are then not written); partial overlap is
+ *              undefined.
+ *   hit_mask   DEVICE uint8 [B*S]: 1 where a phrase matched.
+ *   slot_ids   DEVICE int32 [B*S]: the matched phrase's row id (its index in
+ *              the loaded phrase list), -1 where nothing matched.
+ *   match_len  DEVICE uint8 [B*S] or NULL: matched n, 0 where nothing matched.
+ *   gate, scale: see tfe_gate.
+ * Tiered tables additionally read host rows that are not cached (zero-copy,
+ * on an internal side stream) and insert them into the cache; results do not
+ * depend on the cache state. */
+tfe_status tfe_lookup_inject(tfe_table *table, const int32_t *tokens, int32_t B, int32_t ctx,
+                             int32_t S, const void *hidden_in, void *hidden_out,
+                             uint8_t *hit_mask, int32_t *slot_ids, uint8_t *match_len,
+                             int32_t gate, float scale, void *stream);
+
+/* Prefetch for the next step (tiered tables; a no-op on resident tables).
+ * Paper: Eq. 14 (top-K next-token candidates), Eq. 15 (candidate phrases via
+ * the token-to-phrase index), Eq. 16 (fetch overlapped with the remaining
+ * layers), Sec. 4.3 (insert into the faster tier).
+ *   tail        DEVICE int32 [B x tail_len]: the last tail_len tokens of each
+ *               row, oldest first (tail_len >= n_max - 1 uses every length).
+ *   candidates  DEVICE int32 [B x K]: predicted next tokens of each row.
+ * For every row b and candidate c the phrases ending at c, i.e. the n-grams
+ * (tail[b, tail_len-n+1 ..], c) for n = n_min..n_max, are looked up; those
+ * present in the table and not cached are copied into the cache.  The work
+ * runs on `side_stream` after the table's previous lookup; the next
+ * tfe_lookup_inject waits for it. */
+tfe_status tfe_prefetch(tfe_table *table, const int32_t *tail, int32_t tail_len,
+                        const int32_t *candidates, int32_t B, int32_t K, void *side_stream);
+
+/* Copies the table's counters (synchronises with the table's pending work). */
+tfe_status tfe_get_stats(tfe_table *table, tfe_stats *out);
+
+/* Resets the table's counters to zero (stream-ordered after pending work). */
+tfe_status tfe_reset_stats(tfe_table *table);
+
+/* Message describing the last error returned on this host thread ("" if none). */
+const char *tfe_last_error(void);
+
+/* ---- Host-only index utilities (no GPU needed) ----------------------------
+ * The index is an open-addressing table of 16-byte slots grouped in buckets
+ * of 8 (128 bytes): {uint64 key, uint32 key_ext, int32 row}.  A phrase of n
+ * tokens x0..x{n-1} (oldest first) has key = n << 61 | x{n-3} << 36 |
+ * x{n-2} << 18 | x{n-1} (absent tokens are 0) and key_ext = x0 when n = 4,
+ * else 0.  Its home bucket is murmur3-fmix64(key ^ key_ext * 0x9E3779B97F4A7C15)
+ * mod (capacity / 8); a phrase lives in the first bucket at or after its home
+ * bucket (cyclically) that had a free slot when it was inserted; an empty slot
+ * has key = ~0.  Capacity = smallest power of two >= max(8, P / load factor). */
+
+/* Number of slots for n_phrases phrases at the given load factor (0 = 0.5). */
+int64_t tfe_index_capacity(int64_t n_phrases, double max_load_factor);
+
+/* Builds the index into caller memory `slots` of 16 * capacity bytes (HOST).
+ * Same validation as tfe_table_load. */
+tfe_status tfe_index_build_host(const int32_t *phrase_tokens, const uint8_t *phrase_len,
+                                int64_t n_phrases, int32_t n_min, int32_t n_max,
+                                int32_t vocab, void *slots, int64_t capacity);
+
+/* Looks one phrase up in a host-built index.  *row = its row or -1;
+ * *buckets_read = buckets inspected (>= 1); *home = its home bucket. */
+tfe_status tfe_index_probe_host(const void *slots, int64_t capacity, const int32_t *tokens,
+                                int32_t n, int32_t *row, int32_t *buckets_read, int64_t *home);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TFE_H_ */

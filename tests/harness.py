@@ -1,0 +1,111 @@
+"""Shared driving code for the GPU tests and the benchmark: loads synthetic
+phrase tables into libtfe, runs lookup + inject through the C ABI binding and
+computes the oracle's answer for the same seeded inputs."""
+import numpy as np
+import torch
+
+import oracle
+import synth
+from paper_2607_07388_amd import tfe
+
+TORCH_DT = {synth.F32: torch.float32, synth.BF16: torch.bfloat16}
+
+
+def cur_stream():
+    return torch.cuda.current_stream().cuda_stream
+
+
+def device_values(table):
+    """The table's value rows drawn on the device (bit-identical to the host draw)."""
+    v = torch.empty((table.n_phrases, table.dim), dtype=TORCH_DT[table.dtype], device="cuda")
+    if table.n_phrases:
+        synth.normal_fill_device(v.data_ptr(), 0, table.n_phrases, table.dim, table.seed,
+                                 synth.TAG_VALUES, table.sigma, table.dtype, cur_stream())
+    return v
+
+
+def to_device(a, dtype):
+    """Host array (float32, or uint16 bf16 patterns) -> device tensor."""
+    if dtype == synth.BF16:
+        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).cuda().view(torch.bfloat16)
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def to_host(t, dtype):
+    t = t.detach().cpu()
+    if dtype == synth.BF16:
+        return t.view(torch.int16).numpy().view(np.uint16)
+    return t.numpy()
+
+
+class GpuTable:
+    """A phrase table loaded through tfe_table_load."""
+
+    def __init__(self, table, values_on_device=None, lf=0.5):
+        self.table = table
+        if values_on_device is None:
+            values_on_device = table.n_phrases * table.dim > (1 << 22)
+        vals = device_values(table) if values_on_device else table.all_values()
+        torch.cuda.synchronize()
+        desc = tfe.make_desc(table.tokens, table.lens, table.n_min, table.n_max, table.vocab,
+                             vals if table.n_phrases else None, table.dim, table.dtype,
+                             values_on_device, lf)
+        self.handle = tfe.tfe_table_load(desc, cur_stream())
+        del vals
+
+    def close(self):
+        if self.handle:
+            tfe.tfe_table_free(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        self.close()
+
+
+class Outputs:
+    def __init__(self, T, dim, dtype, with_len=True):
+        self.hit = torch.full((T,), 0xEE, dtype=torch.uint8, device="cuda")
+        self.slot = torch.full((T,), -7, dtype=torch.int32, device="cuda")
+        self.len = torch.full((T,), 0xEE, dtype=torch.uint8, device="cuda") if with_len else None
+        self.out = torch.empty((T, dim), dtype=TORCH_DT[dtype], device="cuda")
+
+
+def run(gt, tokens_d, B, ctx, S, hidden_d, outs, gate=tfe.TFE_GATE_SIGMOID, scale=1.0,
+        inplace=False, stream=None):
+    hout = hidden_d if inplace else outs.out
+    tfe.tfe_lookup_inject(gt.handle, tokens_d, B, ctx, S, hidden_d, hout, outs.hit, outs.slot,
+                          outs.len, gate, scale, stream if stream is not None else cur_stream())
+    return hout
+
+
+def oracle_answer(table, otable, tokens, ctx, S, hidden, gate=oracle.GATE_SIGMOID, scale=1.0,
+                  positions=None):
+    """Oracle lookup + inject.  Value rows are drawn on the host for the
+    matched rows only.  `positions` restricts the injection to a sample."""
+    hit, row, ln = otable.lookup(tokens, ctx, S)
+    if positions is None:
+        positions = np.arange(hit.size)
+    sel = row[positions].astype(np.int64)
+    uniq, inv = np.unique(sel[sel >= 0], return_inverse=True)
+    vals = table.value_rows(uniq) if uniq.size else np.zeros((0, table.dim), np.float32)
+    idx = np.full(sel.size, -1, np.int64)
+    idx[sel >= 0] = inv
+    out = oracle.inject(hidden[positions], vals, idx, table.dtype, gate, scale)
+    return hit, row, ln, out
+
+
+def assert_close(got, want, dtype):
+    """fp32: max abs error 1e-5.  bf16: |a - b| <= 2e-2 max(|b|, 1e-3)."""
+    if dtype == synth.F32:
+        err = np.abs(got.astype(np.float64) - want.astype(np.float64))
+        assert err.max() <= 1e-5, err.max()
+    else:
+        a = synth.bf16_to_f32(got).astype(np.float64)
+        b = synth.bf16_to_f32(want).astype(np.float64)
+        bound = 2e-2 * np.maximum(np.abs(b), 1e-3)
+        bad = np.abs(a - b) > bound
+        assert not bad.any(), (int(bad.sum()), a[bad][:5], b[bad][:5])
+
+
+def oracle_table(table):
+    return oracle.Table(table.tokens, table.lens, table.n_min, table.n_max, table.vocab)

@@ -1,0 +1,196 @@
+"""GPU parity: the HIP path through the C ABI against the CPU oracle on the
+same seeded inputs.  Hit masks, slot (row) ids and match lengths must be
+bit-exact; fp32 outputs within 1e-5 absolute, bf16 within 2e-2 relative."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+from paper_2607_07388_amd import tfe
+
+from . import harness as H
+
+pytestmark = pytest.mark.gpu
+
+
+def check(table, gt, ot, tokens, ctx, S, hidden, gate=tfe.TFE_GATE_SIGMOID, scale=1.0,
+          inplace=False, positions=None):
+    B = tokens.shape[0]
+    T = B * S
+    tok_d = torch.from_numpy(np.ascontiguousarray(tokens, np.int32)).cuda()
+    h_d = H.to_device(hidden, table.dtype)
+    outs = H.Outputs(T, table.dim, table.dtype)
+    hout = H.run(gt, tok_d, B, ctx, S, h_d, outs, gate, scale, inplace)
+    torch.cuda.synchronize()
+    hit, row, ln, want = H.oracle_answer(table, ot, tokens, ctx, S, hidden, gate, scale, positions)
+    np.testing.assert_array_equal(outs.hit.cpu().numpy(), hit)
+    np.testing.assert_array_equal(outs.slot.cpu().numpy(), row)
+    np.testing.assert_array_equal(outs.len.cpu().numpy(), ln)
+    got = H.to_host(hout, table.dtype)
+    if positions is not None:
+        got = got[positions]
+    H.assert_close(got, want, table.dtype)
+    # Rows without a match keep their bytes.
+    miss = hit == 0 if positions is None else hit[positions] == 0
+    src = hidden if positions is None else hidden[positions]
+    assert got[miss].tobytes() == src[miss].tobytes()
+    return hit, got
+
+
+@pytest.fixture(scope="module")
+def w1():
+    table, batch = synth.config1()
+    gt = H.GpuTable(table)
+    yield table, batch, gt, H.oracle_table(table)
+    gt.close()
+
+
+@pytest.mark.parametrize("gate,scale", [(tfe.TFE_GATE_SIGMOID, 1.0), (tfe.TFE_GATE_CONST, 1.0),
+                                        (tfe.TFE_GATE_SIGMOID, 0.37)])
+def test_workload1_fp32(w1, gate, scale):
+    table, batch, gt, ot = w1
+    hit, _ = check(table, gt, ot, batch.tokens, batch.ctx, batch.S, batch.hidden(), gate, scale)
+    assert 0 < hit.sum() < batch.T
+
+
+def test_workload1_in_place(w1):
+    table, batch, gt, ot = w1
+    check(table, gt, ot, batch.tokens, batch.ctx, batch.S, batch.hidden(), inplace=True)
+
+
+def test_workload1_const_gate_is_index_select_add(w1):
+    """Gather pin: with g = 1 in fp32 the output is the IEEE sum of the hidden
+    row and the gathered value row, i.e. h + index_select(values, slot)."""
+    table, batch, gt, _ = w1
+    tok = torch.from_numpy(batch.tokens).cuda()
+    h = H.to_device(batch.hidden(), synth.F32)
+    outs = H.Outputs(batch.T, table.dim, synth.F32)
+    H.run(gt, tok, 1, 0, batch.S, h, outs, tfe.TFE_GATE_CONST, 1.0)
+    vals = H.device_values(table)
+    slot = outs.slot.long()
+    hitm = slot >= 0
+    want = h.clone()
+    want[hitm] = h[hitm] + torch.index_select(vals, 0, slot[hitm])
+    torch.cuda.synchronize()
+    assert torch.equal(outs.out, want)
+
+
+def test_determinism(w1):
+    table, batch, gt, _ = w1
+    tok = torch.from_numpy(batch.tokens).cuda()
+    h = H.to_device(batch.hidden(), synth.F32)
+    res = []
+    for _ in range(2):
+        outs = H.Outputs(batch.T, table.dim, synth.F32)
+        H.run(gt, tok, 1, 0, batch.S, h, outs)
+        torch.cuda.synchronize()
+        res.append((outs.out.cpu().numpy().tobytes(), outs.slot.cpu().numpy().tobytes()))
+    assert res[0] == res[1]
+
+
+def test_noop_cases(w1):
+    table, batch, gt, _ = w1
+    tok = torch.from_numpy(batch.tokens).cuda()
+    hid = batch.hidden()
+    h = H.to_device(hid, synth.F32)
+    outs = H.Outputs(batch.T, table.dim, synth.F32)
+    H.run(gt, tok, 1, 0, batch.S, h, outs, tfe.TFE_GATE_SIGMOID, 0.0)   # scale 0
+    torch.cuda.synchronize()
+    assert outs.out.cpu().numpy().tobytes() == hid.tobytes()
+    # Zero value rows: every hit is a no-op.
+    zt = synth.PhraseTable(table.tokens, table.lens, 2, 3, synth.F32, table.seed, sigma=0.0)
+    gz = H.GpuTable(zt)
+    outs = H.Outputs(batch.T, table.dim, synth.F32)
+    H.run(gz, tok, 1, 0, batch.S, h, outs)
+    torch.cuda.synchronize()
+    assert outs.hit.sum().item() > 0
+    assert outs.out.cpu().numpy().tobytes() == hid.tobytes()
+    gz.close()
+
+
+def small_table(seed, vocab, counts, dtype, dim, n_max):
+    rng = np.random.default_rng(seed)
+    phrases = set()
+    for n, want in counts:
+        got = set()
+        while len(got) < want:
+            got.add(tuple(int(x) for x in rng.integers(0, vocab, n)))
+        phrases |= got
+    phrases = sorted(phrases)
+    perm = rng.permutation(len(phrases))
+    toks = np.full((len(phrases), n_max), -1, np.int32)
+    lens = np.zeros(len(phrases), np.uint8)
+    for r, i in enumerate(perm):
+        w = phrases[i]
+        toks[r, :len(w)] = w
+        lens[r] = len(w)
+    n_min = min(n for n, _ in counts)
+    return synth.PhraseTable(toks, lens, n_min, n_max, dtype, seed, dim=dim, vocab=vocab)
+
+
+@pytest.mark.parametrize("dtype,dim", [(synth.BF16, 1024), (synth.BF16, 512), (synth.BF16, 4096),
+                                       (synth.F32, 256), (synth.F32, 2048)])
+def test_4grams_pads_ragged_tail(dtype, dim):
+    """Small vocabulary, 2/3/4-grams, pad and out-of-range tokens, history
+    columns, and B*S = 3*37 = 111 positions (not a multiple of the 4 waves
+    of a block)."""
+    vocab = 7
+    table = small_table(21 + dim, vocab, [(2, 20), (3, 150), (4, 900)], dtype, dim, 4)
+    gt = H.GpuTable(table)
+    ot = H.oracle_table(table)
+    rng = np.random.default_rng(dim)
+    B, ctx, S = 3, 3, 37
+    tokens = rng.integers(-1, vocab + 1, (B, ctx + S)).astype(np.int32)
+    hidden = synth.normal_range(7, 77, 0, B * S, dim, 1.0, dtype)
+    hit, _ = check(table, gt, ot, tokens, ctx, S, hidden)
+    _, _, ln = ot.lookup(tokens, ctx, S)
+    assert {0, 2, 3, 4} <= set(ln.tolist())
+    gt.close()
+
+
+def test_empty_table_and_empty_batch():
+    table = synth.PhraseTable(np.zeros((0, 3), np.int32), np.zeros(0, np.uint8), 2, 3, synth.BF16,
+                              0)
+    gt = H.GpuTable(table)
+    ot = H.oracle_table(table)
+    tokens = synth.zipf_tokens(0, 50, 4 * 9, 1.1).reshape(4, 9)
+    hidden = synth.normal_range(0, 51, 0, 4 * 7, 1024, 1.0, synth.BF16)
+    hit, _ = check(table, gt, ot, tokens, 2, 7, hidden)
+    assert hit.sum() == 0
+    # B = 0 and S = 0 enqueue nothing and succeed.
+    outs = H.Outputs(1, 1024, synth.BF16)
+    tfe.tfe_lookup_inject(gt.handle, None, 0, 2, 7, None, None, None, None, None, 0, 1.0, None)
+    tfe.tfe_lookup_inject(gt.handle, None, 4, 2, 0, None, None, None, None, None, 0, 1.0, None)
+    del outs
+    gt.close()
+
+
+@pytest.fixture(scope="module")
+def w2():
+    table = synth.config2_table()
+    gt = H.GpuTable(table)
+    yield table, gt, H.oracle_table(table)
+    gt.close()
+
+
+def test_workload2_decode_batch64(w2):
+    table, gt, ot = w2
+    batch = synth.decode_batch(1, 64)
+    hit, _ = check(table, gt, ot, batch.tokens, batch.ctx, batch.S, batch.hidden())
+    assert 0.4 < hit.mean() < 0.9
+
+
+def test_workload2_stacked_decode_16384_rows(w2):
+    """The benchmark's launch: 256 batch-64 decode steps in one call."""
+    table, gt, ot = w2
+    batch = synth.decode_batch(1, 64 * 256, set_index=1)
+    hit, _ = check(table, gt, ot, batch.tokens, batch.ctx, batch.S, batch.hidden())
+    assert 0.5 < hit.mean() < 0.8
+
+
+def test_workload2_in_place_const_gate(w2):
+    table, gt, ot = w2
+    batch = synth.decode_batch(1, 1000, set_index=2)
+    check(table, gt, ot, batch.tokens, batch.ctx, batch.S, batch.hidden(), tfe.TFE_GATE_CONST,
+          0.5, inplace=True)
