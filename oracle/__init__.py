@@ -67,9 +67,10 @@ class Table:
             raise OracleError(st.value)
 
     def __del__(self):
-        if getattr(self, "_h", None):
-            lib().oracle_table_free(self._h)
-            self._h = None
+        h = getattr(self, "_h", None)
+        if h and _lib is not None:
+            _lib.oracle_table_free(h)
+        self._h = None
 
     def lookup(self, tokens, ctx, S):
         """tokens: int32 [B x (ctx+S)] -> (hit uint8, row int32, len uint8), each [B*S]."""

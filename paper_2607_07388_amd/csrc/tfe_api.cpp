@@ -86,7 +86,12 @@ static tfe_status load(const tfe_table_desc* d, hipStream_t stream, tfe_table** 
 
   tfe_table* t = new (std::nothrow) tfe_table;
   if (!t) return fail(TFE_ERR_OOM, "table object");
-  if (hipGetDevice(&t->device) != hipSuccess) { delete t; return fail(TFE_ERR_HIP, "hipGetDevice"); }
+  if (hipGetDevice(&t->device) != hipSuccess ||
+      hipDeviceGetAttribute(&t->cus, hipDeviceAttributeMultiprocessorCount, t->device) !=
+          hipSuccess) {
+    delete t;
+    return fail(TFE_ERR_HIP, "device query");
+  }
   t->n_phrases = d->n_phrases;
   t->n_min = d->n_min;
   t->n_max = d->n_max;
@@ -130,6 +135,7 @@ static tfe_status lookup_inject(tfe_table* t, const int32_t* tokens, int32_t B, 
   if (!isfinite(scale)) return fail(TFE_ERR_INVALID_ARG, "scale is not finite");
   const int64_t T = (int64_t)B * S;
   if ((int64_t)ctx + S > 0x7FFFFFFFll) return fail(TFE_ERR_INVALID_ARG, "ctx + S overflows");
+  if (T > 0x7FFFFFFFll) return fail(TFE_ERR_UNSUPPORTED, "B * S above 2^31 - 1 positions");
   t->stats.calls++;
   if (T == 0) return TFE_OK;
   if (!tokens || !hin || !hout || !hit || !slot)
@@ -141,7 +147,7 @@ static tfe_status lookup_inject(tfe_table* t, const int32_t* tokens, int32_t B, 
   a.bucket_mask = (uint64_t)(t->capacity / TFE_SLOTS_PER_BUCKET - 1);
   a.values = t->d_values;
   a.tokens = tokens;
-  a.T = T;
+  a.T = (uint32_t)T;
   a.S = S;
   a.ctx = ctx;
   a.W = ctx + S;

@@ -30,7 +30,7 @@ struct LookupArgs {
   uint64_t bucket_mask;       // buckets - 1
   const void* values;         // resident value rows [P x dim]
   const int32_t* tokens;      // [B x W]
-  int64_t T;                  // B * S
+  uint32_t T;                 // B * S (< 2^31)
   int32_t S, ctx, W;          // W = ctx + S
   int32_t n_min, n_max, vocab;
   const void* hin;
@@ -58,6 +58,7 @@ bool dim_supported(int dtype, int dim);
 #if defined(__HIPCC__) || defined(__HIP_PLATFORM_AMD__)
 struct tfe_table {
   int device = 0;
+  int cus = 256;                 // compute units of `device`
   int64_t n_phrases = 0;
   int32_t n_min = 2, n_max = 3, vocab = 0, dim = 0, dtype = 0;
   int64_t capacity = 0;          // index slots

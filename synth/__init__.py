@@ -76,6 +76,8 @@ def dev_lib():
         lib.synth_normal_fill_dev.argtypes = [vp, i64, i64, i64, u64, ctypes.c_float,
                                               ctypes.c_int, vp]
         lib.synth_normal_fill_dev.restype = ctypes.c_int
+        lib.synth_copy_dev.argtypes = [vp, vp, i64, ctypes.c_int, vp]
+        lib.synth_copy_dev.restype = ctypes.c_int
         _dev = lib
     return _dev
 
@@ -154,6 +156,14 @@ def normal_fill_device(ptr, row0, nrows, cols, seed, tag, sigma, dtype, stream=0
                                          ctypes.c_void_p(stream))
     if rc != 0:
         raise RuntimeError("synth_normal_fill_dev failed (%d)" % rc)
+
+
+def copy_device(dst, src, nbytes, blocks=4096, stream=0):
+    """Reference device copy of nbytes (multiple of 16) between device buffers."""
+    rc = dev_lib().synth_copy_dev(ctypes.c_void_p(dst), ctypes.c_void_p(src), int(nbytes),
+                                  int(blocks), ctypes.c_void_p(stream))
+    if rc != 0:
+        raise RuntimeError("synth_copy_dev failed (%d)" % rc)
 
 
 def bf16_to_f32(u16):

@@ -38,3 +38,23 @@ extern "C" int synth_normal_fill_dev(void* out, int64_t row0, int64_t nrows, int
                        nrows, cols, key, scale);
   return hipGetLastError() == hipSuccess ? 0 : -2;
 }
+
+// Plain device copy (16 bytes per lane, non-temporal), used only as the
+// bandwidth reference next to the lookup kernel: its HBM bytes are known
+// exactly, which calibrates the profiler's fetch/write counters.
+typedef uint32_t synth_u32x4 __attribute__((ext_vector_type(4)));
+
+__global__ void k_copy16(const synth_u32x4* __restrict__ src, synth_u32x4* __restrict__ dst,
+                         int64_t n) {
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride)
+    __builtin_nontemporal_store(__builtin_nontemporal_load(src + i), dst + i);
+}
+
+extern "C" int synth_copy_dev(void* dst, const void* src, int64_t nbytes, int blocks,
+                              hipStream_t stream) {
+  if (!dst || !src || nbytes <= 0 || (nbytes & 15) || blocks <= 0) return -1;
+  hipLaunchKernelGGL(k_copy16, dim3((unsigned)blocks), dim3(256), 0, stream, (const synth_u32x4*)src,
+                     (synth_u32x4*)dst, nbytes / 16);
+  return hipGetLastError() == hipSuccess ? 0 : -2;
+}
