@@ -10,7 +10,11 @@
 #include <stdint.h>
 #include <string.h>
 
+#include <sys/mman.h>
+
 #include <algorithm>
+#include <cstdlib>
+#include <new>
 #include <cmath>
 #include <vector>
 
@@ -60,25 +64,41 @@ inline uint32_t part_of(K k) {
 }
 
 
+// Uninitialised array whose pages are first touched by the parallel loops
+// that fill it (value-initialising a multi-GB vector would zero it serially),
+// backed by transparent huge pages where the kernel allows them: a
+// multi-GB scratch array otherwise costs millions of 4 KiB page faults.
+template <class T>
+struct RawArray {
+  T* p = nullptr;
+  size_t bytes = 0;
+  explicit RawArray(int64_t n) {
+    const size_t huge = (size_t)2 << 20;
+    bytes = (sizeof(T) * (size_t)(n > 0 ? n : 1) + huge - 1) / huge * huge;
+    p = static_cast<T*>(std::aligned_alloc(huge, bytes));
+    if (!p) throw std::bad_alloc();
+    madvise(p, bytes, MADV_HUGEPAGE);
+  }
+  ~RawArray() { std::free(p); }
+  RawArray(const RawArray&) = delete;
+  RawArray& operator=(const RawArray&) = delete;
+  T& operator[](int64_t i) { return p[i]; }
+};
+
 template <class K>
 int64_t ngram_top(const int32_t* tok, int64_t ntok, int n, int V, int64_t skip,
                   int64_t want, int32_t* out_tuples, int64_t* out_counts) {
   const int64_t nk = ntok - n + 1;
   if (nk <= 0 || want <= 0) return 0;
-  const int NP = 256;
+  const int NP = 1024;
   // Fixed chunking: the scatter order never depends on the thread count.
-  const int NCH = 64;
+  const int NCH = 128;
   std::vector<int64_t> hist((size_t)NCH * NP, 0);
-  std::vector<K> keys(nk);
 #pragma omp parallel for schedule(static)
   for (int c = 0; c < NCH; ++c) {
     int64_t a = nk * c / NCH, b = nk * (c + 1) / NCH;
     int64_t* h = &hist[(size_t)c * NP];
-    for (int64_t i = a; i < b; ++i) {
-      K k = pack_tuple<K>(tok + i, n, V);
-      keys[i] = k;
-      h[part_of(k)]++;
-    }
+    for (int64_t i = a; i < b; ++i) h[part_of(pack_tuple<K>(tok + i, n, V)) % NP]++;
   }
   std::vector<int64_t> off((size_t)NCH * NP + 1, 0), pstart(NP + 1, 0);
   {
@@ -89,30 +109,33 @@ int64_t ngram_top(const int32_t* tok, int64_t ntok, int n, int V, int64_t skip,
     }
     pstart[NP] = acc;
   }
-  std::vector<K> part(nk);
+  RawArray<K> part(nk);
 #pragma omp parallel for schedule(static)
   for (int c = 0; c < NCH; ++c) {
     int64_t a = nk * c / NCH, b = nk * (c + 1) / NCH;
     int64_t* o = &off[(size_t)c * NP];
-    for (int64_t i = a; i < b; ++i) { K k = keys[i]; part[o[part_of(k)]++] = k; }
+    for (int64_t i = a; i < b; ++i) {
+      K k = pack_tuple<K>(tok + i, n, V);
+      part[o[part_of(k) % NP]++] = k;
+    }
   }
-  std::vector<K>().swap(keys);
-  // Per partition: sort and run-length count, in place (distinct keys are
-  // compacted to the front of the partition, counts kept alongside).
+  // Per partition: sort and run-length count in place (distinct keys are
+  // compacted to the front of the partition; counts go to a parallel array).
+  RawArray<int64_t> cnt(nk);
   std::vector<int64_t> ndist(NP, 0);
-  std::vector<std::vector<int64_t>> pcount(NP);
 #pragma omp parallel for schedule(dynamic, 1)
   for (int p = 0; p < NP; ++p) {
-    K* a = part.data() + pstart[p];
+    K* a = part.p + pstart[p];
+    int64_t* c = cnt.p + pstart[p];
     int64_t m = pstart[p + 1] - pstart[p];
     std::sort(a, a + m);
-    std::vector<int64_t>& cnt = pcount[p];
     int64_t d = 0;
     for (int64_t i = 0; i < m;) {
       int64_t j = i + 1;
       while (j < m && a[j] == a[i]) ++j;
-      a[d++] = a[i];
-      cnt.push_back(j - i);
+      a[d] = a[i];
+      c[d] = j - i;
+      ++d;
       i = j;
     }
     ndist[p] = d;
@@ -124,18 +147,18 @@ int64_t ngram_top(const int32_t* tok, int64_t ntok, int n, int V, int64_t skip,
   // Threshold count: the K_-th largest count.
   std::vector<int64_t> allc;
   allc.reserve(total);
-  for (int p = 0; p < NP; ++p) allc.insert(allc.end(), pcount[p].begin(), pcount[p].end());
+  for (int p = 0; p < NP; ++p) allc.insert(allc.end(), cnt.p + pstart[p], cnt.p + pstart[p] + ndist[p]);
   std::nth_element(allc.begin(), allc.begin() + (K_ - 1), allc.end(), std::greater<int64_t>());
   const int64_t cstar = allc[K_ - 1];
   std::vector<int64_t>().swap(allc);
   std::vector<std::pair<int64_t, K>> sel;  // (-count, key)
   std::vector<K> ties;
   for (int p = 0; p < NP; ++p) {
-    const K* a = part.data() + pstart[p];
+    const K* a = part.p + pstart[p];
+    const int64_t* c = cnt.p + pstart[p];
     for (int64_t i = 0; i < ndist[p]; ++i) {
-      int64_t c = pcount[p][i];
-      if (c > cstar) sel.push_back({-c, a[i]});
-      else if (c == cstar) ties.push_back(a[i]);
+      if (c[i] > cstar) sel.push_back({-c[i], a[i]});
+      else if (c[i] == cstar) ties.push_back(a[i]);
     }
   }
   std::sort(ties.begin(), ties.end());

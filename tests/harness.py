@@ -79,10 +79,14 @@ def run(gt, tokens_d, B, ctx, S, hidden_d, outs, gate=tfe.TFE_GATE_SIGMOID, scal
 
 
 def oracle_answer(table, otable, tokens, ctx, S, hidden, gate=oracle.GATE_SIGMOID, scale=1.0,
-                  positions=None):
+                  positions=None, row_map=None):
     """Oracle lookup + inject.  Value rows are drawn on the host for the
-    matched rows only.  `positions` restricts the injection to a sample."""
+    matched rows only.  `positions` restricts the injection to a sample.
+    `row_map` maps the oracle table's rows to the full table's rows when the
+    oracle holds only the phrases that can match (see subset_rows)."""
     hit, row, ln = otable.lookup(tokens, ctx, S)
+    if row_map is not None:
+        row = np.where(row >= 0, row_map[np.maximum(row, 0)], -1).astype(np.int32)
     if positions is None:
         positions = np.arange(hit.size)
     sel = row[positions].astype(np.int64)
@@ -109,3 +113,31 @@ def assert_close(got, want, dtype):
 
 def oracle_table(table):
     return oracle.Table(table.tokens, table.lens, table.n_min, table.n_max, table.vocab)
+
+
+def subset_rows(table, tokens, ctx, S):
+    """Rows of `table` whose phrase equals some n-gram window of the query
+    (n_min..n_max, exact tuple comparison by packed integer keys, n <= 3).
+    An oracle built from these rows answers the query exactly as one built
+    from the whole table, since no other phrase can match."""
+    assert table.n_max <= 3
+    V = np.uint64(table.vocab)
+    want = []
+    for n in range(table.n_min, table.n_max + 1):
+        cols = [tokens[:, j:tokens.shape[1] - n + 1 + j].astype(np.int64) for j in range(n)]
+        w = np.stack(cols, axis=-1).reshape(-1, n)
+        w = w[np.all((w >= 0) & (w < table.vocab), axis=1)]
+        k = np.zeros(w.shape[0], np.uint64)
+        for j in range(n):
+            k = k * V + w[:, j].astype(np.uint64)
+        want.append((n, np.unique(k)))
+    rows = []
+    for n, k in want:
+        idx = np.flatnonzero(table.lens == n)
+        t = table.tokens[idx, :n].astype(np.uint64)
+        pk = np.zeros(idx.size, np.uint64)
+        for j in range(n):
+            pk = pk * V + t[:, j]
+        pos = np.minimum(np.searchsorted(k, pk), k.size - 1) if k.size else None
+        rows.append(idx[k[pos] == pk] if k.size else idx[:0])
+    return np.sort(np.concatenate(rows)).astype(np.int64)

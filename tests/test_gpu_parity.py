@@ -15,7 +15,7 @@ pytestmark = pytest.mark.gpu
 
 
 def check(table, gt, ot, tokens, ctx, S, hidden, gate=tfe.TFE_GATE_SIGMOID, scale=1.0,
-          inplace=False, positions=None):
+          inplace=False, positions=None, row_map=None):
     B = tokens.shape[0]
     T = B * S
     tok_d = torch.from_numpy(np.ascontiguousarray(tokens, np.int32)).cuda()
@@ -23,7 +23,8 @@ def check(table, gt, ot, tokens, ctx, S, hidden, gate=tfe.TFE_GATE_SIGMOID, scal
     outs = H.Outputs(T, table.dim, table.dtype)
     hout = H.run(gt, tok_d, B, ctx, S, h_d, outs, gate, scale, inplace)
     torch.cuda.synchronize()
-    hit, row, ln, want = H.oracle_answer(table, ot, tokens, ctx, S, hidden, gate, scale, positions)
+    hit, row, ln, want = H.oracle_answer(table, ot, tokens, ctx, S, hidden, gate, scale, positions,
+                                         row_map)
     np.testing.assert_array_equal(outs.hit.cpu().numpy(), hit)
     np.testing.assert_array_equal(outs.slot.cpu().numpy(), row)
     np.testing.assert_array_equal(outs.len.cpu().numpy(), ln)
@@ -194,3 +195,31 @@ def test_workload2_in_place_const_gate(w2):
     batch = synth.decode_batch(1, 1000, set_index=2)
     check(table, gt, ot, batch.tokens, batch.ctx, batch.S, batch.hidden(), tfe.TFE_GATE_CONST,
           0.5, inplace=True)
+
+
+def test_workload3_prefill_full():
+    """8 x 4096 prefill against the 4M-phrase 2/3/4-gram table (8 GiB of
+    values): every position compared; hit rate in [0.30, 0.40]."""
+    table = synth.config3_table()
+    gt = H.GpuTable(table)
+    ot = H.oracle_table(table)
+    batch = synth.prefill_batch(2, 8, 4096)
+    hit, _ = check(table, gt, ot, batch.tokens, batch.ctx, batch.S, batch.hidden())
+    assert 0.30 <= hit.mean() <= 0.40
+    _, _, ln = ot.lookup(batch.tokens, batch.ctx, batch.S)
+    assert {0, 2, 3, 4} <= set(ln.tolist())
+    gt.close()
+
+
+def test_workload4_large_table():
+    """Batch-256 decode against the 2^25-phrase table (64 GiB of values);
+    the oracle holds the phrases that can match the query (found by exact
+    tuple comparison over the whole table)."""
+    table = synth.config4_table()
+    gt = H.GpuTable(table)
+    batch = synth.decode_batch(3, 256, s=1.05)
+    rows = H.subset_rows(table, batch.tokens, batch.ctx, batch.S)
+    ot = oracle.Table(table.tokens[rows], table.lens[rows], 2, 3, synth.V)
+    hit, _ = check(table, gt, ot, batch.tokens, batch.ctx, batch.S, batch.hidden(), row_map=rows)
+    assert 0.5 < hit.mean() < 0.95
+    gt.close()

@@ -351,3 +351,14 @@ def test_workload1_has_both_match_lengths():
     _, _, ln = t.lookup(batch.tokens, 0, 64)
     assert {2, 3} <= set(ln.tolist())
     assert table.n_phrases == 4096
+
+
+@pytest.mark.slow
+def test_workload3_hit_rate_in_range():
+    """Workload 3 asks for a hit rate of about 30-40%; the oracle measures it."""
+    table = synth.config3_table()
+    t = oracle.Table(table.tokens, table.lens, 2, 4, V)
+    batch = synth.prefill_batch(2, 8, 4096)
+    hit, _, ln = t.lookup(batch.tokens, batch.ctx, batch.S)
+    assert 0.30 <= hit.mean() <= 0.40
+    assert np.bincount(ln, minlength=5)[4] > 0
