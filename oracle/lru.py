@@ -1,0 +1,147 @@
+"""Reference model of the HBM cache tier's replacement policy.
+
+TEST INFRASTRUCTURE ONLY (see the package docstring).  A plain Python model
+of the residency bookkeeping that the tiered table keeps on the device, used
+to check the device's cache statistics exactly.  It follows the paper's
+lookup through the hierarchy (Sec. 4.3: check the GPU cache, else stage the
+entry from host memory and insert it into the faster tier) with recency as
+the cache-ranking signal (Sec. 4.3 lists recency among the ranking inputs)
+and the prefetch of candidate phrases (Eq. 15) into the cache.
+
+Policy (the precise reading; a call is one lookup or one prefetch):
+* The cache has C slots.  At load, slot s holds row s for s < prefill; the
+  recency order from least to most recent is: empty slots by ascending slot,
+  then filled slots by descending row (the least frequent row goes first).
+* Lookup: positions are taken in consecutive groups of GROUP = 1024.  In a
+  group, every matched row that is cached marks its slot referenced; then the
+  distinct matched rows that are not cached, in order of first position, each
+  take the least recent slot that is not referenced in this call (its old row
+  leaves the cache, and the slot counts as referenced from then on); a row
+  that finds no such slot is read from host memory without being cached.
+  Finally every slot referenced for the first time in this call by the group
+  becomes most recent, in order of the first position that named its row.
+* Prefetch: the candidates' matched rows, in candidate order, that are
+  distinct and not cached each take the least recent slot not filled by this
+  prefetch; the filled slots become most recent in that order and are marked
+  prefetched.  Prefetch never changes the recency of cached rows.
+* Statistics: hits = matched positions; cache_hits = matched positions whose
+  row was cached when their group started (cache_misses = the rest);
+  prefetch_used counts a prefetched slot the first time a lookup finds it
+  cached; host_bytes = row bytes x (rows filled + positions read directly).
+"""
+import collections
+
+GROUP = 1024
+
+
+class LruModel:
+    def __init__(self, cache_rows, prefill_rows, row_bytes):
+        self.C = cache_rows
+        self.row_bytes = row_bytes
+        self.slot_row = [-1] * cache_rows
+        self.where = {}
+        # Recency order: OrderedDict of slot -> None, least recent first.
+        self.order = collections.OrderedDict()
+        for s in range(prefill_rows, cache_rows):
+            self.order[s] = None
+        for s in range(prefill_rows - 1, -1, -1):
+            self.order[s] = None
+        for s in range(prefill_rows):
+            self.slot_row[s] = s
+            self.where[s] = s
+        self.prefetched = set()
+        self.stats = collections.Counter()
+
+    def _victim(self, referenced):
+        for s in self.order:
+            if s not in referenced:
+                return s
+        return None
+
+    def _fill(self, row, slot):
+        old = self.slot_row[slot]
+        if old >= 0:
+            del self.where[old]
+        self.slot_row[slot] = row
+        self.where[row] = slot
+
+    def lookup(self, rows):
+        """rows: matched row per position (-1 = no match).  Returns the list of
+        per-position sources: ('cache', slot), ('fill', slot), ('host', None)
+        or None for a miss."""
+        out = []
+        referenced = set()
+        for g in range(0, len(rows), GROUP):
+            grp = rows[g:g + GROUP]
+            first_pos = {}
+            status = {}
+            for r in grp:
+                if r >= 0 and r not in first_pos:
+                    first_pos[r] = len(first_pos)
+            newly = []
+            for r in first_pos:
+                if r in self.where:
+                    s = self.where[r]
+                    if s not in referenced:
+                        newly.append((first_pos[r], s))
+                    referenced.add(s)
+                    status[r] = ("cache", s)
+            filled = {}
+            for r in first_pos:
+                if r in status:
+                    continue
+                v = self._victim(referenced)
+                if v is None:
+                    status[r] = ("host", None)
+                else:
+                    self._fill(r, v)
+                    self.prefetched.discard(v)
+                    filled[r] = v
+                    referenced.add(v)
+                    newly.append((first_pos[r], v))
+                    status[r] = ("fill", v)
+            for _, s in sorted(newly):
+                self.order.move_to_end(s)
+            for r in grp:
+                if r < 0:
+                    out.append(None)
+                    continue
+                self.stats["hits"] += 1
+                kind, s = status[r]
+                out.append((kind, s))
+                if kind == "cache":
+                    self.stats["cache_hits"] += 1
+                    if s in self.prefetched:
+                        self.prefetched.discard(s)
+                        self.stats["prefetch_used"] += 1
+                else:
+                    self.stats["cache_misses"] += 1
+                    if kind == "host":
+                        self.stats["host_bytes"] += self.row_bytes
+            self.stats["host_bytes"] += self.row_bytes * len(filled)
+        self.stats["positions"] += len(rows)
+        return out
+
+    def prefetch(self, cand_rows):
+        """cand_rows: matched row per candidate (-1 = none), candidate order."""
+        self.stats["prefetch_keys"] += len(cand_rows)
+        self.stats["prefetch_found"] += sum(1 for r in cand_rows if r >= 0)
+        taken = set()
+        seen = set()
+        for r in cand_rows:
+            if r < 0 or r in seen or r in self.where:
+                seen.add(r)
+                continue
+            seen.add(r)
+            v = self._victim(taken)
+            if v is None:
+                break
+            self._fill(r, v)
+            taken.add(v)
+            self.order.move_to_end(v)
+            self.prefetched.add(v)
+            self.stats["prefetch_filled"] += 1
+            self.stats["host_bytes"] += self.row_bytes
+
+    def resident(self):
+        return dict(self.where)

@@ -5,6 +5,8 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <stddef.h>
+
 #include <new>
 #include <vector>
 
@@ -44,8 +46,16 @@ static void release(tfe_table* t) {
   (void)hipGetDevice(&cur);
   (void)hipSetDevice(t->device);
   (void)hipDeviceSynchronize();
-  if (t->d_slots) (void)hipFree(t->d_slots);
-  if (t->d_values) (void)hipFree(t->d_values);
+  void* dev_bufs[] = {t->d_slots, t->d_values, t->d_cache, t->d_where, t->d_owner, t->d_stamp,
+                      t->d_filled_at, t->d_pref, t->d_ring, t->d_ring2, t->d_ctl, t->d_row_of,
+                      t->d_slot_of, t->d_phase, t->d_jobs};
+  for (void* b : dev_bufs)
+    if (b) (void)hipFree(b);
+  if (t->own_h_values && t->h_values) (void)hipHostFree(t->h_values);
+  if (t->fill_stream) (void)hipStreamDestroy(t->fill_stream);
+  hipEvent_t evs[] = {t->ev_resolved, t->ev_filled, t->ev_lookup, t->ev_prefetch};
+  for (hipEvent_t e : evs)
+    if (e) (void)hipEventDestroy(e);
   (void)hipSetDevice(cur);
   delete t;
 }
@@ -59,6 +69,227 @@ static tfe_status check_device(const tfe_table* t) {
   return TFE_OK;
 }
 
+static tfe_status load_resident(tfe_table* t, const tfe_table_desc* d, hipStream_t stream) {
+  if (d->n_phrases == 0) return TFE_OK;
+  const size_t vbytes = (size_t)d->n_phrases * d->dim * elem_size(d->dtype);
+  if (hipMalloc(&t->d_values, vbytes) != hipSuccess)
+    return fail(TFE_ERR_OOM, "device values (%zu bytes)", vbytes);
+  TFE_HIP(hipMemcpyAsync(t->d_values, d->values, vbytes,
+                         d->values_on_device ? hipMemcpyDeviceToDevice : hipMemcpyHostToDevice,
+                         stream),
+          "values upload");
+  TFE_HIP(hipStreamSynchronize(stream), "values upload");
+  return TFE_OK;
+}
+
+template <class T>
+static tfe_status dev_alloc(T** p, size_t n, const char* what) {
+  if (hipMalloc((void**)p, n * sizeof(T) + (n == 0)) != hipSuccess)
+    return fail(TFE_ERR_OOM, "%s (%zu bytes)", what, n * sizeof(T));
+  return TFE_OK;
+}
+
+#define TFE_TRY(x)                   \
+  do {                               \
+    tfe_status st_ = (x);            \
+    if (st_ != TFE_OK) return st_;   \
+  } while (0)
+
+static tfe::TierArgs tier_args(tfe_table* t) {
+  tfe::TierArgs a = {};
+  a.host_values = t->h_values_dev;
+  a.cache = t->d_cache;
+  a.where = t->d_where;
+  a.owner = t->d_owner;
+  a.stamp = t->d_stamp;
+  a.filled_at = t->d_filled_at;
+  a.pref = t->d_pref;
+  a.ring = t->d_ring;
+  a.ring_mask = t->ring_cap - 1;
+  a.ctl = t->d_ctl;
+  a.row_of = t->d_row_of;
+  a.slot_of = t->d_slot_of;
+  a.phase = t->d_phase;
+  a.jobs = t->d_jobs;
+  a.clock = t->clock;
+  a.row_bytes = (uint32_t)(t->dim * elem_size(t->dtype));
+  a.look.slots = t->d_slots;
+  a.look.bucket_mask = (uint64_t)(t->capacity / TFE_SLOTS_PER_BUCKET - 1);
+  a.look.n_min = t->n_min;
+  a.look.n_max = t->n_max;
+  a.look.vocab = t->vocab;
+  return a;
+}
+
+static uint64_t pow2_at_least(uint64_t n) {
+  uint64_t c = 1;
+  while (c < n) c <<= 1;
+  return c;
+}
+
+// Tiered load: value rows in pinned host memory (the caller's, or a copy),
+// an HBM cache of hbm_cache_rows rows with rows [0, prefill_rows) preloaded,
+// and the residency / recency state of every slot.
+static tfe_status load_tiered(tfe_table* t, const tfe_table_desc* d, hipStream_t stream) {
+  const int64_t P = d->n_phrases, C = d->hbm_cache_rows;
+  const size_t row_bytes = (size_t)d->dim * elem_size(d->dtype);
+  t->cache_rows = C;
+  t->prefill_rows = d->prefill_rows;
+  if (P > 0 && d->adopt_host_values) {
+    hipPointerAttribute_t attr;
+    const hipError_t pe = hipPointerGetAttributes(&attr, d->values);
+    if (pe != hipSuccess) (void)hipGetLastError();  // unknown memory: clear the error state
+    if (pe != hipSuccess || attr.type != hipMemoryTypeHost)
+      return fail(TFE_ERR_INVALID_ARG, "adopted values are not pinned host memory (hipHostMalloc)");
+    t->h_values = const_cast<void*>(d->values);
+  } else if (P > 0) {
+    if (hipHostMalloc(&t->h_values, (size_t)P * row_bytes, hipHostMallocDefault) != hipSuccess) {
+      t->h_values = nullptr;
+      return fail(TFE_ERR_OOM, "pinned host values (%zu bytes)", (size_t)P * row_bytes);
+    }
+    t->own_h_values = true;
+    TFE_HIP(hipMemcpy(t->h_values, d->values, (size_t)P * row_bytes,
+                      d->values_on_device ? hipMemcpyDeviceToHost : hipMemcpyHostToHost),
+            "values to pinned host memory");
+  }
+  if (t->h_values) {
+    void* dp = nullptr;
+    TFE_HIP(hipHostGetDevicePointer(&dp, t->h_values, 0), "hipHostGetDevicePointer");
+    t->h_values_dev = dp;
+  }
+  TFE_TRY(dev_alloc((char**)&t->d_cache, (size_t)C * row_bytes, "HBM cache"));
+  TFE_TRY(dev_alloc(&t->d_where, (size_t)P, "residency map"));
+  TFE_TRY(dev_alloc(&t->d_owner, (size_t)C, "slot owners"));
+  TFE_TRY(dev_alloc(&t->d_stamp, (size_t)C, "slot stamps"));
+  TFE_TRY(dev_alloc(&t->d_filled_at, (size_t)C, "slot fill stamps"));
+  TFE_TRY(dev_alloc(&t->d_pref, (size_t)C, "prefetch flags"));
+  t->ring_cap = pow2_at_least((uint64_t)C * 4 < 4096 ? 4096 : (uint64_t)C * 4);
+  TFE_TRY(dev_alloc(&t->d_ring, t->ring_cap, "recency ring"));
+  TFE_TRY(dev_alloc(&t->d_ring2, t->ring_cap, "recency ring"));
+  TFE_TRY(dev_alloc(&t->d_ctl, 1, "tier control block"));
+  TFE_HIP(hipMemsetAsync(t->d_where, 0xFF, (size_t)P * sizeof(int32_t), stream), "init");
+  TFE_HIP(hipMemsetAsync(t->d_ctl, 0, sizeof(tfe::TierCtl), stream), "init");
+  tfe::TierArgs a = tier_args(t);
+  TFE_HIP(tfe::launch_tier_init(a, (uint32_t)C, (uint32_t)d->prefill_rows, stream), "init launch");
+  if (d->prefill_rows > 0)
+    TFE_HIP(hipMemcpyAsync(t->d_cache, t->h_values, (size_t)d->prefill_rows * row_bytes,
+                           hipMemcpyHostToDevice, stream),
+            "cache prefill");
+  t->ring_bound = (uint64_t)C;
+  TFE_HIP(hipStreamCreateWithFlags(&t->fill_stream, hipStreamNonBlocking), "fill stream");
+  hipEvent_t* evs[] = {&t->ev_resolved, &t->ev_filled, &t->ev_lookup, &t->ev_prefetch};
+  for (hipEvent_t* ev : evs)
+    TFE_HIP(hipEventCreateWithFlags(ev, hipEventDisableTiming), "events");
+  TFE_HIP(hipStreamSynchronize(stream), "tiered init");
+  return TFE_OK;
+}
+
+// Grows the per-call scratch (rows, slots, phases, fill jobs) to n entries.
+static tfe_status ensure_scratch(tfe_table* t, uint32_t n) {
+  if (n <= t->scratch_cap) return TFE_OK;
+  TFE_HIP(hipDeviceSynchronize(), "scratch regrow");
+  void* olds[] = {t->d_row_of, t->d_slot_of, t->d_phase, t->d_jobs};
+  for (void* b : olds)
+    if (b) (void)hipFree(b);
+  t->d_row_of = t->d_slot_of = nullptr;
+  t->d_phase = nullptr;
+  t->d_jobs = nullptr;
+  t->scratch_cap = 0;
+  const uint32_t cap = (uint32_t)pow2_at_least(n < 1024 ? 1024 : n);
+  TFE_TRY(dev_alloc(&t->d_row_of, cap, "scratch"));
+  TFE_TRY(dev_alloc(&t->d_slot_of, cap, "scratch"));
+  TFE_TRY(dev_alloc(&t->d_phase, cap, "scratch"));
+  TFE_TRY(dev_alloc(&t->d_jobs, cap, "scratch"));
+  t->scratch_cap = cap;
+  return TFE_OK;
+}
+
+// Before a call that appends at most `appends` recency entries: drops the
+// dead entries when the ring could overflow (every slot keeps exactly one
+// live entry, so afterwards the ring holds cache_rows entries), growing the
+// ring if even that would not leave room.
+static tfe_status reserve_ring(tfe_table* t, uint64_t appends, hipStream_t stream) {
+  if (t->ring_bound + appends <= t->ring_cap) {
+    t->ring_bound += appends;
+    return TFE_OK;
+  }
+  const uint64_t need = (uint64_t)t->cache_rows + appends;
+  tfe::TierArgs a = tier_args(t);
+  if (need > t->ring_cap) {
+    const uint64_t cap = pow2_at_least(2 * need);
+    uint64_t *r1 = nullptr, *r2 = nullptr;
+    TFE_TRY(dev_alloc(&r1, cap, "recency ring"));
+    if (dev_alloc(&r2, cap, "recency ring") != TFE_OK) {
+      (void)hipFree(r1);
+      return TFE_ERR_OOM;
+    }
+    TFE_HIP(tfe::launch_ring_compact(a, r1, cap - 1, stream), "ring compaction");
+    TFE_HIP(hipStreamSynchronize(stream), "ring regrow");
+    (void)hipFree(t->d_ring);
+    (void)hipFree(t->d_ring2);
+    t->d_ring = r1;
+    t->d_ring2 = r2;
+    t->ring_cap = cap;
+  } else {
+    TFE_HIP(tfe::launch_ring_compact(a, t->d_ring2, t->ring_cap - 1, stream), "ring compaction");
+    uint64_t* tmp = t->d_ring;
+    t->d_ring = t->d_ring2;
+    t->d_ring2 = tmp;
+  }
+  t->ring_bound = (uint64_t)t->cache_rows + appends;
+  return TFE_OK;
+}
+
+static tfe_status lookup_tiered(tfe_table* t, const LookupArgs& look, hipStream_t stream) {
+  TFE_TRY(ensure_scratch(t, look.T));
+  // Calls on one table are ordered: after the previous lookup and after a
+  // pending prefetch (which filled the cache this lookup may read).
+  if (t->lookup_recorded) TFE_HIP(hipStreamWaitEvent(stream, t->ev_lookup, 0), "wait lookup");
+  if (t->prefetch_pending) {
+    TFE_HIP(hipStreamWaitEvent(stream, t->ev_prefetch, 0), "wait prefetch");
+    t->prefetch_pending = false;
+  }
+  TFE_TRY(reserve_ring(t, look.T, stream));
+  t->clock++;
+  tfe::TierArgs a = tier_args(t);
+  a.look = look;
+  TFE_HIP(tfe::launch_tier_probe(a, stream), "tier probe");
+  TFE_HIP(tfe::launch_resolve_lookup(a, stream), "tier resolve");
+  TFE_HIP(hipEventRecord(t->ev_resolved, stream), "record");
+  // Host rows that missed the cache are copied on the side stream while the
+  // rows that were already cached are injected on the caller's stream.
+  TFE_HIP(hipStreamWaitEvent(t->fill_stream, t->ev_resolved, 0), "wait resolve");
+  TFE_HIP(tfe::launch_fill(a, t->dtype, t->dim, look.T, t->fill_stream), "tier fill");
+  TFE_HIP(hipEventRecord(t->ev_filled, t->fill_stream), "record");
+  TFE_HIP(tfe::launch_tier_inject(a, t->dtype, t->dim, (1u << 0) | (1u << 3), stream), "inject");
+  TFE_HIP(hipStreamWaitEvent(stream, t->ev_filled, 0), "wait fill");
+  TFE_HIP(tfe::launch_tier_inject(a, t->dtype, t->dim, (1u << 1) | (1u << 2), stream), "inject");
+  TFE_HIP(hipEventRecord(t->ev_lookup, stream), "record");
+  t->lookup_recorded = true;
+  return TFE_OK;
+}
+
+static tfe_status prefetch_tiered(tfe_table* t, const int32_t* tail, int32_t tail_len,
+                                  const int32_t* cand, int32_t B, int32_t K, hipStream_t side) {
+  const uint64_t N = (uint64_t)B * K;
+  if (N == 0) return TFE_OK;
+  if (N > 0x7FFFFFFFull) return fail(TFE_ERR_UNSUPPORTED, "B * K above 2^31 - 1");
+  TFE_TRY(check_device(t));
+  TFE_TRY(ensure_scratch(t, (uint32_t)N));
+  if (t->lookup_recorded) TFE_HIP(hipStreamWaitEvent(side, t->ev_lookup, 0), "wait lookup");
+  if (t->prefetch_pending) TFE_HIP(hipStreamWaitEvent(side, t->ev_prefetch, 0), "wait prefetch");
+  TFE_TRY(reserve_ring(t, N, side));
+  t->clock++;
+  tfe::TierArgs a = tier_args(t);
+  TFE_HIP(tfe::launch_prefetch_probe(a, tail, tail_len, cand, (uint32_t)B, (uint32_t)K, side),
+          "prefetch probe");
+  TFE_HIP(tfe::launch_resolve_prefetch(a, (uint32_t)N, side), "prefetch resolve");
+  TFE_HIP(tfe::launch_fill(a, t->dtype, t->dim, (uint32_t)N, side), "prefetch fill");
+  TFE_HIP(hipEventRecord(t->ev_prefetch, side), "record");
+  t->prefetch_pending = true;
+  return TFE_OK;
+}
+
 static tfe_status load(const tfe_table_desc* d, hipStream_t stream, tfe_table** out) {
   if (!d || !out) return fail(TFE_ERR_INVALID_ARG, "null desc or out");
   *out = nullptr;
@@ -68,7 +299,12 @@ static tfe_status load(const tfe_table_desc* d, hipStream_t stream, tfe_table** 
   double lf = d->max_load_factor == 0.0 ? 0.5 : d->max_load_factor;
   if (!(lf > 0.0 && lf <= 0.9)) return fail(TFE_ERR_INVALID_ARG, "max_load_factor not in (0, 0.9]");
   if (d->hbm_cache_rows < 0) return fail(TFE_ERR_INVALID_ARG, "hbm_cache_rows < 0");
-  if (d->hbm_cache_rows > 0) return fail(TFE_ERR_UNSUPPORTED, "tiered tables not built yet");
+  if (d->hbm_cache_rows > 0x7FFFFFFFll) return fail(TFE_ERR_UNSUPPORTED, "hbm_cache_rows above 2^31 - 1");
+  if (d->prefill_rows < 0 || d->prefill_rows > d->hbm_cache_rows ||
+      d->prefill_rows > d->n_phrases)
+    return fail(TFE_ERR_INVALID_ARG, "prefill_rows outside [0, min(hbm_cache_rows, n_phrases)]");
+  if (d->adopt_host_values && (d->hbm_cache_rows == 0 || d->values_on_device))
+    return fail(TFE_ERR_INVALID_ARG, "adopt_host_values needs a tiered table and host values");
   tfe_status st = validate_phrases(d->phrase_tokens, d->phrase_len, d->n_phrases, d->n_min,
                                    d->n_max, d->vocab);
   if (st != TFE_OK) return st;
@@ -106,20 +342,15 @@ static tfe_status load(const tfe_table_desc* d, hipStream_t stream, tfe_table** 
     return fail(TFE_ERR_OOM, "device index (%zu bytes)", slot_bytes);
   }
   hipError_t e = hipMemcpyAsync(t->d_slots, slots.data(), slot_bytes, hipMemcpyHostToDevice, stream);
-  if (e == hipSuccess && d->n_phrases > 0) {
-    const size_t vbytes = (size_t)d->n_phrases * d->dim * elem_size(d->dtype);
-    if (hipMalloc(&t->d_values, vbytes) != hipSuccess) {
-      release(t);
-      return fail(TFE_ERR_OOM, "device values (%zu bytes)", vbytes);
-    }
-    e = hipMemcpyAsync(t->d_values, d->values, vbytes,
-                       d->values_on_device ? hipMemcpyDeviceToDevice : hipMemcpyHostToDevice,
-                       stream);
-  }
   if (e == hipSuccess) e = hipStreamSynchronize(stream);
   if (e != hipSuccess) {
     release(t);
-    return hip_fail(e, "table upload");
+    return hip_fail(e, "index upload");
+  }
+  st = d->hbm_cache_rows > 0 ? load_tiered(t, d, stream) : load_resident(t, d, stream);
+  if (st != TFE_OK) {
+    release(t);
+    return st;
   }
   *out = t;
   return TFE_OK;
@@ -164,6 +395,7 @@ static tfe_status lookup_inject(tfe_table* t, const int32_t* tokens, int32_t B, 
   a.scale = scale;
   a.inv_d = 1.0f / (float)t->dim;
   a.inv_sqrt_d = (float)(1.0 / sqrt((double)t->dim));
+  if (t->cache_rows > 0) return lookup_tiered(t, a, stream);
   TFE_HIP(launch_lookup_inject(a, t->dtype, t->dim, stream), "lookup_inject launch");
   t->stats.positions += (uint64_t)T;
   return TFE_OK;
@@ -196,18 +428,33 @@ tfe_status tfe_lookup_inject(tfe_table* table, const int32_t* tokens, int32_t B,
 tfe_status tfe_prefetch(tfe_table* table, const int32_t* tail, int32_t tail_len,
                         const int32_t* candidates, int32_t B, int32_t K, void* side_stream) {
   tfe::clear_error();
-  (void)side_stream;
   if (!table) return tfe::fail(TFE_ERR_INVALID_ARG, "null table");
   if (tail_len < 0 || B < 0 || K < 0) return tfe::fail(TFE_ERR_INVALID_ARG, "negative size");
   if ((int64_t)B * K > 0 && (!candidates || (tail_len > 0 && !tail)))
     return tfe::fail(TFE_ERR_INVALID_ARG, "null tail or candidates");
-  return TFE_OK;  // resident tables have nothing to prefetch
+  if (table->cache_rows == 0) return TFE_OK;  // resident tables have nothing to prefetch
+  return tfe::prefetch_tiered(table, tail, tail_len, candidates, B, K, (hipStream_t)side_stream);
 }
 
 tfe_status tfe_get_stats(tfe_table* table, tfe_stats* out) {
   tfe::clear_error();
   if (!table || !out) return tfe::fail(TFE_ERR_INVALID_ARG, "null table or out");
   *out = table->stats;
+  if (table->cache_rows > 0) {
+    tfe::TierCtl c;
+    hipError_t e = hipDeviceSynchronize();
+    if (e == hipSuccess) e = hipMemcpy(&c, table->d_ctl, sizeof c, hipMemcpyDeviceToHost);
+    if (e != hipSuccess) return tfe::fail(TFE_ERR_HIP, "stats: %s", hipGetErrorString(e));
+    out->positions = c.stats.positions;
+    out->hits = c.stats.hits;
+    out->cache_hits = c.stats.cache_hits;
+    out->cache_misses = c.stats.cache_misses;
+    out->prefetch_keys = c.stats.prefetch_keys;
+    out->prefetch_found = c.stats.prefetch_found;
+    out->prefetch_filled = c.stats.prefetch_filled;
+    out->prefetch_used = c.stats.prefetch_used;
+    out->host_bytes = c.stats.host_bytes;
+  }
   return TFE_OK;
 }
 
@@ -215,6 +462,12 @@ tfe_status tfe_reset_stats(tfe_table* table) {
   tfe::clear_error();
   if (!table) return tfe::fail(TFE_ERR_INVALID_ARG, "null table");
   table->stats = tfe_stats{};
+  if (table->cache_rows > 0) {
+    hipError_t e = hipDeviceSynchronize();
+    if (e == hipSuccess)
+      e = hipMemset((char*)table->d_ctl + offsetof(tfe::TierCtl, stats), 0, sizeof(tfe::TierStats));
+    if (e != hipSuccess) return tfe::fail(TFE_ERR_HIP, "reset stats: %s", hipGetErrorString(e));
+  }
   return TFE_OK;
 }
 

@@ -45,6 +45,51 @@ struct LookupArgs {
   float inv_sqrt_d;           // 1 / sqrt(dim)
 };
 
+// Device-side bookkeeping of a tiered table (see tfe_tiered.hip).
+struct TierStats {
+  unsigned long long positions, hits, cache_hits, cache_misses, prefetch_keys, prefetch_found,
+      prefetch_filled, prefetch_used, host_bytes;
+};
+struct TierCtl {
+  unsigned long long head, tail;  // recency ring cursors (monotone)
+  unsigned long long njobs;       // host -> cache copies of the current call
+  TierStats stats;
+};
+struct TierJob {
+  int32_t row, slot;
+};
+struct TierArgs {
+  LookupArgs look;            // probe and inject arguments of the call
+  const void* host_values;    // device address of the pinned host rows [P x dim]
+  void* cache;                // HBM cache [C x dim]
+  int32_t* where;             // [P]  slot or -1
+  int32_t* owner;             // [C]  row or -1
+  uint32_t* stamp;            // [C]  clock of the last reference
+  uint32_t* filled_at;        // [C]  clock of the last fill
+  uint8_t* pref;              // [C]  filled by a prefetch and not used yet
+  uint64_t* ring;             // recency ring of (slot << 32 | stamp)
+  uint64_t ring_mask;
+  TierCtl* ctl;
+  int32_t* row_of;            // [cap] matched row per position / candidate
+  int32_t* slot_of;           // [cap]
+  uint8_t* phase;             // [cap]
+  TierJob* jobs;              // [cap]
+  uint32_t clock;
+  uint32_t row_bytes;
+};
+
+hipError_t launch_tier_init(const TierArgs& t, uint32_t C, uint32_t prefill, hipStream_t s);
+hipError_t launch_ring_compact(const TierArgs& t, uint64_t* dst, uint64_t dst_mask,
+                               hipStream_t s);
+hipError_t launch_tier_probe(const TierArgs& t, hipStream_t s);
+hipError_t launch_resolve_lookup(const TierArgs& t, hipStream_t s);
+hipError_t launch_prefetch_probe(const TierArgs& t, const int32_t* tail, int32_t tail_len,
+                                 const int32_t* cand, uint32_t B, uint32_t K, hipStream_t s);
+hipError_t launch_resolve_prefetch(const TierArgs& t, uint32_t N, hipStream_t s);
+hipError_t launch_fill(const TierArgs& t, int dtype, int dim, uint32_t max_jobs, hipStream_t s);
+hipError_t launch_tier_inject(const TierArgs& t, int dtype, int dim, uint32_t phases,
+                              hipStream_t s);
+
 // Launches the fused resident-table kernel; returns the launch error.
 hipError_t launch_lookup_inject(const LookupArgs& a, int dtype, int dim, hipStream_t stream);
 
@@ -64,7 +109,34 @@ struct tfe_table {
   int64_t capacity = 0;          // index slots
   tfe_slot* d_slots = nullptr;   // [capacity]
   void* d_values = nullptr;      // resident: [P x dim]
-  int64_t cache_rows = 0;        // tiered mode when > 0
-  tfe_stats stats = {};
+  tfe_stats stats = {};          // host-side counters (calls, resident positions)
+
+  // Tiered mode (cache_rows > 0).
+  int64_t cache_rows = 0;
+  int64_t prefill_rows = 0;
+  void* h_values = nullptr;      // pinned host rows [P x dim]
+  const void* h_values_dev = nullptr;
+  bool own_h_values = false;
+  void* d_cache = nullptr;
+  int32_t* d_where = nullptr;
+  int32_t* d_owner = nullptr;
+  uint32_t* d_stamp = nullptr;
+  uint32_t* d_filled_at = nullptr;
+  uint8_t* d_pref = nullptr;
+  uint64_t* d_ring = nullptr;
+  uint64_t* d_ring2 = nullptr;
+  uint64_t ring_cap = 0;         // entries, power of two
+  uint64_t ring_bound = 0;       // upper bound of ring occupancy (host view)
+  tfe::TierCtl* d_ctl = nullptr;
+  int32_t* d_row_of = nullptr;
+  int32_t* d_slot_of = nullptr;
+  uint8_t* d_phase = nullptr;
+  tfe::TierJob* d_jobs = nullptr;
+  uint32_t scratch_cap = 0;
+  uint32_t clock = 0;
+  hipStream_t fill_stream = nullptr;
+  hipEvent_t ev_resolved = nullptr, ev_filled = nullptr, ev_lookup = nullptr,
+             ev_prefetch = nullptr;
+  bool lookup_recorded = false, prefetch_pending = false;
 };
 #endif

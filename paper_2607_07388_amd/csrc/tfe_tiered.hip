@@ -1,0 +1,520 @@
+// Tiered tables: HBM cache of value rows in front of pinned host memory
+// (paper Sec. 4.3, Eq. 12; the SSD tier is not built), with exact
+// least-recently-used replacement kept entirely on the device, and the
+// prefetch of predicted next-token phrases (Sec. 4.4, Eq. 14-16).
+//
+// Residency (the second level of Eq. 10: phrase id -> tier and offset):
+//   where[row]   cache slot holding the row, or -1 (host only)
+//   owner[slot]  row held by the slot, or -1 (empty)
+//   stamp[slot]  clock of the last call that referenced the slot
+// Recency order: a ring of (slot, stamp) entries in the order the slots were
+// last referenced.  An entry is live while stamp[slot] still equals its
+// stamp; a slot referenced again gets a new entry and its old one dies.  The
+// least recent slot is the first live entry from the tail.  Every slot has
+// exactly one live entry, so compaction (dropping dead entries) leaves
+// exactly `cache_rows` entries.
+//
+// A lookup call runs: probe (wide) -> resolve (one block: residency, victim
+// choice, fill list, recency update, all in position order so the policy is
+// deterministic) -> fill (wide, on a side stream: host rows -> cache slots
+// over PCIe) while the rows that were already cached are injected on the
+// main stream -> inject of the filled rows once the fill is done.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "tfe_device.h"
+#include "tfe_internal.h"
+
+namespace tfe {
+namespace {
+
+using dev::u32x4;
+
+constexpr int kResolveThreads = 1024;
+constexpr int kHashSize = 2048;  // open-addressing dedupe table in LDS
+
+// Exclusive prefix sum of v over the block (kResolveThreads threads);
+// *total receives the block sum.  All threads must call it.
+__device__ uint32_t block_scan(uint32_t v, uint32_t* total) {
+  __shared__ uint32_t s_wave[kResolveThreads / 64 + 1];
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  uint32_t x = v;
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    const uint32_t y = __shfl_up(x, d, 64);
+    if (lane >= d) x += y;
+  }
+  if (lane == 63) s_wave[wave] = x;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint32_t run = 0;
+    for (int w = 0; w < kResolveThreads / 64; ++w) {
+      const uint32_t t = s_wave[w];
+      s_wave[w] = run;
+      run += t;
+    }
+    s_wave[kResolveThreads / 64] = run;
+  }
+  __syncthreads();
+  const uint32_t res = x - v + s_wave[wave];
+  *total = s_wave[kResolveThreads / 64];
+  __syncthreads();
+  return res;
+}
+
+__device__ uint32_t block_min(uint32_t v) {
+  __shared__ uint32_t s_min;
+  if (threadIdx.x == 0) s_min = 0xFFFFFFFFu;
+  __syncthreads();
+  atomicMin(&s_min, v);
+  __syncthreads();
+  const uint32_t r = s_min;
+  __syncthreads();
+  return r;
+}
+
+__device__ __forceinline__ uint64_t ring_entry(uint32_t slot, uint32_t stamp) {
+  return ((uint64_t)slot << 32) | stamp;
+}
+
+// Takes up to `need` least-recent slots not referenced in this call (stamp
+// below the call's clock) from the tail of the ring into vict[0..got).
+// Dead entries passed on the way are dropped.  Returns got (block-uniform).
+__device__ uint32_t pop_victims(const TierArgs& t, uint32_t need, uint32_t* vict) {
+  __shared__ unsigned long long s_tail, s_head, s_last;
+  __shared__ uint32_t s_got, s_stop;
+  if (threadIdx.x == 0) {
+    s_tail = t.ctl->tail;
+    s_head = t.ctl->head;
+    s_got = 0;
+    s_stop = 0;
+  }
+  __syncthreads();
+  for (;;) {
+    const uint32_t got = s_got;
+    const unsigned long long base = s_tail, head = s_head;
+    if (got >= need || s_stop || base >= head) break;
+    const unsigned long long i = base + threadIdx.x;
+    const bool in = i < head;
+    const uint64_t e = in ? t.ring[i & t.ring_mask] : 0;
+    const uint32_t slot = (uint32_t)(e >> 32), st = (uint32_t)e;
+    const bool cur = in && st == t.clock;  // entries of this call end the search
+    const bool live = in && !cur && t.stamp[slot] == st;
+    uint32_t nlive;
+    const uint32_t rank = block_scan(live ? 1u : 0u, &nlive);
+    const uint32_t first_cur = block_min(cur ? threadIdx.x : 0xFFFFFFFFu);
+    const uint32_t take = nlive < need - got ? nlive : need - got;
+    if (live && rank < take) {
+      vict[got + rank] = slot;
+      if (rank == take - 1) s_last = i;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      if (take > 0 && take == need - got) {
+        s_tail = s_last + 1;
+        s_got = need;
+      } else {
+        s_got = got + take;
+        if (first_cur != 0xFFFFFFFFu) {
+          s_tail = base + first_cur;
+          s_stop = 1;
+        } else {
+          s_tail = head < base + kResolveThreads ? head : base + kResolveThreads;
+        }
+      }
+    }
+    __syncthreads();
+  }
+  const uint32_t got = s_got;
+  if (threadIdx.x == 0) t.ctl->tail = s_tail;
+  __syncthreads();
+  return got;
+}
+
+// First occurrence of each row among the block's positions: returns true for
+// the lowest position naming the row.  Rows < 0 never count.
+__device__ bool first_of_row(int32_t r, uint32_t pos, int32_t* hkey, uint32_t* hpos) {
+  for (int i = threadIdx.x; i < kHashSize; i += kResolveThreads) {
+    hkey[i] = -1;
+    hpos[i] = 0xFFFFFFFFu;
+  }
+  __syncthreads();
+  int h = -1;
+  if (r >= 0) {
+    h = (int)(((uint32_t)r * 2654435761u) >> 21) & (kHashSize - 1);
+    for (;;) {
+      const int old = atomicCAS(&hkey[h], -1, r);
+      if (old == -1 || old == r) break;
+      h = (h + 1) & (kHashSize - 1);
+    }
+    atomicMin(&hpos[h], pos);
+  }
+  __syncthreads();
+  const bool first = r >= 0 && hpos[h] == pos;
+  __syncthreads();
+  return first;
+}
+
+// Residency resolution of one lookup call (single block), positions in
+// groups of kResolveThreads in order.  Per position: slot_of (cache slot or
+// -1) and phase (0: cached before this call, 1: filled in this call, 2: read
+// from host memory, 3: no match).
+__global__ __launch_bounds__(kResolveThreads) void k_resolve_lookup(const TierArgs t, uint32_t T) {
+  __shared__ int32_t hkey[kHashSize];
+  __shared__ uint32_t hpos[kHashSize];
+  __shared__ uint32_t vict[kResolveThreads];
+  if (threadIdx.x == 0) t.ctl->njobs = 0;
+  unsigned long long n_hits = 0, n_cache = 0, n_used = 0, n_direct = 0, n_fill = 0;
+  for (uint32_t base = 0; base < T; base += kResolveThreads) {
+    const uint32_t p = base + threadIdx.x;
+    const bool valid = p < T;
+    const int32_t r = valid ? t.row_of[p] : -1;
+    const bool first = first_of_row(r, p, hkey, hpos);
+    const int32_t s0 = r >= 0 ? t.where[r] : -1;  // slot at the start of the group
+    bool append = false;
+    if (first && s0 >= 0) {
+      append = t.stamp[s0] != t.clock;  // first reference in this call
+      t.stamp[s0] = t.clock;
+    }
+    __syncthreads();
+    const bool miss_first = first && s0 < 0;
+    uint32_t need;
+    const uint32_t mrank = block_scan(miss_first ? 1u : 0u, &need);
+    const uint32_t got = need ? pop_victims(t, need, vict) : 0;
+    if (miss_first && mrank < got) {
+      const uint32_t v = vict[mrank];
+      const int32_t old = t.owner[v];
+      if (old >= 0) t.where[old] = -1;
+      t.owner[v] = r;
+      t.where[r] = (int32_t)v;
+      t.stamp[v] = t.clock;
+      t.filled_at[v] = t.clock;
+      t.pref[v] = 0;
+      const unsigned long long j = t.ctl->njobs + mrank;
+      t.jobs[j] = TierJob{r, (int32_t)v};
+      append = true;
+    }
+    __syncthreads();
+    const int32_t s1 = r >= 0 ? t.where[r] : -1;
+    uint8_t ph = 3;
+    if (r >= 0) ph = s1 < 0 ? 2 : (t.filled_at[s1] == t.clock ? 1 : 0);
+    if (valid) {
+      t.slot_of[p] = s1;
+      t.phase[p] = ph;
+    }
+    bool used = false;
+    if (first && s0 >= 0 && t.pref[s0]) {
+      t.pref[s0] = 0;
+      used = true;
+    }
+    uint32_t napp;
+    const uint32_t arank = block_scan(append ? 1u : 0u, &napp);
+    if (append) {
+      const uint32_t slot = (uint32_t)(s0 >= 0 ? s0 : s1);
+      t.ring[(t.ctl->head + arank) & t.ring_mask] = ring_entry(slot, t.clock);
+    }
+    uint32_t c_hit, c_cache, c_used, c_direct;
+    block_scan(r >= 0 ? 1u : 0u, &c_hit);
+    block_scan(r >= 0 && s0 >= 0 ? 1u : 0u, &c_cache);
+    block_scan(used ? 1u : 0u, &c_used);
+    block_scan(ph == 2 ? 1u : 0u, &c_direct);
+    if (threadIdx.x == 0) {
+      t.ctl->head += napp;
+      t.ctl->njobs += got;
+    }
+    n_hits += c_hit;
+    n_cache += c_cache;
+    n_used += c_used;
+    n_direct += c_direct;
+    n_fill += got;
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    TierStats& st = t.ctl->stats;
+    st.positions += T;
+    st.hits += n_hits;
+    st.cache_hits += n_cache;
+    st.cache_misses += n_hits - n_cache;
+    st.prefetch_used += n_used;
+    st.host_bytes += (n_fill + n_direct) * t.row_bytes;
+  }
+}
+
+// Prefetch resolution (single block): the candidates' rows in candidate
+// order; each distinct row that is not cached takes the least recent slot
+// (stopping when none is left) and is marked prefetched.
+__global__ __launch_bounds__(kResolveThreads) void k_resolve_prefetch(const TierArgs t, uint32_t N) {
+  __shared__ int32_t hkey[kHashSize];
+  __shared__ uint32_t hpos[kHashSize];
+  __shared__ uint32_t vict[kResolveThreads];
+  __shared__ uint32_t s_stop;
+  if (threadIdx.x == 0) {
+    t.ctl->njobs = 0;
+    s_stop = 0;
+  }
+  unsigned long long n_found = 0, n_fill = 0;
+  for (uint32_t base = 0; base < N; base += kResolveThreads) {
+    const uint32_t p = base + threadIdx.x;
+    const int32_t r = p < N ? t.row_of[p] : -1;
+    const bool first = first_of_row(r, p, hkey, hpos);
+    // A row filled by an earlier group of this prefetch is cached by now.
+    const bool miss_first = first && r >= 0 && !s_stop && t.where[r] < 0;
+    uint32_t need;
+    const uint32_t mrank = block_scan(miss_first ? 1u : 0u, &need);
+    const uint32_t got = need ? pop_victims(t, need, vict) : 0;
+    if (miss_first && mrank < got) {
+      const uint32_t v = vict[mrank];
+      const int32_t old = t.owner[v];
+      if (old >= 0) t.where[old] = -1;
+      t.owner[v] = r;
+      t.where[r] = (int32_t)v;
+      t.stamp[v] = t.clock;
+      t.filled_at[v] = t.clock;
+      t.pref[v] = 1;
+      t.jobs[t.ctl->njobs + mrank] = TierJob{r, (int32_t)v};
+      t.ring[(t.ctl->head + mrank) & t.ring_mask] = ring_entry(v, t.clock);
+    }
+    uint32_t c_found;
+    block_scan(r >= 0 ? 1u : 0u, &c_found);
+    if (threadIdx.x == 0) {
+      t.ctl->head += got;
+      t.ctl->njobs += got;
+      if (got < need) s_stop = 1;
+    }
+    n_found += c_found;
+    n_fill += got;
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    TierStats& st = t.ctl->stats;
+    st.prefetch_keys += N;
+    st.prefetch_found += n_found;
+    st.prefetch_filled += n_fill;
+    st.host_bytes += n_fill * t.row_bytes;
+  }
+}
+
+// Host row -> cache slot copies of the current fill list, one wave per job,
+// reading the pinned host rows directly over PCIe (zero-copy).
+template <int NCH>
+__global__ __launch_bounds__(256) void k_fill(const TierArgs t, uint32_t max_jobs) {
+  const int lane = threadIdx.x & 63;
+  const uint32_t j = blockIdx.x * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  if (j >= max_jobs || j >= t.ctl->njobs) return;
+  const TierJob job = t.jobs[j];
+  const u32x4* src = (const u32x4*)t.host_values + (size_t)job.row * (NCH * 64);
+  u32x4* dst = (u32x4*)t.cache + (size_t)job.slot * (NCH * 64);
+  u32x4 v[NCH];
+#pragma unroll
+  for (int k = 0; k < NCH; ++k) v[k] = __builtin_nontemporal_load(src + k * 64 + lane);
+#pragma unroll
+  for (int k = 0; k < NCH; ++k) dst[k * 64 + lane] = v[k];
+}
+
+// Probe of a tiered lookup: the resident kernel's key formation and probe,
+// writing the caller's hit/slot/len and the matched row per position.
+template <int WPB>
+__global__ __launch_bounds__(WPB * 64) void k_tier_probe(const TierArgs t) {
+  const LookupArgs& a = t.look;
+  const int lane = threadIdx.x & 63;
+  const uint32_t p = blockIdx.x * WPB + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  if (p >= a.T) return;
+  int32_t tw[4];
+  dev::window_tokens(a, p, tw);
+  const dev::Probe pr = dev::probe_begin(a, tw, lane);
+  int len;
+  const int32_t row = dev::probe_finish(a, pr, lane, &len);
+  if (lane == 0) {
+    dev::write_result(a, p, row, len);
+    t.row_of[p] = row;
+  }
+}
+
+// Probe of the prefetch candidates: candidate k of row b ends the window
+// (tail[b, tail_len-3 ..], cand[b, k]); its longest match is the row the
+// next lookup selects if that candidate is the next token.
+template <int WPB>
+__global__ __launch_bounds__(WPB * 64) void k_prefetch_probe(const TierArgs t,
+                                                             const int32_t* __restrict__ tail,
+                                                             int32_t tail_len,
+                                                             const int32_t* __restrict__ cand,
+                                                             uint32_t B, uint32_t K) {
+  const LookupArgs& a = t.look;
+  const int lane = threadIdx.x & 63;
+  const uint32_t q = blockIdx.x * WPB + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  if (q >= B * K) return;
+  const uint32_t b = q / K;
+  int32_t tw[4];
+  tw[0] = cand[q];
+  for (int j = 1; j < 4; ++j)
+    tw[j] = tail_len - j >= 0 ? tail[(size_t)b * tail_len + (tail_len - j)] : -1;
+  const dev::Probe pr = dev::probe_begin(a, tw, lane);
+  int len;
+  const int32_t row = dev::probe_finish(a, pr, lane, &len);
+  if (lane == 0) t.row_of[q] = row;
+}
+
+// Inject of the positions whose phase is in `phases` (bit mask): value rows
+// come from the cache (phases 0, 1) or straight from host memory (phase 2);
+// phase 3 (no match) copies the hidden row (out of place).
+template <int DT, int NCH, int WPB>
+__global__ __launch_bounds__(WPB * 64) void k_tier_inject(const TierArgs t, uint32_t phases) {
+  constexpr int ROW_VECS = NCH * 64;
+  const LookupArgs& a = t.look;
+  const int lane = threadIdx.x & 63;
+  const uint32_t p = blockIdx.x * WPB + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  if (p >= a.T) return;
+  const uint32_t ph = t.phase[p];
+  if (!((phases >> ph) & 1u)) return;
+  u32x4 hv[NCH];
+  const u32x4* hin = (const u32x4*)a.hin + (size_t)p * ROW_VECS;
+#pragma unroll
+  for (int k = 0; k < NCH; ++k) hv[k] = __builtin_nontemporal_load(hin + k * 64 + lane);
+  u32x4* out = (u32x4*)a.hout + (size_t)p * ROW_VECS;
+  if (ph == 3) {
+    if (!a.inplace) {
+#pragma unroll
+      for (int k = 0; k < NCH; ++k) __builtin_nontemporal_store(hv[k], out + k * 64 + lane);
+    }
+    return;
+  }
+  const u32x4* mrow = ph == 2 ? (const u32x4*)t.host_values + (size_t)t.row_of[p] * ROW_VECS
+                              : (const u32x4*)t.cache + (size_t)t.slot_of[p] * ROW_VECS;
+  u32x4 mv[NCH];
+#pragma unroll
+  for (int k = 0; k < NCH; ++k) mv[k] = mrow[k * 64 + lane];
+  const float g = dev::gate_of<DT, NCH>(a, hv, mv);
+  dev::store_injected<DT, NCH>(out, hv, mv, g, lane);
+}
+
+// Initial state: slot s < prefill holds row s; the ring lists the empty
+// slots in ascending order, then the filled slots by descending row.
+__global__ void k_tier_init(const TierArgs t, uint32_t C, uint32_t prefill) {
+  const uint32_t i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= C) return;
+  const uint32_t empty = C - prefill;
+  const uint32_t slot = i < empty ? prefill + i : prefill - 1 - (i - empty);
+  t.ring[i] = ring_entry(slot, 0);
+  t.owner[i] = i < prefill ? (int32_t)i : -1;
+  t.stamp[i] = 0;
+  t.filled_at[i] = 0;
+  t.pref[i] = 0;
+  if (i < prefill) t.where[i] = (int32_t)i;
+  if (i == 0) {
+    t.ctl->head = C;
+    t.ctl->tail = 0;
+    t.ctl->njobs = 0;
+  }
+}
+
+// Drops dead entries: live entries move, in order, to `dst` (single block).
+__global__ __launch_bounds__(kResolveThreads) void k_ring_compact(const TierArgs t, uint64_t* dst,
+                                                                  uint64_t dst_mask) {
+  __shared__ unsigned long long s_out;
+  if (threadIdx.x == 0) s_out = 0;
+  __syncthreads();
+  const unsigned long long tail = t.ctl->tail, head = t.ctl->head;
+  for (unsigned long long base = tail; base < head; base += kResolveThreads) {
+    const unsigned long long i = base + threadIdx.x;
+    const bool in = i < head;
+    const uint64_t e = in ? t.ring[i & t.ring_mask] : 0;
+    const bool live = in && t.stamp[(uint32_t)(e >> 32)] == (uint32_t)e;
+    uint32_t n;
+    const uint32_t rank = block_scan(live ? 1u : 0u, &n);
+    if (live) dst[(s_out + rank) & dst_mask] = e;
+    __syncthreads();
+    if (threadIdx.x == 0) s_out += n;
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    t.ctl->tail = 0;
+    t.ctl->head = s_out;
+  }
+}
+
+template <int NCH>
+hipError_t launch_fill_t(const TierArgs& t, uint32_t max_jobs, hipStream_t s) {
+  if (max_jobs == 0) return hipSuccess;
+  hipLaunchKernelGGL(k_fill<NCH>, dim3((max_jobs + 3) / 4), dim3(256), 0, s, t, max_jobs);
+  return hipGetLastError();
+}
+
+template <int DT, int NCH>
+hipError_t launch_inject_t(const TierArgs& t, uint32_t phases, hipStream_t s) {
+  constexpr int WPB = 1;
+  hipLaunchKernelGGL((k_tier_inject<DT, NCH, WPB>), dim3(t.look.T), dim3(64), 0, s, t, phases);
+  return hipGetLastError();
+}
+
+int chunks_of(int dtype, int dim) { return dim / (dtype == TFE_F32 ? 256 : 512); }
+
+}  // namespace
+
+hipError_t launch_tier_init(const TierArgs& t, uint32_t C, uint32_t prefill, hipStream_t s) {
+  hipLaunchKernelGGL(k_tier_init, dim3((C + 255) / 256), dim3(256), 0, s, t, C, prefill);
+  return hipGetLastError();
+}
+
+hipError_t launch_ring_compact(const TierArgs& t, uint64_t* dst, uint64_t dst_mask,
+                               hipStream_t s) {
+  hipLaunchKernelGGL(k_ring_compact, dim3(1), dim3(kResolveThreads), 0, s, t, dst, dst_mask);
+  return hipGetLastError();
+}
+
+hipError_t launch_tier_probe(const TierArgs& t, hipStream_t s) {
+  if (t.look.T == 0) return hipSuccess;
+  hipLaunchKernelGGL(k_tier_probe<1>, dim3(t.look.T), dim3(64), 0, s, t);
+  return hipGetLastError();
+}
+
+hipError_t launch_resolve_lookup(const TierArgs& t, hipStream_t s) {
+  hipLaunchKernelGGL(k_resolve_lookup, dim3(1), dim3(kResolveThreads), 0, s, t, t.look.T);
+  return hipGetLastError();
+}
+
+hipError_t launch_prefetch_probe(const TierArgs& t, const int32_t* tail, int32_t tail_len,
+                                 const int32_t* cand, uint32_t B, uint32_t K, hipStream_t s) {
+  hipLaunchKernelGGL(k_prefetch_probe<1>, dim3(B * K), dim3(64), 0, s, t, tail, tail_len, cand, B,
+                     K);
+  return hipGetLastError();
+}
+
+hipError_t launch_resolve_prefetch(const TierArgs& t, uint32_t N, hipStream_t s) {
+  hipLaunchKernelGGL(k_resolve_prefetch, dim3(1), dim3(kResolveThreads), 0, s, t, N);
+  return hipGetLastError();
+}
+
+hipError_t launch_fill(const TierArgs& t, int dtype, int dim, uint32_t max_jobs, hipStream_t s) {
+  switch (chunks_of(dtype, dim)) {
+    case 1: return launch_fill_t<1>(t, max_jobs, s);
+    case 2: return launch_fill_t<2>(t, max_jobs, s);
+    case 4: return launch_fill_t<4>(t, max_jobs, s);
+    case 8: return launch_fill_t<8>(t, max_jobs, s);
+  }
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_tier_inject(const TierArgs& t, int dtype, int dim, uint32_t phases,
+                              hipStream_t s) {
+  if (t.look.T == 0) return hipSuccess;
+  const int nch = chunks_of(dtype, dim);
+  if (dtype == TFE_F32) {
+    switch (nch) {
+      case 1: return launch_inject_t<0, 1>(t, phases, s);
+      case 2: return launch_inject_t<0, 2>(t, phases, s);
+      case 4: return launch_inject_t<0, 4>(t, phases, s);
+      case 8: return launch_inject_t<0, 8>(t, phases, s);
+    }
+  } else {
+    switch (nch) {
+      case 1: return launch_inject_t<1, 1>(t, phases, s);
+      case 2: return launch_inject_t<1, 2>(t, phases, s);
+      case 4: return launch_inject_t<1, 4>(t, phases, s);
+      case 8: return launch_inject_t<1, 8>(t, phases, s);
+    }
+  }
+  return hipErrorInvalidValue;
+}
+
+}  // namespace tfe

@@ -78,6 +78,8 @@ def dev_lib():
         lib.synth_normal_fill_dev.restype = ctypes.c_int
         lib.synth_copy_dev.argtypes = [vp, vp, i64, ctypes.c_int, vp]
         lib.synth_copy_dev.restype = ctypes.c_int
+        lib.synth_host_device_ptr.argtypes = [vp, ctypes.POINTER(vp)]
+        lib.synth_host_device_ptr.restype = ctypes.c_int
         _dev = lib
     return _dev
 
@@ -164,6 +166,14 @@ def copy_device(dst, src, nbytes, blocks=4096, stream=0):
                                   int(blocks), ctypes.c_void_p(stream))
     if rc != 0:
         raise RuntimeError("synth_copy_dev failed (%d)" % rc)
+
+
+def host_device_ptr(host_ptr):
+    """Device address of a pinned host buffer."""
+    out = ctypes.c_void_p()
+    if dev_lib().synth_host_device_ptr(ctypes.c_void_p(host_ptr), ctypes.byref(out)) != 0:
+        raise RuntimeError("not pinned host memory")
+    return out.value
 
 
 def bf16_to_f32(u16):

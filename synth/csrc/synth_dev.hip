@@ -58,3 +58,9 @@ extern "C" int synth_copy_dev(void* dst, const void* src, int64_t nbytes, int bl
                      (synth_u32x4*)dst, nbytes / 16);
   return hipGetLastError() == hipSuccess ? 0 : -2;
 }
+
+// Device address of pinned host memory (hipHostMalloc), so that the device
+// filler can draw value tables straight into host memory.
+extern "C" int synth_host_device_ptr(void* host, void** dev) {
+  return hipHostGetDevicePointer(dev, host, 0) == hipSuccess ? 0 : -1;
+}

@@ -1,0 +1,209 @@
+"""Tiered tables (HBM cache in front of pinned host memory, LRU, prefetch).
+
+The tier never changes results: every output must equal the oracle's and be
+byte-identical to a fully resident table's.  The cache statistics must equal
+the reference model of the replacement policy (oracle/lru.py) exactly."""
+import numpy as np
+import pytest
+import torch
+
+import synth
+from oracle.lru import LruModel
+from paper_2607_07388_amd import tfe
+
+from . import harness as H
+
+pytestmark = pytest.mark.gpu
+
+STAT_KEYS = ("positions", "hits", "cache_hits", "cache_misses", "prefetch_keys",
+             "prefetch_found", "prefetch_filled", "prefetch_used", "host_bytes")
+
+
+def pinned_values(table):
+    """The table's value rows in pinned host memory, drawn by the device."""
+    v = torch.empty((table.n_phrases, table.dim), dtype=H.TORCH_DT[table.dtype], pin_memory=True)
+    synth.normal_fill_device(synth.host_device_ptr(v.data_ptr()), 0, table.n_phrases, table.dim,
+                             table.seed, synth.TAG_VALUES, table.sigma, table.dtype,
+                             H.cur_stream())
+    torch.cuda.synchronize()
+    return v
+
+
+class TieredTable:
+    def __init__(self, table, cache_rows, prefill_rows, adopt=True):
+        self.table = table
+        if adopt:
+            self.values = pinned_values(table)
+            vals = self.values
+        else:
+            self.values = None
+            vals = table.all_values()
+        desc = tfe.make_desc(table.tokens, table.lens, table.n_min, table.n_max, table.vocab,
+                             vals, table.dim, table.dtype, 0, 0.5, hbm_cache_rows=cache_rows,
+                             adopt_host_values=int(adopt), prefill_rows=prefill_rows)
+        self.handle = tfe.tfe_table_load(desc, H.cur_stream())
+
+    def close(self):
+        if self.handle:
+            tfe.tfe_table_free(self.handle)
+            self.handle = None
+
+
+def run_both(resident, tiered, tokens, ctx, S, hidden_np, dtype, dim, gate=0, scale=1.0):
+    """One call on each table; asserts identical outputs; returns them."""
+    B = tokens.shape[0]
+    T = B * S
+    tok = torch.from_numpy(np.ascontiguousarray(tokens, np.int32)).cuda()
+    h = H.to_device(hidden_np, dtype)
+    o1, o2 = H.Outputs(T, dim, dtype), H.Outputs(T, dim, dtype)
+    H.run(resident, tok, B, ctx, S, h, o1, gate, scale)
+    tfe.tfe_lookup_inject(tiered.handle, tok, B, ctx, S, h, o2.out, o2.hit, o2.slot, o2.len, gate,
+                          scale, H.cur_stream())
+    torch.cuda.synchronize()
+    assert torch.equal(o1.hit, o2.hit)
+    assert torch.equal(o1.slot, o2.slot)
+    assert torch.equal(o1.len, o2.len)
+    assert o1.out.view(torch.int16 if dtype == synth.BF16 else torch.int32).equal(
+        o2.out.view(torch.int16 if dtype == synth.BF16 else torch.int32))
+    return o2
+
+
+def check_stats(tiered, model):
+    got = tfe.tfe_get_stats(tiered.handle)
+    for k in STAT_KEYS:
+        assert got[k] == model.stats[k], (k, got[k], model.stats[k])
+
+
+@pytest.fixture(scope="module")
+def w2_tables():
+    table = synth.config2_table()
+    res = H.GpuTable(table)
+    yield table, res, H.oracle_table(table)
+    res.close()
+
+
+def test_tiered_decode_steps_match_oracle_resident_and_lru_model(w2_tables):
+    table, res, ot = w2_tables
+    C, pre = 4096, 2048
+    tier = TieredTable(table, C, pre)
+    model = LruModel(C, pre, table.dim * 2)
+    for step in range(8):
+        batch = synth.decode_batch(1, 64, set_index=40 + step)
+        hidden = batch.hidden()
+        o = run_both(res, tier, batch.tokens, batch.ctx, batch.S, hidden, table.dtype, table.dim)
+        hit, row, ln, want = H.oracle_answer(table, ot, batch.tokens, batch.ctx, batch.S, hidden)
+        np.testing.assert_array_equal(o.slot.cpu().numpy(), row)
+        H.assert_close(H.to_host(o.out, table.dtype), want, table.dtype)
+        model.lookup([int(r) for r in row])
+        check_stats(tier, model)
+    st = tfe.tfe_get_stats(tier.handle)
+    assert st["cache_hits"] > 0 and st["cache_misses"] > 0
+    tier.close()
+
+
+def test_tiered_prefetch_workload5_shape(w2_tables):
+    """Decode at batch 64 over per-row token streams; each step prefetches the
+    phrases of 8 predicted next tokens (true next token with p = 0.7) on a
+    side stream; stats (including prefetch_used) follow the model exactly."""
+    table, res, ot = w2_tables
+    C, pre, B, K, steps = 8192, 4096, 64, 8, 10
+    tier = TieredTable(table, C, pre)
+    model = LruModel(C, pre, table.dim * 2)
+    seqs = synth.zipf_tokens(1, 700, B * (steps + 3), 1.1).reshape(B, steps + 3)
+    side = torch.cuda.Stream()
+    for s in range(steps):
+        window = np.ascontiguousarray(seqs[:, s:s + 3])
+        hidden = synth.normal_range(1, 701 + s, 0, B, table.dim, 1.0, synth.BF16)
+        o = run_both(res, tier, window, 2, 1, hidden, table.dtype, table.dim)
+        model.lookup([int(r) for r in o.slot.cpu().numpy()])
+        check_stats(tier, model)
+        tail = np.ascontiguousarray(seqs[:, s + 1:s + 3])
+        cand = synth.workloads.candidates(1, B, K, seqs[:, s + 3], step=s)
+        win = np.concatenate([np.repeat(tail, K, axis=0), cand.reshape(-1, 1)], axis=1)
+        _, crow, _ = ot.lookup(win, 2, 1)
+        tfe.tfe_prefetch(tier.handle, torch.from_numpy(tail).cuda(), 2,
+                         torch.from_numpy(cand).cuda(), B, K, side)
+        model.prefetch([int(r) for r in crow])
+        check_stats(tier, model)
+    st = tfe.tfe_get_stats(tier.handle)
+    assert st["prefetch_filled"] > 0 and st["prefetch_used"] > 0
+    tier.close()
+
+
+def test_tiny_cache_direct_reads_and_ring_compaction(w2_tables):
+    """16 cache rows for 64-row batches: most misses find no victim and are
+    read straight from host memory; 120 calls overflow the 4096-entry recency
+    ring several times, exercising compaction."""
+    table, res, ot = w2_tables
+    C, pre = 16, 8
+    tier = TieredTable(table, C, pre)
+    model = LruModel(C, pre, table.dim * 2)
+    for step in range(120):
+        batch = synth.decode_batch(1, 64, set_index=200 + step % 8)
+        hidden = batch.hidden() if step < 8 else synth.normal_range(9, step, 0, 64, 1024, 1.0,
+                                                                    synth.BF16)
+        o = run_both(res, tier, batch.tokens, batch.ctx, batch.S, hidden, table.dtype, table.dim)
+        model.lookup([int(r) for r in o.slot.cpu().numpy()])
+        if step % 20 == 19:
+            check_stats(tier, model)
+    check_stats(tier, model)
+    tier.close()
+
+
+def test_multi_group_lookup_and_in_place(w2_tables):
+    """3000 positions (three resolve groups of 1024) with many repeats, in
+    place, against a cache that fits part of them."""
+    table, res, ot = w2_tables
+    C, pre = 1500, 700
+    tier = TieredTable(table, C, pre)
+    model = LruModel(C, pre, table.dim * 2)
+    for step in range(3):
+        batch = synth.decode_batch(1, 3000, set_index=60 + step)
+        hidden = batch.hidden()
+        tok = torch.from_numpy(batch.tokens).cuda()
+        h1 = H.to_device(hidden, synth.BF16)
+        h2 = h1.clone()
+        o1, o2 = H.Outputs(3000, 1024, synth.BF16), H.Outputs(3000, 1024, synth.BF16)
+        H.run(res, tok, 3000, 2, 1, h1, o1, inplace=True)
+        tfe.tfe_lookup_inject(tier.handle, tok, 3000, 2, 1, h2, h2, o2.hit, o2.slot, o2.len, 0,
+                              1.0, H.cur_stream())
+        torch.cuda.synchronize()
+        assert torch.equal(h1.view(torch.int16), h2.view(torch.int16))
+        assert torch.equal(o1.slot, o2.slot)
+        model.lookup([int(r) for r in o2.slot.cpu().numpy()])
+        check_stats(tier, model)
+    tier.close()
+
+
+def test_tiered_fp32_copied_values_workload1():
+    """Values copied by the library into its own pinned buffer (no adopt)."""
+    table, batch = synth.config1()
+    res = H.GpuTable(table)
+    tier = TieredTable(table, 32, 0, adopt=False)
+    ot = H.oracle_table(table)
+    model = LruModel(32, 0, table.dim * 4)
+    for rep in range(3):
+        hidden = batch.hidden()
+        o = run_both(res, tier, batch.tokens, batch.ctx, batch.S, hidden, synth.F32, table.dim)
+        hit, row, ln, want = H.oracle_answer(table, ot, batch.tokens, batch.ctx, batch.S, hidden)
+        H.assert_close(H.to_host(o.out, synth.F32), want, synth.F32)
+        model.lookup([int(r) for r in row])
+        check_stats(tier, model)
+    tier.close()
+    res.close()
+
+
+def test_tiered_load_errors():
+    table, _ = synth.config1()
+    vals = table.all_values()
+    bad = [
+        dict(hbm_cache_rows=8, prefill_rows=9),                 # prefill above the cache
+        dict(hbm_cache_rows=8, prefill_rows=-1),
+        dict(hbm_cache_rows=8, prefill_rows=0, adopt_host_values=1),  # pageable, not pinned
+        dict(hbm_cache_rows=0, prefill_rows=0, adopt_host_values=1),  # adopt on a resident table
+    ]
+    for kw in bad:
+        desc = tfe.make_desc(table.tokens, table.lens, 2, 3, synth.V, vals, table.dim, table.dtype,
+                             0, 0.5, **kw)
+        with pytest.raises(tfe.TfeError):
+            tfe.tfe_table_load(desc, H.cur_stream())
