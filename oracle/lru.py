@@ -27,7 +27,9 @@ Policy (the precise reading; a call is one lookup or one prefetch):
 * Statistics: hits = matched positions; cache_hits = matched positions whose
   row was cached when their group started (cache_misses = the rest);
   prefetch_used counts a prefetched slot the first time a lookup finds it
-  cached; host_bytes = row bytes x (rows filled + positions read directly).
+  cached.  A position is served from host memory when its row was not cached
+  when the call began (it was filled by this call or found no slot);
+  host_bytes = row bytes x (rows filled + positions served from host).
 """
 import collections
 
@@ -71,6 +73,7 @@ class LruModel:
         or None for a miss."""
         out = []
         referenced = set()
+        filled_now = set()
         for g in range(0, len(rows), GROUP):
             grp = rows[g:g + GROUP]
             first_pos = {}
@@ -97,6 +100,7 @@ class LruModel:
                     self._fill(r, v)
                     self.prefetched.discard(v)
                     filled[r] = v
+                    filled_now.add(r)
                     referenced.add(v)
                     newly.append((first_pos[r], v))
                     status[r] = ("fill", v)
@@ -116,8 +120,8 @@ class LruModel:
                         self.stats["prefetch_used"] += 1
                 else:
                     self.stats["cache_misses"] += 1
-                    if kind == "host":
-                        self.stats["host_bytes"] += self.row_bytes
+                if kind != "cache" or r in filled_now:
+                    self.stats["host_bytes"] += self.row_bytes
             self.stats["host_bytes"] += self.row_bytes * len(filled)
         self.stats["positions"] += len(rows)
         return out

@@ -34,7 +34,7 @@ def build(verbose=False):
         if verbose and out.strip():
             print(out)
         objs.append(obj)
-    cmd = ["hipcc", "--offload-arch=gfx950", "-shared", "-fPIC", "-o", SO + ".tmp"] + objs
+    cmd = ["hipcc", "--offload-arch=gfx950", "-shared", "-fPIC", "-pthread", "-o", SO + ".tmp"] + objs
     r = subprocess.run(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True)
     if r.returncode != 0:
         raise RuntimeError("libtfe link failed:\n" + r.stdout)

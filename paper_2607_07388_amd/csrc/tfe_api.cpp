@@ -242,30 +242,34 @@ static tfe_status reserve_ring(tfe_table* t, uint64_t appends, hipStream_t strea
 
 static tfe_status lookup_tiered(tfe_table* t, const LookupArgs& look, hipStream_t stream) {
   TFE_TRY(ensure_scratch(t, look.T));
-  // Calls on one table are ordered: after the previous lookup and after a
-  // pending prefetch (which filled the cache this lookup may read).
-  if (t->lookup_recorded) TFE_HIP(hipStreamWaitEvent(stream, t->ev_lookup, 0), "wait lookup");
-  if (t->prefetch_pending) {
-    TFE_HIP(hipStreamWaitEvent(stream, t->ev_prefetch, 0), "wait prefetch");
-    t->prefetch_pending = false;
-  }
+  // Calls on one table are ordered: after the previous lookup (when it ran
+  // on another stream) and after a pending prefetch.
+  if (t->lookup_recorded && stream != t->last_stream)
+    TFE_HIP(hipStreamWaitEvent(stream, t->ev_lookup, 0), "wait lookup");
   TFE_TRY(reserve_ring(t, look.T, stream));
   t->clock++;
   tfe::TierArgs a = tier_args(t);
   a.look = look;
   TFE_HIP(tfe::launch_tier_probe(a, stream), "tier probe");
+  if (t->prefetch_pending) {
+    TFE_HIP(hipStreamWaitEvent(stream, t->ev_prefetch, 0), "wait prefetch");
+    t->prefetch_pending = false;
+  }
+  // The previous call's cache fill must land before this call reuses its
+  // slots, and before the fill list is rewritten.
+  if (t->fill_recorded) TFE_HIP(hipStreamWaitEvent(stream, t->ev_filled, 0), "wait fill");
   TFE_HIP(tfe::launch_resolve_lookup(a, stream), "tier resolve");
   TFE_HIP(hipEventRecord(t->ev_resolved, stream), "record");
-  // Host rows that missed the cache are copied on the side stream while the
-  // rows that were already cached are injected on the caller's stream.
+  // Missed rows are copied into their new cache slots on the side stream,
+  // overlapped with the injection, which reads them from host memory.
   TFE_HIP(hipStreamWaitEvent(t->fill_stream, t->ev_resolved, 0), "wait resolve");
   TFE_HIP(tfe::launch_fill(a, t->dtype, t->dim, look.T, t->fill_stream), "tier fill");
   TFE_HIP(hipEventRecord(t->ev_filled, t->fill_stream), "record");
-  TFE_HIP(tfe::launch_tier_inject(a, t->dtype, t->dim, (1u << 0) | (1u << 3), stream), "inject");
-  TFE_HIP(hipStreamWaitEvent(stream, t->ev_filled, 0), "wait fill");
-  TFE_HIP(tfe::launch_tier_inject(a, t->dtype, t->dim, (1u << 1) | (1u << 2), stream), "inject");
+  t->fill_recorded = true;
+  TFE_HIP(tfe::launch_tier_inject(a, t->dtype, t->dim, stream), "inject");
   TFE_HIP(hipEventRecord(t->ev_lookup, stream), "record");
   t->lookup_recorded = true;
+  t->last_stream = stream;
   return TFE_OK;
 }
 
@@ -277,6 +281,7 @@ static tfe_status prefetch_tiered(tfe_table* t, const int32_t* tail, int32_t tai
   TFE_TRY(check_device(t));
   TFE_TRY(ensure_scratch(t, (uint32_t)N));
   if (t->lookup_recorded) TFE_HIP(hipStreamWaitEvent(side, t->ev_lookup, 0), "wait lookup");
+  if (t->fill_recorded) TFE_HIP(hipStreamWaitEvent(side, t->ev_filled, 0), "wait fill");
   if (t->prefetch_pending) TFE_HIP(hipStreamWaitEvent(side, t->ev_prefetch, 0), "wait prefetch");
   TFE_TRY(reserve_ring(t, N, side));
   t->clock++;

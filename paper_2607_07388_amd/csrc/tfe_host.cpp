@@ -2,6 +2,10 @@
 #include <stdint.h>
 #include <string.h>
 
+#include <atomic>
+#include <thread>
+#include <vector>
+
 #include "../../include/tfe.h"
 #include "tfe_index.h"
 #include "tfe_internal.h"
@@ -25,6 +29,24 @@ static inline void phrase_key(const int32_t* w, int n, uint64_t* key, uint32_t* 
   *ext = n == 4 ? (uint32_t)w[0] : 0u;
 }
 
+// Runs fn(begin, end) over [0, n) on up to `threads` host threads.
+template <class F>
+static void parallel_ranges(int64_t n, F fn) {
+  unsigned hw = std::thread::hardware_concurrency();
+  int64_t threads = hw ? (int64_t)hw : 1;
+  if (threads > 32) threads = 32;
+  const int64_t min_per_thread = 1 << 16;
+  if (threads > n / min_per_thread) threads = n / min_per_thread;
+  if (threads <= 1) {
+    fn((int64_t)0, n);
+    return;
+  }
+  std::vector<std::thread> pool;
+  for (int64_t i = 0; i < threads; ++i)
+    pool.emplace_back(fn, n * i / threads, n * (i + 1) / threads);
+  for (auto& th : pool) th.join();
+}
+
 tfe_status validate_phrases(const int32_t* tokens, const uint8_t* lens, int64_t P, int n_min,
                             int n_max, int vocab) {
   if (P < 0) return fail(TFE_ERR_INVALID_ARG, "n_phrases < 0");
@@ -34,54 +56,100 @@ tfe_status validate_phrases(const int32_t* tokens, const uint8_t* lens, int64_t 
     return fail(TFE_ERR_INVALID_ARG, "vocab must be in [1, 2^18]");
   if (P > 0x7FFFFFFFll) return fail(TFE_ERR_UNSUPPORTED, "more than 2^31-1 phrases");
   if (P > 0 && (!tokens || !lens)) return fail(TFE_ERR_INVALID_ARG, "null phrase arrays");
-  for (int64_t i = 0; i < P; ++i) {
+  // First bad phrase (lowest index) wins, so the message does not depend on
+  // the thread schedule.
+  std::atomic<int64_t> first_bad(P);
+  parallel_ranges(P, [&](int64_t a, int64_t b) {
+    for (int64_t i = a; i < b && i < first_bad.load(std::memory_order_relaxed); ++i) {
+      const int n = lens[i];
+      bool bad = n < n_min || n > n_max;
+      for (int j = 0; j < n && !bad; ++j) {
+        const int32_t x = tokens[i * n_max + j];
+        bad = x < 0 || x >= vocab;
+      }
+      if (bad) {
+        int64_t cur = first_bad.load();
+        while (i < cur && !first_bad.compare_exchange_weak(cur, i)) {
+        }
+        return;
+      }
+    }
+  });
+  const int64_t i = first_bad.load();
+  if (i < P) {
     const int n = lens[i];
     if (n < n_min || n > n_max)
       return fail(TFE_ERR_INVALID_ARG, "phrase %lld has length %d outside [%d, %d]",
                   (long long)i, n, n_min, n_max);
-    const int32_t* w = tokens + i * n_max;
-    for (int j = 0; j < n; ++j)
-      if (w[j] < 0 || w[j] >= vocab)
-        return fail(TFE_ERR_INVALID_ARG, "phrase %lld token %d = %d outside [0, %d)",
-                    (long long)i, j, w[j], vocab);
+    return fail(TFE_ERR_INVALID_ARG, "phrase %lld has a token outside [0, %d)", (long long)i,
+                vocab);
   }
   return TFE_OK;
 }
 
+// Inserts the phrases from several host threads.  A slot is claimed by a
+// compare-and-swap of its key from empty; its extension word and row follow,
+// the row last (release), so a thread that meets an equal key waits for the
+// row before it compares the extension.  Within a bucket the claimed slots
+// stay a prefix, so a lookup may still stop at the first empty slot.  Which
+// slot a phrase lands in depends on the schedule; what a lookup returns does
+// not.
 tfe_status build_index(const int32_t* tokens, const uint8_t* lens, int64_t P, int n_max,
                        tfe_slot* slots, int64_t cap) {
   if (cap < TFE_SLOTS_PER_BUCKET || (cap & (cap - 1)) != 0)
     return fail(TFE_ERR_INVALID_ARG, "capacity must be a power of two >= 8");
   if (P >= cap) return fail(TFE_ERR_INVALID_ARG, "capacity %lld too small for %lld phrases",
                             (long long)cap, (long long)P);
-  for (int64_t s = 0; s < cap; ++s) {
-    slots[s].key = TFE_EMPTY_KEY;
-    slots[s].key_ext = 0;
-    slots[s].row = -1;
-  }
-  const int64_t nb = cap / TFE_SLOTS_PER_BUCKET;
-  for (int64_t i = 0; i < P; ++i) {
-    uint64_t key;
-    uint32_t ext;
-    phrase_key(tokens + i * n_max, lens[i], &key, &ext);
-    int64_t b = (int64_t)(tfe_hash(key, ext) & (uint64_t)(nb - 1));
-    for (;;) {
-      tfe_slot* bk = slots + b * TFE_SLOTS_PER_BUCKET;
-      int free_at = -1;
-      for (int q = 0; q < TFE_SLOTS_PER_BUCKET; ++q) {
-        if (bk[q].key == TFE_EMPTY_KEY) { free_at = q; break; }
-        if (bk[q].key == key && bk[q].key_ext == ext)
-          return fail(TFE_ERR_DUPLICATE_KEY, "phrase %lld repeats phrase %d", (long long)i,
-                      bk[q].row);
-      }
-      if (free_at >= 0) {
-        bk[free_at].key = key;
-        bk[free_at].key_ext = ext;
-        bk[free_at].row = (int32_t)i;
-        break;
-      }
-      b = (b + 1) & (nb - 1);
+  parallel_ranges(cap, [&](int64_t a, int64_t b) {
+    for (int64_t s = a; s < b; ++s) {
+      slots[s].key = TFE_EMPTY_KEY;
+      slots[s].key_ext = 0;
+      slots[s].row = -1;
     }
+  });
+  const int64_t nb = cap / TFE_SLOTS_PER_BUCKET;
+  std::atomic<int64_t> dup_row(-1), dup_of(-1);
+  parallel_ranges(P, [&](int64_t a, int64_t b) {
+    for (int64_t i = a; i < b && dup_row.load(std::memory_order_relaxed) < 0; ++i) {
+      uint64_t key;
+      uint32_t ext;
+      phrase_key(tokens + i * n_max, lens[i], &key, &ext);
+      int64_t bk = (int64_t)(tfe_hash(key, ext) & (uint64_t)(nb - 1));
+      bool placed = false;
+      while (!placed) {
+        tfe_slot* s = slots + bk * TFE_SLOTS_PER_BUCKET;
+        for (int q = 0; q < TFE_SLOTS_PER_BUCKET && !placed; ++q) {
+          uint64_t k = __atomic_load_n(&s[q].key, __ATOMIC_ACQUIRE);
+          if (k == TFE_EMPTY_KEY) {
+            uint64_t expected = TFE_EMPTY_KEY;
+            if (__atomic_compare_exchange_n(&s[q].key, &expected, key, false, __ATOMIC_ACQ_REL,
+                                            __ATOMIC_ACQUIRE)) {
+              __atomic_store_n(&s[q].key_ext, ext, __ATOMIC_RELAXED);
+              __atomic_store_n(&s[q].row, (int32_t)i, __ATOMIC_RELEASE);
+              placed = true;
+              break;
+            }
+            k = expected;
+          }
+          if (k == key) {
+            int32_t other;
+            while ((other = __atomic_load_n(&s[q].row, __ATOMIC_ACQUIRE)) < 0) {
+            }
+            if (__atomic_load_n(&s[q].key_ext, __ATOMIC_RELAXED) == ext) {
+              int64_t none = -1;
+              if (dup_row.compare_exchange_strong(none, i)) dup_of.store(other);
+              return;
+            }
+          }
+        }
+        bk = (bk + 1) & (nb - 1);
+      }
+    }
+  });
+  if (dup_row.load() >= 0) {
+    const int64_t x = dup_row.load(), y = dup_of.load();
+    return fail(TFE_ERR_DUPLICATE_KEY, "phrases %lld and %lld are the same", (long long)(x < y ? x : y),
+                (long long)(x < y ? y : x));
   }
   return TFE_OK;
 }

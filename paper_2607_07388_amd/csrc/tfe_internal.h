@@ -87,8 +87,7 @@ hipError_t launch_prefetch_probe(const TierArgs& t, const int32_t* tail, int32_t
                                  const int32_t* cand, uint32_t B, uint32_t K, hipStream_t s);
 hipError_t launch_resolve_prefetch(const TierArgs& t, uint32_t N, hipStream_t s);
 hipError_t launch_fill(const TierArgs& t, int dtype, int dim, uint32_t max_jobs, hipStream_t s);
-hipError_t launch_tier_inject(const TierArgs& t, int dtype, int dim, uint32_t phases,
-                              hipStream_t s);
+hipError_t launch_tier_inject(const TierArgs& t, int dtype, int dim, hipStream_t s);
 
 // Launches the fused resident-table kernel; returns the launch error.
 hipError_t launch_lookup_inject(const LookupArgs& a, int dtype, int dim, hipStream_t stream);
@@ -137,6 +136,7 @@ struct tfe_table {
   hipStream_t fill_stream = nullptr;
   hipEvent_t ev_resolved = nullptr, ev_filled = nullptr, ev_lookup = nullptr,
              ev_prefetch = nullptr;
-  bool lookup_recorded = false, prefetch_pending = false;
+  bool lookup_recorded = false, prefetch_pending = false, fill_recorded = false;
+  hipStream_t last_stream = nullptr;   // stream of the last lookup
 };
 #endif

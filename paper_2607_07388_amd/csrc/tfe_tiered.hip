@@ -16,9 +16,10 @@
 //
 // A lookup call runs: probe (wide) -> resolve (one block: residency, victim
 // choice, fill list, recency update, all in position order so the policy is
-// deterministic) -> fill (wide, on a side stream: host rows -> cache slots
-// over PCIe) while the rows that were already cached are injected on the
-// main stream -> inject of the filled rows once the fill is done.
+// deterministic) -> inject (wide; cached rows from HBM, the others straight
+// from pinned host memory over PCIe), while a side stream copies the missed
+// rows from host memory into their new cache slots for later calls.  The
+// next call's inject waits for that copy; nothing in this call does.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -133,8 +134,9 @@ __device__ uint32_t pop_victims(const TierArgs& t, uint32_t need, uint32_t* vict
 }
 
 // First occurrence of each row among the block's positions: returns true for
-// the lowest position naming the row.  Rows < 0 never count.
-__device__ bool first_of_row(int32_t r, uint32_t pos, int32_t* hkey, uint32_t* hpos) {
+// the lowest position naming the row, and the row's entry index in the LDS
+// table in *hidx (-1 for rows < 0), where callers keep per-row results.
+__device__ bool first_of_row(int32_t r, uint32_t pos, int32_t* hkey, uint32_t* hpos, int* hidx) {
   for (int i = threadIdx.x; i < kHashSize; i += kResolveThreads) {
     hkey[i] = -1;
     hpos[i] = 0xFFFFFFFFu;
@@ -152,92 +154,112 @@ __device__ bool first_of_row(int32_t r, uint32_t pos, int32_t* hkey, uint32_t* h
   }
   __syncthreads();
   const bool first = r >= 0 && hpos[h] == pos;
-  __syncthreads();
+  *hidx = h;
   return first;
 }
 
 // Residency resolution of one lookup call (single block), positions in
 // groups of kResolveThreads in order.  Per position: slot_of (cache slot or
-// -1) and phase (0: cached before this call, 1: filled in this call, 2: read
-// from host memory, 3: no match).
+// -1) and phase (0: cached before this call, read from the cache; 1: filled
+// in this call; 2: no slot free, not cached; 3: no match).  Rows of phases 1
+// and 2 are read from host memory by the inject; phase-1 rows are also
+// copied into their slot on the side stream for later calls.
 __global__ __launch_bounds__(kResolveThreads) void k_resolve_lookup(const TierArgs t, uint32_t T) {
   __shared__ int32_t hkey[kHashSize];
   __shared__ uint32_t hpos[kHashSize];
+  __shared__ int32_t hslot[kHashSize];  // per row: slot after this group (-1: none)
+  __shared__ uint8_t hphase[kHashSize];
+  __shared__ uint8_t hcached[kHashSize];  // per row: cached when the group began
   __shared__ uint32_t vict[kResolveThreads];
-  if (threadIdx.x == 0) t.ctl->njobs = 0;
-  unsigned long long n_hits = 0, n_cache = 0, n_used = 0, n_direct = 0, n_fill = 0;
+  __shared__ unsigned long long s_njobs, s_head;
+  __shared__ uint32_t s_cnt[5];  // hits, cache hits, prefetch used, host-served, fills
+  if (threadIdx.x == 0) {
+    s_njobs = 0;
+    s_head = t.ctl->head;
+    for (int i = 0; i < 5; ++i) s_cnt[i] = 0;
+  }
   for (uint32_t base = 0; base < T; base += kResolveThreads) {
     const uint32_t p = base + threadIdx.x;
     const bool valid = p < T;
     const int32_t r = valid ? t.row_of[p] : -1;
-    const bool first = first_of_row(r, p, hkey, hpos);
-    const int32_t s0 = r >= 0 ? t.where[r] : -1;  // slot at the start of the group
+    int h;
+    const bool first = first_of_row(r, p, hkey, hpos, &h);
+    // First occurrences read the row's slot; a cached row's slot becomes
+    // referenced (a stamp of this call keeps it from being a victim).
+    int32_t s0 = -1;
     bool append = false;
-    if (first && s0 >= 0) {
-      append = t.stamp[s0] != t.clock;  // first reference in this call
-      t.stamp[s0] = t.clock;
+    if (first) {
+      s0 = t.where[r];
+      hcached[h] = s0 >= 0;
+      if (s0 >= 0) {
+        // Only a later group of this call can find its own stamp here.
+        append = base == 0 || t.stamp[s0] != t.clock;
+        t.stamp[s0] = t.clock;
+        hslot[h] = s0;
+        hphase[h] = (base != 0 && t.filled_at[s0] == t.clock) ? 1 : 0;
+        if (t.pref[s0]) {
+          t.pref[s0] = 0;
+          atomicAdd(&s_cnt[2], 1u);
+        }
+      }
     }
     __syncthreads();
     const bool miss_first = first && s0 < 0;
     uint32_t need;
     const uint32_t mrank = block_scan(miss_first ? 1u : 0u, &need);
     const uint32_t got = need ? pop_victims(t, need, vict) : 0;
-    if (miss_first && mrank < got) {
-      const uint32_t v = vict[mrank];
-      const int32_t old = t.owner[v];
-      if (old >= 0) t.where[old] = -1;
-      t.owner[v] = r;
-      t.where[r] = (int32_t)v;
-      t.stamp[v] = t.clock;
-      t.filled_at[v] = t.clock;
-      t.pref[v] = 0;
-      const unsigned long long j = t.ctl->njobs + mrank;
-      t.jobs[j] = TierJob{r, (int32_t)v};
-      append = true;
+    if (miss_first) {
+      if (mrank < got) {
+        const uint32_t v = vict[mrank];
+        const int32_t old = t.owner[v];
+        if (old >= 0) t.where[old] = -1;
+        t.owner[v] = r;
+        t.where[r] = (int32_t)v;
+        t.stamp[v] = t.clock;
+        t.filled_at[v] = t.clock;
+        t.pref[v] = 0;
+        t.jobs[s_njobs + mrank] = TierJob{r, (int32_t)v};
+        hslot[h] = (int32_t)v;
+        hphase[h] = 1;
+        append = true;
+      } else {
+        hslot[h] = -1;
+        hphase[h] = 2;
+      }
     }
     __syncthreads();
-    const int32_t s1 = r >= 0 ? t.where[r] : -1;
-    uint8_t ph = 3;
-    if (r >= 0) ph = s1 < 0 ? 2 : (t.filled_at[s1] == t.clock ? 1 : 0);
     if (valid) {
+      const int32_t s1 = r >= 0 ? hslot[h] : -1;
+      const uint8_t ph = r >= 0 ? hphase[h] : 3;
       t.slot_of[p] = s1;
       t.phase[p] = ph;
-    }
-    bool used = false;
-    if (first && s0 >= 0 && t.pref[s0]) {
-      t.pref[s0] = 0;
-      used = true;
+      if (r >= 0) {
+        atomicAdd(&s_cnt[0], 1u);
+        if (hcached[h]) atomicAdd(&s_cnt[1], 1u);
+        if (ph != 0) atomicAdd(&s_cnt[3], 1u);
+      }
     }
     uint32_t napp;
     const uint32_t arank = block_scan(append ? 1u : 0u, &napp);
-    if (append) {
-      const uint32_t slot = (uint32_t)(s0 >= 0 ? s0 : s1);
-      t.ring[(t.ctl->head + arank) & t.ring_mask] = ring_entry(slot, t.clock);
-    }
-    uint32_t c_hit, c_cache, c_used, c_direct;
-    block_scan(r >= 0 ? 1u : 0u, &c_hit);
-    block_scan(r >= 0 && s0 >= 0 ? 1u : 0u, &c_cache);
-    block_scan(used ? 1u : 0u, &c_used);
-    block_scan(ph == 2 ? 1u : 0u, &c_direct);
+    if (append) t.ring[(s_head + arank) & t.ring_mask] = ring_entry((uint32_t)hslot[h], t.clock);
+    __syncthreads();
     if (threadIdx.x == 0) {
-      t.ctl->head += napp;
-      t.ctl->njobs += got;
+      s_head += napp;
+      s_njobs += got;
+      s_cnt[4] += got;
+      t.ctl->head = s_head;
     }
-    n_hits += c_hit;
-    n_cache += c_cache;
-    n_used += c_used;
-    n_direct += c_direct;
-    n_fill += got;
     __syncthreads();
   }
   if (threadIdx.x == 0) {
+    t.ctl->njobs = s_njobs;
     TierStats& st = t.ctl->stats;
     st.positions += T;
-    st.hits += n_hits;
-    st.cache_hits += n_cache;
-    st.cache_misses += n_hits - n_cache;
-    st.prefetch_used += n_used;
-    st.host_bytes += (n_fill + n_direct) * t.row_bytes;
+    st.hits += s_cnt[0];
+    st.cache_hits += s_cnt[1];
+    st.cache_misses += s_cnt[0] - s_cnt[1];
+    st.prefetch_used += s_cnt[2];
+    st.host_bytes += (unsigned long long)(s_cnt[4] + s_cnt[3]) * t.row_bytes;
   }
 }
 
@@ -257,7 +279,9 @@ __global__ __launch_bounds__(kResolveThreads) void k_resolve_prefetch(const Tier
   for (uint32_t base = 0; base < N; base += kResolveThreads) {
     const uint32_t p = base + threadIdx.x;
     const int32_t r = p < N ? t.row_of[p] : -1;
-    const bool first = first_of_row(r, p, hkey, hpos);
+    int h;
+    const bool first = first_of_row(r, p, hkey, hpos, &h);
+    __syncthreads();
     // A row filled by an earlier group of this prefetch is cached by now.
     const bool miss_first = first && r >= 0 && !s_stop && t.where[r] < 0;
     uint32_t need;
@@ -355,18 +379,18 @@ __global__ __launch_bounds__(WPB * 64) void k_prefetch_probe(const TierArgs t,
   if (lane == 0) t.row_of[q] = row;
 }
 
-// Inject of the positions whose phase is in `phases` (bit mask): value rows
-// come from the cache (phases 0, 1) or straight from host memory (phase 2);
-// phase 3 (no match) copies the hidden row (out of place).
+// Inject of every position: value rows come from the cache (phase 0) or
+// straight from pinned host memory over PCIe (phases 1 and 2: rows that were
+// not cached when the call began); phase 3 (no match) copies the hidden row
+// (out of place).
 template <int DT, int NCH, int WPB>
-__global__ __launch_bounds__(WPB * 64) void k_tier_inject(const TierArgs t, uint32_t phases) {
+__global__ __launch_bounds__(WPB * 64) void k_tier_inject(const TierArgs t) {
   constexpr int ROW_VECS = NCH * 64;
   const LookupArgs& a = t.look;
   const int lane = threadIdx.x & 63;
   const uint32_t p = blockIdx.x * WPB + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   if (p >= a.T) return;
   const uint32_t ph = t.phase[p];
-  if (!((phases >> ph) & 1u)) return;
   u32x4 hv[NCH];
   const u32x4* hin = (const u32x4*)a.hin + (size_t)p * ROW_VECS;
 #pragma unroll
@@ -379,7 +403,7 @@ __global__ __launch_bounds__(WPB * 64) void k_tier_inject(const TierArgs t, uint
     }
     return;
   }
-  const u32x4* mrow = ph == 2 ? (const u32x4*)t.host_values + (size_t)t.row_of[p] * ROW_VECS
+  const u32x4* mrow = ph != 0 ? (const u32x4*)t.host_values + (size_t)t.row_of[p] * ROW_VECS
                               : (const u32x4*)t.cache + (size_t)t.slot_of[p] * ROW_VECS;
   u32x4 mv[NCH];
 #pragma unroll
@@ -441,9 +465,9 @@ hipError_t launch_fill_t(const TierArgs& t, uint32_t max_jobs, hipStream_t s) {
 }
 
 template <int DT, int NCH>
-hipError_t launch_inject_t(const TierArgs& t, uint32_t phases, hipStream_t s) {
+hipError_t launch_inject_t(const TierArgs& t, hipStream_t s) {
   constexpr int WPB = 1;
-  hipLaunchKernelGGL((k_tier_inject<DT, NCH, WPB>), dim3(t.look.T), dim3(64), 0, s, t, phases);
+  hipLaunchKernelGGL((k_tier_inject<DT, NCH, WPB>), dim3(t.look.T), dim3(64), 0, s, t);
   return hipGetLastError();
 }
 
@@ -495,23 +519,22 @@ hipError_t launch_fill(const TierArgs& t, int dtype, int dim, uint32_t max_jobs,
   return hipErrorInvalidValue;
 }
 
-hipError_t launch_tier_inject(const TierArgs& t, int dtype, int dim, uint32_t phases,
-                              hipStream_t s) {
+hipError_t launch_tier_inject(const TierArgs& t, int dtype, int dim, hipStream_t s) {
   if (t.look.T == 0) return hipSuccess;
   const int nch = chunks_of(dtype, dim);
   if (dtype == TFE_F32) {
     switch (nch) {
-      case 1: return launch_inject_t<0, 1>(t, phases, s);
-      case 2: return launch_inject_t<0, 2>(t, phases, s);
-      case 4: return launch_inject_t<0, 4>(t, phases, s);
-      case 8: return launch_inject_t<0, 8>(t, phases, s);
+      case 1: return launch_inject_t<0, 1>(t, s);
+      case 2: return launch_inject_t<0, 2>(t, s);
+      case 4: return launch_inject_t<0, 4>(t, s);
+      case 8: return launch_inject_t<0, 8>(t, s);
     }
   } else {
     switch (nch) {
-      case 1: return launch_inject_t<1, 1>(t, phases, s);
-      case 2: return launch_inject_t<1, 2>(t, phases, s);
-      case 4: return launch_inject_t<1, 4>(t, phases, s);
-      case 8: return launch_inject_t<1, 8>(t, phases, s);
+      case 1: return launch_inject_t<1, 1>(t, s);
+      case 2: return launch_inject_t<1, 2>(t, s);
+      case 4: return launch_inject_t<1, 4>(t, s);
+      case 8: return launch_inject_t<1, 8>(t, s);
     }
   }
   return hipErrorInvalidValue;

@@ -80,6 +80,8 @@ def dev_lib():
         lib.synth_copy_dev.restype = ctypes.c_int
         lib.synth_host_device_ptr.argtypes = [vp, ctypes.POINTER(vp)]
         lib.synth_host_device_ptr.restype = ctypes.c_int
+        lib.synth_spin_dev.argtypes = [ctypes.c_double, vp]
+        lib.synth_spin_dev.restype = ctypes.c_int
         _dev = lib
     return _dev
 
@@ -166,6 +168,12 @@ def copy_device(dst, src, nbytes, blocks=4096, stream=0):
                                   int(blocks), ctypes.c_void_p(stream))
     if rc != 0:
         raise RuntimeError("synth_copy_dev failed (%d)" % rc)
+
+
+def spin_device(us, stream=0):
+    """Enqueue a device busy-wait of `us` microseconds (a compute stand-in)."""
+    if dev_lib().synth_spin_dev(float(us), ctypes.c_void_p(stream)) != 0:
+        raise RuntimeError("synth_spin_dev failed")
 
 
 def host_device_ptr(host_ptr):

@@ -64,3 +64,20 @@ extern "C" int synth_copy_dev(void* dst, const void* src, int64_t nbytes, int bl
 extern "C" int synth_host_device_ptr(void* host, void** dev) {
   return hipHostGetDevicePointer(dev, host, 0) == hipSuccess ? 0 : -1;
 }
+
+// Busy-waits `us` microseconds on the device (bounded by the 100 MHz
+// real-time counter and an iteration cap), standing in for the transformer
+// layers that run between an early-exit prefetch and the next lookup.
+__global__ void k_spin(uint64_t ticks) {
+  const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
+  for (uint32_t it = 0; it < (1u << 26); ++it) {
+    if (__builtin_amdgcn_s_memrealtime() - t0 >= ticks) break;
+    __builtin_amdgcn_s_sleep(1);
+  }
+}
+
+extern "C" int synth_spin_dev(double us, hipStream_t stream) {
+  if (!(us >= 0.0) || us > 1e5) return -1;
+  hipLaunchKernelGGL(k_spin, dim3(1), dim3(64), 0, stream, (uint64_t)(us * 100.0));
+  return hipGetLastError() == hipSuccess ? 0 : -2;
+}

@@ -13,8 +13,10 @@
    filter), which puts the hit rate in [0.30, 0.40]; values 8 GiB bf16.
 4  large table, decode at batch 256: 2^24 2-grams + 2^24 3-grams of a
    Zipf(1.05) stream (2^25 phrases, 64 GiB bf16 values); Zipf(1.05) queries.
-5  tiered: 2^25 2-grams + 2^25 3-grams of a Zipf(1.1) stream (2^26 phrases,
-   128 GiB bf16 values in pinned host memory), decode at batch 64.
+5  tiered: 2^(L-1) 2-grams + 2^(L-1) 3-grams of a Zipf(1.1) stream, decode at
+   batch 64 with the values in pinned host memory.  The workload's full size
+   is L = 26 (128 GiB of values); the default L = 25 (64 GiB) fits hosts
+   that cannot pin 128 GiB.  The HBM cache has 4M rows (8 GiB).
 """
 import functools
 
@@ -109,8 +111,10 @@ def config4_table():
 
 
 @functools.lru_cache(maxsize=None)
-def config5_table():
-    toks, lens = _freq_table(4, 1.1, 3 << 27, [(2, 1 << 25), (3, 1 << 25)])
+def config5_table(log2_phrases=25):
+    half = 1 << (log2_phrases - 1)
+    stream = (3 << 27) if log2_phrases >= 26 else (1 << 28)
+    toks, lens = _freq_table(4, 1.1, stream, [(2, half), (3, half)])
     return PhraseTable(toks, lens, 2, 3, BF16, 4)
 
 

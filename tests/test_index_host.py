@@ -143,3 +143,16 @@ def test_empty_table_index():
     slots, cap = build(np.zeros((0, 3), np.int32), np.zeros(0, np.uint8), 2, 3)
     assert cap == 8
     assert tfe.tfe_index_probe_host(slots, cap, np.array([1, 2], np.int32), 2)[0] == -1
+
+
+def test_parallel_build_finds_a_planted_duplicate():
+    """The multi-threaded build reports a repeated phrase wherever it lands."""
+    table = synth.config2_table()
+    for src, dst in ((5, table.n_phrases - 1), (777777, 3)):
+        toks = table.tokens.copy()
+        lens = table.lens.copy()
+        toks[dst], lens[dst] = toks[src], lens[src]
+        with pytest.raises(tfe.TfeError) as e:
+            build(toks, lens, 2, 3)
+        assert e.value.status == tfe.TFE_ERR_DUPLICATE_KEY
+        assert str(min(src, dst)) in tfe.tfe_last_error()
