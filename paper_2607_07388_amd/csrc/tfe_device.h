@@ -7,10 +7,46 @@
 
 #include "tfe_internal.h"
 
+// Cache hints of the streamed rows (tuning knobs): hidden rows in and out
+// are touched once (non-temporal); value rows default to the cached path.
+#ifndef TFE_NT_HIDDEN_LOAD
+#define TFE_NT_HIDDEN_LOAD 1
+#endif
+#ifndef TFE_NT_OUT_STORE
+#define TFE_NT_OUT_STORE 1
+#endif
+#ifndef TFE_NT_VALUE_LOAD
+#define TFE_NT_VALUE_LOAD 0
+#endif
+
 namespace tfe {
 namespace dev {
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ u32x4 load_hidden(const u32x4* p) {
+#if TFE_NT_HIDDEN_LOAD
+  return __builtin_nontemporal_load(p);
+#else
+  return *p;
+#endif
+}
+
+__device__ __forceinline__ u32x4 load_value(const u32x4* p) {
+#if TFE_NT_VALUE_LOAD
+  return __builtin_nontemporal_load(p);
+#else
+  return *p;
+#endif
+}
+
+__device__ __forceinline__ void store_out(u32x4 v, u32x4* p) {
+#if TFE_NT_OUT_STORE
+  __builtin_nontemporal_store(v, p);
+#else
+  *p = v;
+#endif
+}
 
 // Elements of type DT held by one 16-byte vector.
 template <int DT> struct Vec;
@@ -204,7 +240,7 @@ __device__ __forceinline__ void store_injected(u32x4* out, const u32x4* hv, cons
     unpack<DT>(mv[k], m);
 #pragma unroll
     for (int i = 0; i < VN; ++i) o[i] = fmaf(g, m[i], h[i]);
-    __builtin_nontemporal_store(pack<DT>(o), out + k * 64 + lane);
+    store_out(pack<DT>(o), out + k * 64 + lane);
   }
 }
 

@@ -52,7 +52,7 @@ __global__ __launch_bounds__(WPB * 64) void k_lookup_inject(const LookupArgs a) 
   u32x4 hv[NCH];
   const u32x4* hin = (const u32x4*)a.hin + (size_t)p * ROW_VECS;
 #pragma unroll
-  for (int k = 0; k < NCH; ++k) hv[k] = __builtin_nontemporal_load(hin + k * 64 + lane);
+  for (int k = 0; k < NCH; ++k) hv[k] = dev::load_hidden(hin + k * 64 + lane);
 
   int32_t tw[4];
   dev::window_tokens(a, p, tw);
@@ -65,14 +65,14 @@ __global__ __launch_bounds__(WPB * 64) void k_lookup_inject(const LookupArgs a) 
   if (row < 0) {
     if (!a.inplace) {
 #pragma unroll
-      for (int k = 0; k < NCH; ++k) __builtin_nontemporal_store(hv[k], out + k * 64 + lane);
+      for (int k = 0; k < NCH; ++k) dev::store_out(hv[k], out + k * 64 + lane);
     }
     return;
   }
   u32x4 mv[NCH];
   const u32x4* mrow = (const u32x4*)a.values + (size_t)row * ROW_VECS;
 #pragma unroll
-  for (int k = 0; k < NCH; ++k) mv[k] = mrow[k * 64 + lane];
+  for (int k = 0; k < NCH; ++k) mv[k] = dev::load_value(mrow + k * 64 + lane);
   const float g = dev::gate_of<DT, NCH>(a, hv, mv);
   dev::store_injected<DT, NCH>(out, hv, mv, g, lane);
 }

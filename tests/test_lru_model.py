@@ -1,0 +1,78 @@
+"""The reference model of the cache tier's policy, pinned to the textbook
+least-recently-used cache: with one matched row per lookup call it must hit
+and miss exactly like an LRU cache of the same size, and its statistics must
+follow their definitions."""
+import collections
+
+import numpy as np
+
+from oracle.lru import GROUP, LruModel
+
+
+def textbook_lru(capacity, prefill, seq):
+    """Classic LRU over rows: hit if present (becomes most recent), else the
+    least recent row leaves and the new row enters as most recent."""
+    c = collections.OrderedDict()
+    for r in range(prefill - 1, -1, -1):  # least recent = highest row
+        c[r] = None
+    out = []
+    for r in seq:
+        if r in c:
+            c.move_to_end(r)
+            out.append(True)
+        else:
+            if len(c) >= capacity:
+                c.popitem(last=False)
+            c[r] = None
+            out.append(False)
+    return out
+
+
+def test_single_row_calls_are_textbook_lru():
+    rng = np.random.default_rng(0)
+    for capacity, prefill in ((8, 8), (8, 0), (16, 5), (64, 64)):
+        seq = [int(x) for x in rng.zipf(1.3, 3000) % 200]
+        m = LruModel(capacity, prefill, row_bytes=1)
+        got = []
+        for r in seq:
+            before = m.stats["cache_hits"]
+            m.lookup([r])
+            got.append(m.stats["cache_hits"] > before)
+        assert got == textbook_lru(capacity, prefill, seq)
+
+
+def test_statistics_definitions():
+    m = LruModel(4, 2, row_bytes=10)
+    # rows 0, 1 cached; 5 and 6 miss and take the two empty slots; 0 hits twice.
+    m.lookup([0, 5, -1, 0, 6, 5])
+    assert m.stats["positions"] == 6
+    assert m.stats["hits"] == 5
+    assert m.stats["cache_hits"] == 2
+    assert m.stats["cache_misses"] == 3
+    # host bytes: 2 rows filled + 3 positions served from host (5, 6, 5).
+    assert m.stats["host_bytes"] == 10 * (2 + 3)
+    assert set(m.resident()) == {0, 1, 5, 6}
+    # Cache full; 7 evicts the least recent slot that is not referenced: row 1.
+    m.lookup([7, 0])
+    assert set(m.resident()) == {0, 5, 6, 7}
+    # Prefetch fills a non-cached row and marks it; its first lookup counts.
+    m.prefetch([9, 9, 0, -1])
+    assert m.stats["prefetch_keys"] == 4 and m.stats["prefetch_found"] == 3
+    assert m.stats["prefetch_filled"] == 1 and 9 in m.resident()
+    m.lookup([9, 9])
+    assert m.stats["prefetch_used"] == 1
+
+
+def test_no_free_slot_reads_from_host_without_caching():
+    m = LruModel(2, 2, row_bytes=1)
+    src = m.lookup([0, 1, 7])      # 0, 1 referenced: 7 finds no victim
+    assert src[2] == ("host", None) and 7 not in m.resident()
+
+
+def test_groups_split_long_calls():
+    m = LruModel(GROUP, 0, row_bytes=1)
+    rows = list(range(GROUP)) + [0]
+    m.lookup(rows)
+    # Row 0 was filled in the first group: cached when the second began.
+    assert m.stats["cache_hits"] == 1
+    assert m.stats["host_bytes"] == GROUP + (GROUP + 1)
