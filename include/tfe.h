@@ -96,6 +96,7 @@ typedef struct {
   uint64_t prefetch_filled;  /* tiered: rows copied host -> HBM by tfe_prefetch */
   uint64_t prefetch_used;    /* tiered: prefetched rows later hit by a lookup */
   uint64_t host_bytes;       /* tiered: bytes read from host memory (both paths) */
+  uint64_t prefetch_dropped; /* tiered: candidate rows worth fetching but over budget */
 } tfe_stats;
 
 /* Builds the exact-match phrase index and places the value rows.
@@ -130,9 +131,10 @@ tfe_status tfe_table_free(tfe_table *table);
  *              the loaded phrase list), -1 where nothing matched.
  *   match_len  DEVICE uint8 [B*S] or NULL: matched n, 0 where nothing matched.
  *   gate, scale: see tfe_gate.
- * Tiered tables additionally read host rows that are not cached (zero-copy,
- * on an internal side stream) and insert them into the cache; results do not
- * depend on the cache state. */
+ * Tiered tables read the rows that are not cached straight from pinned host
+ * memory (zero-copy over PCIe) while an internal side stream inserts them
+ * into the HBM cache for later calls; results do not depend on the cache
+ * state. */
 tfe_status tfe_lookup_inject(tfe_table *table, const int32_t *tokens, int32_t B, int32_t ctx,
                              int32_t S, const void *hidden_in, void *hidden_out,
                              uint8_t *hit_mask, int32_t *slot_ids, uint8_t *match_len,
@@ -152,6 +154,25 @@ tfe_status tfe_lookup_inject(tfe_table *table, const int32_t *tokens, int32_t B,
  * tfe_lookup_inject waits for it. */
 tfe_status tfe_prefetch(tfe_table *table, const int32_t *tail, int32_t tail_len,
                         const int32_t *candidates, int32_t B, int32_t K, void *side_stream);
+
+/* Priority-scored, budgeted prefetch (tiered tables; a no-op on resident
+ * tables).  Paper: Eq. 17 (s_i = p_i * r_i * c_i; high-priority candidates
+ * first, low-priority ones dropped when the I/O budget is exhausted) and the
+ * tunable top-K budget and queue size (Sec. 4.4).
+ * Same windows as tfe_prefetch; additionally
+ *   cand_prob   DEVICE float [B x K]: p_i, the predicted probability of each
+ *               candidate token (values <= 0 or NaN count as 0);
+ *   budget      at most this many rows are fetched (<= 1024).
+ * Each candidate's longest match r gets s = p * len(r) * c, with c = 1 when
+ * the row is only in host memory and 0 when it is cached (r_i reads as the
+ * phrase length: longer phrases are the more specific entries).  A row named
+ * by several candidates keeps its highest score.  Rows with a positive score
+ * are fetched by descending score (ties: lowest candidate index) until the
+ * budget or the free cache slots run out; the rest count as dropped.
+ * B * K <= 2048. */
+tfe_status tfe_prefetch_scored(tfe_table *table, const int32_t *tail, int32_t tail_len,
+                               const int32_t *candidates, const float *cand_prob, int32_t B,
+                               int32_t K, int32_t budget, void *side_stream);
 
 /* Copies the table's counters (synchronises with the table's pending work). */
 tfe_status tfe_get_stats(tfe_table *table, tfe_stats *out);

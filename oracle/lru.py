@@ -147,5 +147,43 @@ class LruModel:
             self.stats["prefetch_filled"] += 1
             self.stats["host_bytes"] += self.row_bytes
 
+    def prefetch_scored(self, cand_rows, cand_lens, cand_probs, budget):
+        """Priority-scored, budgeted prefetch (Eq. 17, s = p * r * c): each
+        candidate's matched row scores float32(p) * float32(len) when it is
+        not cached (c = 1) and 0 when cached; a row keeps its best score and
+        its first candidate index; rows with a positive score are filled by
+        descending score, then candidate index, up to `budget` fills or until
+        no slot is free; the others count as dropped."""
+        import numpy as np
+        self.stats["prefetch_keys"] += len(cand_rows)
+        self.stats["prefetch_found"] += sum(1 for r in cand_rows if r >= 0)
+        best = {}
+        for q, r in enumerate(cand_rows):
+            if r < 0:
+                continue
+            p = np.float32(cand_probs[q])
+            p = p if p > 0 else np.float32(0)
+            s = np.float32(p * np.float32(cand_lens[q]))
+            if r not in best:
+                best[r] = [s, q]
+            elif s > best[r][0]:
+                best[r][0] = s
+        entries = [(r, s, q) for r, (s, q) in best.items() if s > 0 and r not in self.where]
+        entries.sort(key=lambda e: (-float(e[1]), e[2]))
+        taken = set()
+        fills = 0
+        for r, _, _ in entries[:budget]:
+            v = self._victim(taken)
+            if v is None:
+                break
+            self._fill(r, v)
+            taken.add(v)
+            self.order.move_to_end(v)
+            self.prefetched.add(v)
+            fills += 1
+        self.stats["prefetch_filled"] += fills
+        self.stats["prefetch_dropped"] += len(entries) - fills
+        self.stats["host_bytes"] += self.row_bytes * fills
+
     def resident(self):
         return dict(self.where)

@@ -244,8 +244,10 @@ static tfe_status lookup_tiered(tfe_table* t, const LookupArgs& look, hipStream_
   TFE_TRY(ensure_scratch(t, look.T));
   // Calls on one table are ordered: after the previous lookup (when it ran
   // on another stream) and after a pending prefetch.
-  if (t->lookup_recorded && stream != t->last_stream)
+  if (t->lookup_recorded && stream != t->last_stream) {
+    TFE_HIP(hipEventRecord(t->ev_lookup, t->last_stream), "record");
     TFE_HIP(hipStreamWaitEvent(stream, t->ev_lookup, 0), "wait lookup");
+  }
   TFE_TRY(reserve_ring(t, look.T, stream));
   t->clock++;
   tfe::TierArgs a = tier_args(t);
@@ -267,20 +269,28 @@ static tfe_status lookup_tiered(tfe_table* t, const LookupArgs& look, hipStream_
   TFE_HIP(hipEventRecord(t->ev_filled, t->fill_stream), "record");
   t->fill_recorded = true;
   TFE_HIP(tfe::launch_tier_inject(a, t->dtype, t->dim, stream), "inject");
-  TFE_HIP(hipEventRecord(t->ev_lookup, stream), "record");
   t->lookup_recorded = true;
   t->last_stream = stream;
   return TFE_OK;
 }
 
 static tfe_status prefetch_tiered(tfe_table* t, const int32_t* tail, int32_t tail_len,
-                                  const int32_t* cand, int32_t B, int32_t K, hipStream_t side) {
+                                  const int32_t* cand, const float* prob, int32_t B, int32_t K,
+                                  int32_t budget, hipStream_t side) {
   const uint64_t N = (uint64_t)B * K;
   if (N == 0) return TFE_OK;
   if (N > 0x7FFFFFFFull) return fail(TFE_ERR_UNSUPPORTED, "B * K above 2^31 - 1");
+  if (prob && N > tfe::scored_prefetch_max())
+    return fail(TFE_ERR_UNSUPPORTED, "scored prefetch takes at most %u candidates",
+                tfe::scored_prefetch_max());
   TFE_TRY(check_device(t));
   TFE_TRY(ensure_scratch(t, (uint32_t)N));
-  if (t->lookup_recorded) TFE_HIP(hipStreamWaitEvent(side, t->ev_lookup, 0), "wait lookup");
+  // After the table's last lookup (all work submitted to its stream so far),
+  // its cache fill, and any earlier prefetch.
+  if (t->lookup_recorded) {
+    TFE_HIP(hipEventRecord(t->ev_lookup, t->last_stream), "record");
+    TFE_HIP(hipStreamWaitEvent(side, t->ev_lookup, 0), "wait lookup");
+  }
   if (t->fill_recorded) TFE_HIP(hipStreamWaitEvent(side, t->ev_filled, 0), "wait fill");
   if (t->prefetch_pending) TFE_HIP(hipStreamWaitEvent(side, t->ev_prefetch, 0), "wait prefetch");
   TFE_TRY(reserve_ring(t, N, side));
@@ -288,7 +298,11 @@ static tfe_status prefetch_tiered(tfe_table* t, const int32_t* tail, int32_t tai
   tfe::TierArgs a = tier_args(t);
   TFE_HIP(tfe::launch_prefetch_probe(a, tail, tail_len, cand, (uint32_t)B, (uint32_t)K, side),
           "prefetch probe");
-  TFE_HIP(tfe::launch_resolve_prefetch(a, (uint32_t)N, side), "prefetch resolve");
+  if (prob)
+    TFE_HIP(tfe::launch_resolve_prefetch_scored(a, (uint32_t)N, prob, (uint32_t)budget, side),
+            "prefetch resolve");
+  else
+    TFE_HIP(tfe::launch_resolve_prefetch(a, (uint32_t)N, side), "prefetch resolve");
   TFE_HIP(tfe::launch_fill(a, t->dtype, t->dim, (uint32_t)N, side), "prefetch fill");
   TFE_HIP(hipEventRecord(t->ev_prefetch, side), "record");
   t->prefetch_pending = true;
@@ -438,7 +452,22 @@ tfe_status tfe_prefetch(tfe_table* table, const int32_t* tail, int32_t tail_len,
   if ((int64_t)B * K > 0 && (!candidates || (tail_len > 0 && !tail)))
     return tfe::fail(TFE_ERR_INVALID_ARG, "null tail or candidates");
   if (table->cache_rows == 0) return TFE_OK;  // resident tables have nothing to prefetch
-  return tfe::prefetch_tiered(table, tail, tail_len, candidates, B, K, (hipStream_t)side_stream);
+  return tfe::prefetch_tiered(table, tail, tail_len, candidates, nullptr, B, K, 0,
+                              (hipStream_t)side_stream);
+}
+
+tfe_status tfe_prefetch_scored(tfe_table* table, const int32_t* tail, int32_t tail_len,
+                               const int32_t* candidates, const float* cand_prob, int32_t B,
+                               int32_t K, int32_t budget, void* side_stream) {
+  tfe::clear_error();
+  if (!table) return tfe::fail(TFE_ERR_INVALID_ARG, "null table");
+  if (tail_len < 0 || B < 0 || K < 0) return tfe::fail(TFE_ERR_INVALID_ARG, "negative size");
+  if (budget < 0 || budget > 1024) return tfe::fail(TFE_ERR_INVALID_ARG, "budget outside [0, 1024]");
+  if ((int64_t)B * K > 0 && (!candidates || !cand_prob || (tail_len > 0 && !tail)))
+    return tfe::fail(TFE_ERR_INVALID_ARG, "null tail, candidates or probabilities");
+  if (table->cache_rows == 0) return TFE_OK;
+  return tfe::prefetch_tiered(table, tail, tail_len, candidates, cand_prob, B, K, budget,
+                              (hipStream_t)side_stream);
 }
 
 tfe_status tfe_get_stats(tfe_table* table, tfe_stats* out) {
@@ -459,6 +488,7 @@ tfe_status tfe_get_stats(tfe_table* table, tfe_stats* out) {
     out->prefetch_filled = c.stats.prefetch_filled;
     out->prefetch_used = c.stats.prefetch_used;
     out->host_bytes = c.stats.host_bytes;
+    out->prefetch_dropped = c.stats.prefetch_dropped;
   }
   return TFE_OK;
 }

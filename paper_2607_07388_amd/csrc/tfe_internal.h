@@ -48,7 +48,7 @@ struct LookupArgs {
 // Device-side bookkeeping of a tiered table (see tfe_tiered.hip).
 struct TierStats {
   unsigned long long positions, hits, cache_hits, cache_misses, prefetch_keys, prefetch_found,
-      prefetch_filled, prefetch_used, host_bytes;
+      prefetch_filled, prefetch_used, host_bytes, prefetch_dropped;
 };
 struct TierCtl {
   unsigned long long head, tail;  // recency ring cursors (monotone)
@@ -86,6 +86,9 @@ hipError_t launch_resolve_lookup(const TierArgs& t, hipStream_t s);
 hipError_t launch_prefetch_probe(const TierArgs& t, const int32_t* tail, int32_t tail_len,
                                  const int32_t* cand, uint32_t B, uint32_t K, hipStream_t s);
 hipError_t launch_resolve_prefetch(const TierArgs& t, uint32_t N, hipStream_t s);
+hipError_t launch_resolve_prefetch_scored(const TierArgs& t, uint32_t N, const float* prob,
+                                         uint32_t budget, hipStream_t s);
+uint32_t scored_prefetch_max();
 hipError_t launch_fill(const TierArgs& t, int dtype, int dim, uint32_t max_jobs, hipStream_t s);
 hipError_t launch_tier_inject(const TierArgs& t, int dtype, int dim, hipStream_t s);
 

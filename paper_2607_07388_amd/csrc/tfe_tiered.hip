@@ -319,6 +319,113 @@ __global__ __launch_bounds__(kResolveThreads) void k_resolve_prefetch(const Tier
   }
 }
 
+// Priority-scored, budgeted prefetch (Eq. 17: s = p * r * c), single block,
+// at most kScoredMax candidates.  For candidate q with matched row r:
+// p = prob[q] (the predicted token's probability), r = the matched phrase
+// length (longer phrases are the more specific entries), c = 1 if the row is
+// only in host memory and 0 if it is cached (no benefit).  A row named by
+// several candidates keeps its highest score and its first candidate index.
+// Rows with a positive score are fetched in order of score (descending),
+// then first candidate index, until `budget` rows are fetched or no free
+// slot is left; the rest are dropped.  Scores are float32 products, compared
+// as float32.
+constexpr int kScoredMax = 2048;
+constexpr int kScoredHash = 4096;
+
+__global__ __launch_bounds__(kResolveThreads) void k_resolve_prefetch_scored(
+    const TierArgs t, uint32_t N, const float* __restrict__ prob, uint32_t budget) {
+  __shared__ int32_t hkey[kScoredHash];
+  __shared__ uint32_t hpos[kScoredHash];
+  __shared__ uint32_t hscore[kScoredHash];
+  __shared__ int32_t qrow[kScoredMax];
+  __shared__ unsigned long long keys[kScoredMax];
+  __shared__ uint32_t vict[kResolveThreads];
+  __shared__ uint32_t s_n, s_found;
+  for (int i = threadIdx.x; i < kScoredHash; i += kResolveThreads) {
+    hkey[i] = -1;
+    hpos[i] = 0xFFFFFFFFu;
+    hscore[i] = 0;
+  }
+  if (threadIdx.x == 0) {
+    s_n = 0;
+    s_found = 0;
+    t.ctl->njobs = 0;
+  }
+  __syncthreads();
+  for (uint32_t q = threadIdx.x; q < N; q += kResolveThreads) {
+    const int32_t r = t.row_of[q];
+    qrow[q] = r;
+    if (r < 0) continue;
+    atomicAdd(&s_found, 1u);
+    int h = (int)(((uint32_t)r * 2654435761u) >> 20) & (kScoredHash - 1);
+    for (;;) {
+      const int old = atomicCAS(&hkey[h], -1, r);
+      if (old == -1 || old == r) break;
+      h = (h + 1) & (kScoredHash - 1);
+    }
+    atomicMin(&hpos[h], q);
+    const float p = prob[q];
+    const float sc = (p > 0.0f ? p : 0.0f) * (float)t.phase[q];  // NaN and p <= 0 score 0
+    atomicMax(&hscore[h], __float_as_uint(sc));
+  }
+  __syncthreads();
+  // Rows worth fetching: positive score and not cached.
+  for (int e = threadIdx.x; e < kScoredHash; e += kResolveThreads) {
+    const int32_t r = hkey[e];
+    if (r < 0 || hscore[e] == 0 || t.where[r] >= 0) continue;
+    const uint32_t k = atomicAdd(&s_n, 1u);
+    keys[k] = ((unsigned long long)(~hscore[e]) << 32) | hpos[e];
+  }
+  __syncthreads();
+  const uint32_t n = s_n;
+  uint32_t p2 = 1;
+  while (p2 < n) p2 <<= 1;
+  for (uint32_t i = n + threadIdx.x; i < p2; i += kResolveThreads) keys[i] = ~0ull;
+  __syncthreads();
+  // Bitonic sort, ascending: highest score first, then lowest candidate index.
+  for (uint32_t size = 2; size <= p2; size <<= 1) {
+    for (uint32_t stride = size >> 1; stride > 0; stride >>= 1) {
+      for (uint32_t i = threadIdx.x; i < p2 / 2; i += kResolveThreads) {
+        const uint32_t a = 2 * i - (i & (stride - 1));
+        const uint32_t b = a + stride;
+        const bool up = (a & size) == 0;
+        const unsigned long long ka = keys[a], kb = keys[b];
+        if ((ka > kb) == up) {
+          keys[a] = kb;
+          keys[b] = ka;
+        }
+      }
+      __syncthreads();
+    }
+  }
+  const uint32_t want = n < budget ? n : budget;
+  const uint32_t got = want ? pop_victims(t, want, vict) : 0;
+  if (threadIdx.x < got) {
+    const uint32_t v = vict[threadIdx.x];
+    const int32_t r = qrow[(uint32_t)keys[threadIdx.x]];
+    const int32_t old = t.owner[v];
+    if (old >= 0) t.where[old] = -1;
+    t.owner[v] = r;
+    t.where[r] = (int32_t)v;
+    t.stamp[v] = t.clock;
+    t.filled_at[v] = t.clock;
+    t.pref[v] = 1;
+    t.jobs[threadIdx.x] = TierJob{r, (int32_t)v};
+    t.ring[(t.ctl->head + threadIdx.x) & t.ring_mask] = ring_entry(v, t.clock);
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    t.ctl->head += got;
+    t.ctl->njobs = got;
+    TierStats& st = t.ctl->stats;
+    st.prefetch_keys += N;
+    st.prefetch_found += s_found;
+    st.prefetch_filled += got;
+    st.prefetch_dropped += n - got;
+    st.host_bytes += (unsigned long long)got * t.row_bytes;
+  }
+}
+
 // Host row -> cache slot copies of the current fill list, one wave per job,
 // reading the pinned host rows directly over PCIe (zero-copy).
 template <int NCH>
@@ -376,7 +483,10 @@ __global__ __launch_bounds__(WPB * 64) void k_prefetch_probe(const TierArgs t,
   const dev::Probe pr = dev::probe_begin(a, tw, lane);
   int len;
   const int32_t row = dev::probe_finish(a, pr, lane, &len);
-  if (lane == 0) t.row_of[q] = row;
+  if (lane == 0) {
+    t.row_of[q] = row;
+    t.phase[q] = (uint8_t)len;
+  }
 }
 
 // Inject of every position: value rows come from the cache (phase 0) or
@@ -508,6 +618,15 @@ hipError_t launch_resolve_prefetch(const TierArgs& t, uint32_t N, hipStream_t s)
   hipLaunchKernelGGL(k_resolve_prefetch, dim3(1), dim3(kResolveThreads), 0, s, t, N);
   return hipGetLastError();
 }
+
+hipError_t launch_resolve_prefetch_scored(const TierArgs& t, uint32_t N, const float* prob,
+                                         uint32_t budget, hipStream_t s) {
+  hipLaunchKernelGGL(k_resolve_prefetch_scored, dim3(1), dim3(kResolveThreads), 0, s, t, N, prob,
+                     budget);
+  return hipGetLastError();
+}
+
+uint32_t scored_prefetch_max() { return kScoredMax; }
 
 hipError_t launch_fill(const TierArgs& t, int dtype, int dim, uint32_t max_jobs, hipStream_t s) {
   switch (chunks_of(dtype, dim)) {

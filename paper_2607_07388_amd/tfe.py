@@ -44,7 +44,7 @@ class tfe_table_desc(ctypes.Structure):
 class tfe_stats(ctypes.Structure):
     _fields_ = [(n, ctypes.c_uint64) for n in (
         "calls", "positions", "hits", "cache_hits", "cache_misses", "prefetch_keys",
-        "prefetch_found", "prefetch_filled", "prefetch_used", "host_bytes")]
+        "prefetch_found", "prefetch_filled", "prefetch_used", "host_bytes", "prefetch_dropped")]
 
     def as_dict(self):
         return {n: int(getattr(self, n)) for n, _ in self._fields_}
@@ -67,6 +67,7 @@ def _load():
         "tfe_lookup_inject": ([vp, vp, i32, i32, i32, vp, vp, vp, vp, vp, i32, ctypes.c_float, vp],
                               ctypes.c_int),
         "tfe_prefetch": ([vp, vp, i32, vp, i32, i32, vp], ctypes.c_int),
+        "tfe_prefetch_scored": ([vp, vp, i32, vp, vp, i32, i32, i32, vp], ctypes.c_int),
         "tfe_get_stats": ([vp, ctypes.POINTER(tfe_stats)], ctypes.c_int),
         "tfe_reset_stats": ([vp], ctypes.c_int),
         "tfe_last_error": ([], ctypes.c_char_p),
@@ -85,6 +86,7 @@ def _load():
 lib = _load()
 # Every symbol the C header declares (checked by the CPU test suite).
 EXPORTED = ("tfe_table_load", "tfe_table_free", "tfe_lookup_inject", "tfe_prefetch",
+            "tfe_prefetch_scored",
             "tfe_get_stats", "tfe_reset_stats", "tfe_last_error", "tfe_index_capacity",
             "tfe_index_build_host", "tfe_index_probe_host")
 
@@ -139,6 +141,13 @@ def tfe_lookup_inject(table, tokens, B, ctx, S, hidden_in, hidden_out, hit_mask,
 def tfe_prefetch(table, tail, tail_len, candidates, B, K, side_stream=None):
     return _check(lib.tfe_prefetch(table, addr(tail), tail_len, addr(candidates), B, K,
                                    stream_handle(side_stream)))
+
+
+def tfe_prefetch_scored(table, tail, tail_len, candidates, cand_prob, B, K, budget,
+                        side_stream=None):
+    return _check(lib.tfe_prefetch_scored(table, addr(tail), tail_len, addr(candidates),
+                                          addr(cand_prob), B, K, budget,
+                                          stream_handle(side_stream)))
 
 
 def tfe_get_stats(table):

@@ -16,7 +16,8 @@ from . import harness as H
 pytestmark = pytest.mark.gpu
 
 STAT_KEYS = ("positions", "hits", "cache_hits", "cache_misses", "prefetch_keys",
-             "prefetch_found", "prefetch_filled", "prefetch_used", "host_bytes")
+             "prefetch_found", "prefetch_filled", "prefetch_used", "host_bytes",
+             "prefetch_dropped")
 
 
 def pinned_values(table):
@@ -127,6 +128,44 @@ def test_tiered_prefetch_workload5_shape(w2_tables):
         check_stats(tier, model)
     st = tfe.tfe_get_stats(tier.handle)
     assert st["prefetch_filled"] > 0 and st["prefetch_used"] > 0
+    tier.close()
+
+
+@pytest.mark.parametrize("budget", [16, 1024])
+def test_scored_budgeted_prefetch(w2_tables, budget):
+    """Eq. 17: candidates carry probabilities; rows are fetched by score
+    p * len * (not cached) up to the budget.  Stats (filled, dropped, used)
+    follow the model exactly; outputs stay identical to a resident table."""
+    table, res, ot = w2_tables
+    C, pre, B, K, steps = 8192, 4096, 64, 8, 8
+    tier = TieredTable(table, C, pre)
+    model = LruModel(C, pre, table.dim * 2)
+    seqs = synth.zipf_tokens(1, 800, B * (steps + 3), 1.1).reshape(B, steps + 3)
+    rng = np.random.default_rng(budget)
+    side = torch.cuda.Stream()
+    for s in range(steps):
+        window = np.ascontiguousarray(seqs[:, s:s + 3])
+        hidden = synth.normal_range(1, 801 + s, 0, B, table.dim, 1.0, synth.BF16)
+        o = run_both(res, tier, window, 2, 1, hidden, table.dtype, table.dim)
+        model.lookup([int(r) for r in o.slot.cpu().numpy()])
+        tail = np.ascontiguousarray(seqs[:, s + 1:s + 3])
+        cand = synth.workloads.candidates(1, B, K, seqs[:, s + 3], step=100 + s)
+        # Softmax-like probabilities falling with the candidate's rank, with
+        # exact ties and a few non-positive entries.
+        prob = (rng.dirichlet(np.ones(K) * 0.5, B) if s % 2 else
+                np.tile(np.float32(0.5) ** np.arange(K), (B, 1))).astype(np.float32)
+        prob[0, 0], prob[1, 1] = 0.0, -1.0
+        win = np.concatenate([np.repeat(tail, K, axis=0), cand.reshape(-1, 1)], axis=1)
+        _, crow, clen = ot.lookup(win, 2, 1)
+        tfe.tfe_prefetch_scored(tier.handle, torch.from_numpy(tail).cuda(), 2,
+                                torch.from_numpy(cand).cuda(), torch.from_numpy(prob).cuda(),
+                                B, K, budget, side)
+        model.prefetch_scored([int(r) for r in crow], [int(x) for x in clen], prob.ravel(), budget)
+        check_stats(tier, model)
+    st = tfe.tfe_get_stats(tier.handle)
+    assert st["prefetch_filled"] > 0
+    if budget == 16:
+        assert st["prefetch_dropped"] > 0
     tier.close()
 
 

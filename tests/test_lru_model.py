@@ -76,3 +76,17 @@ def test_groups_split_long_calls():
     # Row 0 was filled in the first group: cached when the second began.
     assert m.stats["cache_hits"] == 1
     assert m.stats["host_bytes"] == GROUP + (GROUP + 1)
+
+
+def test_scored_prefetch_orders_by_score_and_respects_budget():
+    import numpy as np
+    m = LruModel(8, 0, row_bytes=1)
+    rows = [10, 11, 12, 10, 13, -1]
+    lens = [2, 3, 2, 3, 2, 0]
+    prob = np.array([0.5, 0.1, 0.2, 0.3, 0.0, 0.9], np.float32)
+    # scores: 10 -> max(1.0, 0.9) = 1.0; 11 -> 0.3; 12 -> 0.4; 13 -> 0 (not fetched)
+    m.prefetch_scored(rows, lens, prob, budget=2)
+    assert set(m.resident()) == {10, 12}
+    assert m.stats["prefetch_filled"] == 2 and m.stats["prefetch_dropped"] == 1
+    # Recency: 10 then 12 were filled in score order (10 first = less recent).
+    assert list(m.order)[-2:] == [m.resident()[10], m.resident()[12]]
