@@ -89,6 +89,7 @@ def main():
     ap.add_argument("--tier-steps", type=int, default=2000)
     ap.add_argument("--tier-warmup", type=int, default=100)
     ap.add_argument("--t-hide-us", default="0,100")
+    ap.add_argument("--prefetch-budget", type=int, default=64)
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path "
@@ -320,6 +321,11 @@ def run_tiered(args):
     cands = np.stack([synth.workloads.candidates(4, B, K, seqs[:, s + 3], step=s)
                       for s in range(n_steps)])
     cands_d = torch.from_numpy(cands).cuda()
+    # Candidate probabilities for the scored prefetch: falling geometrically
+    # with the candidate's rank (0.5^k, normalised), as a softmax's top-K
+    # list does.
+    pk = np.float32(0.5) ** np.arange(K, dtype=np.float32)
+    probs_d = torch.from_numpy(np.tile(pk / pk.sum(), (B, 1)).astype(np.float32)).cuda()
     tails_d = [seqs_d[:, s + 1:s + 3].contiguous() for s in range(n_steps)]
     wins_d = [seqs_d[:, s:s + 3].contiguous() for s in range(n_steps)]
     hid = [torch.empty((B, D), dtype=torch.bfloat16, device="cuda") for _ in range(8)]
@@ -332,7 +338,7 @@ def run_tiered(args):
 
     results = []
     for t_hide in [float(x) for x in args.t_hide_us.split(",")]:
-        for prefetch in (False, True):
+        for prefetch in ("off", "all", "scored"):
             desc = tfe.make_desc(table.tokens, table.lens, 2, 3, synth.V, vals, D, synth.BF16, 0,
                                  0.5, hbm_cache_rows=C, adopt_host_values=1, prefill_rows=C)
             handle = tfe.tfe_table_load(desc, stream.cuda_stream)
@@ -342,8 +348,11 @@ def run_tiered(args):
                 tfe.tfe_lookup_inject(handle, wins_d[s], B, 2, 1, hid[s % 8], outs.out, outs.hit,
                                       outs.slot, outs.len, tfe.TFE_GATE_SIGMOID, 1.0,
                                       stream.cuda_stream)
-                if prefetch:
+                if prefetch == "all":
                     tfe.tfe_prefetch(handle, tails_d[s], 2, cands_d[s], B, K, side)
+                elif prefetch == "scored":
+                    tfe.tfe_prefetch_scored(handle, tails_d[s], 2, cands_d[s], probs_d, B, K,
+                                            args.prefetch_budget, side)
                 if t_hide > 0:
                     synth.spin_device(t_hide, stream.cuda_stream)
 
@@ -368,6 +377,7 @@ def run_tiered(args):
                 "hbm_cache_hit_rate": st["cache_hits"] / max(1, st["hits"]),
                 "prefetch_precision": st["prefetch_used"] / max(1, st["prefetch_filled"]),
                 "prefetch_filled_per_step": st["prefetch_filled"] / n,
+                "prefetch_dropped_per_step": st["prefetch_dropped"] / n,
                 "host_bytes_per_step": st["host_bytes"] / n,
                 "host_link_gbps": st["host_bytes"] / wall / 1e9,
             })
@@ -391,6 +401,7 @@ def run_tiered(args):
             "workload": "tiered: 2^25-phrase 2/3-gram table, 64 GiB bf16 values in pinned host "
                         "memory, 4M-row HBM cache (LRU), batch-64 decode, 8 candidates per row",
             "h2d_copy_gbps": h2d_gbps,
+            "prefetch_budget_scored": args.prefetch_budget,
         },
         "runs": results,
     }))
