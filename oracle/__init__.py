@@ -15,6 +15,7 @@ from . import _build
 
 OK, INVALID, DUPLICATE = 0, -1, -2
 GATE_SIGMOID, GATE_CONST = 0, 1
+WEIGHT_LENGTH, WEIGHT_UNIFORM = 0, 1
 EPS = 1e-6
 
 _lib = None
@@ -33,6 +34,10 @@ def lib():
         L.oracle_table_free.argtypes = [vp]
         L.oracle_table_free.restype = None
         L.oracle_lookup.argtypes = [vp, vp, i64, i64, i64, vp, vp, vp]
+        L.oracle_lookup_all.argtypes = [vp, vp, i64, i64, i64, vp, vp]
+        L.oracle_inject_multi.argtypes = [vp, vp, i64, vp, i64, ctypes.c_int, ctypes.c_int, i64,
+                                          ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                                          ctypes.c_double, vp]
         L.oracle_inject.argtypes = [vp, vp, i64, vp, i64, i64, ctypes.c_int, ctypes.c_int,
                                     ctypes.c_double, vp]
         L.oracle_gate.argtypes = [vp, vp, i64, ctypes.c_int, ctypes.c_int, ctypes.c_double]
@@ -58,6 +63,7 @@ class Table:
     padded), lens: uint8 [P]."""
 
     def __init__(self, tokens, lens, n_min, n_max, vocab):
+        self.n_min, self.n_max = n_min, n_max
         self.tokens = np.ascontiguousarray(tokens, np.int32).reshape(-1, n_max)
         self.lens = np.ascontiguousarray(lens, np.uint8)
         st = ctypes.c_int(0)
@@ -86,6 +92,22 @@ class Table:
         return hit, row, ln
 
 
+    def lookup_all(self, tokens, ctx, S):
+        """All matched lengths: -> (mask uint8 [B*S], rows int32 [B*S x L]);
+        column j is the phrase of length n_min + j (-1 if none), bit j of the
+        mask is set where it matched."""
+        tokens = np.ascontiguousarray(tokens, np.int32)
+        B = tokens.shape[0]
+        assert tokens.shape[1] == ctx + S
+        L = self.n_max - self.n_min + 1
+        mask = np.empty(B * S, np.uint8)
+        rows = np.empty((B * S, L), np.int32)
+        st = lib().oracle_lookup_all(self._h, _p(tokens), B, ctx, S, _p(mask), _p(rows))
+        if st != OK:
+            raise OracleError(st)
+        return mask, rows
+
+
 def inject(hidden, values, index, dtype, gate=GATE_SIGMOID, lam=1.0):
     """hidden [T x D] (float32, or uint16 bf16 patterns), values [R x D] of the
     same type, index int64 [T] (row of `values` or -1) -> out like hidden."""
@@ -97,6 +119,26 @@ def inject(hidden, values, index, dtype, gate=GATE_SIGMOID, lam=1.0):
     R = values.shape[0] if values.ndim == 2 else 0
     st = lib().oracle_inject(_p(hidden), _p(values) if R else None, R, _p(index), T, D, dtype,
                              gate, float(lam), _p(out))
+    if st != OK:
+        raise OracleError(st)
+    return out
+
+
+def inject_multi(hidden, values, index, n_min, dtype, weighting=WEIGHT_LENGTH,
+                 gate=GATE_SIGMOID, lam=1.0):
+    """hidden [T x D], values [R x D] of the same type, index int64 [T x L]
+    (row of `values` retained for length n_min + j, or -1) -> out like hidden:
+    h + g * sum_j alpha_j v_j (Eq. 4, Eq. 11, Eq. 5)."""
+    hidden = np.ascontiguousarray(hidden)
+    values = np.ascontiguousarray(values)
+    index = np.ascontiguousarray(index, np.int64)
+    T, D = hidden.shape
+    assert index.ndim == 2 and index.shape[0] == T
+    out = np.empty_like(hidden)
+    R = values.shape[0] if values.ndim == 2 else 0
+    st = lib().oracle_inject_multi(_p(hidden), _p(values) if R else None, R, _p(index), T,
+                                   index.shape[1], n_min, D, dtype, weighting, gate, float(lam),
+                                   _p(out))
     if st != OK:
         raise OracleError(st)
     return out

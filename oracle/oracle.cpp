@@ -22,7 +22,10 @@
 //    rms(x) = sqrt(mean(x^2) + eps): a train-free reading of "a learned
 //    function of the current hidden state and retrieved memory" (Sec. 2.2,
 //    Sec. 4.2: nothing is trained), or the constant gate g = lambda;
-//  * a position without a match is left unchanged.
+//  * a position without a match is left unchanged;
+//  * the multi-match variant retains every matched phrase and injects their
+//    weighted sum (Eq. 4, Eq. 11), with weights proportional to the phrase
+//    length or uniform, normalised to add up to 1.
 // All arithmetic is in double; the result is rounded once, to nearest-even,
 // to the output type.
 #include <stdint.h>
@@ -146,6 +149,41 @@ int oracle_lookup(const void* table, const int32_t* tokens, int64_t B, int64_t c
   return OR_OK;
 }
 
+// All-matches lookup (Eq. 4, Eq. 11: every matched entry is retained).
+// Same windows as oracle_lookup.  Outputs per position p = b*S + s:
+// rows[p*L + j] is the row of the length-(n_min + j) window, or -1 when that
+// window is absent or not in the table, L = n_max - n_min + 1; bit j of
+// mask[p] is set where rows[p*L + j] >= 0.
+int oracle_lookup_all(const void* table, const int32_t* tokens, int64_t B, int64_t ctx,
+                      int64_t S, uint8_t* mask, int32_t* rows) {
+  const Table* t = (const Table*)table;
+  if (!t || B < 0 || ctx < 0 || S < 0) return OR_INVALID;
+  const int64_t W = ctx + S;
+  const int L = t->n_max - t->n_min + 1;
+  for (int64_t b = 0; b < B; ++b) {
+    for (int64_t s = 0; s < S; ++s) {
+      const int64_t c = ctx + s, p = b * S + s;
+      mask[p] = 0;
+      for (int j = 0; j < L; ++j) {
+        const int n = t->n_min + j;
+        rows[p * L + j] = -1;
+        const int64_t first = c - n + 1;
+        if (first < 0) continue;
+        std::vector<int32_t> w(tokens + b * W + first, tokens + b * W + c + 1);
+        bool valid = true;
+        for (int32_t x : w)
+          if (x < 0 || x >= t->vocab) valid = false;
+        if (!valid) continue;
+        auto it = t->phrase_to_row.find(w);
+        if (it == t->phrase_to_row.end()) continue;
+        rows[p * L + j] = (int32_t)it->second;
+        mask[p] |= (uint8_t)(1u << j);
+      }
+    }
+  }
+  return OR_OK;
+}
+
 // Gated residual injection (Eq. 5).  hidden, out: [T x D]; values: [R x D];
 // index[p] is the row of `values` matched at position p, or -1 for a miss.
 // dtype 0 = float32, 1 = bfloat16 (bit patterns); gate 0 = sigmoid of the
@@ -181,6 +219,59 @@ int oracle_inject(const void* hidden, const void* values, int64_t R, const int64
       g = lambda / (1.0 + std::exp(-z));
     }
     for (int64_t j = 0; j < D; ++j) store_elem(out, p * D + j, dtype, h[j] + g * m[j]);
+  }
+  return OR_OK;
+}
+
+// Injection of an aggregated memory signal (Eq. 4 / Eq. 11, then Eq. 5).
+// index: [T x L]; index[p*L + j] is the row of `values` retained at position
+// p for the phrase of length n_min + j, or -1.  The retained rows are
+// combined as m = sum_j alpha_j v_j with
+//   weighting 0 (by length):  alpha_j = n_j / sum_k n_k,
+//   weighting 1 (uniform):    alpha_j = 1 / |retained|,
+// the sums running over the retained rows only, so the weights add up to 1.
+// m then goes through the same gate and residual as oracle_inject; a
+// position with no retained row is copied unchanged.
+int oracle_inject_multi(const void* hidden, const void* values, int64_t R, const int64_t* index,
+                        int64_t T, int L, int n_min, int64_t D, int dtype, int weighting,
+                        int gate, double lambda, void* out) {
+  if (T < 0 || D <= 0 || L < 1 || (dtype != 0 && dtype != 1) || (gate != 0 && gate != 1) ||
+      (weighting != 0 && weighting != 1))
+    return OR_INVALID;
+  const size_t esz = dtype == 0 ? 4 : 2;
+  const double eps = 1e-6;
+  for (int64_t p = 0; p < T; ++p) {
+    double wsum = 0;
+    for (int j = 0; j < L; ++j) {
+      const int64_t r = index[p * L + j];
+      if (r >= R) return OR_INVALID;
+      if (r >= 0) wsum += weighting == 0 ? (double)(n_min + j) : 1.0;
+    }
+    if (wsum == 0) {
+      memcpy((char*)out + p * D * esz, (const char*)hidden + p * D * esz, D * esz);
+      continue;
+    }
+    std::vector<double> h(D), m(D, 0.0);
+    for (int64_t k = 0; k < D; ++k) h[k] = load_elem(hidden, p * D + k, dtype);
+    for (int j = 0; j < L; ++j) {
+      const int64_t r = index[p * L + j];
+      if (r < 0) continue;
+      const double alpha = (weighting == 0 ? (double)(n_min + j) : 1.0) / wsum;
+      for (int64_t k = 0; k < D; ++k) m[k] += alpha * load_elem(values, r * D + k, dtype);
+    }
+    double g = lambda;
+    if (gate == 0) {
+      double shh = 0, smm = 0, shm = 0;
+      for (int64_t k = 0; k < D; ++k) {
+        shh += h[k] * h[k];
+        smm += m[k] * m[k];
+        shm += h[k] * m[k];
+      }
+      const double z = shm / (std::sqrt(shh / (double)D + eps) * std::sqrt(smm / (double)D + eps)) /
+                       std::sqrt((double)D);
+      g = lambda / (1.0 + std::exp(-z));
+    }
+    for (int64_t k = 0; k < D; ++k) store_elem(out, p * D + k, dtype, h[k] + g * m[k]);
   }
   return OR_OK;
 }
