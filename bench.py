@@ -24,6 +24,11 @@ next token among them with probability 0.7):
 
   python bench.py --workload tiered [--tier-steps N] [--t-hide-us 0,20,100,500]
 
+Multi-match workload (every matched phrase retained and combined with
+length weights, Eq. 4 / Eq. 11), same stacked decode launch as the default:
+
+  python bench.py --workload multi
+
 Each configuration (prefetch off / on, emulated compute window T_hide between
 a step's lookup and the next) starts from a freshly loaded table.  A step is
 one tfe_lookup_inject (plus, with prefetch, one tfe_prefetch for the next
@@ -75,6 +80,12 @@ def algorithmic_bytes(T, hits, keys, window):
     return (T * 2 * D * ESZ + hits * (D * ESZ + 4) + keys * 8 + T * window * 4 + T * (1 + 4 + 1))
 
 
+def algorithmic_bytes_multi(T, rows, keys, window, L):
+    """Multi-match variant: one value row and row id per retained phrase, a
+    match mask and L row ids per position."""
+    return (T * 2 * D * ESZ + rows * (D * ESZ + 4) + keys * 8 + T * window * 4 + T * (1 + 4 * L))
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -85,7 +96,7 @@ def main():
     ap.add_argument("--latency-steps", type=int, default=2000)
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--workload", choices=("decode", "tiered"), default="decode")
+    ap.add_argument("--workload", choices=("decode", "multi", "tiered"), default="decode")
     ap.add_argument("--tier-steps", type=int, default=2000)
     ap.add_argument("--tier-warmup", type=int, default=100)
     ap.add_argument("--t-hide-us", default="0,100")
@@ -125,16 +136,32 @@ def main():
         sets.append((batch, tok, hid, H.Outputs(B, D, synth.BF16)))
     torch.cuda.synchronize()
 
+    multi = args.workload == "multi"
+    L = table.n_max - table.n_min + 1
+    if multi:
+        mslots = [torch.full((B, L), -7, dtype=torch.int32, device="cuda") for _ in sets]
+
     def call(k):
         _, tok, hid, outs = sets[k % len(sets)]
-        tfe.tfe_lookup_inject(gt.handle, tok, B, ctx, S, hid, outs.out, outs.hit, outs.slot,
-                              outs.len, tfe.TFE_GATE_SIGMOID, 1.0, stream.cuda_stream)
+        if multi:
+            tfe.tfe_lookup_inject_multi(gt.handle, tok, B, ctx, S, hid, outs.out, outs.hit,
+                                        mslots[k % len(sets)], tfe.TFE_WEIGHT_LENGTH,
+                                        tfe.TFE_GATE_SIGMOID, 1.0, stream.cuda_stream)
+        else:
+            tfe.tfe_lookup_inject(gt.handle, tok, B, ctx, S, hid, outs.out, outs.hit, outs.slot,
+                                  outs.len, tfe.TFE_GATE_SIGMOID, 1.0, stream.cuda_stream)
 
     for k in range(args.warmup):
         call(k)
     torch.cuda.synchronize()
-    hits = [int(s[3].hit.sum().item()) for s in sets]
-    keys = B * (table.n_max - table.n_min + 1)
+    if multi:
+        # Retained rows per set: the population count of the match masks.
+        hits = [int(sum(((s[3].hit >> j) & 1).sum().item() for j in range(L))) for s in sets]
+        positions_hit = [int((s[3].hit > 0).sum().item()) for s in sets]
+    else:
+        hits = [int(s[3].hit.sum().item()) for s in sets]
+        positions_hit = hits
+    keys = B * L
 
     # Timed region: K back-to-back calls bracketed by HIP events on the launch
     # stream; their elapsed time over K is the kernel's average launch duration.
@@ -148,7 +175,10 @@ def main():
     torch.cuda.synchronize()
     wall = time.perf_counter() - w0
     avg_launch = e0.elapsed_time(e1) * 1e-3 / args.steps  # seconds
-    bytes_per_call = [algorithmic_bytes(B, h, keys, window) for h in hits]
+    if multi:
+        bytes_per_call = [algorithmic_bytes_multi(B, h, keys, window, L) for h in hits]
+    else:
+        bytes_per_call = [algorithmic_bytes(B, h, keys, window) for h in hits]
     avg_bytes = float(np.mean([bytes_per_call[k % len(sets)] for k in range(args.steps)]))
     achieved = avg_bytes / avg_launch / 1e9
     tokens_per_s = B * args.steps / wall
@@ -170,6 +200,11 @@ def main():
     torch.cuda.synchronize()
     copy_gbps = 2 * nb * 200 / (c0.elapsed_time(c1) * 1e-3) / 1e9
     del cbufs
+
+    if multi:
+        return finish_multi(args, table, gt, sets, mslots, B, ctx, S, window, L, tokens_per_s,
+                            wall, achieved, avg_bytes, avg_launch, copy_gbps, hits,
+                            positions_hit)
 
     # Latency mode: one batch-64 decode step per call.
     lat_sets = []
@@ -280,6 +315,85 @@ def main():
         }
     gt.close()
     print(json.dumps(result))
+
+
+def finish_multi(args, table, gt, sets, mslots, B, ctx, S, window, L, tokens_per_s, wall,
+                 achieved, avg_bytes, avg_launch, copy_gbps, hits, positions_hit):
+    """JSON line of the multi-match workload (Eq. 4, Eq. 11): the stacked
+    decode launch with every matched phrase retained, length weights."""
+    result = {
+        "metric": "multi-match lookup+inject tokens/sec and achieved HBM GB/s, batch-64 decode, "
+                  "1 MI355X",
+        "value": tokens_per_s,
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": wall / args.steps * 1e3,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": "batch-64 decode, stacked throughput mode: %d batch-64 steps per call "
+                        "(%d rows, 3-token windows, Zipf(1.1) ids), 2^20-phrase 2/3-gram table, "
+                        "every matched phrase retained, length weights, sigmoid gate, out of "
+                        "place" % (args.stack, B),
+            "table_phrases": table.n_phrases,
+            "rows_per_call": B,
+            "rotating_sets": args.sets,
+            "hit_rate": float(np.mean(positions_hit) / B),
+            "retained_rows_per_position": float(np.mean(hits) / B),
+        },
+        "hbm_gbps_algorithmic": achieved,
+        "roofline": {
+            "bound": "hbm",
+            "kernel": "k_lookup_inject_multi<bf16, D=1024>",
+            "achieved": achieved,
+            "peak": HBM_PEAK_GBPS,
+            "unit": "GB/s",
+            "frac": achieved / HBM_PEAK_GBPS,
+            "traffic": None,
+            "bytes_per_launch": avg_bytes,
+            "avg_launch_us": avg_launch * 1e6,
+            "copy_reference_gbps": copy_gbps,
+            "frac_of_copy_reference": achieved / copy_gbps,
+        },
+    }
+    if not args.no_cpu_baseline:
+        import oracle
+        from tests import harness as H
+        ot = H.oracle_table(table)
+        batch = sets[0][0]
+        hidden = synth_hidden(batch, B)
+        _, rows = ot.lookup_all(batch.tokens, ctx, S)
+        uniq, inv = np.unique(rows[rows >= 0].astype(np.int64), return_inverse=True)
+        vals = table.value_rows(uniq)
+        idx = np.full(rows.shape, -1, np.int64)
+        idx[rows >= 0] = inv
+        done, c0 = 0, time.perf_counter()
+        while time.perf_counter() - c0 < args.cpu_seconds:
+            ot.lookup_all(batch.tokens, ctx, S)
+            oracle.inject_multi(hidden, vals, idx, table.n_min, table.dtype)
+            done += B
+        csec = time.perf_counter() - c0
+        result["cpu_baseline"] = {
+            "value": done / csec,
+            "unit": "tokens/s",
+            "cores": 1,
+            "kind": "oracle",
+            "sample": "%d passes of the all-matches std::map lookup + double-precision weighted "
+                      "inject over one %d-row stacked decode set (%.1f s, single thread)"
+                      % (done // B, B, csec),
+        }
+    gt.close()
+    print(json.dumps(result))
+
+
+def synth_hidden(batch, B):
+    import synth
+    return synth.normal_range(batch.seed, batch.hidden_tag, 0, B, D, 1.0, synth.BF16)
 
 
 def run_tiered(args):

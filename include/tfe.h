@@ -61,6 +61,14 @@ typedef enum { TFE_F32 = 0, TFE_BF16 = 1 } tfe_dtype;
  * `scale` is the memory-injection scale of the evaluation (Sec. 5.1). */
 typedef enum { TFE_GATE_SIGMOID = 0, TFE_GATE_CONST = 1 } tfe_gate;
 
+/* Weights of the multi-match aggregation m = sum_i alpha_i v_i (Eq. 4,
+ * Eq. 11; the paper lets alpha depend on phrase length, frequency or
+ * confidence).  Over the phrases retained at one position:
+ *   TFE_WEIGHT_LENGTH:  alpha_i = n_i / sum_k n_k  (n = phrase length);
+ *   TFE_WEIGHT_UNIFORM: alpha_i = 1 / (number retained).
+ * Both add up to 1, so one retained phrase injects its own row. */
+typedef enum { TFE_WEIGHT_LENGTH = 0, TFE_WEIGHT_UNIFORM = 1 } tfe_weighting;
+
 typedef struct {
   /* Phrases (Sec. 4.2): phrase i is phrase_tokens[i*n_max .. i*n_max+len-1],
    * oldest token first, len = phrase_len[i]; unused columns are ignored.
@@ -139,6 +147,25 @@ tfe_status tfe_lookup_inject(tfe_table *table, const int32_t *tokens, int32_t B,
                              int32_t S, const void *hidden_in, void *hidden_out,
                              uint8_t *hit_mask, int32_t *slot_ids, uint8_t *match_len,
                              int32_t gate, float scale, void *stream);
+
+/* Multi-match lookup + inject (resident tables).
+ * Paper: Eq. 4 and Eq. 11 (every matched phrase retained, memory vectors
+ * aggregated with weights alpha_i), Eq. 3, Eq. 5.
+ * Same tokens, windows, hidden_in / hidden_out, gate and scale as
+ * tfe_lookup_inject; every n-gram ending at the position that is in the
+ * table is retained (at most one per length) and m = sum_i alpha_i v_i with
+ * the weights of `weighting` (tfe_weighting) replaces the single row.  The
+ * aggregate is kept in float32 and rounded only in h'.
+ *   match_mask DEVICE uint8 [B*S]: bit j set where the phrase of length
+ *              n_min + j matched (0: no match, the row is left unchanged).
+ *   slot_ids   DEVICE int32 [B*S x L], L = n_max - n_min + 1: column j is
+ *              the row id of the matched phrase of length n_min + j, -1 if
+ *              none.
+ * Returns TFE_ERR_UNSUPPORTED for tiered tables (hbm_cache_rows > 0). */
+tfe_status tfe_lookup_inject_multi(tfe_table *table, const int32_t *tokens, int32_t B,
+                                   int32_t ctx, int32_t S, const void *hidden_in,
+                                   void *hidden_out, uint8_t *match_mask, int32_t *slot_ids,
+                                   int32_t weighting, int32_t gate, float scale, void *stream);
 
 /* Prefetch for the next step (tiered tables; a no-op on resident tables).
  * Paper: Eq. 14 (top-K next-token candidates), Eq. 15 (candidate phrases via

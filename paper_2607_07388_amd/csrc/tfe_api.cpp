@@ -378,7 +378,8 @@ static tfe_status load(const tfe_table_desc* d, hipStream_t stream, tfe_table** 
 static tfe_status lookup_inject(tfe_table* t, const int32_t* tokens, int32_t B, int32_t ctx,
                                 int32_t S, const void* hin, void* hout, uint8_t* hit,
                                 int32_t* slot, uint8_t* len, int32_t gate, float scale,
-                                hipStream_t stream) {
+                                hipStream_t stream, int32_t weighting = -1) {
+  const bool multi = weighting >= 0;
   if (!t) return fail(TFE_ERR_INVALID_ARG, "null table");
   if (B < 0 || ctx < 0 || S < 0) return fail(TFE_ERR_INVALID_ARG, "negative B, ctx or S");
   if (gate != TFE_GATE_SIGMOID && gate != TFE_GATE_CONST) return fail(TFE_ERR_INVALID_ARG, "bad gate");
@@ -386,10 +387,14 @@ static tfe_status lookup_inject(tfe_table* t, const int32_t* tokens, int32_t B, 
   const int64_t T = (int64_t)B * S;
   if ((int64_t)ctx + S > 0x7FFFFFFFll) return fail(TFE_ERR_INVALID_ARG, "ctx + S overflows");
   if (T > 0x7FFFFFFFll) return fail(TFE_ERR_UNSUPPORTED, "B * S above 2^31 - 1 positions");
+  if (multi && weighting != TFE_WEIGHT_LENGTH && weighting != TFE_WEIGHT_UNIFORM)
+    return fail(TFE_ERR_INVALID_ARG, "bad weighting");
+  if (multi && t->cache_rows > 0)
+    return fail(TFE_ERR_UNSUPPORTED, "multi-match lookup on a tiered table");
   t->stats.calls++;
   if (T == 0) return TFE_OK;
   if (!tokens || !hin || !hout || !hit || !slot)
-    return fail(TFE_ERR_INVALID_ARG, "null tokens, hidden, hit_mask or slot_ids");
+    return fail(TFE_ERR_INVALID_ARG, "null tokens, hidden, mask or slot_ids");
   tfe_status st = check_device(t);
   if (st != TFE_OK) return st;
   LookupArgs a;
@@ -414,6 +419,13 @@ static tfe_status lookup_inject(tfe_table* t, const int32_t* tokens, int32_t B, 
   a.scale = scale;
   a.inv_d = 1.0f / (float)t->dim;
   a.inv_sqrt_d = (float)(1.0 / sqrt((double)t->dim));
+  a.weighting = weighting;
+  if (multi) {
+    a.len_out = nullptr;
+    TFE_HIP(launch_lookup_inject_multi(a, t->dtype, t->dim, stream), "lookup_inject_multi launch");
+    t->stats.positions += (uint64_t)T;
+    return TFE_OK;
+  }
   if (t->cache_rows > 0) return lookup_tiered(t, a, stream);
   TFE_HIP(launch_lookup_inject(a, t->dtype, t->dim, stream), "lookup_inject launch");
   t->stats.positions += (uint64_t)T;
@@ -442,6 +454,16 @@ tfe_status tfe_lookup_inject(tfe_table* table, const int32_t* tokens, int32_t B,
   tfe::clear_error();
   return tfe::lookup_inject(table, tokens, B, ctx, S, hidden_in, hidden_out, hit_mask, slot_ids,
                             match_len, gate, scale, (hipStream_t)stream);
+}
+
+tfe_status tfe_lookup_inject_multi(tfe_table* table, const int32_t* tokens, int32_t B,
+                                   int32_t ctx, int32_t S, const void* hidden_in,
+                                   void* hidden_out, uint8_t* match_mask, int32_t* slot_ids,
+                                   int32_t weighting, int32_t gate, float scale, void* stream) {
+  tfe::clear_error();
+  if (weighting < 0) return tfe::fail(TFE_ERR_INVALID_ARG, "bad weighting");
+  return tfe::lookup_inject(table, tokens, B, ctx, S, hidden_in, hidden_out, match_mask,
+                            slot_ids, nullptr, gate, scale, (hipStream_t)stream, weighting);
 }
 
 tfe_status tfe_prefetch(tfe_table* table, const int32_t* tail, int32_t tail_len,

@@ -159,12 +159,17 @@ __device__ __forceinline__ Probe probe_begin(const LookupArgs& a, const int32_t*
   return pr;
 }
 
+// Outcome of a probe: bit l of `found` is set where lane l read the slot of
+// its group's key (at most one lane per group), and `myrow` is the row id in
+// that slot (meaningful in the lanes whose bit is set).
+struct Walk {
+  uint64_t found;
+  int32_t myrow;
+};
+
 // Consumes the bucket reads: a key group stops at its key (a match) or at an
-// empty slot (absent), and otherwise walks on to the next bucket.  Returns
-// the matched phrase row (-1 on a miss) in every lane and its length in *len;
-// the longest match is the lowest matching lane group.
-__device__ __forceinline__ int32_t probe_finish(const LookupArgs& a, const Probe& pr, int lane,
-                                                int* len) {
+// empty slot (absent), and otherwise walks on to the next bucket.
+__device__ __forceinline__ Walk probe_walk(const LookupArgs& a, const Probe& pr, int lane) {
   bool matched = false;
   bool active = pr.active;
   int32_t myrow = -1;
@@ -187,14 +192,33 @@ __device__ __forceinline__ int32_t probe_finish(const LookupArgs& a, const Probe
     bucket = (bucket + 1) & a.bucket_mask;
     round(*(const u32x4*)(a.slots + bucket * TFE_SLOTS_PER_BUCKET + (lane & 7)));
   }
-  const uint64_t found = __builtin_amdgcn_ballot_w64(matched);
-  if (found == 0) {
+  return Walk{__builtin_amdgcn_ballot_w64(matched), myrow};
+}
+
+// Longest match: the phrase row (-1 on a miss) in every lane and its length
+// in *len; the longest match is the lowest matching lane group.
+__device__ __forceinline__ int32_t probe_finish(const LookupArgs& a, const Probe& pr, int lane,
+                                                int* len) {
+  const Walk w = probe_walk(a, pr, lane);
+  if (w.found == 0) {
     *len = 0;
     return -1;
   }
-  const int sel = __builtin_amdgcn_readfirstlane(__builtin_ctzll(found));
+  const int sel = __builtin_amdgcn_readfirstlane(__builtin_ctzll(w.found));
   *len = a.n_max - (sel >> 3);
-  return __builtin_amdgcn_readlane(myrow, sel);
+  return __builtin_amdgcn_readlane(w.myrow, sel);
+}
+
+// Gate of Eq. 5 from this lane's partial sums of h.h, m.m and h.m.
+__device__ __forceinline__ float gate_finish(const LookupArgs& a, float shh, float smm,
+                                             float shm) {
+  shh = wave_sum(shh);
+  smm = wave_sum(smm);
+  shm = wave_sum(shm);
+  const float inv_rh = __builtin_amdgcn_rsqf(fmaf(shh, a.inv_d, 1e-6f));
+  const float inv_rm = __builtin_amdgcn_rsqf(fmaf(smm, a.inv_d, 1e-6f));
+  const float z = shm * inv_rh * inv_rm * a.inv_sqrt_d;
+  return a.scale * __builtin_amdgcn_rcpf(1.0f + __expf(-z));
 }
 
 // Gate of Eq. 5 for one row held across the wave (hv, mv: NCH 16-byte
@@ -219,13 +243,7 @@ __device__ __forceinline__ float gate_of(const LookupArgs& a, const u32x4* hv, c
       shm = fmaf(h[i], m[i], shm);
     }
   }
-  shh = wave_sum(shh);
-  smm = wave_sum(smm);
-  shm = wave_sum(shm);
-  const float inv_rh = __builtin_amdgcn_rsqf(fmaf(shh, a.inv_d, 1e-6f));
-  const float inv_rm = __builtin_amdgcn_rsqf(fmaf(smm, a.inv_d, 1e-6f));
-  const float z = shm * inv_rh * inv_rm * a.inv_sqrt_d;
-  return a.scale * __builtin_amdgcn_rcpf(1.0f + __expf(-z));
+  return gate_finish(a, shh, smm, shm);
 }
 
 // h' = h + g m for one row, rounded to nearest even, stored non-temporally.

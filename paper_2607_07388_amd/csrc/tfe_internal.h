@@ -43,6 +43,7 @@ struct LookupArgs {
   float scale;
   float inv_d;                // 1 / dim
   float inv_sqrt_d;           // 1 / sqrt(dim)
+  int32_t weighting;          // multi-match kernel: tfe_weighting
 };
 
 // Device-side bookkeeping of a tiered table (see tfe_tiered.hip).
@@ -94,6 +95,10 @@ hipError_t launch_tier_inject(const TierArgs& t, int dtype, int dim, hipStream_t
 
 // Launches the fused resident-table kernel; returns the launch error.
 hipError_t launch_lookup_inject(const LookupArgs& a, int dtype, int dim, hipStream_t stream);
+// Multi-match variant: `hit` receives the match mask, `slot_out` the
+// [T x (n_max - n_min + 1)] row ids.
+hipError_t launch_lookup_inject_multi(const LookupArgs& a, int dtype, int dim,
+                                      hipStream_t stream);
 
 // True if (dtype, dim) has a kernel instantiation.
 bool dim_supported(int dtype, int dim);

@@ -20,6 +20,7 @@ TFE_ERR_HIP = -4
 TFE_ERR_UNSUPPORTED = -5
 TFE_F32, TFE_BF16 = 0, 1
 TFE_GATE_SIGMOID, TFE_GATE_CONST = 0, 1
+TFE_WEIGHT_LENGTH, TFE_WEIGHT_UNIFORM = 0, 1
 
 
 class tfe_table_desc(ctypes.Structure):
@@ -66,6 +67,8 @@ def _load():
         "tfe_table_free": ([vp], ctypes.c_int),
         "tfe_lookup_inject": ([vp, vp, i32, i32, i32, vp, vp, vp, vp, vp, i32, ctypes.c_float, vp],
                               ctypes.c_int),
+        "tfe_lookup_inject_multi": ([vp, vp, i32, i32, i32, vp, vp, vp, vp, i32, i32,
+                                     ctypes.c_float, vp], ctypes.c_int),
         "tfe_prefetch": ([vp, vp, i32, vp, i32, i32, vp], ctypes.c_int),
         "tfe_prefetch_scored": ([vp, vp, i32, vp, vp, i32, i32, i32, vp], ctypes.c_int),
         "tfe_get_stats": ([vp, ctypes.POINTER(tfe_stats)], ctypes.c_int),
@@ -85,7 +88,8 @@ def _load():
 
 lib = _load()
 # Every symbol the C header declares (checked by the CPU test suite).
-EXPORTED = ("tfe_table_load", "tfe_table_free", "tfe_lookup_inject", "tfe_prefetch",
+EXPORTED = ("tfe_table_load", "tfe_table_free", "tfe_lookup_inject", "tfe_lookup_inject_multi",
+            "tfe_prefetch",
             "tfe_prefetch_scored",
             "tfe_get_stats", "tfe_reset_stats", "tfe_last_error", "tfe_index_capacity",
             "tfe_index_build_host", "tfe_index_probe_host")
@@ -136,6 +140,14 @@ def tfe_lookup_inject(table, tokens, B, ctx, S, hidden_in, hidden_out, hit_mask,
     return _check(lib.tfe_lookup_inject(table, addr(tokens), B, ctx, S, addr(hidden_in),
                                         addr(hidden_out), addr(hit_mask), addr(slot_ids),
                                         addr(match_len), gate, scale, stream_handle(stream)))
+
+
+def tfe_lookup_inject_multi(table, tokens, B, ctx, S, hidden_in, hidden_out, match_mask,
+                            slot_ids, weighting, gate, scale, stream=None):
+    return _check(lib.tfe_lookup_inject_multi(table, addr(tokens), B, ctx, S, addr(hidden_in),
+                                              addr(hidden_out), addr(match_mask),
+                                              addr(slot_ids), weighting, gate, scale,
+                                              stream_handle(stream)))
 
 
 def tfe_prefetch(table, tail, tail_len, candidates, B, K, side_stream=None):
