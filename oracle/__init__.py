@@ -3,8 +3,9 @@
 TEST INFRASTRUCTURE ONLY: the tests, the smoke check and the benchmark's
 CPU-baseline leg may import this package; the product path never does.  The
 arithmetic lives in ``oracle.cpp`` (std::map on token tuples, scalar double
-loops); this file only marshals numpy arrays.  ``lru.py`` is the reference
-model of the HBM cache tier's replacement policy.
+loops); this file only marshals numpy arrays.  ``head.cpp`` is the
+early-exit prefetch head; ``lru.py`` is the reference model of the HBM cache
+tier's replacement policy.
 """
 import ctypes
 import os
@@ -42,6 +43,7 @@ def lib():
                                     ctypes.c_double, vp]
         L.oracle_gate.argtypes = [vp, vp, i64, ctypes.c_int, ctypes.c_int, ctypes.c_double]
         L.oracle_gate.restype = ctypes.c_double
+        L.oracle_head_topk.argtypes = [vp, vp, i64, i64, i64, i64, ctypes.c_int, vp, vp, vp]
         L.oracle_round_bf16.argtypes = [ctypes.c_double]
         L.oracle_round_bf16.restype = ctypes.c_uint16
         _lib = L
@@ -148,6 +150,25 @@ def gate_value(h, m, dtype, gate=GATE_SIGMOID, lam=1.0):
     h = np.ascontiguousarray(h)
     m = np.ascontiguousarray(m)
     return float(lib().oracle_gate(_p(h), _p(m), h.size, dtype, gate, float(lam)))
+
+
+def head_topk(w, h, K, dtype, with_logits=False):
+    """Early-exit head (Eq. 13, Eq. 14): w [V x D], h [B x D] (float32, or
+    uint16 bf16 patterns) -> ids int32 [B x K], probs float64 [B x K] (and
+    the float64 logits [B x V] when asked)."""
+    w = np.ascontiguousarray(w)
+    h = np.ascontiguousarray(h)
+    V, D = w.shape
+    B = h.shape[0]
+    assert h.shape[1] == D
+    ids = np.empty((B, K), np.int32)
+    probs = np.empty((B, K), np.float64)
+    logits = np.empty((B, V), np.float64) if with_logits else None
+    st = lib().oracle_head_topk(_p(w), _p(h), V, D, B, K, dtype, _p(ids), _p(probs),
+                                _p(logits) if with_logits else None)
+    if st != OK:
+        raise OracleError(st)
+    return (ids, probs, logits) if with_logits else (ids, probs)
 
 
 def round_bf16(x):
