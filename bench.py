@@ -96,7 +96,8 @@ def main():
     ap.add_argument("--latency-steps", type=int, default=2000)
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--workload", choices=("decode", "multi", "tiered"), default="decode")
+    ap.add_argument("--workload", choices=("decode", "multi", "tiered", "head"), default="decode")
+    ap.add_argument("--head-k", type=int, default=128)
     ap.add_argument("--tier-steps", type=int, default=2000)
     ap.add_argument("--tier-warmup", type=int, default=100)
     ap.add_argument("--t-hide-us", default="0,100")
@@ -117,6 +118,8 @@ def main():
     torch.cuda.set_device(0)
     if args.workload == "tiered":
         return run_tiered(args)
+    if args.workload == "head":
+        return run_head(args)
     t0 = time.time()
     table = synth.config2_table()
     gt = H.GpuTable(table)
@@ -394,6 +397,99 @@ def finish_multi(args, table, gt, sets, mslots, B, ctx, S, window, L, tokens_per
 def synth_hidden(batch, B):
     import synth
     return synth.normal_range(batch.seed, batch.hidden_tag, 0, B, D, 1.0, synth.BF16)
+
+
+def run_head(args):
+    """Early-exit prefetch head (Eq. 13, Eq. 14): softmax(W h) and its top K
+    for one batch-64 decode step, W = 151936 x 1024 bf16 (311 MB)."""
+    import torch
+
+    import synth
+    from paper_2607_07388_amd import tfe
+
+    V, Dh, B, K = synth.V, 1024, 64, args.head_k
+    stream = torch.cuda.current_stream()
+    w = torch.empty((V, Dh), dtype=torch.bfloat16, device="cuda")
+    synth.normal_fill_device(w.data_ptr(), 0, V, Dh, 5, 42, 0.1, synth.BF16, stream.cuda_stream)
+    sets = []
+    for k in range(args.sets):
+        h = torch.empty((B, Dh), dtype=torch.bfloat16, device="cuda")
+        synth.normal_fill_device(h.data_ptr(), 0, B, Dh, 5, 43 + 16 * k, 1.0, synth.BF16,
+                                 stream.cuda_stream)
+        sets.append((h, torch.empty((B, K), dtype=torch.int32, device="cuda"),
+                     torch.empty((B, K), dtype=torch.float32, device="cuda")))
+    head = tfe.tfe_head_create(w, V, Dh, B, K)
+    torch.cuda.synchronize()
+
+    def call(k):
+        h, ids, prob = sets[k % len(sets)]
+        tfe.tfe_head_topk(head, h, B, K, ids, prob, stream.cuda_stream)
+
+    for k in range(args.warmup):
+        call(k)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    w0 = time.perf_counter()
+    e0.record(stream)
+    for k in range(args.steps):
+        call(k)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - w0
+    avg = e0.elapsed_time(e1) * 1e-3 / args.steps
+    # Algorithmic bytes of one call: W once, the hidden rows, the outputs.
+    nbytes = V * Dh * 2 + B * Dh * 2 + B * K * 8
+    flops = 2.0 * V * Dh * B
+    result = {
+        "metric": "early-exit prefetch head calls/sec (softmax(W h) + top-K), batch-64 decode, "
+                  "1 MI355X",
+        "value": args.steps / wall,
+        "unit": "calls/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": wall / args.steps * 1e3,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": "early-exit head: W 151936 x 1024 bf16 ~N(0, 0.1), 64 hidden "
+                               "rows ~N(0, 1), top %d" % K, "vocab": V, "dim": Dh, "batch": B,
+                   "k": K},
+        "roofline": {
+            "bound": "hbm",
+            "kernel": "tfe_head_topk (k_head_logits + k_head_select + k_head_merge)",
+            "achieved": nbytes / avg / 1e9,
+            "peak": HBM_PEAK_GBPS,
+            "unit": "GB/s",
+            "frac": nbytes / avg / 1e9 / HBM_PEAK_GBPS,
+            "traffic": None,
+            "bytes_per_launch": nbytes,
+            "avg_launch_us": avg * 1e6,
+            "mfma_tflops": flops / avg / 1e12,
+        },
+    }
+    if not args.no_cpu_baseline:
+        import oracle
+        wh = synth.normal_range(5, 42, 0, V, Dh, 0.1, synth.BF16)
+        hh = synth.normal_range(5, 43, 0, B, Dh, 1.0, synth.BF16)
+        done, c0 = 0, time.perf_counter()
+        while time.perf_counter() - c0 < args.cpu_seconds:
+            oracle.head_topk(wh, hh[done % B:done % B + 1], K, synth.BF16)
+            done += 1
+        csec = time.perf_counter() - c0
+        result["cpu_baseline"] = {
+            "value": done / B / csec,
+            "unit": "calls/s",
+            "cores": 1,
+            "kind": "oracle",
+            "sample": "%d of the 64 rows of one call (double-precision logits over the full "
+                      "vocabulary + partial sort), %.1f s, single thread, scaled to calls"
+                      % (done, csec),
+        }
+    tfe.tfe_head_free(head)
+    print(json.dumps(result))
 
 
 def run_tiered(args):

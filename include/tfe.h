@@ -201,6 +201,36 @@ tfe_status tfe_prefetch_scored(tfe_table *table, const int32_t *tail, int32_t ta
                                const int32_t *candidates, const float *cand_prob, int32_t B,
                                int32_t K, int32_t budget, void *side_stream);
 
+/* ---- Early-exit prefetch head ---------------------------------------------
+ * Paper: Eq. 13 (approximate next-token distribution softmax(W_pref h) from
+ * the hidden state of an intermediate layer), Eq. 14 (its top-K tokens), and
+ * Sec. 4.4 (the candidates drive the prefetch: pass top_ids and top_prob to
+ * tfe_prefetch_scored as candidates and cand_prob). */
+typedef struct tfe_head tfe_head; /* opaque; owned by the library */
+
+/* Prepares a head for the projection w_pref: DEVICE bf16 [vocab x dim],
+ * row-major, 16-byte aligned, on the current device.  The head keeps the
+ * pointer (no copy): w_pref must stay valid and unchanged until
+ * tfe_head_free.  dim is 256, 512 or 1024; 1 <= vocab <= 2^18;
+ * 1 <= max_k <= min(256, vocab); 1 <= max_batch <= 65535 sizes the scratch
+ * (max_batch x vocab float32 logits plus candidate lists). */
+tfe_status tfe_head_create(const void *w_pref, int32_t vocab, int32_t dim, int32_t max_batch,
+                           int32_t max_k, tfe_head **out);
+
+/* For each of the B rows of `hidden` (DEVICE bf16 [B x dim], 16-byte
+ * aligned): top_ids[b*K + i] (DEVICE int32) is the token of i-th largest
+ * probability under softmax(W_pref h_b) (ties in logit go to the lower id)
+ * and top_prob[b*K + i] (DEVICE float32) its probability.  Logits and the
+ * softmax are computed in float32 (bf16 products, float32 accumulation).
+ * 0 <= B <= max_batch, 0 <= K <= max_k; stream-ordered on `stream`.  Calls
+ * on one head share its scratch: they must be ordered (same stream, or
+ * synchronised). */
+tfe_status tfe_head_topk(tfe_head *head, const void *hidden, int32_t B, int32_t K,
+                         int32_t *top_ids, float *top_prob, void *stream);
+
+/* Releases a head (waits for the device first).  NULL is accepted. */
+tfe_status tfe_head_free(tfe_head *head);
+
 /* Copies the table's counters (synchronises with the table's pending work). */
 tfe_status tfe_get_stats(tfe_table *table, tfe_stats *out);
 

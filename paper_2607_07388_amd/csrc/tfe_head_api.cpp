@@ -1,0 +1,172 @@
+// C ABI of the early-exit prefetch head: create / top-K / free.
+#include <hip/hip_runtime_api.h>
+#include <stdint.h>
+
+#include <new>
+
+#include "../../include/tfe.h"
+#include "tfe_head.h"
+#include "tfe_internal.h"
+
+struct tfe_head {
+  int device = 0;
+  int cus = 256;
+  const void* w = nullptr;   // caller's [V x D] bf16 projection (not owned)
+  uint32_t V = 0, D = 0, max_batch = 0, max_k = 0, C = 1;
+  float* d_logits = nullptr;  // [max_batch x V]
+  uint64_t* d_cand = nullptr; // [max_batch x C x max_k]
+  uint32_t* d_cnt = nullptr;  // [max_batch x C]
+  float* d_part = nullptr;    // [max_batch x C x 2]
+};
+
+namespace tfe {
+namespace {
+
+tfe_status hip_fail(hipError_t e, const char* what) {
+  return fail(TFE_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+#define HEAD_HIP(call, what)                         \
+  do {                                               \
+    hipError_t e_ = (call);                          \
+    if (e_ != hipSuccess) return hip_fail(e_, what); \
+  } while (0)
+
+void release(tfe_head* h) {
+  if (!h) return;
+  int cur = 0;
+  (void)hipGetDevice(&cur);
+  (void)hipSetDevice(h->device);
+  (void)hipDeviceSynchronize();
+  void* bufs[] = {h->d_logits, h->d_cand, h->d_cnt, h->d_part};
+  for (void* b : bufs)
+    if (b) (void)hipFree(b);
+  (void)hipSetDevice(cur);
+  delete h;
+}
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+tfe_status create(const void* w, int32_t vocab, int32_t dim, int32_t max_batch, int32_t max_k,
+                  tfe_head** out) {
+  if (!out) return fail(TFE_ERR_INVALID_ARG, "null output handle");
+  *out = nullptr;
+  if (!w) return fail(TFE_ERR_INVALID_ARG, "null projection");
+  if (!aligned16(w)) return fail(TFE_ERR_INVALID_ARG, "projection not 16-byte aligned");
+  if (vocab < 1 || vocab > (1 << 18)) return fail(TFE_ERR_INVALID_ARG, "vocab outside [1, 2^18]");
+  if (!head_dim_supported(dim)) return fail(TFE_ERR_UNSUPPORTED, "dim %d (256, 512 or 1024)", dim);
+  if (max_batch < 1 || max_batch > 65535)
+    return fail(TFE_ERR_INVALID_ARG, "max_batch outside [1, 65535]");
+  if (max_k < 1 || max_k > kHeadMaxK || max_k > vocab)
+    return fail(TFE_ERR_INVALID_ARG, "max_k outside [1, min(%d, vocab)]", kHeadMaxK);
+  hipPointerAttribute_t attr;
+  const hipError_t pe = hipPointerGetAttributes(&attr, w);
+  if (pe != hipSuccess || attr.type != hipMemoryTypeDevice) {
+    (void)hipGetLastError();
+    return fail(TFE_ERR_INVALID_ARG, "projection is not device memory");
+  }
+  tfe_head* h = new (std::nothrow) tfe_head;
+  if (!h) return fail(TFE_ERR_OOM, "head");
+  tfe_status st = TFE_OK;
+  do {
+    if (hipGetDevice(&h->device) != hipSuccess) { st = fail(TFE_ERR_HIP, "hipGetDevice"); break; }
+    if (attr.device != h->device) {
+      st = fail(TFE_ERR_INVALID_ARG, "projection lives on device %d, device %d is current",
+                attr.device, h->device);
+      break;
+    }
+    int lds = 0;
+    if (hipDeviceGetAttribute(&h->cus, hipDeviceAttributeMultiprocessorCount, h->device) !=
+            hipSuccess ||
+        hipDeviceGetAttribute(&lds, hipDeviceAttributeMaxSharedMemoryPerBlock, h->device) !=
+            hipSuccess) {
+      st = fail(TFE_ERR_HIP, "device attributes");
+      break;
+    }
+    if ((uint32_t)lds < head_lds_bytes(dim)) {
+      st = fail(TFE_ERR_UNSUPPORTED, "dim %d needs %u bytes of LDS per block, device has %d",
+                dim, head_lds_bytes(dim), lds);
+      break;
+    }
+    h->w = w;
+    h->V = (uint32_t)vocab;
+    h->D = (uint32_t)dim;
+    h->max_batch = (uint32_t)max_batch;
+    h->max_k = (uint32_t)max_k;
+    h->C = head_chunks(h->V);
+    const size_t nb = h->max_batch;
+    if (hipMalloc(&h->d_logits, nb * h->V * sizeof(float)) != hipSuccess ||
+        hipMalloc(&h->d_cand, nb * h->C * h->max_k * sizeof(uint64_t)) != hipSuccess ||
+        hipMalloc(&h->d_cnt, nb * h->C * sizeof(uint32_t)) != hipSuccess ||
+        hipMalloc(&h->d_part, nb * h->C * 2 * sizeof(float)) != hipSuccess) {
+      (void)hipGetLastError();
+      st = fail(TFE_ERR_OOM, "head scratch for %u rows", h->max_batch);
+      break;
+    }
+  } while (0);
+  if (st != TFE_OK) {
+    release(h);
+    return st;
+  }
+  *out = h;
+  return TFE_OK;
+}
+
+tfe_status topk(tfe_head* h, const void* hidden, int32_t B, int32_t K, int32_t* ids, float* prob,
+                hipStream_t stream) {
+  if (!h) return fail(TFE_ERR_INVALID_ARG, "null head");
+  if (B < 0 || (uint32_t)B > h->max_batch)
+    return fail(TFE_ERR_INVALID_ARG, "B outside [0, %u]", h->max_batch);
+  if (K < 0 || (uint32_t)K > h->max_k) return fail(TFE_ERR_INVALID_ARG, "K outside [0, %u]", h->max_k);
+  if (B == 0 || K == 0) return TFE_OK;
+  if (!hidden || !ids || !prob) return fail(TFE_ERR_INVALID_ARG, "null hidden, ids or probs");
+  if (!aligned16(hidden)) return fail(TFE_ERR_INVALID_ARG, "hidden not 16-byte aligned");
+  int cur = -1;
+  HEAD_HIP(hipGetDevice(&cur), "hipGetDevice");
+  if (cur != h->device)
+    return fail(TFE_ERR_INVALID_ARG, "head lives on device %d but device %d is current",
+                h->device, cur);
+  HeadArgs a;
+  a.w = h->w;
+  a.hidden = hidden;
+  a.logits = h->d_logits;
+  a.cand = h->d_cand;
+  a.cnt = h->d_cnt;
+  a.part = h->d_part;
+  a.top_ids = ids;
+  a.top_prob = prob;
+  a.V = h->V;
+  a.D = h->D;
+  a.B = (uint32_t)B;
+  a.K = (uint32_t)K;
+  a.C = h->C;
+  HEAD_HIP(launch_head_logits(a, (uint32_t)h->cus, stream), "head logits launch");
+  HEAD_HIP(launch_head_select(a, stream), "head select launch");
+  HEAD_HIP(launch_head_merge(a, stream), "head merge launch");
+  return TFE_OK;
+}
+
+}  // namespace
+}  // namespace tfe
+
+extern "C" {
+
+tfe_status tfe_head_create(const void* w_pref, int32_t vocab, int32_t dim, int32_t max_batch,
+                           int32_t max_k, tfe_head** out) {
+  tfe::clear_error();
+  return tfe::create(w_pref, vocab, dim, max_batch, max_k, out);
+}
+
+tfe_status tfe_head_topk(tfe_head* head, const void* hidden, int32_t B, int32_t K,
+                         int32_t* top_ids, float* top_prob, void* stream) {
+  tfe::clear_error();
+  return tfe::topk(head, hidden, B, K, top_ids, top_prob, (hipStream_t)stream);
+}
+
+tfe_status tfe_head_free(tfe_head* head) {
+  tfe::clear_error();
+  tfe::release(head);
+  return TFE_OK;
+}
+
+}  // extern "C"

@@ -71,6 +71,9 @@ def _load():
                                      ctypes.c_float, vp], ctypes.c_int),
         "tfe_prefetch": ([vp, vp, i32, vp, i32, i32, vp], ctypes.c_int),
         "tfe_prefetch_scored": ([vp, vp, i32, vp, vp, i32, i32, i32, vp], ctypes.c_int),
+        "tfe_head_create": ([vp, i32, i32, i32, i32, ctypes.POINTER(vp)], ctypes.c_int),
+        "tfe_head_topk": ([vp, vp, i32, i32, vp, vp, vp], ctypes.c_int),
+        "tfe_head_free": ([vp], ctypes.c_int),
         "tfe_get_stats": ([vp, ctypes.POINTER(tfe_stats)], ctypes.c_int),
         "tfe_reset_stats": ([vp], ctypes.c_int),
         "tfe_last_error": ([], ctypes.c_char_p),
@@ -90,7 +93,7 @@ lib = _load()
 # Every symbol the C header declares (checked by the CPU test suite).
 EXPORTED = ("tfe_table_load", "tfe_table_free", "tfe_lookup_inject", "tfe_lookup_inject_multi",
             "tfe_prefetch",
-            "tfe_prefetch_scored",
+            "tfe_prefetch_scored", "tfe_head_create", "tfe_head_topk", "tfe_head_free",
             "tfe_get_stats", "tfe_reset_stats", "tfe_last_error", "tfe_index_capacity",
             "tfe_index_build_host", "tfe_index_probe_host")
 
@@ -160,6 +163,21 @@ def tfe_prefetch_scored(table, tail, tail_len, candidates, cand_prob, B, K, budg
     return _check(lib.tfe_prefetch_scored(table, addr(tail), tail_len, addr(candidates),
                                           addr(cand_prob), B, K, budget,
                                           stream_handle(side_stream)))
+
+
+def tfe_head_create(w_pref, vocab, dim, max_batch, max_k):
+    h = ctypes.c_void_p()
+    _check(lib.tfe_head_create(addr(w_pref), vocab, dim, max_batch, max_k, ctypes.byref(h)))
+    return h.value
+
+
+def tfe_head_topk(head, hidden, B, K, top_ids, top_prob, stream=None):
+    return _check(lib.tfe_head_topk(head, addr(hidden), B, K, addr(top_ids), addr(top_prob),
+                                    stream_handle(stream)))
+
+
+def tfe_head_free(head):
+    return _check(lib.tfe_head_free(head))
 
 
 def tfe_get_stats(table):
