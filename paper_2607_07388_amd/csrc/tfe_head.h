@@ -6,32 +6,29 @@
 
 namespace tfe {
 
-// Chunks per batch row of the top-K selection and its limits.
+// Limits of the top-K selection.
 constexpr int kHeadMaxK = 256;
-constexpr int kHeadMaxChunks = 16;
-constexpr int kHeadChunkMax = 16384;  // logits per chunk (keys held in registers)
+constexpr int kHeadMaxTiles = 16384;  // 16-token tiles per row: vocab <= 2^18
 
 struct HeadArgs {
   const void* w;        // [V x D] bf16, row-major
   const void* hidden;   // [B x D] bf16
-  float* logits;        // [B x V] scratch
-  uint64_t* cand;       // [B x C x K] scratch: selected (logit, id) keys per chunk
-  uint32_t* cnt;        // [B x C] keys selected per chunk
-  float* part;          // [B x C x 2] chunk max logit and sum of exp(logit - max)
+  // Scratch: groups of 64 rows (B rounded up), tpitch 16-token tiles per
+  // group (V rounded up to 32, over 16), tblocks = tpitch / 16 rounded up.
+  float* logits;        // [groups x tpitch x 64 x 16], tile-major
+  uint64_t* tkey;       // [groups x tblocks x 64 x 16]: largest (logit, id) key per tile
+  float* tsum;          // [groups x tblocks x 64 x 16]: sum of exp(logit - tile max)
   int32_t* top_ids;     // [B x K]
   float* top_prob;      // [B x K]
-  uint32_t V, D, B, K, C;
+  uint32_t V, tpitch, tblocks, D, B, K;
 };
 
-// Chunks per row for a vocabulary of V tokens.
-uint32_t head_chunks(uint32_t V);
 // True if D has a logits kernel.
 bool head_dim_supported(int D);
 // Bytes of static LDS the logits kernel uses for D (checked against the device).
 uint32_t head_lds_bytes(int D);
 
 hipError_t launch_head_logits(const HeadArgs& a, uint32_t blocks, hipStream_t s);
-hipError_t launch_head_select(const HeadArgs& a, hipStream_t s);
-hipError_t launch_head_merge(const HeadArgs& a, hipStream_t s);
+hipError_t launch_head_rows(const HeadArgs& a, hipStream_t s);
 
 }  // namespace tfe

@@ -3,26 +3,27 @@
 // (Eq. 13) and its K most likely tokens (Eq. 14), which are the candidates
 // the cache prefetch consumes.
 //
-// Three launches:
+// Two launches:
 //   k_head_logits  logits = W h for up to 64 rows h per block: a dense
 //                  contraction, so it runs on the matrix cores
 //                  (v_mfma_f32_16x16x32_bf16).  W ([V x D] bf16, 311 MB for
 //                  the 151936 x 1024 head) is streamed from HBM exactly once
 //                  per 64 rows; the 64 hidden rows are staged in LDS and read
-//                  by every wave.  One wave computes a 16-token x 64-row
-//                  tile: it loads its 16 W rows whole (D/32 16-byte loads per
-//                  lane, all in flight before the first MFMA), then runs D/32
-//                  k-steps of 4 MFMAs.  fp32 logits go to a scratch buffer.
-//   k_head_select  per (row, chunk of the vocabulary): the chunk's K largest
-//                  (logit, -id) keys by an exact 8-bit radix select over
-//                  64-bit keys, plus the chunk's max logit and sum of
-//                  exp(logit - max).
-//   k_head_merge   per row: bitonic sort of the chunks' candidates, the top
-//                  K with their probabilities exp(l - M) / S, M and S merged
-//                  from the chunk partials (a log-sum-exp merge).
-// Ties in logit go to the lower token id, so the answer is unique.  The
-// exponentials use the full-accuracy expf (about 1 ulp): their cost is small
-// next to the logits, and the probabilities feed a priority score.
+//                  by every wave.  One wave computes a 32-token x 64-row
+//                  super-tile (two MFMA row tiles sharing each LDS read of
+//                  h): half of its 32 W rows at a time, D/64 16-byte loads
+//                  per lane and row tile all in flight before the MFMAs.
+//                  The epilogue writes the fp32 logits and, per (row,
+//                  16-token tile), the largest (logit, id) key and the sum of
+//                  exp(logit - tile max).
+//   k_head_rows    per row: the log-sum-exp from the tile statistics, the
+//                  K-th largest tile key by radix select, then the logits of
+//                  those K tiles (every top-K logit lies in one) sorted in LDS.
+// Ties in logit go to the lower token id, so the answer is unique.  The K
+// output probabilities use the full-accuracy expf (about 1 ulp); the chunk
+// sums of exp(l - max) use the hardware exponential, whose relative error
+// (about |l - max| 2^-24 plus an ulp) is negligible in a sum dominated by
+// terms near the maximum.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -35,12 +36,15 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
-constexpr int kLogitWaves = 8;   // waves per logits block
+#ifndef TFE_HEAD_WAVES
+#define TFE_HEAD_WAVES 8
+#endif
+#ifndef TFE_HEAD_NT
+#define TFE_HEAD_NT 0
+#endif
+
+constexpr int kLogitWaves = TFE_HEAD_WAVES;  // waves per logits block (tuning knob)
 constexpr int kCols = 64;        // hidden rows per logits block (4 MFMA column tiles)
-constexpr int kSelThreads = 256;
-constexpr int kSelPer = kHeadChunkMax / kSelThreads;  // logits per thread in a chunk
-constexpr int kMergeThreads = 256;
-constexpr int kMergeMax = kHeadMaxChunks * kHeadMaxK;  // candidates per row
 
 // Order-preserving float -> uint32 map (larger float, larger key).
 __device__ __forceinline__ uint32_t f2key(float f) {
@@ -50,16 +54,90 @@ __device__ __forceinline__ uint32_t f2key(float f) {
 __device__ __forceinline__ float key2f(uint32_t k) {
   return __uint_as_float((k & 0x80000000u) ? (k & 0x7FFFFFFFu) : ~k);
 }
+// 64-bit unsigned max / min (the generic max/min overloads can resolve to
+// floating point for mixed integer types, which would round the keys).
+__device__ __forceinline__ uint64_t umax64(uint64_t x, uint64_t y) { return x > y ? x : y; }
+__device__ __forceinline__ uint64_t umin64(uint64_t x, uint64_t y) { return x < y ? x : y; }
+__device__ __forceinline__ uint64_t shfl_xor64(uint64_t x, int m) {
+  return (uint64_t)__shfl_xor((unsigned long long)x, m, 64);
+}
 // (logit, token) -> 64-bit key: higher logit first, then lower token id.
-__device__ __forceinline__ uint64_t make_key(float l, uint32_t id) {
+// Keys are distinct, and 0 is below every real key.
+__device__ __forceinline__ uint64_t tkey64(float l, uint32_t id) {
   return ((uint64_t)f2key(l) << 32) | (uint64_t)(0xFFFFFFFFu - id);
+}
+
+// Reductions over the four lanes r, r + 16, r + 32, r + 48 that hold one
+// MFMA output column: permlane16_swap pairs rows 0-1 and 2-3 of the wave,
+// permlane32_swap pairs the two halves; combining both outputs of each swap
+// leaves every lane with the reduction in a fixed order.
+__device__ __forceinline__ uint64_t col_max64(uint64_t k) {
+  uint32_t hi = (uint32_t)(k >> 32), lo = (uint32_t)k;
+  const auto h16 = __builtin_amdgcn_permlane16_swap(hi, hi, false, false);
+  const auto l16 = __builtin_amdgcn_permlane16_swap(lo, lo, false, false);
+  k = umax64(((uint64_t)h16[0] << 32) | l16[0], ((uint64_t)h16[1] << 32) | l16[1]);
+  hi = (uint32_t)(k >> 32);
+  lo = (uint32_t)k;
+  const auto h32 = __builtin_amdgcn_permlane32_swap(hi, hi, false, false);
+  const auto l32 = __builtin_amdgcn_permlane32_swap(lo, lo, false, false);
+  return umax64(((uint64_t)h32[0] << 32) | l32[0], ((uint64_t)h32[1] << 32) | l32[1]);
+}
+__device__ __forceinline__ float col_sum(float x) {
+  uint32_t u = __float_as_uint(x);
+  const auto a = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+  u = __float_as_uint(__uint_as_float(a[0]) + __uint_as_float(a[1]));
+  const auto b = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+  return __uint_as_float(b[0]) + __uint_as_float(b[1]);
+}
+
+// Stores one 16-token x 64-row tile of logits and its statistics.  Logits
+// are tile-major: logits[((grp * tpitch + t) * 64 + c) * 16 + i] for column
+// c = j - 64 grp and token 16 t + i, so a tile is one contiguous 4 KB block
+// (each store instruction writes 1 KB of whole lines) and a row's 16 logits
+// of a tile are 64 contiguous bytes.  Statistics are blocked by 16 tiles:
+// entry (t, c) at ((grp * tblocks + t / 16) * 64 + c) * 16 + t % 16, so 16
+// consecutive tiles of a row fill one 128-byte line (written by the block's
+// waves close together in time, read whole by the top-K kernel).
+// D operand: lane (r, g) holds tokens t*16 + 4 g + q, q = 0..3, of column r.
+// The scratch is padded (whole 32-token super-tiles, rows up to a multiple
+// of 64), so the logits stores are in bounds and unconditional (columns
+// past B and tokens past V hold junk that nothing reads).
+__device__ __forceinline__ void tile_epilogue(const HeadArgs& a, uint32_t t, int r, int g,
+                                              const f32x4* acc) {
+  const uint32_t i0 = t * 16 + 4 * g;
+  const size_t tile = (size_t)blockIdx.y * a.tpitch + t;
+#pragma unroll
+  for (int bt = 0; bt < 4; ++bt) {
+    const uint32_t c = bt * 16 + r;
+    *(f32x4*)(a.logits + (tile * 64 + c) * 16 + 4 * g) = acc[bt];
+    // Tile statistics of column c: the largest (logit, id) key of the 16
+    // tokens and the sum of exp(logit - tile max); all four lanes of the
+    // column hold the same values and the first one writes them.
+    uint64_t best = 0;
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      best = umax64(best, i0 + q < a.V ? tkey64(acc[bt][q], i0 + q) : (uint64_t)0);
+    best = col_max64(best);
+    const float m = key2f((uint32_t)(best >> 32));
+    float sum = 0.f;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) sum += i0 + q < a.V ? __expf(acc[bt][q] - m) : 0.f;
+    sum = col_sum(sum);
+    if (g == 0) {
+      const size_t o = (((size_t)blockIdx.y * a.tblocks + (t >> 4)) * 64 + c) * 16 + (t & 15);
+      a.tkey[o] = best;
+      a.tsum[o] = sum;
+    }
+  }
 }
 
 template <int KS>  // KS = D / 32 k-steps
 __global__ __launch_bounds__(kLogitWaves * 64) void k_head_logits(const HeadArgs a) {
   constexpr int D = KS * 32;
   constexpr int STRIDE = D + 8;  // staged row pitch (elements): conflict-free b128 reads
+  constexpr int HALF = KS / 2;
   __shared__ __attribute__((aligned(16))) __bf16 hs[kCols * STRIDE];
+  __shared__ uint32_t s_next;
   const uint32_t col0 = blockIdx.y * kCols;
   const int ncols = (int)min((uint32_t)kCols, a.B - col0);
   for (int e = threadIdx.x; e < kCols * (D / 8); e += kLogitWaves * 64) {
@@ -68,50 +146,77 @@ __global__ __launch_bounds__(kLogitWaves * 64) void k_head_logits(const HeadArgs
     if (j < ncols) v = *((const u32x4*)a.hidden + ((size_t)(col0 + j) * D) / 8 + c);
     *(u32x4*)(hs + j * STRIDE + c * 8) = v;
   }
+  // The block owns a contiguous range of 32-token super-tiles; its waves
+  // claim them one at a time, so every wave stays busy until the range is
+  // done (the block's share of W is fixed; only the split among its waves
+  // is dynamic).
+  const uint32_t nst = (a.V + 31) >> 5;
+  const uint32_t st_lo = (uint32_t)((uint64_t)nst * blockIdx.x / gridDim.x);
+  const uint32_t st_hi = (uint32_t)((uint64_t)nst * (blockIdx.x + 1) / gridDim.x);
+  if (threadIdx.x == 0) s_next = st_lo;
   __syncthreads();
-  const int nbt = (ncols + 15) >> 4;  // live 16-row column tiles
   const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
   const int r = lane & 15, g = lane >> 4;
-  const uint32_t ntiles = (a.V + 15) >> 4;
-  for (uint32_t t = blockIdx.x * kLogitWaves + wave; t < ntiles; t += gridDim.x * kLogitWaves) {
-    // A operand: W rows t*16 + r (clamped in the last tile), k = 32 s + 8 g.
-    const uint32_t row = min(t * 16 + r, a.V - 1);
-    const u32x4* wp = (const u32x4*)a.w + ((size_t)row * D) / 8 + g;
-    u32x4 av[KS];
-#pragma unroll
-    for (int s = 0; s < KS; ++s) av[s] = __builtin_nontemporal_load(wp + 4 * s);
-    f32x4 acc[4];
-#pragma unroll
-    for (int bt = 0; bt < 4; ++bt) acc[bt] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int s = 0; s < KS; ++s) {
-#pragma unroll
-      for (int bt = 0; bt < 4; ++bt) {
-        if (bt < nbt) {
-          const u32x4 bv = *(const u32x4*)(hs + (bt * 16 + r) * STRIDE + 32 * s + 8 * g);
-          acc[bt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-              __builtin_bit_cast(bf16x8, av[s]), __builtin_bit_cast(bf16x8, bv), acc[bt], 0, 0,
-              0);
-        }
-      }
-    }
-    // D operand: lane (r, g) holds tokens t*16 + 4 g + q, q = 0..3, of column r.
-    const uint32_t i0 = t * 16 + 4 * g;
+  // The staged hidden rows do not change across tiles; hiding the offset
+  // from the optimiser keeps their LDS reads inside the loop (hoisted, the
+  // whole 128 KB B operand would be held in registers and spill).
+  int hoff = r * STRIDE + 8 * g;
+  for (;;) {
+    uint32_t st = 0;
+    if (lane == 0) st = atomicAdd(&s_next, 1u);
+    st = __builtin_amdgcn_readfirstlane(st);
+    if (st >= st_hi) break;
+    asm volatile("" : "+v"(hoff));
+    // A operands: tile u (u = 0, 1) holds W rows 32 st + 16 u + r (clamped
+    // past the vocabulary), k = 32 s + 8 g.  Each half of the rows is
+    // loaded whole (2 x 16 loads in flight per wave) before its MFMAs; each
+    // LDS read of the hidden rows feeds both tiles.
+    const u32x4* wp0 = (const u32x4*)a.w + ((size_t)min(st * 32 + r, a.V - 1) * D) / 8 + g;
+    const u32x4* wp1 = (const u32x4*)a.w + ((size_t)min(st * 32 + 16 + r, a.V - 1) * D) / 8 + g;
+    f32x4 acc0[4], acc1[4];
 #pragma unroll
     for (int bt = 0; bt < 4; ++bt) {
-      const int j = bt * 16 + r;
-      if (bt < nbt && j < ncols) {
-        float* dst = a.logits + (size_t)(col0 + j) * a.V + i0;
-        if ((a.V & 3u) == 0 && i0 + 3 < a.V) {
-          *(f32x4*)dst = acc[bt];
-        } else {
+      acc0[bt] = f32x4{0.f, 0.f, 0.f, 0.f};
+      acc1[bt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
 #pragma unroll
-          for (int q = 0; q < 4; ++q)
-            if (i0 + q < a.V) dst[q] = acc[bt][q];
+    for (int h = 0; h < 2; ++h) {
+      u32x4 av0[HALF], av1[HALF];
+#pragma unroll
+      for (int s = 0; s < HALF; ++s) {
+#if TFE_HEAD_NT
+        av0[s] = __builtin_nontemporal_load(wp0 + 4 * (h * HALF + s));
+        av1[s] = __builtin_nontemporal_load(wp1 + 4 * (h * HALF + s));
+#else
+        av0[s] = wp0[4 * (h * HALF + s)];
+        av1[s] = wp1[4 * (h * HALF + s)];
+#endif
+      }
+      // Keep the half's loads together ahead of its MFMAs (left alone, the
+      // scheduler interleaves them and keeps only a few in flight).
+      __builtin_amdgcn_sched_barrier(0);
+      // All four column tiles are computed even when fewer rows are live
+      // (the staged rows past B are zero): a branch per tile would
+      // serialise every MFMA behind its own LDS read.
+#pragma unroll
+      for (int s = 0; s < HALF; ++s) {
+        u32x4 bv[4];
+#pragma unroll
+        for (int bt = 0; bt < 4; ++bt)
+          bv[bt] = *(const u32x4*)(hs + hoff + bt * 16 * STRIDE + 32 * (h * HALF + s));
+#pragma unroll
+        for (int bt = 0; bt < 4; ++bt) {
+          acc0[bt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, av0[s]),
+                                                             __builtin_bit_cast(bf16x8, bv[bt]),
+                                                             acc0[bt], 0, 0, 0);
+          acc1[bt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, av1[s]),
+                                                             __builtin_bit_cast(bf16x8, bv[bt]),
+                                                             acc1[bt], 0, 0, 0);
         }
       }
     }
+    tile_epilogue(a, 2 * st, r, g, acc0);
+    tile_epilogue(a, 2 * st + 1, r, g, acc1);
   }
 }
 
@@ -126,8 +231,10 @@ __device__ __forceinline__ float wave_add(float x) {
   return x;
 }
 
-// Inclusive block prefix sum over kSelThreads values.
-__device__ uint32_t sel_scan(uint32_t v, uint32_t* s_wave) {
+// Exclusive block prefix sum over the block's threads (NT of them); *total
+// receives the sum.
+template <int NT>
+__device__ uint32_t block_excl_scan(uint32_t v, uint32_t* s_wave, uint32_t* total) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   uint32_t x = v;
 #pragma unroll
@@ -137,169 +244,209 @@ __device__ uint32_t sel_scan(uint32_t v, uint32_t* s_wave) {
   }
   if (lane == 63) s_wave[wave] = x;
   __syncthreads();
-  uint32_t off = 0;
-  for (int w = 0; w < wave; ++w) off += s_wave[w];
+  uint32_t off = 0, tot = 0;
+#pragma unroll
+  for (int w = 0; w < NT / 64; ++w) {
+    off += w < wave ? s_wave[w] : 0u;
+    tot += s_wave[w];
+  }
   __syncthreads();
-  return x + off;
+  *total = tot;
+  return x - v + off;
 }
 
-__global__ __launch_bounds__(kSelThreads) void k_head_select(const HeadArgs a) {
-  __shared__ uint32_t hist[256];
-  __shared__ uint32_t s_wave[kSelThreads / 64];
-  __shared__ uint32_t s_bin, s_above, s_cnt, s_out;
-  __shared__ float s_red[kSelThreads / 64];
-  const uint32_t b = blockIdx.y, c = blockIdx.x;
-  const uint32_t lo = (uint32_t)((uint64_t)a.V * c / a.C);
-  const uint32_t hi = (uint32_t)((uint64_t)a.V * (c + 1) / a.C);
-  const uint32_t n = hi - lo;
-  const float* lg = a.logits + (size_t)b * a.V;
-  const int tid = threadIdx.x;
-
-  uint32_t key[kSelPer];
-  uint32_t kmax = 0;
-#pragma unroll
-  for (int i = 0; i < kSelPer; ++i) {
-    const uint32_t e = tid + i * kSelThreads;
-    key[i] = e < n ? f2key(lg[lo + e]) : 0u;
-    kmax = max(kmax, key[i]);
-  }
-  // Chunk max and sum of exp(l - max).
-  {
-    float m = key2f(kmax);
-    if (kmax == 0u) m = -INFINITY;
-    m = wave_max(m);
-    if ((tid & 63) == 0) s_red[tid >> 6] = m;
-    __syncthreads();
-    m = s_red[0];
-    for (int w = 1; w < kSelThreads / 64; ++w) m = fmaxf(m, s_red[w]);
-    __syncthreads();
-    float s = 0.f;
-#pragma unroll
-    for (int i = 0; i < kSelPer; ++i) {
-      const uint32_t e = tid + i * kSelThreads;
-      if (e < n) s += expf(key2f(key[i]) - m);
-    }
-    s = wave_add(s);
-    if ((tid & 63) == 0) s_red[tid >> 6] = s;
-    __syncthreads();
-    if (tid == 0) {
-      float t = 0.f;
-      for (int w = 0; w < kSelThreads / 64; ++w) t += s_red[w];
-      a.part[((size_t)b * a.C + c) * 2] = m;
-      a.part[((size_t)b * a.C + c) * 2 + 1] = t;
-    }
-  }
-
-  // Exact radix select of the K-th largest 64-bit key, 8 bits per pass from
-  // the top.  Keys are distinct (they contain the token id), so at the
-  // latest the last pass leaves one key in the chosen bin.
-  const uint32_t take = min(a.K, n);
-  uint64_t prefix = 0, mask = 0;
-  if (take < n) {
-    uint32_t need = take;
-    for (int pass = 0; pass < 8; ++pass) {
-      const int shift = 56 - 8 * pass;
-      hist[tid] = 0u;
-      __syncthreads();
-#pragma unroll
-      for (int i = 0; i < kSelPer; ++i) {
-        const uint32_t e = tid + i * kSelThreads;
-        if (e < n) {
-          const uint64_t k = ((uint64_t)key[i] << 32) | (uint64_t)(0xFFFFFFFFu - (lo + e));
-          if ((k & mask) == prefix) atomicAdd(&hist[(uint32_t)(k >> shift) & 255u], 1u);
+// Bitonic sort of a[0, N2) in LDS, descending; N2 a power of two.
+template <int NT>
+__device__ void lds_sort_desc(uint64_t* a, uint32_t N2) {
+  for (uint32_t size = 2; size <= N2; size <<= 1) {
+    for (uint32_t stride = size >> 1; stride > 0; stride >>= 1) {
+      for (uint32_t e = threadIdx.x; e < N2 / 2; e += NT) {
+        const uint32_t i = 2 * e - (e & (stride - 1));
+        const uint32_t j = i + stride;
+        const bool desc = (i & size) == 0;
+        const uint64_t x = a[i], y = a[j];
+        if ((x < y) == desc) {
+          a[i] = y;
+          a[j] = x;
         }
       }
       __syncthreads();
-      // Thread t looks at bin 255 - t: prefix sums count keys from the top.
-      const uint32_t v = hist[255 - tid];
-      const uint32_t incl = sel_scan(v, s_wave);
-      if (incl - v < need && need <= incl) {
+    }
+  }
+}
+
+__device__ __forceinline__ uint32_t pow2_ceil(uint32_t x) {
+  uint32_t p = 1;
+  while (p < x) p <<= 1;
+  return p;
+}
+
+constexpr int kRowThreads = 1024;
+constexpr int kRowTiles = kHeadMaxTiles / kRowThreads;  // tile entries per thread
+constexpr int kRowCand = 16 * kHeadMaxK;                // logits of the candidate tiles
+
+// Per row: the K most likely tokens and their probabilities from the tile
+// statistics and the logits.
+//   1. M = max logit, S = sum over tiles of tsum * exp(tile max - M).
+//   2. tau = the K-th largest tile-max key, by an exact radix select (8-bit
+//      digits from the top, per-wave histograms; keys are distinct, so a
+//      chosen bin ends up holding exactly the keys still needed).  Each of
+//      the K tiles at or above tau holds a logit at or above tau, so the
+//      K-th largest logit is at least tau and every top-K logit lies in one
+//      of these K tiles.
+//   3. The logits of those tiles at or above tau (at most 16 K) are sorted in
+//      LDS; the first K are the answer.
+__global__ __launch_bounds__(kRowThreads) void k_head_rows(const HeadArgs a) {
+  __shared__ uint64_t s_cand[kRowCand];
+  __shared__ uint32_t whist[kRowThreads / 64][256];
+  __shared__ uint32_t s_tiles[kHeadMaxK];
+  __shared__ uint32_t s_wave[kRowThreads / 64];
+  __shared__ float s_red[kRowThreads / 64];
+  __shared__ uint32_t s_bin, s_above, s_cnt;
+  const uint32_t b = blockIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const uint32_t NT = (a.V + 15) >> 4;
+  // Statistics of tile t of this row: block t / 16 of the row's 64-row
+  // group, column c, slot t % 16.
+  const size_t grp = b >> 6, c = b & 63;
+  const uint64_t* tk = a.tkey + (grp * a.tblocks * 64 + c) * 16;
+  const float* ts = a.tsum + (grp * a.tblocks * 64 + c) * 16;
+  auto sidx = [](uint32_t t) { return (size_t)(t >> 4) * 1024 + (t & 15); };
+
+  uint64_t key[kRowTiles];
+  uint64_t kmax = 0;
+#pragma unroll
+  for (int i = 0; i < kRowTiles; ++i) {
+    const uint32_t t = tid + i * kRowThreads;
+    key[i] = t < NT ? tk[sidx(t)] : 0;
+    kmax = umax64(kmax, key[i]);
+  }
+  // 1. Log-sum-exp over the tiles.
+  for (int d = 32; d >= 1; d >>= 1) kmax = umax64(kmax, shfl_xor64(kmax, d));
+  if (lane == 0) s_cand[wave] = kmax;
+  __syncthreads();
+  uint64_t gmax = 0;
+  for (int w = 0; w < kRowThreads / 64; ++w) gmax = umax64(gmax, s_cand[w]);
+  const float M = key2f((uint32_t)(gmax >> 32));
+  float part = 0.f;
+#pragma unroll
+  for (int i = 0; i < kRowTiles; ++i) {
+    const uint32_t t = tid + i * kRowThreads;
+    if (t < NT) part += ts[sidx(t)] * expf(key2f((uint32_t)(key[i] >> 32)) - M);
+  }
+  part = wave_add(part);
+  if (lane == 0) s_red[wave] = part;
+  __syncthreads();
+  float S = 0.f;
+  for (int w = 0; w < kRowThreads / 64; ++w) S += s_red[w];
+
+  // 2. The K-th largest tile key (all tiles when there are at most K).
+  const uint32_t take = min(a.K, NT);
+  uint64_t prefix = 0, mask = 0;
+  if (take < NT) {
+    uint32_t need = take;
+    for (int pass = 0; pass < 8; ++pass) {
+      const int shift = 56 - 8 * pass;
+      for (int e = lane; e < 256; e += 64) whist[wave][e] = 0u;
+      __syncthreads();
+#pragma unroll
+      for (int i = 0; i < kRowTiles; ++i) {
+        if (tid + i * kRowThreads < NT && (key[i] & mask) == prefix)
+          atomicAdd(&whist[wave][(uint32_t)(key[i] >> shift) & 255u], 1u);
+      }
+      __syncthreads();
+      // Thread t < 256 owns bin 255 - t: prefix sums count keys from the top.
+      uint32_t v = 0;
+      if (tid < 256)
+        for (int w = 0; w < kRowThreads / 64; ++w) v += whist[w][255 - tid];
+      uint32_t tot;
+      const uint32_t excl = block_excl_scan<kRowThreads>(v, s_wave, &tot);
+      if (tid < 256 && excl < need && need <= excl + v) {
         s_bin = 255 - tid;
-        s_above = incl - v;
+        s_above = excl;
         s_cnt = v;
       }
       __syncthreads();
       need -= s_above;
       prefix |= (uint64_t)s_bin << shift;
       mask |= (uint64_t)0xFF << shift;
-      const bool done = s_cnt == need;  // the whole bin is taken
+      const bool done = s_cnt == need;
       __syncthreads();
       if (done) break;
     }
   }
-  // Every key whose masked bits are at least the prefix is selected: exactly
-  // `take` keys.
-  if (tid == 0) s_out = 0u;
-  __syncthreads();
-  uint64_t* out = a.cand + ((size_t)b * a.C + c) * a.K;
+  // Candidate tiles: the `take` keys whose masked bits reach the prefix.
+  uint32_t mine = 0;
 #pragma unroll
-  for (int i = 0; i < kSelPer; ++i) {
-    const uint32_t e = tid + i * kSelThreads;
-    if (e < n) {
-      const uint64_t k = ((uint64_t)key[i] << 32) | (uint64_t)(0xFFFFFFFFu - (lo + e));
-      if ((k & mask) >= prefix) {
-        const uint32_t slot = atomicAdd(&s_out, 1u);
-        if (slot < a.K) out[slot] = k;
-      }
-    }
-  }
-  if (tid == 0) a.cnt[(size_t)b * a.C + c] = take;
-}
-
-__global__ __launch_bounds__(kMergeThreads) void k_head_merge(const HeadArgs a) {
-  __shared__ uint64_t keys[kMergeMax];
-  const uint32_t b = blockIdx.x;
-  const uint32_t N = a.C * a.K;
-  uint32_t N2 = 1;
-  while (N2 < N) N2 <<= 1;
-  for (uint32_t e = threadIdx.x; e < N2; e += kMergeThreads) {
-    uint64_t k = 0;  // below every real key
-    if (e < N) {
-      const uint32_t c = e / a.K, i = e - c * a.K;
-      if (i < a.cnt[(size_t)b * a.C + c]) k = a.cand[((size_t)b * a.C + c) * a.K + i];
-    }
-    keys[e] = k;
+  for (int i = 0; i < kRowTiles; ++i)
+    mine += (tid + i * kRowThreads < NT && (key[i] & mask) >= prefix) ? 1u : 0u;
+  uint32_t ntile;
+  uint32_t off = block_excl_scan<kRowThreads>(mine, s_wave, &ntile);
+#pragma unroll
+  for (int i = 0; i < kRowTiles; ++i) {
+    const uint32_t t = tid + i * kRowThreads;
+    if (t < NT && (key[i] & mask) >= prefix) s_tiles[off++] = t;
   }
   __syncthreads();
-  // Bitonic sort, descending.
-  for (uint32_t size = 2; size <= N2; size <<= 1) {
-    for (uint32_t stride = size >> 1; stride > 0; stride >>= 1) {
-      for (uint32_t e = threadIdx.x; e < N2 / 2; e += kMergeThreads) {
-        const uint32_t i = 2 * e - (e & (stride - 1));
-        const uint32_t j = i + stride;
-        const bool desc = (i & size) == 0;
-        const uint64_t x = keys[i], y = keys[j];
-        if ((x < y) == desc) {
-          keys[i] = y;
-          keys[j] = x;
+  // The smallest candidate tile key: every answer logit is at or above it.
+  // (With all tiles taken, every logit is a candidate.)
+  uint64_t floor_key = ~0ull;
+  for (uint32_t e = tid; e < ntile; e += kRowThreads) floor_key = umin64(floor_key, tk[sidx(s_tiles[e])]);
+  for (int d = 32; d >= 1; d >>= 1) floor_key = umin64(floor_key, shfl_xor64(floor_key, d));
+  __syncthreads();
+  if (lane == 0) s_cand[wave] = floor_key;
+  __syncthreads();
+  uint64_t tau = ~0ull;
+  for (int w = 0; w < kRowThreads / 64; ++w) tau = umin64(tau, s_cand[w]);
+  if (take == NT) tau = 0;
+  __syncthreads();
+
+  // 3. Gather the candidate tiles' logits at or above tau, sort, emit.
+  const float* lg = a.logits + (grp * a.tpitch * 64 + c) * 16;  // tile t at lg[1024 t]
+  uint64_t ck = 0;
+  bool keep = false;
+  if ((uint32_t)tid < 16 * ntile) {
+    const uint32_t t = s_tiles[tid >> 4], v = 16 * t + (tid & 15);
+    if (v < a.V) {
+      ck = tkey64(lg[1024 * (size_t)t + (tid & 15)], v);
+      keep = ck >= tau;
+    }
+  }
+  // 16 * ntile <= 16 K <= kRowCand; kRowThreads covers 16 * 64 tiles per
+  // round, so larger K take several rounds.
+  uint32_t n_c = 0;
+  for (uint32_t base = 0; base < 16 * ntile; base += kRowThreads) {
+    if (base > 0) {
+      ck = 0;
+      keep = false;
+      const uint32_t e = base + tid;
+      if (e < 16 * ntile) {
+        const uint32_t t = s_tiles[e >> 4], v = 16 * t + (e & 15);
+        if (v < a.V) {
+          ck = tkey64(lg[1024 * (size_t)t + (e & 15)], v);
+          keep = ck >= tau;
         }
       }
-      __syncthreads();
     }
+    uint32_t cnt;
+    const uint32_t o = block_excl_scan<kRowThreads>(keep ? 1u : 0u, s_wave, &cnt);
+    if (keep) s_cand[n_c + o] = ck;
+    n_c += cnt;
+    __syncthreads();
   }
-  // Log-sum-exp merge of the chunk partials.
-  float M = -INFINITY;
-  for (uint32_t c = 0; c < a.C; ++c) M = fmaxf(M, a.part[((size_t)b * a.C + c) * 2]);
-  float S = 0.f;
-  for (uint32_t c = 0; c < a.C; ++c) {
-    const float mc = a.part[((size_t)b * a.C + c) * 2];
-    const float sc = a.part[((size_t)b * a.C + c) * 2 + 1];
-    if (sc > 0.f) S += sc * expf(mc - M);
-  }
+  const uint32_t N2 = pow2_ceil(max(n_c, 2u));
+  for (uint32_t e = n_c + tid; e < N2; e += kRowThreads) s_cand[e] = 0;
+  __syncthreads();
+  lds_sort_desc<kRowThreads>(s_cand, N2);
   const float invS = 1.0f / S;
-  for (uint32_t i = threadIdx.x; i < a.K; i += kMergeThreads) {
-    const uint64_t k = keys[i];
+  for (uint32_t i = tid; i < a.K; i += kRowThreads) {
+    const uint64_t k = s_cand[i];
     a.top_ids[(size_t)b * a.K + i] = (int32_t)(0xFFFFFFFFu - (uint32_t)k);
     a.top_prob[(size_t)b * a.K + i] = expf(key2f((uint32_t)(k >> 32)) - M) * invS;
   }
 }
 
 }  // namespace
-
-uint32_t head_chunks(uint32_t V) {
-  uint32_t c = (V + 4095) / 4096;
-  return c < 1 ? 1 : (c > (uint32_t)kHeadMaxChunks ? (uint32_t)kHeadMaxChunks : c);
-}
 
 bool head_dim_supported(int D) { return D == 256 || D == 512 || D == 1024; }
 
@@ -316,13 +463,8 @@ hipError_t launch_head_logits(const HeadArgs& a, uint32_t blocks, hipStream_t s)
   return hipGetLastError();
 }
 
-hipError_t launch_head_select(const HeadArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL(k_head_select, dim3(a.C, a.B), dim3(kSelThreads), 0, s, a);
-  return hipGetLastError();
-}
-
-hipError_t launch_head_merge(const HeadArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL(k_head_merge, dim3(a.B), dim3(kMergeThreads), 0, s, a);
+hipError_t launch_head_rows(const HeadArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL(k_head_rows, dim3(a.B), dim3(kRowThreads), 0, s, a);
   return hipGetLastError();
 }
 

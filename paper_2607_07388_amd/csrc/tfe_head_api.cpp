@@ -12,11 +12,13 @@ struct tfe_head {
   int device = 0;
   int cus = 256;
   const void* w = nullptr;   // caller's [V x D] bf16 projection (not owned)
-  uint32_t V = 0, D = 0, max_batch = 0, max_k = 0, C = 1;
-  float* d_logits = nullptr;  // [max_batch x V]
-  uint64_t* d_cand = nullptr; // [max_batch x C x max_k]
-  uint32_t* d_cnt = nullptr;  // [max_batch x C]
-  float* d_part = nullptr;    // [max_batch x C x 2]
+  uint32_t V = 0, D = 0, max_batch = 0, max_k = 0;
+  // Scratch, rows = max_batch rounded up to 64 (the logits kernel writes
+  // whole 64-row groups), tiles = V rounded up to 32 (whole 32-token
+  // super-tiles), over 16.
+  float* d_logits = nullptr;  // [rows x tiles x 16]
+  uint64_t* d_tkey = nullptr; // [rows x tiles rounded up to 16]
+  float* d_tsum = nullptr;    // [rows x tiles rounded up to 16]
 };
 
 namespace tfe {
@@ -38,7 +40,7 @@ void release(tfe_head* h) {
   (void)hipGetDevice(&cur);
   (void)hipSetDevice(h->device);
   (void)hipDeviceSynchronize();
-  void* bufs[] = {h->d_logits, h->d_cand, h->d_cnt, h->d_part};
+  void* bufs[] = {h->d_logits, h->d_tkey, h->d_tsum};
   for (void* b : bufs)
     if (b) (void)hipFree(b);
   (void)hipSetDevice(cur);
@@ -93,12 +95,11 @@ tfe_status create(const void* w, int32_t vocab, int32_t dim, int32_t max_batch, 
     h->D = (uint32_t)dim;
     h->max_batch = (uint32_t)max_batch;
     h->max_k = (uint32_t)max_k;
-    h->C = head_chunks(h->V);
-    const size_t nb = h->max_batch;
-    if (hipMalloc(&h->d_logits, nb * h->V * sizeof(float)) != hipSuccess ||
-        hipMalloc(&h->d_cand, nb * h->C * h->max_k * sizeof(uint64_t)) != hipSuccess ||
-        hipMalloc(&h->d_cnt, nb * h->C * sizeof(uint32_t)) != hipSuccess ||
-        hipMalloc(&h->d_part, nb * h->C * 2 * sizeof(float)) != hipSuccess) {
+    const size_t nb = ((size_t)h->max_batch + 63) / 64 * 64, nt = (h->V + 31) / 32 * 2;
+    const size_t nt16 = (nt + 15) / 16 * 16;
+    if (hipMalloc(&h->d_logits, nb * nt * 16 * sizeof(float)) != hipSuccess ||
+        hipMalloc(&h->d_tkey, nb * nt16 * sizeof(uint64_t)) != hipSuccess ||
+        hipMalloc(&h->d_tsum, nb * nt16 * sizeof(float)) != hipSuccess) {
       (void)hipGetLastError();
       st = fail(TFE_ERR_OOM, "head scratch for %u rows", h->max_batch);
       break;
@@ -130,19 +131,18 @@ tfe_status topk(tfe_head* h, const void* hidden, int32_t B, int32_t K, int32_t* 
   a.w = h->w;
   a.hidden = hidden;
   a.logits = h->d_logits;
-  a.cand = h->d_cand;
-  a.cnt = h->d_cnt;
-  a.part = h->d_part;
+  a.tkey = h->d_tkey;
+  a.tsum = h->d_tsum;
   a.top_ids = ids;
   a.top_prob = prob;
   a.V = h->V;
+  a.tpitch = (h->V + 31) / 32 * 2;
+  a.tblocks = (a.tpitch + 15) / 16;
   a.D = h->D;
   a.B = (uint32_t)B;
   a.K = (uint32_t)K;
-  a.C = h->C;
   HEAD_HIP(launch_head_logits(a, (uint32_t)h->cus, stream), "head logits launch");
-  HEAD_HIP(launch_head_select(a, stream), "head select launch");
-  HEAD_HIP(launch_head_merge(a, stream), "head merge launch");
+  HEAD_HIP(launch_head_rows(a, stream), "head top-K launch");
   return TFE_OK;
 }
 
