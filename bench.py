@@ -459,7 +459,7 @@ def run_head(args):
                    "k": K},
         "roofline": {
             "bound": "hbm",
-            "kernel": "tfe_head_topk (k_head_logits + k_head_select + k_head_merge)",
+            "kernel": "tfe_head_topk (k_head_logits + k_head_rows)",
             "achieved": nbytes / avg / 1e9,
             "peak": HBM_PEAK_GBPS,
             "unit": "GB/s",

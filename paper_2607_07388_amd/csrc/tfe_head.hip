@@ -9,10 +9,11 @@
 //                  (v_mfma_f32_16x16x32_bf16).  W ([V x D] bf16, 311 MB for
 //                  the 151936 x 1024 head) is streamed from HBM exactly once
 //                  per 64 rows; the 64 hidden rows are staged in LDS and read
-//                  by every wave.  One wave computes a 32-token x 64-row
-//                  super-tile (two MFMA row tiles sharing each LDS read of
-//                  h): half of its 32 W rows at a time, D/64 16-byte loads
-//                  per lane and row tile all in flight before the MFMAs.
+//                  by every wave.  One wave computes a 16-token x 64-row
+//                  tile: W is read 128 contiguous bytes per row and load
+//                  instruction (half a row, D/32 16-byte loads per lane, in
+//                  flight together), then passed through a small per-wave
+//                  LDS staging tile into the MFMA operand layout.
 //                  The epilogue writes the fp32 logits and, per (row,
 //                  16-token tile), the largest (logit, id) key and the sum of
 //                  exp(logit - tile max).
@@ -40,7 +41,7 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 #define TFE_HEAD_WAVES 8
 #endif
 #ifndef TFE_HEAD_NT
-#define TFE_HEAD_NT 0
+#define TFE_HEAD_NT 1
 #endif
 
 constexpr int kLogitWaves = TFE_HEAD_WAVES;  // waves per logits block (tuning knob)
@@ -134,9 +135,12 @@ __device__ __forceinline__ void tile_epilogue(const HeadArgs& a, uint32_t t, int
 template <int KS>  // KS = D / 32 k-steps
 __global__ __launch_bounds__(kLogitWaves * 64) void k_head_logits(const HeadArgs a) {
   constexpr int D = KS * 32;
-  constexpr int STRIDE = D + 8;  // staged row pitch (elements): conflict-free b128 reads
-  constexpr int HALF = KS / 2;
+  constexpr int STRIDE = D + 8;  // staged hidden row pitch (elements): conflict-free b128 reads
+  constexpr int NCH = D / 64;    // 64-element chunks per W row
+  constexpr int HC = NCH / 2;    // chunks per half row
+  constexpr int SP = 72;         // W staging row pitch (elements): conflict-free b128 reads
   __shared__ __attribute__((aligned(16))) __bf16 hs[kCols * STRIDE];
+  __shared__ __attribute__((aligned(16))) __bf16 stage[kLogitWaves][16 * SP];
   __shared__ uint32_t s_next;
   const uint32_t col0 = blockIdx.y * kCols;
   const int ncols = (int)min((uint32_t)kCols, a.B - col0);
@@ -146,77 +150,76 @@ __global__ __launch_bounds__(kLogitWaves * 64) void k_head_logits(const HeadArgs
     if (j < ncols) v = *((const u32x4*)a.hidden + ((size_t)(col0 + j) * D) / 8 + c);
     *(u32x4*)(hs + j * STRIDE + c * 8) = v;
   }
-  // The block owns a contiguous range of 32-token super-tiles; its waves
-  // claim them one at a time, so every wave stays busy until the range is
-  // done (the block's share of W is fixed; only the split among its waves
-  // is dynamic).
-  const uint32_t nst = (a.V + 31) >> 5;
-  const uint32_t st_lo = (uint32_t)((uint64_t)nst * blockIdx.x / gridDim.x);
-  const uint32_t st_hi = (uint32_t)((uint64_t)nst * (blockIdx.x + 1) / gridDim.x);
-  if (threadIdx.x == 0) s_next = st_lo;
+  // The block owns a contiguous range of 16-token tiles; its waves claim
+  // them one at a time, so every wave stays busy until the range is done.
+  const uint32_t nt = (a.V + 15) >> 4;
+  const uint32_t t_lo = (uint32_t)((uint64_t)nt * blockIdx.x / gridDim.x);
+  const uint32_t t_hi = (uint32_t)((uint64_t)nt * (blockIdx.x + 1) / gridDim.x);
+  if (threadIdx.x == 0) s_next = t_lo;
   __syncthreads();
-  const int lane = threadIdx.x & 63;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int r = lane & 15, g = lane >> 4;
+  __bf16* st = stage[wave];
   // The staged hidden rows do not change across tiles; hiding the offset
   // from the optimiser keeps their LDS reads inside the loop (hoisted, the
   // whole 128 KB B operand would be held in registers and spill).
   int hoff = r * STRIDE + 8 * g;
   for (;;) {
-    uint32_t st = 0;
-    if (lane == 0) st = atomicAdd(&s_next, 1u);
-    st = __builtin_amdgcn_readfirstlane(st);
-    if (st >= st_hi) break;
+    uint32_t t = 0;
+    if (lane == 0) t = atomicAdd(&s_next, 1u);
+    t = __builtin_amdgcn_readfirstlane(t);
+    if (t >= t_hi) break;
     asm volatile("" : "+v"(hoff));
-    // A operands: tile u (u = 0, 1) holds W rows 32 st + 16 u + r (clamped
-    // past the vocabulary), k = 32 s + 8 g.  Each half of the rows is
-    // loaded whole (2 x 16 loads in flight per wave) before its MFMAs; each
-    // LDS read of the hidden rows feeds both tiles.
-    const u32x4* wp0 = (const u32x4*)a.w + ((size_t)min(st * 32 + r, a.V - 1) * D) / 8 + g;
-    const u32x4* wp1 = (const u32x4*)a.w + ((size_t)min(st * 32 + 16 + r, a.V - 1) * D) / 8 + g;
-    f32x4 acc0[4], acc1[4];
+    // W rows are read 128 contiguous bytes per row and instruction (8 lanes
+    // x 16 B, 8 rows): lane l holds row (l >> 3) (E) or 8 + (l >> 3) (O),
+    // elements 64 c + 8 (l & 7) .. + 8 of chunk c.  The MFMA wants lane
+    // (g, i) to hold row i, so each chunk passes through a per-wave LDS
+    // staging tile (16 rows x 64 elements) and is read back in MFMA layout:
+    // step x of the chunk takes elements 64 c + 32 x + 8 g .. + 8.
+    const u32x4* wE = (const u32x4*)a.w + ((size_t)min(t * 16 + (lane >> 3), a.V - 1) * D) / 8 +
+                      (lane & 7);
+    const u32x4* wO =
+        (const u32x4*)a.w + ((size_t)min(t * 16 + 8 + (lane >> 3), a.V - 1) * D) / 8 + (lane & 7);
+    f32x4 acc[4];
 #pragma unroll
-    for (int bt = 0; bt < 4; ++bt) {
-      acc0[bt] = f32x4{0.f, 0.f, 0.f, 0.f};
-      acc1[bt] = f32x4{0.f, 0.f, 0.f, 0.f};
-    }
+    for (int bt = 0; bt < 4; ++bt) acc[bt] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
-      u32x4 av0[HALF], av1[HALF];
+      u32x4 ev[HC], ov[HC];
 #pragma unroll
-      for (int s = 0; s < HALF; ++s) {
+      for (int cc = 0; cc < HC; ++cc) {
 #if TFE_HEAD_NT
-        av0[s] = __builtin_nontemporal_load(wp0 + 4 * (h * HALF + s));
-        av1[s] = __builtin_nontemporal_load(wp1 + 4 * (h * HALF + s));
+        ev[cc] = __builtin_nontemporal_load(wE + 8 * (h * HC + cc));
+        ov[cc] = __builtin_nontemporal_load(wO + 8 * (h * HC + cc));
 #else
-        av0[s] = wp0[4 * (h * HALF + s)];
-        av1[s] = wp1[4 * (h * HALF + s)];
+        ev[cc] = wE[8 * (h * HC + cc)];
+        ov[cc] = wO[8 * (h * HC + cc)];
 #endif
       }
       // Keep the half's loads together ahead of its MFMAs (left alone, the
       // scheduler interleaves them and keeps only a few in flight).
       __builtin_amdgcn_sched_barrier(0);
-      // All four column tiles are computed even when fewer rows are live
-      // (the staged rows past B are zero): a branch per tile would
-      // serialise every MFMA behind its own LDS read.
 #pragma unroll
-      for (int s = 0; s < HALF; ++s) {
-        u32x4 bv[4];
+      for (int cc = 0; cc < HC; ++cc) {
+        const int c = h * HC + cc;
+        *(u32x4*)(st + (lane >> 3) * SP + (lane & 7) * 8) = ev[cc];
+        *(u32x4*)(st + (8 + (lane >> 3)) * SP + (lane & 7) * 8) = ov[cc];
 #pragma unroll
-        for (int bt = 0; bt < 4; ++bt)
-          bv[bt] = *(const u32x4*)(hs + hoff + bt * 16 * STRIDE + 32 * (h * HALF + s));
+        for (int x = 0; x < 2; ++x) {
+          const u32x4 av = *(const u32x4*)(st + r * SP + (4 * x + g) * 8);
+          u32x4 bv[4];
 #pragma unroll
-        for (int bt = 0; bt < 4; ++bt) {
-          acc0[bt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, av0[s]),
-                                                             __builtin_bit_cast(bf16x8, bv[bt]),
-                                                             acc0[bt], 0, 0, 0);
-          acc1[bt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, av1[s]),
-                                                             __builtin_bit_cast(bf16x8, bv[bt]),
-                                                             acc1[bt], 0, 0, 0);
+          for (int bt = 0; bt < 4; ++bt)
+            bv[bt] = *(const u32x4*)(hs + hoff + bt * 16 * STRIDE + 64 * c + 32 * x);
+#pragma unroll
+          for (int bt = 0; bt < 4; ++bt)
+            acc[bt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, av),
+                                                              __builtin_bit_cast(bf16x8, bv[bt]),
+                                                              acc[bt], 0, 0, 0);
         }
       }
     }
-    tile_epilogue(a, 2 * st, r, g, acc0);
-    tile_epilogue(a, 2 * st + 1, r, g, acc1);
+    tile_epilogue(a, t, r, g, acc);
   }
 }
 
@@ -450,7 +453,9 @@ __global__ __launch_bounds__(kRowThreads) void k_head_rows(const HeadArgs a) {
 
 bool head_dim_supported(int D) { return D == 256 || D == 512 || D == 1024; }
 
-uint32_t head_lds_bytes(int D) { return (uint32_t)(kCols * (D + 8) * 2); }
+uint32_t head_lds_bytes(int D) {
+  return (uint32_t)(kCols * (D + 8) * 2 + kLogitWaves * 16 * 72 * 2 + 4);
+}
 
 hipError_t launch_head_logits(const HeadArgs& a, uint32_t blocks, hipStream_t s) {
   const dim3 grid(blocks, (a.B + kCols - 1) / kCols);
