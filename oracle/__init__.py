@@ -4,7 +4,8 @@ TEST INFRASTRUCTURE ONLY: the tests, the smoke check and the benchmark's
 CPU-baseline leg may import this package; the product path never does.  The
 arithmetic lives in ``oracle.cpp`` (std::map on token tuples, scalar double
 loops); this file only marshals numpy arrays.  ``head.cpp`` is the
-early-exit prefetch head; ``lru.py`` is the reference model of the HBM cache
+early-exit prefetch head, ``ngram.cpp`` the frequency-ranked phrase-table
+construction; ``lru.py`` is the reference model of the HBM cache
 tier's replacement policy.
 """
 import ctypes
@@ -44,6 +45,8 @@ def lib():
         L.oracle_gate.argtypes = [vp, vp, i64, ctypes.c_int, ctypes.c_int, ctypes.c_double]
         L.oracle_gate.restype = ctypes.c_double
         L.oracle_head_topk.argtypes = [vp, vp, i64, i64, i64, i64, ctypes.c_int, vp, vp, vp]
+        L.oracle_ngram_top.argtypes = [vp, i64, ctypes.c_int, ctypes.c_int, i64, i64, vp, vp]
+        L.oracle_ngram_top.restype = i64
         L.oracle_round_bf16.argtypes = [ctypes.c_double]
         L.oracle_round_bf16.restype = ctypes.c_uint16
         _lib = L
@@ -169,6 +172,19 @@ def head_topk(w, h, K, dtype, with_logits=False):
     if st != OK:
         raise OracleError(st)
     return (ids, probs, logits) if with_logits else (ids, probs)
+
+
+def ngram_top(tokens, vocab, n, skip, top):
+    """Offline table construction by frequency: the distinct n-grams of the
+    stream ranked by count (ties: tuple ascending); ranks [skip, skip + top)
+    -> (tuples int32 [m x n], counts int64 [m])."""
+    tokens = np.ascontiguousarray(tokens, np.int32)
+    tup = np.empty((max(top, 0), n), np.int32)
+    cnt = np.empty(max(top, 0), np.int64)
+    m = lib().oracle_ngram_top(_p(tokens), tokens.size, vocab, n, skip, top, _p(tup), _p(cnt))
+    if m < 0:
+        raise OracleError(int(m))
+    return tup[:m], cnt[:m]
 
 
 def round_bf16(x):

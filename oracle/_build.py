@@ -8,7 +8,8 @@ SO = os.path.join(HERE, "liboracle.so")
 
 def build():
     cmd = ["g++", "-O2", "-fPIC", "-shared", "-std=c++17", "-Wall", "-o", SO + ".tmp",
-           os.path.join(HERE, "oracle.cpp"), os.path.join(HERE, "head.cpp")]
+           os.path.join(HERE, "oracle.cpp"), os.path.join(HERE, "head.cpp"),
+           os.path.join(HERE, "ngram.cpp")]
     r = subprocess.run(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True)
     if r.returncode != 0:
         raise RuntimeError("oracle build failed:\n" + r.stdout)
