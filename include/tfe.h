@@ -231,6 +231,28 @@ tfe_status tfe_head_topk(tfe_head *head, const void *hidden, int32_t B, int32_t 
 /* Releases a head (waits for the device first).  NULL is accepted. */
 tfe_status tfe_head_free(tfe_head *head);
 
+/* ---- Offline phrase-table construction -----------------------------------
+ * Paper: Sec. 4.2 (candidate phrases mined from a corpus and selected by
+ * frequency; n-gram extraction is the dominant construction cost reported in
+ * the evaluation).
+ * Counts the distinct n-grams of a token stream and returns the most
+ * frequent ones: every window tokens[i .. i+n-1] whose tokens all lie in
+ * [0, vocab) is one occurrence of its tuple (tokens outside the range, e.g.
+ * -1 document separators, break windows); distinct tuples are ranked by
+ * count, most frequent first, equal counts by the tuple in lexicographic
+ * order (oldest token first); ranks [skip, skip + top) are written.
+ *   tokens      DEVICE int32 [n_tokens], n_tokens <= 2^28
+ *   vocab       1 <= vocab <= 2^18;  n: 1 <= n <= 3
+ *   out_tuples  DEVICE int32 [top x n], oldest token first
+ *   out_counts  DEVICE int64 [top]
+ *   written     HOST: number of ranks written (fewer than top when the
+ *               stream has fewer than skip + top distinct tuples)
+ * Synchronous: returns once the outputs are complete.  Allocates its
+ * scratch (about 20 bytes per token) for the duration of the call. */
+tfe_status tfe_ngram_top(const int32_t *tokens, int64_t n_tokens, int32_t vocab, int32_t n,
+                         int64_t skip, int64_t top, int32_t *out_tuples, int64_t *out_counts,
+                         int64_t *written, void *stream);
+
 /* Copies the table's counters (synchronises with the table's pending work). */
 tfe_status tfe_get_stats(tfe_table *table, tfe_stats *out);
 

@@ -1,0 +1,527 @@
+// Offline phrase-table construction on the GPU: the most frequent distinct
+// n-grams of a token stream (Sec. 4.2: candidate phrases selected by corpus
+// frequency; n-gram extraction dominates the construction time reported in
+// the evaluation).
+//
+// Steps, all on the device:
+//   1. key formation: every window of n tokens that are all in [0, vocab)
+//      becomes one 64-bit key, the tokens in 18-bit fields, oldest in the
+//      highest field, so that key order is tuple order (blocks compact their
+//      valid windows and append them through one atomic offset each);
+//   2. LSD radix sort of the keys, 8-bit digits over the 18 n key bits: per
+//      pass a digit histogram per 4096-key tile, one exclusive scan of the
+//      digit-major histogram, and a stable scatter (each wave ranks its keys
+//      with ballot-based digit matching, the tile is reordered in LDS and
+//      written out in digit runs);
+//   3. run-length count: run starts flagged and scanned into a unique-key
+//      array; a run's count is the distance to the next start;
+//   4. selection of ranks [0, skip + top): radix select of the (skip+top)-th
+//      largest count c*, then an order-preserving compaction of the runs
+//      with count > c* and the first needed ones with count == c* (key order
+//      = tuple order, which breaks the ties);
+//   5. ranking: a stable radix sort of the selected runs by descending count
+//      (payload: the key), which keeps tuple order among equal counts;
+//   6. ranks [skip, skip + top) are unpacked into tuples and counts.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <algorithm>
+#include <vector>
+
+#include "../../include/tfe.h"
+#include "tfe_internal.h"
+
+namespace tfe {
+namespace {
+
+constexpr int kTileThreads = 256;
+constexpr int kTileItems = 16;
+constexpr int kTile = kTileThreads * kTileItems;  // keys per radix tile
+constexpr int kWaves = kTileThreads / 64;
+constexpr int kScanThreads = 1024;
+constexpr int kScanItems = 16;
+constexpr int kScanBlock = kScanThreads * kScanItems;
+
+// ---- 1. keys -----------------------------------------------------------------
+
+__global__ __launch_bounds__(256) void k_ng_keys(const int32_t* tok, uint64_t nwin, int n,
+                                                 int32_t vocab, uint64_t* keys,
+                                                 unsigned long long* count) {
+  __shared__ uint32_t s_wave[4];
+  __shared__ unsigned long long s_base;
+  const uint64_t i = (uint64_t)blockIdx.x * 256 + threadIdx.x;
+  uint64_t key = 0;
+  bool ok = i < nwin;
+  if (ok) {
+    for (int j = 0; j < n; ++j) {
+      const int32_t t = tok[i + j];
+      ok = ok && t >= 0 && t < vocab;
+      key = (key << 18) | (uint64_t)(uint32_t)(t & 0x3FFFF);
+    }
+  }
+  const uint64_t bal = __builtin_amdgcn_ballot_w64(ok);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const uint32_t below = __builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32),
+                                                   __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0));
+  if (lane == 0) s_wave[wave] = (uint32_t)__builtin_popcountll(bal);
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const uint32_t tot = s_wave[0] + s_wave[1] + s_wave[2] + s_wave[3];
+    s_base = tot ? atomicAdd(count, (unsigned long long)tot) : 0ull;
+  }
+  __syncthreads();
+  uint32_t off = 0;
+  for (int w = 0; w < wave; ++w) off += s_wave[w];
+  if (ok) keys[s_base + off + below] = key;
+}
+
+// ---- device-wide exclusive scan of uint32 (totals below 2^32) ----------------
+
+template <int NT>
+__device__ uint32_t block_scan_excl(uint32_t v, uint32_t* s_wave, uint32_t* total) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  uint32_t x = v;
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    const uint32_t y = __shfl_up(x, d, 64);
+    if (lane >= d) x += y;
+  }
+  if (lane == 63) s_wave[wave] = x;
+  __syncthreads();
+  uint32_t off = 0, tot = 0;
+#pragma unroll
+  for (int w = 0; w < NT / 64; ++w) {
+    off += w < wave ? s_wave[w] : 0u;
+    tot += s_wave[w];
+  }
+  __syncthreads();
+  *total = tot;
+  return x - v + off;
+}
+
+// Pass 1: per-block sums.
+__global__ __launch_bounds__(kScanThreads) void k_scan_reduce(const uint32_t* in, uint64_t n,
+                                                              uint32_t* part) {
+  __shared__ uint32_t s_wave[kScanThreads / 64];
+  const uint64_t base = (uint64_t)blockIdx.x * kScanBlock;
+  uint32_t s = 0;
+  for (int k = 0; k < kScanItems; ++k) {
+    const uint64_t i = base + (uint64_t)k * kScanThreads + threadIdx.x;
+    if (i < n) s += in[i];
+  }
+  uint32_t tot;
+  (void)block_scan_excl<kScanThreads>(s, s_wave, &tot);
+  if (threadIdx.x == 0) part[blockIdx.x] = tot;
+}
+
+// Pass 2: exclusive scan of the block sums in one block (nb <= kScanBlock).
+__global__ __launch_bounds__(kScanThreads) void k_scan_partials(uint32_t* part, uint32_t nb,
+                                                                uint32_t* total) {
+  __shared__ uint32_t s_wave[kScanThreads / 64];
+  uint32_t v[kScanItems];
+  uint32_t s = 0;
+  for (int k = 0; k < kScanItems; ++k) {
+    const uint32_t i = threadIdx.x * kScanItems + k;
+    v[k] = i < nb ? part[i] : 0u;
+    s += v[k];
+  }
+  uint32_t tot;
+  uint32_t run = block_scan_excl<kScanThreads>(s, s_wave, &tot);
+  for (int k = 0; k < kScanItems; ++k) {
+    const uint32_t i = threadIdx.x * kScanItems + k;
+    if (i < nb) part[i] = run;
+    run += v[k];
+  }
+  if (threadIdx.x == 0 && total) *total = tot;
+}
+
+// Pass 3: scan within blocks plus the block offset.
+__global__ __launch_bounds__(kScanThreads) void k_scan_down(const uint32_t* in, uint64_t n,
+                                                            const uint32_t* part, uint32_t* out) {
+  __shared__ uint32_t s_wave[kScanThreads / 64];
+  const uint64_t base = (uint64_t)blockIdx.x * kScanBlock;
+  uint32_t run = part[blockIdx.x];
+  for (int k = 0; k < kScanItems; ++k) {
+    const uint64_t i = base + (uint64_t)k * kScanThreads + threadIdx.x;
+    const uint32_t v = i < n ? in[i] : 0u;
+    uint32_t tot;
+    const uint32_t ex = block_scan_excl<kScanThreads>(v, s_wave, &tot);
+    if (i < n) out[i] = run + ex;
+    run += tot;
+  }
+}
+
+// ---- 2. stable LSD radix sort (8-bit digits) --------------------------------
+
+template <class K>
+__device__ __forceinline__ uint32_t digit_of(K k, int shift) {
+  return (uint32_t)(k >> shift) & 255u;
+}
+
+template <class K>
+__global__ __launch_bounds__(kTileThreads) void k_rs_hist(const K* keys, uint64_t n, int shift,
+                                                          uint32_t* hist, uint32_t ntiles) {
+  __shared__ uint32_t h[256];
+  h[threadIdx.x] = 0u;
+  __syncthreads();
+  const uint64_t base = (uint64_t)blockIdx.x * kTile;
+  for (int k = 0; k < kTileItems; ++k) {
+    const uint64_t i = base + (uint64_t)k * kTileThreads + threadIdx.x;
+    if (i < n) atomicAdd(&h[digit_of(keys[i], shift)], 1u);
+  }
+  __syncthreads();
+  hist[(size_t)threadIdx.x * ntiles + blockIdx.x] = h[threadIdx.x];
+}
+
+// Lanes of the wave whose 8-bit digit equals this lane's (active lanes only).
+__device__ __forceinline__ uint64_t match_digit(uint32_t d, bool active) {
+  uint64_t m = __builtin_amdgcn_ballot_w64(active);
+#pragma unroll
+  for (int b = 0; b < 8; ++b) {
+    const uint64_t bb = __builtin_amdgcn_ballot_w64(active && ((d >> b) & 1u));
+    m &= ((d >> b) & 1u) ? bb : ~bb;
+  }
+  return m;
+}
+
+// Scatter of one tile.  Wave w ranks the keys [w 1024, (w+1) 1024) of the
+// tile in 16 rounds of 64 consecutive keys: the rank of a key among the
+// wave's earlier keys of its digit is the wave's running count plus the
+// matching lanes below it; the first lane of each digit group advances the
+// count.  Tile positions follow (digit, wave, rank), i.e. the stable order.
+template <class K, bool PAIRS>
+__global__ __launch_bounds__(kTileThreads) void k_rs_scatter(const K* keys, const uint64_t* vals,
+                                                             uint64_t n, int shift,
+                                                             const uint32_t* offs,
+                                                             uint32_t ntiles, K* keys_out,
+                                                             uint64_t* vals_out) {
+  __shared__ uint32_t wcnt[kWaves][256];
+  __shared__ uint32_t s_loc[256];  // tile-local start of each digit
+  __shared__ uint32_t s_glob[256]; // global start of each digit's run of this tile
+  __shared__ uint32_t s_wave[kWaves];
+  __shared__ K s_keys[kTile];
+  __shared__ uint64_t s_vals[PAIRS ? kTile : 1];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  for (int e = threadIdx.x; e < kWaves * 256; e += kTileThreads) (&wcnt[0][0])[e] = 0u;
+  __syncthreads();
+  const uint64_t base = (uint64_t)blockIdx.x * kTile + (uint64_t)wave * (64 * kTileItems);
+  const uint64_t lt = (1ull << lane) - 1ull;
+  K kk[kTileItems];
+  uint64_t vv[PAIRS ? kTileItems : 1];
+  uint32_t rank[kTileItems];
+#pragma unroll
+  for (int r = 0; r < kTileItems; ++r) {
+    const uint64_t i = base + (uint64_t)r * 64 + lane;
+    const bool act = i < n;
+    kk[r] = act ? keys[i] : (K)0;
+    if (PAIRS) vv[PAIRS ? r : 0] = act ? vals[i] : 0ull;
+    const uint32_t d = digit_of(kk[r], shift);
+    const uint64_t m = match_digit(d, act);
+    const uint32_t before = wcnt[wave][d];
+    rank[r] = before + (uint32_t)__builtin_popcountll(m & lt);
+    // The lowest matching lane advances the wave's count of this digit.
+    if (act && (m & lt) == 0) wcnt[wave][d] = before + (uint32_t)__builtin_popcountll(m);
+  }
+  __syncthreads();
+  // Per digit: counts of earlier waves, the tile's digit starts.
+  const uint32_t d = threadIdx.x;
+  uint32_t tot = 0;
+  for (int w = 0; w < kWaves; ++w) {
+    const uint32_t c = wcnt[w][d];
+    wcnt[w][d] = tot;  // becomes the offset of wave w within the digit
+    tot += c;
+  }
+  uint32_t all;
+  const uint32_t loc = block_scan_excl<kTileThreads>(tot, s_wave, &all);
+  s_loc[d] = loc;
+  s_glob[d] = offs[(size_t)d * ntiles + blockIdx.x];
+  __syncthreads();
+#pragma unroll
+  for (int r = 0; r < kTileItems; ++r) {
+    const uint64_t i = base + (uint64_t)r * 64 + lane;
+    if (i < n) {
+      const uint32_t dd = digit_of(kk[r], shift);
+      const uint32_t pos = s_loc[dd] + wcnt[wave][dd] + rank[r];
+      s_keys[pos] = kk[r];
+      if (PAIRS) s_vals[PAIRS ? pos : 0] = vv[PAIRS ? r : 0];
+    }
+  }
+  __syncthreads();
+  const uint64_t tile0 = (uint64_t)blockIdx.x * kTile;
+  const uint32_t cnt = (uint32_t)min((uint64_t)kTile, n - tile0);
+  for (uint32_t p = threadIdx.x; p < cnt; p += kTileThreads) {
+    const K k = s_keys[p];
+    const uint32_t dd = digit_of(k, shift);
+    const uint64_t dst = (uint64_t)s_glob[dd] + (p - s_loc[dd]);
+    keys_out[dst] = k;
+    if (PAIRS) vals_out[dst] = s_vals[PAIRS ? p : 0];
+  }
+}
+
+// ---- 3. run-length count ----------------------------------------------------
+
+__global__ __launch_bounds__(256) void k_run_flags(const uint64_t* keys, uint64_t n,
+                                                   uint32_t* flag) {
+  const uint64_t i = (uint64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i < n) flag[i] = (i == 0 || keys[i] != keys[i - 1]) ? 1u : 0u;
+}
+
+__global__ __launch_bounds__(256) void k_run_starts(const uint64_t* keys, uint64_t n,
+                                                    const uint32_t* flag, const uint32_t* idx,
+                                                    uint64_t* ukey, uint32_t* ustart) {
+  const uint64_t i = (uint64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i < n && flag[i]) {
+    ukey[idx[i]] = keys[i];
+    ustart[idx[i]] = (uint32_t)i;
+  }
+}
+
+__global__ __launch_bounds__(256) void k_run_counts(const uint32_t* ustart, uint32_t u,
+                                                    uint32_t n, uint32_t* ucount) {
+  const uint32_t i = blockIdx.x * 256 + threadIdx.x;
+  if (i < u) ucount[i] = (i + 1 < u ? ustart[i + 1] : n) - ustart[i];
+}
+
+// ---- 4. selection -----------------------------------------------------------
+
+// Histogram of digit `shift` of the counts whose higher digits equal
+// `prefix` (under `mask`): one pass of a radix select on a 32-bit value.
+__global__ __launch_bounds__(256) void k_sel_hist(const uint32_t* cnt, uint32_t u,
+                                                  const uint32_t* state, int shift,
+                                                  uint32_t* hist) {
+  __shared__ uint32_t h[256];
+  h[threadIdx.x] = 0u;
+  __syncthreads();
+  const uint32_t prefix = state[0], mask = state[1];
+  for (uint32_t i = blockIdx.x * 256 + threadIdx.x; i < u; i += gridDim.x * 256) {
+    const uint32_t c = cnt[i];
+    if ((c & mask) == prefix) atomicAdd(&h[(c >> shift) & 255u], 1u);
+  }
+  __syncthreads();
+  if (h[threadIdx.x]) atomicAdd(&hist[threadIdx.x], h[threadIdx.x]);
+}
+
+// One block: pick the digit bin holding the need-th largest, update the
+// state {prefix, mask, need, above} and clear the histogram.
+__global__ __launch_bounds__(256) void k_sel_pick(uint32_t* hist, uint32_t* state, int shift) {
+  __shared__ uint32_t s_wave[4];
+  const uint32_t t = threadIdx.x;
+  // Every thread reads the state before the scan's barriers, so the one
+  // update below cannot be seen by a late reader.
+  const uint32_t need = state[2];
+  const uint32_t v = hist[255 - t];  // thread t looks at bin 255 - t
+  uint32_t tot;
+  const uint32_t ex = block_scan_excl<256>(v, s_wave, &tot);
+  if (ex < need && need <= ex + v) {
+    state[0] |= (255u - t) << shift;
+    state[1] |= 255u << shift;
+    state[2] = need - ex;
+    state[3] += ex;
+  }
+  hist[255 - t] = 0u;
+}
+
+// keep[i]: count > c*, or count == c* and among the first `need` such runs.
+__global__ __launch_bounds__(256) void k_sel_eq(const uint32_t* cnt, uint32_t u,
+                                                const uint32_t* state, uint32_t* eq) {
+  const uint32_t i = blockIdx.x * 256 + threadIdx.x;
+  if (i < u) eq[i] = cnt[i] == state[0] ? 1u : 0u;
+}
+
+__global__ __launch_bounds__(256) void k_sel_keep(const uint32_t* cnt, uint32_t u,
+                                                  const uint32_t* state, const uint32_t* eqrank,
+                                                  uint32_t* keep) {
+  const uint32_t i = blockIdx.x * 256 + threadIdx.x;
+  if (i < u) {
+    const uint32_t c = cnt[i], cstar = state[0];
+    keep[i] = (c > cstar || (c == cstar && eqrank[i] < state[2])) ? 1u : 0u;
+  }
+}
+
+__global__ __launch_bounds__(256) void k_sel_compact(const uint64_t* ukey, const uint32_t* cnt,
+                                                     uint32_t u, const uint32_t* keep,
+                                                     const uint32_t* pos, uint32_t* rkey,
+                                                     uint64_t* rval) {
+  const uint32_t i = blockIdx.x * 256 + threadIdx.x;
+  if (i < u && keep[i]) {
+    rkey[pos[i]] = ~cnt[i];  // ascending ~count = descending count
+    rval[pos[i]] = ukey[i];
+  }
+}
+
+// ---- 6. output ----------------------------------------------------------------
+
+__global__ __launch_bounds__(256) void k_unpack(const uint32_t* rkey, const uint64_t* rval,
+                                                uint64_t skip, uint64_t m, int n,
+                                                int32_t* tuples, int64_t* counts) {
+  const uint64_t i = (uint64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i < m) {
+    const uint64_t k = rval[skip + i];
+    for (int j = 0; j < n; ++j)
+      tuples[i * n + j] = (int32_t)((k >> (18 * (n - 1 - j))) & 0x3FFFFu);
+    counts[i] = (int64_t)(uint32_t)~rkey[skip + i];
+  }
+}
+
+uint32_t blocks_for(uint64_t n, uint64_t per) { return (uint32_t)((n + per - 1) / per); }
+
+// Exclusive scan of n uint32 values (in may equal out); total to *total (device).
+hipError_t scan_u32(const uint32_t* in, uint32_t* out, uint64_t n, uint32_t* part,
+                    uint32_t* total, hipStream_t s) {
+  const uint32_t nb = blocks_for(n, kScanBlock);
+  if (nb == 0) return hipSuccess;
+  hipLaunchKernelGGL(k_scan_reduce, dim3(nb), dim3(kScanThreads), 0, s, in, n, part);
+  hipLaunchKernelGGL(k_scan_partials, dim3(1), dim3(kScanThreads), 0, s, part, nb, total);
+  hipLaunchKernelGGL(k_scan_down, dim3(nb), dim3(kScanThreads), 0, s, in, n, part, out);
+  return hipGetLastError();
+}
+
+template <class K, bool PAIRS>
+hipError_t radix_sort(K*& keys, K*& keys_alt, uint64_t*& vals, uint64_t*& vals_alt, uint64_t n,
+                      int bits, uint32_t* hist, uint32_t* part, hipStream_t s) {
+  const uint32_t ntiles = blocks_for(n, kTile);
+  if (ntiles == 0) return hipSuccess;
+  for (int shift = 0; shift < bits; shift += 8) {
+    hipLaunchKernelGGL((k_rs_hist<K>), dim3(ntiles), dim3(kTileThreads), 0, s, keys, n, shift,
+                       hist, ntiles);
+    hipError_t e = scan_u32(hist, hist, (uint64_t)256 * ntiles, part, nullptr, s);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((k_rs_scatter<K, PAIRS>), dim3(ntiles), dim3(kTileThreads), 0, s, keys,
+                       vals, n, shift, hist, ntiles, keys_alt, vals_alt);
+    std::swap(keys, keys_alt);
+    if (PAIRS) std::swap(vals, vals_alt);
+  }
+  return hipGetLastError();
+}
+
+struct Scratch {
+  std::vector<void*> bufs;
+  ~Scratch() {
+    for (void* p : bufs) (void)hipFree(p);
+  }
+  template <class T>
+  T* get(uint64_t count) {
+    void* p = nullptr;
+    if (hipMalloc(&p, std::max<uint64_t>(count, 1) * sizeof(T)) != hipSuccess) return nullptr;
+    bufs.push_back(p);
+    return (T*)p;
+  }
+};
+
+#define BUILD_HIP(call, what)                                                        \
+  do {                                                                               \
+    hipError_t e_ = (call);                                                          \
+    if (e_ != hipSuccess) return fail(TFE_ERR_HIP, "%s: %s", what, hipGetErrorString(e_)); \
+  } while (0)
+
+tfe_status ngram_top(const int32_t* tokens, int64_t N, int32_t vocab, int32_t n, int64_t skip,
+                     int64_t top, int32_t* out_tuples, int64_t* out_counts, int64_t* written,
+                     hipStream_t s) {
+  if (!written) return fail(TFE_ERR_INVALID_ARG, "null written");
+  *written = 0;
+  // The two-level scans cover up to 2^28 elements.
+  if (N < 0 || N > (1ll << 28)) return fail(TFE_ERR_INVALID_ARG, "N outside [0, 2^28]");
+  if (vocab < 1 || vocab > (1 << 18)) return fail(TFE_ERR_INVALID_ARG, "vocab outside [1, 2^18]");
+  if (n < 1 || n > 3) return fail(TFE_ERR_UNSUPPORTED, "n = %d (1..3 supported)", n);
+  if (skip < 0 || top < 0) return fail(TFE_ERR_INVALID_ARG, "negative skip or top");
+  if (N < n || top == 0) return TFE_OK;
+  if (!tokens || !out_tuples || !out_counts)
+    return fail(TFE_ERR_INVALID_ARG, "null tokens or outputs");
+  const uint64_t nwin = (uint64_t)(N - n + 1);
+  Scratch sc;
+  uint64_t* keys = sc.get<uint64_t>(nwin);
+  uint64_t* keys_alt = sc.get<uint64_t>(nwin);
+  const uint32_t ntiles = blocks_for(nwin, kTile);
+  uint32_t* hist = sc.get<uint32_t>((uint64_t)256 * ntiles);
+  uint32_t* part = sc.get<uint32_t>(kScanBlock);
+  unsigned long long* d_count = sc.get<unsigned long long>(1);
+  uint32_t* d_small = sc.get<uint32_t>(8);
+  if (!keys || !keys_alt || !hist || !part || !d_count || !d_small)
+    return fail(TFE_ERR_OOM, "n-gram scratch for %llu windows", (unsigned long long)nwin);
+  // 1. keys of the valid windows.
+  BUILD_HIP(hipMemsetAsync(d_count, 0, sizeof(unsigned long long), s), "memset");
+  hipLaunchKernelGGL(k_ng_keys, dim3(blocks_for(nwin, 256)), dim3(256), 0, s, tokens, nwin, n,
+                     vocab, keys, d_count);
+  BUILD_HIP(hipGetLastError(), "keys launch");
+  unsigned long long m_host = 0;
+  BUILD_HIP(hipMemcpyAsync(&m_host, d_count, sizeof m_host, hipMemcpyDeviceToHost, s), "copy");
+  BUILD_HIP(hipStreamSynchronize(s), "sync");
+  const uint64_t M = m_host;
+  if (M == 0) return TFE_OK;
+  // 2. sort.
+  uint64_t* no_vals = nullptr;
+  uint64_t* no_vals2 = nullptr;
+  BUILD_HIP((radix_sort<uint64_t, false>(keys, keys_alt, no_vals, no_vals2, M, 18 * n, hist,
+                                         part, s)),
+            "key sort");
+  // 3. runs.
+  uint32_t* flag = (uint32_t*)keys_alt;  // keys_alt is free now: M x 8 bytes
+  uint32_t* idx = flag + M;
+  hipLaunchKernelGGL(k_run_flags, dim3(blocks_for(M, 256)), dim3(256), 0, s, keys, M, flag);
+  BUILD_HIP(scan_u32(flag, idx, M, part, d_small, s), "run scan");
+  uint32_t U = 0;
+  BUILD_HIP(hipMemcpyAsync(&U, d_small, sizeof U, hipMemcpyDeviceToHost, s), "copy");
+  BUILD_HIP(hipStreamSynchronize(s), "sync");
+  uint64_t* ukey = sc.get<uint64_t>(U);
+  uint32_t* ustart = sc.get<uint32_t>(U);
+  uint32_t* ucnt = sc.get<uint32_t>(U);
+  uint32_t* eq = sc.get<uint32_t>(U);
+  if (!ukey || !ustart || !ucnt || !eq) return fail(TFE_ERR_OOM, "run arrays");
+  hipLaunchKernelGGL(k_run_starts, dim3(blocks_for(M, 256)), dim3(256), 0, s, keys, M, flag, idx,
+                     ukey, ustart);
+  hipLaunchKernelGGL(k_run_counts, dim3(blocks_for(U, 256)), dim3(256), 0, s, ustart, U,
+                     (uint32_t)M, ucnt);
+  BUILD_HIP(hipGetLastError(), "run launches");
+  const uint64_t R = std::min<uint64_t>((uint64_t)skip + (uint64_t)top, U);
+  if (R <= (uint64_t)skip) return TFE_OK;
+  // 4. the R-th largest count and the runs that make ranks [0, R).
+  uint32_t* selh = hist;  // 256 bins, cleared by each pick
+  const uint32_t state0[4] = {0u, 0u, (uint32_t)R, 0u};
+  BUILD_HIP(hipMemsetAsync(selh, 0, 256 * sizeof(uint32_t), s), "memset");
+  BUILD_HIP(hipMemcpyAsync(d_small, state0, sizeof state0, hipMemcpyHostToDevice, s), "copy");
+  const uint32_t sel_blocks = std::min<uint32_t>(blocks_for(U, 256), 4096);
+  for (int shift = 24; shift >= 0; shift -= 8) {
+    hipLaunchKernelGGL(k_sel_hist, dim3(sel_blocks), dim3(256), 0, s, ucnt, U, d_small, shift,
+                       selh);
+    hipLaunchKernelGGL(k_sel_pick, dim3(1), dim3(256), 0, s, selh, d_small, shift);
+  }
+  BUILD_HIP(hipGetLastError(), "select launches");
+  // state = {c*, ~0, needed runs with count c*, runs above c*}.
+  hipLaunchKernelGGL(k_sel_eq, dim3(blocks_for(U, 256)), dim3(256), 0, s, ucnt, U, d_small, eq);
+  BUILD_HIP(scan_u32(eq, eq, U, part, nullptr, s), "tie scan");
+  uint32_t* keep = ustart;  // the run starts are no longer needed
+  hipLaunchKernelGGL(k_sel_keep, dim3(blocks_for(U, 256)), dim3(256), 0, s, ucnt, U, d_small, eq,
+                     keep);
+  uint32_t* pos = eq;
+  BUILD_HIP(scan_u32(keep, pos, U, part, nullptr, s), "keep scan");
+  uint32_t* rkey = sc.get<uint32_t>(R);
+  uint32_t* rkey_alt = sc.get<uint32_t>(R);
+  uint64_t* rval = sc.get<uint64_t>(R);
+  uint64_t* rval_alt = sc.get<uint64_t>(R);
+  if (!rkey || !rkey_alt || !rval || !rval_alt) return fail(TFE_ERR_OOM, "rank arrays");
+  hipLaunchKernelGGL(k_sel_compact, dim3(blocks_for(U, 256)), dim3(256), 0, s, ukey, ucnt, U,
+                     keep, pos, rkey, rval);
+  BUILD_HIP(hipGetLastError(), "compact launch");
+  // 5. rank by count (stable: tuple order among equal counts).
+  BUILD_HIP((radix_sort<uint32_t, true>(rkey, rkey_alt, rval, rval_alt, R, 32, hist, part, s)),
+            "rank sort");
+  // 6. ranks [skip, R).
+  const uint64_t m = R - (uint64_t)skip;
+  hipLaunchKernelGGL(k_unpack, dim3(blocks_for(m, 256)), dim3(256), 0, s, rkey, rval,
+                     (uint64_t)skip, m, n, out_tuples, out_counts);
+  BUILD_HIP(hipGetLastError(), "unpack launch");
+  BUILD_HIP(hipStreamSynchronize(s), "sync");
+  *written = (int64_t)m;
+  return TFE_OK;
+}
+
+}  // namespace
+}  // namespace tfe
+
+extern "C" tfe_status tfe_ngram_top(const int32_t* tokens, int64_t n_tokens, int32_t vocab,
+                                    int32_t n, int64_t skip, int64_t top, int32_t* out_tuples,
+                                    int64_t* out_counts, int64_t* written, void* stream) {
+  tfe::clear_error();
+  return tfe::ngram_top(tokens, n_tokens, vocab, n, skip, top, out_tuples, out_counts, written,
+                        (hipStream_t)stream);
+}

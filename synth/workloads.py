@@ -26,7 +26,8 @@ from . import (BF16, D, F32, TAG_CAND, TAG_HIDDEN, TAG_QUERY, TAG_STREAM, V, Phr
                QueryBatch, ngram_top, stack_tables, zipf_tokens)
 
 __all__ = ["config1", "config2_table", "config3_table", "config4_table", "config5_table",
-           "decode_batch", "prefill_batch", "CONFIG3_STOP", "windows_of"]
+           "decode_batch", "prefill_batch", "CONFIG3_STOP", "windows_of", "corpus_stream",
+           "workload2_stream", "workload3_stream"]
 
 # Stop-phrase filter of workload 3: the number of most frequent 2-, 3- and
 # 4-grams skipped before the table's phrases are taken (chosen with
@@ -79,8 +80,23 @@ def config1():
     return table, batch
 
 
+def corpus_stream(seed, s, stream_len):
+    """The seeded Zipf(s) token stream a frequency table is mined from."""
+    return zipf_tokens(seed, TAG_STREAM, stream_len, s)
+
+
+def workload2_stream():
+    """Stream of the 2^20-phrase decode table: 2^26 Zipf(1.1) tokens."""
+    return corpus_stream(1, 1.1, 1 << 26)
+
+
+def workload3_stream():
+    """Stream of the 4M-phrase prefill table: 200M Zipf(1.1) tokens."""
+    return corpus_stream(2, 1.1, 200_000_000)
+
+
 def _freq_table(seed, s, stream_len, per_n, stop=None):
-    stream = zipf_tokens(seed, TAG_STREAM, stream_len, s)
+    stream = corpus_stream(seed, s, stream_len)
     parts = []
     for j, (n, want) in enumerate(per_n):
         skip = 0 if stop is None else stop[j]
