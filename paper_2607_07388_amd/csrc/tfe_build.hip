@@ -4,11 +4,12 @@
 // the evaluation).
 //
 // Steps, all on the device:
-//   1. key formation: every window of n tokens that are all in [0, vocab)
-//      becomes one 64-bit key, the tokens in 18-bit fields, oldest in the
-//      highest field, so that key order is tuple order (blocks compact their
-//      valid windows and append them through one atomic offset each);
-//   2. LSD radix sort of the keys, 8-bit digits over the 18 n key bits: per
+//   1. key formation: every window of n tokens becomes one 64-bit key, the
+//      tokens in 18-bit fields, oldest in the highest field, so that key
+//      order is tuple order; a window with a token outside [0, vocab) gets
+//      the key 2^(18 n), above every valid one;
+//   2. LSD radix sort of the keys, 8-bit digits over the 18 n + 1 key bits
+//      (the valid keys end up first; a binary search counts them): per
 //      pass a digit histogram per 4096-key tile, one exclusive scan of the
 //      digit-major histogram, and a stable scatter (each wave ranks its keys
 //      with ballot-based digit matching, the tile is reordered in LDS and
@@ -44,35 +45,34 @@ constexpr int kScanBlock = kScanThreads * kScanItems;
 
 // ---- 1. keys -----------------------------------------------------------------
 
+// One key per window, in window order (no compaction: the sort moves the
+// invalid windows, marked with a key just above every valid one, to the end).
 __global__ __launch_bounds__(256) void k_ng_keys(const int32_t* tok, uint64_t nwin, int n,
-                                                 int32_t vocab, uint64_t* keys,
-                                                 unsigned long long* count) {
-  __shared__ uint32_t s_wave[4];
-  __shared__ unsigned long long s_base;
+                                                 int32_t vocab, uint64_t* keys) {
   const uint64_t i = (uint64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= nwin) return;
   uint64_t key = 0;
-  bool ok = i < nwin;
-  if (ok) {
-    for (int j = 0; j < n; ++j) {
-      const int32_t t = tok[i + j];
-      ok = ok && t >= 0 && t < vocab;
-      key = (key << 18) | (uint64_t)(uint32_t)(t & 0x3FFFF);
-    }
+  bool ok = true;
+  for (int j = 0; j < n; ++j) {
+    const int32_t t = tok[i + j];
+    ok = ok && t >= 0 && t < vocab;
+    key = (key << 18) | (uint64_t)(uint32_t)(t & 0x3FFFF);
   }
-  const uint64_t bal = __builtin_amdgcn_ballot_w64(ok);
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const uint32_t below = __builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32),
-                                                   __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0));
-  if (lane == 0) s_wave[wave] = (uint32_t)__builtin_popcountll(bal);
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    const uint32_t tot = s_wave[0] + s_wave[1] + s_wave[2] + s_wave[3];
-    s_base = tot ? atomicAdd(count, (unsigned long long)tot) : 0ull;
+  keys[i] = ok ? key : (1ull << (18 * n));
+}
+
+// Number of sorted keys below the invalid-window mark (one thread: binary
+// search).
+__global__ void k_count_valid(const uint64_t* keys, uint64_t nwin, int n,
+                              unsigned long long* count) {
+  const uint64_t mark = 1ull << (18 * n);
+  uint64_t lo = 0, hi = nwin;
+  while (lo < hi) {
+    const uint64_t mid = lo + (hi - lo) / 2;
+    if (keys[mid] < mark) lo = mid + 1;
+    else hi = mid;
   }
-  __syncthreads();
-  uint32_t off = 0;
-  for (int w = 0; w < wave; ++w) off += s_wave[w];
-  if (ok) keys[s_base + off + below] = key;
+  *count = lo;
 }
 
 // ---- device-wide exclusive scan of uint32 (totals below 2^32) ----------------
@@ -438,22 +438,23 @@ tfe_status ngram_top(const int32_t* tokens, int64_t N, int32_t vocab, int32_t n,
   uint32_t* d_small = sc.get<uint32_t>(8);
   if (!keys || !keys_alt || !hist || !part || !d_count || !d_small)
     return fail(TFE_ERR_OOM, "n-gram scratch for %llu windows", (unsigned long long)nwin);
-  // 1. keys of the valid windows.
-  BUILD_HIP(hipMemsetAsync(d_count, 0, sizeof(unsigned long long), s), "memset");
+  // 1. keys of all windows; 2. sort (one bit above the key fields carries
+  // the invalid-window mark); the valid keys are the first M.
   hipLaunchKernelGGL(k_ng_keys, dim3(blocks_for(nwin, 256)), dim3(256), 0, s, tokens, nwin, n,
-                     vocab, keys, d_count);
+                     vocab, keys);
   BUILD_HIP(hipGetLastError(), "keys launch");
+  uint64_t* no_vals = nullptr;
+  uint64_t* no_vals2 = nullptr;
+  BUILD_HIP((radix_sort<uint64_t, false>(keys, keys_alt, no_vals, no_vals2, nwin, 18 * n + 1,
+                                         hist, part, s)),
+            "key sort");
+  hipLaunchKernelGGL(k_count_valid, dim3(1), dim3(1), 0, s, keys, nwin, n, d_count);
+  BUILD_HIP(hipGetLastError(), "count launch");
   unsigned long long m_host = 0;
   BUILD_HIP(hipMemcpyAsync(&m_host, d_count, sizeof m_host, hipMemcpyDeviceToHost, s), "copy");
   BUILD_HIP(hipStreamSynchronize(s), "sync");
   const uint64_t M = m_host;
   if (M == 0) return TFE_OK;
-  // 2. sort.
-  uint64_t* no_vals = nullptr;
-  uint64_t* no_vals2 = nullptr;
-  BUILD_HIP((radix_sort<uint64_t, false>(keys, keys_alt, no_vals, no_vals2, M, 18 * n, hist,
-                                         part, s)),
-            "key sort");
   // 3. runs.
   uint32_t* flag = (uint32_t*)keys_alt;  // keys_alt is free now: M x 8 bytes
   uint32_t* idx = flag + M;
@@ -479,7 +480,8 @@ tfe_status ngram_top(const int32_t* tokens, int64_t N, int32_t vocab, int32_t n,
   const uint32_t state0[4] = {0u, 0u, (uint32_t)R, 0u};
   BUILD_HIP(hipMemsetAsync(selh, 0, 256 * sizeof(uint32_t), s), "memset");
   BUILD_HIP(hipMemcpyAsync(d_small, state0, sizeof state0, hipMemcpyHostToDevice, s), "copy");
-  const uint32_t sel_blocks = std::min<uint32_t>(blocks_for(U, 256), 4096);
+  // Few blocks: each adds its LDS histogram to the 256 global bins once.
+  const uint32_t sel_blocks = std::min<uint32_t>(blocks_for(U, 256), 512);
   for (int shift = 24; shift >= 0; shift -= 8) {
     hipLaunchKernelGGL(k_sel_hist, dim3(sel_blocks), dim3(256), 0, s, ucnt, U, d_small, shift,
                        selh);
