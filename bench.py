@@ -324,6 +324,38 @@ def main():
                       "%d-row stacked decode set (%.1f s, single thread)"
                       % (rows_done // B, B, csec),
         }
+        # The same oracle calls on every host core: the rows of the set split
+        # over threads (the oracle's table is read-only, and its C calls
+        # release the interpreter lock).
+        import threading
+        nthr = max(1, min(16, os.cpu_count() or 1))
+        bounds = [B * t // nthr for t in range(nthr + 1)]
+        parts = []
+        for t in range(nthr):
+            lo, hi = bounds[t], bounds[t + 1]
+            parts.append((np.ascontiguousarray(batch.tokens[lo:hi]), hidden[lo:hi].copy(),
+                          idx[lo:hi].copy()))
+        counts = [0] * nthr
+        stop = time.perf_counter() + args.cpu_seconds
+
+        def work(t):
+            tk, hd, ix = parts[t]
+            while time.perf_counter() < stop:
+                ot.lookup(tk, ctx, S)
+                oracle.inject(hd, vals, ix, synth.BF16)
+                counts[t] += tk.shape[0]
+
+        threads = [threading.Thread(target=work, args=(t,)) for t in range(nthr)]
+        c0 = time.perf_counter()
+        for th in threads:
+            th.start()
+        for th in threads:
+            th.join()
+        psec = time.perf_counter() - c0
+        result["cpu_baseline_threads"] = {
+            "value": sum(counts) / psec, "unit": "tokens/s", "cores": nthr, "kind": "oracle",
+            "sample": "the same passes with the set's rows split over %d threads (%.1f s)"
+                      % (nthr, psec)}
     gt.close()
     print(json.dumps(result))
 

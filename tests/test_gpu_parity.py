@@ -223,3 +223,26 @@ def test_workload4_large_table():
     hit, _ = check(table, gt, ot, batch.tokens, batch.ctx, batch.S, batch.hidden(), row_map=rows)
     assert 0.5 < hit.mean() < 0.95
     gt.close()
+
+
+def test_negative_zero_is_value_equal_on_noop_hits(w1):
+    """Zero value rows make every hit a no-op, but h = -0.0 turns into
+    -0 + g * (+0) = +0: the invariant holds by value there, by bytes
+    elsewhere, and misses keep their bytes exactly."""
+    table, batch, _, _ = w1
+    zt = synth.PhraseTable(table.tokens, table.lens, 2, 3, synth.F32, table.seed, sigma=0.0)
+    gz = H.GpuTable(zt)
+    hid = batch.hidden().copy()
+    hid[:, ::7] = -0.0
+    tok = torch.from_numpy(batch.tokens).cuda()
+    outs = H.Outputs(batch.T, table.dim, synth.F32)
+    H.run(gz, tok, 1, 0, batch.S, H.to_device(hid, synth.F32), outs)
+    torch.cuda.synchronize()
+    out = outs.out.cpu().numpy()
+    hit = outs.hit.cpu().numpy().astype(bool)
+    assert hit.any() and (~hit).any()
+    assert np.array_equal(out, hid)
+    assert out[~hit].tobytes() == hid[~hit].tobytes()
+    negz = np.signbit(hid[hit]) & (hid[hit] == 0)
+    assert negz.any() and not np.signbit(out[hit][negz]).any()
+    gz.close()
