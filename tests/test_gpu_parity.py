@@ -226,9 +226,10 @@ def test_workload4_large_table():
 
 
 def test_negative_zero_is_value_equal_on_noop_hits(w1):
-    """Zero value rows make every hit a no-op, but h = -0.0 turns into
-    -0 + g * (+0) = +0: the invariant holds by value there, by bytes
-    elsewhere, and misses keep their bytes exactly."""
+    """Zero value rows make every hit a no-op by value, but signed zeros
+    follow IEEE addition: h = -0 plus g * (+0) gives +0 (the zero rows hold
+    both +0 and -0).  So: equal to the input by value, byte-identical to the
+    oracle (same signed-zero arithmetic), and misses keep their bytes."""
     table, batch, _, _ = w1
     zt = synth.PhraseTable(table.tokens, table.lens, 2, 3, synth.F32, table.seed, sigma=0.0)
     gz = H.GpuTable(zt)
@@ -243,6 +244,8 @@ def test_negative_zero_is_value_equal_on_noop_hits(w1):
     assert hit.any() and (~hit).any()
     assert np.array_equal(out, hid)
     assert out[~hit].tobytes() == hid[~hit].tobytes()
-    negz = np.signbit(hid[hit]) & (hid[hit] == 0)
-    assert negz.any() and not np.signbit(out[hit][negz]).any()
+    _, _, _, want = H.oracle_answer(zt, H.oracle_table(zt), batch.tokens, 0, batch.S, hid)
+    assert out.tobytes() == want.tobytes()
+    flipped = np.signbit(hid) & ~np.signbit(out)
+    assert flipped.any() and (hid[flipped] == 0).all()
     gz.close()
