@@ -246,6 +246,41 @@ def main():
     torch.cuda.synchronize()
     lwall = time.perf_counter() - l0
     lhits = float(np.mean([s[2].hit.float().mean().item() for s in lat_sets]))
+    # Graph-replayed: 64 decode steps (rotating over the sets) captured once
+    # and replayed, as a decode loop without per-call launch overhead.
+    graph_us = None
+    try:
+        gsteps = 64
+
+        def gloop():
+            cs = torch.cuda.current_stream().cuda_stream
+            for k in range(gsteps):
+                tok, hid, outs = lat_sets[k % len(lat_sets)]
+                tfe.tfe_lookup_inject(gt.handle, tok, 64, ctx, S, hid, outs.out, outs.hit,
+                                      outs.slot, outs.len, tfe.TFE_GATE_SIGMOID, 1.0, cs)
+
+        side = torch.cuda.Stream()
+        side.wait_stream(stream)
+        with torch.cuda.stream(side):
+            gloop()
+        stream.wait_stream(side)
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            gloop()
+        graph.replay()
+        torch.cuda.synchronize()
+        reps = max(1, args.latency_steps // gsteps)
+        g0, g1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        g0.record(stream)
+        for _ in range(reps):
+            graph.replay()
+        g1.record(stream)
+        torch.cuda.synchronize()
+        graph_us = g0.elapsed_time(g1) * 1e3 / (reps * gsteps)
+        del graph
+    except RuntimeError as e:  # graphs unavailable: report without them
+        print("# graph replay skipped: %s" % e, file=sys.stderr)
 
     traffic = None
     if (kernel_sources_sha256() == PROFILED_TRAFFIC["sources_sha256"] and args.stack == 256):
@@ -293,6 +328,8 @@ def main():
             "mean_us_per_step": float(ldur.mean() * 1e6),
             "back_to_back_us_per_step": lwall / args.latency_steps * 1e6,
             "tokens_per_s_back_to_back": 64 * args.latency_steps / lwall,
+            "graph_replay_us_per_step": graph_us,
+            "tokens_per_s_graph_replay": (64e6 / graph_us) if graph_us else None,
             "hit_rate": lhits,
             "algorithmic_gbps_median": algorithmic_bytes(64, lhits * 64, 128, 3) /
                                        float(np.median(ldur)) / 1e9,
