@@ -754,6 +754,37 @@ def run_tiered(args):
                 "host_link_gbps": st["host_bytes"] / wall / 1e9,
             })
             print(json.dumps(results[-1]), file=sys.stderr, flush=True)
+    # Miss path against the host link: a cold cache (nothing prefilled) and
+    # stacked calls of 16384 decode rows, so that most matched rows are
+    # copied from pinned host memory into the cache by the side-stream fill.
+    desc = tfe.make_desc(table.tokens, table.lens, 2, 3, synth.V, vals, D, synth.BF16, 0, 0.5,
+                         hbm_cache_rows=C, adopt_host_values=1, prefill_rows=0)
+    handle = tfe.tfe_table_load(desc, stream.cuda_stream)
+    RB = 16384
+    cold = []
+    for k in range(4):
+        bt = synth.decode_batch(6, RB, set_index=500 + k)
+        tok = torch.from_numpy(bt.tokens).cuda()
+        hd = torch.empty((RB, D), dtype=torch.bfloat16, device="cuda")
+        synth.normal_fill_device(hd.data_ptr(), 0, RB, D, bt.seed, bt.hidden_tag, 1.0,
+                                 synth.BF16, stream.cuda_stream)
+        ob = H.Outputs(RB, D, synth.BF16)
+        torch.cuda.synchronize()
+        tfe.tfe_reset_stats(handle)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        tfe.tfe_lookup_inject(handle, tok, RB, 2, 1, hd, ob.out, ob.hit, ob.slot, ob.len,
+                              tfe.TFE_GATE_SIGMOID, 1.0, stream.cuda_stream)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        st = tfe.tfe_get_stats(handle)
+        sec = e0.elapsed_time(e1) * 1e-3
+        cold.append({"call": k, "us": sec * 1e6, "hits": st["hits"],
+                     "cache_misses": st["cache_misses"], "host_bytes": st["host_bytes"],
+                     "host_link_gbps": st["host_bytes"] / sec / 1e9})
+        print(json.dumps(cold[-1]), file=sys.stderr, flush=True)
+    tfe.tfe_table_free(handle)
+    first = cold[0]
     best = max((r for r in results if r["t_hide_us"] == 0.0), key=lambda r: r["tokens_per_s"],
                default=results[0])
     print(json.dumps({
@@ -774,6 +805,14 @@ def run_tiered(args):
                         "memory, 4M-row HBM cache (LRU), batch-64 decode, 8 candidates per row",
             "h2d_copy_gbps": h2d_gbps,
             "prefetch_budget_scored": args.prefetch_budget,
+        },
+        "miss_path": {
+            "rows_per_call": RB,
+            "calls": cold,
+            "roofline": {"bound": "host-link", "achieved": first["host_link_gbps"],
+                         "peak": h2d_gbps, "unit": "GB/s",
+                         "frac": first["host_link_gbps"] / h2d_gbps,
+                         "note": "peak = pinned host-to-device copy measured in the same run"},
         },
         "runs": results,
     }))
