@@ -297,8 +297,9 @@ constexpr int kRowCand = 16 * kHeadMaxK;                // logits of the candida
 //      the K tiles at or above tau holds a logit at or above tau, so the
 //      K-th largest logit is at least tau and every top-K logit lies in one
 //      of these K tiles.
-//   3. The logits of those tiles at or above tau (at most 16 K) are sorted in
-//      LDS; the first K are the answer.
+//   3. The logits of those tiles at or above tau (at most 16 K, usually a
+//      little over K) are ranked in LDS, by counting when there are at most
+//      1024 of them, else by a bitonic sort; the first K are the answer.
 __global__ __launch_bounds__(kRowThreads) void k_head_rows(const HeadArgs a) {
   __shared__ uint64_t s_cand[kRowCand];
   __shared__ uint32_t whist[kRowThreads / 64][256];
@@ -316,12 +317,15 @@ __global__ __launch_bounds__(kRowThreads) void k_head_rows(const HeadArgs a) {
   const float* ts = a.tsum + (grp * a.tblocks * 64 + c) * 16;
   auto sidx = [](uint32_t t) { return (size_t)(t >> 4) * 1024 + (t & 15); };
 
+  // Tile keys and sums are loaded together (one round trip).
   uint64_t key[kRowTiles];
+  float tsv[kRowTiles];
   uint64_t kmax = 0;
 #pragma unroll
   for (int i = 0; i < kRowTiles; ++i) {
     const uint32_t t = tid + i * kRowThreads;
     key[i] = t < NT ? tk[sidx(t)] : 0;
+    tsv[i] = t < NT ? ts[sidx(t)] : 0.f;
     kmax = umax64(kmax, key[i]);
   }
   // 1. Log-sum-exp over the tiles.
@@ -335,7 +339,7 @@ __global__ __launch_bounds__(kRowThreads) void k_head_rows(const HeadArgs a) {
 #pragma unroll
   for (int i = 0; i < kRowTiles; ++i) {
     const uint32_t t = tid + i * kRowThreads;
-    if (t < NT) part += ts[sidx(t)] * expf(key2f((uint32_t)(key[i] >> 32)) - M);
+    if (t < NT) part += tsv[i] * expf(key2f((uint32_t)(key[i] >> 32)) - M);
   }
   part = wave_add(part);
   if (lane == 0) s_red[wave] = part;
@@ -379,10 +383,17 @@ __global__ __launch_bounds__(kRowThreads) void k_head_rows(const HeadArgs a) {
     }
   }
   // Candidate tiles: the `take` keys whose masked bits reach the prefix.
+  // The smallest candidate tile key (every answer logit is at or above it)
+  // comes from the keys held in registers.
   uint32_t mine = 0;
+  uint64_t floor_key = ~0ull;
 #pragma unroll
-  for (int i = 0; i < kRowTiles; ++i)
-    mine += (tid + i * kRowThreads < NT && (key[i] & mask) >= prefix) ? 1u : 0u;
+  for (int i = 0; i < kRowTiles; ++i) {
+    if (tid + i * kRowThreads < NT && (key[i] & mask) >= prefix) {
+      ++mine;
+      floor_key = umin64(floor_key, key[i]);
+    }
+  }
   uint32_t ntile;
   uint32_t off = block_excl_scan<kRowThreads>(mine, s_wave, &ntile);
 #pragma unroll
@@ -390,11 +401,7 @@ __global__ __launch_bounds__(kRowThreads) void k_head_rows(const HeadArgs a) {
     const uint32_t t = tid + i * kRowThreads;
     if (t < NT && (key[i] & mask) >= prefix) s_tiles[off++] = t;
   }
-  __syncthreads();
-  // The smallest candidate tile key: every answer logit is at or above it.
   // (With all tiles taken, every logit is a candidate.)
-  uint64_t floor_key = ~0ull;
-  for (uint32_t e = tid; e < ntile; e += kRowThreads) floor_key = umin64(floor_key, tk[sidx(s_tiles[e])]);
   for (int d = 32; d >= 1; d >>= 1) floor_key = umin64(floor_key, shfl_xor64(floor_key, d));
   __syncthreads();
   if (lane == 0) s_cand[wave] = floor_key;
@@ -437,16 +444,28 @@ __global__ __launch_bounds__(kRowThreads) void k_head_rows(const HeadArgs a) {
     n_c += cnt;
     __syncthreads();
   }
-  const uint32_t N2 = pow2_ceil(max(n_c, 2u));
+  const float invS = 1.0f / S;
+  auto emit = [&](uint32_t i, uint64_t k) {
+    a.top_ids[(size_t)b * a.K + i] = (int32_t)(0xFFFFFFFFu - (uint32_t)k);
+    a.top_prob[(size_t)b * a.K + i] = expf(key2f((uint32_t)(k >> 32)) - M) * invS;
+  };
+  if (n_c <= (uint32_t)kRowThreads) {
+    // Usually a little over K candidates: each thread ranks its own by
+    // counting the larger ones (keys are distinct; every thread reads the
+    // same LDS word at a time), with no sorting network.
+    if ((uint32_t)tid < n_c) {
+      const uint64_t k = s_cand[tid];
+      uint32_t rank = 0;
+      for (uint32_t u = 0; u < n_c; ++u) rank += s_cand[u] > k ? 1u : 0u;
+      if (rank < a.K) emit(rank, k);
+    }
+    return;
+  }
+  const uint32_t N2 = pow2_ceil(n_c);
   for (uint32_t e = n_c + tid; e < N2; e += kRowThreads) s_cand[e] = 0;
   __syncthreads();
   lds_sort_desc<kRowThreads>(s_cand, N2);
-  const float invS = 1.0f / S;
-  for (uint32_t i = tid; i < a.K; i += kRowThreads) {
-    const uint64_t k = s_cand[i];
-    a.top_ids[(size_t)b * a.K + i] = (int32_t)(0xFFFFFFFFu - (uint32_t)k);
-    a.top_prob[(size_t)b * a.K + i] = expf(key2f((uint32_t)(k >> 32)) - M) * invS;
-  }
+  for (uint32_t i = tid; i < a.K; i += kRowThreads) emit(i, s_cand[i]);
 }
 
 }  // namespace
