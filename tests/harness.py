@@ -60,7 +60,9 @@ class GpuTable:
             self.handle = None
 
     def __del__(self):
-        self.close()
+        # At interpreter shutdown the binding may already be torn down.
+        if tfe is not None and getattr(tfe, "lib", None) is not None:
+            self.close()
 
 
 class Outputs:
