@@ -569,11 +569,26 @@ def run_head(args):
     print(json.dumps(result))
 
 
+def build_bytes_per_window(n):
+    """Data the construction pipeline moves per window of the stream.  n <= 3:
+    key formation (4 B token read, 8 B key write), one radix pass per 8 key
+    bits (18n + 1 bits; 8 B histogram read + 16 B scatter read/write), run
+    flags and starts (8 + 4 + 4 + 4 B).  n = 4: key formation writes both
+    words (4 + 16 B), seven passes over the 54-bit low word carry the high
+    word (8 + 32 B each), the high word is narrowed (8 + 4 B), three passes
+    over its 19 bits carry the low word (4 + 24 B each), and the run flags
+    read it too (24 B).  The selection and ranking work on far fewer items."""
+    if n <= 3:
+        return 12 + 24 * ((18 * n + 8) // 8) + 20
+    return 20 + 7 * 40 + 12 + 3 * 28 + 24
+
+
 def run_build(args):
-    """Offline phrase-table construction (Sec. 4.2): the most frequent 2- and
-    3-grams of the workload streams, as the decode and prefill tables are
-    built (2^26 tokens -> top 2^19 of each length; 200M tokens -> 2^21 2-grams
-    and 2^20 3-grams after skipping the 80000 most frequent of each)."""
+    """Offline phrase-table construction (Sec. 4.2): the most frequent 2-, 3-
+    and 4-grams of the workload streams, as the decode and prefill tables are
+    built (2^26 tokens -> top 2^19 2- and 3-grams; 200M tokens -> 2^21
+    2-grams, 2^20 3-grams and 2^20 4-grams after skipping the 80000 most
+    frequent of each)."""
     import torch
 
     import synth
@@ -584,7 +599,8 @@ def run_build(args):
     cases = [("2^26-token Zipf(1.1) stream", synth.workload2_stream(), [(2, 0, 1 << 19),
                                                                           (3, 0, 1 << 19)]),
              ("200M-token Zipf(1.1) stream", synth.workload3_stream(),
-              [(2, synth.CONFIG3_STOP[0], 1 << 21), (3, synth.CONFIG3_STOP[1], 1 << 20)])]
+              [(2, synth.CONFIG3_STOP[0], 1 << 21), (3, synth.CONFIG3_STOP[1], 1 << 20),
+               (4, synth.CONFIG3_STOP[2], 1 << 20)])]
     cpu_sample = None
     for name, toks, jobs in cases:
         tok_d = torch.from_numpy(toks).cuda()
@@ -602,12 +618,7 @@ def run_build(args):
                 m = tfe.tfe_ngram_top(tok_d, N, synth.V, n, skip, top, tup, cnt,
                                       stream.cuda_stream)
             sec = (time.perf_counter() - t0) / reps
-            passes = (18 * n + 7) // 8
-            # Data the pipeline moves per window: key formation (4 B read of
-            # the token, 8 B key write), each radix pass (8 B histogram read
-            # + 16 B scatter read/write), run flags and starts (8 + 4 + 4 +
-            # 4 B).  The selection and ranking work on far fewer items.
-            moved = N * (12 + 24 * passes + 20)
+            moved = N * build_bytes_per_window(n)
             runs.append({"stream": name, "n": n, "skip": skip, "top": top, "written": m,
                          "ms": sec * 1e3, "tokens_per_s": N / sec,
                          "pipeline_gbps": moved / sec / 1e9})

@@ -242,7 +242,7 @@ tfe_status tfe_head_free(tfe_head *head);
  * count, most frequent first, equal counts by the tuple in lexicographic
  * order (oldest token first); ranks [skip, skip + top) are written.
  *   tokens      DEVICE int32 [n_tokens], n_tokens <= 2^28
- *   vocab       1 <= vocab <= 2^18;  n: 1 <= n <= 3
+ *   vocab       1 <= vocab <= 2^18;  n: 1 <= n <= 4
  *   out_tuples  DEVICE int32 [top x n], oldest token first
  *   out_counts  DEVICE int64 [top]
  *   written     HOST: number of ranks written (fewer than top when the

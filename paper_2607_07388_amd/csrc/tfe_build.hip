@@ -21,8 +21,11 @@
 //      with count > c* and the first needed ones with count == c* (key order
 //      = tuple order, which breaks the ties);
 //   5. ranking: a stable radix sort of the selected runs by descending count
-//      (payload: the key), which keeps tuple order among equal counts;
+//      (payload: the run index), which keeps tuple order among equal counts;
 //   6. ranks [skip, skip + top) are unpacked into tuples and counts.
+// 4-grams need 72 key bits: the three newest tokens form the low word and
+// the oldest token the high word; the LSD sort runs over the low word (high
+// word as payload) and then stably over the high word.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -61,6 +64,30 @@ __global__ __launch_bounds__(256) void k_ng_keys(const int32_t* tok, uint64_t nw
   keys[i] = ok ? key : (1ull << (18 * n));
 }
 
+// 4-grams: 72 key bits in two words, lo = the three newest tokens (54 bits)
+// and hi = the oldest token, or the mark 2^18 for an invalid window.
+__global__ __launch_bounds__(256) void k_ng_keys4(const int32_t* tok, uint64_t nwin, int32_t vocab,
+                                                  uint64_t* lo, uint64_t* hi) {
+  const uint64_t i = (uint64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= nwin) return;
+  uint64_t key = 0;
+  bool ok = true;
+  for (int j = 1; j < 4; ++j) {
+    const int32_t t = tok[i + j];
+    ok = ok && t >= 0 && t < vocab;
+    key = (key << 18) | (uint64_t)(uint32_t)(t & 0x3FFFF);
+  }
+  const int32_t t0 = tok[i];
+  ok = ok && t0 >= 0 && t0 < vocab;
+  lo[i] = key;
+  hi[i] = ok ? (uint64_t)(uint32_t)t0 : (1ull << 18);
+}
+
+__global__ __launch_bounds__(256) void k_narrow(const uint64_t* in, uint64_t n, uint32_t* out) {
+  const uint64_t i = (uint64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i < n) out[i] = (uint32_t)in[i];
+}
+
 // Number of sorted keys below the invalid-window mark (one thread: binary
 // search).
 __global__ void k_count_valid(const uint64_t* keys, uint64_t nwin, int n,
@@ -71,6 +98,16 @@ __global__ void k_count_valid(const uint64_t* keys, uint64_t nwin, int n,
     const uint64_t mid = lo + (hi - lo) / 2;
     if (keys[mid] < mark) lo = mid + 1;
     else hi = mid;
+  }
+  *count = lo;
+}
+
+__global__ void k_count_valid_hi(const uint32_t* hi, uint64_t nwin, unsigned long long* count) {
+  uint64_t lo = 0, top = nwin;
+  while (lo < top) {
+    const uint64_t mid = lo + (top - lo) / 2;
+    if (hi[mid] < (1u << 18)) lo = mid + 1;
+    else top = mid;
   }
   *count = lo;
 }
@@ -260,18 +297,22 @@ __global__ __launch_bounds__(kTileThreads) void k_rs_scatter(const K* keys, cons
 
 // ---- 3. run-length count ----------------------------------------------------
 
-__global__ __launch_bounds__(256) void k_run_flags(const uint64_t* keys, uint64_t n,
-                                                   uint32_t* flag) {
+// hi: the high key word (4-grams) or null.
+__global__ __launch_bounds__(256) void k_run_flags(const uint64_t* keys, const uint32_t* hi,
+                                                   uint64_t n, uint32_t* flag) {
   const uint64_t i = (uint64_t)blockIdx.x * 256 + threadIdx.x;
-  if (i < n) flag[i] = (i == 0 || keys[i] != keys[i - 1]) ? 1u : 0u;
+  if (i < n)
+    flag[i] = (i == 0 || keys[i] != keys[i - 1] || (hi && hi[i] != hi[i - 1])) ? 1u : 0u;
 }
 
-__global__ __launch_bounds__(256) void k_run_starts(const uint64_t* keys, uint64_t n,
-                                                    const uint32_t* flag, const uint32_t* idx,
-                                                    uint64_t* ukey, uint32_t* ustart) {
+__global__ __launch_bounds__(256) void k_run_starts(const uint64_t* keys, const uint32_t* hi,
+                                                    uint64_t n, const uint32_t* flag,
+                                                    const uint32_t* idx, uint64_t* ukey,
+                                                    uint32_t* uhi, uint32_t* ustart) {
   const uint64_t i = (uint64_t)blockIdx.x * 256 + threadIdx.x;
   if (i < n && flag[i]) {
     ukey[idx[i]] = keys[i];
+    if (hi) uhi[idx[i]] = hi[i];
     ustart[idx[i]] = (uint32_t)i;
   }
 }
@@ -338,27 +379,31 @@ __global__ __launch_bounds__(256) void k_sel_keep(const uint32_t* cnt, uint32_t 
   }
 }
 
-__global__ __launch_bounds__(256) void k_sel_compact(const uint64_t* ukey, const uint32_t* cnt,
-                                                     uint32_t u, const uint32_t* keep,
-                                                     const uint32_t* pos, uint32_t* rkey,
-                                                     uint64_t* rval) {
+__global__ __launch_bounds__(256) void k_sel_compact(const uint32_t* cnt, uint32_t u,
+                                                     const uint32_t* keep, const uint32_t* pos,
+                                                     uint32_t* rkey, uint64_t* rval) {
   const uint32_t i = blockIdx.x * 256 + threadIdx.x;
   if (i < u && keep[i]) {
     rkey[pos[i]] = ~cnt[i];  // ascending ~count = descending count
-    rval[pos[i]] = ukey[i];
+    rval[pos[i]] = i;        // the run; runs are in tuple order
   }
 }
 
 // ---- 6. output ----------------------------------------------------------------
 
 __global__ __launch_bounds__(256) void k_unpack(const uint32_t* rkey, const uint64_t* rval,
+                                                const uint64_t* ukey, const uint32_t* uhi,
                                                 uint64_t skip, uint64_t m, int n,
                                                 int32_t* tuples, int64_t* counts) {
   const uint64_t i = (uint64_t)blockIdx.x * 256 + threadIdx.x;
   if (i < m) {
-    const uint64_t k = rval[skip + i];
-    for (int j = 0; j < n; ++j)
-      tuples[i * n + j] = (int32_t)((k >> (18 * (n - 1 - j))) & 0x3FFFFu);
+    const uint64_t run = rval[skip + i];
+    const uint64_t k = ukey[run];
+    const int nlo = uhi ? 3 : n;  // tokens held in the low word
+    int32_t* t = tuples + i * n;
+    if (uhi) t[0] = (int32_t)uhi[run];
+    for (int j = 0; j < nlo; ++j)
+      t[n - nlo + j] = (int32_t)((k >> (18 * (nlo - 1 - j))) & 0x3FFFFu);
     counts[i] = (int64_t)(uint32_t)~rkey[skip + i];
   }
 }
@@ -422,33 +467,52 @@ tfe_status ngram_top(const int32_t* tokens, int64_t N, int32_t vocab, int32_t n,
   // The two-level scans cover up to 2^28 elements.
   if (N < 0 || N > (1ll << 28)) return fail(TFE_ERR_INVALID_ARG, "N outside [0, 2^28]");
   if (vocab < 1 || vocab > (1 << 18)) return fail(TFE_ERR_INVALID_ARG, "vocab outside [1, 2^18]");
-  if (n < 1 || n > 3) return fail(TFE_ERR_UNSUPPORTED, "n = %d (1..3 supported)", n);
+  if (n < 1 || n > 4) return fail(TFE_ERR_UNSUPPORTED, "n = %d (1..4 supported)", n);
   if (skip < 0 || top < 0) return fail(TFE_ERR_INVALID_ARG, "negative skip or top");
   if (N < n || top == 0) return TFE_OK;
   if (!tokens || !out_tuples || !out_counts)
     return fail(TFE_ERR_INVALID_ARG, "null tokens or outputs");
   const uint64_t nwin = (uint64_t)(N - n + 1);
+  const bool wide = n == 4;
   Scratch sc;
   uint64_t* keys = sc.get<uint64_t>(nwin);
   uint64_t* keys_alt = sc.get<uint64_t>(nwin);
+  uint64_t* wv = wide ? sc.get<uint64_t>(nwin) : nullptr;      // 4-grams: high word payload
+  uint64_t* wv_alt = wide ? sc.get<uint64_t>(nwin) : nullptr;
+  uint32_t* hi = wide ? sc.get<uint32_t>(nwin) : nullptr;      // 4-grams: high word keys
+  uint32_t* hi_alt = wide ? sc.get<uint32_t>(nwin) : nullptr;
   const uint32_t ntiles = blocks_for(nwin, kTile);
   uint32_t* hist = sc.get<uint32_t>((uint64_t)256 * ntiles);
   uint32_t* part = sc.get<uint32_t>(kScanBlock);
   unsigned long long* d_count = sc.get<unsigned long long>(1);
   uint32_t* d_small = sc.get<uint32_t>(8);
-  if (!keys || !keys_alt || !hist || !part || !d_count || !d_small)
+  if (!keys || !keys_alt || !hist || !part || !d_count || !d_small ||
+      (wide && (!wv || !wv_alt || !hi || !hi_alt)))
     return fail(TFE_ERR_OOM, "n-gram scratch for %llu windows", (unsigned long long)nwin);
   // 1. keys of all windows; 2. sort (one bit above the key fields carries
-  // the invalid-window mark); the valid keys are the first M.
-  hipLaunchKernelGGL(k_ng_keys, dim3(blocks_for(nwin, 256)), dim3(256), 0, s, tokens, nwin, n,
-                     vocab, keys);
-  BUILD_HIP(hipGetLastError(), "keys launch");
+  // the invalid-window mark); the valid keys are the first M.  4-grams sort
+  // by the low word, then stably by the high word (LSD over both words).
   uint64_t* no_vals = nullptr;
   uint64_t* no_vals2 = nullptr;
-  BUILD_HIP((radix_sort<uint64_t, false>(keys, keys_alt, no_vals, no_vals2, nwin, 18 * n + 1,
-                                         hist, part, s)),
-            "key sort");
-  hipLaunchKernelGGL(k_count_valid, dim3(1), dim3(1), 0, s, keys, nwin, n, d_count);
+  if (!wide) {
+    hipLaunchKernelGGL(k_ng_keys, dim3(blocks_for(nwin, 256)), dim3(256), 0, s, tokens, nwin, n,
+                       vocab, keys);
+    BUILD_HIP(hipGetLastError(), "keys launch");
+    BUILD_HIP((radix_sort<uint64_t, false>(keys, keys_alt, no_vals, no_vals2, nwin, 18 * n + 1,
+                                           hist, part, s)),
+              "key sort");
+    hipLaunchKernelGGL(k_count_valid, dim3(1), dim3(1), 0, s, keys, nwin, n, d_count);
+  } else {
+    hipLaunchKernelGGL(k_ng_keys4, dim3(blocks_for(nwin, 256)), dim3(256), 0, s, tokens, nwin,
+                       vocab, keys, wv);
+    BUILD_HIP(hipGetLastError(), "keys launch");
+    BUILD_HIP((radix_sort<uint64_t, true>(keys, keys_alt, wv, wv_alt, nwin, 54, hist, part, s)),
+              "low-word sort");
+    hipLaunchKernelGGL(k_narrow, dim3(blocks_for(nwin, 256)), dim3(256), 0, s, wv, nwin, hi);
+    BUILD_HIP((radix_sort<uint32_t, true>(hi, hi_alt, keys, keys_alt, nwin, 19, hist, part, s)),
+              "high-word sort");
+    hipLaunchKernelGGL(k_count_valid_hi, dim3(1), dim3(1), 0, s, hi, nwin, d_count);
+  }
   BUILD_HIP(hipGetLastError(), "count launch");
   unsigned long long m_host = 0;
   BUILD_HIP(hipMemcpyAsync(&m_host, d_count, sizeof m_host, hipMemcpyDeviceToHost, s), "copy");
@@ -458,18 +522,19 @@ tfe_status ngram_top(const int32_t* tokens, int64_t N, int32_t vocab, int32_t n,
   // 3. runs.
   uint32_t* flag = (uint32_t*)keys_alt;  // keys_alt is free now: M x 8 bytes
   uint32_t* idx = flag + M;
-  hipLaunchKernelGGL(k_run_flags, dim3(blocks_for(M, 256)), dim3(256), 0, s, keys, M, flag);
+  hipLaunchKernelGGL(k_run_flags, dim3(blocks_for(M, 256)), dim3(256), 0, s, keys, hi, M, flag);
   BUILD_HIP(scan_u32(flag, idx, M, part, d_small, s), "run scan");
   uint32_t U = 0;
   BUILD_HIP(hipMemcpyAsync(&U, d_small, sizeof U, hipMemcpyDeviceToHost, s), "copy");
   BUILD_HIP(hipStreamSynchronize(s), "sync");
   uint64_t* ukey = sc.get<uint64_t>(U);
+  uint32_t* uhi = wide ? sc.get<uint32_t>(U) : nullptr;
   uint32_t* ustart = sc.get<uint32_t>(U);
   uint32_t* ucnt = sc.get<uint32_t>(U);
   uint32_t* eq = sc.get<uint32_t>(U);
-  if (!ukey || !ustart || !ucnt || !eq) return fail(TFE_ERR_OOM, "run arrays");
-  hipLaunchKernelGGL(k_run_starts, dim3(blocks_for(M, 256)), dim3(256), 0, s, keys, M, flag, idx,
-                     ukey, ustart);
+  if (!ukey || !ustart || !ucnt || !eq || (wide && !uhi)) return fail(TFE_ERR_OOM, "run arrays");
+  hipLaunchKernelGGL(k_run_starts, dim3(blocks_for(M, 256)), dim3(256), 0, s, keys, hi, M, flag,
+                     idx, ukey, uhi, ustart);
   hipLaunchKernelGGL(k_run_counts, dim3(blocks_for(U, 256)), dim3(256), 0, s, ustart, U,
                      (uint32_t)M, ucnt);
   BUILD_HIP(hipGetLastError(), "run launches");
@@ -501,15 +566,15 @@ tfe_status ngram_top(const int32_t* tokens, int64_t N, int32_t vocab, int32_t n,
   uint64_t* rval = sc.get<uint64_t>(R);
   uint64_t* rval_alt = sc.get<uint64_t>(R);
   if (!rkey || !rkey_alt || !rval || !rval_alt) return fail(TFE_ERR_OOM, "rank arrays");
-  hipLaunchKernelGGL(k_sel_compact, dim3(blocks_for(U, 256)), dim3(256), 0, s, ukey, ucnt, U,
-                     keep, pos, rkey, rval);
+  hipLaunchKernelGGL(k_sel_compact, dim3(blocks_for(U, 256)), dim3(256), 0, s, ucnt, U, keep,
+                     pos, rkey, rval);
   BUILD_HIP(hipGetLastError(), "compact launch");
   // 5. rank by count (stable: tuple order among equal counts).
   BUILD_HIP((radix_sort<uint32_t, true>(rkey, rkey_alt, rval, rval_alt, R, 32, hist, part, s)),
             "rank sort");
   // 6. ranks [skip, R).
   const uint64_t m = R - (uint64_t)skip;
-  hipLaunchKernelGGL(k_unpack, dim3(blocks_for(m, 256)), dim3(256), 0, s, rkey, rval,
+  hipLaunchKernelGGL(k_unpack, dim3(blocks_for(m, 256)), dim3(256), 0, s, rkey, rval, ukey, uhi,
                      (uint64_t)skip, m, n, out_tuples, out_counts);
   BUILD_HIP(hipGetLastError(), "unpack launch");
   BUILD_HIP(hipStreamSynchronize(s), "sync");

@@ -37,7 +37,7 @@ def test_hand_counted():
     assert t.tolist() == [[1, 2], [2, 1], [2, 3]] and c.tolist() == [3, 2, 1]
 
 
-@pytest.mark.parametrize("n", [1, 2, 3])
+@pytest.mark.parametrize("n", [1, 2, 3, 4])
 @pytest.mark.parametrize("N,vocab", [(10007, 6), (70001, 40), (300000, 151936)])
 def test_random_streams_with_separators(n, N, vocab):
     """Several radix tiles and a ragged last one; -1 and out-of-range tokens
@@ -63,9 +63,27 @@ def test_ties_broken_by_tuple():
     check(tok, 4, 2, 3, 5)
 
 
+def test_four_grams_split_on_the_oldest_token():
+    """4-gram keys span two words (the oldest token alone in the high word):
+    tuples that share their three newest tokens and differ only in the
+    oldest, with token values using all 18 bits, must stay distinct and keep
+    tuple order among equal counts."""
+    rng = np.random.default_rng(44)
+    vocab = 1 << 18
+    tails = rng.integers(0, vocab, (5, 3)).astype(np.int32)
+    heads = np.array([0, 1, vocab - 1, vocab - 2, 1 << 17, 12345], np.int32)
+    parts = []
+    for r in range(3000):
+        parts.append(np.concatenate([[heads[r % 6]], tails[(r * 7) % 5], [-1]]))
+    tok = np.concatenate(parts).astype(np.int32)
+    t, c = check(tok, vocab, 4, 0, 100)
+    assert len(t) == 30 and int(c.sum()) == 3000
+    check(tok, vocab, 4, 7, 11)
+
+
 def test_zipf_stream_matches_generator_and_oracle():
     toks = synth.zipf_tokens(4, 88, 1 << 20, 1.1)
-    for n in (2, 3):
+    for n in (2, 3, 4):
         t, c = check(toks, synth.V, n, 50, 20000)
         wt, wc = synth.ngram_top(toks, n, 20000, skip=50)
         np.testing.assert_array_equal(t, wt)
@@ -74,9 +92,9 @@ def test_zipf_stream_matches_generator_and_oracle():
 
 def test_workload2_stream_full_size():
     """The 2^26-token Zipf(1.1) stream of the 2^20-phrase decode table: top
-    2^19 2-grams and 3-grams, against the generator's partitioned count."""
+    2^19 2-, 3- and 4-grams, against the generator's partitioned count."""
     toks = synth.workload2_stream()
-    for n in (2, 3):
+    for n in (2, 3, 4):
         t, c = gpu_top(toks, synth.V, n, 0, 1 << 19)
         wt, wc = synth.ngram_top(toks, n, 1 << 19)
         np.testing.assert_array_equal(t, wt)
@@ -88,11 +106,13 @@ def test_errors_and_empty():
     out_t = torch.zeros((4, 4), dtype=torch.int32, device="cuda")
     out_c = torch.zeros(4, dtype=torch.int64, device="cuda")
     with pytest.raises(tfe.TfeError) as e:
-        tfe.tfe_ngram_top(tok, 10, 100, 4, 0, 4, out_t, out_c)
+        tfe.tfe_ngram_top(tok, 10, 100, 5, 0, 4, out_t, out_c)
     assert e.value.status == -5
     with pytest.raises(tfe.TfeError):
         tfe.tfe_ngram_top(tok, 10, 1 << 19, 2, 0, 4, out_t, out_c)
     assert tfe.tfe_ngram_top(tok, 1, 100, 2, 0, 4, out_t, out_c) == 0
+    assert tfe.tfe_ngram_top(tok, 3, 100, 4, 0, 4, out_t, out_c) == 0
+    assert tfe.tfe_ngram_top(tok, 4, 100, 4, 0, 4, out_t, out_c) == 1
     assert tfe.tfe_ngram_top(tok, 10, 100, 2, 0, 0, out_t, out_c) == 0
     neg = torch.full((10,), -1, dtype=torch.int32, device="cuda")
     assert tfe.tfe_ngram_top(neg, 10, 100, 2, 0, 4, out_t, out_c) == 0
