@@ -69,6 +69,18 @@ typedef enum { TFE_GATE_SIGMOID = 0, TFE_GATE_CONST = 1 } tfe_gate;
  * Both add up to 1, so one retained phrase injects its own row. */
 typedef enum { TFE_WEIGHT_LENGTH = 0, TFE_WEIGHT_UNIFORM = 1 } tfe_weighting;
 
+/* Tiered tables: how a row that a lookup finds only in host memory reaches
+ * the cache slot it is given (staging into the faster tier, Sec. 4.3).
+ * Either way the lookup injects the row read straight from host memory and
+ * never waits for the copy.
+ *   TFE_FILL_INLINE:      the injection kernel that reads the row also writes
+ *                         it into the slot: one host read per missed row and
+ *                         no cross-stream events;
+ *   TFE_FILL_SIDE_STREAM: a copy kernel on the table's side stream, overlapped
+ *                         with the injection, reads the row from host memory a
+ *                         second time; the next call waits for it. */
+typedef enum { TFE_FILL_INLINE = 0, TFE_FILL_SIDE_STREAM = 1 } tfe_fill_mode;
+
 typedef struct {
   /* Phrases (Sec. 4.2): phrase i is phrase_tokens[i*n_max .. i*n_max+len-1],
    * oldest token first, len = phrase_len[i]; unused columns are ignored.
@@ -91,6 +103,7 @@ typedef struct {
   int32_t adopt_host_values;    /* tiered: 1 = use the caller's `values` in place; it
                                    must come from hipHostMalloc and outlive the table */
   int64_t prefill_rows;         /* tiered: rows [0, prefill_rows) start cached */
+  int32_t miss_fill;            /* tiered: tfe_fill_mode (0 = inline); must be 0 or 1 */
 } tfe_table_desc;
 
 typedef struct {

@@ -29,7 +29,10 @@ Policy (the precise reading; a call is one lookup or one prefetch):
   prefetch_used counts a prefetched slot the first time a lookup finds it
   cached.  A position is served from host memory when its row was not cached
   when the call began (it was filled by this call or found no slot);
-  host_bytes = row bytes x (rows filled + positions served from host).
+  host_bytes = row bytes x positions served from host, plus row bytes x rows
+  filled when the fill is a separate copy that reads the row from host
+  memory again (fill_rereads=True; the library's side-stream fill).  Rows
+  filled by a prefetch always count once.
 """
 import collections
 
@@ -37,9 +40,10 @@ GROUP = 1024
 
 
 class LruModel:
-    def __init__(self, cache_rows, prefill_rows, row_bytes):
+    def __init__(self, cache_rows, prefill_rows, row_bytes, fill_rereads=False):
         self.C = cache_rows
         self.row_bytes = row_bytes
+        self.fill_rereads = fill_rereads
         self.slot_row = [-1] * cache_rows
         self.where = {}
         # Recency order: OrderedDict of slot -> None, least recent first.
@@ -122,7 +126,8 @@ class LruModel:
                     self.stats["cache_misses"] += 1
                 if kind != "cache" or r in filled_now:
                     self.stats["host_bytes"] += self.row_bytes
-            self.stats["host_bytes"] += self.row_bytes * len(filled)
+            if self.fill_rereads:
+                self.stats["host_bytes"] += self.row_bytes * len(filled)
         self.stats["positions"] += len(rows)
         return out
 

@@ -113,6 +113,7 @@ static tfe::TierArgs tier_args(tfe_table* t) {
   a.jobs = t->d_jobs;
   a.clock = t->clock;
   a.row_bytes = (uint32_t)(t->dim * elem_size(t->dtype));
+  a.fill_inline = t->fill_mode == TFE_FILL_INLINE ? 1u : 0u;
   a.look.slots = t->d_slots;
   a.look.bucket_mask = (uint64_t)(t->capacity / TFE_SLOTS_PER_BUCKET - 1);
   a.look.n_min = t->n_min;
@@ -135,6 +136,7 @@ static tfe_status load_tiered(tfe_table* t, const tfe_table_desc* d, hipStream_t
   const size_t row_bytes = (size_t)d->dim * elem_size(d->dtype);
   t->cache_rows = C;
   t->prefill_rows = d->prefill_rows;
+  t->fill_mode = d->miss_fill;
   if (P > 0 && d->adopt_host_values) {
     hipPointerAttribute_t attr;
     const hipError_t pe = hipPointerGetAttributes(&attr, d->values);
@@ -261,13 +263,16 @@ static tfe_status lookup_tiered(tfe_table* t, const LookupArgs& look, hipStream_
   // slots, and before the fill list is rewritten.
   if (t->fill_recorded) TFE_HIP(hipStreamWaitEvent(stream, t->ev_filled, 0), "wait fill");
   TFE_HIP(tfe::launch_resolve_lookup(a, stream), "tier resolve");
-  TFE_HIP(hipEventRecord(t->ev_resolved, stream), "record");
-  // Missed rows are copied into their new cache slots on the side stream,
-  // overlapped with the injection, which reads them from host memory.
-  TFE_HIP(hipStreamWaitEvent(t->fill_stream, t->ev_resolved, 0), "wait resolve");
-  TFE_HIP(tfe::launch_fill(a, t->dtype, t->dim, look.T, t->fill_stream), "tier fill");
-  TFE_HIP(hipEventRecord(t->ev_filled, t->fill_stream), "record");
-  t->fill_recorded = true;
+  if (t->fill_mode == TFE_FILL_SIDE_STREAM) {
+    // Missed rows are copied into their new cache slots on the side stream,
+    // overlapped with the injection, which reads them from host memory.
+    TFE_HIP(hipEventRecord(t->ev_resolved, stream), "record");
+    TFE_HIP(hipStreamWaitEvent(t->fill_stream, t->ev_resolved, 0), "wait resolve");
+    TFE_HIP(tfe::launch_fill(a, t->dtype, t->dim, look.T, t->fill_stream), "tier fill");
+    TFE_HIP(hipEventRecord(t->ev_filled, t->fill_stream), "record");
+    t->fill_recorded = true;
+  }
+  // Inline fill: the injection writes each missed row into its slot.
   TFE_HIP(tfe::launch_tier_inject(a, t->dtype, t->dim, stream), "inject");
   t->lookup_recorded = true;
   t->last_stream = stream;
@@ -322,6 +327,8 @@ static tfe_status load(const tfe_table_desc* d, hipStream_t stream, tfe_table** 
   if (d->prefill_rows < 0 || d->prefill_rows > d->hbm_cache_rows ||
       d->prefill_rows > d->n_phrases)
     return fail(TFE_ERR_INVALID_ARG, "prefill_rows outside [0, min(hbm_cache_rows, n_phrases)]");
+  if (d->miss_fill != TFE_FILL_INLINE && d->miss_fill != TFE_FILL_SIDE_STREAM)
+    return fail(TFE_ERR_INVALID_ARG, "miss_fill must be TFE_FILL_INLINE or TFE_FILL_SIDE_STREAM");
   if (d->adopt_host_values && (d->hbm_cache_rows == 0 || d->values_on_device))
     return fail(TFE_ERR_INVALID_ARG, "adopt_host_values needs a tiered table and host values");
   tfe_status st = validate_phrases(d->phrase_tokens, d->phrase_len, d->n_phrases, d->n_min,

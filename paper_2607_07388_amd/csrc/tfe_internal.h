@@ -77,7 +77,12 @@ struct TierArgs {
   TierJob* jobs;              // [cap]
   uint32_t clock;
   uint32_t row_bytes;
+  uint32_t fill_inline;       // the inject writes missed rows into their slots
 };
+
+// Phase bit of a position whose inject writes its row into slot_of (inline
+// fill: the first position of each row filled by the call).
+constexpr uint8_t kPhaseWrite = 0x10;
 
 hipError_t launch_tier_init(const TierArgs& t, uint32_t C, uint32_t prefill, hipStream_t s);
 hipError_t launch_ring_compact(const TierArgs& t, uint64_t* dst, uint64_t dst_mask,
@@ -121,6 +126,7 @@ struct tfe_table {
   // Tiered mode (cache_rows > 0).
   int64_t cache_rows = 0;
   int64_t prefill_rows = 0;
+  int32_t fill_mode = 0;         // tfe_fill_mode
   void* h_values = nullptr;      // pinned host rows [P x dim]
   const void* h_values_dev = nullptr;
   bool own_h_values = false;

@@ -17,9 +17,10 @@
 // A lookup call runs: probe (wide) -> resolve (one block: residency, victim
 // choice, fill list, recency update, all in position order so the policy is
 // deterministic) -> inject (wide; cached rows from HBM, the others straight
-// from pinned host memory over PCIe), while a side stream copies the missed
-// rows from host memory into their new cache slots for later calls.  The
-// next call's inject waits for that copy; nothing in this call does.
+// from pinned host memory over PCIe).  A missed row given a slot is written
+// into it either by the inject itself, from the copy it read (inline fill),
+// or by a copy kernel on a side stream that reads it from host memory again;
+// the next call waits for that copy, nothing in this call does.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -231,8 +232,9 @@ __global__ __launch_bounds__(kResolveThreads) void k_resolve_lookup(const TierAr
     if (valid) {
       const int32_t s1 = r >= 0 ? hslot[h] : -1;
       const uint8_t ph = r >= 0 ? hphase[h] : 3;
+      const bool writes = t.fill_inline && miss_first && mrank < got;
       t.slot_of[p] = s1;
-      t.phase[p] = ph;
+      t.phase[p] = writes ? (uint8_t)(ph | kPhaseWrite) : ph;
       if (r >= 0) {
         atomicAdd(&s_cnt[0], 1u);
         if (hcached[h]) atomicAdd(&s_cnt[1], 1u);
@@ -259,7 +261,8 @@ __global__ __launch_bounds__(kResolveThreads) void k_resolve_lookup(const TierAr
     st.cache_hits += s_cnt[1];
     st.cache_misses += s_cnt[0] - s_cnt[1];
     st.prefetch_used += s_cnt[2];
-    st.host_bytes += (unsigned long long)(s_cnt[4] + s_cnt[3]) * t.row_bytes;
+    st.host_bytes +=
+        (unsigned long long)((t.fill_inline ? 0u : s_cnt[4]) + s_cnt[3]) * t.row_bytes;
   }
 }
 
@@ -492,7 +495,8 @@ __global__ __launch_bounds__(WPB * 64) void k_prefetch_probe(const TierArgs t,
 // Inject of every position: value rows come from the cache (phase 0) or
 // straight from pinned host memory over PCIe (phases 1 and 2: rows that were
 // not cached when the call began); phase 3 (no match) copies the hidden row
-// (out of place).
+// (out of place).  With kPhaseWrite the wave also stores the row it read into
+// its new cache slot.
 template <int DT, int NCH, int WPB>
 __global__ __launch_bounds__(WPB * 64) void k_tier_inject(const TierArgs t) {
   constexpr int ROW_VECS = NCH * 64;
@@ -500,7 +504,8 @@ __global__ __launch_bounds__(WPB * 64) void k_tier_inject(const TierArgs t) {
   const int lane = threadIdx.x & 63;
   const uint32_t p = blockIdx.x * WPB + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   if (p >= a.T) return;
-  const uint32_t ph = t.phase[p];
+  const uint32_t ph_w = t.phase[p];
+  const uint32_t ph = ph_w & 3u;
   u32x4 hv[NCH];
   const u32x4* hin = (const u32x4*)a.hin + (size_t)p * ROW_VECS;
 #pragma unroll
@@ -518,6 +523,11 @@ __global__ __launch_bounds__(WPB * 64) void k_tier_inject(const TierArgs t) {
   u32x4 mv[NCH];
 #pragma unroll
   for (int k = 0; k < NCH; ++k) mv[k] = mrow[k * 64 + lane];
+  if (ph_w & kPhaseWrite) {
+    u32x4* dst = (u32x4*)t.cache + (size_t)t.slot_of[p] * ROW_VECS;
+#pragma unroll
+    for (int k = 0; k < NCH; ++k) dst[k * 64 + lane] = mv[k];
+  }
   const float g = dev::gate_of<DT, NCH>(a, hv, mv);
   dev::store_injected<DT, NCH>(out, hv, mv, g, lane);
 }

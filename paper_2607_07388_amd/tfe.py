@@ -21,6 +21,7 @@ TFE_ERR_UNSUPPORTED = -5
 TFE_F32, TFE_BF16 = 0, 1
 TFE_GATE_SIGMOID, TFE_GATE_CONST = 0, 1
 TFE_WEIGHT_LENGTH, TFE_WEIGHT_UNIFORM = 0, 1
+TFE_FILL_INLINE, TFE_FILL_SIDE_STREAM = 0, 1
 
 
 class tfe_table_desc(ctypes.Structure):
@@ -39,6 +40,7 @@ class tfe_table_desc(ctypes.Structure):
         ("hbm_cache_rows", ctypes.c_int64),
         ("adopt_host_values", ctypes.c_int32),
         ("prefill_rows", ctypes.c_int64),
+        ("miss_fill", ctypes.c_int32),
     ]
 
 
@@ -220,7 +222,7 @@ def tfe_index_probe_host(slots, capacity, tokens, n):
 
 def make_desc(phrase_tokens, phrase_len, n_min, n_max, vocab, values, dim, dtype,
               values_on_device, max_load_factor=0.5, hbm_cache_rows=0, adopt_host_values=0,
-              prefill_rows=0):
+              prefill_rows=0, miss_fill=0):
     """Fills a tfe_table_desc; the caller keeps the arrays alive until
     tfe_table_load returns (and `values` for the table's life if adopted)."""
     d = tfe_table_desc()
@@ -234,4 +236,5 @@ def make_desc(phrase_tokens, phrase_len, n_min, n_max, vocab, values, dim, dtype
     d.hbm_cache_rows = hbm_cache_rows
     d.adopt_host_values = adopt_host_values
     d.prefill_rows = prefill_rows
+    d.miss_fill = miss_fill
     return d

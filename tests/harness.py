@@ -16,6 +16,16 @@ def cur_stream():
     return torch.cuda.current_stream().cuda_stream
 
 
+def release_pinned():
+    """Returns the pinned host blocks torch keeps cached after their tensors
+    died, so that a large pinned allocation that follows finds the memory."""
+    import gc
+    gc.collect()
+    empty = getattr(torch._C, "_host_emptyCache", None)
+    if empty is not None:
+        empty()
+
+
 def device_values(table):
     """The table's value rows drawn on the device (bit-identical to the host draw)."""
     v = torch.empty((table.n_phrases, table.dim), dtype=TORCH_DT[table.dtype], device="cuda")

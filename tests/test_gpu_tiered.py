@@ -30,8 +30,11 @@ def pinned_values(table):
     return v
 
 
+FILLS = [tfe.TFE_FILL_INLINE, tfe.TFE_FILL_SIDE_STREAM]
+
+
 class TieredTable:
-    def __init__(self, table, cache_rows, prefill_rows, adopt=True):
+    def __init__(self, table, cache_rows, prefill_rows, adopt=True, fill=tfe.TFE_FILL_INLINE):
         self.table = table
         if adopt:
             self.values = pinned_values(table)
@@ -41,7 +44,8 @@ class TieredTable:
             vals = table.all_values()
         desc = tfe.make_desc(table.tokens, table.lens, table.n_min, table.n_max, table.vocab,
                              vals, table.dim, table.dtype, 0, 0.5, hbm_cache_rows=cache_rows,
-                             adopt_host_values=int(adopt), prefill_rows=prefill_rows)
+                             adopt_host_values=int(adopt), prefill_rows=prefill_rows,
+                             miss_fill=fill)
         self.handle = tfe.tfe_table_load(desc, H.cur_stream())
 
     def close(self):
@@ -81,13 +85,15 @@ def w2_tables():
     res = H.GpuTable(table)
     yield table, res, H.oracle_table(table)
     res.close()
+    H.release_pinned()
 
 
-def test_tiered_decode_steps_match_oracle_resident_and_lru_model(w2_tables):
+@pytest.mark.parametrize("fill", FILLS)
+def test_tiered_decode_steps_match_oracle_resident_and_lru_model(w2_tables, fill):
     table, res, ot = w2_tables
     C, pre = 4096, 2048
-    tier = TieredTable(table, C, pre)
-    model = LruModel(C, pre, table.dim * 2)
+    tier = TieredTable(table, C, pre, fill=fill)
+    model = LruModel(C, pre, table.dim * 2, fill_rereads=fill == tfe.TFE_FILL_SIDE_STREAM)
     for step in range(8):
         batch = synth.decode_batch(1, 64, set_index=40 + step)
         hidden = batch.hidden()
@@ -102,14 +108,15 @@ def test_tiered_decode_steps_match_oracle_resident_and_lru_model(w2_tables):
     tier.close()
 
 
-def test_tiered_prefetch_workload5_shape(w2_tables):
+@pytest.mark.parametrize("fill", FILLS)
+def test_tiered_prefetch_workload5_shape(w2_tables, fill):
     """Decode at batch 64 over per-row token streams; each step prefetches the
     phrases of 8 predicted next tokens (true next token with p = 0.7) on a
     side stream; stats (including prefetch_used) follow the model exactly."""
     table, res, ot = w2_tables
     C, pre, B, K, steps = 8192, 4096, 64, 8, 10
-    tier = TieredTable(table, C, pre)
-    model = LruModel(C, pre, table.dim * 2)
+    tier = TieredTable(table, C, pre, fill=fill)
+    model = LruModel(C, pre, table.dim * 2, fill_rereads=fill == tfe.TFE_FILL_SIDE_STREAM)
     seqs = synth.zipf_tokens(1, 700, B * (steps + 3), 1.1).reshape(B, steps + 3)
     side = torch.cuda.Stream()
     for s in range(steps):
@@ -189,13 +196,14 @@ def test_tiny_cache_direct_reads_and_ring_compaction(w2_tables):
     tier.close()
 
 
-def test_multi_group_lookup_and_in_place(w2_tables):
+@pytest.mark.parametrize("fill", FILLS)
+def test_multi_group_lookup_and_in_place(w2_tables, fill):
     """3000 positions (three resolve groups of 1024) with many repeats, in
     place, against a cache that fits part of them."""
     table, res, ot = w2_tables
     C, pre = 1500, 700
-    tier = TieredTable(table, C, pre)
-    model = LruModel(C, pre, table.dim * 2)
+    tier = TieredTable(table, C, pre, fill=fill)
+    model = LruModel(C, pre, table.dim * 2, fill_rereads=fill == tfe.TFE_FILL_SIDE_STREAM)
     for step in range(3):
         batch = synth.decode_batch(1, 3000, set_index=60 + step)
         hidden = batch.hidden()
@@ -240,6 +248,7 @@ def test_tiered_load_errors():
         dict(hbm_cache_rows=8, prefill_rows=-1),
         dict(hbm_cache_rows=8, prefill_rows=0, adopt_host_values=1),  # pageable, not pinned
         dict(hbm_cache_rows=0, prefill_rows=0, adopt_host_values=1),  # adopt on a resident table
+        dict(hbm_cache_rows=8, prefill_rows=0, miss_fill=2),     # no such fill mode
     ]
     for kw in bad:
         desc = tfe.make_desc(table.tokens, table.lens, 2, 3, synth.V, vals, table.dim, table.dtype,

@@ -24,6 +24,9 @@ def test_workload5_full_scale_tiered_equals_resident_and_oracle():
     table = synth.config5_table()
     print("# table %d phrases (%.0f s)" % (table.n_phrases, time.time() - t0), flush=True)
     P, D, C, B, K, steps = table.n_phrases, table.dim, 4 << 20, 64, 8, 6
+    H.release_pinned()
+    held = torch.cuda.host_memory_stats().get("allocated_bytes.current", 0)
+    print("# pinned bytes still held by torch: %d" % held, flush=True)
     vals = torch.empty((P, D), dtype=torch.bfloat16, pin_memory=True)
     synth.normal_fill_device(synth.host_device_ptr(vals.data_ptr()), 0, P, D, table.seed,
                              synth.TAG_VALUES, table.sigma, synth.BF16, H.cur_stream())
@@ -65,3 +68,5 @@ def test_workload5_full_scale_tiered_equals_resident_and_oracle():
     assert hits > steps * B // 2
     tfe.tfe_table_free(tiered)
     resident.close()
+    del vals
+    H.release_pinned()

@@ -49,9 +49,14 @@ def test_statistics_definitions():
     assert m.stats["hits"] == 5
     assert m.stats["cache_hits"] == 2
     assert m.stats["cache_misses"] == 3
-    # host bytes: 2 rows filled + 3 positions served from host (5, 6, 5).
-    assert m.stats["host_bytes"] == 10 * (2 + 3)
+    # host bytes: 3 positions served from host (5, 6, 5); the fill copies the
+    # rows those reads brought in.
+    assert m.stats["host_bytes"] == 10 * 3
     assert set(m.resident()) == {0, 1, 5, 6}
+    # A fill that reads the rows again adds the 2 filled rows.
+    m2 = LruModel(4, 2, row_bytes=10, fill_rereads=True)
+    m2.lookup([0, 5, -1, 0, 6, 5])
+    assert m2.stats["host_bytes"] == 10 * (2 + 3)
     # Cache full; 7 evicts the least recent slot that is not referenced: row 1.
     m.lookup([7, 0])
     assert set(m.resident()) == {0, 5, 6, 7}
@@ -73,9 +78,13 @@ def test_groups_split_long_calls():
     m = LruModel(GROUP, 0, row_bytes=1)
     rows = list(range(GROUP)) + [0]
     m.lookup(rows)
-    # Row 0 was filled in the first group: cached when the second began.
+    # Row 0 was filled in the first group: cached when the second began, but
+    # still served from host memory (it was not cached when the call began).
     assert m.stats["cache_hits"] == 1
-    assert m.stats["host_bytes"] == GROUP + (GROUP + 1)
+    assert m.stats["host_bytes"] == GROUP + 1
+    m2 = LruModel(GROUP, 0, row_bytes=1, fill_rereads=True)
+    m2.lookup(rows)
+    assert m2.stats["host_bytes"] == GROUP + (GROUP + 1)
 
 
 def test_scored_prefetch_orders_by_score_and_respects_budget():
