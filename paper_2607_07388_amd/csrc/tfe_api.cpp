@@ -254,7 +254,8 @@ static tfe_status lookup_tiered(tfe_table* t, const LookupArgs& look, hipStream_
   t->clock++;
   tfe::TierArgs a = tier_args(t);
   a.look = look;
-  TFE_HIP(tfe::launch_tier_probe(a, stream), "tier probe");
+  const bool fused = tfe::lookup_resolve_fused(look.T);
+  if (!fused) TFE_HIP(tfe::launch_tier_probe(a, stream), "tier probe");
   if (t->prefetch_pending) {
     TFE_HIP(hipStreamWaitEvent(stream, t->ev_prefetch, 0), "wait prefetch");
     t->prefetch_pending = false;
@@ -262,7 +263,10 @@ static tfe_status lookup_tiered(tfe_table* t, const LookupArgs& look, hipStream_
   // The previous call's cache fill must land before this call reuses its
   // slots, and before the fill list is rewritten.
   if (t->fill_recorded) TFE_HIP(hipStreamWaitEvent(stream, t->ev_filled, 0), "wait fill");
-  TFE_HIP(tfe::launch_resolve_lookup(a, stream), "tier resolve");
+  if (fused)
+    TFE_HIP(tfe::launch_lookup_resolve_small(a, stream), "tier probe + resolve");
+  else
+    TFE_HIP(tfe::launch_resolve_lookup(a, stream), "tier resolve");
   if (t->fill_mode == TFE_FILL_SIDE_STREAM) {
     // Missed rows are copied into their new cache slots on the side stream,
     // overlapped with the injection, which reads them from host memory.

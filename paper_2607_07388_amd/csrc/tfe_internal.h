@@ -89,6 +89,9 @@ hipError_t launch_ring_compact(const TierArgs& t, uint64_t* dst, uint64_t dst_ma
                                hipStream_t s);
 hipError_t launch_tier_probe(const TierArgs& t, hipStream_t s);
 hipError_t launch_resolve_lookup(const TierArgs& t, hipStream_t s);
+// Decode-sized lookups: probe + resolve in one single-block launch.
+bool lookup_resolve_fused(uint32_t T);
+hipError_t launch_lookup_resolve_small(const TierArgs& t, hipStream_t s);
 hipError_t launch_prefetch_probe(const TierArgs& t, const int32_t* tail, int32_t tail_len,
                                  const int32_t* cand, uint32_t B, uint32_t K, hipStream_t s);
 hipError_t launch_resolve_prefetch(const TierArgs& t, uint32_t N, hipStream_t s);

@@ -35,43 +35,47 @@ using dev::u32x4;
 constexpr int kResolveThreads = 1024;
 constexpr int kHashSize = 2048;  // open-addressing dedupe table in LDS
 
-// Exclusive prefix sum of v over the block (kResolveThreads threads);
-// *total receives the block sum.  All threads must call it.
-__device__ uint32_t block_scan(uint32_t v, uint32_t* total) {
-  __shared__ uint32_t s_wave[kResolveThreads / 64 + 1];
-  const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
-  uint32_t x = v;
-#pragma unroll
-  for (int d = 1; d < 64; d <<= 1) {
-    const uint32_t y = __shfl_up(x, d, 64);
-    if (lane >= d) x += y;
-  }
-  if (lane == 63) s_wave[wave] = x;
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    uint32_t run = 0;
-    for (int w = 0; w < kResolveThreads / 64; ++w) {
-      const uint32_t t = s_wave[w];
-      s_wave[w] = run;
-      run += t;
-    }
-    s_wave[kResolveThreads / 64] = run;
-  }
-  __syncthreads();
-  const uint32_t res = x - v + s_wave[wave];
-  *total = s_wave[kResolveThreads / 64];
-  __syncthreads();
-  return res;
+constexpr int kWaves = kResolveThreads / 64;
+
+// Number of set bits of the ballot m in the lanes below this one.
+__device__ __forceinline__ uint32_t lanes_below(uint64_t m) {
+  return __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32),
+                                   __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
 }
 
-__device__ uint32_t block_min(uint32_t v) {
-  __shared__ uint32_t s_min;
-  if (threadIdx.x == 0) s_min = 0xFFFFFFFFu;
+// Block-wide count of a flag (kResolveThreads threads): returns how many
+// threads below this one have it set and the block total in *total.  A
+// ballot counts within each wave; every thread then adds the counts of the
+// waves before its own.  All threads must call it.
+__device__ uint32_t block_count(bool f, uint32_t* total) {
+  __shared__ uint32_t s_n[kWaves];
+  const int wave = threadIdx.x >> 6;
+  const uint64_t m = __builtin_amdgcn_ballot_w64(f);
+  if ((threadIdx.x & 63) == 0) s_n[wave] = (uint32_t)__builtin_popcountll(m);
   __syncthreads();
-  atomicMin(&s_min, v);
+  uint32_t before = 0, all = 0;
+#pragma unroll
+  for (int w = 0; w < kWaves; ++w) {
+    const uint32_t c = s_n[w];
+    before += w < wave ? c : 0u;
+    all += c;
+  }
   __syncthreads();
-  const uint32_t r = s_min;
+  *total = all;
+  return before + lanes_below(m);
+}
+
+// Lowest thread index whose flag is set, or 0xFFFFFFFF.  All threads must
+// call it.
+__device__ uint32_t block_first(bool f) {
+  __shared__ uint32_t s_f[kWaves];
+  const uint64_t m = __builtin_amdgcn_ballot_w64(f);
+  if ((threadIdx.x & 63) == 0)
+    s_f[threadIdx.x >> 6] = m ? (threadIdx.x & ~63u) + (uint32_t)__builtin_ctzll(m) : 0xFFFFFFFFu;
+  __syncthreads();
+  uint32_t r = 0xFFFFFFFFu;
+#pragma unroll
+  for (int w = 0; w < kWaves; ++w) r = min(r, s_f[w]);
   __syncthreads();
   return r;
 }
@@ -104,8 +108,8 @@ __device__ uint32_t pop_victims(const TierArgs& t, uint32_t need, uint32_t* vict
     const bool cur = in && st == t.clock;  // entries of this call end the search
     const bool live = in && !cur && t.stamp[slot] == st;
     uint32_t nlive;
-    const uint32_t rank = block_scan(live ? 1u : 0u, &nlive);
-    const uint32_t first_cur = block_min(cur ? threadIdx.x : 0xFFFFFFFFu);
+    const uint32_t rank = block_count(live, &nlive);
+    const uint32_t first_cur = block_first(cur);
     const uint32_t take = nlive < need - got ? nlive : need - got;
     if (live && rank < take) {
       vict[got + rank] = slot;
@@ -207,7 +211,7 @@ __global__ __launch_bounds__(kResolveThreads) void k_resolve_lookup(const TierAr
     __syncthreads();
     const bool miss_first = first && s0 < 0;
     uint32_t need;
-    const uint32_t mrank = block_scan(miss_first ? 1u : 0u, &need);
+    const uint32_t mrank = block_count(miss_first, &need);
     const uint32_t got = need ? pop_victims(t, need, vict) : 0;
     if (miss_first) {
       if (mrank < got) {
@@ -242,7 +246,7 @@ __global__ __launch_bounds__(kResolveThreads) void k_resolve_lookup(const TierAr
       }
     }
     uint32_t napp;
-    const uint32_t arank = block_scan(append ? 1u : 0u, &napp);
+    const uint32_t arank = block_count(append, &napp);
     if (append) t.ring[(s_head + arank) & t.ring_mask] = ring_entry((uint32_t)hslot[h], t.clock);
     __syncthreads();
     if (threadIdx.x == 0) {
@@ -263,6 +267,210 @@ __global__ __launch_bounds__(kResolveThreads) void k_resolve_lookup(const TierAr
     st.prefetch_used += s_cnt[2];
     st.host_bytes +=
         (unsigned long long)((t.fill_inline ? 0u : s_cnt[4]) + s_cnt[3]) * t.row_bytes;
+  }
+}
+
+// Decode-sized lookups (T <= kSmallT): probe and residency resolution in
+// one block, with the policy of k_resolve_lookup for a single group.  The
+// kernel reads everything it needs first, decides in LDS, and writes last,
+// so no store ever holds up a load:
+//   reads: two chains side by side in every wave -- tokens -> buckets -> the
+//     matched rows' `where` -> their `pref` flags for the wave's positions,
+//     and the ring cursors -> one entry of the least-recent window of the
+//     recency ring per thread -> that slot's stamp and owner;
+//   decisions: dedupe, the set of slots this call references, victims from
+//     the window (an entry is live if its stamp still matches and its slot
+//     is not referenced), all in LDS;
+//   writes: outputs, residency, recency appends, counters.
+// If the window holds too few live entries the block falls back to
+// pop_victims, after writing this call's stamps for it to see.
+constexpr uint32_t kSmallT = 64;
+constexpr int kSmallPer = (int)kSmallT / kWaves;  // positions per wave
+constexpr int kRefHash = 128;                     // referenced-slot set
+
+__device__ __forceinline__ uint32_t slot_hash(uint32_t s) { return (s * 2654435761u) >> 25; }
+
+__global__ __launch_bounds__(kResolveThreads) void k_lookup_resolve_small(const TierArgs t) {
+  const LookupArgs& a = t.look;
+  const uint32_t T = a.T;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  __shared__ int32_t s_row[kSmallT];
+  __shared__ int32_t s_where[kSmallT];
+  __shared__ uint8_t s_len[kSmallT];
+  __shared__ uint8_t s_pref[kSmallT];
+  __shared__ int32_t hkey[kHashSize];
+  __shared__ uint32_t hpos[kHashSize];
+  __shared__ int32_t hslot[kHashSize];
+  __shared__ uint8_t hphase[kHashSize];
+  __shared__ int32_t rset[kRefHash];
+  __shared__ uint32_t vict[kResolveThreads];
+  __shared__ int32_t vown[kResolveThreads];
+  __shared__ uint32_t s_cnt[4];  // hits, cache hits, prefetch used, host-served
+  __shared__ unsigned long long s_last;
+  if (threadIdx.x < kRefHash) rset[threadIdx.x] = -1;
+  if (threadIdx.x < 4) s_cnt[threadIdx.x] = 0;
+
+  // ---- reads.  Round 1: ring cursors, counters (no other kernel touches the
+  // table's state while this one runs), the tokens of the wave's positions.
+  const unsigned long long tail0 = t.ctl->tail, head0 = t.ctl->head;
+  const TierStats st0 = t.ctl->stats;
+  int32_t tw[kSmallPer][4];
+#pragma unroll
+  for (int k = 0; k < kSmallPer; ++k)
+    dev::window_tokens(a, (uint32_t)(wave + kWaves * k), tw[k]);  // beyond T: invalid
+  // Round 2: one ring entry per thread; the first bucket of every key.
+  const unsigned long long wi = tail0 + threadIdx.x;
+  const bool win = wi < head0;
+  const uint64_t e = win ? t.ring[wi & t.ring_mask] : 0;
+  dev::Probe pr[kSmallPer];
+#pragma unroll
+  for (int k = 0; k < kSmallPer; ++k) pr[k] = dev::probe_begin(a, tw[k], lane);
+  // Round 3: the entry's slot state; the matches (lane k of the wave holds
+  // position wave + kWaves k) and their residency.
+  const uint32_t eslot = (uint32_t)(e >> 32), est = (uint32_t)e;
+  const uint32_t estamp = win ? t.stamp[eslot] : 0u;
+  const int32_t eowner = win ? t.owner[eslot] : -1;
+  int32_t myrow = -1;
+  int mylen = 0;
+#pragma unroll
+  for (int k = 0; k < kSmallPer; ++k) {
+    int len;
+    const int32_t row = dev::probe_finish(a, pr[k], lane, &len);
+    if (lane == k) {
+      myrow = row;
+      mylen = len;
+    }
+  }
+  const int32_t mywhere = myrow >= 0 ? t.where[myrow] : -1;
+  // Round 4: prefetched flags of the cached matches.
+  const uint8_t mypref = mywhere >= 0 ? t.pref[mywhere] : (uint8_t)0;
+  if (lane < kSmallPer && wave + kWaves * lane < (int)T) {
+    const uint32_t q = wave + kWaves * lane;
+    s_row[q] = myrow;
+    s_len[q] = (uint8_t)mylen;
+    s_where[q] = mywhere;
+    s_pref[q] = mypref;
+  }
+  __syncthreads();
+
+  // ---- decisions (LDS).  Dedupe; cached first occurrences are referenced.
+  const uint32_t p = threadIdx.x;
+  const bool valid = p < T;
+  const int32_t r = valid ? s_row[p] : -1;
+  int h;
+  const bool first = first_of_row(r, p, hkey, hpos, &h);
+  const int32_t s0 = first ? s_where[p] : -1;
+  bool append = false;
+  if (s0 >= 0) {
+    append = true;
+    hslot[h] = s0;
+    hphase[h] = 0;
+    if (s_pref[p]) atomicAdd(&s_cnt[2], 1u);
+    int q = (int)slot_hash((uint32_t)s0);
+    while (atomicCAS(&rset[q], -1, s0) != -1) q = (q + 1) & (kRefHash - 1);
+  }
+  const bool miss_first = first && s0 < 0;
+  uint32_t need;
+  const uint32_t mrank = block_count(miss_first, &need);  // its barrier publishes rset
+  bool referenced = false;
+  if (win) {
+    for (int q = (int)slot_hash(eslot);; q = (q + 1) & (kRefHash - 1)) {
+      const int32_t v = rset[q];
+      if (v == -1) break;
+      if ((uint32_t)v == eslot) {
+        referenced = true;
+        break;
+      }
+    }
+  }
+  const bool cur = win && est == t.clock;
+  const bool live = win && !cur && estamp == est && !referenced;
+  uint32_t nlive;
+  const uint32_t lrank = block_count(live, &nlive);
+  const uint32_t first_cur = block_first(cur);
+  const bool window_ends = first_cur != 0xFFFFFFFFu || tail0 + kResolveThreads >= head0;
+  const bool fast = need == 0 || nlive >= need || window_ends;
+  uint32_t got = 0;
+  if (fast) {
+    got = nlive < need ? nlive : need;
+    if (live && lrank < got) {
+      vict[lrank] = eslot;
+      vown[lrank] = eowner;
+      if (lrank == got - 1) s_last = wi;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0 && need > 0) {
+      if (got == need) t.ctl->tail = s_last + 1;
+      else if (first_cur != 0xFFFFFFFFu) t.ctl->tail = tail0 + first_cur;
+      else t.ctl->tail = head0;
+    }
+  } else {
+    // The ring walk reads stamps: make this call's references visible first.
+    if (s0 >= 0) t.stamp[s0] = t.clock;
+    __threadfence_block();
+    __syncthreads();
+    got = pop_victims(t, need, vict);
+  }
+  bool writes = false;
+  uint32_t v = 0;
+  int32_t old = -1;
+  if (miss_first) {
+    if (mrank < got) {
+      v = vict[mrank];
+      old = fast ? vown[mrank] : t.owner[v];
+      hslot[h] = (int32_t)v;
+      hphase[h] = 1;
+      append = true;
+      writes = t.fill_inline != 0;
+    } else {
+      hslot[h] = -1;
+      hphase[h] = 2;
+    }
+  }
+  __syncthreads();
+
+  // ---- writes.
+  if (s0 >= 0) {
+    t.stamp[s0] = t.clock;
+    if (s_pref[p]) t.pref[s0] = 0;
+  }
+  if (miss_first && mrank < got) {
+    if (old >= 0) t.where[old] = -1;
+    t.owner[v] = r;
+    t.where[r] = (int32_t)v;
+    t.stamp[v] = t.clock;
+    t.filled_at[v] = t.clock;
+    t.pref[v] = 0;
+    t.jobs[mrank] = TierJob{r, (int32_t)v};
+  }
+  if (valid) {
+    const int32_t s1 = r >= 0 ? hslot[h] : -1;
+    const uint8_t ph = r >= 0 ? hphase[h] : 3;
+    dev::write_result(a, p, r, s_len[p]);
+    t.row_of[p] = r;
+    t.slot_of[p] = s1;
+    t.phase[p] = writes ? (uint8_t)(ph | kPhaseWrite) : ph;
+    if (r >= 0) {
+      atomicAdd(&s_cnt[0], 1u);
+      if (ph == 0) atomicAdd(&s_cnt[1], 1u);
+      else atomicAdd(&s_cnt[3], 1u);
+    }
+  }
+  uint32_t napp;
+  const uint32_t arank = block_count(append, &napp);
+  if (append) t.ring[(head0 + arank) & t.ring_mask] = ring_entry((uint32_t)hslot[h], t.clock);
+  if (threadIdx.x == 0) {
+    t.ctl->head = head0 + napp;
+    t.ctl->njobs = got;
+    TierStats st = st0;
+    st.positions += T;
+    st.hits += s_cnt[0];
+    st.cache_hits += s_cnt[1];
+    st.cache_misses += s_cnt[0] - s_cnt[1];
+    st.prefetch_used += s_cnt[2];
+    st.host_bytes += (unsigned long long)((t.fill_inline ? 0u : got) + s_cnt[3]) * t.row_bytes;
+    t.ctl->stats = st;
   }
 }
 
@@ -288,7 +496,7 @@ __global__ __launch_bounds__(kResolveThreads) void k_resolve_prefetch(const Tier
     // A row filled by an earlier group of this prefetch is cached by now.
     const bool miss_first = first && r >= 0 && !s_stop && t.where[r] < 0;
     uint32_t need;
-    const uint32_t mrank = block_scan(miss_first ? 1u : 0u, &need);
+    const uint32_t mrank = block_count(miss_first, &need);
     const uint32_t got = need ? pop_victims(t, need, vict) : 0;
     if (miss_first && mrank < got) {
       const uint32_t v = vict[mrank];
@@ -303,7 +511,7 @@ __global__ __launch_bounds__(kResolveThreads) void k_resolve_prefetch(const Tier
       t.ring[(t.ctl->head + mrank) & t.ring_mask] = ring_entry(v, t.clock);
     }
     uint32_t c_found;
-    block_scan(r >= 0 ? 1u : 0u, &c_found);
+    block_count(r >= 0, &c_found);
     if (threadIdx.x == 0) {
       t.ctl->head += got;
       t.ctl->njobs += got;
@@ -565,7 +773,7 @@ __global__ __launch_bounds__(kResolveThreads) void k_ring_compact(const TierArgs
     const uint64_t e = in ? t.ring[i & t.ring_mask] : 0;
     const bool live = in && t.stamp[(uint32_t)(e >> 32)] == (uint32_t)e;
     uint32_t n;
-    const uint32_t rank = block_scan(live ? 1u : 0u, &n);
+    const uint32_t rank = block_count(live, &n);
     if (live) dst[(s_out + rank) & dst_mask] = e;
     __syncthreads();
     if (threadIdx.x == 0) s_out += n;
@@ -609,6 +817,13 @@ hipError_t launch_ring_compact(const TierArgs& t, uint64_t* dst, uint64_t dst_ma
 hipError_t launch_tier_probe(const TierArgs& t, hipStream_t s) {
   if (t.look.T == 0) return hipSuccess;
   hipLaunchKernelGGL(k_tier_probe<1>, dim3(t.look.T), dim3(64), 0, s, t);
+  return hipGetLastError();
+}
+
+bool lookup_resolve_fused(uint32_t T) { return T <= kSmallT; }
+
+hipError_t launch_lookup_resolve_small(const TierArgs& t, hipStream_t s) {
+  hipLaunchKernelGGL(k_lookup_resolve_small, dim3(1), dim3(kResolveThreads), 0, s, t);
   return hipGetLastError();
 }
 
