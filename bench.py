@@ -66,10 +66,22 @@ KERNEL_SOURCES = ("paper_2607_07388_amd/csrc/tfe_lookup.hip",
                   "paper_2607_07388_amd/csrc/tfe_index.h")
 
 
-def kernel_sources_sha256():
+# The same for one call of the early-exit head (W 151936 x 1024 bf16, 64 rows,
+# K = 128): k_head_logits + k_head_rows, from the passes in
+# profiles/k_head_logits_rows_v151936_d1024_b64_k128.md.
+PROFILED_TRAFFIC_HEAD = {
+    "sources_sha256": "eadfccbe994d094a1e919986451edfc7f6664f35b69483d3249b6c58863a2e7b",
+    "bytes_per_launch": 372549456,
+}
+HEAD_SOURCES = ("paper_2607_07388_amd/csrc/tfe_head.hip",
+                "paper_2607_07388_amd/csrc/tfe_head.h",
+                "paper_2607_07388_amd/csrc/tfe_head_api.cpp")
+
+
+def kernel_sources_sha256(files=KERNEL_SOURCES):
     import hashlib
     h = hashlib.sha256()
-    for f in KERNEL_SOURCES:
+    for f in files:
         with open(os.path.join(ROOT, f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()
@@ -543,7 +555,10 @@ def run_head(args):
             "peak": HBM_PEAK_GBPS,
             "unit": "GB/s",
             "frac": nbytes / avg / 1e9 / HBM_PEAK_GBPS,
-            "traffic": None,
+            "traffic": (PROFILED_TRAFFIC_HEAD["bytes_per_launch"]
+                        if kernel_sources_sha256(HEAD_SOURCES) ==
+                        PROFILED_TRAFFIC_HEAD["sources_sha256"] and (V, Dh, B, K) ==
+                        (151936, 1024, 64, 128) else None),
             "bytes_per_launch": nbytes,
             "avg_launch_us": avg * 1e6,
             "mfma_tflops": flops / avg / 1e12,
