@@ -260,11 +260,19 @@ tfe_status tfe_head_free(tfe_head *head);
  *   out_counts  DEVICE int64 [top]
  *   written     HOST: number of ranks written (fewer than top when the
  *               stream has fewer than skip + top distinct tuples)
- * Synchronous: returns once the outputs are complete.  Allocates its
- * scratch (about 20 bytes per token) for the duration of the call. */
+ * Synchronous: returns once the outputs are complete.  Its scratch (device
+ * memory of the current device: about 20 bytes per token, 40 for 4-grams)
+ * stays with the library after the call and is reused by later calls of a
+ * similar size, until tfe_ngram_release; a call that finds no fitting idle
+ * buffer first returns the idle ones.  Safe to call from several host
+ * threads (each call takes buffers of its own). */
 tfe_status tfe_ngram_top(const int32_t *tokens, int64_t n_tokens, int32_t vocab, int32_t n,
                          int64_t skip, int64_t top, int32_t *out_tuples, int64_t *out_counts,
                          int64_t *written, void *stream);
+
+/* Returns the idle scratch that tfe_ngram_top keeps for reuse (all devices)
+ * to the device allocator.  Buffers of calls still running are kept. */
+tfe_status tfe_ngram_release(void);
 
 /* Copies the table's counters (synchronises with the table's pending work). */
 tfe_status tfe_get_stats(tfe_table *table, tfe_stats *out);

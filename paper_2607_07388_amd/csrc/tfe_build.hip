@@ -30,6 +30,7 @@
 #include <stdint.h>
 
 #include <algorithm>
+#include <mutex>
 #include <vector>
 
 #include "../../include/tfe.h"
@@ -38,10 +39,20 @@
 namespace tfe {
 namespace {
 
-constexpr int kTileThreads = 256;
-constexpr int kTileItems = 16;
-constexpr int kTile = kTileThreads * kTileItems;  // keys per radix tile
-constexpr int kWaves = kTileThreads / 64;
+// Radix tiles: the scatter runs 512 threads per tile (two tiles share a CU,
+// so one's ranking overlaps the other's memory traffic), 16 keys per thread
+// for keys alone and 8 with a 64-bit payload (the tile's reorder buffer in
+// LDS: 64 KiB).  Longer tiles give longer digit runs, i.e. better coalesced
+// writes; measured on MI355X, 8192 keys x 512 threads beat 4096 x 256 and
+// 16384 x 1024.  The histogram of a tile is counted by 1024 threads.
+constexpr int kTileThreads = 512;
+constexpr int kTileWaves = kTileThreads / 64;
+constexpr int kHistThreads = 1024;
+template <class K, bool PAIRS>
+constexpr int tile_items() { return (sizeof(K) + (PAIRS ? 8 : 0)) > 8 ? 8 : 16; }
+template <class K, bool PAIRS>
+constexpr int tile_keys() { return kTileThreads * tile_items<K, PAIRS>(); }
+constexpr int kMinTile = kTileThreads * 8;  // smallest tile: sizes the histogram matrix
 constexpr int kScanThreads = 1024;
 constexpr int kScanItems = 16;
 constexpr int kScanBlock = kScanThreads * kScanItems;
@@ -172,19 +183,51 @@ __global__ __launch_bounds__(kScanThreads) void k_scan_partials(uint32_t* part, 
   if (threadIdx.x == 0 && total) *total = tot;
 }
 
-// Pass 3: scan within blocks plus the block offset.
+// Inclusive sum over the lanes up to this one: DPP shifts within each
+// 16-lane row, then the totals of the rows below (read out as scalars).
+__device__ __forceinline__ uint32_t wave_incl_scan(uint32_t x) {
+  const int lane = threadIdx.x & 63;
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x111, 0xF, 0xF, false);  // row_shr:1
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x112, 0xF, 0xF, false);  // row_shr:2
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x114, 0xF, 0xF, false);  // row_shr:4
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x118, 0xF, 0xF, false);  // row_shr:8
+  const uint32_t r0 = (uint32_t)__builtin_amdgcn_readlane((int)x, 15);
+  const uint32_t r1 = (uint32_t)__builtin_amdgcn_readlane((int)x, 31);
+  const uint32_t r2 = (uint32_t)__builtin_amdgcn_readlane((int)x, 47);
+  const int row = lane >> 4;
+  return x + (row >= 1 ? r0 : 0u) + (row >= 2 ? r1 : 0u) + (row >= 3 ? r2 : 0u);
+}
+
+// Pass 3: scan within blocks plus the block offset.  Wave w of a block scans
+// its contiguous kScanItems x 64 elements in rounds of 64 (coalesced), with
+// a running carry; one exchange of wave totals places the waves.
 __global__ __launch_bounds__(kScanThreads) void k_scan_down(const uint32_t* in, uint64_t n,
                                                             const uint32_t* part, uint32_t* out) {
-  __shared__ uint32_t s_wave[kScanThreads / 64];
-  const uint64_t base = (uint64_t)blockIdx.x * kScanBlock;
-  uint32_t run = part[blockIdx.x];
+  __shared__ uint32_t s_tot[kScanThreads / 64];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const uint64_t base = (uint64_t)blockIdx.x * kScanBlock + (uint64_t)wave * (64 * kScanItems);
+  uint32_t v[kScanItems];
+#pragma unroll
   for (int k = 0; k < kScanItems; ++k) {
-    const uint64_t i = base + (uint64_t)k * kScanThreads + threadIdx.x;
-    const uint32_t v = i < n ? in[i] : 0u;
-    uint32_t tot;
-    const uint32_t ex = block_scan_excl<kScanThreads>(v, s_wave, &tot);
-    if (i < n) out[i] = run + ex;
-    run += tot;
+    const uint64_t i = base + (uint64_t)k * 64 + lane;
+    v[k] = i < n ? in[i] : 0u;
+  }
+  uint32_t carry = 0;
+#pragma unroll
+  for (int k = 0; k < kScanItems; ++k) {
+    const uint32_t inc = wave_incl_scan(v[k]);
+    const uint32_t ex = carry + inc - v[k];
+    carry += (uint32_t)__builtin_amdgcn_readlane((int)inc, 63);
+    v[k] = ex;
+  }
+  if (lane == 0) s_tot[wave] = carry;
+  __syncthreads();
+  uint32_t off = part[blockIdx.x];
+  for (int w = 0; w < wave; ++w) off += s_tot[w];
+#pragma unroll
+  for (int k = 0; k < kScanItems; ++k) {
+    const uint64_t i = base + (uint64_t)k * 64 + lane;
+    if (i < n) out[i] = off + v[k];
   }
 }
 
@@ -193,21 +236,6 @@ __global__ __launch_bounds__(kScanThreads) void k_scan_down(const uint32_t* in, 
 template <class K>
 __device__ __forceinline__ uint32_t digit_of(K k, int shift) {
   return (uint32_t)(k >> shift) & 255u;
-}
-
-template <class K>
-__global__ __launch_bounds__(kTileThreads) void k_rs_hist(const K* keys, uint64_t n, int shift,
-                                                          uint32_t* hist, uint32_t ntiles) {
-  __shared__ uint32_t h[256];
-  h[threadIdx.x] = 0u;
-  __syncthreads();
-  const uint64_t base = (uint64_t)blockIdx.x * kTile;
-  for (int k = 0; k < kTileItems; ++k) {
-    const uint64_t i = base + (uint64_t)k * kTileThreads + threadIdx.x;
-    if (i < n) atomicAdd(&h[digit_of(keys[i], shift)], 1u);
-  }
-  __syncthreads();
-  hist[(size_t)threadIdx.x * ntiles + blockIdx.x] = h[threadIdx.x];
 }
 
 // Lanes of the wave whose 8-bit digit equals this lane's (active lanes only).
@@ -221,37 +249,68 @@ __device__ __forceinline__ uint64_t match_digit(uint32_t d, bool active) {
   return m;
 }
 
-// Scatter of one tile.  Wave w ranks the keys [w 1024, (w+1) 1024) of the
-// tile in 16 rounds of 64 consecutive keys: the rank of a key among the
-// wave's earlier keys of its digit is the wave's running count plus the
-// matching lanes below it; the first lane of each digit group advances the
-// count.  Tile positions follow (digit, wave, rank), i.e. the stable order.
-template <class K, bool PAIRS>
+// Digit histogram of one tile of TILE keys (kHistThreads threads; the keys
+// are loaded first).  Plain LDS atomics: on MI355X they beat counting each
+// group of equal digits once, also for skewed digits.
+template <class K, int TILE>
+__global__ __launch_bounds__(kHistThreads) void k_rs_hist(const K* keys, uint64_t n, int shift,
+                                                          uint32_t* hist, uint32_t ntiles) {
+  constexpr int ITEMS = TILE / kHistThreads;
+  __shared__ uint32_t h[256];
+  for (int e = threadIdx.x; e < 256; e += kHistThreads) h[e] = 0u;
+  const uint64_t base = (uint64_t)blockIdx.x * TILE;
+  K kk[ITEMS];
+#pragma unroll
+  for (int k = 0; k < ITEMS; ++k) {
+    const uint64_t i = base + (uint64_t)k * kHistThreads + threadIdx.x;
+    kk[k] = i < n ? keys[i] : (K)0;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int k = 0; k < ITEMS; ++k)
+    if (base + (uint64_t)k * kHistThreads + threadIdx.x < n)
+      atomicAdd(&h[digit_of(kk[k], shift)], 1u);
+  __syncthreads();
+  for (int e = threadIdx.x; e < 256; e += kHistThreads)
+    hist[(size_t)e * ntiles + blockIdx.x] = h[e];
+}
+
+// Scatter of one tile.  Wave w ranks the keys [w 64 ITEMS, (w+1) 64 ITEMS)
+// of the tile in ITEMS rounds of 64 consecutive keys: the rank of a key
+// among the wave's earlier keys of its digit is the wave's running count
+// plus the matching lanes below it; the first lane of each digit group
+// advances the count.  Tile positions follow (digit, wave, rank), i.e. the
+// stable order; the tile is reordered in LDS and written in digit runs.
+template <class K, bool PAIRS, int ITEMS>
 __global__ __launch_bounds__(kTileThreads) void k_rs_scatter(const K* keys, const uint64_t* vals,
                                                              uint64_t n, int shift,
                                                              const uint32_t* offs,
                                                              uint32_t ntiles, K* keys_out,
                                                              uint64_t* vals_out) {
-  __shared__ uint32_t wcnt[kWaves][256];
-  __shared__ uint32_t s_loc[256];  // tile-local start of each digit
-  __shared__ uint32_t s_glob[256]; // global start of each digit's run of this tile
-  __shared__ uint32_t s_wave[kWaves];
-  __shared__ K s_keys[kTile];
-  __shared__ uint64_t s_vals[PAIRS ? kTile : 1];
+  constexpr int TILE = kTileThreads * ITEMS;
+  __shared__ uint32_t wcnt[kTileWaves][256];
+  __shared__ uint32_t s_loc[256];   // tile-local start of each digit
+  __shared__ uint32_t s_glob[256];  // global start of each digit's run of this tile
+  __shared__ uint32_t s_wave[kTileWaves];
+  __shared__ K s_keys[TILE];
+  __shared__ uint64_t s_vals[PAIRS ? TILE : 1];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  for (int e = threadIdx.x; e < kWaves * 256; e += kTileThreads) (&wcnt[0][0])[e] = 0u;
-  __syncthreads();
-  const uint64_t base = (uint64_t)blockIdx.x * kTile + (uint64_t)wave * (64 * kTileItems);
+  for (int e = threadIdx.x; e < kTileWaves * 256; e += kTileThreads) (&wcnt[0][0])[e] = 0u;
+  const uint64_t base = (uint64_t)blockIdx.x * TILE + (uint64_t)wave * (64 * ITEMS);
   const uint64_t lt = (1ull << lane) - 1ull;
-  K kk[kTileItems];
-  uint64_t vv[PAIRS ? kTileItems : 1];
-  uint32_t rank[kTileItems];
+  K kk[ITEMS];
+  uint64_t vv[PAIRS ? ITEMS : 1];
+  uint32_t rank[ITEMS];
 #pragma unroll
-  for (int r = 0; r < kTileItems; ++r) {
+  for (int r = 0; r < ITEMS; ++r) {
     const uint64_t i = base + (uint64_t)r * 64 + lane;
-    const bool act = i < n;
-    kk[r] = act ? keys[i] : (K)0;
-    if (PAIRS) vv[PAIRS ? r : 0] = act ? vals[i] : 0ull;
+    kk[r] = i < n ? keys[i] : (K)0;
+    if (PAIRS) vv[PAIRS ? r : 0] = i < n ? vals[i] : 0ull;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int r = 0; r < ITEMS; ++r) {
+    const bool act = base + (uint64_t)r * 64 + lane < n;
     const uint32_t d = digit_of(kk[r], shift);
     const uint64_t m = match_digit(d, act);
     const uint32_t before = wcnt[wave][d];
@@ -260,21 +319,26 @@ __global__ __launch_bounds__(kTileThreads) void k_rs_scatter(const K* keys, cons
     if (act && (m & lt) == 0) wcnt[wave][d] = before + (uint32_t)__builtin_popcountll(m);
   }
   __syncthreads();
-  // Per digit: counts of earlier waves, the tile's digit starts.
+  // Per digit (threads below 256): counts of earlier waves, the tile's digit
+  // starts.
   const uint32_t d = threadIdx.x;
   uint32_t tot = 0;
-  for (int w = 0; w < kWaves; ++w) {
-    const uint32_t c = wcnt[w][d];
-    wcnt[w][d] = tot;  // becomes the offset of wave w within the digit
-    tot += c;
+  if (d < 256) {
+    for (int w = 0; w < kTileWaves; ++w) {
+      const uint32_t c = wcnt[w][d];
+      wcnt[w][d] = tot;  // becomes the offset of wave w within the digit
+      tot += c;
+    }
   }
   uint32_t all;
   const uint32_t loc = block_scan_excl<kTileThreads>(tot, s_wave, &all);
-  s_loc[d] = loc;
-  s_glob[d] = offs[(size_t)d * ntiles + blockIdx.x];
+  if (d < 256) {
+    s_loc[d] = loc;
+    s_glob[d] = offs[(size_t)d * ntiles + blockIdx.x];
+  }
   __syncthreads();
 #pragma unroll
-  for (int r = 0; r < kTileItems; ++r) {
+  for (int r = 0; r < ITEMS; ++r) {
     const uint64_t i = base + (uint64_t)r * 64 + lane;
     if (i < n) {
       const uint32_t dd = digit_of(kk[r], shift);
@@ -284,8 +348,8 @@ __global__ __launch_bounds__(kTileThreads) void k_rs_scatter(const K* keys, cons
     }
   }
   __syncthreads();
-  const uint64_t tile0 = (uint64_t)blockIdx.x * kTile;
-  const uint32_t cnt = (uint32_t)min((uint64_t)kTile, n - tile0);
+  const uint64_t tile0 = (uint64_t)blockIdx.x * TILE;
+  const uint32_t cnt = (uint32_t)min((uint64_t)TILE, n - tile0);
   for (uint32_t p = threadIdx.x; p < cnt; p += kTileThreads) {
     const K k = s_keys[p];
     const uint32_t dd = digit_of(k, shift);
@@ -421,34 +485,95 @@ hipError_t scan_u32(const uint32_t* in, uint32_t* out, uint64_t n, uint32_t* par
   return hipGetLastError();
 }
 
+// hist holds 256 x ceil(n / kMinTile) entries.
 template <class K, bool PAIRS>
 hipError_t radix_sort(K*& keys, K*& keys_alt, uint64_t*& vals, uint64_t*& vals_alt, uint64_t n,
                       int bits, uint32_t* hist, uint32_t* part, hipStream_t s) {
-  const uint32_t ntiles = blocks_for(n, kTile);
+  constexpr int ITEMS = tile_items<K, PAIRS>();
+  const uint32_t ntiles = blocks_for(n, tile_keys<K, PAIRS>());
   if (ntiles == 0) return hipSuccess;
   for (int shift = 0; shift < bits; shift += 8) {
-    hipLaunchKernelGGL((k_rs_hist<K>), dim3(ntiles), dim3(kTileThreads), 0, s, keys, n, shift,
-                       hist, ntiles);
+    hipLaunchKernelGGL((k_rs_hist<K, tile_keys<K, PAIRS>()>), dim3(ntiles), dim3(kHistThreads), 0,
+                       s, keys, n, shift, hist, ntiles);
     hipError_t e = scan_u32(hist, hist, (uint64_t)256 * ntiles, part, nullptr, s);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL((k_rs_scatter<K, PAIRS>), dim3(ntiles), dim3(kTileThreads), 0, s, keys,
-                       vals, n, shift, hist, ntiles, keys_alt, vals_alt);
+    hipLaunchKernelGGL((k_rs_scatter<K, PAIRS, ITEMS>), dim3(ntiles), dim3(kTileThreads), 0, s,
+                       keys, vals, n, shift, hist, ntiles, keys_alt, vals_alt);
     std::swap(keys, keys_alt);
     if (PAIRS) std::swap(vals, vals_alt);
   }
   return hipGetLastError();
 }
 
+// Scratch of the construction: device buffers kept for reuse by later calls
+// (a hipMalloc / hipFree pair costs about 25 / 150 us per buffer and
+// synchronises the device; a construction takes a dozen buffers) until
+// tfe_ngram_release.  A request takes the smallest idle buffer of the device
+// that holds it without wasting more than half; on a miss the device's idle
+// buffers are returned first, so the cache never holds more than the calls
+// in flight plus the buffers of one call.
+struct CachedBuf {
+  void* p;
+  size_t bytes;
+  int device;
+  bool used;
+};
+std::mutex g_cache_mu;
+std::vector<CachedBuf> g_cache;
+
+void* cache_get(int device, size_t bytes) {
+  constexpr size_t kGrain = (size_t)2 << 20;
+  std::lock_guard<std::mutex> lock(g_cache_mu);
+  int best = -1;
+  for (size_t i = 0; i < g_cache.size(); ++i) {
+    const CachedBuf& c = g_cache[i];
+    if (!c.used && c.device == device && c.bytes >= bytes && c.bytes <= 2 * bytes + kGrain &&
+        (best < 0 || c.bytes < g_cache[(size_t)best].bytes))
+      best = (int)i;
+  }
+  if (best >= 0) {
+    g_cache[(size_t)best].used = true;
+    return g_cache[(size_t)best].p;
+  }
+  for (size_t i = 0; i < g_cache.size();) {
+    if (!g_cache[i].used && g_cache[i].device == device) {
+      (void)hipFree(g_cache[i].p);
+      g_cache[i] = g_cache.back();
+      g_cache.pop_back();
+    } else {
+      ++i;
+    }
+  }
+  const size_t rounded = (bytes + kGrain - 1) / kGrain * kGrain;
+  void* p = nullptr;
+  if (hipMalloc(&p, rounded) != hipSuccess) {
+    (void)hipGetLastError();
+    return nullptr;
+  }
+  g_cache.push_back(CachedBuf{p, rounded, device, true});
+  return p;
+}
+
+void cache_put(void* p) {
+  std::lock_guard<std::mutex> lock(g_cache_mu);
+  for (CachedBuf& c : g_cache)
+    if (c.p == p) c.used = false;
+}
+
 struct Scratch {
+  hipStream_t s;
+  int device = 0;
   std::vector<void*> bufs;
+  explicit Scratch(hipStream_t stream) : s(stream) { (void)hipGetDevice(&device); }
   ~Scratch() {
-    for (void* p : bufs) (void)hipFree(p);
+    // Idle only once the stream is done with them (error paths return early).
+    (void)hipStreamSynchronize(s);
+    for (void* p : bufs) cache_put(p);
   }
   template <class T>
   T* get(uint64_t count) {
-    void* p = nullptr;
-    if (hipMalloc(&p, std::max<uint64_t>(count, 1) * sizeof(T)) != hipSuccess) return nullptr;
-    bufs.push_back(p);
+    void* p = cache_get(device, std::max<uint64_t>(count, 1) * sizeof(T));
+    if (p) bufs.push_back(p);
     return (T*)p;
   }
 };
@@ -474,14 +599,14 @@ tfe_status ngram_top(const int32_t* tokens, int64_t N, int32_t vocab, int32_t n,
     return fail(TFE_ERR_INVALID_ARG, "null tokens or outputs");
   const uint64_t nwin = (uint64_t)(N - n + 1);
   const bool wide = n == 4;
-  Scratch sc;
+  Scratch sc(s);
   uint64_t* keys = sc.get<uint64_t>(nwin);
   uint64_t* keys_alt = sc.get<uint64_t>(nwin);
   uint64_t* wv = wide ? sc.get<uint64_t>(nwin) : nullptr;      // 4-grams: high word payload
   uint64_t* wv_alt = wide ? sc.get<uint64_t>(nwin) : nullptr;
   uint32_t* hi = wide ? sc.get<uint32_t>(nwin) : nullptr;      // 4-grams: high word keys
   uint32_t* hi_alt = wide ? sc.get<uint32_t>(nwin) : nullptr;
-  const uint32_t ntiles = blocks_for(nwin, kTile);
+  const uint32_t ntiles = blocks_for(nwin, kMinTile);
   uint32_t* hist = sc.get<uint32_t>((uint64_t)256 * ntiles);
   uint32_t* part = sc.get<uint32_t>(kScanBlock);
   unsigned long long* d_count = sc.get<unsigned long long>(1);
@@ -584,6 +709,25 @@ tfe_status ngram_top(const int32_t* tokens, int64_t N, int32_t vocab, int32_t n,
 
 }  // namespace
 }  // namespace tfe
+
+extern "C" tfe_status tfe_ngram_release(void) {
+  tfe::clear_error();
+  std::lock_guard<std::mutex> lock(tfe::g_cache_mu);
+  int cur = 0;
+  (void)hipGetDevice(&cur);
+  for (size_t i = 0; i < tfe::g_cache.size();) {
+    if (!tfe::g_cache[i].used) {
+      (void)hipSetDevice(tfe::g_cache[i].device);
+      (void)hipFree(tfe::g_cache[i].p);
+      tfe::g_cache[i] = tfe::g_cache.back();
+      tfe::g_cache.pop_back();
+    } else {
+      ++i;
+    }
+  }
+  (void)hipSetDevice(cur);
+  return TFE_OK;
+}
 
 extern "C" tfe_status tfe_ngram_top(const int32_t* tokens, int64_t n_tokens, int32_t vocab,
                                     int32_t n, int64_t skip, int64_t top, int32_t* out_tuples,

@@ -76,6 +76,7 @@ def _load():
         "tfe_head_create": ([vp, i32, i32, i32, i32, ctypes.POINTER(vp)], ctypes.c_int),
         "tfe_head_topk": ([vp, vp, i32, i32, vp, vp, vp], ctypes.c_int),
         "tfe_head_free": ([vp], ctypes.c_int),
+        "tfe_ngram_release": ([], ctypes.c_int),
         "tfe_ngram_top": ([vp, i64, i32, i32, i64, i64, vp, vp, ctypes.POINTER(i64), vp],
                           ctypes.c_int),
         "tfe_get_stats": ([vp, ctypes.POINTER(tfe_stats)], ctypes.c_int),
@@ -98,7 +99,7 @@ lib = _load()
 EXPORTED = ("tfe_table_load", "tfe_table_free", "tfe_lookup_inject", "tfe_lookup_inject_multi",
             "tfe_prefetch",
             "tfe_prefetch_scored", "tfe_head_create", "tfe_head_topk", "tfe_head_free",
-            "tfe_ngram_top",
+            "tfe_ngram_top", "tfe_ngram_release",
             "tfe_get_stats", "tfe_reset_stats", "tfe_last_error", "tfe_index_capacity",
             "tfe_index_build_host", "tfe_index_probe_host")
 
@@ -191,6 +192,10 @@ def tfe_ngram_top(tokens, n_tokens, vocab, n, skip, top, out_tuples, out_counts,
     _check(lib.tfe_ngram_top(addr(tokens), n_tokens, vocab, n, skip, top, addr(out_tuples),
                              addr(out_counts), ctypes.byref(w), stream_handle(stream)))
     return w.value
+
+
+def tfe_ngram_release():
+    return _check(lib.tfe_ngram_release())
 
 
 def tfe_get_stats(table):

@@ -101,6 +101,30 @@ def test_workload2_stream_full_size():
         np.testing.assert_array_equal(c, wc)
 
 
+def test_scratch_reuse_and_release():
+    """Later calls reuse the scratch an earlier call left (same and smaller
+    sizes, then a larger one that returns the idle buffers first); release
+    hands it back; results never change."""
+    rng = np.random.default_rng(7)
+    big = rng.integers(0, 300, 200000).astype(np.int32)
+    small = big[:50000].copy()
+    want_big = oracle.ngram_top(big, 300, 3, 0, 500)
+    want_small = oracle.ngram_top(small, 300, 2, 3, 400)
+    for tok, n, skip, top, want in [(big, 3, 0, 500, want_big), (small, 2, 3, 400, want_small),
+                                    (big, 3, 0, 500, want_big)]:
+        got = gpu_top(tok, 300, n, skip, top)
+        np.testing.assert_array_equal(got[0], want[0])
+        np.testing.assert_array_equal(got[1], want[1])
+    tfe.tfe_ngram_release()
+    huge = rng.integers(0, 300, 600000).astype(np.int32)
+    got = gpu_top(huge, 300, 4, 0, 300)
+    want = oracle.ngram_top(huge, 300, 4, 0, 300)
+    np.testing.assert_array_equal(got[0], want[0])
+    np.testing.assert_array_equal(got[1], want[1])
+    tfe.tfe_ngram_release()
+    tfe.tfe_ngram_release()  # nothing idle: a no-op
+
+
 def test_errors_and_empty():
     tok = torch.zeros(10, dtype=torch.int32, device="cuda")
     out_t = torch.zeros((4, 4), dtype=torch.int32, device="cuda")
