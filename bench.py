@@ -587,17 +587,21 @@ def run_head(args):
 
 
 def build_bytes_per_window(n):
-    """Data the construction pipeline moves per window of the stream.  n <= 3:
-    key formation (4 B token read, 8 B key write), one radix pass per 8 key
-    bits (18n + 1 bits; 8 B histogram read + 16 B scatter read/write), run
-    flags and starts (8 + 4 + 4 + 4 B).  n = 4: key formation writes both
-    words (4 + 16 B), seven passes over the 54-bit low word carry the high
-    word (8 + 32 B each), the high word is narrowed (8 + 4 B), three passes
-    over its 19 bits carry the low word (4 + 24 B each), and the run flags
-    read it too (24 B).  The selection and ranking work on far fewer items."""
+    """Data the construction pipeline moves per window of the stream.  n <= 3
+    (P = one radix pass per 8 of the 18 n + 1 key bits): the first pass forms
+    the keys from the tokens (4 B read by its histogram, 4 B read and the
+    8 B key written by its scatter), every later pass reads the keys for its
+    histogram (8 B) and reads and writes them in its scatter (16 B); the run
+    count reads the sorted keys twice (16 B).  n = 4: the low word's first
+    pass writes key and payload (4 + 4 + 16 B), its six later passes move a
+    64-bit payload too (8 + 32 B each), the high word is narrowed (8 + 4 B),
+    three passes over its 19 bits carry the low word (4 + 24 B each), and
+    the run count reads both words twice (24 B).  The selection and ranking
+    work on far fewer items."""
     if n <= 3:
-        return 12 + 24 * ((18 * n + 8) // 8) + 20
-    return 20 + 7 * 40 + 12 + 3 * 28 + 24
+        passes = (18 * n + 8) // 8
+        return 16 + 24 * (passes - 1) + 16
+    return 24 + 6 * 40 + 12 + 3 * 28 + 24
 
 
 def run_build(args):

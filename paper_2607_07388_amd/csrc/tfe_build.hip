@@ -7,19 +7,22 @@
 //   1. key formation: every window of n tokens becomes one 64-bit key, the
 //      tokens in 18-bit fields, oldest in the highest field, so that key
 //      order is tuple order; a window with a token outside [0, vocab) gets
-//      the key 2^(18 n), above every valid one;
+//      the key 2^(18 n), above every valid one (formed by the first pass of
+//      the sort, from the tokens);
 //   2. LSD radix sort of the keys, 8-bit digits over the 18 n + 1 key bits
 //      (the valid keys end up first; a binary search counts them): per
-//      pass a digit histogram per 4096-key tile, one exclusive scan of the
-//      digit-major histogram, and a stable scatter (each wave ranks its keys
-//      with ballot-based digit matching, the tile is reordered in LDS and
-//      written out in digit runs);
-//   3. run-length count: run starts flagged and scanned into a unique-key
-//      array; a run's count is the distance to the next start;
-//   4. selection of ranks [0, skip + top): radix select of the (skip+top)-th
-//      largest count c*, then an order-preserving compaction of the runs
-//      with count > c* and the first needed ones with count == c* (key order
-//      = tuple order, which breaks the ties);
+//      pass a digit histogram per tile (8192 keys; 4096 with a payload), one
+//      exclusive scan of the digit-major histogram, and a stable scatter
+//      (each wave ranks its keys with ballot-based digit matching, the tile
+//      is reordered in LDS and written out in digit runs);
+//   3. run-length count: per-block counts of run starts, their scan, the
+//      starts written at their ranks into a unique-key array; a run's count
+//      is the distance to the next start;
+//   4. selection of ranks [0, skip + top): the (skip+top)-th largest count
+//      c* from a histogram of the small counts (a radix select over the
+//      counts when c* is large), then an order-preserving compaction of the
+//      runs with count > c* and the first needed ones with count == c* (key
+//      order = tuple order, which breaks the ties);
 //   5. ranking: a stable radix sort of the selected runs by descending count
 //      (payload: the run index), which keeps tuple order among equal counts;
 //   6. ranks [skip, skip + top) are unpacked into tuples and counts.
@@ -61,37 +64,63 @@ constexpr int kScanBlock = kScanThreads * kScanItems;
 
 // One key per window, in window order (no compaction: the sort moves the
 // invalid windows, marked with a key just above every valid one, to the end).
-__global__ __launch_bounds__(256) void k_ng_keys(const int32_t* tok, uint64_t nwin, int n,
-                                                 int32_t vocab, uint64_t* keys) {
-  const uint64_t i = (uint64_t)blockIdx.x * 256 + threadIdx.x;
-  if (i >= nwin) return;
+// The keys are formed from the tokens by the first radix pass itself.
+struct TokSrc {
+  const int32_t* tok;
+  int n;
+  int32_t vocab;
+};
+
+// Key sources: the key array, windows of 1, 2 or 3 tokens (the source is
+// the window length, known at compile time so that the token loads of all
+// of a thread's windows are in flight together), or 4-gram words.
+enum { kSrcKeys = 0, kSrcNgram4 = 4 };
+
+// Key of window i (NG <= 3 tokens, oldest in the highest field); an invalid
+// window gets 2^(18 NG).
+template <int NG>
+__device__ __forceinline__ uint64_t ngram_key(const TokSrc& ts, uint64_t i) {
   uint64_t key = 0;
   bool ok = true;
-  for (int j = 0; j < n; ++j) {
-    const int32_t t = tok[i + j];
-    ok = ok && t >= 0 && t < vocab;
+#pragma unroll
+  for (int j = 0; j < NG; ++j) {
+    const int32_t t = ts.tok[i + j];
+    ok = ok && t >= 0 && t < ts.vocab;
     key = (key << 18) | (uint64_t)(uint32_t)(t & 0x3FFFF);
   }
-  keys[i] = ok ? key : (1ull << (18 * n));
+  return ok ? key : (1ull << (18 * NG));
 }
 
 // 4-grams: 72 key bits in two words, lo = the three newest tokens (54 bits)
 // and hi = the oldest token, or the mark 2^18 for an invalid window.
-__global__ __launch_bounds__(256) void k_ng_keys4(const int32_t* tok, uint64_t nwin, int32_t vocab,
-                                                  uint64_t* lo, uint64_t* hi) {
-  const uint64_t i = (uint64_t)blockIdx.x * 256 + threadIdx.x;
-  if (i >= nwin) return;
+__device__ __forceinline__ uint64_t ngram4_lo(const TokSrc& ts, uint64_t i) {
   uint64_t key = 0;
+#pragma unroll
+  for (int j = 1; j < 4; ++j) key = (key << 18) | (uint64_t)(uint32_t)(ts.tok[i + j] & 0x3FFFF);
+  return key;
+}
+
+__device__ __forceinline__ uint64_t ngram4_hi(const TokSrc& ts, uint64_t i) {
   bool ok = true;
-  for (int j = 1; j < 4; ++j) {
-    const int32_t t = tok[i + j];
-    ok = ok && t >= 0 && t < vocab;
-    key = (key << 18) | (uint64_t)(uint32_t)(t & 0x3FFFF);
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int32_t t = ts.tok[i + j];
+    ok = ok && t >= 0 && t < ts.vocab;
   }
-  const int32_t t0 = tok[i];
-  ok = ok && t0 >= 0 && t0 < vocab;
-  lo[i] = key;
-  hi[i] = ok ? (uint64_t)(uint32_t)t0 : (1ull << 18);
+  return ok ? (uint64_t)(uint32_t)ts.tok[i] : (1ull << 18);
+}
+
+template <int SRC, class K>
+__device__ __forceinline__ K key_at(const K* keys, const TokSrc& ts, uint64_t i) {
+  if (SRC >= 1 && SRC <= 3) return (K)ngram_key<(SRC >= 1 && SRC <= 3) ? SRC : 1>(ts, i);
+  if (SRC == kSrcNgram4) return (K)ngram4_lo(ts, i);
+  return keys[i];
+}
+
+template <int SRC>
+__device__ __forceinline__ uint64_t val_at(const uint64_t* vals, const TokSrc& ts, uint64_t i) {
+  if (SRC == kSrcNgram4) return ngram4_hi(ts, i);
+  return vals[i];
 }
 
 __global__ __launch_bounds__(256) void k_narrow(const uint64_t* in, uint64_t n, uint32_t* out) {
@@ -250,11 +279,15 @@ __device__ __forceinline__ uint64_t match_digit(uint32_t d, bool active) {
 }
 
 // Digit histogram of one tile of TILE keys (kHistThreads threads; the keys
-// are loaded first).  Plain LDS atomics: on MI355X they beat counting each
-// group of equal digits once, also for skewed digits.
-template <class K, int TILE>
-__global__ __launch_bounds__(kHistThreads) void k_rs_hist(const K* keys, uint64_t n, int shift,
-                                                          uint32_t* hist, uint32_t ntiles) {
+// are loaded first).  Per round, the lanes holding the first lane's digit
+// add their number with one atomic and the others add 1 each: Zipf-skewed
+// digits (high bits of frequent tokens are mostly 0) would otherwise pile
+// same-address LDS atomics onto one bin; measured on MI355X this beats both
+// plain atomics and counting every group of equal digits once.
+template <class K, int TILE, int SRC>
+__global__ __launch_bounds__(kHistThreads) void k_rs_hist(const K* keys, TokSrc ts, uint64_t n,
+                                                          int shift, uint32_t* hist,
+                                                          uint32_t ntiles) {
   constexpr int ITEMS = TILE / kHistThreads;
   __shared__ uint32_t h[256];
   for (int e = threadIdx.x; e < 256; e += kHistThreads) h[e] = 0u;
@@ -263,13 +296,22 @@ __global__ __launch_bounds__(kHistThreads) void k_rs_hist(const K* keys, uint64_
 #pragma unroll
   for (int k = 0; k < ITEMS; ++k) {
     const uint64_t i = base + (uint64_t)k * kHistThreads + threadIdx.x;
-    kk[k] = i < n ? keys[i] : (K)0;
+    kk[k] = i < n ? key_at<SRC>(keys, ts, i) : (K)0;
   }
   __syncthreads();
+  const uint64_t lt = (1ull << (threadIdx.x & 63)) - 1ull;
 #pragma unroll
-  for (int k = 0; k < ITEMS; ++k)
-    if (base + (uint64_t)k * kHistThreads + threadIdx.x < n)
-      atomicAdd(&h[digit_of(kk[k], shift)], 1u);
+  for (int k = 0; k < ITEMS; ++k) {
+    const bool act = base + (uint64_t)k * kHistThreads + threadIdx.x < n;
+    const uint32_t d = digit_of(kk[k], shift);
+    const uint32_t d0 = __builtin_amdgcn_readfirstlane(d);
+    const uint64_t m = __builtin_amdgcn_ballot_w64(act && d == d0);
+    if (act && d == d0) {
+      if ((m & lt) == 0) atomicAdd(&h[d0], (uint32_t)__builtin_popcountll(m));
+    } else if (act) {
+      atomicAdd(&h[d], 1u);
+    }
+  }
   __syncthreads();
   for (int e = threadIdx.x; e < 256; e += kHistThreads)
     hist[(size_t)e * ntiles + blockIdx.x] = h[e];
@@ -281,9 +323,9 @@ __global__ __launch_bounds__(kHistThreads) void k_rs_hist(const K* keys, uint64_
 // plus the matching lanes below it; the first lane of each digit group
 // advances the count.  Tile positions follow (digit, wave, rank), i.e. the
 // stable order; the tile is reordered in LDS and written in digit runs.
-template <class K, bool PAIRS, int ITEMS>
+template <class K, bool PAIRS, int ITEMS, int SRC>
 __global__ __launch_bounds__(kTileThreads) void k_rs_scatter(const K* keys, const uint64_t* vals,
-                                                             uint64_t n, int shift,
+                                                             TokSrc ts, uint64_t n, int shift,
                                                              const uint32_t* offs,
                                                              uint32_t ntiles, K* keys_out,
                                                              uint64_t* vals_out) {
@@ -304,8 +346,8 @@ __global__ __launch_bounds__(kTileThreads) void k_rs_scatter(const K* keys, cons
 #pragma unroll
   for (int r = 0; r < ITEMS; ++r) {
     const uint64_t i = base + (uint64_t)r * 64 + lane;
-    kk[r] = i < n ? keys[i] : (K)0;
-    if (PAIRS) vv[PAIRS ? r : 0] = i < n ? vals[i] : 0ull;
+    kk[r] = i < n ? key_at<SRC>(keys, ts, i) : (K)0;
+    if (PAIRS) vv[PAIRS ? r : 0] = i < n ? val_at<SRC>(vals, ts, i) : 0ull;
   }
   __syncthreads();
 #pragma unroll
@@ -361,33 +403,124 @@ __global__ __launch_bounds__(kTileThreads) void k_rs_scatter(const K* keys, cons
 
 // ---- 3. run-length count ----------------------------------------------------
 
-// hi: the high key word (4-grams) or null.
-__global__ __launch_bounds__(256) void k_run_flags(const uint64_t* keys, const uint32_t* hi,
-                                                   uint64_t n, uint32_t* flag) {
-  const uint64_t i = (uint64_t)blockIdx.x * 256 + threadIdx.x;
-  if (i < n)
-    flag[i] = (i == 0 || keys[i] != keys[i - 1] || (hi && hi[i] != hi[i - 1])) ? 1u : 0u;
+// Runs of equal keys in the sorted valid keys (hi: the high key word of
+// 4-grams, or null), in two passes shaped like the scan: the number of run
+// starts per block, then (after the scan of those counts) each start's key
+// and position at its rank.  A start is a key that differs from the one
+// before it.  Wave w of a block covers kScanItems rounds of 64 keys.
+__device__ __forceinline__ bool run_start(const uint64_t* keys, const uint32_t* hi, uint64_t i,
+                                          uint64_t n) {
+  return i < n && (i == 0 || keys[i] != keys[i - 1] || (hi && hi[i] != hi[i - 1]));
 }
 
-__global__ __launch_bounds__(256) void k_run_starts(const uint64_t* keys, const uint32_t* hi,
-                                                    uint64_t n, const uint32_t* flag,
-                                                    const uint32_t* idx, uint64_t* ukey,
-                                                    uint32_t* uhi, uint32_t* ustart) {
-  const uint64_t i = (uint64_t)blockIdx.x * 256 + threadIdx.x;
-  if (i < n && flag[i]) {
-    ukey[idx[i]] = keys[i];
-    if (hi) uhi[idx[i]] = hi[i];
-    ustart[idx[i]] = (uint32_t)i;
+__global__ __launch_bounds__(kScanThreads) void k_runs_reduce(const uint64_t* keys,
+                                                              const uint32_t* hi, uint64_t n,
+                                                              uint32_t* part) {
+  __shared__ uint32_t s_tot[kScanThreads / 64];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const uint64_t base = (uint64_t)blockIdx.x * kScanBlock + (uint64_t)wave * (64 * kScanItems);
+  uint32_t c = 0;
+#pragma unroll
+  for (int k = 0; k < kScanItems; ++k)
+    c += (uint32_t)__builtin_popcountll(
+        __builtin_amdgcn_ballot_w64(run_start(keys, hi, base + (uint64_t)k * 64 + lane, n)));
+  if (lane == 0) s_tot[wave] = c;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint32_t t = 0;
+    for (int w = 0; w < kScanThreads / 64; ++w) t += s_tot[w];
+    part[blockIdx.x] = t;
   }
 }
 
-__global__ __launch_bounds__(256) void k_run_counts(const uint32_t* ustart, uint32_t u,
-                                                    uint32_t n, uint32_t* ucount) {
-  const uint32_t i = blockIdx.x * 256 + threadIdx.x;
-  if (i < u) ucount[i] = (i + 1 < u ? ustart[i + 1] : n) - ustart[i];
+__global__ __launch_bounds__(kScanThreads) void k_runs_write(const uint64_t* keys,
+                                                             const uint32_t* hi, uint64_t n,
+                                                             const uint32_t* part, uint64_t* ukey,
+                                                             uint32_t* uhi, uint32_t* ustart) {
+  __shared__ uint32_t s_tot[kScanThreads / 64];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const uint64_t base = (uint64_t)blockIdx.x * kScanBlock + (uint64_t)wave * (64 * kScanItems);
+  uint64_t m[kScanItems];
+  uint32_t c = 0;
+#pragma unroll
+  for (int k = 0; k < kScanItems; ++k) {
+    m[k] = __builtin_amdgcn_ballot_w64(run_start(keys, hi, base + (uint64_t)k * 64 + lane, n));
+    c += (uint32_t)__builtin_popcountll(m[k]);
+  }
+  if (lane == 0) s_tot[wave] = c;
+  __syncthreads();
+  uint32_t r = part[blockIdx.x];
+  for (int w = 0; w < wave; ++w) r += s_tot[w];
+  const uint64_t lt = (1ull << lane) - 1ull;
+#pragma unroll
+  for (int k = 0; k < kScanItems; ++k) {
+    const uint64_t i = base + (uint64_t)k * 64 + lane;
+    if ((m[k] >> lane) & 1ull) {
+      const uint32_t idx = r + (uint32_t)__builtin_popcountll(m[k] & lt);
+      ukey[idx] = keys[i];
+      if (hi) uhi[idx] = hi[i];
+      ustart[idx] = (uint32_t)i;
+    }
+    r += (uint32_t)__builtin_popcountll(m[k]);
+  }
+}
+
+// Run lengths, and the histogram of min(count, kSelBins - 1) for the
+// selection (per-block LDS bins added to the global ones).
+constexpr int kSelBins = 4096;
+
+__global__ __launch_bounds__(1024) void k_run_counts(const uint32_t* ustart, uint32_t u,
+                                                     uint32_t n, uint32_t* ucount,
+                                                     uint32_t* bins) {
+  __shared__ uint32_t h[kSelBins];
+  for (int e = threadIdx.x; e < kSelBins; e += 1024) h[e] = 0u;
+  __syncthreads();
+  const uint32_t base = blockIdx.x * (1024u * 16u);
+  for (int k = 0; k < 16; ++k) {
+    const uint32_t i = base + (uint32_t)k * 1024u + threadIdx.x;
+    if (i < u) {
+      const uint32_t c = (i + 1 < u ? ustart[i + 1] : n) - ustart[i];
+      ucount[i] = c;
+      atomicAdd(&h[c < (uint32_t)kSelBins ? c : (uint32_t)kSelBins - 1u], 1u);
+    }
+  }
+  __syncthreads();
+  for (int e = threadIdx.x; e < kSelBins; e += 1024)
+    if (h[e]) atomicAdd(&bins[e], h[e]);
 }
 
 // ---- 4. selection -----------------------------------------------------------
+
+// The selection state: {prefix, mask, need, above, done}.  After the
+// selection, prefix = c* (the R-th largest count), need = how many runs of
+// count c* belong to ranks [0, R), above = the runs with larger counts.
+
+// From the histogram of min(count, kSelBins - 1) (one block, 1024 threads,
+// 4 bins each from the top): if c* < kSelBins - 1 the selection is done;
+// otherwise the radix passes below find it.
+__global__ __launch_bounds__(1024) void k_sel_small(const uint32_t* bins, uint32_t* state) {
+  __shared__ uint32_t s_wave[16];
+  const uint32_t t = threadIdx.x;
+  const uint32_t need = state[2];
+  uint32_t v[4], sum = 0;
+  for (int k = 0; k < 4; ++k) {
+    v[k] = bins[kSelBins - 1 - (4 * t + k)];  // bins in descending count order
+    sum += v[k];
+  }
+  uint32_t tot;
+  uint32_t ex = block_scan_excl<1024>(sum, s_wave, &tot);
+  for (int k = 0; k < 4; ++k) {
+    const uint32_t c = kSelBins - 1 - (4 * t + k);
+    if (ex < need && need <= ex + v[k] && c < (uint32_t)kSelBins - 1) {
+      state[0] = c;
+      state[1] = 0xFFFFFFFFu;
+      state[2] = need - ex;
+      state[3] = ex;
+      state[4] = 1u;
+    }
+    ex += v[k];
+  }
+}
 
 // Histogram of digit `shift` of the counts whose higher digits equal
 // `prefix` (under `mask`): one pass of a radix select on a 32-bit value.
@@ -395,6 +528,7 @@ __global__ __launch_bounds__(256) void k_sel_hist(const uint32_t* cnt, uint32_t 
                                                   const uint32_t* state, int shift,
                                                   uint32_t* hist) {
   __shared__ uint32_t h[256];
+  if (state[4]) return;  // done from the small-count histogram
   h[threadIdx.x] = 0u;
   __syncthreads();
   const uint32_t prefix = state[0], mask = state[1];
@@ -413,6 +547,7 @@ __global__ __launch_bounds__(256) void k_sel_pick(uint32_t* hist, uint32_t* stat
   const uint32_t t = threadIdx.x;
   // Every thread reads the state before the scan's barriers, so the one
   // update below cannot be seen by a late reader.
+  if (state[4]) return;
   const uint32_t need = state[2];
   const uint32_t v = hist[255 - t];  // thread t looks at bin 255 - t
   uint32_t tot;
@@ -485,20 +620,37 @@ hipError_t scan_u32(const uint32_t* in, uint32_t* out, uint64_t n, uint32_t* par
   return hipGetLastError();
 }
 
-// hist holds 256 x ceil(n / kMinTile) entries.
-template <class K, bool PAIRS>
-hipError_t radix_sort(K*& keys, K*& keys_alt, uint64_t*& vals, uint64_t*& vals_alt, uint64_t n,
-                      int bits, uint32_t* hist, uint32_t* part, hipStream_t s) {
+template <class K, bool PAIRS, int SRC>
+hipError_t radix_pass(K* keys, K* keys_alt, uint64_t* vals, uint64_t* vals_alt, const TokSrc& ts,
+                      uint64_t n, int shift, uint32_t ntiles, uint32_t* hist, uint32_t* part,
+                      hipStream_t s) {
   constexpr int ITEMS = tile_items<K, PAIRS>();
+  hipLaunchKernelGGL((k_rs_hist<K, tile_keys<K, PAIRS>(), SRC>), dim3(ntiles), dim3(kHistThreads),
+                     0, s, keys, ts, n, shift, hist, ntiles);
+  hipError_t e = scan_u32(hist, hist, (uint64_t)256 * ntiles, part, nullptr, s);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((k_rs_scatter<K, PAIRS, ITEMS, SRC>), dim3(ntiles), dim3(kTileThreads), 0, s,
+                     keys, vals, ts, n, shift, hist, ntiles, keys_alt, vals_alt);
+  return hipGetLastError();
+}
+
+// Stable LSD sort of n keys (and payloads) by their low `bits` bits; the
+// first pass reads its keys (and payloads) from SRC.  hist holds
+// 256 x ceil(n / kMinTile) entries.
+template <class K, bool PAIRS, int SRC = kSrcKeys>
+hipError_t radix_sort(K*& keys, K*& keys_alt, uint64_t*& vals, uint64_t*& vals_alt, uint64_t n,
+                      int bits, uint32_t* hist, uint32_t* part, hipStream_t s,
+                      const TokSrc& ts = TokSrc{nullptr, 0, 0}) {
   const uint32_t ntiles = blocks_for(n, tile_keys<K, PAIRS>());
   if (ntiles == 0) return hipSuccess;
   for (int shift = 0; shift < bits; shift += 8) {
-    hipLaunchKernelGGL((k_rs_hist<K, tile_keys<K, PAIRS>()>), dim3(ntiles), dim3(kHistThreads), 0,
-                       s, keys, n, shift, hist, ntiles);
-    hipError_t e = scan_u32(hist, hist, (uint64_t)256 * ntiles, part, nullptr, s);
+    const hipError_t e =
+        shift == 0
+            ? radix_pass<K, PAIRS, SRC>(keys, keys_alt, vals, vals_alt, ts, n, shift, ntiles,
+                                        hist, part, s)
+            : radix_pass<K, PAIRS, kSrcKeys>(keys, keys_alt, vals, vals_alt, ts, n, shift,
+                                             ntiles, hist, part, s);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL((k_rs_scatter<K, PAIRS, ITEMS>), dim3(ntiles), dim3(kTileThreads), 0, s,
-                       keys, vals, n, shift, hist, ntiles, keys_alt, vals_alt);
     std::swap(keys, keys_alt);
     if (PAIRS) std::swap(vals, vals_alt);
   }
@@ -611,27 +763,30 @@ tfe_status ngram_top(const int32_t* tokens, int64_t N, int32_t vocab, int32_t n,
   uint32_t* part = sc.get<uint32_t>(kScanBlock);
   unsigned long long* d_count = sc.get<unsigned long long>(1);
   uint32_t* d_small = sc.get<uint32_t>(8);
-  if (!keys || !keys_alt || !hist || !part || !d_count || !d_small ||
+  uint32_t* sel_bins = sc.get<uint32_t>(kSelBins);
+  if (!keys || !keys_alt || !hist || !part || !d_count || !d_small || !sel_bins ||
       (wide && (!wv || !wv_alt || !hi || !hi_alt)))
     return fail(TFE_ERR_OOM, "n-gram scratch for %llu windows", (unsigned long long)nwin);
-  // 1. keys of all windows; 2. sort (one bit above the key fields carries
-  // the invalid-window mark); the valid keys are the first M.  4-grams sort
-  // by the low word, then stably by the high word (LSD over both words).
+  // 1-2. keys of all windows, formed by the first radix pass, sorted (one
+  // bit above the key fields carries the invalid-window mark); the valid
+  // keys are the first M.  4-grams sort by the low word, then stably by the
+  // high word (LSD over both words).
   uint64_t* no_vals = nullptr;
   uint64_t* no_vals2 = nullptr;
+  const TokSrc ts{tokens, n, vocab};
   if (!wide) {
-    hipLaunchKernelGGL(k_ng_keys, dim3(blocks_for(nwin, 256)), dim3(256), 0, s, tokens, nwin, n,
-                       vocab, keys);
-    BUILD_HIP(hipGetLastError(), "keys launch");
-    BUILD_HIP((radix_sort<uint64_t, false>(keys, keys_alt, no_vals, no_vals2, nwin, 18 * n + 1,
-                                           hist, part, s)),
-              "key sort");
+    const int bits = 18 * n + 1;
+    hipError_t e = n == 1   ? radix_sort<uint64_t, false, 1>(keys, keys_alt, no_vals, no_vals2,
+                                                             nwin, bits, hist, part, s, ts)
+                   : n == 2 ? radix_sort<uint64_t, false, 2>(keys, keys_alt, no_vals, no_vals2,
+                                                             nwin, bits, hist, part, s, ts)
+                            : radix_sort<uint64_t, false, 3>(keys, keys_alt, no_vals, no_vals2,
+                                                             nwin, bits, hist, part, s, ts);
+    BUILD_HIP(e, "key sort");
     hipLaunchKernelGGL(k_count_valid, dim3(1), dim3(1), 0, s, keys, nwin, n, d_count);
   } else {
-    hipLaunchKernelGGL(k_ng_keys4, dim3(blocks_for(nwin, 256)), dim3(256), 0, s, tokens, nwin,
-                       vocab, keys, wv);
-    BUILD_HIP(hipGetLastError(), "keys launch");
-    BUILD_HIP((radix_sort<uint64_t, true>(keys, keys_alt, wv, wv_alt, nwin, 54, hist, part, s)),
+    BUILD_HIP((radix_sort<uint64_t, true, kSrcNgram4>(keys, keys_alt, wv, wv_alt, nwin, 54, hist,
+                                                      part, s, ts)),
               "low-word sort");
     hipLaunchKernelGGL(k_narrow, dim3(blocks_for(nwin, 256)), dim3(256), 0, s, wv, nwin, hi);
     BUILD_HIP((radix_sort<uint32_t, true>(hi, hi_alt, keys, keys_alt, nwin, 19, hist, part, s)),
@@ -645,10 +800,10 @@ tfe_status ngram_top(const int32_t* tokens, int64_t N, int32_t vocab, int32_t n,
   const uint64_t M = m_host;
   if (M == 0) return TFE_OK;
   // 3. runs.
-  uint32_t* flag = (uint32_t*)keys_alt;  // keys_alt is free now: M x 8 bytes
-  uint32_t* idx = flag + M;
-  hipLaunchKernelGGL(k_run_flags, dim3(blocks_for(M, 256)), dim3(256), 0, s, keys, hi, M, flag);
-  BUILD_HIP(scan_u32(flag, idx, M, part, d_small, s), "run scan");
+  const uint32_t nbr = blocks_for(M, kScanBlock);
+  hipLaunchKernelGGL(k_runs_reduce, dim3(nbr), dim3(kScanThreads), 0, s, keys, hi, M, part);
+  hipLaunchKernelGGL(k_scan_partials, dim3(1), dim3(kScanThreads), 0, s, part, nbr, d_small);
+  BUILD_HIP(hipGetLastError(), "run count launches");
   uint32_t U = 0;
   BUILD_HIP(hipMemcpyAsync(&U, d_small, sizeof U, hipMemcpyDeviceToHost, s), "copy");
   BUILD_HIP(hipStreamSynchronize(s), "sync");
@@ -658,18 +813,22 @@ tfe_status ngram_top(const int32_t* tokens, int64_t N, int32_t vocab, int32_t n,
   uint32_t* ucnt = sc.get<uint32_t>(U);
   uint32_t* eq = sc.get<uint32_t>(U);
   if (!ukey || !ustart || !ucnt || !eq || (wide && !uhi)) return fail(TFE_ERR_OOM, "run arrays");
-  hipLaunchKernelGGL(k_run_starts, dim3(blocks_for(M, 256)), dim3(256), 0, s, keys, hi, M, flag,
-                     idx, ukey, uhi, ustart);
-  hipLaunchKernelGGL(k_run_counts, dim3(blocks_for(U, 256)), dim3(256), 0, s, ustart, U,
-                     (uint32_t)M, ucnt);
+  hipLaunchKernelGGL(k_runs_write, dim3(nbr), dim3(kScanThreads), 0, s, keys, hi, M, part, ukey,
+                     uhi, ustart);
+  BUILD_HIP(hipMemsetAsync(sel_bins, 0, kSelBins * sizeof(uint32_t), s), "memset");
+  hipLaunchKernelGGL(k_run_counts, dim3(blocks_for(U, 16384)), dim3(1024), 0, s, ustart, U,
+                     (uint32_t)M, ucnt, sel_bins);
   BUILD_HIP(hipGetLastError(), "run launches");
   const uint64_t R = std::min<uint64_t>((uint64_t)skip + (uint64_t)top, U);
   if (R <= (uint64_t)skip) return TFE_OK;
-  // 4. the R-th largest count and the runs that make ranks [0, R).
+  // 4. the R-th largest count and the runs that make ranks [0, R): from the
+  // small-count histogram when it lies below kSelBins - 1, else by a radix
+  // select over the counts (its passes return at once when done).
   uint32_t* selh = hist;  // 256 bins, cleared by each pick
-  const uint32_t state0[4] = {0u, 0u, (uint32_t)R, 0u};
+  const uint32_t state0[5] = {0u, 0u, (uint32_t)R, 0u, 0u};
   BUILD_HIP(hipMemsetAsync(selh, 0, 256 * sizeof(uint32_t), s), "memset");
   BUILD_HIP(hipMemcpyAsync(d_small, state0, sizeof state0, hipMemcpyHostToDevice, s), "copy");
+  hipLaunchKernelGGL(k_sel_small, dim3(1), dim3(1024), 0, s, sel_bins, d_small);
   // Few blocks: each adds its LDS histogram to the 256 global bins once.
   const uint32_t sel_blocks = std::min<uint32_t>(blocks_for(U, 256), 512);
   for (int shift = 24; shift >= 0; shift -= 8) {
