@@ -66,6 +66,16 @@ KERNEL_SOURCES = ("paper_2607_07388_amd/csrc/tfe_lookup.hip",
                   "paper_2607_07388_amd/csrc/tfe_index.h")
 
 
+# The same for the multi-match kernel in the same 16384-row launch, from the
+# passes in profiles/k_lookup_inject_multi_bf16_d1024_decode_stacked16384.md.
+PROFILED_TRAFFIC_MULTI = {
+    "sources_sha256": "6b7bf0f91a867e01e24035c7c89adb958b829f0501ee257948cd0865ba0ebdf6",
+    "bytes_per_launch": 98469819,
+}
+MULTI_SOURCES = ("paper_2607_07388_amd/csrc/tfe_multi.hip",
+                 "paper_2607_07388_amd/csrc/tfe_device.h",
+                 "paper_2607_07388_amd/csrc/tfe_index.h")
+
 # The same for one call of the early-exit head (W 151936 x 1024 bf16, 64 rows,
 # K = 128): k_head_logits + k_head_rows, from the passes in
 # profiles/k_head_logits_rows_v151936_d1024_b64_k128.md.
@@ -448,7 +458,9 @@ def finish_multi(args, table, gt, sets, mslots, B, ctx, S, window, L, tokens_per
             "peak": HBM_PEAK_GBPS,
             "unit": "GB/s",
             "frac": achieved / HBM_PEAK_GBPS,
-            "traffic": None,
+            "traffic": (PROFILED_TRAFFIC_MULTI["bytes_per_launch"]
+                        if kernel_sources_sha256(MULTI_SOURCES) ==
+                        PROFILED_TRAFFIC_MULTI["sources_sha256"] and args.stack == 256 else None),
             "bytes_per_launch": avg_bytes,
             "avg_launch_us": avg_launch * 1e6,
             "copy_reference_gbps": copy_gbps,
