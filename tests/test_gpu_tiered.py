@@ -240,6 +240,40 @@ def test_tiered_fp32_copied_values_workload1():
     res.close()
 
 
+@pytest.mark.parametrize("fill", FILLS)
+def test_tiered_4grams_pads_both_launch_shapes(fill):
+    """2/3/4-gram table (4-gram keys carry the extension word), pads, out of
+    range tokens and history columns, on a 48-row cache: calls of 63
+    positions (the fused decode kernel) and of 111 (probe + grouped
+    resolve) alternate; outputs equal the oracle and a resident copy byte
+    for byte, statistics equal the policy model."""
+    from .test_gpu_parity import small_table
+    vocab = 7
+    table = small_table(321, vocab, [(2, 20), (3, 150), (4, 900)], synth.BF16, 1024, 4)
+    res = H.GpuTable(table)
+    ot = H.oracle_table(table)
+    C, pre = 48, 16
+    tier = TieredTable(table, C, pre, fill=fill)
+    model = LruModel(C, pre, table.dim * 2, fill_rereads=fill == tfe.TFE_FILL_SIDE_STREAM)
+    rng = np.random.default_rng(5 + fill)
+    lens_seen = set()
+    for step in range(8):
+        B, ctx, S = (3, 3, 21) if step % 2 == 0 else (3, 3, 37)
+        tokens = rng.integers(-1, vocab + 1, (B, ctx + S)).astype(np.int32)
+        hidden = synth.normal_range(8, 800 + step, 0, B * S, table.dim, 1.0, synth.BF16)
+        o = run_both(res, tier, tokens, ctx, S, hidden, table.dtype, table.dim)
+        hit, row, ln, want = H.oracle_answer(table, ot, tokens, ctx, S, hidden)
+        np.testing.assert_array_equal(o.slot.cpu().numpy(), row)
+        np.testing.assert_array_equal(o.len.cpu().numpy(), ln)
+        H.assert_close(H.to_host(o.out, table.dtype), want, table.dtype)
+        model.lookup([int(r) for r in row])
+        check_stats(tier, model)
+        lens_seen |= set(ln.tolist())
+    assert {0, 2, 3, 4} <= lens_seen
+    tier.close()
+    res.close()
+
+
 def test_tiered_load_errors():
     table, _ = synth.config1()
     vals = table.all_values()
