@@ -56,11 +56,13 @@ template <> struct Vec<1> { static constexpr int N = 8; };  // bfloat16
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
 
-// float32 -> bfloat16 bits, nearest even; NaN stays NaN.
-__device__ __forceinline__ uint32_t to_bf16(float f) {
-  const uint32_t u = __float_as_uint(f);
-  if ((u & 0x7FFFFFFFu) > 0x7F800000u) return (u >> 16) | 0x40u;
-  return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+
+// Two float32 -> two bfloat16 (low half = a), nearest even: one
+// v_cvt_pk_bf16_f32 on gfx950.
+__device__ __forceinline__ uint32_t to_bf16x2(float a, float b) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{a, b}, bf16x2_t));
 }
 
 template <int DT>
@@ -82,7 +84,7 @@ __device__ __forceinline__ u32x4 pack(const float* f) {
     for (int i = 0; i < 4; ++i) v[i] = __float_as_uint(f[i]);
   } else {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) v[i] = to_bf16(f[2 * i]) | (to_bf16(f[2 * i + 1]) << 16);
+    for (int i = 0; i < 4; ++i) v[i] = to_bf16x2(f[2 * i], f[2 * i + 1]);
   }
   return v;
 }
