@@ -80,8 +80,8 @@ MULTI_SOURCES = ("paper_2607_07388_amd/csrc/tfe_multi.hip",
 # K = 128): k_head_logits + k_head_rows, from the passes in
 # profiles/k_head_logits_rows_v151936_d1024_b64_k128.md.
 PROFILED_TRAFFIC_HEAD = {
-    "sources_sha256": "eadfccbe994d094a1e919986451edfc7f6664f35b69483d3249b6c58863a2e7b",
-    "bytes_per_launch": 372549456,
+    "sources_sha256": "ab8f3c5b1361dacdd2cebbcd92a70214106b38a326e92b1e3aabaca4d0f5123a",
+    "bytes_per_launch": 372542834,
 }
 HEAD_SOURCES = ("paper_2607_07388_amd/csrc/tfe_head.hip",
                 "paper_2607_07388_amd/csrc/tfe_head.h",

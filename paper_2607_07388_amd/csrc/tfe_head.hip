@@ -59,9 +59,6 @@ __device__ __forceinline__ float key2f(uint32_t k) {
 // floating point for mixed integer types, which would round the keys).
 __device__ __forceinline__ uint64_t umax64(uint64_t x, uint64_t y) { return x > y ? x : y; }
 __device__ __forceinline__ uint64_t umin64(uint64_t x, uint64_t y) { return x < y ? x : y; }
-__device__ __forceinline__ uint64_t shfl_xor64(uint64_t x, int m) {
-  return (uint64_t)__shfl_xor((unsigned long long)x, m, 64);
-}
 // (logit, token) -> 64-bit key: higher logit first, then lower token id.
 // Keys are distinct, and 0 is below every real key.
 __device__ __forceinline__ uint64_t tkey64(float l, uint32_t id) {
@@ -223,15 +220,50 @@ __global__ __launch_bounds__(kLogitWaves * 64) void k_head_logits(const HeadArgs
   }
 }
 
-__device__ __forceinline__ float wave_max(float x) {
-#pragma unroll
-  for (int d = 32; d >= 1; d >>= 1) x = fmaxf(x, __shfl_xor(x, d, 64));
-  return x;
+// Wave-wide reductions and scans with DPP (rows of 16 lanes) and readlane,
+// in a fixed order, without LDS round trips.
+template <int CTRL>
+__device__ __forceinline__ uint32_t dpp_u32(uint32_t x) {
+  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, CTRL, 0xF, 0xF, false);
 }
+
 __device__ __forceinline__ float wave_add(float x) {
-#pragma unroll
-  for (int d = 32; d >= 1; d >>= 1) x += __shfl_xor(x, d, 64);
-  return x;
+  x += __uint_as_float(dpp_u32<0xB1>(__float_as_uint(x)));   // quad_perm [1,0,3,2]
+  x += __uint_as_float(dpp_u32<0x4E>(__float_as_uint(x)));   // quad_perm [2,3,0,1]
+  x += __uint_as_float(dpp_u32<0x141>(__float_as_uint(x)));  // row_half_mirror
+  x += __uint_as_float(dpp_u32<0x140>(__float_as_uint(x)));  // row_mirror
+  const float r0 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), 0));
+  const float r1 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), 16));
+  const float r2 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), 32));
+  const float r3 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), 48));
+  return (r0 + r1) + (r2 + r3);
+}
+
+__device__ __forceinline__ uint32_t wave_max_u32(uint32_t x) {
+  x = max(x, dpp_u32<0xB1>(x));
+  x = max(x, dpp_u32<0x4E>(x));
+  x = max(x, dpp_u32<0x141>(x));
+  x = max(x, dpp_u32<0x140>(x));
+  const uint32_t r0 = (uint32_t)__builtin_amdgcn_readlane((int)x, 0);
+  const uint32_t r1 = (uint32_t)__builtin_amdgcn_readlane((int)x, 16);
+  const uint32_t r2 = (uint32_t)__builtin_amdgcn_readlane((int)x, 32);
+  const uint32_t r3 = (uint32_t)__builtin_amdgcn_readlane((int)x, 48);
+  return max(max(r0, r1), max(r2, r3));
+}
+
+// Inclusive sum over the lanes up to this one: shifts within each 16-lane
+// row, then the totals of the rows below.
+__device__ __forceinline__ uint32_t wave_incl_scan(uint32_t x) {
+  const int lane = threadIdx.x & 63;
+  x += dpp_u32<0x111>(x);  // row_shr:1
+  x += dpp_u32<0x112>(x);  // row_shr:2
+  x += dpp_u32<0x114>(x);  // row_shr:4
+  x += dpp_u32<0x118>(x);  // row_shr:8
+  const uint32_t r0 = (uint32_t)__builtin_amdgcn_readlane((int)x, 15);
+  const uint32_t r1 = (uint32_t)__builtin_amdgcn_readlane((int)x, 31);
+  const uint32_t r2 = (uint32_t)__builtin_amdgcn_readlane((int)x, 47);
+  const int row = lane >> 4;
+  return x + (row >= 1 ? r0 : 0u) + (row >= 2 ? r1 : 0u) + (row >= 3 ? r2 : 0u);
 }
 
 // Exclusive block prefix sum over the block's threads (NT of them); *total
@@ -239,13 +271,8 @@ __device__ __forceinline__ float wave_add(float x) {
 template <int NT>
 __device__ uint32_t block_excl_scan(uint32_t v, uint32_t* s_wave, uint32_t* total) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  uint32_t x = v;
-#pragma unroll
-  for (int d = 1; d < 64; d <<= 1) {
-    const uint32_t y = __shfl_up(x, d, 64);
-    if (lane >= d) x += y;
-  }
-  if (lane == 63) s_wave[wave] = x;
+  const uint32_t inc = wave_incl_scan(v);
+  if (lane == 63) s_wave[wave] = inc;
   __syncthreads();
   uint32_t off = 0, tot = 0;
 #pragma unroll
@@ -255,7 +282,7 @@ __device__ uint32_t block_excl_scan(uint32_t v, uint32_t* s_wave, uint32_t* tota
   }
   __syncthreads();
   *total = tot;
-  return x - v + off;
+  return inc - v + off;
 }
 
 // Bitonic sort of a[0, N2) in LDS, descending; N2 a power of two.
@@ -302,9 +329,10 @@ constexpr int kRowCand = 16 * kHeadMaxK;                // logits of the candida
 //      1024 of them, else by a bitonic sort; the first K are the answer.
 __global__ __launch_bounds__(kRowThreads) void k_head_rows(const HeadArgs a) {
   __shared__ uint64_t s_cand[kRowCand];
-  __shared__ uint32_t whist[kRowThreads / 64][256];
+  __shared__ uint32_t hist[256];
   __shared__ uint32_t s_tiles[kHeadMaxK];
   __shared__ uint32_t s_wave[kRowThreads / 64];
+  __shared__ uint32_t s_wmin[kRowThreads / 64];
   __shared__ float s_red[kRowThreads / 64];
   __shared__ uint32_t s_bin, s_above, s_cnt;
   const uint32_t b = blockIdx.x;
@@ -320,26 +348,43 @@ __global__ __launch_bounds__(kRowThreads) void k_head_rows(const HeadArgs a) {
   // Tile keys and sums are loaded together (one round trip).
   uint64_t key[kRowTiles];
   float tsv[kRowTiles];
-  uint64_t kmax = 0;
 #pragma unroll
   for (int i = 0; i < kRowTiles; ++i) {
     const uint32_t t = tid + i * kRowThreads;
     key[i] = t < NT ? tk[sidx(t)] : 0;
     tsv[i] = t < NT ? ts[sidx(t)] : 0.f;
-    kmax = umax64(kmax, key[i]);
   }
-  // 1. Log-sum-exp over the tiles.
-  for (int d = 32; d >= 1; d >>= 1) kmax = umax64(kmax, shfl_xor64(kmax, d));
-  if (lane == 0) s_cand[wave] = kmax;
+  // High key words of this thread's tiles (absent tiles hold key 0, below
+  // every real one, so they only count for the minimum when skipped).
+  uint32_t hmax = 0, hmin = 0xFFFFFFFFu;
+#pragma unroll
+  for (int i = 0; i < kRowTiles; ++i) {
+    const uint32_t hw = (uint32_t)(key[i] >> 32);
+    hmax = max(hmax, hw);
+    hmin = min(hmin, key[i] ? hw : 0xFFFFFFFFu);
+  }
+  // 1. Log-sum-exp over the tiles.  The largest logit is the largest high
+  // key word; the tile terms use the hardware exponential (the tile sums do
+  // too; relative error about an ulp per term).
+  hmax = wave_max_u32(hmax);
+  hmin = ~wave_max_u32(~hmin);
+  if (lane == 0) {
+    s_wave[wave] = hmax;
+    s_wmin[wave] = hmin;
+  }
   __syncthreads();
-  uint64_t gmax = 0;
-  for (int w = 0; w < kRowThreads / 64; ++w) gmax = umax64(gmax, s_cand[w]);
-  const float M = key2f((uint32_t)(gmax >> 32));
+  hmax = 0;
+  hmin = 0xFFFFFFFFu;
+  for (int w = 0; w < kRowThreads / 64; ++w) {
+    hmax = max(hmax, s_wave[w]);
+    hmin = min(hmin, s_wmin[w]);
+  }
+  const float M = key2f(hmax);
   float part = 0.f;
 #pragma unroll
   for (int i = 0; i < kRowTiles; ++i) {
     const uint32_t t = tid + i * kRowThreads;
-    if (t < NT) part += tsv[i] * expf(key2f((uint32_t)(key[i] >> 32)) - M);
+    if (t < NT) part += tsv[i] * __expf(key2f((uint32_t)(key[i] >> 32)) - M);
   }
   part = wave_add(part);
   if (lane == 0) s_red[wave] = part;
@@ -349,51 +394,77 @@ __global__ __launch_bounds__(kRowThreads) void k_head_rows(const HeadArgs a) {
 
   // 2. The K-th largest tile key (all tiles when there are at most K).
   const uint32_t take = min(a.K, NT);
-  uint64_t prefix = 0, mask = 0;
+  uint64_t prefix = 0, mask = 0, common = 0;
   if (take < NT) {
-    uint32_t need = take;
-    for (int pass = 0; pass < 8; ++pass) {
-      const int shift = 56 - 8 * pass;
-      for (int e = lane; e < 256; e += 64) whist[wave][e] = 0u;
+    // Radix select from the highest bit in which the tile keys differ (the
+    // high words of all keys lie between hmin and hmax, so they agree above
+    // the top bit of hmin ^ hmax), 8 bits per pass.  It stops once the bins
+    // at and above the chosen one hold at most kStopCand tiles: every
+    // answer lies in those tiles, so the K-th largest key itself is not
+    // needed.
+    constexpr uint32_t kStopCand = 192;
+    const uint32_t dhi = hmin ^ hmax;
+    const int top = dhi ? 63 - __builtin_clz(dhi) : 31;  // highest differing bit (low word: 31)
+    const int shift0 = max(top - 7, 0);
+    // Bits above the first digit, shared by every key (all in the high word).
+    if (shift0 + 8 < 64) common = ((uint64_t)hmax << 32) & ~((1ull << (shift0 + 8)) - 1ull);
+    uint32_t need = take, above = 0;
+    const uint64_t lt = (1ull << lane) - 1ull;
+    for (int shift = shift0;; shift = max(shift - 8, 0)) {
+      if (tid < 256) hist[tid] = 0u;
       __syncthreads();
+      // The lanes holding the first active lane's digit add their number
+      // with one atomic (the top digits of tile maxima are mostly equal).
 #pragma unroll
       for (int i = 0; i < kRowTiles; ++i) {
-        if (tid + i * kRowThreads < NT && (key[i] & mask) == prefix)
-          atomicAdd(&whist[wave][(uint32_t)(key[i] >> shift) & 255u], 1u);
+        if (tid + i * kRowThreads < NT && (key[i] & mask) == prefix) {
+          const uint32_t d = (uint32_t)(key[i] >> shift) & 255u;
+          const uint32_t d0 = __builtin_amdgcn_readfirstlane(d);
+          const uint64_t m = __builtin_amdgcn_ballot_w64(d == d0);
+          if (d != d0) atomicAdd(&hist[d], 1u);
+          else if ((m & lt) == 0) atomicAdd(&hist[d0], (uint32_t)__builtin_popcountll(m));
+        }
       }
       __syncthreads();
-      // Thread t < 256 owns bin 255 - t: prefix sums count keys from the top.
-      uint32_t v = 0;
-      if (tid < 256)
-        for (int w = 0; w < kRowThreads / 64; ++w) v += whist[w][255 - tid];
-      uint32_t tot;
-      const uint32_t excl = block_excl_scan<kRowThreads>(v, s_wave, &tot);
-      if (tid < 256 && excl < need && need <= excl + v) {
-        s_bin = 255 - tid;
-        s_above = excl;
-        s_cnt = v;
+      // Wave 0 finds the bin holding the need-th largest key: lane l holds
+      // bins 255 - 4 l - k, k = 0..3 (descending order).
+      if (wave == 0) {
+        uint32_t v[4], sum = 0;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          v[k] = hist[255 - 4 * lane - k];
+          sum += v[k];
+        }
+        const uint32_t inc = wave_incl_scan(sum);
+        uint32_t ex = inc - sum;
+        if (ex < need && need <= inc) {
+#pragma unroll
+          for (int k = 0; k < 4; ++k) {
+            if (ex < need && need <= ex + v[k]) {
+              s_bin = 255u - 4u * (uint32_t)lane - (uint32_t)k;
+              s_above = ex;
+              s_cnt = v[k];
+            }
+            ex += v[k];
+          }
+        }
       }
       __syncthreads();
       need -= s_above;
-      prefix |= (uint64_t)s_bin << shift;
+      above += s_above;
+      prefix |= (uint64_t)s_bin << shift;  // bits below the previous digit only
       mask |= (uint64_t)0xFF << shift;
-      const bool done = s_cnt == need;
-      __syncthreads();
-      if (done) break;
+      // Every thread has read s_bin / s_above / s_cnt before wave 0 can
+      // write them again (two barriers of the next pass come first).
+      if (s_cnt == need || above + s_cnt <= kStopCand || shift == 0) break;
     }
   }
-  // Candidate tiles: the `take` keys whose masked bits reach the prefix.
-  // The smallest candidate tile key (every answer logit is at or above it)
-  // comes from the keys held in registers.
+  // Candidate tiles: the keys whose masked bits reach the prefix (at most
+  // max(K, kStopCand) of them); every answer logit is at or above the prefix.
   uint32_t mine = 0;
-  uint64_t floor_key = ~0ull;
 #pragma unroll
-  for (int i = 0; i < kRowTiles; ++i) {
-    if (tid + i * kRowThreads < NT && (key[i] & mask) >= prefix) {
-      ++mine;
-      floor_key = umin64(floor_key, key[i]);
-    }
-  }
+  for (int i = 0; i < kRowTiles; ++i)
+    if (tid + i * kRowThreads < NT && (key[i] & mask) >= prefix) ++mine;
   uint32_t ntile;
   uint32_t off = block_excl_scan<kRowThreads>(mine, s_wave, &ntile);
 #pragma unroll
@@ -402,13 +473,7 @@ __global__ __launch_bounds__(kRowThreads) void k_head_rows(const HeadArgs a) {
     if (t < NT && (key[i] & mask) >= prefix) s_tiles[off++] = t;
   }
   // (With all tiles taken, every logit is a candidate.)
-  for (int d = 32; d >= 1; d >>= 1) floor_key = umin64(floor_key, shfl_xor64(floor_key, d));
-  __syncthreads();
-  if (lane == 0) s_cand[wave] = floor_key;
-  __syncthreads();
-  uint64_t tau = ~0ull;
-  for (int w = 0; w < kRowThreads / 64; ++w) tau = umin64(tau, s_cand[w]);
-  if (take == NT) tau = 0;
+  const uint64_t tau = take == NT ? 0 : (common | prefix);
   __syncthreads();
 
   // 3. Gather the candidate tiles' logits at or above tau, sort, emit.
