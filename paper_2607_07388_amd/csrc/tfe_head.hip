@@ -17,9 +17,11 @@
 //                  The epilogue writes the fp32 logits and, per (row,
 //                  16-token tile), the largest (logit, id) key and the sum of
 //                  exp(logit - tile max).
-//   k_head_rows    per row: the log-sum-exp from the tile statistics, the
-//                  K-th largest tile key by radix select, then the logits of
-//                  those K tiles (every top-K logit lies in one) sorted in LDS.
+//   k_head_rows    per row: the log-sum-exp from the tile statistics, a
+//                  radix select over the tile keys down to a set of at least
+//                  K tiles (every top-K logit lies in one of the K tiles with
+//                  the largest maxima), then those tiles' logits ranked in
+//                  LDS.
 // Ties in logit go to the lower token id, so the answer is unique.  The K
 // output probabilities use the full-accuracy expf (about 1 ulp); the chunk
 // sums of exp(l - max) use the hardware exponential, whose relative error
@@ -318,15 +320,15 @@ constexpr int kRowCand = 16 * kHeadMaxK;                // logits of the candida
 // Per row: the K most likely tokens and their probabilities from the tile
 // statistics and the logits.
 //   1. M = max logit, S = sum over tiles of tsum * exp(tile max - M).
-//   2. tau = the K-th largest tile-max key, by an exact radix select (8-bit
-//      digits from the top, per-wave histograms; keys are distinct, so a
-//      chosen bin ends up holding exactly the keys still needed).  Each of
-//      the K tiles at or above tau holds a logit at or above tau, so the
-//      K-th largest logit is at least tau and every top-K logit lies in one
-//      of these K tiles.
-//   3. The logits of those tiles at or above tau (at most 16 K, usually a
-//      little over K) are ranked in LDS, by counting when there are at most
-//      1024 of them, else by a bitonic sort; the first K are the answer.
+//   2. A radix select over the tile-max keys (8-bit digits from the highest
+//      bit in which they differ; one LDS histogram per pass) narrows the
+//      tiles to the bins at and above the one holding the K-th largest key;
+//      it stops when those hold at most 192 tiles (or exactly K).  The K
+//      tiles with the largest maxima are among them and hold every top-K
+//      logit, and every top-K logit is at or above the bins' lower bound.
+//   3. The logits of those tiles at or above that bound are ranked in LDS,
+//      by counting when there are at most 1024 of them, else by a bitonic
+//      sort; the first K are the answer.
 __global__ __launch_bounds__(kRowThreads) void k_head_rows(const HeadArgs a) {
   __shared__ uint64_t s_cand[kRowCand];
   __shared__ uint32_t hist[256];
