@@ -63,6 +63,7 @@ class Head:
     (200, 256, 3, 200),        # K = V: every token, in order
     (40000, 1024, 100, 64),    # two column groups (64 + 36 rows), ten chunks
     (151936, 1024, 64, 128),   # the backbone vocabulary, one batch-64 decode step
+    (1 << 18, 256, 3, 256),    # the largest vocabulary (16384 tiles) and the largest K
 ])
 def test_integer_logits_bit_exact_ids(V, D, B, K):
     w, h = int_inputs(V + D + B, V, D, B)
