@@ -101,6 +101,57 @@ def test_workload2_stream_full_size():
         np.testing.assert_array_equal(c, wc)
 
 
+def de_bruijn(k, n):
+    """The de Bruijn sequence B(k, n) (every n-gram over k symbols exactly
+    once, cyclically), by concatenating the Lyndon words whose length
+    divides n, in lexicographic order."""
+    seq, a = [], [0] * (k * n)
+
+    def db(t, p):
+        if t > n:
+            if n % p == 0:
+                seq.extend(a[1:p + 1])
+            return
+        a[t] = a[t - p]
+        db(t + 1, p)
+        for j in range(a[t - p] + 1, k):
+            a[t] = j
+            db(t + 1, t)
+
+    db(1, 1)
+    return np.array(seq, np.int32)
+
+
+def test_largest_stream_closed_form_counts():
+    """n_tokens = 2^28 (the largest stream; its run scan fills the 16384
+    block partials exactly): 65536 periods of B(16, 3), so every 3-gram over
+    16 symbols occurs 65536 times except the two that wrap around the end
+    (65535), and every 2-gram 16 x 65536 times except the last (one less).
+    Ranks: by count, then by tuple."""
+    period = de_bruijn(16, 3)
+    assert period.size == 4096 and len({tuple(np.roll(period, -i)[:3]) for i in range(4096)}) == 4096
+    N = 1 << 28
+    tok = torch.from_numpy(period).cuda().repeat(N // period.size)
+    cyc = np.concatenate([period, period[:2]])
+    for n, top in ((3, 4096), (2, 256)):
+        windows = np.stack([cyc[i:i + n] for i in range(period.size)])
+        uniq, counts = np.unique(windows, axis=0, return_counts=True)
+        counts = counts.astype(np.int64) * (N // period.size)
+        # The windows that wrap around the stream's end are missing once.
+        for i in range(period.size - n + 1, period.size):
+            counts[np.flatnonzero((uniq == windows[i]).all(1))[0]] -= 1
+        order = np.lexsort(tuple(uniq[:, j] for j in range(n - 1, -1, -1)) + (-counts,))
+        want_t, want_c = uniq[order][:top], counts[order][:top]
+        tup = torch.full((top, n), -7, dtype=torch.int32, device="cuda")
+        cnt = torch.full((top,), -7, dtype=torch.int64, device="cuda")
+        m = tfe.tfe_ngram_top(tok, N, 16, n, 0, top, tup, cnt, H.cur_stream())
+        assert m == top
+        np.testing.assert_array_equal(tup.cpu().numpy(), want_t)
+        np.testing.assert_array_equal(cnt.cpu().numpy(), want_c)
+    del tok
+    tfe.tfe_ngram_release()
+
+
 def test_scratch_reuse_and_release():
     """Later calls reuse the scratch an earlier call left (same and smaller
     sizes, then a larger one that returns the idle buffers first); release
