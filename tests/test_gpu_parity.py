@@ -150,6 +150,31 @@ def test_4grams_pads_ragged_tail(dtype, dim):
     gt.close()
 
 
+@pytest.mark.parametrize("lengths", [(2,), (3,), (4,), (3, 4), (2, 4)])
+def test_length_ranges(lengths):
+    """n_min..n_max covering one length, a range without 2-grams, and 2/4-gram
+    tables with no 3-grams (that lane group probes and never matches); both
+    entry points, the multi-match one with its n_max - n_min + 1 columns."""
+    from .test_gpu_multi import check_multi
+    vocab = 7
+    want = {2: 20, 3: 150, 4: 900}
+    table = small_table(500 + sum(lengths) * 7 + len(lengths), vocab,
+                        [(n, want[n]) for n in lengths], synth.BF16, 1024, max(lengths))
+    gt = H.GpuTable(table)
+    ot = H.oracle_table(table)
+    rng = np.random.default_rng(len(lengths) * 10 + lengths[0])
+    B, ctx, S = 3, 3, 37
+    tokens = rng.integers(-1, vocab + 1, (B, ctx + S)).astype(np.int32)
+    hidden = synth.normal_range(7, 90 + lengths[0], 0, B * S, 1024, 1.0, synth.BF16)
+    check(table, gt, ot, tokens, ctx, S, hidden)
+    _, _, ln = ot.lookup(tokens, ctx, S)
+    assert set(ln.tolist()) == {0} | set(lengths)
+    mask, _ = check_multi(table, gt, ot, tokens, ctx, S, hidden, tfe.TFE_WEIGHT_LENGTH)
+    if len(lengths) == 2:  # both lengths matched at some position
+        assert (mask == (1 | 1 << (lengths[1] - lengths[0]))).any()
+    gt.close()
+
+
 def test_empty_table_and_empty_batch():
     table = synth.PhraseTable(np.zeros((0, 3), np.int32), np.zeros(0, np.uint8), 2, 3, synth.BF16,
                               0)
