@@ -80,7 +80,7 @@ MULTI_SOURCES = ("paper_2607_07388_amd/csrc/tfe_multi.hip",
 # K = 128): k_head_logits + k_head_rows, from the passes in
 # profiles/k_head_logits_rows_v151936_d1024_b64_k128.md.
 PROFILED_TRAFFIC_HEAD = {
-    "sources_sha256": "cbe925735db8887667a45b78ef1fa2b691951ab83046562c870fae14524467d9",
+    "sources_sha256": "a974fe4357de216f1cc8bccb408f007f145b3e7eaf98ff8d07141076c35d223a",
     "bytes_per_launch": 372542834,
 }
 HEAD_SOURCES = ("paper_2607_07388_amd/csrc/tfe_head.hip",

@@ -405,6 +405,7 @@ __global__ __launch_bounds__(kRowThreads) void k_head_rows(const HeadArgs a) {
     // answer lies in those tiles, so the K-th largest key itself is not
     // needed.
     constexpr uint32_t kStopCand = 192;
+    static_assert(kStopCand <= kHeadMaxK, "candidate tiles must fit s_tiles");
     const uint32_t dhi = hmin ^ hmax;
     const int top = dhi ? 63 - __builtin_clz(dhi) : 31;  // highest differing bit (low word: 31)
     const int shift0 = max(top - 7, 0);
