@@ -274,6 +274,51 @@ def test_tiered_4grams_pads_both_launch_shapes(fill):
     res.close()
 
 
+@pytest.mark.parametrize("dtype,dim", [(synth.BF16, 512), (synth.BF16, 1024), (synth.BF16, 2048),
+                                       (synth.BF16, 4096), (synth.F32, 256), (synth.F32, 2048)])
+def test_tiered_row_widths_call_sizes_in_place(dtype, dim):
+    """Every row width through both launch shapes of a tiered lookup (calls
+    of at most 64 positions: the single-block probe + residency kernel;
+    longer calls: the wide probe and the grouped resolve), then the inject:
+    calls of 1, 17, 64 and 65 positions, in place and out of place, on a
+    24-row cache, so cached, newly filled, directly read and unmatched
+    positions all occur.  Outputs equal the oracle and a resident copy byte
+    for byte; statistics equal the model."""
+    from .test_gpu_parity import small_table
+    vocab = 6
+    table = small_table(77 + dim, vocab, [(2, 30), (3, 200)], dtype, dim, 3)
+    res = H.GpuTable(table)
+    ot = H.oracle_table(table)
+    C, pre = 24, 8
+    tier = TieredTable(table, C, pre)
+    esz = 2 if dtype == synth.BF16 else 4
+    model = LruModel(C, pre, dim * esz)
+    rng = np.random.default_rng(dim + dtype)
+    view = torch.int16 if dtype == synth.BF16 else torch.int32
+    for step, (T, inplace) in enumerate([(64, False), (1, True), (17, False), (65, True),
+                                         (64, True), (17, True), (1, False), (65, False)]):
+        tokens = rng.integers(-1, vocab + 1, (T, 4)).astype(np.int32)
+        hidden = synth.normal_range(8, 900 + step, 0, T, dim, 1.0, dtype)
+        tok = torch.from_numpy(tokens).cuda()
+        h1, h2 = H.to_device(hidden, dtype), H.to_device(hidden, dtype)
+        o1, o2 = H.Outputs(T, dim, dtype), H.Outputs(T, dim, dtype)
+        out1 = H.run(res, tok, T, 3, 1, h1, o1, inplace=inplace)
+        out2 = h2 if inplace else o2.out
+        tfe.tfe_lookup_inject(tier.handle, tok, T, 3, 1, h2, out2, o2.hit, o2.slot, o2.len,
+                              tfe.TFE_GATE_SIGMOID, 1.0, H.cur_stream())
+        torch.cuda.synchronize()
+        assert torch.equal(o1.hit, o2.hit) and torch.equal(o1.slot, o2.slot)
+        assert torch.equal(o1.len, o2.len)
+        assert out1.view(view).equal(out2.view(view)), (T, inplace)
+        hit, row, ln, want = H.oracle_answer(table, ot, tokens, 3, 1, hidden)
+        np.testing.assert_array_equal(o2.slot.cpu().numpy(), row)
+        H.assert_close(H.to_host(out2, dtype), want, dtype)
+        model.lookup([int(r) for r in row])
+        check_stats(tier, model)
+    tier.close()
+    res.close()
+
+
 def test_tiered_load_errors():
     table, _ = synth.config1()
     vals = table.all_values()
