@@ -99,6 +99,21 @@ D = 1024
 ESZ = 2  # bf16
 
 
+def host_cpu():
+    """The host processor the CPU baseline ran on: model name and the
+    threads the operating system exposes."""
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return {"host_cpu": model, "host_threads": os.cpu_count()}
+
+
 def algorithmic_bytes(T, hits, keys, window):
     """Bytes the method must move for T positions (bf16, out of place):
     hidden row in and out, one value row and one row id per hit, one 8-byte
@@ -380,7 +395,7 @@ def main():
             "value": rows_done / csec,
             "unit": "tokens/s",
             "cores": 1,
-            "kind": "oracle",
+            "kind": "oracle", **host_cpu(),
             "sample": "%d passes of std::map lookup + double-precision gate/inject over one "
                       "%d-row stacked decode set (%.1f s, single thread)"
                       % (rows_done // B, B, csec),
@@ -415,6 +430,7 @@ def main():
         psec = time.perf_counter() - c0
         result["cpu_baseline_threads"] = {
             "value": sum(counts) / psec, "unit": "tokens/s", "cores": nthr, "kind": "oracle",
+            **host_cpu(),
             "sample": "the same passes with the set's rows split over %d threads (%.1f s)"
                       % (nthr, psec)}
     gt.close()
@@ -488,7 +504,7 @@ def finish_multi(args, table, gt, sets, mslots, B, ctx, S, window, L, tokens_per
             "value": done / csec,
             "unit": "tokens/s",
             "cores": 1,
-            "kind": "oracle",
+            "kind": "oracle", **host_cpu(),
             "sample": "%d passes of the all-matches std::map lookup + double-precision weighted "
                       "inject over one %d-row stacked decode set (%.1f s, single thread)"
                       % (done // B, B, csec),
@@ -589,7 +605,7 @@ def run_head(args):
             "value": done / B / csec,
             "unit": "calls/s",
             "cores": 1,
-            "kind": "oracle",
+            "kind": "oracle", **host_cpu(),
             "sample": "%d of the 64 rows of one call (double-precision logits over the full "
                       "vocabulary + partial sort), %.1f s, single thread, scaled to calls"
                       % (done, csec),
@@ -693,6 +709,7 @@ def run_build(args):
         csec = time.perf_counter() - c0
         result["cpu_baseline"] = {
             "value": done / csec, "unit": "tokens/s", "cores": 1, "kind": "oracle",
+            **host_cpu(),
             "sample": "2-gram top-2^19 of the first 2^20 tokens of the stream, repeated "
                       "(%.1f s, single thread)" % csec}
     print(json.dumps(result))
