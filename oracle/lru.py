@@ -12,7 +12,7 @@ Policy (the precise reading; a call is one lookup or one prefetch):
 * The cache has C slots.  At load, slot s holds row s for s < prefill; the
   recency order from least to most recent is: empty slots by ascending slot,
   then filled slots by descending row (the least frequent row goes first).
-* Lookup: positions are taken in consecutive groups of GROUP = 1024.  In a
+* Lookup: positions are taken in consecutive groups of GROUP = 4096.  In a
   group, every matched row that is cached marks its slot referenced; then the
   distinct matched rows that are not cached, in order of first position, each
   take the least recent slot that is not referenced in this call (its old row
@@ -36,7 +36,7 @@ Policy (the precise reading; a call is one lookup or one prefetch):
 """
 import collections
 
-GROUP = 1024
+GROUP = 4096
 
 
 class LruModel:

@@ -160,7 +160,9 @@ static tfe_status load_tiered(tfe_table* t, const tfe_table_desc* d, hipStream_t
     t->h_values_dev = dp;
   }
   TFE_TRY(dev_alloc((char**)&t->d_cache, (size_t)C * row_bytes, "HBM cache"));
-  TFE_TRY(dev_alloc(&t->d_where, (size_t)P, "residency map"));
+  // At least one entry: the resolve kernels read entry 0 unconditionally.
+  const size_t where_n = P > 0 ? (size_t)P : 1;
+  TFE_TRY(dev_alloc(&t->d_where, where_n, "residency map"));
   TFE_TRY(dev_alloc(&t->d_owner, (size_t)C, "slot owners"));
   TFE_TRY(dev_alloc(&t->d_stamp, (size_t)C, "slot stamps"));
   TFE_TRY(dev_alloc(&t->d_filled_at, (size_t)C, "slot fill stamps"));
@@ -169,7 +171,7 @@ static tfe_status load_tiered(tfe_table* t, const tfe_table_desc* d, hipStream_t
   TFE_TRY(dev_alloc(&t->d_ring, t->ring_cap, "recency ring"));
   TFE_TRY(dev_alloc(&t->d_ring2, t->ring_cap, "recency ring"));
   TFE_TRY(dev_alloc(&t->d_ctl, 1, "tier control block"));
-  TFE_HIP(hipMemsetAsync(t->d_where, 0xFF, (size_t)P * sizeof(int32_t), stream), "init");
+  TFE_HIP(hipMemsetAsync(t->d_where, 0xFF, where_n * sizeof(int32_t), stream), "init");
   TFE_HIP(hipMemsetAsync(t->d_ctl, 0, sizeof(tfe::TierCtl), stream), "init");
   tfe::TierArgs a = tier_args(t);
   TFE_HIP(tfe::launch_tier_init(a, (uint32_t)C, (uint32_t)d->prefill_rows, stream), "init launch");

@@ -163,19 +163,194 @@ __device__ bool first_of_row(int32_t r, uint32_t pos, int32_t* hkey, uint32_t* h
   return first;
 }
 
+// Versions of the block helpers for N items per thread: item k of thread x
+// stands for index k * kResolveThreads + x, and counts and minima follow
+// that index order.
+//
+// Ranks of the set flags (rank[k] = set flags at lower indices) and their
+// total.  All threads must call it.
+template <int N>
+__device__ __forceinline__ void block_count_n(const bool* f, uint32_t* rank, uint32_t* total) {
+  static_assert(kWaves == 16, "one DPP row holds the per-wave counts");
+  __shared__ uint32_t s_n[N][kWaves];
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  uint64_t m[N];
+#pragma unroll
+  for (int k = 0; k < N; ++k) {
+    m[k] = __builtin_amdgcn_ballot_w64(f[k]);
+    if (lane == 0) s_n[k][wave] = (uint32_t)__builtin_popcountll(m[k]);
+  }
+  __syncthreads();
+  // Lane w < 16 holds wave w's count; an inclusive scan along the row
+  // (DPP shifts by 1, 2, 4, 8) gives every wave's offset by readlane.
+  uint32_t run = 0;
+#pragma unroll
+  for (int k = 0; k < N; ++k) {
+    uint32_t x = lane < kWaves ? s_n[k][lane] : 0u;
+    x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x111, 0xF, 0xF, false);  // row_shr:1
+    x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x112, 0xF, 0xF, false);  // row_shr:2
+    x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x114, 0xF, 0xF, false);  // row_shr:4
+    x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x118, 0xF, 0xF, false);  // row_shr:8
+    const uint32_t before = wave > 0 ? (uint32_t)__builtin_amdgcn_readlane((int)x, wave - 1) : 0u;
+    const uint32_t all = (uint32_t)__builtin_amdgcn_readlane((int)x, kWaves - 1);
+    rank[k] = run + before + lanes_below(m[k]);
+    run += all;
+  }
+  __syncthreads();
+  *total = run;
+}
+
+// Lowest index whose flag is set, or 0xFFFFFFFF.  All threads must call it.
+template <int N>
+__device__ __forceinline__ uint32_t block_first_n(const bool* f) {
+  __shared__ uint32_t s_f[kWaves];
+  uint32_t best = 0xFFFFFFFFu;
+#pragma unroll
+  for (int k = N - 1; k >= 0; --k) {
+    const uint64_t m = __builtin_amdgcn_ballot_w64(f[k]);
+    if (m) best = (uint32_t)k * kResolveThreads + (threadIdx.x & ~63u) + (uint32_t)__builtin_ctzll(m);
+  }
+  if ((threadIdx.x & 63) == 0) s_f[threadIdx.x >> 6] = best;
+  __syncthreads();
+  uint32_t r = 0xFFFFFFFFu;
+#pragma unroll
+  for (int w = 0; w < kWaves; ++w) r = min(r, s_f[w]);
+  __syncthreads();
+  return r;
+}
+
+// pop_victims over windows of N kResolveThreads ring entries per round.
+template <int N>
+__device__ __forceinline__ uint32_t pop_victims_n(const TierArgs& t, uint32_t need, uint32_t* vict) {
+  __shared__ unsigned long long s_tail, s_head, s_last;
+  __shared__ uint32_t s_got, s_stop;
+  if (threadIdx.x == 0) {
+    s_tail = t.ctl->tail;
+    s_head = t.ctl->head;
+    s_got = 0;
+    s_stop = 0;
+  }
+  __syncthreads();
+  for (;;) {
+    const uint32_t got = s_got;
+    const unsigned long long base = s_tail, head = s_head;
+    if (got >= need || s_stop || base >= head) break;
+    // Unconditional loads (the ring index wraps in bounds; entries past the
+    // head read slot 0's stamp), issued back to back.
+    uint64_t e[N];
+#pragma unroll
+    for (int k = 0; k < N; ++k) {
+      const unsigned long long i = base + (uint64_t)k * kResolveThreads + threadIdx.x;
+      const uint64_t x = t.ring[i & t.ring_mask];
+      e[k] = i < head ? x : 0;
+    }
+    uint32_t st_now[N];
+#pragma unroll
+    for (int k = 0; k < N; ++k) st_now[k] = t.stamp[(uint32_t)(e[k] >> 32)];
+    bool live[N], cur[N];
+#pragma unroll
+    for (int k = 0; k < N; ++k) {
+      const unsigned long long i = base + (uint64_t)k * kResolveThreads + threadIdx.x;
+      const bool in = i < head;
+      cur[k] = in && (uint32_t)e[k] == t.clock;  // entries of this call end the search
+      live[k] = in && !cur[k] && st_now[k] == (uint32_t)e[k];
+    }
+    uint32_t rank[N], nlive;
+    block_count_n<N>(live, rank, &nlive);
+    const uint32_t first_cur = block_first_n<N>(cur);
+    const uint32_t take = nlive < need - got ? nlive : need - got;
+#pragma unroll
+    for (int k = 0; k < N; ++k) {
+      if (live[k] && rank[k] < take) {
+        vict[got + rank[k]] = (uint32_t)(e[k] >> 32);
+        if (rank[k] == take - 1) s_last = base + (uint64_t)k * kResolveThreads + threadIdx.x;
+      }
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      if (take > 0 && take == need - got) {
+        s_tail = s_last + 1;
+        s_got = need;
+      } else {
+        s_got = got + take;
+        if (first_cur != 0xFFFFFFFFu) {
+          s_tail = base + first_cur;
+          s_stop = 1;
+        } else {
+          const unsigned long long end = base + (uint64_t)N * kResolveThreads;
+          s_tail = head < end ? head : end;
+        }
+      }
+    }
+    __syncthreads();
+  }
+  const uint32_t got = s_got;
+  if (threadIdx.x == 0) t.ctl->tail = s_tail;
+  __syncthreads();
+  return got;
+}
+
+// first_of_row for N positions per thread and an LDS table of HS entries
+// (a power of two, at least twice the block's positions).
+template <int N, int HS>
+__device__ __forceinline__ void first_of_rows(const int32_t* r, const uint32_t* pos, int32_t* hkey,
+                              uint32_t* hpos, int* hidx, bool* first) {
+  static_assert((HS & (HS - 1)) == 0 && HS >= 2 * N * kResolveThreads, "hash size");
+  constexpr int shift = 32 - __builtin_ctz(HS);
+  for (int i = threadIdx.x; i < HS; i += kResolveThreads) {
+    hkey[i] = -1;
+    hpos[i] = 0xFFFFFFFFu;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int k = 0; k < N; ++k) {
+    int h = -1;
+    if (r[k] >= 0) {
+      h = (int)(((uint32_t)r[k] * 2654435761u) >> shift);
+      for (;;) {
+        const int old = atomicCAS(&hkey[h], -1, r[k]);
+        if (old == -1 || old == r[k]) break;
+        h = (h + 1) & (HS - 1);
+      }
+      atomicMin(&hpos[h], pos[k]);
+    }
+    hidx[k] = h;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int k = 0; k < N; ++k) first[k] = r[k] >= 0 && hpos[hidx[k]] == pos[k];
+}
+
+// Number of set flags in the wave, added once per wave to an LDS counter
+// (one atomic per wave instead of one per lane).
+__device__ __forceinline__ void wave_tally(bool f, uint32_t* counter) {
+  const uint64_t m = __builtin_amdgcn_ballot_w64(f);
+  if ((threadIdx.x & 63) == 0 && m) atomicAdd(counter, (uint32_t)__builtin_popcountll(m));
+}
+
 // Residency resolution of one lookup call (single block), positions in
-// groups of kResolveThreads in order.  Per position: slot_of (cache slot or
-// -1) and phase (0: cached before this call, read from the cache; 1: filled
-// in this call; 2: no slot free, not cached; 3: no match).  Rows of phases 1
-// and 2 are read from host memory by the inject; phase-1 rows are also
-// copied into their slot on the side stream for later calls.
+// consecutive groups of kGroup = kGroupItems x kResolveThreads (thread x
+// handles positions base + k kResolveThreads + x), in order.  Per position:
+// slot_of (cache slot or -1) and phase (0: cached before this call, read from
+// the cache; 1: filled in this call; 2: no slot free, not cached; 3: no
+// match).  Rows of phases 1 and 2 are read from host memory by the inject;
+// phase-1 rows are also written into their slot, by the inject (inline
+// fill) or by a copy on the side stream.  Each group reads its rows' state,
+// then the ring window, then writes: a few dependent round trips per 4096
+// positions.
+constexpr int kGroupItems = 4;
+constexpr int kGroup = kGroupItems * kResolveThreads;
+constexpr int kGroupHash = 2 * kGroup;
+
 __global__ __launch_bounds__(kResolveThreads) void k_resolve_lookup(const TierArgs t, uint32_t T) {
-  __shared__ int32_t hkey[kHashSize];
-  __shared__ uint32_t hpos[kHashSize];
-  __shared__ int32_t hslot[kHashSize];  // per row: slot after this group (-1: none)
-  __shared__ uint8_t hphase[kHashSize];
-  __shared__ uint8_t hcached[kHashSize];  // per row: cached when the group began
-  __shared__ uint32_t vict[kResolveThreads];
+  constexpr int N = kGroupItems;
+  __shared__ int32_t hkey[kGroupHash];
+  __shared__ uint32_t hpos[kGroupHash];
+  __shared__ int32_t hslot[kGroupHash];    // per row: slot after this group (-1: none)
+  __shared__ uint8_t hphase[kGroupHash];
+  __shared__ uint8_t hcached[kGroupHash];  // per row: cached when the group began
+  __shared__ uint32_t vict[kGroup];
   __shared__ unsigned long long s_njobs, s_head;
   __shared__ uint32_t s_cnt[5];  // hits, cache hits, prefetch used, host-served, fills
   if (threadIdx.x == 0) {
@@ -183,71 +358,124 @@ __global__ __launch_bounds__(kResolveThreads) void k_resolve_lookup(const TierAr
     s_head = t.ctl->head;
     for (int i = 0; i < 5; ++i) s_cnt[i] = 0;
   }
-  for (uint32_t base = 0; base < T; base += kResolveThreads) {
-    const uint32_t p = base + threadIdx.x;
-    const bool valid = p < T;
-    const int32_t r = valid ? t.row_of[p] : -1;
-    int h;
-    const bool first = first_of_row(r, p, hkey, hpos, &h);
+  for (uint32_t base = 0; base < T; base += kGroup) {
+    // Per-item flags are bit k of a per-thread word (registers, not lane
+    // masks); position of item k: base + k kResolveThreads + threadIdx.x.
+    int32_t r[N];
+    uint32_t pos[N];
+#pragma unroll
+    for (int k = 0; k < N; ++k) {
+      pos[k] = base + k * kResolveThreads + threadIdx.x;
+      const int32_t rr = t.row_of[pos[k] < T ? pos[k] : 0u];
+      r[k] = pos[k] < T ? rr : -1;
+    }
+    int h[N];
+    bool fb[N];
+    first_of_rows<N, kGroupHash>(r, pos, hkey, hpos, h, fb);
+    uint32_t f_first = 0;
+#pragma unroll
+    for (int k = 0; k < N; ++k) f_first |= fb[k] ? 1u << k : 0u;
     // First occurrences read the row's slot; a cached row's slot becomes
-    // referenced (a stamp of this call keeps it from being a victim).
-    int32_t s0 = -1;
-    bool append = false;
-    if (first) {
-      s0 = t.where[r];
-      hcached[h] = s0 >= 0;
-      if (s0 >= 0) {
+    // referenced (a stamp of this call keeps it from being a victim).  The
+    // rows of a group are distinct and so are their slots, so all reads go
+    // before the writes; they are unconditional (index 0 where there is
+    // nothing to read) so that they issue back to back.
+    int32_t s0[N];
+#pragma unroll
+    for (int k = 0; k < N; ++k) {
+      const int32_t w = t.where[(uint32_t)max(r[k], 0)];
+      s0[k] = (f_first >> k) & 1u ? w : -1;
+    }
+    uint32_t st_old[N], fat[N], pf[N];
+#pragma unroll
+    for (int k = 0; k < N; ++k) {
+      const uint32_t sl = (uint32_t)max(s0[k], 0);
+      st_old[k] = t.stamp[sl];
+      fat[k] = t.filled_at[sl];
+      pf[k] = t.pref[sl];
+    }
+    uint32_t f_app = 0, f_miss = 0;
+#pragma unroll
+    for (int k = 0; k < N; ++k) {
+      bool used = false;
+      if ((f_first >> k) & 1u) hcached[h[k]] = s0[k] >= 0;
+      if (s0[k] >= 0) {
         // Only a later group of this call can find its own stamp here.
-        append = base == 0 || t.stamp[s0] != t.clock;
-        t.stamp[s0] = t.clock;
-        hslot[h] = s0;
-        hphase[h] = (base != 0 && t.filled_at[s0] == t.clock) ? 1 : 0;
-        if (t.pref[s0]) {
-          t.pref[s0] = 0;
-          atomicAdd(&s_cnt[2], 1u);
+        if (base == 0 || st_old[k] != t.clock) f_app |= 1u << k;
+        t.stamp[s0[k]] = t.clock;
+        hslot[h[k]] = s0[k];
+        hphase[h[k]] = (base != 0 && fat[k] == t.clock) ? 1 : 0;
+        if (pf[k]) {
+          t.pref[s0[k]] = 0;
+          used = true;
         }
+      } else if ((f_first >> k) & 1u) {
+        f_miss |= 1u << k;
+      }
+      wave_tally(used, &s_cnt[2]);
+    }
+    __syncthreads();
+    bool mb[N];
+#pragma unroll
+    for (int k = 0; k < N; ++k) mb[k] = (f_miss >> k) & 1u;
+    uint32_t mrank[N], need;
+    block_count_n<N>(mb, mrank, &need);
+    const uint32_t got = need ? pop_victims_n<N>(t, need, vict) : 0;
+    uint32_t f_fill = 0;
+#pragma unroll
+    for (int k = 0; k < N; ++k) f_fill |= ((f_miss >> k) & 1u) && mrank[k] < got ? 1u << k : 0u;
+    uint32_t v[N];
+    int32_t old[N];
+#pragma unroll
+    for (int k = 0; k < N; ++k) {
+      v[k] = (f_fill >> k) & 1u ? vict[mrank[k]] : 0u;
+      old[k] = t.owner[v[k]];
+    }
+#pragma unroll
+    for (int k = 0; k < N; ++k) {
+      if ((f_fill >> k) & 1u) {
+        // Evicted rows were cached and filled rows were not: the two sets
+        // are disjoint, so these writes never collide.
+        if (old[k] >= 0) t.where[old[k]] = -1;
+        t.owner[v[k]] = r[k];
+        t.where[r[k]] = (int32_t)v[k];
+        t.stamp[v[k]] = t.clock;
+        t.filled_at[v[k]] = t.clock;
+        t.pref[v[k]] = 0;
+        t.jobs[s_njobs + mrank[k]] = TierJob{r[k], (int32_t)v[k]};
+        hslot[h[k]] = (int32_t)v[k];
+        hphase[h[k]] = 1;
+        f_app |= 1u << k;
+      } else if ((f_miss >> k) & 1u) {
+        hslot[h[k]] = -1;
+        hphase[h[k]] = 2;
       }
     }
     __syncthreads();
-    const bool miss_first = first && s0 < 0;
-    uint32_t need;
-    const uint32_t mrank = block_count(miss_first, &need);
-    const uint32_t got = need ? pop_victims(t, need, vict) : 0;
-    if (miss_first) {
-      if (mrank < got) {
-        const uint32_t v = vict[mrank];
-        const int32_t old = t.owner[v];
-        if (old >= 0) t.where[old] = -1;
-        t.owner[v] = r;
-        t.where[r] = (int32_t)v;
-        t.stamp[v] = t.clock;
-        t.filled_at[v] = t.clock;
-        t.pref[v] = 0;
-        t.jobs[s_njobs + mrank] = TierJob{r, (int32_t)v};
-        hslot[h] = (int32_t)v;
-        hphase[h] = 1;
-        append = true;
-      } else {
-        hslot[h] = -1;
-        hphase[h] = 2;
+#pragma unroll
+    for (int k = 0; k < N; ++k) {
+      const bool valid = pos[k] < T;
+      const bool m = r[k] >= 0;
+      const int32_t s1 = m ? hslot[h[k]] : -1;
+      const uint8_t ph = m ? hphase[h[k]] : 3;
+      const bool writes = t.fill_inline && ((f_fill >> k) & 1u);
+      if (valid) {
+        t.slot_of[pos[k]] = s1;
+        t.phase[pos[k]] = writes ? (uint8_t)(ph | kPhaseWrite) : ph;
       }
+      wave_tally(m, &s_cnt[0]);
+      wave_tally(m && hcached[h[k]], &s_cnt[1]);
+      wave_tally(m && ph != 0, &s_cnt[3]);
     }
-    __syncthreads();
-    if (valid) {
-      const int32_t s1 = r >= 0 ? hslot[h] : -1;
-      const uint8_t ph = r >= 0 ? hphase[h] : 3;
-      const bool writes = t.fill_inline && miss_first && mrank < got;
-      t.slot_of[p] = s1;
-      t.phase[p] = writes ? (uint8_t)(ph | kPhaseWrite) : ph;
-      if (r >= 0) {
-        atomicAdd(&s_cnt[0], 1u);
-        if (hcached[h]) atomicAdd(&s_cnt[1], 1u);
-        if (ph != 0) atomicAdd(&s_cnt[3], 1u);
-      }
-    }
-    uint32_t napp;
-    const uint32_t arank = block_count(append, &napp);
-    if (append) t.ring[(s_head + arank) & t.ring_mask] = ring_entry((uint32_t)hslot[h], t.clock);
+    bool ab[N];
+#pragma unroll
+    for (int k = 0; k < N; ++k) ab[k] = (f_app >> k) & 1u;
+    uint32_t arank[N], napp;
+    block_count_n<N>(ab, arank, &napp);
+#pragma unroll
+    for (int k = 0; k < N; ++k)
+      if ((f_app >> k) & 1u)
+        t.ring[(s_head + arank[k]) & t.ring_mask] = ring_entry((uint32_t)hslot[h[k]], t.clock);
     __syncthreads();
     if (threadIdx.x == 0) {
       s_head += napp;

@@ -198,21 +198,26 @@ def test_tiny_cache_direct_reads_and_ring_compaction(w2_tables):
 
 @pytest.mark.parametrize("fill", FILLS)
 def test_multi_group_lookup_and_in_place(w2_tables, fill):
-    """3000 positions (three resolve groups of 1024) with many repeats, in
-    place, against a cache that fits part of them."""
+    """9000 positions (resolve groups of 4096, 4096 and 808) with many
+    repeats, in place, against a cache that fits part of them: rows filled by
+    one group and referenced by a later one, victims taken across several
+    ring windows."""
+    from oracle.lru import GROUP
     table, res, ot = w2_tables
-    C, pre = 1500, 700
+    T = 9000
+    assert GROUP < T < 3 * GROUP
+    C, pre = 4000, 1800
     tier = TieredTable(table, C, pre, fill=fill)
     model = LruModel(C, pre, table.dim * 2, fill_rereads=fill == tfe.TFE_FILL_SIDE_STREAM)
     for step in range(3):
-        batch = synth.decode_batch(1, 3000, set_index=60 + step)
+        batch = synth.decode_batch(1, T, set_index=60 + step)
         hidden = batch.hidden()
         tok = torch.from_numpy(batch.tokens).cuda()
         h1 = H.to_device(hidden, synth.BF16)
         h2 = h1.clone()
-        o1, o2 = H.Outputs(3000, 1024, synth.BF16), H.Outputs(3000, 1024, synth.BF16)
-        H.run(res, tok, 3000, 2, 1, h1, o1, inplace=True)
-        tfe.tfe_lookup_inject(tier.handle, tok, 3000, 2, 1, h2, h2, o2.hit, o2.slot, o2.len, 0,
+        o1, o2 = H.Outputs(T, 1024, synth.BF16), H.Outputs(T, 1024, synth.BF16)
+        H.run(res, tok, T, 2, 1, h1, o1, inplace=True)
+        tfe.tfe_lookup_inject(tier.handle, tok, T, 2, 1, h2, h2, o2.hit, o2.slot, o2.len, 0,
                               1.0, H.cur_stream())
         torch.cuda.synchronize()
         assert torch.equal(h1.view(torch.int16), h2.view(torch.int16))
