@@ -169,10 +169,15 @@ __device__ bool first_of_row(int32_t r, uint32_t pos, int32_t* hkey, uint32_t* h
 //
 // Ranks of the set flags (rank[k] = set flags at lower indices) and their
 // total.  All threads must call it.
+//
+// With g non-null, *first also receives the lowest index whose g flag is
+// set (0xFFFFFFFF if none), from the same exchange.
 template <int N>
-__device__ __forceinline__ void block_count_n(const bool* f, uint32_t* rank, uint32_t* total) {
+__device__ __forceinline__ void block_count_n(const bool* f, uint32_t* rank, uint32_t* total,
+                                              const bool* g = nullptr, uint32_t* first = nullptr) {
   static_assert(kWaves == 16, "one DPP row holds the per-wave counts");
   __shared__ uint32_t s_n[N][kWaves];
+  __shared__ uint32_t s_f[kWaves];
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   uint64_t m[N];
@@ -181,7 +186,23 @@ __device__ __forceinline__ void block_count_n(const bool* f, uint32_t* rank, uin
     m[k] = __builtin_amdgcn_ballot_w64(f[k]);
     if (lane == 0) s_n[k][wave] = (uint32_t)__builtin_popcountll(m[k]);
   }
+  if (g) {
+    uint32_t best = 0xFFFFFFFFu;
+#pragma unroll
+    for (int k = N - 1; k >= 0; --k) {
+      const uint64_t mg = __builtin_amdgcn_ballot_w64(g[k]);
+      if (mg) best = (uint32_t)k * kResolveThreads + (uint32_t)wave * 64u + (uint32_t)__builtin_ctzll(mg);
+    }
+    if (lane == 0) s_f[wave] = best;
+  }
   __syncthreads();
+  if (g) {
+    uint32_t x = lane < kWaves ? s_f[lane] : 0xFFFFFFFFu;
+    uint32_t r = x;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) r = min(r, (uint32_t)__builtin_amdgcn_readlane((int)x, w));
+    *first = r;
+  }
   // Lane w < 16 holds wave w's count; an inclusive scan along the row
   // (DPP shifts by 1, 2, 4, 8) gives every wave's offset by readlane.
   uint32_t run = 0;
@@ -201,28 +222,11 @@ __device__ __forceinline__ void block_count_n(const bool* f, uint32_t* rank, uin
   *total = run;
 }
 
-// Lowest index whose flag is set, or 0xFFFFFFFF.  All threads must call it.
+// pop_victims over windows of N kResolveThreads ring entries per round; the
+// row each victim slot holds is read with its stamp and kept in vown[].
 template <int N>
-__device__ __forceinline__ uint32_t block_first_n(const bool* f) {
-  __shared__ uint32_t s_f[kWaves];
-  uint32_t best = 0xFFFFFFFFu;
-#pragma unroll
-  for (int k = N - 1; k >= 0; --k) {
-    const uint64_t m = __builtin_amdgcn_ballot_w64(f[k]);
-    if (m) best = (uint32_t)k * kResolveThreads + (threadIdx.x & ~63u) + (uint32_t)__builtin_ctzll(m);
-  }
-  if ((threadIdx.x & 63) == 0) s_f[threadIdx.x >> 6] = best;
-  __syncthreads();
-  uint32_t r = 0xFFFFFFFFu;
-#pragma unroll
-  for (int w = 0; w < kWaves; ++w) r = min(r, s_f[w]);
-  __syncthreads();
-  return r;
-}
-
-// pop_victims over windows of N kResolveThreads ring entries per round.
-template <int N>
-__device__ __forceinline__ uint32_t pop_victims_n(const TierArgs& t, uint32_t need, uint32_t* vict) {
+__device__ __forceinline__ uint32_t pop_victims_n(const TierArgs& t, uint32_t need, uint32_t* vict,
+                                                  int32_t* vown) {
   __shared__ unsigned long long s_tail, s_head, s_last;
   __shared__ uint32_t s_got, s_stop;
   if (threadIdx.x == 0) {
@@ -246,8 +250,12 @@ __device__ __forceinline__ uint32_t pop_victims_n(const TierArgs& t, uint32_t ne
       e[k] = i < head ? x : 0;
     }
     uint32_t st_now[N];
+    int32_t own[N];
 #pragma unroll
-    for (int k = 0; k < N; ++k) st_now[k] = t.stamp[(uint32_t)(e[k] >> 32)];
+    for (int k = 0; k < N; ++k) {
+      st_now[k] = t.stamp[(uint32_t)(e[k] >> 32)];
+      own[k] = t.owner[(uint32_t)(e[k] >> 32)];
+    }
     bool live[N], cur[N];
 #pragma unroll
     for (int k = 0; k < N; ++k) {
@@ -256,14 +264,14 @@ __device__ __forceinline__ uint32_t pop_victims_n(const TierArgs& t, uint32_t ne
       cur[k] = in && (uint32_t)e[k] == t.clock;  // entries of this call end the search
       live[k] = in && !cur[k] && st_now[k] == (uint32_t)e[k];
     }
-    uint32_t rank[N], nlive;
-    block_count_n<N>(live, rank, &nlive);
-    const uint32_t first_cur = block_first_n<N>(cur);
+    uint32_t rank[N], nlive, first_cur;
+    block_count_n<N>(live, rank, &nlive, cur, &first_cur);
     const uint32_t take = nlive < need - got ? nlive : need - got;
 #pragma unroll
     for (int k = 0; k < N; ++k) {
       if (live[k] && rank[k] < take) {
         vict[got + rank[k]] = (uint32_t)(e[k] >> 32);
+        vown[got + rank[k]] = own[k];
         if (rank[k] == take - 1) s_last = base + (uint64_t)k * kResolveThreads + threadIdx.x;
       }
     }
@@ -351,6 +359,7 @@ __global__ __launch_bounds__(kResolveThreads) void k_resolve_lookup(const TierAr
   __shared__ uint8_t hphase[kGroupHash];
   __shared__ uint8_t hcached[kGroupHash];  // per row: cached when the group began
   __shared__ uint32_t vict[kGroup];
+  __shared__ int32_t vown[kGroup];  // row held by each victim slot
   __shared__ unsigned long long s_njobs, s_head;
   __shared__ uint32_t s_cnt[5];  // hits, cache hits, prefetch used, host-served, fills
   if (threadIdx.x == 0) {
@@ -420,30 +429,26 @@ __global__ __launch_bounds__(kResolveThreads) void k_resolve_lookup(const TierAr
     for (int k = 0; k < N; ++k) mb[k] = (f_miss >> k) & 1u;
     uint32_t mrank[N], need;
     block_count_n<N>(mb, mrank, &need);
-    const uint32_t got = need ? pop_victims_n<N>(t, need, vict) : 0;
+    const uint32_t got = need ? pop_victims_n<N>(t, need, vict, vown) : 0;
     uint32_t f_fill = 0;
 #pragma unroll
     for (int k = 0; k < N; ++k) f_fill |= ((f_miss >> k) & 1u) && mrank[k] < got ? 1u << k : 0u;
-    uint32_t v[N];
-    int32_t old[N];
-#pragma unroll
-    for (int k = 0; k < N; ++k) {
-      v[k] = (f_fill >> k) & 1u ? vict[mrank[k]] : 0u;
-      old[k] = t.owner[v[k]];
-    }
 #pragma unroll
     for (int k = 0; k < N; ++k) {
       if ((f_fill >> k) & 1u) {
         // Evicted rows were cached and filled rows were not: the two sets
-        // are disjoint, so these writes never collide.
-        if (old[k] >= 0) t.where[old[k]] = -1;
-        t.owner[v[k]] = r[k];
-        t.where[r[k]] = (int32_t)v[k];
-        t.stamp[v[k]] = t.clock;
-        t.filled_at[v[k]] = t.clock;
-        t.pref[v[k]] = 0;
-        t.jobs[s_njobs + mrank[k]] = TierJob{r[k], (int32_t)v[k]};
-        hslot[h[k]] = (int32_t)v[k];
+        // are disjoint, so these writes never collide.  A victim is never a
+        // slot of this call, so its owner is still the one the pop read.
+        const uint32_t vk = vict[mrank[k]];
+        const int32_t old = vown[mrank[k]];
+        if (old >= 0) t.where[old] = -1;
+        t.owner[vk] = r[k];
+        t.where[r[k]] = (int32_t)vk;
+        t.stamp[vk] = t.clock;
+        t.filled_at[vk] = t.clock;
+        t.pref[vk] = 0;
+        t.jobs[s_njobs + mrank[k]] = TierJob{r[k], (int32_t)vk};
+        hslot[h[k]] = (int32_t)vk;
         hphase[h[k]] = 1;
         f_app |= 1u << k;
       } else if ((f_miss >> k) & 1u) {
