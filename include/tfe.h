@@ -153,9 +153,10 @@ tfe_status tfe_table_free(tfe_table *table);
  *   match_len  DEVICE uint8 [B*S] or NULL: matched n, 0 where nothing matched.
  *   gate, scale: see tfe_gate.
  * Tiered tables read the rows that are not cached straight from pinned host
- * memory (zero-copy over PCIe) while an internal side stream inserts them
- * into the HBM cache for later calls; results do not depend on the cache
- * state. */
+ * memory (zero-copy over PCIe) and insert them into the HBM cache for later
+ * calls, from the copy the inject read (TFE_FILL_INLINE) or with a second
+ * read on an internal side stream (TFE_FILL_SIDE_STREAM); results do not
+ * depend on the cache state. */
 tfe_status tfe_lookup_inject(tfe_table *table, const int32_t *tokens, int32_t B, int32_t ctx,
                              int32_t S, const void *hidden_in, void *hidden_out,
                              uint8_t *hit_mask, int32_t *slot_ids, uint8_t *match_len,
@@ -188,10 +189,11 @@ tfe_status tfe_lookup_inject_multi(tfe_table *table, const int32_t *tokens, int3
  *               row, oldest first (tail_len >= n_max - 1 uses every length).
  *   candidates  DEVICE int32 [B x K]: predicted next tokens of each row.
  * For every row b and candidate c the phrases ending at c, i.e. the n-grams
- * (tail[b, tail_len-n+1 ..], c) for n = n_min..n_max, are looked up; those
- * present in the table and not cached are copied into the cache.  The work
- * runs on `side_stream` after the table's previous lookup; the next
- * tfe_lookup_inject waits for it. */
+ * (tail[b, tail_len-n+1 ..], c) for n = n_min..n_max, are looked up; the
+ * longest one present in the table (the phrase the next lookup selects if c
+ * is the next token) is copied into the cache unless it is cached already.
+ * The work runs on `side_stream` after the table's previous lookup; the
+ * next tfe_lookup_inject waits for it. */
 tfe_status tfe_prefetch(tfe_table *table, const int32_t *tail, int32_t tail_len,
                         const int32_t *candidates, int32_t B, int32_t K, void *side_stream);
 
