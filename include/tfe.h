@@ -28,6 +28,12 @@
  *     A failed HIP call returns TFE_ERR_HIP.  No C++ exception crosses the ABI.
  *   - A table handle is not thread-safe: calls on one handle must be issued
  *     from one host thread at a time.
+ *   - HIP graph capture: lookups on resident tables (tfe_lookup_inject,
+ *     tfe_lookup_inject_multi) and tfe_head_topk enqueue kernels only and may
+ *     be captured.  Lookups on tiered tables, tfe_prefetch,
+ *     tfe_prefetch_scored and tfe_ngram_top keep per-call host state or
+ *     synchronise; on a capturing stream they return TFE_ERR_UNSUPPORTED
+ *     without enqueuing anything.
  */
 #ifndef TFE_H_
 #define TFE_H_

@@ -27,6 +27,16 @@ tfe_status fail(tfe_status st, const char* fmt, ...) {
 
 void clear_error() { g_err[0] = 0; }
 
+tfe_status refuse_capture(hipStream_t stream, const char* what) {
+  hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+  const hipError_t e = hipStreamIsCapturing(stream, &cs);
+  if (e != hipSuccess) return fail(TFE_ERR_HIP, "%s: hipStreamIsCapturing: %s", what,
+                                   hipGetErrorString(e));
+  if (cs != hipStreamCaptureStatusNone)
+    return fail(TFE_ERR_UNSUPPORTED, "%s cannot be captured into a graph", what);
+  return TFE_OK;
+}
+
 static tfe_status hip_fail(hipError_t e, const char* what) {
   return fail(TFE_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
 }
@@ -245,6 +255,9 @@ static tfe_status reserve_ring(tfe_table* t, uint64_t appends, hipStream_t strea
 }
 
 static tfe_status lookup_tiered(tfe_table* t, const LookupArgs& look, hipStream_t stream) {
+  // The recency clock, the ring bound and the cross-stream events live on
+  // the host and change with every call: a replayed graph would reuse them.
+  TFE_TRY(refuse_capture(stream, "a lookup on a tiered table"));
   TFE_TRY(ensure_scratch(t, look.T));
   // Calls on one table are ordered: after the previous lookup (when it ran
   // on another stream) and after a pending prefetch.
@@ -295,6 +308,7 @@ static tfe_status prefetch_tiered(tfe_table* t, const int32_t* tail, int32_t tai
     return fail(TFE_ERR_UNSUPPORTED, "scored prefetch takes at most %u candidates",
                 tfe::scored_prefetch_max());
   TFE_TRY(check_device(t));
+  TFE_TRY(refuse_capture(side, "a prefetch"));
   TFE_TRY(ensure_scratch(t, (uint32_t)N));
   // After the table's last lookup (all work submitted to its stream so far),
   // its cache fill, and any earlier prefetch.

@@ -749,6 +749,11 @@ tfe_status ngram_top(const int32_t* tokens, int64_t N, int32_t vocab, int32_t n,
   if (N < n || top == 0) return TFE_OK;
   if (!tokens || !out_tuples || !out_counts)
     return fail(TFE_ERR_INVALID_ARG, "null tokens or outputs");
+  // Allocates scratch and waits for the stream: not capturable.
+  {
+    const tfe_status st = refuse_capture(s, "tfe_ngram_top");
+    if (st != TFE_OK) return st;
+  }
   const uint64_t nwin = (uint64_t)(N - n + 1);
   const bool wide = n == 4;
   Scratch sc(s);

@@ -14,6 +14,10 @@ namespace tfe {
 
 // Thread-local error message; fail() formats it and returns the status.
 tfe_status fail(tfe_status st, const char* fmt, ...);
+// TFE_ERR_UNSUPPORTED if `stream` is being captured into a graph (for calls
+// that keep per-call host state or synchronise), TFE_ERR_HIP if the query
+// fails, else TFE_OK.
+tfe_status refuse_capture(hipStream_t stream, const char* what);
 void clear_error();
 
 int64_t index_capacity(int64_t n, double lf);

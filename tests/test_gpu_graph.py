@@ -56,3 +56,61 @@ def test_captured_decode_steps_replay_exactly():
             assert torch.equal(o.hit.cpu(), wh) and torch.equal(o.slot.cpu(), ws)
     del g
     gt.close()
+
+
+def test_calls_with_host_state_refuse_capture():
+    """Lookups on tiered tables, prefetch and n-gram construction keep
+    per-call host state or synchronise: on a capturing stream they return
+    TFE_ERR_UNSUPPORTED and enqueue nothing, while a resident lookup in the
+    same capture is recorded and replays correctly; the tiered table still
+    works eagerly afterwards."""
+    from .test_gpu_tiered import TieredTable
+    table, batch = synth.config1()
+    res = H.GpuTable(table)
+    tier = TieredTable(table, 32, 0, adopt=False)
+    tok = torch.from_numpy(batch.tokens).cuda()
+    h = H.to_device(batch.hidden(), table.dtype)
+    o_res, o_tier = H.Outputs(batch.T, table.dim, table.dtype), H.Outputs(batch.T, table.dim,
+                                                                          table.dtype)
+    tail = tok[:, -2:].contiguous()
+    cand = torch.zeros((batch.B, 2), dtype=torch.int32, device="cuda")
+    tup = torch.zeros((8, 2), dtype=torch.int32, device="cuda")
+    cnt = torch.zeros(8, dtype=torch.int64, device="cuda")
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    statuses = []
+    with torch.cuda.graph(g):
+        s = torch.cuda.current_stream().cuda_stream
+        H.run(res, tok, batch.B, batch.ctx, batch.S, h, o_res, stream=s)
+        calls = [
+            lambda: tfe.tfe_lookup_inject(tier.handle, tok, batch.B, batch.ctx, batch.S, h,
+                                          o_tier.out, o_tier.hit, o_tier.slot, o_tier.len,
+                                          tfe.TFE_GATE_SIGMOID, 1.0, s),
+            lambda: tfe.tfe_prefetch(tier.handle, tail, 2, cand, batch.B, 2, s),
+            lambda: tfe.tfe_ngram_top(tok, tok.numel(), synth.V, 2, 0, 8, tup, cnt, s),
+        ]
+        for call in calls:
+            try:
+                call()
+                statuses.append(0)
+            except tfe.TfeError as e:
+                statuses.append(e.status)
+    assert statuses == [tfe.TFE_ERR_UNSUPPORTED] * 3
+    o_res.out.fill_(0)
+    o_res.slot.fill_(-7)
+    torch.cuda.synchronize()
+    g.replay()
+    torch.cuda.synchronize()
+    hit, row, ln, want = H.oracle_answer(table, H.oracle_table(table), batch.tokens, batch.ctx,
+                                         batch.S, batch.hidden())
+    np.testing.assert_array_equal(o_res.slot.cpu().numpy(), row)
+    H.assert_close(H.to_host(o_res.out, table.dtype), want, table.dtype)
+    tfe.tfe_lookup_inject(tier.handle, tok, batch.B, batch.ctx, batch.S, h, o_tier.out,
+                          o_tier.hit, o_tier.slot, o_tier.len, tfe.TFE_GATE_SIGMOID, 1.0,
+                          H.cur_stream())
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(o_tier.slot.cpu().numpy(), row)
+    H.assert_close(H.to_host(o_tier.out, table.dtype), want, table.dtype)
+    del g
+    tier.close()
+    res.close()
