@@ -33,6 +33,13 @@ length weights, Eq. 4 / Eq. 11), same stacked decode launch as the default:
 
   python bench.py --workload multi
 
+The other two resident table shapes: 8 x 4096 prefill against the
+2^22-phrase 2/3/4-gram table (8 GiB of values), and batch-256 decode against
+the 2^25-phrase table (64 GiB), per call and with 64 steps stacked per call:
+
+  python bench.py --workload prefill
+  python bench.py --workload large
+
 Each configuration (prefetch off / on, emulated compute window T_hide between
 a step's lookup and the next) starts from a freshly loaded table.  A step is
 one tfe_lookup_inject (plus, with prefetch, one tfe_prefetch for the next
@@ -137,7 +144,8 @@ def main():
     ap.add_argument("--latency-steps", type=int, default=2000)
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--workload", choices=("decode", "multi", "tiered", "head", "build"),
+    ap.add_argument("--workload",
+                    choices=("decode", "multi", "tiered", "head", "build", "prefill", "large"),
                     default="decode")
     ap.add_argument("--head-k", type=int, default=128)
     ap.add_argument("--build-reps", type=int, default=3)
@@ -167,6 +175,8 @@ def main():
         return run_head(args)
     if args.workload == "build":
         return run_build(args)
+    if args.workload in ("prefill", "large"):
+        return run_resident_config(args)
     t0 = time.time()
     table = synth.config2_table()
     gt = H.GpuTable(table)
@@ -509,6 +519,115 @@ def finish_multi(args, table, gt, sets, mslots, B, ctx, S, window, L, tokens_per
                       "inject over one %d-row stacked decode set (%.1f s, single thread)"
                       % (done // B, B, csec),
         }
+    gt.close()
+    print(json.dumps(result))
+
+
+def keys_formed(B, ctx, S, n_min, n_max):
+    """Keys the lookup forms for B rows of ctx + S tokens (every token valid):
+    position s has ctx + s + 1 tokens up to it, so lengths n <= ctx + s + 1."""
+    per_row = sum(sum(1 for n in range(n_min, n_max + 1) if n <= ctx + s + 1) for s in range(S))
+    return B * per_row
+
+
+def run_resident_config(args):
+    """Throughput of the resident lookup + inject on the two other table
+    shapes: 8 x 4096 prefill against the 2^22-phrase 2/3/4-gram table (8 GiB
+    of values), and batch-256 decode against the 2^25-phrase table (64 GiB),
+    per call and stacked (64 batch-256 steps per call).  The prefill and
+    stacked shapes rotate input sets that together exceed the 256 MB
+    last-level cache; the per-call batch-256 shape is bound by launch time
+    (its 8 input sets stay cached, the value rows do not)."""
+    import torch
+
+    import synth
+    from paper_2607_07388_amd import tfe
+    from tests import harness as H
+
+    stream = torch.cuda.current_stream()
+    t0 = time.time()
+    if args.workload == "prefill":
+        table = synth.config3_table()
+        shapes = [("prefill 8 x 4096", 4, lambda k: synth.prefill_batch(2, 8, 4096, set_index=k))]
+    else:
+        table = synth.config4_table()
+        shapes = [("batch-256 decode", 8,
+                   lambda k: synth.decode_batch(3, 256, s=1.05, set_index=k)),
+                  ("batch-256 decode, 64 steps stacked per call", 8,
+                   lambda k: synth.decode_batch(3, 256 * 64, s=1.05, set_index=40 + k))]
+    gt = H.GpuTable(table)
+    print("# table loaded (%d phrases) in %.1f s" % (table.n_phrases, time.time() - t0),
+          file=sys.stderr, flush=True)
+    runs = []
+    for name, nsets, make in shapes:
+        sets = []
+        for k in range(nsets):
+            batch = make(k)
+            B, ctx, S = batch.tokens.shape[0], batch.ctx, batch.S
+            T = B * S
+            tok = torch.from_numpy(batch.tokens).cuda()
+            hid = torch.empty((T, D), dtype=torch.bfloat16, device="cuda")
+            synth.normal_fill_device(hid.data_ptr(), 0, T, D, batch.seed, batch.hidden_tag, 1.0,
+                                     synth.BF16, stream.cuda_stream)
+            sets.append((tok, hid, H.Outputs(T, D, synth.BF16), B, ctx, S))
+        torch.cuda.synchronize()
+
+        def call(k):
+            tok, hid, outs, B, ctx, S = sets[k % nsets]
+            tfe.tfe_lookup_inject(gt.handle, tok, B, ctx, S, hid, outs.out, outs.hit, outs.slot,
+                                  outs.len, tfe.TFE_GATE_SIGMOID, 1.0, stream.cuda_stream)
+
+        for k in range(args.warmup):
+            call(k)
+        torch.cuda.synchronize()
+        hits = [int(st[2].hit.sum().item()) for st in sets]
+        _, _, _, B, ctx, S = sets[0]
+        T = B * S
+        keys = keys_formed(B, ctx, S, table.n_min, table.n_max)
+        window = (ctx + S) / S
+        steps = args.steps
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        w0 = time.perf_counter()
+        e0.record(stream)
+        for k in range(steps):
+            call(k)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - w0
+        avg_launch = e0.elapsed_time(e1) * 1e-3 / steps
+        avg_bytes = float(np.mean([algorithmic_bytes(T, hits[k % nsets], keys, window)
+                                   for k in range(steps)]))
+        runs.append({
+            "shape": name, "positions_per_call": T, "sets": nsets,
+            "hit_rate": float(np.mean(hits)) / T,
+            "us_per_call": avg_launch * 1e6,
+            "tokens_per_s": T * steps / wall,
+            "bytes_per_call": avg_bytes,
+            "hbm_gbps_algorithmic": avg_bytes / avg_launch / 1e9,
+            "frac_of_8tbs": avg_bytes / avg_launch / 8e12,
+        })
+        print("# %s: %.2f us per call" % (name, avg_launch * 1e6), file=sys.stderr, flush=True)
+        del sets
+    head = runs[-1]
+    result = {
+        "metric": "lookup+inject tokens/sec, %s, 1 MI355X" % head["shape"],
+        "value": head["tokens_per_s"], "unit": "tokens/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": head["us_per_call"] * 1e-3, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": ("8 x 4096 prefill (ctx 0), 2^21 2-grams + 2^20 3-grams + "
+                                "2^20 4-grams of a 200M-token Zipf(1.1) stream (8 GiB bf16 "
+                                "values), sigmoid gate, out of place"
+                                if args.workload == "prefill" else
+                                "batch-256 decode (3-token windows, Zipf(1.05) ids), 2^25-phrase "
+                                "2/3-gram table (64 GiB bf16 values), sigmoid gate, out of place"),
+                   "table_phrases": table.n_phrases},
+        "roofline": {"bound": "hbm", "kernel": "k_lookup_inject<bf16, D=1024>",
+                     "achieved": head["hbm_gbps_algorithmic"], "peak": 8000.0, "unit": "GB/s",
+                     "frac": head["frac_of_8tbs"], "traffic": None},
+        "runs": runs,
+    }
     gt.close()
     print(json.dumps(result))
 
