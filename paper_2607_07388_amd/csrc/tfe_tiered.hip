@@ -43,41 +43,24 @@ __device__ __forceinline__ uint32_t lanes_below(uint64_t m) {
                                    __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
 }
 
-// Block-wide count of a flag (kResolveThreads threads): returns how many
-// threads below this one have it set and the block total in *total.  A
-// ballot counts within each wave; every thread then adds the counts of the
-// waves before its own.  All threads must call it.
-__device__ uint32_t block_count(bool f, uint32_t* total) {
-  __shared__ uint32_t s_n[kWaves];
-  const int wave = threadIdx.x >> 6;
-  const uint64_t m = __builtin_amdgcn_ballot_w64(f);
-  if ((threadIdx.x & 63) == 0) s_n[wave] = (uint32_t)__builtin_popcountll(m);
-  __syncthreads();
-  uint32_t before = 0, all = 0;
-#pragma unroll
-  for (int w = 0; w < kWaves; ++w) {
-    const uint32_t c = s_n[w];
-    before += w < wave ? c : 0u;
-    all += c;
-  }
-  __syncthreads();
-  *total = all;
-  return before + lanes_below(m);
+// Block-wide rank of a flag among the block's threads and its total, and
+// the lowest thread index whose flag is set: the one-item forms of
+// block_count_n (defined below).  All threads must call them.
+template <int N>
+__device__ __forceinline__ void block_count_n(const bool* f, uint32_t* rank, uint32_t* total,
+                                              const bool* g = nullptr, uint32_t* first = nullptr);
+
+__device__ __forceinline__ uint32_t block_count(bool f, uint32_t* total) {
+  uint32_t rank;
+  block_count_n<1>(&f, &rank, total, nullptr, nullptr);
+  return rank;
 }
 
-// Lowest thread index whose flag is set, or 0xFFFFFFFF.  All threads must
-// call it.
-__device__ uint32_t block_first(bool f) {
-  __shared__ uint32_t s_f[kWaves];
-  const uint64_t m = __builtin_amdgcn_ballot_w64(f);
-  if ((threadIdx.x & 63) == 0)
-    s_f[threadIdx.x >> 6] = m ? (threadIdx.x & ~63u) + (uint32_t)__builtin_ctzll(m) : 0xFFFFFFFFu;
-  __syncthreads();
-  uint32_t r = 0xFFFFFFFFu;
-#pragma unroll
-  for (int w = 0; w < kWaves; ++w) r = min(r, s_f[w]);
-  __syncthreads();
-  return r;
+__device__ __forceinline__ uint32_t block_first(bool f) {
+  uint32_t rank, total, first;
+  const bool none = false;
+  block_count_n<1>(&none, &rank, &total, &f, &first);
+  return first;
 }
 
 __device__ __forceinline__ uint64_t ring_entry(uint32_t slot, uint32_t stamp) {
@@ -174,7 +157,7 @@ __device__ bool first_of_row(int32_t r, uint32_t pos, int32_t* hkey, uint32_t* h
 // set (0xFFFFFFFF if none), from the same exchange.
 template <int N>
 __device__ __forceinline__ void block_count_n(const bool* f, uint32_t* rank, uint32_t* total,
-                                              const bool* g = nullptr, uint32_t* first = nullptr) {
+                                              const bool* g, uint32_t* first) {
   static_assert(kWaves == 16, "one DPP row holds the per-wave counts");
   __shared__ uint32_t s_n[N][kWaves];
   __shared__ uint32_t s_f[kWaves];
