@@ -255,9 +255,6 @@ static tfe_status reserve_ring(tfe_table* t, uint64_t appends, hipStream_t strea
 }
 
 static tfe_status lookup_tiered(tfe_table* t, const LookupArgs& look, hipStream_t stream) {
-  // The recency clock, the ring bound and the cross-stream events live on
-  // the host and change with every call: a replayed graph would reuse them.
-  TFE_TRY(refuse_capture(stream, "a lookup on a tiered table"));
   TFE_TRY(ensure_scratch(t, look.T));
   // Calls on one table are ordered: after the previous lookup (when it ran
   // on another stream) and after a pending prefetch.
@@ -418,6 +415,10 @@ static tfe_status lookup_inject(tfe_table* t, const int32_t* tokens, int32_t B, 
     return fail(TFE_ERR_INVALID_ARG, "bad weighting");
   if (multi && t->cache_rows > 0)
     return fail(TFE_ERR_UNSUPPORTED, "multi-match lookup on a tiered table");
+  // The recency clock, the ring bound and the cross-stream events of a
+  // tiered table live on the host and change with every call: a replayed
+  // graph would reuse them.  Refused before anything is counted.
+  if (t->cache_rows > 0) TFE_TRY(refuse_capture(stream, "a lookup on a tiered table"));
   t->stats.calls++;
   if (T == 0) return TFE_OK;
   if (!tokens || !hin || !hout || !hit || !slot)

@@ -96,6 +96,7 @@ def test_calls_with_host_state_refuse_capture():
             except tfe.TfeError as e:
                 statuses.append(e.status)
     assert statuses == [tfe.TFE_ERR_UNSUPPORTED] * 3
+    assert tfe.tfe_get_stats(tier.handle)["calls"] == 0  # refused before counting
     o_res.out.fill_(0)
     o_res.slot.fill_(-7)
     torch.cuda.synchronize()
@@ -109,6 +110,7 @@ def test_calls_with_host_state_refuse_capture():
                           o_tier.hit, o_tier.slot, o_tier.len, tfe.TFE_GATE_SIGMOID, 1.0,
                           H.cur_stream())
     torch.cuda.synchronize()
+    assert tfe.tfe_get_stats(tier.handle)["calls"] == 1
     np.testing.assert_array_equal(o_tier.slot.cpu().numpy(), row)
     H.assert_close(H.to_host(o_tier.out, table.dtype), want, table.dtype)
     del g
