@@ -174,7 +174,9 @@ __device__ __forceinline__ void block_count_n(const bool* f, uint32_t* rank, uin
 #pragma unroll
     for (int k = N - 1; k >= 0; --k) {
       const uint64_t mg = __builtin_amdgcn_ballot_w64(g[k]);
-      if (mg) best = (uint32_t)k * kResolveThreads + (uint32_t)wave * 64u + (uint32_t)__builtin_ctzll(mg);
+      if (mg)
+        best = (uint32_t)k * kResolveThreads + (uint32_t)wave * 64u +
+               (uint32_t)__builtin_ctzll(mg);
     }
     if (lane == 0) s_f[wave] = best;
   }
@@ -527,22 +529,23 @@ __global__ __launch_bounds__(kResolveThreads) void k_lookup_resolve_small(const 
   if (threadIdx.x < kRefHash) rset[threadIdx.x] = -1;
   if (threadIdx.x < 4) s_cnt[threadIdx.x] = 0;
 
-  // ---- reads.  Round 1: ring cursors, counters (no other kernel touches the
-  // table's state while this one runs), the tokens of the wave's positions.
+  // ---- reads.  Read step 1: ring cursors, counters (no other kernel
+  // touches the table's state while this one runs), the tokens of the
+  // wave's positions.
   const unsigned long long tail0 = t.ctl->tail, head0 = t.ctl->head;
   const TierStats st0 = t.ctl->stats;
   int32_t tw[kSmallPer][4];
 #pragma unroll
   for (int k = 0; k < kSmallPer; ++k)
     dev::window_tokens(a, (uint32_t)(wave + kWaves * k), tw[k]);  // beyond T: invalid
-  // Round 2: one ring entry per thread; the first bucket of every key.
+  // Read step 2: one ring entry per thread; the first bucket of every key.
   const unsigned long long wi = tail0 + threadIdx.x;
   const bool win = wi < head0;
   const uint64_t e = win ? t.ring[wi & t.ring_mask] : 0;
   dev::Probe pr[kSmallPer];
 #pragma unroll
   for (int k = 0; k < kSmallPer; ++k) pr[k] = dev::probe_begin(a, tw[k], lane);
-  // Round 3: the entry's slot state; the matches (lane k of the wave holds
+  // Read step 3: the entry's slot state; the matches (lane k of the wave holds
   // position wave + kWaves k) and their residency.
   const uint32_t eslot = (uint32_t)(e >> 32), est = (uint32_t)e;
   const uint32_t estamp = win ? t.stamp[eslot] : 0u;
@@ -559,7 +562,7 @@ __global__ __launch_bounds__(kResolveThreads) void k_lookup_resolve_small(const 
     }
   }
   const int32_t mywhere = myrow >= 0 ? t.where[myrow] : -1;
-  // Round 4: prefetched flags of the cached matches.
+  // Read step 4: prefetched flags of the cached matches.
   const uint8_t mypref = mywhere >= 0 ? t.pref[mywhere] : (uint8_t)0;
   if (lane < kSmallPer && wave + kWaves * lane < (int)T) {
     const uint32_t q = wave + kWaves * lane;
