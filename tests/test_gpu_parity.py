@@ -274,3 +274,36 @@ def test_negative_zero_is_value_equal_on_noop_hits(w1):
     flipped = np.signbit(hid) & ~np.signbit(out)
     assert flipped.any() and (hid[flipped] == 0).all()
     gz.close()
+
+
+def test_vocab_boundary_ids_pack_and_match():
+    """vocab = 2^18 (18-bit token fields fully used): phrases over the ids
+    {0, 1, 2^17, 2^18 - 2, 2^18 - 1} in every length 2-4, queried with
+    those ids, ids in no phrase (5, 2^18 - 3), the first invalid id (2^18)
+    and -1; both entry points against the oracle, bit-exact rows."""
+    from .test_gpu_multi import check_multi
+    vocab = 1 << 18
+    ids = np.array([0, 1, 1 << 17, vocab - 2, vocab - 1], np.int64)
+    rng = np.random.default_rng(18)
+    tuples = [tuple(int(x) for x in ids[list(ix)]) for ix in np.ndindex(5, 5)]
+    tuples += [tuple(int(x) for x in ids[list(ix)]) for ix in np.ndindex(5, 5, 5)]
+    four = {tuple(int(x) for x in rng.choice(ids, 4)) for _ in range(400)}
+    tuples += sorted(four)
+    perm = rng.permutation(len(tuples))
+    toks = np.full((len(tuples), 4), -1, np.int32)
+    lens = np.zeros(len(tuples), np.uint8)
+    for r, i in enumerate(perm):
+        toks[r, :len(tuples[i])] = tuples[i]
+        lens[r] = len(tuples[i])
+    table = synth.PhraseTable(toks, lens, 2, 4, synth.BF16, 18, dim=1024, vocab=vocab)
+    gt = H.GpuTable(table)
+    ot = H.oracle_table(table)
+    pool = np.concatenate([ids, [5, vocab - 3, vocab, -1]]).astype(np.int32)
+    weights = np.array([4, 4, 4, 4, 4, 1, 1, 1, 1], np.float64)
+    tokens = rng.choice(pool, size=(4, 64), p=weights / weights.sum()).astype(np.int32)
+    hidden = synth.normal_range(8, 1818, 0, 4 * 61, 1024, 1.0, synth.BF16)
+    hit, _ = check(table, gt, ot, tokens, 3, 61, hidden)
+    _, _, ln = ot.lookup(tokens, 3, 61)
+    assert {0, 2, 3, 4} <= set(ln.tolist())
+    check_multi(table, gt, ot, tokens, 3, 61, hidden, tfe.TFE_WEIGHT_LENGTH)
+    gt.close()
