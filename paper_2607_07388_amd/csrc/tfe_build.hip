@@ -267,6 +267,16 @@ __device__ __forceinline__ uint32_t digit_of(K k, int shift) {
   return (uint32_t)(k >> shift) & 255u;
 }
 
+// Radix tile of this block.  Workgroups are dispatched round-robin over the
+// 8 XCDs (each with its own L2); giving every XCD a contiguous range of
+// tiles keeps the 32 tiles that share a 128-byte line of the digit-major
+// histogram matrix on one XCD, so each line is written and read through
+// one L2 instead of eight.  A bijection of [0, G) for any G.
+__device__ __forceinline__ uint32_t xcd_tile(uint32_t b, uint32_t G) {
+  const uint32_t q = G >> 3, r = G & 7u, x = b & 7u;
+  return x * q + min(x, r) + (b >> 3);
+}
+
 // Lanes of the wave whose 8-bit digit equals this lane's (active lanes only).
 __device__ __forceinline__ uint64_t match_digit(uint32_t d, bool active) {
   uint64_t m = __builtin_amdgcn_ballot_w64(active);
@@ -291,7 +301,8 @@ __global__ __launch_bounds__(kHistThreads) void k_rs_hist(const K* keys, TokSrc 
   constexpr int ITEMS = TILE / kHistThreads;
   __shared__ uint32_t h[256];
   for (int e = threadIdx.x; e < 256; e += kHistThreads) h[e] = 0u;
-  const uint64_t base = (uint64_t)blockIdx.x * TILE;
+  const uint32_t tile = xcd_tile(blockIdx.x, gridDim.x);
+  const uint64_t base = (uint64_t)tile * TILE;
   K kk[ITEMS];
 #pragma unroll
   for (int k = 0; k < ITEMS; ++k) {
@@ -314,7 +325,7 @@ __global__ __launch_bounds__(kHistThreads) void k_rs_hist(const K* keys, TokSrc 
   }
   __syncthreads();
   for (int e = threadIdx.x; e < 256; e += kHistThreads)
-    hist[(size_t)e * ntiles + blockIdx.x] = h[e];
+    hist[(size_t)e * ntiles + tile] = h[e];
 }
 
 // Scatter of one tile.  Wave w ranks the keys [w 64 ITEMS, (w+1) 64 ITEMS)
@@ -338,7 +349,8 @@ __global__ __launch_bounds__(kTileThreads) void k_rs_scatter(const K* keys, cons
   __shared__ uint64_t s_vals[PAIRS ? TILE : 1];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   for (int e = threadIdx.x; e < kTileWaves * 256; e += kTileThreads) (&wcnt[0][0])[e] = 0u;
-  const uint64_t base = (uint64_t)blockIdx.x * TILE + (uint64_t)wave * (64 * ITEMS);
+  const uint32_t tile = xcd_tile(blockIdx.x, gridDim.x);
+  const uint64_t base = (uint64_t)tile * TILE + (uint64_t)wave * (64 * ITEMS);
   const uint64_t lt = (1ull << lane) - 1ull;
   K kk[ITEMS];
   uint64_t vv[PAIRS ? ITEMS : 1];
@@ -376,7 +388,7 @@ __global__ __launch_bounds__(kTileThreads) void k_rs_scatter(const K* keys, cons
   const uint32_t loc = block_scan_excl<kTileThreads>(tot, s_wave, &all);
   if (d < 256) {
     s_loc[d] = loc;
-    s_glob[d] = offs[(size_t)d * ntiles + blockIdx.x];
+    s_glob[d] = offs[(size_t)d * ntiles + tile];
   }
   __syncthreads();
 #pragma unroll
@@ -390,7 +402,7 @@ __global__ __launch_bounds__(kTileThreads) void k_rs_scatter(const K* keys, cons
     }
   }
   __syncthreads();
-  const uint64_t tile0 = (uint64_t)blockIdx.x * TILE;
+  const uint64_t tile0 = (uint64_t)tile * TILE;
   const uint32_t cnt = (uint32_t)min((uint64_t)TILE, n - tile0);
   for (uint32_t p = threadIdx.x; p < cnt; p += kTileThreads) {
     const K k = s_keys[p];
