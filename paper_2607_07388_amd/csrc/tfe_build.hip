@@ -76,51 +76,71 @@ struct TokSrc {
 // of a thread's windows are in flight together), or 4-gram words.
 enum { kSrcKeys = 0, kSrcNgram4 = 4 };
 
-// Key of window i (NG <= 3 tokens, oldest in the highest field); an invalid
-// window gets 2^(18 NG).
+// Tokens a tile of windows [w0, w0 + TILE) needs: [w0, w0 + TILE + 3),
+// clipped to the stream (n windows of `ts.n` tokens: n + ts.n - 1 tokens),
+// staged in LDS with coalesced loads (16 bytes per lane when the stream is
+// 16-byte aligned) so that each window's tokens are read from LDS instead of
+// with one global load per token and window.  Past the stream: -1.
+template <int TILE, int NT>
+__device__ __forceinline__ void stage_tokens(const TokSrc& ts, uint64_t n, uint64_t w0,
+                                             int32_t* s_tok) {
+  constexpr int CNT = TILE + 3;
+  const uint64_t ntok = n + (uint64_t)ts.n - 1;
+  const uint64_t avail = ntok > w0 ? ntok - w0 : 0;
+  const int32_t* src = ts.tok + w0;
+  if ((((uintptr_t)src) & 15u) == 0) {
+    typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
+    for (int v = threadIdx.x; v < (CNT + 3) / 4; v += NT) {
+      const uint64_t e = 4ull * (uint64_t)v;
+      if (e + 4 <= avail) {
+        const i32x4 x = *(const i32x4*)(src + e);
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          if (e + q < (uint64_t)CNT) s_tok[e + q] = x[q];
+      } else {
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          if (e + q < (uint64_t)CNT) s_tok[e + q] = e + q < avail ? src[e + q] : -1;
+      }
+    }
+  } else {
+    for (int e = threadIdx.x; e < CNT; e += NT) s_tok[e] = (uint64_t)e < avail ? src[e] : -1;
+  }
+}
+
+// Key of the window starting at staged token j (NG <= 3 tokens, oldest in
+// the highest field); an invalid window gets 2^(18 NG).  4-grams: 72 key bits
+// in two words, lo = the three newest tokens (54 bits) and, as the payload,
+// hi = the oldest token, or the mark 2^18 for an invalid window.
 template <int NG>
-__device__ __forceinline__ uint64_t ngram_key(const TokSrc& ts, uint64_t i) {
+__device__ __forceinline__ uint64_t ngram_key_lds(const int32_t* s, uint32_t j, int32_t vocab) {
   uint64_t key = 0;
   bool ok = true;
 #pragma unroll
-  for (int j = 0; j < NG; ++j) {
-    const int32_t t = ts.tok[i + j];
-    ok = ok && t >= 0 && t < ts.vocab;
+  for (int q = 0; q < NG; ++q) {
+    const int32_t t = s[j + q];
+    ok = ok && t >= 0 && t < vocab;
     key = (key << 18) | (uint64_t)(uint32_t)(t & 0x3FFFF);
   }
   return ok ? key : (1ull << (18 * NG));
 }
 
-// 4-grams: 72 key bits in two words, lo = the three newest tokens (54 bits)
-// and hi = the oldest token, or the mark 2^18 for an invalid window.
-__device__ __forceinline__ uint64_t ngram4_lo(const TokSrc& ts, uint64_t i) {
-  uint64_t key = 0;
+template <int SRC, class K>
+__device__ __forceinline__ K key_at_lds(const int32_t* s, uint32_t j, int32_t vocab) {
+  if (SRC == kSrcNgram4) {
+    uint64_t key = 0;
 #pragma unroll
-  for (int j = 1; j < 4; ++j) key = (key << 18) | (uint64_t)(uint32_t)(ts.tok[i + j] & 0x3FFFF);
-  return key;
+    for (int q = 1; q < 4; ++q) key = (key << 18) | (uint64_t)(uint32_t)(s[j + q] & 0x3FFFF);
+    return (K)key;
+  }
+  return (K)ngram_key_lds<(SRC >= 1 && SRC <= 3) ? SRC : 1>(s, j, vocab);
 }
 
-__device__ __forceinline__ uint64_t ngram4_hi(const TokSrc& ts, uint64_t i) {
+__device__ __forceinline__ uint64_t val4_at_lds(const int32_t* s, uint32_t j, int32_t vocab) {
   bool ok = true;
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int32_t t = ts.tok[i + j];
-    ok = ok && t >= 0 && t < ts.vocab;
-  }
-  return ok ? (uint64_t)(uint32_t)ts.tok[i] : (1ull << 18);
-}
-
-template <int SRC, class K>
-__device__ __forceinline__ K key_at(const K* keys, const TokSrc& ts, uint64_t i) {
-  if (SRC >= 1 && SRC <= 3) return (K)ngram_key<(SRC >= 1 && SRC <= 3) ? SRC : 1>(ts, i);
-  if (SRC == kSrcNgram4) return (K)ngram4_lo(ts, i);
-  return keys[i];
-}
-
-template <int SRC>
-__device__ __forceinline__ uint64_t val_at(const uint64_t* vals, const TokSrc& ts, uint64_t i) {
-  if (SRC == kSrcNgram4) return ngram4_hi(ts, i);
-  return vals[i];
+  for (int q = 0; q < 4; ++q) ok = ok && s[j + q] >= 0 && s[j + q] < vocab;
+  return ok ? (uint64_t)(uint32_t)s[j] : (1ull << 18);
 }
 
 __global__ __launch_bounds__(256) void k_narrow(const uint64_t* in, uint64_t n, uint32_t* out) {
@@ -299,15 +319,24 @@ __global__ __launch_bounds__(kHistThreads) void k_rs_hist(const K* keys, TokSrc 
                                                           int shift, uint32_t* hist,
                                                           uint32_t ntiles) {
   constexpr int ITEMS = TILE / kHistThreads;
+  constexpr bool kTok = SRC != kSrcKeys;
   __shared__ uint32_t h[256];
+  __shared__ int32_t s_tok[kTok ? TILE + 3 : 1];
   for (int e = threadIdx.x; e < 256; e += kHistThreads) h[e] = 0u;
   const uint32_t tile = xcd_tile(blockIdx.x, gridDim.x);
   const uint64_t base = (uint64_t)tile * TILE;
+  if (kTok) {
+    stage_tokens<TILE, kHistThreads>(ts, n, base, s_tok);
+    __syncthreads();
+  }
   K kk[ITEMS];
 #pragma unroll
   for (int k = 0; k < ITEMS; ++k) {
     const uint64_t i = base + (uint64_t)k * kHistThreads + threadIdx.x;
-    kk[k] = i < n ? key_at<SRC>(keys, ts, i) : (K)0;
+    if (kTok)
+      kk[k] = i < n ? key_at_lds<SRC, K>(s_tok, (uint32_t)(i - base), ts.vocab) : (K)0;
+    else
+      kk[k] = i < n ? keys[i] : (K)0;
   }
   __syncthreads();
   const uint64_t lt = (1ull << (threadIdx.x & 63)) - 1ull;
@@ -352,14 +381,29 @@ __global__ __launch_bounds__(kTileThreads) void k_rs_scatter(const K* keys, cons
   const uint32_t tile = xcd_tile(blockIdx.x, gridDim.x);
   const uint64_t base = (uint64_t)tile * TILE + (uint64_t)wave * (64 * ITEMS);
   const uint64_t lt = (1ull << lane) - 1ull;
+  // Token-sourced keys: the tile's tokens are staged in the reorder buffer,
+  // which is free until the keys are placed (two barriers later).
+  constexpr bool kTok = SRC != kSrcKeys;
+  static_assert(!kTok || (TILE + 3) * 4 <= TILE * (int)sizeof(K), "token staging fits");
+  int32_t* s_tok = (int32_t*)s_keys;
+  if (kTok) {
+    stage_tokens<TILE, kTileThreads>(ts, n, (uint64_t)tile * TILE, s_tok);
+    __syncthreads();
+  }
   K kk[ITEMS];
   uint64_t vv[PAIRS ? ITEMS : 1];
   uint32_t rank[ITEMS];
 #pragma unroll
   for (int r = 0; r < ITEMS; ++r) {
     const uint64_t i = base + (uint64_t)r * 64 + lane;
-    kk[r] = i < n ? key_at<SRC>(keys, ts, i) : (K)0;
-    if (PAIRS) vv[PAIRS ? r : 0] = i < n ? val_at<SRC>(vals, ts, i) : 0ull;
+    const uint32_t j = (uint32_t)(i - (uint64_t)tile * TILE);
+    if (kTok) {
+      kk[r] = i < n ? key_at_lds<SRC, K>(s_tok, j, ts.vocab) : (K)0;
+      if (PAIRS) vv[PAIRS ? r : 0] = i < n ? val4_at_lds(s_tok, j, ts.vocab) : 0ull;
+    } else {
+      kk[r] = i < n ? keys[i] : (K)0;
+      if (PAIRS) vv[PAIRS ? r : 0] = i < n ? vals[i] : 0ull;
+    }
   }
   __syncthreads();
 #pragma unroll
