@@ -1,0 +1,47 @@
+"""Host-side logic of bench.py (no GPU): the one-GPU refusal, the
+algorithmic-bytes formulas and the key counts they use."""
+import os
+import subprocess
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+sys.path.insert(0, ROOT)
+import bench  # noqa: E402
+
+
+def test_more_than_one_gpu_is_refused():
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
+                       stdout=subprocess.PIPE, stderr=subprocess.PIPE, text=True, timeout=120)
+    assert r.returncode == 2
+    assert "one GPU" in r.stderr and r.stdout == ""
+
+
+def test_algorithmic_bytes_per_decode_token():
+    """bf16, D = 1024, out of place: hidden in + out (4096), the value row
+    and row id per hit (2052 h), 8 per key, 4 per window token, 6 outputs."""
+    T, hits = 16384, 10666
+    b = bench.algorithmic_bytes(T, hits, 2 * T, 3)
+    assert b == T * 4096 + hits * 2052 + 2 * T * 8 + T * 3 * 4 + T * 6
+    # The stacked decode launch at hit rate 0.651: 5465.6 bytes per token.
+    assert bench.algorithmic_bytes(1, 0.651, 2, 3) == pytest.approx(5465.9, abs=0.5)
+
+
+def test_keys_formed_counts_short_prefixes():
+    # Decode windows: every position forms n_max - n_min + 1 keys.
+    assert bench.keys_formed(64, 2, 1, 2, 3) == 64 * 2
+    # Prefill from column 0: position s forms the lengths n <= s + 1.
+    assert bench.keys_formed(8, 0, 4096, 2, 4) == 8 * (0 + 1 + 2 + 3 * 4093)
+    assert bench.keys_formed(1, 0, 1, 2, 4) == 0
+
+
+def test_build_bytes_per_window():
+    assert bench.build_bytes_per_window(2) == 128
+    assert bench.build_bytes_per_window(4) == 384
+    assert bench.build_bytes_per_window(3) > bench.build_bytes_per_window(2)
+
+
+def test_host_cpu_fields():
+    h = bench.host_cpu()
+    assert set(h) == {"host_cpu", "host_threads"} and h["host_threads"] >= 1
