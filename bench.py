@@ -95,6 +95,16 @@ HEAD_SOURCES = ("paper_2607_07388_amd/csrc/tfe_head.hip",
                 "paper_2607_07388_amd/csrc/tfe_head_api.cpp")
 
 
+# The same for one construction of the 2^26-token stream's top 2^19 2-grams
+# (every kernel of the call summed), from the passes in
+# profiles/tfe_ngram_top_zipf_streams.md.
+PROFILED_TRAFFIC_BUILD = {
+    "sources_sha256": "12af0e2da19131513d6dffb1d79e48e0fe4ebe4067629d1dbb72c8d1589a66b9",
+    "bytes_per_call": 10285566827,
+}
+BUILD_SOURCES = ("paper_2607_07388_amd/csrc/tfe_build.hip",)
+
+
 def kernel_sources_sha256(files=KERNEL_SOURCES):
     import hashlib
     h = hashlib.sha256()
@@ -815,7 +825,9 @@ def run_build(args):
             "peak": HBM_PEAK_GBPS,
             "unit": "GB/s",
             "frac": main_run["pipeline_gbps"] / HBM_PEAK_GBPS,
-            "traffic": None,
+            "traffic": (PROFILED_TRAFFIC_BUILD["bytes_per_call"]
+                        if kernel_sources_sha256(BUILD_SOURCES) ==
+                        PROFILED_TRAFFIC_BUILD["sources_sha256"] else None),
         },
         "runs": runs,
     }
