@@ -42,17 +42,19 @@
 namespace tfe {
 namespace {
 
-// Radix tiles: the scatter runs 512 threads per tile (two tiles share a CU,
-// so one's ranking overlaps the other's memory traffic), 16 keys per thread
-// for keys alone and 8 with a 64-bit payload (the tile's reorder buffer in
-// LDS: 64 KiB).  Longer tiles give longer digit runs, i.e. better coalesced
-// writes; measured on MI355X, 8192 keys x 512 threads beat 4096 x 256 and
-// 16384 x 1024.  The histogram of a tile is counted by 1024 threads.
+// Radix tiles: the scatter runs 512 threads per tile, 10 keys per thread
+// for keys alone (5120 keys: 51 KB of LDS, so three tiles share a CU and one
+// tile's ranking overlaps the others' memory traffic) and 8 with a 64-bit
+// payload (the tile's reorder buffer in LDS: 64 KiB, two tiles per CU).
+// Measured on MI355X for keys alone: 5120 keys beat 4096 (2.71 against 2.73
+// ms for the 2^26-token 2-gram table) and 8192 (2.83 ms), whose 74 KB allow
+// two tiles per CU; 4096 x 256 and 16384 x 1024 threads were slower still.
+// The histogram of a tile is counted by 1024 threads.
 constexpr int kTileThreads = 512;
 constexpr int kTileWaves = kTileThreads / 64;
 constexpr int kHistThreads = 1024;
 template <class K, bool PAIRS>
-constexpr int tile_items() { return (sizeof(K) + (PAIRS ? 8 : 0)) > 8 ? 8 : 16; }
+constexpr int tile_items() { return (sizeof(K) + (PAIRS ? 8 : 0)) > 8 ? 8 : 10; }
 template <class K, bool PAIRS>
 constexpr int tile_keys() { return kTileThreads * tile_items<K, PAIRS>(); }
 constexpr int kMinTile = kTileThreads * 8;  // smallest tile: sizes the histogram matrix
