@@ -743,22 +743,25 @@ def run_head(args):
     print(json.dumps(result))
 
 
-def build_bytes_per_window(n):
-    """Data the construction pipeline moves per window of the stream.  n <= 3
-    (P = one radix pass per 8 of the 18 n + 1 key bits): the first pass forms
-    the keys from the tokens (4 B read by its histogram, 4 B read and the
-    8 B key written by its scatter), every later pass reads the keys for its
-    histogram (8 B) and reads and writes them in its scatter (16 B); the run
-    count reads the sorted keys twice (16 B).  n = 4: the low word's first
-    pass writes key and payload (4 + 4 + 16 B), its six later passes move a
-    64-bit payload too (8 + 32 B each), the high word is narrowed (8 + 4 B),
-    three passes over its 19 bits carry the low word (4 + 24 B each), and
-    the run count reads both words twice (24 B).  The selection and ranking
-    work on far fewer items."""
+def build_bytes_per_window(n, vocab):
+    """Data the construction pipeline moves per window of the stream.  A key
+    holds 18 n bits (one more when vocab = 2^18, whose invalid-window mark
+    needs a bit above the token fields); the radix passes take 9 bits each.
+    n <= 3: the first pass forms the keys from the tokens (4 B read by its
+    histogram, 4 B read and the 8 B key written by its scatter), every later
+    pass reads the keys for its histogram (8 B) and reads and writes them in
+    its scatter (16 B); the run count reads the sorted keys twice (16 B).
+    n = 4: the low word's first pass writes key and payload (4 + 4 + 16 B),
+    its five later passes move a 64-bit payload too (8 + 32 B each), the high
+    word is narrowed (8 + 4 B), the passes over its 18 (19) bits carry the low
+    word (4 + 24 B each), and the run count reads both words twice (24 B).
+    The selection and ranking work on far fewer items."""
+    extra = 1 if vocab >= (1 << 18) else 0
     if n <= 3:
-        passes = (18 * n + 8) // 8
+        passes = (18 * n + extra + 8) // 9
         return 16 + 24 * (passes - 1) + 16
-    return 24 + 6 * 40 + 12 + 3 * 28 + 24
+    hi_passes = (18 + extra + 8) // 9
+    return 24 + 5 * 40 + 12 + hi_passes * 28 + 24
 
 
 def run_build(args):
@@ -796,7 +799,7 @@ def run_build(args):
                 m = tfe.tfe_ngram_top(tok_d, N, synth.V, n, skip, top, tup, cnt,
                                       stream.cuda_stream)
             sec = (time.perf_counter() - t0) / reps
-            moved = N * build_bytes_per_window(n)
+            moved = N * build_bytes_per_window(n, synth.V)
             runs.append({"stream": name, "n": n, "skip": skip, "top": top, "written": m,
                          "ms": sec * 1e3, "tokens_per_s": N / sec,
                          "pipeline_gbps": moved / sec / 1e9})

@@ -7,12 +7,14 @@
 //   1. key formation: every window of n tokens becomes one 64-bit key, the
 //      tokens in 18-bit fields, oldest in the highest field, so that key
 //      order is tuple order; a window with a token outside [0, vocab) gets
-//      the key 2^(18 n), above every valid one (formed by the first pass of
-//      the sort, from the tokens);
-//   2. LSD radix sort of the keys, 8-bit digits over the 18 n + 1 key bits
-//      (the valid keys end up first; a binary search counts them): per
-//      pass a digit histogram per tile (8192 keys; 4096 with a payload), one
-//      exclusive scan of the digit-major histogram, and a stable scatter
+//      a mark above every valid key: vocab in the oldest field when vocab <
+//      2^18 (the keys keep 18 n bits), else 2^(18 n) (formed by the first
+//      pass of the sort, from the tokens);
+//   2. LSD radix sort of the keys, 9-bit digits (an 18-bit token field is
+//      two digits) over the key bits (the valid keys end up first; a binary
+//      search counts them): per pass a digit histogram per tile (4096 keys;
+//      3072 with a payload), one exclusive scan of the digit-major
+//      histogram, and a stable scatter
 //      (each wave ranks its keys with ballot-based digit matching, the tile
 //      is reordered in LDS and written out in digit runs);
 //   3. run-length count: per-block counts of run starts, their scan, the
@@ -42,22 +44,28 @@
 namespace tfe {
 namespace {
 
-// Radix tiles: the scatter runs 512 threads per tile, 10 keys per thread
-// for keys alone (5120 keys: 51 KB of LDS, so three tiles share a CU and one
-// tile's ranking overlaps the others' memory traffic) and 8 with a 64-bit
-// payload (the tile's reorder buffer in LDS: 64 KiB, two tiles per CU).
-// Measured on MI355X for keys alone: 5120 keys beat 4096 (2.71 against 2.73
-// ms for the 2^26-token 2-gram table) and 8192 (2.83 ms), whose 74 KB allow
-// two tiles per CU; 4096 x 256 and 16384 x 1024 threads were slower still.
-// The histogram of a tile is counted by 1024 threads.
+// Radix tiles: the scatter runs 512 threads per tile (one per digit), 8
+// keys per thread for keys alone (4096 keys: 52 KB of LDS with the 512-bin
+// counts, so three tiles share a CU and one tile's ranking overlaps the
+// others' memory traffic) and 6 with a 64-bit payload (68 KB, two tiles per
+// CU).  Measured on MI355X with 8-bit digits for keys alone: 5120-key tiles
+// beat 4096 (2.71 against 2.73 ms for the 2^26-token 2-gram table) and 8192
+// (2.83 ms), whose 74 KB allow two tiles per CU; with 9-bit digits the 36-bit
+// 2-gram keys take four passes instead of five (2.50 ms).  The histogram of
+// a tile is counted by 1024 threads.
 constexpr int kTileThreads = 512;
 constexpr int kTileWaves = kTileThreads / 64;
 constexpr int kHistThreads = 1024;
 template <class K, bool PAIRS>
-constexpr int tile_items() { return (sizeof(K) + (PAIRS ? 8 : 0)) > 8 ? 8 : 10; }
+constexpr int tile_items() { return (sizeof(K) + (PAIRS ? 8 : 0)) > 8 ? 6 : 8; }
 template <class K, bool PAIRS>
 constexpr int tile_keys() { return kTileThreads * tile_items<K, PAIRS>(); }
-constexpr int kMinTile = kTileThreads * 8;  // smallest tile: sizes the histogram matrix
+constexpr int kMinTile = kTileThreads * 6;  // smallest tile: sizes the histogram matrix
+// Radix digits: 9 bits (512 bins), so that 18-bit token fields take two
+// digits each.
+constexpr int kDigitBits = 9;
+constexpr uint32_t kBins = 1u << kDigitBits;
+static_assert(kBins <= (uint32_t)kTileThreads, "one scatter thread per digit");
 constexpr int kScanThreads = 1024;
 constexpr int kScanItems = 16;
 constexpr int kScanBlock = kScanThreads * kScanItems;
@@ -71,6 +79,8 @@ struct TokSrc {
   const int32_t* tok;
   int n;
   int32_t vocab;
+  uint64_t mark;   // key of an invalid window: just above every valid key
+  uint32_t mark4;  // 4-grams: high word of an invalid window
 };
 
 // Key sources: the key array, windows of 1, 2 or 3 tokens (the source is
@@ -111,38 +121,39 @@ __device__ __forceinline__ void stage_tokens(const TokSrc& ts, uint64_t n, uint6
 }
 
 // Key of the window starting at staged token j (NG <= 3 tokens, oldest in
-// the highest field); an invalid window gets 2^(18 NG).  4-grams: 72 key bits
+// the highest field); an invalid window gets ts.mark.  4-grams: 72 key bits
 // in two words, lo = the three newest tokens (54 bits) and, as the payload,
-// hi = the oldest token, or the mark 2^18 for an invalid window.
+// hi = the oldest token, or ts.mark4 for an invalid window.
 template <int NG>
-__device__ __forceinline__ uint64_t ngram_key_lds(const int32_t* s, uint32_t j, int32_t vocab) {
+__device__ __forceinline__ uint64_t ngram_key_lds(const int32_t* s, uint32_t j,
+                                                  const TokSrc& ts) {
   uint64_t key = 0;
   bool ok = true;
 #pragma unroll
   for (int q = 0; q < NG; ++q) {
     const int32_t t = s[j + q];
-    ok = ok && t >= 0 && t < vocab;
+    ok = ok && t >= 0 && t < ts.vocab;
     key = (key << 18) | (uint64_t)(uint32_t)(t & 0x3FFFF);
   }
-  return ok ? key : (1ull << (18 * NG));
+  return ok ? key : ts.mark;
 }
 
 template <int SRC, class K>
-__device__ __forceinline__ K key_at_lds(const int32_t* s, uint32_t j, int32_t vocab) {
+__device__ __forceinline__ K key_at_lds(const int32_t* s, uint32_t j, const TokSrc& ts) {
   if (SRC == kSrcNgram4) {
     uint64_t key = 0;
 #pragma unroll
     for (int q = 1; q < 4; ++q) key = (key << 18) | (uint64_t)(uint32_t)(s[j + q] & 0x3FFFF);
     return (K)key;
   }
-  return (K)ngram_key_lds<(SRC >= 1 && SRC <= 3) ? SRC : 1>(s, j, vocab);
+  return (K)ngram_key_lds<(SRC >= 1 && SRC <= 3) ? SRC : 1>(s, j, ts);
 }
 
-__device__ __forceinline__ uint64_t val4_at_lds(const int32_t* s, uint32_t j, int32_t vocab) {
+__device__ __forceinline__ uint64_t val4_at_lds(const int32_t* s, uint32_t j, const TokSrc& ts) {
   bool ok = true;
 #pragma unroll
-  for (int q = 0; q < 4; ++q) ok = ok && s[j + q] >= 0 && s[j + q] < vocab;
-  return ok ? (uint64_t)(uint32_t)s[j] : (1ull << 18);
+  for (int q = 0; q < 4; ++q) ok = ok && s[j + q] >= 0 && s[j + q] < ts.vocab;
+  return ok ? (uint64_t)(uint32_t)s[j] : (uint64_t)ts.mark4;
 }
 
 __global__ __launch_bounds__(256) void k_narrow(const uint64_t* in, uint64_t n, uint32_t* out) {
@@ -152,9 +163,8 @@ __global__ __launch_bounds__(256) void k_narrow(const uint64_t* in, uint64_t n, 
 
 // Number of sorted keys below the invalid-window mark (one thread: binary
 // search).
-__global__ void k_count_valid(const uint64_t* keys, uint64_t nwin, int n,
+__global__ void k_count_valid(const uint64_t* keys, uint64_t nwin, uint64_t mark,
                               unsigned long long* count) {
-  const uint64_t mark = 1ull << (18 * n);
   uint64_t lo = 0, hi = nwin;
   while (lo < hi) {
     const uint64_t mid = lo + (hi - lo) / 2;
@@ -164,11 +174,12 @@ __global__ void k_count_valid(const uint64_t* keys, uint64_t nwin, int n,
   *count = lo;
 }
 
-__global__ void k_count_valid_hi(const uint32_t* hi, uint64_t nwin, unsigned long long* count) {
+__global__ void k_count_valid_hi(const uint32_t* hi, uint64_t nwin, uint32_t mark,
+                                 unsigned long long* count) {
   uint64_t lo = 0, top = nwin;
   while (lo < top) {
     const uint64_t mid = lo + (top - lo) / 2;
-    if (hi[mid] < (1u << 18)) lo = mid + 1;
+    if (hi[mid] < mark) lo = mid + 1;
     else top = mid;
   }
   *count = lo;
@@ -282,11 +293,11 @@ __global__ __launch_bounds__(kScanThreads) void k_scan_down(const uint32_t* in, 
   }
 }
 
-// ---- 2. stable LSD radix sort (8-bit digits) --------------------------------
+// ---- 2. stable LSD radix sort (9-bit digits) --------------------------------
 
 template <class K>
 __device__ __forceinline__ uint32_t digit_of(K k, int shift) {
-  return (uint32_t)(k >> shift) & 255u;
+  return (uint32_t)(k >> shift) & (kBins - 1u);
 }
 
 // Radix tile of this block.  Workgroups are dispatched round-robin over the
@@ -299,11 +310,11 @@ __device__ __forceinline__ uint32_t xcd_tile(uint32_t b, uint32_t G) {
   return x * q + min(x, r) + (b >> 3);
 }
 
-// Lanes of the wave whose 8-bit digit equals this lane's (active lanes only).
+// Lanes of the wave whose digit equals this lane's (active lanes only).
 __device__ __forceinline__ uint64_t match_digit(uint32_t d, bool active) {
   uint64_t m = __builtin_amdgcn_ballot_w64(active);
 #pragma unroll
-  for (int b = 0; b < 8; ++b) {
+  for (int b = 0; b < kDigitBits; ++b) {
     const uint64_t bb = __builtin_amdgcn_ballot_w64(active && ((d >> b) & 1u));
     m &= ((d >> b) & 1u) ? bb : ~bb;
   }
@@ -322,9 +333,9 @@ __global__ __launch_bounds__(kHistThreads) void k_rs_hist(const K* keys, TokSrc 
                                                           uint32_t ntiles) {
   constexpr int ITEMS = TILE / kHistThreads;
   constexpr bool kTok = SRC != kSrcKeys;
-  __shared__ uint32_t h[256];
+  __shared__ uint32_t h[kBins];
   __shared__ int32_t s_tok[kTok ? TILE + 3 : 1];
-  for (int e = threadIdx.x; e < 256; e += kHistThreads) h[e] = 0u;
+  for (int e = threadIdx.x; e < (int)kBins; e += kHistThreads) h[e] = 0u;
   const uint32_t tile = xcd_tile(blockIdx.x, gridDim.x);
   const uint64_t base = (uint64_t)tile * TILE;
   if (kTok) {
@@ -336,7 +347,7 @@ __global__ __launch_bounds__(kHistThreads) void k_rs_hist(const K* keys, TokSrc 
   for (int k = 0; k < ITEMS; ++k) {
     const uint64_t i = base + (uint64_t)k * kHistThreads + threadIdx.x;
     if (kTok)
-      kk[k] = i < n ? key_at_lds<SRC, K>(s_tok, (uint32_t)(i - base), ts.vocab) : (K)0;
+      kk[k] = i < n ? key_at_lds<SRC, K>(s_tok, (uint32_t)(i - base), ts) : (K)0;
     else
       kk[k] = i < n ? keys[i] : (K)0;
   }
@@ -355,7 +366,7 @@ __global__ __launch_bounds__(kHistThreads) void k_rs_hist(const K* keys, TokSrc 
     }
   }
   __syncthreads();
-  for (int e = threadIdx.x; e < 256; e += kHistThreads)
+  for (int e = threadIdx.x; e < (int)kBins; e += kHistThreads)
     hist[(size_t)e * ntiles + tile] = h[e];
 }
 
@@ -372,14 +383,14 @@ __global__ __launch_bounds__(kTileThreads) void k_rs_scatter(const K* keys, cons
                                                              uint32_t ntiles, K* keys_out,
                                                              uint64_t* vals_out) {
   constexpr int TILE = kTileThreads * ITEMS;
-  __shared__ uint32_t wcnt[kTileWaves][256];
-  __shared__ uint32_t s_loc[256];   // tile-local start of each digit
-  __shared__ uint32_t s_glob[256];  // global start of each digit's run of this tile
+  __shared__ uint32_t wcnt[kTileWaves][kBins];
+  __shared__ uint32_t s_loc[kBins];   // tile-local start of each digit
+  __shared__ uint32_t s_glob[kBins];  // global start of each digit's run of this tile
   __shared__ uint32_t s_wave[kTileWaves];
   __shared__ K s_keys[TILE];
   __shared__ uint64_t s_vals[PAIRS ? TILE : 1];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  for (int e = threadIdx.x; e < kTileWaves * 256; e += kTileThreads) (&wcnt[0][0])[e] = 0u;
+  for (int e = threadIdx.x; e < kTileWaves * (int)kBins; e += kTileThreads) (&wcnt[0][0])[e] = 0u;
   const uint32_t tile = xcd_tile(blockIdx.x, gridDim.x);
   const uint64_t base = (uint64_t)tile * TILE + (uint64_t)wave * (64 * ITEMS);
   const uint64_t lt = (1ull << lane) - 1ull;
@@ -400,8 +411,8 @@ __global__ __launch_bounds__(kTileThreads) void k_rs_scatter(const K* keys, cons
     const uint64_t i = base + (uint64_t)r * 64 + lane;
     const uint32_t j = (uint32_t)(i - (uint64_t)tile * TILE);
     if (kTok) {
-      kk[r] = i < n ? key_at_lds<SRC, K>(s_tok, j, ts.vocab) : (K)0;
-      if (PAIRS) vv[PAIRS ? r : 0] = i < n ? val4_at_lds(s_tok, j, ts.vocab) : 0ull;
+      kk[r] = i < n ? key_at_lds<SRC, K>(s_tok, j, ts) : (K)0;
+      if (PAIRS) vv[PAIRS ? r : 0] = i < n ? val4_at_lds(s_tok, j, ts) : 0ull;
     } else {
       kk[r] = i < n ? keys[i] : (K)0;
       if (PAIRS) vv[PAIRS ? r : 0] = i < n ? vals[i] : 0ull;
@@ -419,11 +430,11 @@ __global__ __launch_bounds__(kTileThreads) void k_rs_scatter(const K* keys, cons
     if (act && (m & lt) == 0) wcnt[wave][d] = before + (uint32_t)__builtin_popcountll(m);
   }
   __syncthreads();
-  // Per digit (threads below 256): counts of earlier waves, the tile's digit
+  // Per digit (one thread each): counts of earlier waves, the tile's digit
   // starts.
   const uint32_t d = threadIdx.x;
   uint32_t tot = 0;
-  if (d < 256) {
+  if (d < kBins) {
     for (int w = 0; w < kTileWaves; ++w) {
       const uint32_t c = wcnt[w][d];
       wcnt[w][d] = tot;  // becomes the offset of wave w within the digit
@@ -432,7 +443,7 @@ __global__ __launch_bounds__(kTileThreads) void k_rs_scatter(const K* keys, cons
   }
   uint32_t all;
   const uint32_t loc = block_scan_excl<kTileThreads>(tot, s_wave, &all);
-  if (d < 256) {
+  if (d < kBins) {
     s_loc[d] = loc;
     s_glob[d] = offs[(size_t)d * ntiles + tile];
   }
@@ -685,7 +696,7 @@ hipError_t radix_pass(K* keys, K* keys_alt, uint64_t* vals, uint64_t* vals_alt, 
   constexpr int ITEMS = tile_items<K, PAIRS>();
   hipLaunchKernelGGL((k_rs_hist<K, tile_keys<K, PAIRS>(), SRC>), dim3(ntiles), dim3(kHistThreads),
                      0, s, keys, ts, n, shift, hist, ntiles);
-  hipError_t e = scan_u32(hist, hist, (uint64_t)256 * ntiles, part, nullptr, s);
+  hipError_t e = scan_u32(hist, hist, (uint64_t)kBins * ntiles, part, nullptr, s);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL((k_rs_scatter<K, PAIRS, ITEMS, SRC>), dim3(ntiles), dim3(kTileThreads), 0, s,
                      keys, vals, ts, n, shift, hist, ntiles, keys_alt, vals_alt);
@@ -694,14 +705,14 @@ hipError_t radix_pass(K* keys, K* keys_alt, uint64_t* vals, uint64_t* vals_alt, 
 
 // Stable LSD sort of n keys (and payloads) by their low `bits` bits; the
 // first pass reads its keys (and payloads) from SRC.  hist holds
-// 256 x ceil(n / kMinTile) entries.
+// kBins x ceil(n / kMinTile) entries.
 template <class K, bool PAIRS, int SRC = kSrcKeys>
 hipError_t radix_sort(K*& keys, K*& keys_alt, uint64_t*& vals, uint64_t*& vals_alt, uint64_t n,
                       int bits, uint32_t* hist, uint32_t* part, hipStream_t s,
-                      const TokSrc& ts = TokSrc{nullptr, 0, 0}) {
+                      const TokSrc& ts = TokSrc{nullptr, 0, 0, 0, 0}) {
   const uint32_t ntiles = blocks_for(n, tile_keys<K, PAIRS>());
   if (ntiles == 0) return hipSuccess;
-  for (int shift = 0; shift < bits; shift += 8) {
+  for (int shift = 0; shift < bits; shift += kDigitBits) {
     const hipError_t e =
         shift == 0
             ? radix_pass<K, PAIRS, SRC>(keys, keys_alt, vals, vals_alt, ts, n, shift, ntiles,
@@ -822,7 +833,7 @@ tfe_status ngram_top(const int32_t* tokens, int64_t N, int32_t vocab, int32_t n,
   uint32_t* hi = wide ? sc.get<uint32_t>(nwin) : nullptr;      // 4-grams: high word keys
   uint32_t* hi_alt = wide ? sc.get<uint32_t>(nwin) : nullptr;
   const uint32_t ntiles = blocks_for(nwin, kMinTile);
-  uint32_t* hist = sc.get<uint32_t>((uint64_t)256 * ntiles);
+  uint32_t* hist = sc.get<uint32_t>((uint64_t)kBins * ntiles);
   uint32_t* part = sc.get<uint32_t>(kScanBlock);
   unsigned long long* d_count = sc.get<unsigned long long>(1);
   uint32_t* d_small = sc.get<uint32_t>(8);
@@ -836,9 +847,15 @@ tfe_status ngram_top(const int32_t* tokens, int64_t N, int32_t vocab, int32_t n,
   // high word (LSD over both words).
   uint64_t* no_vals = nullptr;
   uint64_t* no_vals2 = nullptr;
-  const TokSrc ts{tokens, n, vocab};
+  // Invalid windows: with vocab < 2^18 the oldest-token field holds vocab
+  // (above every valid token), so the keys keep 18 n bits; with vocab =
+  // 2^18 one more bit above the fields.
+  const bool narrow = vocab < (1 << 18);
+  const uint64_t mark = narrow ? (uint64_t)vocab << (18 * (n - 1)) : 1ull << (18 * n);
+  const uint32_t mark4 = narrow ? (uint32_t)vocab : (1u << 18);
+  const TokSrc ts{tokens, n, vocab, mark, mark4};
   if (!wide) {
-    const int bits = 18 * n + 1;
+    const int bits = 18 * n + (narrow ? 0 : 1);
     hipError_t e = n == 1   ? radix_sort<uint64_t, false, 1>(keys, keys_alt, no_vals, no_vals2,
                                                              nwin, bits, hist, part, s, ts)
                    : n == 2 ? radix_sort<uint64_t, false, 2>(keys, keys_alt, no_vals, no_vals2,
@@ -846,15 +863,16 @@ tfe_status ngram_top(const int32_t* tokens, int64_t N, int32_t vocab, int32_t n,
                             : radix_sort<uint64_t, false, 3>(keys, keys_alt, no_vals, no_vals2,
                                                              nwin, bits, hist, part, s, ts);
     BUILD_HIP(e, "key sort");
-    hipLaunchKernelGGL(k_count_valid, dim3(1), dim3(1), 0, s, keys, nwin, n, d_count);
+    hipLaunchKernelGGL(k_count_valid, dim3(1), dim3(1), 0, s, keys, nwin, mark, d_count);
   } else {
     BUILD_HIP((radix_sort<uint64_t, true, kSrcNgram4>(keys, keys_alt, wv, wv_alt, nwin, 54, hist,
                                                       part, s, ts)),
               "low-word sort");
     hipLaunchKernelGGL(k_narrow, dim3(blocks_for(nwin, 256)), dim3(256), 0, s, wv, nwin, hi);
-    BUILD_HIP((radix_sort<uint32_t, true>(hi, hi_alt, keys, keys_alt, nwin, 19, hist, part, s)),
+    BUILD_HIP((radix_sort<uint32_t, true>(hi, hi_alt, keys, keys_alt, nwin, narrow ? 18 : 19,
+                                          hist, part, s)),
               "high-word sort");
-    hipLaunchKernelGGL(k_count_valid_hi, dim3(1), dim3(1), 0, s, hi, nwin, d_count);
+    hipLaunchKernelGGL(k_count_valid_hi, dim3(1), dim3(1), 0, s, hi, nwin, mark4, d_count);
   }
   BUILD_HIP(hipGetLastError(), "count launch");
   unsigned long long m_host = 0;

@@ -81,6 +81,25 @@ def test_four_grams_split_on_the_oldest_token():
     check(tok, vocab, 4, 7, 11)
 
 
+@pytest.mark.parametrize("vocab", [1 << 18, (1 << 18) - 1, 5])
+@pytest.mark.parametrize("n", [1, 2, 3, 4])
+def test_top_token_ids_and_invalid_mark(n, vocab):
+    """The mark of an invalid window sits just above every valid key: vocab
+    in the oldest field when vocab < 2^18, one bit above the fields when
+    vocab = 2^18.  Windows of the largest ids (vocab - 1 in every field) must
+    stay valid and in tuple order, and windows with -1 or vocab anywhere must
+    be dropped."""
+    rng = np.random.default_rng(91 + n)
+    ids = np.array([vocab - 1, vocab - 2, 0, 1, vocab // 2], np.int32) % vocab
+    tok = ids[rng.integers(0, ids.size, 40000)]
+    tok[rng.random(tok.size) < 0.02] = vocab
+    tok[rng.random(tok.size) < 0.02] = -1
+    tok[:8] = vocab - 1
+    t, c = check(tok, vocab, n, 0, 10 ** 6)
+    assert (t == vocab - 1).all(axis=1).any()
+    check(tok, vocab, n, 3, 17)
+
+
 def test_zipf_stream_matches_generator_and_oracle():
     toks = synth.zipf_tokens(4, 88, 1 << 20, 1.1)
     for n in (2, 3, 4):
