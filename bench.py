@@ -99,8 +99,8 @@ HEAD_SOURCES = ("paper_2607_07388_amd/csrc/tfe_head.hip",
 # (every kernel of the call summed), from the passes in
 # profiles/tfe_ngram_top_zipf_streams.md.
 PROFILED_TRAFFIC_BUILD = {
-    "sources_sha256": "d1966dcf1923ca47c0178156b6189a48aaa288c9c983e1aa2f2478d80d0730e5",
-    "bytes_per_call": 9152744786,
+    "sources_sha256": "00532e7e0832412b283f3ba89b0672f1fd97134be4cfb40d2df263e335ccbe24",
+    "bytes_per_call": 8902810582,
 }
 BUILD_SOURCES = ("paper_2607_07388_amd/csrc/tfe_build.hip",)
 

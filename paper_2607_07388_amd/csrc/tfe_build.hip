@@ -214,11 +214,16 @@ __global__ __launch_bounds__(kScanThreads) void k_scan_reduce(const uint32_t* in
                                                               uint32_t* part) {
   __shared__ uint32_t s_wave[kScanThreads / 64];
   const uint64_t base = (uint64_t)blockIdx.x * kScanBlock;
-  uint32_t s = 0;
+  // All loads first (masked past n), then the sum: one round trip.
+  uint32_t v[kScanItems];
+#pragma unroll
   for (int k = 0; k < kScanItems; ++k) {
     const uint64_t i = base + (uint64_t)k * kScanThreads + threadIdx.x;
-    if (i < n) s += in[i];
+    v[k] = i < n ? in[i] : 0u;
   }
+  uint32_t s = 0;
+#pragma unroll
+  for (int k = 0; k < kScanItems; ++k) s += v[k];
   uint32_t tot;
   (void)block_scan_excl<kScanThreads>(s, s_wave, &tot);
   if (threadIdx.x == 0) part[blockIdx.x] = tot;
@@ -477,22 +482,75 @@ __global__ __launch_bounds__(kTileThreads) void k_rs_scatter(const K* keys, cons
 // starts per block, then (after the scan of those counts) each start's key
 // and position at its rank.  A start is a key that differs from the one
 // before it.  Wave w of a block covers kScanItems rounds of 64 keys.
-__device__ __forceinline__ bool run_start(const uint64_t* keys, const uint32_t* hi, uint64_t i,
-                                          uint64_t n) {
-  return i < n && (i == 0 || keys[i] != keys[i - 1] || (hi && hi[i] != hi[i - 1]));
+
+// Run starts among the kScanItems rounds of 64 keys of this wave from base:
+// the keys (and high words) are loaded first, at clamped indices, so that
+// all loads are in flight at once; each key's predecessor comes from the
+// lane below (lane 0: lane 63 of the round before, or one load for the
+// wave's first key); then one ballot per round.  cur keeps the keys (and
+// hcur the high words).
+__device__ __forceinline__ uint64_t from_lane_below(uint64_t x, uint64_t carry) {
+  const int lane = threadIdx.x & 63;
+  const uint32_t lo = (uint32_t)__shfl_up((int)(uint32_t)x, 1, 64);
+  const uint32_t hi = (uint32_t)__shfl_up((int)(uint32_t)(x >> 32), 1, 64);
+  return lane == 0 ? carry : ((uint64_t)hi << 32) | lo;
 }
 
+__device__ __forceinline__ uint64_t lane63(uint64_t x) {
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)x, 63);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(x >> 32), 63);
+  return ((uint64_t)hi << 32) | lo;
+}
+
+template <bool WIDE>
+__device__ __forceinline__ void run_starts(const uint64_t* keys, const uint32_t* hi, uint64_t base,
+                                           uint64_t n, uint64_t (&m)[kScanItems],
+                                           uint64_t (&cur)[kScanItems],
+                                           uint32_t (&hcur)[WIDE ? kScanItems : 1]) {
+  const int lane = threadIdx.x & 63;
+  const uint64_t i0 = base > 0 ? (base - 1 < n ? base - 1 : n - 1) : 0;
+  const uint64_t first = keys[i0];
+  const uint32_t hfirst = WIDE ? hi[i0] : 0u;
+#pragma unroll
+  for (int k = 0; k < kScanItems; ++k) {
+    const uint64_t i = base + (uint64_t)k * 64 + lane;
+    const uint64_t ic = i < n ? i : n - 1;
+    cur[k] = keys[ic];
+    if (WIDE) hcur[WIDE ? k : 0] = hi[ic];
+  }
+#pragma unroll
+  for (int k = 0; k < kScanItems; ++k) {
+    const uint64_t i = base + (uint64_t)k * 64 + lane;
+    const uint64_t prv = from_lane_below(cur[k], k == 0 ? first : lane63(cur[k > 0 ? k - 1 : 0]));
+    bool differs = cur[k] != prv;
+    if (WIDE) {
+      const uint32_t hc = hcur[WIDE ? k : 0];
+      const uint32_t hcarry =
+          k == 0 ? hfirst
+                 : (uint32_t)__builtin_amdgcn_readlane((int)hcur[WIDE ? (k > 0 ? k - 1 : 0) : 0], 63);
+      // Shuffled in every lane before the select: a lane that reads an
+      // inactive one gets 0.
+      const uint32_t below = (uint32_t)__shfl_up((int)hc, 1, 64);
+      const uint32_t hp = lane == 0 ? hcarry : below;
+      differs = differs || hc != hp;
+    }
+    m[k] = __builtin_amdgcn_ballot_w64(i < n && (i == 0 || differs));
+  }
+}
+
+template <bool WIDE>
 __global__ __launch_bounds__(kScanThreads) void k_runs_reduce(const uint64_t* keys,
                                                               const uint32_t* hi, uint64_t n,
                                                               uint32_t* part) {
   __shared__ uint32_t s_tot[kScanThreads / 64];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const uint64_t base = (uint64_t)blockIdx.x * kScanBlock + (uint64_t)wave * (64 * kScanItems);
+  uint64_t m[kScanItems], cur[kScanItems];
+  uint32_t hcur[WIDE ? kScanItems : 1];
+  run_starts<WIDE>(keys, hi, base, n, m, cur, hcur);
   uint32_t c = 0;
 #pragma unroll
-  for (int k = 0; k < kScanItems; ++k)
-    c += (uint32_t)__builtin_popcountll(
-        __builtin_amdgcn_ballot_w64(run_start(keys, hi, base + (uint64_t)k * 64 + lane, n)));
+  for (int k = 0; k < kScanItems; ++k) c += (uint32_t)__builtin_popcountll(m[k]);
   if (lane == 0) s_tot[wave] = c;
   __syncthreads();
   if (threadIdx.x == 0) {
@@ -502,6 +560,7 @@ __global__ __launch_bounds__(kScanThreads) void k_runs_reduce(const uint64_t* ke
   }
 }
 
+template <bool WIDE>
 __global__ __launch_bounds__(kScanThreads) void k_runs_write(const uint64_t* keys,
                                                              const uint32_t* hi, uint64_t n,
                                                              const uint32_t* part, uint64_t* ukey,
@@ -509,13 +568,12 @@ __global__ __launch_bounds__(kScanThreads) void k_runs_write(const uint64_t* key
   __shared__ uint32_t s_tot[kScanThreads / 64];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const uint64_t base = (uint64_t)blockIdx.x * kScanBlock + (uint64_t)wave * (64 * kScanItems);
-  uint64_t m[kScanItems];
+  uint64_t m[kScanItems], cur[kScanItems];
+  uint32_t hcur[WIDE ? kScanItems : 1];
+  run_starts<WIDE>(keys, hi, base, n, m, cur, hcur);
   uint32_t c = 0;
 #pragma unroll
-  for (int k = 0; k < kScanItems; ++k) {
-    m[k] = __builtin_amdgcn_ballot_w64(run_start(keys, hi, base + (uint64_t)k * 64 + lane, n));
-    c += (uint32_t)__builtin_popcountll(m[k]);
-  }
+  for (int k = 0; k < kScanItems; ++k) c += (uint32_t)__builtin_popcountll(m[k]);
   if (lane == 0) s_tot[wave] = c;
   __syncthreads();
   uint32_t r = part[blockIdx.x];
@@ -526,8 +584,8 @@ __global__ __launch_bounds__(kScanThreads) void k_runs_write(const uint64_t* key
     const uint64_t i = base + (uint64_t)k * 64 + lane;
     if ((m[k] >> lane) & 1ull) {
       const uint32_t idx = r + (uint32_t)__builtin_popcountll(m[k] & lt);
-      ukey[idx] = keys[i];
-      if (hi) uhi[idx] = hi[i];
+      ukey[idx] = cur[k];
+      if (WIDE) uhi[idx] = hcur[WIDE ? k : 0];
       ustart[idx] = (uint32_t)i;
     }
     r += (uint32_t)__builtin_popcountll(m[k]);
@@ -882,7 +940,11 @@ tfe_status ngram_top(const int32_t* tokens, int64_t N, int32_t vocab, int32_t n,
   if (M == 0) return TFE_OK;
   // 3. runs.
   const uint32_t nbr = blocks_for(M, kScanBlock);
-  hipLaunchKernelGGL(k_runs_reduce, dim3(nbr), dim3(kScanThreads), 0, s, keys, hi, M, part);
+  if (wide)
+    hipLaunchKernelGGL(k_runs_reduce<true>, dim3(nbr), dim3(kScanThreads), 0, s, keys, hi, M, part);
+  else
+    hipLaunchKernelGGL(k_runs_reduce<false>, dim3(nbr), dim3(kScanThreads), 0, s, keys, hi, M,
+                       part);
   hipLaunchKernelGGL(k_scan_partials, dim3(1), dim3(kScanThreads), 0, s, part, nbr, d_small);
   BUILD_HIP(hipGetLastError(), "run count launches");
   uint32_t U = 0;
@@ -894,8 +956,12 @@ tfe_status ngram_top(const int32_t* tokens, int64_t N, int32_t vocab, int32_t n,
   uint32_t* ucnt = sc.get<uint32_t>(U);
   uint32_t* eq = sc.get<uint32_t>(U);
   if (!ukey || !ustart || !ucnt || !eq || (wide && !uhi)) return fail(TFE_ERR_OOM, "run arrays");
-  hipLaunchKernelGGL(k_runs_write, dim3(nbr), dim3(kScanThreads), 0, s, keys, hi, M, part, ukey,
-                     uhi, ustart);
+  if (wide)
+    hipLaunchKernelGGL(k_runs_write<true>, dim3(nbr), dim3(kScanThreads), 0, s, keys, hi, M, part,
+                       ukey, uhi, ustart);
+  else
+    hipLaunchKernelGGL(k_runs_write<false>, dim3(nbr), dim3(kScanThreads), 0, s, keys, hi, M, part,
+                       ukey, uhi, ustart);
   BUILD_HIP(hipMemsetAsync(sel_bins, 0, kSelBins * sizeof(uint32_t), s), "memset");
   hipLaunchKernelGGL(k_run_counts, dim3(blocks_for(U, 16384)), dim3(1024), 0, s, ustart, U,
                      (uint32_t)M, ucnt, sel_bins);
