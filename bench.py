@@ -751,17 +751,18 @@ def build_bytes_per_window(n, vocab):
     histogram, 4 B read and the 8 B key written by its scatter), every later
     pass reads the keys for its histogram (8 B) and reads and writes them in
     its scatter (16 B); the run count reads the sorted keys twice (16 B).
-    n = 4: the low word's first pass writes key and payload (4 + 4 + 16 B),
-    its five later passes move a 64-bit payload too (8 + 32 B each), the high
-    word is narrowed (8 + 4 B), the passes over its 18 (19) bits carry the low
-    word (4 + 24 B each), and the run count reads both words twice (24 B).
+    n = 4: the low word's first pass writes key and 32-bit payload (the
+    oldest token: 4 + 4 + 12 B), its five later passes move the payload too
+    (8 + 24 B each), the passes over the high word's 18 (19) bits carry the
+    low word (4 + 24 B each), and the run count reads both words twice
+    (24 B).
     The selection and ranking work on far fewer items."""
     extra = 1 if vocab >= (1 << 18) else 0
     if n <= 3:
         passes = (18 * n + extra + 8) // 9
         return 16 + 24 * (passes - 1) + 16
     hi_passes = (18 + extra + 8) // 9
-    return 24 + 5 * 40 + 12 + hi_passes * 28 + 24
+    return 20 + 5 * 32 + hi_passes * 28 + 24
 
 
 def run_build(args):

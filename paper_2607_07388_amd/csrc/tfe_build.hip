@@ -30,7 +30,7 @@
 //   6. ranks [skip, skip + top) are unpacked into tuples and counts.
 // 4-grams need 72 key bits: the three newest tokens form the low word and
 // the oldest token the high word; the LSD sort runs over the low word (high
-// word as payload) and then stably over the high word.
+// word as a 32-bit payload) and then stably over the high word.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -56,10 +56,10 @@ namespace {
 constexpr int kTileThreads = 512;
 constexpr int kTileWaves = kTileThreads / 64;
 constexpr int kHistThreads = 1024;
-template <class K, bool PAIRS>
-constexpr int tile_items() { return (sizeof(K) + (PAIRS ? 8 : 0)) > 8 ? 6 : 8; }
-template <class K, bool PAIRS>
-constexpr int tile_keys() { return kTileThreads * tile_items<K, PAIRS>(); }
+template <class K, bool PAIRS, class V>
+constexpr int tile_items() { return (sizeof(K) + (PAIRS ? sizeof(V) : 0)) > 8 ? 6 : 8; }
+template <class K, bool PAIRS, class V>
+constexpr int tile_keys() { return kTileThreads * tile_items<K, PAIRS, V>(); }
 constexpr int kMinTile = kTileThreads * 6;  // smallest tile: sizes the histogram matrix
 // Radix digits: 9 bits (512 bins), so that 18-bit token fields take two
 // digits each.
@@ -154,11 +154,6 @@ __device__ __forceinline__ uint64_t val4_at_lds(const int32_t* s, uint32_t j, co
 #pragma unroll
   for (int q = 0; q < 4; ++q) ok = ok && s[j + q] >= 0 && s[j + q] < ts.vocab;
   return ok ? (uint64_t)(uint32_t)s[j] : (uint64_t)ts.mark4;
-}
-
-__global__ __launch_bounds__(256) void k_narrow(const uint64_t* in, uint64_t n, uint32_t* out) {
-  const uint64_t i = (uint64_t)blockIdx.x * 256 + threadIdx.x;
-  if (i < n) out[i] = (uint32_t)in[i];
 }
 
 // Number of sorted keys below the invalid-window mark (one thread: binary
@@ -381,19 +376,19 @@ __global__ __launch_bounds__(kHistThreads) void k_rs_hist(const K* keys, TokSrc 
 // plus the matching lanes below it; the first lane of each digit group
 // advances the count.  Tile positions follow (digit, wave, rank), i.e. the
 // stable order; the tile is reordered in LDS and written in digit runs.
-template <class K, bool PAIRS, int ITEMS, int SRC>
-__global__ __launch_bounds__(kTileThreads) void k_rs_scatter(const K* keys, const uint64_t* vals,
+template <class K, class V, bool PAIRS, int ITEMS, int SRC>
+__global__ __launch_bounds__(kTileThreads) void k_rs_scatter(const K* keys, const V* vals,
                                                              TokSrc ts, uint64_t n, int shift,
                                                              const uint32_t* offs,
                                                              uint32_t ntiles, K* keys_out,
-                                                             uint64_t* vals_out) {
+                                                             V* vals_out) {
   constexpr int TILE = kTileThreads * ITEMS;
   __shared__ uint32_t wcnt[kTileWaves][kBins];
   __shared__ uint32_t s_loc[kBins];   // tile-local start of each digit
   __shared__ uint32_t s_glob[kBins];  // global start of each digit's run of this tile
   __shared__ uint32_t s_wave[kTileWaves];
   __shared__ K s_keys[TILE];
-  __shared__ uint64_t s_vals[PAIRS ? TILE : 1];
+  __shared__ V s_vals[PAIRS ? TILE : 1];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   for (int e = threadIdx.x; e < kTileWaves * (int)kBins; e += kTileThreads) (&wcnt[0][0])[e] = 0u;
   const uint32_t tile = xcd_tile(blockIdx.x, gridDim.x);
@@ -409,7 +404,7 @@ __global__ __launch_bounds__(kTileThreads) void k_rs_scatter(const K* keys, cons
     __syncthreads();
   }
   K kk[ITEMS];
-  uint64_t vv[PAIRS ? ITEMS : 1];
+  V vv[PAIRS ? ITEMS : 1];
   uint32_t rank[ITEMS];
 #pragma unroll
   for (int r = 0; r < ITEMS; ++r) {
@@ -417,10 +412,10 @@ __global__ __launch_bounds__(kTileThreads) void k_rs_scatter(const K* keys, cons
     const uint32_t j = (uint32_t)(i - (uint64_t)tile * TILE);
     if (kTok) {
       kk[r] = i < n ? key_at_lds<SRC, K>(s_tok, j, ts) : (K)0;
-      if (PAIRS) vv[PAIRS ? r : 0] = i < n ? val4_at_lds(s_tok, j, ts) : 0ull;
+      if (PAIRS) vv[PAIRS ? r : 0] = i < n ? (V)val4_at_lds(s_tok, j, ts) : (V)0;
     } else {
       kk[r] = i < n ? keys[i] : (K)0;
-      if (PAIRS) vv[PAIRS ? r : 0] = i < n ? vals[i] : 0ull;
+      if (PAIRS) vv[PAIRS ? r : 0] = i < n ? vals[i] : (V)0;
     }
   }
   __syncthreads();
@@ -747,16 +742,16 @@ hipError_t scan_u32(const uint32_t* in, uint32_t* out, uint64_t n, uint32_t* par
   return hipGetLastError();
 }
 
-template <class K, bool PAIRS, int SRC>
-hipError_t radix_pass(K* keys, K* keys_alt, uint64_t* vals, uint64_t* vals_alt, const TokSrc& ts,
+template <class K, class V, bool PAIRS, int SRC>
+hipError_t radix_pass(K* keys, K* keys_alt, V* vals, V* vals_alt, const TokSrc& ts,
                       uint64_t n, int shift, uint32_t ntiles, uint32_t* hist, uint32_t* part,
                       hipStream_t s) {
-  constexpr int ITEMS = tile_items<K, PAIRS>();
-  hipLaunchKernelGGL((k_rs_hist<K, tile_keys<K, PAIRS>(), SRC>), dim3(ntiles), dim3(kHistThreads),
+  constexpr int ITEMS = tile_items<K, PAIRS, V>();
+  hipLaunchKernelGGL((k_rs_hist<K, tile_keys<K, PAIRS, V>(), SRC>), dim3(ntiles), dim3(kHistThreads),
                      0, s, keys, ts, n, shift, hist, ntiles);
   hipError_t e = scan_u32(hist, hist, (uint64_t)kBins * ntiles, part, nullptr, s);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((k_rs_scatter<K, PAIRS, ITEMS, SRC>), dim3(ntiles), dim3(kTileThreads), 0, s,
+  hipLaunchKernelGGL((k_rs_scatter<K, V, PAIRS, ITEMS, SRC>), dim3(ntiles), dim3(kTileThreads), 0, s,
                      keys, vals, ts, n, shift, hist, ntiles, keys_alt, vals_alt);
   return hipGetLastError();
 }
@@ -764,18 +759,18 @@ hipError_t radix_pass(K* keys, K* keys_alt, uint64_t* vals, uint64_t* vals_alt, 
 // Stable LSD sort of n keys (and payloads) by their low `bits` bits; the
 // first pass reads its keys (and payloads) from SRC.  hist holds
 // kBins x ceil(n / kMinTile) entries.
-template <class K, bool PAIRS, int SRC = kSrcKeys>
-hipError_t radix_sort(K*& keys, K*& keys_alt, uint64_t*& vals, uint64_t*& vals_alt, uint64_t n,
+template <class K, bool PAIRS, int SRC = kSrcKeys, class V = uint64_t>
+hipError_t radix_sort(K*& keys, K*& keys_alt, V*& vals, V*& vals_alt, uint64_t n,
                       int bits, uint32_t* hist, uint32_t* part, hipStream_t s,
                       const TokSrc& ts = TokSrc{nullptr, 0, 0, 0, 0}) {
-  const uint32_t ntiles = blocks_for(n, tile_keys<K, PAIRS>());
+  const uint32_t ntiles = blocks_for(n, tile_keys<K, PAIRS, V>());
   if (ntiles == 0) return hipSuccess;
   for (int shift = 0; shift < bits; shift += kDigitBits) {
     const hipError_t e =
         shift == 0
-            ? radix_pass<K, PAIRS, SRC>(keys, keys_alt, vals, vals_alt, ts, n, shift, ntiles,
+            ? radix_pass<K, V, PAIRS, SRC>(keys, keys_alt, vals, vals_alt, ts, n, shift, ntiles,
                                         hist, part, s)
-            : radix_pass<K, PAIRS, kSrcKeys>(keys, keys_alt, vals, vals_alt, ts, n, shift,
+            : radix_pass<K, V, PAIRS, kSrcKeys>(keys, keys_alt, vals, vals_alt, ts, n, shift,
                                              ntiles, hist, part, s);
     if (e != hipSuccess) return e;
     std::swap(keys, keys_alt);
@@ -886,10 +881,11 @@ tfe_status ngram_top(const int32_t* tokens, int64_t N, int32_t vocab, int32_t n,
   Scratch sc(s);
   uint64_t* keys = sc.get<uint64_t>(nwin);
   uint64_t* keys_alt = sc.get<uint64_t>(nwin);
-  uint64_t* wv = wide ? sc.get<uint64_t>(nwin) : nullptr;      // 4-grams: high word payload
-  uint64_t* wv_alt = wide ? sc.get<uint64_t>(nwin) : nullptr;
-  uint32_t* hi = wide ? sc.get<uint32_t>(nwin) : nullptr;      // 4-grams: high word keys
-  uint32_t* hi_alt = wide ? sc.get<uint32_t>(nwin) : nullptr;
+  // 4-grams: the high word, payload of the low-word sort, then keys.
+  uint32_t* wv = wide ? sc.get<uint32_t>(nwin) : nullptr;
+  uint32_t* wv_alt = wide ? sc.get<uint32_t>(nwin) : nullptr;
+  uint32_t* hi = nullptr;
+  uint32_t* hi_alt = nullptr;
   const uint32_t ntiles = blocks_for(nwin, kMinTile);
   uint32_t* hist = sc.get<uint32_t>((uint64_t)kBins * ntiles);
   uint32_t* part = sc.get<uint32_t>(kScanBlock);
@@ -897,7 +893,7 @@ tfe_status ngram_top(const int32_t* tokens, int64_t N, int32_t vocab, int32_t n,
   uint32_t* d_small = sc.get<uint32_t>(8);
   uint32_t* sel_bins = sc.get<uint32_t>(kSelBins);
   if (!keys || !keys_alt || !hist || !part || !d_count || !d_small || !sel_bins ||
-      (wide && (!wv || !wv_alt || !hi || !hi_alt)))
+      (wide && (!wv || !wv_alt)))
     return fail(TFE_ERR_OOM, "n-gram scratch for %llu windows", (unsigned long long)nwin);
   // 1-2. keys of all windows, formed by the first radix pass, sorted (one
   // bit above the key fields carries the invalid-window mark); the valid
@@ -923,10 +919,11 @@ tfe_status ngram_top(const int32_t* tokens, int64_t N, int32_t vocab, int32_t n,
     BUILD_HIP(e, "key sort");
     hipLaunchKernelGGL(k_count_valid, dim3(1), dim3(1), 0, s, keys, nwin, mark, d_count);
   } else {
-    BUILD_HIP((radix_sort<uint64_t, true, kSrcNgram4>(keys, keys_alt, wv, wv_alt, nwin, 54, hist,
-                                                      part, s, ts)),
+    BUILD_HIP((radix_sort<uint64_t, true, kSrcNgram4, uint32_t>(keys, keys_alt, wv, wv_alt, nwin,
+                                                                54, hist, part, s, ts)),
               "low-word sort");
-    hipLaunchKernelGGL(k_narrow, dim3(blocks_for(nwin, 256)), dim3(256), 0, s, wv, nwin, hi);
+    hi = wv;  // the high words, now in low-word order, become the keys
+    hi_alt = wv_alt;
     BUILD_HIP((radix_sort<uint32_t, true>(hi, hi_alt, keys, keys_alt, nwin, narrow ? 18 : 19,
                                           hist, part, s)),
               "high-word sort");

@@ -40,8 +40,8 @@ def test_build_bytes_per_window():
     # 36-bit 2-gram keys: four 9-bit passes; 37 bits (vocab 2^18): five.
     assert bench.build_bytes_per_window(2, 151936) == 16 + 3 * 24 + 16
     assert bench.build_bytes_per_window(2, 1 << 18) == 16 + 4 * 24 + 16
-    assert bench.build_bytes_per_window(4, 151936) == 24 + 5 * 40 + 12 + 2 * 28 + 24
-    assert bench.build_bytes_per_window(4, 1 << 18) == 24 + 5 * 40 + 12 + 3 * 28 + 24
+    assert bench.build_bytes_per_window(4, 151936) == 20 + 5 * 32 + 2 * 28 + 24
+    assert bench.build_bytes_per_window(4, 1 << 18) == 20 + 5 * 32 + 3 * 28 + 24
     assert bench.build_bytes_per_window(3, 151936) > bench.build_bytes_per_window(2, 151936)
 
 
