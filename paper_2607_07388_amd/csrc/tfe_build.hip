@@ -69,6 +69,7 @@ static_assert(kBins <= (uint32_t)kTileThreads, "one scatter thread per digit");
 constexpr int kScanThreads = 1024;
 constexpr int kScanItems = 16;
 constexpr int kScanBlock = kScanThreads * kScanItems;
+constexpr uint32_t kScanRawBlocks = 4096;
 
 // ---- 1. keys -----------------------------------------------------------------
 
@@ -262,10 +263,22 @@ __device__ __forceinline__ uint32_t wave_incl_scan(uint32_t x) {
 
 // Pass 3: scan within blocks plus the block offset.  Wave w of a block scans
 // its contiguous kScanItems x 64 elements in rounds of 64 (coalesced), with
-// a running carry; one exchange of wave totals places the waves.
+// a running carry; one exchange of wave totals places the waves.  RAW: part
+// holds the blocks' sums as pass 1 left them (pass 2 skipped) and each block
+// adds up those of the blocks before it itself.
+template <bool RAW>
 __global__ __launch_bounds__(kScanThreads) void k_scan_down(const uint32_t* in, uint64_t n,
                                                             const uint32_t* part, uint32_t* out) {
   __shared__ uint32_t s_tot[kScanThreads / 64];
+  __shared__ uint32_t s_red[kScanThreads / 64];
+  uint32_t off = 0;
+  if (RAW) {
+    uint32_t b = 0;
+    for (uint32_t j = threadIdx.x; j < blockIdx.x; j += kScanThreads) b += part[j];
+    (void)block_scan_excl<kScanThreads>(b, s_red, &off);
+  } else {
+    off = part[blockIdx.x];
+  }
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const uint64_t base = (uint64_t)blockIdx.x * kScanBlock + (uint64_t)wave * (64 * kScanItems);
   uint32_t v[kScanItems];
@@ -284,7 +297,6 @@ __global__ __launch_bounds__(kScanThreads) void k_scan_down(const uint32_t* in, 
   }
   if (lane == 0) s_tot[wave] = carry;
   __syncthreads();
-  uint32_t off = part[blockIdx.x];
   for (int w = 0; w < wave; ++w) off += s_tot[w];
 #pragma unroll
   for (int k = 0; k < kScanItems; ++k) {
@@ -737,8 +749,14 @@ hipError_t scan_u32(const uint32_t* in, uint32_t* out, uint64_t n, uint32_t* par
   const uint32_t nb = blocks_for(n, kScanBlock);
   if (nb == 0) return hipSuccess;
   hipLaunchKernelGGL(k_scan_reduce, dim3(nb), dim3(kScanThreads), 0, s, in, n, part);
-  hipLaunchKernelGGL(k_scan_partials, dim3(1), dim3(kScanThreads), 0, s, part, nb, total);
-  hipLaunchKernelGGL(k_scan_down, dim3(nb), dim3(kScanThreads), 0, s, in, n, part, out);
+  // Up to kScanRawBlocks blocks, each down block sums the earlier blocks'
+  // totals (at most 16 KB, cached) instead of a one-block scan launch.
+  if (!total && nb <= kScanRawBlocks) {
+    hipLaunchKernelGGL(k_scan_down<true>, dim3(nb), dim3(kScanThreads), 0, s, in, n, part, out);
+  } else {
+    hipLaunchKernelGGL(k_scan_partials, dim3(1), dim3(kScanThreads), 0, s, part, nb, total);
+    hipLaunchKernelGGL(k_scan_down<false>, dim3(nb), dim3(kScanThreads), 0, s, in, n, part, out);
+  }
   return hipGetLastError();
 }
 
