@@ -69,7 +69,6 @@ static_assert(kBins <= (uint32_t)kTileThreads, "one scatter thread per digit");
 constexpr int kScanThreads = 1024;
 constexpr int kScanItems = 16;
 constexpr int kScanBlock = kScanThreads * kScanItems;
-constexpr uint32_t kScanRawBlocks = 4096;
 
 // ---- 1. keys -----------------------------------------------------------------
 
@@ -225,7 +224,8 @@ __global__ __launch_bounds__(kScanThreads) void k_scan_reduce(const uint32_t* in
   if (threadIdx.x == 0) part[blockIdx.x] = tot;
 }
 
-// Pass 2: exclusive scan of the block sums in one block (nb <= kScanBlock).
+// Exclusive scan of the block sums in one block (nb <= kScanBlock), and
+// their total: the run count places its starts with it.
 __global__ __launch_bounds__(kScanThreads) void k_scan_partials(uint32_t* part, uint32_t nb,
                                                                 uint32_t* total) {
   __shared__ uint32_t s_wave[kScanThreads / 64];
@@ -263,21 +263,23 @@ __device__ __forceinline__ uint32_t wave_incl_scan(uint32_t x) {
 
 // Pass 3: scan within blocks plus the block offset.  Wave w of a block scans
 // its contiguous kScanItems x 64 elements in rounds of 64 (coalesced), with
-// a running carry; one exchange of wave totals places the waves.  RAW: part
-// holds the blocks' sums as pass 1 left them (pass 2 skipped) and each block
-// adds up those of the blocks before it itself.
-template <bool RAW>
+// a running carry; one exchange of wave totals places the waves.  part
+// holds the blocks' sums as pass 1 left them: each block adds up those of
+// the blocks before it itself (at most kScanItems per thread, from L2),
+// which saves a one-block scan launch.
 __global__ __launch_bounds__(kScanThreads) void k_scan_down(const uint32_t* in, uint64_t n,
                                                             const uint32_t* part, uint32_t* out) {
   __shared__ uint32_t s_tot[kScanThreads / 64];
   __shared__ uint32_t s_red[kScanThreads / 64];
   uint32_t off = 0;
-  if (RAW) {
+  {
     uint32_t b = 0;
-    for (uint32_t j = threadIdx.x; j < blockIdx.x; j += kScanThreads) b += part[j];
+#pragma unroll
+    for (int k = 0; k < kScanItems; ++k) {
+      const uint32_t j = (uint32_t)k * kScanThreads + threadIdx.x;
+      b += j < blockIdx.x ? part[j] : 0u;
+    }
     (void)block_scan_excl<kScanThreads>(b, s_red, &off);
-  } else {
-    off = part[blockIdx.x];
   }
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const uint64_t base = (uint64_t)blockIdx.x * kScanBlock + (uint64_t)wave * (64 * kScanItems);
@@ -745,18 +747,12 @@ uint32_t blocks_for(uint64_t n, uint64_t per) { return (uint32_t)((n + per - 1) 
 
 // Exclusive scan of n uint32 values (in may equal out); total to *total (device).
 hipError_t scan_u32(const uint32_t* in, uint32_t* out, uint64_t n, uint32_t* part,
-                    uint32_t* total, hipStream_t s) {
+                    hipStream_t s) {
   const uint32_t nb = blocks_for(n, kScanBlock);
   if (nb == 0) return hipSuccess;
+  if (nb > (uint32_t)kScanBlock) return hipErrorInvalidValue;
   hipLaunchKernelGGL(k_scan_reduce, dim3(nb), dim3(kScanThreads), 0, s, in, n, part);
-  // Up to kScanRawBlocks blocks, each down block sums the earlier blocks'
-  // totals (at most 16 KB, cached) instead of a one-block scan launch.
-  if (!total && nb <= kScanRawBlocks) {
-    hipLaunchKernelGGL(k_scan_down<true>, dim3(nb), dim3(kScanThreads), 0, s, in, n, part, out);
-  } else {
-    hipLaunchKernelGGL(k_scan_partials, dim3(1), dim3(kScanThreads), 0, s, part, nb, total);
-    hipLaunchKernelGGL(k_scan_down<false>, dim3(nb), dim3(kScanThreads), 0, s, in, n, part, out);
-  }
+  hipLaunchKernelGGL(k_scan_down, dim3(nb), dim3(kScanThreads), 0, s, in, n, part, out);
   return hipGetLastError();
 }
 
@@ -767,7 +763,7 @@ hipError_t radix_pass(K* keys, K* keys_alt, V* vals, V* vals_alt, const TokSrc& 
   constexpr int ITEMS = tile_items<K, PAIRS, V>();
   hipLaunchKernelGGL((k_rs_hist<K, tile_keys<K, PAIRS, V>(), SRC>), dim3(ntiles), dim3(kHistThreads),
                      0, s, keys, ts, n, shift, hist, ntiles);
-  hipError_t e = scan_u32(hist, hist, (uint64_t)kBins * ntiles, part, nullptr, s);
+  hipError_t e = scan_u32(hist, hist, (uint64_t)kBins * ntiles, part, s);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL((k_rs_scatter<K, V, PAIRS, ITEMS, SRC>), dim3(ntiles), dim3(kTileThreads), 0, s,
                      keys, vals, ts, n, shift, hist, ntiles, keys_alt, vals_alt);
@@ -1001,12 +997,12 @@ tfe_status ngram_top(const int32_t* tokens, int64_t N, int32_t vocab, int32_t n,
   BUILD_HIP(hipGetLastError(), "select launches");
   // state = {c*, ~0, needed runs with count c*, runs above c*}.
   hipLaunchKernelGGL(k_sel_eq, dim3(blocks_for(U, 256)), dim3(256), 0, s, ucnt, U, d_small, eq);
-  BUILD_HIP(scan_u32(eq, eq, U, part, nullptr, s), "tie scan");
+  BUILD_HIP(scan_u32(eq, eq, U, part, s), "tie scan");
   uint32_t* keep = ustart;  // the run starts are no longer needed
   hipLaunchKernelGGL(k_sel_keep, dim3(blocks_for(U, 256)), dim3(256), 0, s, ucnt, U, d_small, eq,
                      keep);
   uint32_t* pos = eq;
-  BUILD_HIP(scan_u32(keep, pos, U, part, nullptr, s), "keep scan");
+  BUILD_HIP(scan_u32(keep, pos, U, part, s), "keep scan");
   uint32_t* rkey = sc.get<uint32_t>(R);
   uint32_t* rkey_alt = sc.get<uint32_t>(R);
   uint64_t* rval = sc.get<uint64_t>(R);
