@@ -138,6 +138,35 @@ def algorithmic_bytes(T, hits, keys, window):
     return (T * 2 * D * ESZ + hits * (D * ESZ + 4) + keys * 8 + T * window * 4 + T * (1 + 4 + 1))
 
 
+def counts_after_run(n_sets, run, sync, count):
+    """Per-set counts read from outputs that the set's own call wrote: one
+    untimed call of every rotating set (the warmup may have covered fewer
+    sets than there are), a synchronisation, then count(k) for each set.
+    Output buffers start filled with a sentinel, so counting a set that never
+    ran would read the sentinel, not hits."""
+    for k in range(n_sets):
+        run(k)
+    sync()
+    return [count(k) for k in range(n_sets)]
+
+
+def check_line(result):
+    """Refuses to print a line whose rates cannot be measurements: every hit
+    rate in [0, 1] and every roofline fraction in [0, 1]."""
+    def walk(x, path):
+        if isinstance(x, dict):
+            for k, v in x.items():
+                if k in ("hit_rate", "frac", "frac_of_8tbs") and v is not None:
+                    if not (0.0 <= float(v) <= 1.0):
+                        raise AssertionError("%s.%s = %r is outside [0, 1]" % (path, k, v))
+                walk(v, path + "." + k)
+        elif isinstance(x, list):
+            for i, v in enumerate(x):
+                walk(v, "%s[%d]" % (path, i))
+    walk(result, "line")
+    return result
+
+
 def algorithmic_bytes_multi(T, rows, keys, window, L):
     """Multi-match variant: one value row and row id per retained phrase, a
     match mask and L row ids per position."""
@@ -223,13 +252,15 @@ def main():
 
     for k in range(args.warmup):
         call(k)
-    torch.cuda.synchronize()
     if multi:
         # Retained rows per set: the population count of the match masks.
-        hits = [int(sum(((s[3].hit >> j) & 1).sum().item() for j in range(L))) for s in sets]
+        hits = counts_after_run(
+            len(sets), call, torch.cuda.synchronize,
+            lambda k: int(sum(((sets[k][3].hit >> j) & 1).sum().item() for j in range(L))))
         positions_hit = [int((s[3].hit > 0).sum().item()) for s in sets]
     else:
-        hits = [int(s[3].hit.sum().item()) for s in sets]
+        hits = counts_after_run(len(sets), call, torch.cuda.synchronize,
+                                lambda k: int(sets[k][3].hit.sum().item()))
         positions_hit = hits
     keys = B * L
 
@@ -304,7 +335,13 @@ def main():
                               outs.len, tfe.TFE_GATE_SIGMOID, 1.0, stream.cuda_stream)
     torch.cuda.synchronize()
     lwall = time.perf_counter() - l0
-    lhits = float(np.mean([s[2].hit.float().mean().item() for s in lat_sets]))
+    def lat_call(k):
+        tok, hid, outs = lat_sets[k]
+        tfe.tfe_lookup_inject(gt.handle, tok, 64, ctx, S, hid, outs.out, outs.hit, outs.slot,
+                              outs.len, tfe.TFE_GATE_SIGMOID, 1.0, stream.cuda_stream)
+
+    lhits = float(np.mean(counts_after_run(len(lat_sets), lat_call, torch.cuda.synchronize,
+                                           lambda k: lat_sets[k][2].hit.float().mean().item())))
     # Graph-replayed: 64 decode steps (rotating over the sets) captured once
     # and replayed, as a decode loop without per-call launch overhead.
     graph_us = None
@@ -454,7 +491,7 @@ def main():
             "sample": "the same passes with the set's rows split over %d threads (%.1f s)"
                       % (nthr, psec)}
     gt.close()
-    print(json.dumps(result))
+    print(json.dumps(check_line(result)))
 
 
 def finish_multi(args, table, gt, sets, mslots, B, ctx, S, window, L, tokens_per_s, wall,
@@ -530,7 +567,7 @@ def finish_multi(args, table, gt, sets, mslots, B, ctx, S, window, L, tokens_per
                       % (done // B, B, csec),
         }
     gt.close()
-    print(json.dumps(result))
+    print(json.dumps(check_line(result)))
 
 
 def keys_formed(B, ctx, S, n_min, n_max):
@@ -589,8 +626,8 @@ def run_resident_config(args):
 
         for k in range(args.warmup):
             call(k)
-        torch.cuda.synchronize()
-        hits = [int(st[2].hit.sum().item()) for st in sets]
+        hits = counts_after_run(nsets, call, torch.cuda.synchronize,
+                                lambda k: int(sets[k][2].hit.sum().item()))
         _, _, _, B, ctx, S = sets[0]
         T = B * S
         keys = keys_formed(B, ctx, S, table.n_min, table.n_max)
@@ -639,7 +676,7 @@ def run_resident_config(args):
         "runs": runs,
     }
     gt.close()
-    print(json.dumps(result))
+    print(json.dumps(check_line(result)))
 
 
 def synth_hidden(batch, B):
@@ -740,7 +777,7 @@ def run_head(args):
                       % (done, csec),
         }
     tfe.tfe_head_free(head)
-    print(json.dumps(result))
+    print(json.dumps(check_line(result)))
 
 
 def build_bytes_per_window(n, vocab):
@@ -847,7 +884,7 @@ def run_build(args):
             **host_cpu(),
             "sample": "2-gram top-2^19 of the first 2^20 tokens of the stream, repeated "
                       "(%.1f s, single thread)" % csec}
-    print(json.dumps(result))
+    print(json.dumps(check_line(result)))
 
 
 def run_tiered(args):
@@ -991,7 +1028,7 @@ def run_tiered(args):
     first = cold[0]
     best = max((r for r in results if r["t_hide_us"] == 0.0), key=lambda r: r["tokens_per_s"],
                default=results[0])
-    print(json.dumps({
+    print(json.dumps(check_line({
         "metric": "tiered lookup+inject tokens/sec, batch-64 decode, 1 MI355X",
         "value": best["tokens_per_s"],
         "unit": "tokens/s",
@@ -1022,7 +1059,7 @@ def run_tiered(args):
                                  "host-to-device copy measured in the same run" % first["fill"]},
         },
         "runs": results,
-    }))
+    })))
 
 
 if __name__ == "__main__":

@@ -115,7 +115,7 @@ typedef struct {
 typedef struct {
   uint64_t calls;            /* tfe_lookup_inject calls */
   uint64_t positions;        /* injected positions looked up */
-  uint64_t hits;             /* positions with a match (tiered mode; resident: 0) */
+  uint64_t hits;             /* positions with a match (multi-match: any length) */
   uint64_t cache_hits;       /* tiered: matched rows found in the HBM cache */
   uint64_t cache_misses;     /* tiered: matched rows fetched from host memory */
   uint64_t prefetch_keys;    /* tiered: candidate phrases probed by tfe_prefetch */
@@ -197,7 +197,11 @@ tfe_status tfe_lookup_inject_multi(tfe_table *table, const int32_t *tokens, int3
  * For every row b and candidate c the phrases ending at c, i.e. the n-grams
  * (tail[b, tail_len-n+1 ..], c) for n = n_min..n_max, are looked up; the
  * longest one present in the table (the phrase the next lookup selects if c
- * is the next token) is copied into the cache unless it is cached already.
+ * is the next token) is that candidate's row.  The candidates' rows are
+ * referenced as a lookup references its positions' rows: cached ones are
+ * never evicted by this prefetch and become most recent; the others are
+ * copied into least-recently-used unreferenced slots (in candidate order,
+ * while such slots are left) and become most recent too.
  * The work runs on `side_stream` after the table's previous lookup; the
  * next tfe_lookup_inject waits for it. */
 tfe_status tfe_prefetch(tfe_table *table, const int32_t *tail, int32_t tail_len,
@@ -214,10 +218,12 @@ tfe_status tfe_prefetch(tfe_table *table, const int32_t *tail, int32_t tail_len,
  * Each candidate's longest match r gets s = p * len(r) * c, with c = 1 when
  * the row is only in host memory and 0 when it is cached (r_i reads as the
  * phrase length: longer phrases are the more specific entries).  A row named
- * by several candidates keeps its highest score.  Rows with a positive score
- * are fetched by descending score (ties: lowest candidate index) until the
- * budget or the free cache slots run out; the rest count as dropped.
- * B * K <= 2048. */
+ * by several candidates keeps its highest score.  Cached rows with a
+ * positive p * len are referenced (not evicted by this prefetch; most
+ * recent, by first candidate).  Rows with a positive score are fetched by
+ * descending score (ties: lowest candidate index) until the budget or the
+ * unreferenced cache slots run out; the rest count as dropped.  Any B * K
+ * (scratch of about 40 bytes per candidate stays with the table). */
 tfe_status tfe_prefetch_scored(tfe_table *table, const int32_t *tail, int32_t tail_len,
                                const int32_t *candidates, const float *cand_prob, int32_t B,
                                int32_t K, int32_t budget, void *side_stream);
@@ -282,11 +288,31 @@ tfe_status tfe_ngram_top(const int32_t *tokens, int64_t n_tokens, int32_t vocab,
  * to the device allocator.  Buffers of calls still running are kept. */
 tfe_status tfe_ngram_release(void);
 
-/* Copies the table's counters (synchronises with the table's pending work). */
-tfe_status tfe_get_stats(tfe_table *table, tfe_stats *out);
+/* Copies the table's counters.  Waits on the host for the work the table
+ * has enqueued (its last lookup's stream up to now, a pending prefetch, the
+ * table's internal stream) and for nothing else: other streams keep running.
+ * The stream of the last lookup must still exist.  `calls` and `positions`
+ * count API calls; a lookup captured into a HIP graph counts its matched
+ * positions in `hits` at every replay (once the replay's stream has been
+ * synchronised by the caller), its call and positions once. */
+tfe_status tfe_get_stats(const tfe_table *table, tfe_stats *out);
 
-/* Resets the table's counters to zero (stream-ordered after pending work). */
+/* Resets the table's counters to zero, after the table's pending work (the
+ * same wait as tfe_get_stats). */
 tfe_status tfe_reset_stats(tfe_table *table);
+
+/* Residency of phrase rows: where each phrase's memory vector lives (the
+ * second index level of Eq. 10, phrase id -> storage tier and offset, and the
+ * tiers of Eq. 12).
+ *   rows  DEVICE int32 [n]: phrase row ids.
+ *   out   DEVICE int32 [n]: tiered tables: the HBM cache slot holding the
+ *         row, or -1 where it is only in host memory; resident tables: the
+ *         row itself (every row is in HBM at its own index); -2 for ids
+ *         outside [0, n_phrases).
+ * Stream-ordered on `stream` after the table's last lookup and a pending
+ * prefetch; changes nothing. */
+tfe_status tfe_residency(const tfe_table *table, const int32_t *rows, int64_t n, int32_t *out,
+                         void *stream);
 
 /* Message describing the last error returned on this host thread ("" if none). */
 const char *tfe_last_error(void);

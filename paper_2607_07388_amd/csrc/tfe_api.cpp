@@ -3,6 +3,7 @@
 #include <math.h>
 #include <stdarg.h>
 #include <stdio.h>
+#include <stdlib.h>
 #include <string.h>
 
 #include <stddef.h>
@@ -49,20 +50,40 @@ static tfe_status hip_fail(hipError_t e, const char* what) {
 
 static size_t elem_size(int dtype) { return dtype == TFE_F32 ? 4 : 2; }
 
+// Waits on the host for the work this table has enqueued -- its last
+// lookup, a pending prefetch, its own stream (uploads, side-stream fills) --
+// and for nothing else on the device.  A lookup still being captured into a
+// graph has not run yet and is not waited for.
+static tfe_status sync_table(const tfe_table* ct) {
+  tfe_table* t = const_cast<tfe_table*>(ct);  // events are recorded, nothing observable changes
+  if (t->lookup_recorded && t->ev_lookup) {
+    hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+    TFE_HIP(hipStreamIsCapturing(t->last_stream, &cs), "hipStreamIsCapturing");
+    if (cs == hipStreamCaptureStatusNone) {
+      TFE_HIP(hipEventRecord(t->ev_lookup, t->last_stream), "record");
+      TFE_HIP(hipEventSynchronize(t->ev_lookup), "wait for the last lookup");
+    }
+  }
+  if (t->prefetch_pending && t->ev_prefetch)
+    TFE_HIP(hipEventSynchronize(t->ev_prefetch), "wait for the prefetch");
+  if (t->own_stream) TFE_HIP(hipStreamSynchronize(t->own_stream), "wait for the table stream");
+  return TFE_OK;
+}
+
 static void release(tfe_table* t) {
   if (!t) return;
   // Teardown is best effort: errors here have no one to report to.
   int cur = 0;
   (void)hipGetDevice(&cur);
   (void)hipSetDevice(t->device);
-  (void)hipDeviceSynchronize();
+  (void)sync_table(t);
   void* dev_bufs[] = {t->d_slots, t->d_values, t->d_cache, t->d_where, t->d_owner, t->d_stamp,
-                      t->d_filled_at, t->d_pref, t->d_ring, t->d_ring2, t->d_ctl, t->d_row_of,
-                      t->d_slot_of, t->d_phase, t->d_jobs};
+                      t->d_pref, t->d_ring, t->d_ring2, t->d_ctl, t->d_row_of,
+                      t->d_slot_of, t->d_phase, t->d_jobs, t->d_hit_ctr, t->d_hkey, t->d_hpos, t->d_hval, t->d_blk};
   for (void* b : dev_bufs)
     if (b) (void)hipFree(b);
   if (t->own_h_values && t->h_values) (void)hipHostFree(t->h_values);
-  if (t->fill_stream) (void)hipStreamDestroy(t->fill_stream);
+  if (t->own_stream) (void)hipStreamDestroy(t->own_stream);
   hipEvent_t evs[] = {t->ev_resolved, t->ev_filled, t->ev_lookup, t->ev_prefetch};
   for (hipEvent_t e : evs)
     if (e) (void)hipEventDestroy(e);
@@ -80,6 +101,13 @@ static tfe_status check_device(const tfe_table* t) {
 }
 
 static tfe_status load_resident(tfe_table* t, const tfe_table_desc* d, hipStream_t stream) {
+  const size_t ctr_bytes = (size_t)kHitCounters * kHitStride * sizeof(unsigned long long);
+  if (hipMalloc((void**)&t->d_hit_ctr, ctr_bytes) != hipSuccess) {
+    t->d_hit_ctr = nullptr;
+    return fail(TFE_ERR_OOM, "hit counters (%zu bytes)", ctr_bytes);
+  }
+  TFE_HIP(hipMemsetAsync(t->d_hit_ctr, 0, ctr_bytes, stream), "hit counters");
+  TFE_HIP(hipStreamSynchronize(stream), "hit counters");
   if (d->n_phrases == 0) return TFE_OK;
   const size_t vbytes = (size_t)d->n_phrases * d->dim * elem_size(d->dtype);
   if (hipMalloc(&t->d_values, vbytes) != hipSuccess)
@@ -112,7 +140,6 @@ static tfe::TierArgs tier_args(tfe_table* t) {
   a.where = t->d_where;
   a.owner = t->d_owner;
   a.stamp = t->d_stamp;
-  a.filled_at = t->d_filled_at;
   a.pref = t->d_pref;
   a.ring = t->d_ring;
   a.ring_mask = t->ring_cap - 1;
@@ -121,6 +148,11 @@ static tfe::TierArgs tier_args(tfe_table* t) {
   a.slot_of = t->d_slot_of;
   a.phase = t->d_phase;
   a.jobs = t->d_jobs;
+  a.hkey = t->d_hkey;
+  a.hpos = t->d_hpos;
+  a.hval = t->d_hval;
+  a.hmask = 2 * (uint64_t)t->scratch_cap - 1;
+  a.blk = t->d_blk;
   a.clock = t->clock;
   a.row_bytes = (uint32_t)(t->dim * elem_size(t->dtype));
   a.fill_inline = t->fill_mode == TFE_FILL_INLINE ? 1u : 0u;
@@ -175,7 +207,6 @@ static tfe_status load_tiered(tfe_table* t, const tfe_table_desc* d, hipStream_t
   TFE_TRY(dev_alloc(&t->d_where, where_n, "residency map"));
   TFE_TRY(dev_alloc(&t->d_owner, (size_t)C, "slot owners"));
   TFE_TRY(dev_alloc(&t->d_stamp, (size_t)C, "slot stamps"));
-  TFE_TRY(dev_alloc(&t->d_filled_at, (size_t)C, "slot fill stamps"));
   TFE_TRY(dev_alloc(&t->d_pref, (size_t)C, "prefetch flags"));
   t->ring_cap = pow2_at_least((uint64_t)C * 4 < 4096 ? 4096 : (uint64_t)C * 4);
   TFE_TRY(dev_alloc(&t->d_ring, t->ring_cap, "recency ring"));
@@ -190,31 +221,44 @@ static tfe_status load_tiered(tfe_table* t, const tfe_table_desc* d, hipStream_t
                            hipMemcpyHostToDevice, stream),
             "cache prefill");
   t->ring_bound = (uint64_t)C;
-  TFE_HIP(hipStreamCreateWithFlags(&t->fill_stream, hipStreamNonBlocking), "fill stream");
-  hipEvent_t* evs[] = {&t->ev_resolved, &t->ev_filled, &t->ev_lookup, &t->ev_prefetch};
-  for (hipEvent_t* ev : evs)
-    TFE_HIP(hipEventCreateWithFlags(ev, hipEventDisableTiming), "events");
+  // Test hook: TFE_TIER_CLOCK_START starts the recency clock elsewhere than
+  // 0 (the tests start it just below the 32-bit wrap).  Stamps start at 0,
+  // below any clock a call uses.
+  if (const char* cs = getenv("TFE_TIER_CLOCK_START")) t->clock = (uint32_t)strtoul(cs, nullptr, 0);
   TFE_HIP(hipStreamSynchronize(stream), "tiered init");
   return TFE_OK;
 }
 
-// Grows the per-call scratch (rows, slots, phases, fill jobs) to n entries.
+// Grows the per-call scratch (rows, slots, phases, fill jobs) to n entries,
+// after the table's pending work that may still use the old buffers.
 static tfe_status ensure_scratch(tfe_table* t, uint32_t n) {
   if (n <= t->scratch_cap) return TFE_OK;
-  TFE_HIP(hipDeviceSynchronize(), "scratch regrow");
-  void* olds[] = {t->d_row_of, t->d_slot_of, t->d_phase, t->d_jobs};
+  TFE_TRY(sync_table(t));
+  void* olds[] = {t->d_row_of, t->d_slot_of, t->d_phase, t->d_jobs, t->d_hkey, t->d_hpos,
+                  t->d_hval, t->d_blk};
   for (void* b : olds)
     if (b) (void)hipFree(b);
   t->d_row_of = t->d_slot_of = nullptr;
   t->d_phase = nullptr;
   t->d_jobs = nullptr;
+  t->d_hkey = t->d_hpos = t->d_hval = t->d_blk = nullptr;
   t->scratch_cap = 0;
-  const uint32_t cap = (uint32_t)pow2_at_least(n < 1024 ? 1024 : n);
+  const uint64_t cap = pow2_at_least(n < 1024 ? 1024 : n);
   TFE_TRY(dev_alloc(&t->d_row_of, cap, "scratch"));
   TFE_TRY(dev_alloc(&t->d_slot_of, cap, "scratch"));
   TFE_TRY(dev_alloc(&t->d_phase, cap, "scratch"));
   TFE_TRY(dev_alloc(&t->d_jobs, cap, "scratch"));
-  t->scratch_cap = cap;
+  TFE_TRY(dev_alloc(&t->d_hkey, 2 * cap, "scratch"));
+  TFE_TRY(dev_alloc(&t->d_hpos, 2 * cap, "scratch"));
+  TFE_TRY(dev_alloc(&t->d_hval, 2 * cap, "scratch"));
+  TFE_TRY(dev_alloc(&t->d_blk, cap / 1024 + 1, "scratch"));
+  // Clock 0 tags every entry of the call-wide row table as empty (calls use
+  // clocks from 1).
+  TFE_HIP(hipMemsetAsync(t->d_hkey, 0, 2 * cap * sizeof(uint64_t), t->own_stream), "scratch");
+  TFE_HIP(hipMemsetAsync(t->d_hpos, 0, 2 * cap * sizeof(uint64_t), t->own_stream), "scratch");
+  TFE_HIP(hipMemsetAsync(t->d_hval, 0, 2 * cap * sizeof(uint64_t), t->own_stream), "scratch");
+  TFE_HIP(hipStreamSynchronize(t->own_stream), "scratch");
+  t->scratch_cap = (uint32_t)cap;
   return TFE_OK;
 }
 
@@ -237,7 +281,7 @@ static tfe_status reserve_ring(tfe_table* t, uint64_t appends, hipStream_t strea
       (void)hipFree(r1);
       return TFE_ERR_OOM;
     }
-    TFE_HIP(tfe::launch_ring_compact(a, r1, cap - 1, stream), "ring compaction");
+    TFE_HIP(tfe::launch_ring_compact(a, r1, cap - 1, false, stream), "ring compaction");
     TFE_HIP(hipStreamSynchronize(stream), "ring regrow");
     (void)hipFree(t->d_ring);
     (void)hipFree(t->d_ring2);
@@ -245,12 +289,40 @@ static tfe_status reserve_ring(tfe_table* t, uint64_t appends, hipStream_t strea
     t->d_ring2 = r2;
     t->ring_cap = cap;
   } else {
-    TFE_HIP(tfe::launch_ring_compact(a, t->d_ring2, t->ring_cap - 1, stream), "ring compaction");
+    TFE_HIP(tfe::launch_ring_compact(a, t->d_ring2, t->ring_cap - 1, false, stream),
+            "ring compaction");
     uint64_t* tmp = t->d_ring;
     t->d_ring = t->d_ring2;
     t->d_ring2 = tmp;
   }
   t->ring_bound = (uint64_t)t->cache_rows + appends;
+  return TFE_OK;
+}
+
+// Starts the next call's recency clock.  Stamps and the call-wide row
+// table hold 32-bit clocks; before the clock would wrap, every live recency
+// entry and slot stamp restart at 0 (order kept) and the row table is
+// cleared, so clocks 1, 2, ... can be used again.
+static tfe_status advance_clock(tfe_table* t, uint64_t appends, hipStream_t stream) {
+  if (t->clock == 0xFFFFFFFFu) {
+    tfe::TierArgs a = tier_args(t);
+    TFE_HIP(tfe::launch_ring_compact(a, t->d_ring2, t->ring_cap - 1, true, stream),
+            "clock restart");
+    uint64_t* tmp = t->d_ring;
+    t->d_ring = t->d_ring2;
+    t->d_ring2 = tmp;
+    t->ring_bound = (uint64_t)t->cache_rows + appends;  // this call's reservation
+    if (t->scratch_cap) {
+      TFE_HIP(hipMemsetAsync(t->d_hkey, 0, 2 * (size_t)t->scratch_cap * sizeof(uint64_t), stream),
+              "clock restart");
+      TFE_HIP(hipMemsetAsync(t->d_hpos, 0, 2 * (size_t)t->scratch_cap * sizeof(uint64_t), stream),
+              "clock restart");
+      TFE_HIP(hipMemsetAsync(t->d_hval, 0, 2 * (size_t)t->scratch_cap * sizeof(uint64_t), stream),
+              "clock restart");
+    }
+    t->clock = 0;
+  }
+  t->clock++;
   return TFE_OK;
 }
 
@@ -262,19 +334,21 @@ static tfe_status lookup_tiered(tfe_table* t, const LookupArgs& look, hipStream_
     TFE_HIP(hipEventRecord(t->ev_lookup, t->last_stream), "record");
     TFE_HIP(hipStreamWaitEvent(stream, t->ev_lookup, 0), "wait lookup");
   }
-  TFE_TRY(reserve_ring(t, look.T, stream));
-  t->clock++;
-  tfe::TierArgs a = tier_args(t);
-  a.look = look;
-  const bool fused = tfe::lookup_resolve_fused(look.T);
-  if (!fused) TFE_HIP(tfe::launch_tier_probe(a, stream), "tier probe");
+  // A pending prefetch and the previous call's side-stream cache fill use
+  // the same per-call scratch (matched rows, fill list), the recency ring
+  // and the residency state as everything below, so every kernel of this
+  // call -- ring compaction and the probe included -- waits for them.
   if (t->prefetch_pending) {
     TFE_HIP(hipStreamWaitEvent(stream, t->ev_prefetch, 0), "wait prefetch");
     t->prefetch_pending = false;
   }
-  // The previous call's cache fill must land before this call reuses its
-  // slots, and before the fill list is rewritten.
   if (t->fill_recorded) TFE_HIP(hipStreamWaitEvent(stream, t->ev_filled, 0), "wait fill");
+  TFE_TRY(reserve_ring(t, look.T, stream));
+  TFE_TRY(advance_clock(t, look.T, stream));
+  tfe::TierArgs a = tier_args(t);
+  a.look = look;
+  const bool fused = tfe::lookup_resolve_fused(look.T);
+  if (!fused) TFE_HIP(tfe::launch_tier_probe(a, stream), "tier probe");
   if (fused)
     TFE_HIP(tfe::launch_lookup_resolve_small(a, stream), "tier probe + resolve");
   else
@@ -283,9 +357,9 @@ static tfe_status lookup_tiered(tfe_table* t, const LookupArgs& look, hipStream_
     // Missed rows are copied into their new cache slots on the side stream,
     // overlapped with the injection, which reads them from host memory.
     TFE_HIP(hipEventRecord(t->ev_resolved, stream), "record");
-    TFE_HIP(hipStreamWaitEvent(t->fill_stream, t->ev_resolved, 0), "wait resolve");
-    TFE_HIP(tfe::launch_fill(a, t->dtype, t->dim, look.T, t->fill_stream), "tier fill");
-    TFE_HIP(hipEventRecord(t->ev_filled, t->fill_stream), "record");
+    TFE_HIP(hipStreamWaitEvent(t->own_stream, t->ev_resolved, 0), "wait resolve");
+    TFE_HIP(tfe::launch_fill(a, t->dtype, t->dim, look.T, t->own_stream), "tier fill");
+    TFE_HIP(hipEventRecord(t->ev_filled, t->own_stream), "record");
     t->fill_recorded = true;
   }
   // Inline fill: the injection writes each missed row into its slot.
@@ -301,9 +375,6 @@ static tfe_status prefetch_tiered(tfe_table* t, const int32_t* tail, int32_t tai
   const uint64_t N = (uint64_t)B * K;
   if (N == 0) return TFE_OK;
   if (N > 0x7FFFFFFFull) return fail(TFE_ERR_UNSUPPORTED, "B * K above 2^31 - 1");
-  if (prob && N > tfe::scored_prefetch_max())
-    return fail(TFE_ERR_UNSUPPORTED, "scored prefetch takes at most %u candidates",
-                tfe::scored_prefetch_max());
   TFE_TRY(check_device(t));
   TFE_TRY(refuse_capture(side, "a prefetch"));
   TFE_TRY(ensure_scratch(t, (uint32_t)N));
@@ -316,15 +387,19 @@ static tfe_status prefetch_tiered(tfe_table* t, const int32_t* tail, int32_t tai
   if (t->fill_recorded) TFE_HIP(hipStreamWaitEvent(side, t->ev_filled, 0), "wait fill");
   if (t->prefetch_pending) TFE_HIP(hipStreamWaitEvent(side, t->ev_prefetch, 0), "wait prefetch");
   TFE_TRY(reserve_ring(t, N, side));
-  t->clock++;
+  TFE_TRY(advance_clock(t, N, side));
   tfe::TierArgs a = tier_args(t);
   TFE_HIP(tfe::launch_prefetch_probe(a, tail, tail_len, cand, (uint32_t)B, (uint32_t)K, side),
           "prefetch probe");
-  if (prob)
+  if (prob) {
     TFE_HIP(tfe::launch_resolve_prefetch_scored(a, (uint32_t)N, prob, (uint32_t)budget, side),
             "prefetch resolve");
-  else
-    TFE_HIP(tfe::launch_resolve_prefetch(a, (uint32_t)N, side), "prefetch resolve");
+  } else {
+    // The candidates are referenced like a lookup's positions.
+    a.look.T = (uint32_t)N;
+    a.prefetch = 1;
+    TFE_HIP(tfe::launch_resolve_lookup(a, side), "prefetch resolve");
+  }
   TFE_HIP(tfe::launch_fill(a, t->dtype, t->dim, (uint32_t)N, side), "prefetch fill");
   TFE_HIP(hipEventRecord(t->ev_prefetch, side), "record");
   t->prefetch_pending = true;
@@ -378,6 +453,16 @@ static tfe_status load(const tfe_table_desc* d, hipStream_t stream, tfe_table** 
   t->dim = d->dim;
   t->dtype = d->dtype;
   t->capacity = cap;
+  {
+    hipError_t ce = hipStreamCreateWithFlags(&t->own_stream, hipStreamNonBlocking);
+    hipEvent_t* evs[] = {&t->ev_resolved, &t->ev_filled, &t->ev_lookup, &t->ev_prefetch};
+    for (hipEvent_t* ev : evs)
+      if (ce == hipSuccess) ce = hipEventCreateWithFlags(ev, hipEventDisableTiming);
+    if (ce != hipSuccess) {
+      release(t);
+      return hip_fail(ce, "table stream and events");
+    }
+  }
 
   const size_t slot_bytes = (size_t)cap * sizeof(tfe_slot);
   if (hipMalloc((void**)&t->d_slots, slot_bytes) != hipSuccess) {
@@ -448,15 +533,20 @@ static tfe_status lookup_inject(tfe_table* t, const int32_t* tokens, int32_t B, 
   a.inv_d = 1.0f / (float)t->dim;
   a.inv_sqrt_d = (float)(1.0 / sqrt((double)t->dim));
   a.weighting = weighting;
+  a.hit_ctr = t->cache_rows > 0 ? nullptr : t->d_hit_ctr;
   if (multi) {
     a.len_out = nullptr;
     TFE_HIP(launch_lookup_inject_multi(a, t->dtype, t->dim, stream), "lookup_inject_multi launch");
     t->stats.positions += (uint64_t)T;
+    t->lookup_recorded = true;
+    t->last_stream = stream;
     return TFE_OK;
   }
   if (t->cache_rows > 0) return lookup_tiered(t, a, stream);
   TFE_HIP(launch_lookup_inject(a, t->dtype, t->dim, stream), "lookup_inject launch");
   t->stats.positions += (uint64_t)T;
+  t->lookup_recorded = true;
+  t->last_stream = stream;
   return TFE_OK;
 }
 
@@ -512,7 +602,9 @@ tfe_status tfe_prefetch_scored(tfe_table* table, const int32_t* tail, int32_t ta
   tfe::clear_error();
   if (!table) return tfe::fail(TFE_ERR_INVALID_ARG, "null table");
   if (tail_len < 0 || B < 0 || K < 0) return tfe::fail(TFE_ERR_INVALID_ARG, "negative size");
-  if (budget < 0 || budget > 1024) return tfe::fail(TFE_ERR_INVALID_ARG, "budget outside [0, 1024]");
+  if (budget < 0 || budget > (int32_t)tfe::scored_prefetch_budget_max())
+    return tfe::fail(TFE_ERR_INVALID_ARG, "budget outside [0, %u]",
+                     tfe::scored_prefetch_budget_max());
   if ((int64_t)B * K > 0 && (!candidates || !cand_prob || (tail_len > 0 && !tail)))
     return tfe::fail(TFE_ERR_INVALID_ARG, "null tail, candidates or probabilities");
   if (table->cache_rows == 0) return TFE_OK;
@@ -520,39 +612,86 @@ tfe_status tfe_prefetch_scored(tfe_table* table, const int32_t* tail, int32_t ta
                               (hipStream_t)side_stream);
 }
 
-tfe_status tfe_get_stats(tfe_table* table, tfe_stats* out) {
+tfe_status tfe_get_stats(const tfe_table* table, tfe_stats* out) {
   tfe::clear_error();
   if (!table || !out) return tfe::fail(TFE_ERR_INVALID_ARG, "null table or out");
-  *out = table->stats;
+  tfe_status st = tfe::sync_table(table);
+  if (st != TFE_OK) return st;
+  tfe_stats s = table->stats;
   if (table->cache_rows > 0) {
     tfe::TierCtl c;
-    hipError_t e = hipDeviceSynchronize();
-    if (e == hipSuccess) e = hipMemcpy(&c, table->d_ctl, sizeof c, hipMemcpyDeviceToHost);
+    hipError_t e = hipMemcpyAsync(&c, table->d_ctl, sizeof c, hipMemcpyDeviceToHost,
+                                  table->own_stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(table->own_stream);
     if (e != hipSuccess) return tfe::fail(TFE_ERR_HIP, "stats: %s", hipGetErrorString(e));
-    out->positions = c.stats.positions;
-    out->hits = c.stats.hits;
-    out->cache_hits = c.stats.cache_hits;
-    out->cache_misses = c.stats.cache_misses;
-    out->prefetch_keys = c.stats.prefetch_keys;
-    out->prefetch_found = c.stats.prefetch_found;
-    out->prefetch_filled = c.stats.prefetch_filled;
-    out->prefetch_used = c.stats.prefetch_used;
-    out->host_bytes = c.stats.host_bytes;
-    out->prefetch_dropped = c.stats.prefetch_dropped;
+    s.positions = c.stats.positions;
+    s.hits = c.stats.hits;
+    s.cache_hits = c.stats.cache_hits;
+    s.cache_misses = c.stats.cache_misses;
+    s.prefetch_keys = c.stats.prefetch_keys;
+    s.prefetch_found = c.stats.prefetch_found;
+    s.prefetch_filled = c.stats.prefetch_filled;
+    s.prefetch_used = c.stats.prefetch_used;
+    s.host_bytes = c.stats.host_bytes;
+    s.prefetch_dropped = c.stats.prefetch_dropped;
+  } else if (table->d_hit_ctr) {
+    unsigned long long ctr[tfe::kHitCounters * tfe::kHitStride];
+    hipError_t e = hipMemcpyAsync(ctr, table->d_hit_ctr, sizeof ctr, hipMemcpyDeviceToHost,
+                                  table->own_stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(table->own_stream);
+    if (e != hipSuccess) return tfe::fail(TFE_ERR_HIP, "stats: %s", hipGetErrorString(e));
+    s.hits = 0;
+    for (int i = 0; i < tfe::kHitCounters; ++i) s.hits += ctr[i * tfe::kHitStride];
   }
+  *out = s;
   return TFE_OK;
 }
 
 tfe_status tfe_reset_stats(tfe_table* table) {
   tfe::clear_error();
   if (!table) return tfe::fail(TFE_ERR_INVALID_ARG, "null table");
+  tfe_status st = tfe::sync_table(table);
+  if (st != TFE_OK) return st;
   table->stats = tfe_stats{};
-  if (table->cache_rows > 0) {
-    hipError_t e = hipDeviceSynchronize();
-    if (e == hipSuccess)
-      e = hipMemset((char*)table->d_ctl + offsetof(tfe::TierCtl, stats), 0, sizeof(tfe::TierStats));
-    if (e != hipSuccess) return tfe::fail(TFE_ERR_HIP, "reset stats: %s", hipGetErrorString(e));
+  hipError_t e = hipSuccess;
+  if (table->cache_rows > 0)
+    e = hipMemsetAsync((char*)table->d_ctl + offsetof(tfe::TierCtl, stats), 0,
+                       sizeof(tfe::TierStats), table->own_stream);
+  else if (table->d_hit_ctr)
+    e = hipMemsetAsync(table->d_hit_ctr, 0,
+                       sizeof(unsigned long long) * tfe::kHitCounters * tfe::kHitStride,
+                       table->own_stream);
+  if (e == hipSuccess) e = hipStreamSynchronize(table->own_stream);
+  if (e != hipSuccess) return tfe::fail(TFE_ERR_HIP, "reset stats: %s", hipGetErrorString(e));
+  return TFE_OK;
+}
+
+tfe_status tfe_residency(const tfe_table* table, const int32_t* rows, int64_t n, int32_t* out,
+                         void* stream) {
+  tfe::clear_error();
+  if (!table) return tfe::fail(TFE_ERR_INVALID_ARG, "null table");
+  if (n < 0 || n > 0x7FFFFFFF00ll) return tfe::fail(TFE_ERR_INVALID_ARG, "bad n");
+  if (n > 0 && (!rows || !out)) return tfe::fail(TFE_ERR_INVALID_ARG, "null rows or out");
+  tfe_status st = tfe::check_device(table);
+  if (st != TFE_OK) return st;
+  if (n == 0) return TFE_OK;
+  hipStream_t s = (hipStream_t)stream;
+  tfe_table* t = const_cast<tfe_table*>(table);  // events only
+  if (t->cache_rows > 0) {
+    // After the table's last lookup and a pending prefetch.
+    if (t->lookup_recorded && s != t->last_stream) {
+      hipError_t e = hipEventRecord(t->ev_lookup, t->last_stream);
+      if (e == hipSuccess) e = hipStreamWaitEvent(s, t->ev_lookup, 0);
+      if (e != hipSuccess) return tfe::fail(TFE_ERR_HIP, "residency: %s", hipGetErrorString(e));
+    }
+    if (t->prefetch_pending) {
+      const hipError_t e = hipStreamWaitEvent(s, t->ev_prefetch, 0);
+      if (e != hipSuccess) return tfe::fail(TFE_ERR_HIP, "residency: %s", hipGetErrorString(e));
+    }
   }
+  const hipError_t e = tfe::launch_residency(t->cache_rows > 0 ? t->d_where : nullptr,
+                                             t->n_phrases, rows, n, out, s);
+  if (e != hipSuccess) return tfe::fail(TFE_ERR_HIP, "residency: %s", hipGetErrorString(e));
   return TFE_OK;
 }
 

@@ -271,5 +271,14 @@ __device__ __forceinline__ void write_result(const LookupArgs& a, uint32_t p, in
   if (a.len_out) a.len_out[p] = (uint8_t)len;
 }
 
+// Resident tables: one matched position added to the table's hit count
+// (called by one lane of the position's wave).  The counter is picked by
+// block, so a launch's additions spread over kHitCounters lines.
+__device__ __forceinline__ void count_hit(const LookupArgs& a, bool matched) {
+  if (a.hit_ctr && matched)
+    __hip_atomic_fetch_add(a.hit_ctr + (blockIdx.x & (kHitCounters - 1)) * kHitStride, 1ull,
+                           __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
 }  // namespace dev
 }  // namespace tfe

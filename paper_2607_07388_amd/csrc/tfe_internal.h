@@ -48,7 +48,14 @@ struct LookupArgs {
   float inv_d;                // 1 / dim
   float inv_sqrt_d;           // 1 / sqrt(dim)
   int32_t weighting;          // multi-match kernel: tfe_weighting
+  // Resident tables: matched-position counters, kHitCounters of them
+  // kHitStride words apart (one 128-byte line each, so that the waves of a
+  // launch spread their additions over many addresses); null for tiered
+  // tables, whose resolve kernels count their own.
+  unsigned long long* hit_ctr;
 };
+constexpr int kHitCounters = 64;
+constexpr int kHitStride = 16;
 
 // Device-side bookkeeping of a tiered table (see tfe_tiered.hip).
 struct TierStats {
@@ -58,6 +65,7 @@ struct TierStats {
 struct TierCtl {
   unsigned long long head, tail;  // recency ring cursors (monotone)
   unsigned long long njobs;       // host -> cache copies of the current call
+  unsigned long long call_head;   // long calls: ring head before the call's appends
   TierStats stats;
 };
 struct TierJob {
@@ -70,7 +78,6 @@ struct TierArgs {
   int32_t* where;             // [P]  slot or -1
   int32_t* owner;             // [C]  row or -1
   uint32_t* stamp;            // [C]  clock of the last reference
-  uint32_t* filled_at;        // [C]  clock of the last fill
   uint8_t* pref;              // [C]  filled by a prefetch and not used yet
   uint64_t* ring;             // recency ring of (slot << 32 | stamp)
   uint64_t ring_mask;
@@ -79,9 +86,16 @@ struct TierArgs {
   int32_t* slot_of;           // [cap]
   uint8_t* phase;             // [cap]
   TierJob* jobs;              // [cap]
+  uint64_t* hkey;             // [2 cap] long calls: call-wide row table (clock << 32 | row)
+  uint64_t* hpos;             // [2 cap] its first positions (clock << 32 | ~position)
+  uint64_t* hval;             // [2 cap] scored prefetch: best score (clock << 32 | bits)
+  uint64_t hmask;             // 2 cap - 1
+  uint64_t* blk;              // [cap / 1024 + 1] per-block first-position counts
   uint32_t clock;
   uint32_t row_bytes;
   uint32_t fill_inline;       // the inject writes missed rows into their slots
+  uint32_t prefetch;          // resolve kernels: the call is a prefetch (fills are marked
+                              // prefetched; prefetch counters instead of lookup counters)
 };
 
 // Phase bit of a position whose inject writes its row into slot_of (inline
@@ -90,18 +104,23 @@ constexpr uint8_t kPhaseWrite = 0x10;
 
 hipError_t launch_tier_init(const TierArgs& t, uint32_t C, uint32_t prefill, hipStream_t s);
 hipError_t launch_ring_compact(const TierArgs& t, uint64_t* dst, uint64_t dst_mask,
-                               hipStream_t s);
+                               bool restamp, hipStream_t s);
 hipError_t launch_tier_probe(const TierArgs& t, hipStream_t s);
+// Calls of at most lookup_resolve_one_block_max() positions: one block;
+// longer calls: the multi-block pipeline (mark, first, pop, assign).
+uint32_t lookup_resolve_one_block_max();
 hipError_t launch_resolve_lookup(const TierArgs& t, hipStream_t s);
 // Decode-sized lookups: probe + resolve in one single-block launch.
 bool lookup_resolve_fused(uint32_t T);
 hipError_t launch_lookup_resolve_small(const TierArgs& t, hipStream_t s);
 hipError_t launch_prefetch_probe(const TierArgs& t, const int32_t* tail, int32_t tail_len,
                                  const int32_t* cand, uint32_t B, uint32_t K, hipStream_t s);
-hipError_t launch_resolve_prefetch(const TierArgs& t, uint32_t N, hipStream_t s);
 hipError_t launch_resolve_prefetch_scored(const TierArgs& t, uint32_t N, const float* prob,
                                          uint32_t budget, hipStream_t s);
-uint32_t scored_prefetch_max();
+uint32_t scored_prefetch_budget_max();
+// out[i] = where[rows[i]] (where = null: rows[i]); -2 outside [0, P).
+hipError_t launch_residency(const int32_t* where, int64_t P, const int32_t* rows, int64_t n,
+                            int32_t* out, hipStream_t s);
 hipError_t launch_fill(const TierArgs& t, int dtype, int dim, uint32_t max_jobs, hipStream_t s);
 hipError_t launch_tier_inject(const TierArgs& t, int dtype, int dim, hipStream_t s);
 
@@ -129,6 +148,8 @@ struct tfe_table {
   tfe_slot* d_slots = nullptr;   // [capacity]
   void* d_values = nullptr;      // resident: [P x dim]
   tfe_stats stats = {};          // host-side counters (calls, resident positions)
+  unsigned long long* d_hit_ctr = nullptr;  // resident: [kHitCounters * kHitStride]
+  hipStream_t own_stream = nullptr;  // the table's own stream: uploads, stats, fills
 
   // Tiered mode (cache_rows > 0).
   int64_t cache_rows = 0;
@@ -141,7 +162,6 @@ struct tfe_table {
   int32_t* d_where = nullptr;
   int32_t* d_owner = nullptr;
   uint32_t* d_stamp = nullptr;
-  uint32_t* d_filled_at = nullptr;
   uint8_t* d_pref = nullptr;
   uint64_t* d_ring = nullptr;
   uint64_t* d_ring2 = nullptr;
@@ -152,12 +172,15 @@ struct tfe_table {
   int32_t* d_slot_of = nullptr;
   uint8_t* d_phase = nullptr;
   tfe::TierJob* d_jobs = nullptr;
+  uint64_t* d_hkey = nullptr;    // [2 scratch_cap]
+  uint64_t* d_hpos = nullptr;    // [2 scratch_cap]
+  uint64_t* d_hval = nullptr;    // [2 scratch_cap]
+  uint64_t* d_blk = nullptr;     // [scratch_cap / 1024 + 1]
   uint32_t scratch_cap = 0;
   uint32_t clock = 0;
-  hipStream_t fill_stream = nullptr;
   hipEvent_t ev_resolved = nullptr, ev_filled = nullptr, ev_lookup = nullptr,
              ev_prefetch = nullptr;
   bool lookup_recorded = false, prefetch_pending = false, fill_recorded = false;
-  hipStream_t last_stream = nullptr;   // stream of the last lookup
+  hipStream_t last_stream = nullptr;   // stream of the last lookup (lookup_recorded)
 };
 #endif

@@ -59,7 +59,10 @@ __global__ __launch_bounds__(WPB * 64) void k_lookup_inject(const LookupArgs a) 
   const dev::Probe pr = dev::probe_begin(a, tw, lane);
   int len;
   const int32_t row = dev::probe_finish(a, pr, lane, &len);
-  if (lane == 0) dev::write_result(a, p, row, len);
+  if (lane == 0) {
+    dev::write_result(a, p, row, len);
+    dev::count_hit(a, row >= 0);
+  }
 
   u32x4* out = (u32x4*)a.hout + (size_t)p * ROW_VECS;
   if (row < 0) {

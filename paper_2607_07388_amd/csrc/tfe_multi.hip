@@ -62,7 +62,10 @@ __global__ __launch_bounds__(WPB * 64) void k_lookup_inject_multi(const LookupAr
     const int j = span - lane;
     a.slot_out[(size_t)p * (span + 1) + lane] = j == 0 ? rows[0] : (j == 1 ? rows[1] : rows[2]);
   }
-  if (lane == 0) a.hit[p] = (uint8_t)mask;
+  if (lane == 0) {
+    a.hit[p] = (uint8_t)mask;
+    dev::count_hit(a, mask != 0);
+  }
 
   u32x4* out = (u32x4*)a.hout + (size_t)p * ROW_VECS;
   if (mask == 0) {

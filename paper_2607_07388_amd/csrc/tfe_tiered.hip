@@ -207,11 +207,11 @@ __device__ __forceinline__ void block_count_n(const bool* f, uint32_t* rank, uin
   *total = run;
 }
 
-// pop_victims over windows of N kResolveThreads ring entries per round; the
-// row each victim slot holds is read with its stamp and kept in vown[].
-template <int N>
-__device__ __forceinline__ uint32_t pop_victims_n(const TierArgs& t, uint32_t need, uint32_t* vict,
-                                                  int32_t* vown) {
+// pop_victims over windows of N kResolveThreads ring entries per round;
+// out(i, slot, owner) receives victim i and the row its slot holds (read
+// with its stamp).
+template <int N, class Out>
+__device__ __forceinline__ uint32_t pop_victims_n(const TierArgs& t, uint32_t need, Out out) {
   __shared__ unsigned long long s_tail, s_head, s_last;
   __shared__ uint32_t s_got, s_stop;
   if (threadIdx.x == 0) {
@@ -255,8 +255,7 @@ __device__ __forceinline__ uint32_t pop_victims_n(const TierArgs& t, uint32_t ne
 #pragma unroll
     for (int k = 0; k < N; ++k) {
       if (live[k] && rank[k] < take) {
-        vict[got + rank[k]] = (uint32_t)(e[k] >> 32);
-        vown[got + rank[k]] = own[k];
+        out(got + rank[k], (uint32_t)(e[k] >> 32), own[k]);
         if (rank[k] == take - 1) s_last = base + (uint64_t)k * kResolveThreads + threadIdx.x;
       }
     }
@@ -322,16 +321,18 @@ __device__ __forceinline__ void wave_tally(bool f, uint32_t* counter) {
   if ((threadIdx.x & 63) == 0 && m) atomicAdd(counter, (uint32_t)__builtin_popcountll(m));
 }
 
-// Residency resolution of one lookup call (single block), positions in
-// consecutive groups of kGroup = kGroupItems x kResolveThreads (thread x
-// handles positions base + k kResolveThreads + x), in order.  Per position:
-// slot_of (cache slot or -1) and phase (0: cached before this call, read from
-// the cache; 1: filled in this call; 2: no slot free, not cached; 3: no
-// match).  Rows of phases 1 and 2 are read from host memory by the inject;
-// phase-1 rows are also written into their slot, by the inject (inline
-// fill) or by a copy on the side stream.  Each group reads its rows' state,
-// then the ring window, then writes: a few dependent round trips per 4096
-// positions.
+// Residency resolution of a lookup call of at most kGroup positions, in one
+// block (thread x handles positions k kResolveThreads + x).  A prefetch
+// (t.prefetch) is resolved the same way, its candidates standing for the
+// positions: it references its cached rows and fills the others, marked
+// prefetched.  Per position:
+// slot_of (cache slot or -1) and phase (0: cached when the call began, read
+// from the cache; 1: filled in this call; 2: not cached, no slot given to
+// it; 3: no match).  Rows of phases 1 and 2 are read from host memory by the
+// inject; a phase-1 row is also written into its slot, by the inject of its
+// first position (inline fill) or by a copy on the side stream.  Every
+// cached row of the call marks its slot referenced before any victim is
+// chosen, so no slot the call uses is evicted.
 constexpr int kGroupItems = 4;
 constexpr int kGroup = kGroupItems * kResolveThreads;
 constexpr int kGroupHash = 2 * kGroup;
@@ -340,151 +341,344 @@ __global__ __launch_bounds__(kResolveThreads) void k_resolve_lookup(const TierAr
   constexpr int N = kGroupItems;
   __shared__ int32_t hkey[kGroupHash];
   __shared__ uint32_t hpos[kGroupHash];
-  __shared__ int32_t hslot[kGroupHash];    // per row: slot after this group (-1: none)
+  __shared__ int32_t hslot[kGroupHash];    // per row: its slot after this call (-1: none)
   __shared__ uint8_t hphase[kGroupHash];
-  __shared__ uint8_t hcached[kGroupHash];  // per row: cached when the group began
   __shared__ uint32_t vict[kGroup];
   __shared__ int32_t vown[kGroup];  // row held by each victim slot
-  __shared__ unsigned long long s_njobs, s_head;
-  __shared__ uint32_t s_cnt[5];  // hits, cache hits, prefetch used, host-served, fills
-  if (threadIdx.x == 0) {
-    s_njobs = 0;
-    s_head = t.ctl->head;
-    for (int i = 0; i < 5; ++i) s_cnt[i] = 0;
+  __shared__ uint32_t s_cnt[4];  // hits, cache hits, prefetch used, host-served
+  if (threadIdx.x < 4) s_cnt[threadIdx.x] = 0;
+  const unsigned long long head0 = t.ctl->head;
+  int32_t r[N];
+  uint32_t pos[N];
+#pragma unroll
+  for (int k = 0; k < N; ++k) {
+    pos[k] = k * kResolveThreads + threadIdx.x;
+    const int32_t rr = t.row_of[pos[k] < T ? pos[k] : 0u];
+    r[k] = pos[k] < T ? rr : -1;
   }
-  for (uint32_t base = 0; base < T; base += kGroup) {
-    // Per-item flags are bit k of a per-thread word (registers, not lane
-    // masks); position of item k: base + k kResolveThreads + threadIdx.x.
-    int32_t r[N];
-    uint32_t pos[N];
+  int h[N];
+  bool fb[N];
+  first_of_rows<N, kGroupHash>(r, pos, hkey, hpos, h, fb);
+  // First occurrences read the row's slot; a cached row's slot becomes
+  // referenced (a stamp of this call keeps it from being a victim).  The
+  // rows are distinct and so are their slots, so all reads go before the
+  // writes; they are unconditional (index 0 where there is nothing to read)
+  // so that they issue back to back.
+  int32_t s0[N];
 #pragma unroll
-    for (int k = 0; k < N; ++k) {
-      pos[k] = base + k * kResolveThreads + threadIdx.x;
-      const int32_t rr = t.row_of[pos[k] < T ? pos[k] : 0u];
-      r[k] = pos[k] < T ? rr : -1;
-    }
-    int h[N];
-    bool fb[N];
-    first_of_rows<N, kGroupHash>(r, pos, hkey, hpos, h, fb);
-    uint32_t f_first = 0;
-#pragma unroll
-    for (int k = 0; k < N; ++k) f_first |= fb[k] ? 1u << k : 0u;
-    // First occurrences read the row's slot; a cached row's slot becomes
-    // referenced (a stamp of this call keeps it from being a victim).  The
-    // rows of a group are distinct and so are their slots, so all reads go
-    // before the writes; they are unconditional (index 0 where there is
-    // nothing to read) so that they issue back to back.
-    int32_t s0[N];
-#pragma unroll
-    for (int k = 0; k < N; ++k) {
-      const int32_t w = t.where[(uint32_t)max(r[k], 0)];
-      s0[k] = (f_first >> k) & 1u ? w : -1;
-    }
-    uint32_t st_old[N], fat[N], pf[N];
-#pragma unroll
-    for (int k = 0; k < N; ++k) {
-      const uint32_t sl = (uint32_t)max(s0[k], 0);
-      st_old[k] = t.stamp[sl];
-      fat[k] = t.filled_at[sl];
-      pf[k] = t.pref[sl];
-    }
-    uint32_t f_app = 0, f_miss = 0;
-#pragma unroll
-    for (int k = 0; k < N; ++k) {
-      bool used = false;
-      if ((f_first >> k) & 1u) hcached[h[k]] = s0[k] >= 0;
-      if (s0[k] >= 0) {
-        // Only a later group of this call can find its own stamp here.
-        if (base == 0 || st_old[k] != t.clock) f_app |= 1u << k;
-        t.stamp[s0[k]] = t.clock;
-        hslot[h[k]] = s0[k];
-        hphase[h[k]] = (base != 0 && fat[k] == t.clock) ? 1 : 0;
-        if (pf[k]) {
-          t.pref[s0[k]] = 0;
-          used = true;
-        }
-      } else if ((f_first >> k) & 1u) {
-        f_miss |= 1u << k;
-      }
-      wave_tally(used, &s_cnt[2]);
-    }
-    __syncthreads();
-    bool mb[N];
-#pragma unroll
-    for (int k = 0; k < N; ++k) mb[k] = (f_miss >> k) & 1u;
-    uint32_t mrank[N], need;
-    block_count_n<N>(mb, mrank, &need);
-    const uint32_t got = need ? pop_victims_n<N>(t, need, vict, vown) : 0;
-    uint32_t f_fill = 0;
-#pragma unroll
-    for (int k = 0; k < N; ++k) f_fill |= ((f_miss >> k) & 1u) && mrank[k] < got ? 1u << k : 0u;
-#pragma unroll
-    for (int k = 0; k < N; ++k) {
-      if ((f_fill >> k) & 1u) {
-        // Evicted rows were cached and filled rows were not: the two sets
-        // are disjoint, so these writes never collide.  A victim is never a
-        // slot of this call, so its owner is still the one the pop read.
-        const uint32_t vk = vict[mrank[k]];
-        const int32_t old = vown[mrank[k]];
-        if (old >= 0) t.where[old] = -1;
-        t.owner[vk] = r[k];
-        t.where[r[k]] = (int32_t)vk;
-        t.stamp[vk] = t.clock;
-        t.filled_at[vk] = t.clock;
-        t.pref[vk] = 0;
-        t.jobs[s_njobs + mrank[k]] = TierJob{r[k], (int32_t)vk};
-        hslot[h[k]] = (int32_t)vk;
-        hphase[h[k]] = 1;
-        f_app |= 1u << k;
-      } else if ((f_miss >> k) & 1u) {
-        hslot[h[k]] = -1;
-        hphase[h[k]] = 2;
-      }
-    }
-    __syncthreads();
-#pragma unroll
-    for (int k = 0; k < N; ++k) {
-      const bool valid = pos[k] < T;
-      const bool m = r[k] >= 0;
-      const int32_t s1 = m ? hslot[h[k]] : -1;
-      const uint8_t ph = m ? hphase[h[k]] : 3;
-      const bool writes = t.fill_inline && ((f_fill >> k) & 1u);
-      if (valid) {
-        t.slot_of[pos[k]] = s1;
-        t.phase[pos[k]] = writes ? (uint8_t)(ph | kPhaseWrite) : ph;
-      }
-      wave_tally(m, &s_cnt[0]);
-      wave_tally(m && hcached[h[k]], &s_cnt[1]);
-      wave_tally(m && ph != 0, &s_cnt[3]);
-    }
-    bool ab[N];
-#pragma unroll
-    for (int k = 0; k < N; ++k) ab[k] = (f_app >> k) & 1u;
-    uint32_t arank[N], napp;
-    block_count_n<N>(ab, arank, &napp);
-#pragma unroll
-    for (int k = 0; k < N; ++k)
-      if ((f_app >> k) & 1u)
-        t.ring[(s_head + arank[k]) & t.ring_mask] = ring_entry((uint32_t)hslot[h[k]], t.clock);
-    __syncthreads();
-    if (threadIdx.x == 0) {
-      s_head += napp;
-      s_njobs += got;
-      s_cnt[4] += got;
-      t.ctl->head = s_head;
-    }
-    __syncthreads();
+  for (int k = 0; k < N; ++k) {
+    const int32_t w = t.where[(uint32_t)max(r[k], 0)];
+    s0[k] = fb[k] ? w : -1;
   }
+  uint32_t pf[N];
+#pragma unroll
+  for (int k = 0; k < N; ++k) pf[k] = t.pref[(uint32_t)max(s0[k], 0)];
+  uint32_t f_app = 0, f_miss = 0;
+#pragma unroll
+  for (int k = 0; k < N; ++k) {
+    bool used = false;
+    if (s0[k] >= 0) {
+      f_app |= 1u << k;
+      t.stamp[s0[k]] = t.clock;
+      hslot[h[k]] = s0[k];
+      hphase[h[k]] = 0;
+      if (pf[k] && !t.prefetch) {  // a lookup uses the prefetched row
+        t.pref[s0[k]] = 0;
+        used = true;
+      }
+    } else if (fb[k]) {
+      f_miss |= 1u << k;
+    }
+    wave_tally(used, &s_cnt[2]);
+  }
+  __threadfence_block();  // this call's stamps, before the ring walk reads them
+  __syncthreads();
+  bool mb[N];
+#pragma unroll
+  for (int k = 0; k < N; ++k) mb[k] = (f_miss >> k) & 1u;
+  uint32_t mrank[N], need;
+  block_count_n<N>(mb, mrank, &need);
+  const uint32_t got =
+      need ? pop_victims_n<N>(t, need, [&](uint32_t i, uint32_t slot, int32_t own) {
+        vict[i] = slot;
+        vown[i] = own;
+      }) : 0;
+  uint32_t f_fill = 0;
+#pragma unroll
+  for (int k = 0; k < N; ++k) f_fill |= ((f_miss >> k) & 1u) && mrank[k] < got ? 1u << k : 0u;
+#pragma unroll
+  for (int k = 0; k < N; ++k) {
+    if ((f_fill >> k) & 1u) {
+      // Evicted rows were cached and filled rows were not: the two sets
+      // are disjoint, so these writes never collide.  A victim is never a
+      // slot of this call, so its owner is still the one the pop read.
+      const uint32_t vk = vict[mrank[k]];
+      const int32_t old = vown[mrank[k]];
+      if (old >= 0) t.where[old] = -1;
+      t.owner[vk] = r[k];
+      t.where[r[k]] = (int32_t)vk;
+      t.stamp[vk] = t.clock;
+      t.pref[vk] = t.prefetch ? 1 : 0;
+      t.jobs[mrank[k]] = TierJob{r[k], (int32_t)vk};
+      hslot[h[k]] = (int32_t)vk;
+      hphase[h[k]] = 1;
+      f_app |= 1u << k;
+    } else if ((f_miss >> k) & 1u) {
+      hslot[h[k]] = -1;
+      hphase[h[k]] = 2;
+    }
+  }
+  __syncthreads();
+#pragma unroll
+  for (int k = 0; k < N; ++k) {
+    const bool valid = pos[k] < T;
+    const bool m = r[k] >= 0;
+    const int32_t s1 = m ? hslot[h[k]] : -1;
+    const uint8_t ph = m ? hphase[h[k]] : 3;
+    const bool writes = t.fill_inline && ((f_fill >> k) & 1u);
+    if (valid) {
+      t.slot_of[pos[k]] = s1;
+      t.phase[pos[k]] = writes ? (uint8_t)(ph | kPhaseWrite) : ph;
+    }
+    wave_tally(m, &s_cnt[0]);
+    wave_tally(m && ph == 0, &s_cnt[1]);
+    wave_tally(m && ph != 0, &s_cnt[3]);
+  }
+  bool ab[N];
+#pragma unroll
+  for (int k = 0; k < N; ++k) ab[k] = (f_app >> k) & 1u;
+  uint32_t arank[N], napp;
+  block_count_n<N>(ab, arank, &napp);
+#pragma unroll
+  for (int k = 0; k < N; ++k)
+    if ((f_app >> k) & 1u)
+      t.ring[(head0 + arank[k]) & t.ring_mask] = ring_entry((uint32_t)hslot[h[k]], t.clock);
   if (threadIdx.x == 0) {
-    t.ctl->njobs = s_njobs;
+    t.ctl->head = head0 + napp;
+    t.ctl->njobs = got;
     TierStats& st = t.ctl->stats;
-    st.positions += T;
-    st.hits += s_cnt[0];
-    st.cache_hits += s_cnt[1];
-    st.cache_misses += s_cnt[0] - s_cnt[1];
-    st.prefetch_used += s_cnt[2];
-    st.host_bytes +=
-        (unsigned long long)((t.fill_inline ? 0u : s_cnt[4]) + s_cnt[3]) * t.row_bytes;
+    if (t.prefetch) {
+      st.prefetch_keys += T;
+      st.prefetch_found += s_cnt[0];
+      st.prefetch_filled += got;
+      st.host_bytes += (unsigned long long)got * t.row_bytes;
+    } else {
+      st.positions += T;
+      st.hits += s_cnt[0];
+      st.cache_hits += s_cnt[1];
+      st.cache_misses += s_cnt[0] - s_cnt[1];
+      st.prefetch_used += s_cnt[2];
+      st.host_bytes += (unsigned long long)((t.fill_inline ? 0u : got) + s_cnt[3]) * t.row_bytes;
+    }
+  }
+}
+
+// ---- Resolution of calls longer than kGroup positions, over many blocks.
+// The same policy as k_resolve_lookup, in four launches of which only the
+// victim pop is a single block:
+//   k_res_mark    every position reads its row's slot; a cached row's slot is
+//                 stamped referenced; the distinct rows of the block enter a
+//                 call-wide hash table that keeps each row's first position;
+//   k_res_first   first positions are found; per block, the number of first
+//                 positions of cached rows and of missed rows; counters;
+//   k_res_pop     those counts are scanned; the missed rows' victims are
+//                 taken from the recency ring (least recent first, skipping
+//                 referenced slots) into the fill list;
+//   k_res_assign  a missed row's first position takes victim number (its
+//                 rank among missed first positions) while any are left;
+//                 residency and recency entries are written in first-position
+//                 order, so the recency update equals the one-block kernel's.
+// The hash table lives in the table's scratch and is never cleared: an
+// entry holds (clock << 32 | row) and counts as empty unless its clock is
+// this call's; the first position is kept as (clock << 32 | ~pos) under an
+// atomic maximum, so a stale entry is replaced by any write of this call.
+constexpr int kMarkThreads = kResolveThreads;
+
+__device__ __forceinline__ uint64_t gh_home(int32_t r, uint64_t mask) {
+  return ((uint64_t)(uint32_t)r * 0x9E3779B97F4A7C15ull >> 29) & mask;
+}
+
+__device__ __forceinline__ uint64_t gh_load(const uint64_t* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Inserts row r (first seen at position p within its block) into the
+// call-wide table.
+__device__ void gh_insert(const TierArgs& t, int32_t r, uint32_t p) {
+  const uint64_t tag = (uint64_t)t.clock << 32;
+  const uint64_t want = tag | (uint32_t)r;
+  uint64_t h = gh_home(r, t.hmask);
+  for (;;) {
+    uint64_t old = gh_load(t.hkey + h);
+    // Entries only ever change from another call's to this call's, so a
+    // failed exchange returns the entry's final value.
+    while (old != want && (old >> 32) != t.clock) {
+      const uint64_t prev = atomicCAS((unsigned long long*)(t.hkey + h), (unsigned long long)old,
+                                      (unsigned long long)want);
+      old = prev == old ? want : prev;
+    }
+    if (old == want) break;
+    h = (h + 1) & t.hmask;
+  }
+  atomicMax((unsigned long long*)(t.hpos + h), (unsigned long long)(tag | (uint32_t)~p));
+}
+
+// True if p is the first position of the call naming row r (r >= 0 was
+// inserted by k_res_mark).
+__device__ __forceinline__ bool gh_is_first(const TierArgs& t, int32_t r, uint32_t p) {
+  const uint64_t tag = (uint64_t)t.clock << 32;
+  const uint64_t want = tag | (uint32_t)r;
+  uint64_t h = gh_home(r, t.hmask);
+  while (gh_load(t.hkey + h) != want) h = (h + 1) & t.hmask;
+  return gh_load(t.hpos + h) == (tag | (uint32_t)~p);
+}
+
+__global__ __launch_bounds__(kMarkThreads) void k_res_mark(const TierArgs t, uint32_t T) {
+  __shared__ int32_t hkey[kHashSize];
+  __shared__ uint32_t hpos[kHashSize];
+  const uint32_t p = blockIdx.x * kMarkThreads + threadIdx.x;
+  const int32_t r = p < T ? t.row_of[p] : -1;
+  const int32_t s = r >= 0 ? t.where[r] : -1;
+  if (p < T) t.slot_of[p] = s;
+  if (s >= 0) t.stamp[s] = t.clock;  // same value from every position naming the row
+  int h;
+  const bool first_here = first_of_row(r, p, hkey, hpos, &h);
+  if (first_here) gh_insert(t, r, p);
+}
+
+__global__ __launch_bounds__(kMarkThreads) void k_res_first(const TierArgs t, uint32_t T) {
+  __shared__ uint32_t s_cnt[3];  // hits, cache hits, prefetch used
+  if (threadIdx.x < 3) s_cnt[threadIdx.x] = 0;
+  const uint32_t p = blockIdx.x * kMarkThreads + threadIdx.x;
+  const int32_t r = p < T ? t.row_of[p] : -1;
+  const int32_t s = p < T ? t.slot_of[p] : -1;
+  const bool first = r >= 0 && gh_is_first(t, r, p);
+  const bool fc = first && s >= 0, fm = first && s < 0;
+  bool used = false;
+  if (fc && !t.prefetch && t.pref[s]) {  // a lookup uses the prefetched row
+    t.pref[s] = 0;
+    used = true;
+  }
+  __syncthreads();
+  wave_tally(r >= 0, &s_cnt[0]);
+  wave_tally(r >= 0 && s >= 0, &s_cnt[1]);
+  wave_tally(used, &s_cnt[2]);
+  uint32_t nc, nm;
+  block_count(fc, &nc);
+  block_count(fm, &nm);
+  if (threadIdx.x == 0) {
+    t.blk[blockIdx.x] = ((uint64_t)nm << 32) | nc;
+    TierStats& st = t.ctl->stats;
+    if (t.prefetch) {
+      atomicAdd(&st.prefetch_found, (unsigned long long)s_cnt[0]);
+    } else {
+      atomicAdd(&st.hits, (unsigned long long)s_cnt[0]);
+      atomicAdd(&st.cache_hits, (unsigned long long)s_cnt[1]);
+      atomicAdd(&st.cache_misses, (unsigned long long)(s_cnt[0] - s_cnt[1]));
+      atomicAdd(&st.prefetch_used, (unsigned long long)s_cnt[2]);
+      atomicAdd(&st.host_bytes, (unsigned long long)(s_cnt[0] - s_cnt[1]) * t.row_bytes);
+    }
+  }
+}
+
+// Exclusive scan of blk[0..n) in place (packed counts: each half stays
+// below 2^31, so the halves add without carries); returns the total.
+__device__ uint64_t block_scan_blk(uint64_t* blk, uint32_t n) {
+  __shared__ uint64_t s_w[kWaves];
+  __shared__ uint64_t s_run;
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  if (threadIdx.x == 0) s_run = 0;
+  __syncthreads();
+  for (uint32_t base = 0; base < n; base += kResolveThreads) {
+    const uint32_t i = base + threadIdx.x;
+    const uint64_t v = i < n ? blk[i] : 0;
+    uint64_t x = v;
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+      const uint64_t y = __shfl_up(x, d, 64);
+      if (lane >= d) x += y;
+    }
+    if (lane == 63) s_w[wave] = x;
+    __syncthreads();
+    uint64_t before = s_run;
+    for (int w = 0; w < wave; ++w) before += s_w[w];
+    if (i < n) blk[i] = before + x - v;
+    __syncthreads();
+    if (threadIdx.x == kResolveThreads - 1) s_run = before + x;
+    __syncthreads();
+  }
+  return s_run;
+}
+
+__global__ __launch_bounds__(kResolveThreads) void k_res_pop(const TierArgs t, uint32_t nblk) {
+  const uint64_t tot = block_scan_blk(t.blk, nblk);
+  const uint32_t ncf = (uint32_t)tot, need = (uint32_t)(tot >> 32);
+  TierJob* jobs = t.jobs;
+  const uint32_t got =
+      need ? pop_victims_n<kGroupItems>(t, need, [&](uint32_t i, uint32_t slot, int32_t own) {
+        jobs[i] = TierJob{own, (int32_t)slot};
+      }) : 0;
+  if (threadIdx.x == 0) {
+    const unsigned long long head0 = t.ctl->head;
+    t.ctl->call_head = head0;
+    t.ctl->head = head0 + ncf + got;
+    t.ctl->njobs = got;
+    TierStats& st = t.ctl->stats;
+    if (t.prefetch) {
+      st.prefetch_filled += got;
+      st.host_bytes += (unsigned long long)got * t.row_bytes;
+    } else if (!t.fill_inline) {
+      st.host_bytes += (unsigned long long)got * t.row_bytes;
+    }
+  }
+}
+
+__global__ __launch_bounds__(kMarkThreads) void k_res_assign(const TierArgs t, uint32_t T) {
+  const uint32_t p = blockIdx.x * kMarkThreads + threadIdx.x;
+  const int32_t r = p < T ? t.row_of[p] : -1;
+  const int32_t s = p < T ? t.slot_of[p] : -1;
+  const bool first = r >= 0 && gh_is_first(t, r, p);
+  const bool fc = first && s >= 0, fm = first && s < 0;
+  uint32_t nc, nm;
+  const uint32_t rc = block_count(fc, &nc);
+  const uint32_t rm = block_count(fm, &nm);
+  const uint64_t off = t.blk[blockIdx.x];
+  const uint32_t got = (uint32_t)t.ctl->njobs;
+  const unsigned long long head0 = t.ctl->call_head;
+  const uint32_t cbefore = (uint32_t)off + rc, mbefore = (uint32_t)(off >> 32) + rm;
+  // Appended entries before this position: every cached first position,
+  // and the missed first positions that got a slot (the first `got` of them).
+  const uint32_t arank = cbefore + (mbefore < got ? mbefore : got);
+  uint8_t ph = 3;
+  int32_t slot = -1;
+  if (r >= 0 && s >= 0) {
+    ph = 0;
+    slot = s;
+    if (fc) t.ring[(head0 + arank) & t.ring_mask] = ring_entry((uint32_t)s, t.clock);
+  } else if (r >= 0) {
+    ph = 2;
+    if (fm && mbefore < got) {
+      const TierJob job = t.jobs[mbefore];
+      const uint32_t v = (uint32_t)job.slot;
+      if (job.row >= 0) t.where[job.row] = -1;
+      t.owner[v] = r;
+      t.where[r] = (int32_t)v;
+      t.stamp[v] = t.clock;
+      t.pref[v] = t.prefetch ? 1 : 0;
+      t.jobs[mbefore] = TierJob{r, (int32_t)v};
+      t.ring[(head0 + arank) & t.ring_mask] = ring_entry(v, t.clock);
+      slot = (int32_t)v;
+      ph = t.fill_inline ? (uint8_t)(1 | kPhaseWrite) : (uint8_t)1;
+    }
+  }
+  if (p < T) {
+    t.slot_of[p] = slot;
+    t.phase[p] = ph;
+  }
+  if (p == 0) {
+    if (t.prefetch) t.ctl->stats.prefetch_keys += T;
+    else t.ctl->stats.positions += T;
   }
 }
 
@@ -659,7 +853,6 @@ __global__ __launch_bounds__(kResolveThreads) void k_lookup_resolve_small(const 
     t.owner[v] = r;
     t.where[r] = (int32_t)v;
     t.stamp[v] = t.clock;
-    t.filled_at[v] = t.clock;
     t.pref[v] = 0;
     t.jobs[mrank] = TierJob{r, (int32_t)v};
   }
@@ -693,124 +886,174 @@ __global__ __launch_bounds__(kResolveThreads) void k_lookup_resolve_small(const 
   }
 }
 
-// Prefetch resolution (single block): the candidates' rows in candidate
-// order; each distinct row that is not cached takes the least recent slot
-// (stopping when none is left) and is marked prefetched.
-__global__ __launch_bounds__(kResolveThreads) void k_resolve_prefetch(const TierArgs t, uint32_t N) {
-  __shared__ int32_t hkey[kHashSize];
-  __shared__ uint32_t hpos[kHashSize];
-  __shared__ uint32_t vict[kResolveThreads];
-  __shared__ uint32_t s_stop;
-  if (threadIdx.x == 0) {
-    t.ctl->njobs = 0;
-    s_stop = 0;
-  }
-  unsigned long long n_found = 0, n_fill = 0;
-  for (uint32_t base = 0; base < N; base += kResolveThreads) {
-    const uint32_t p = base + threadIdx.x;
-    const int32_t r = p < N ? t.row_of[p] : -1;
-    int h;
-    const bool first = first_of_row(r, p, hkey, hpos, &h);
-    __syncthreads();
-    // A row filled by an earlier group of this prefetch is cached by now.
-    const bool miss_first = first && r >= 0 && !s_stop && t.where[r] < 0;
-    uint32_t need;
-    const uint32_t mrank = block_count(miss_first, &need);
-    const uint32_t got = need ? pop_victims(t, need, vict) : 0;
-    if (miss_first && mrank < got) {
-      const uint32_t v = vict[mrank];
-      const int32_t old = t.owner[v];
-      if (old >= 0) t.where[old] = -1;
-      t.owner[v] = r;
-      t.where[r] = (int32_t)v;
-      t.stamp[v] = t.clock;
-      t.filled_at[v] = t.clock;
-      t.pref[v] = 1;
-      t.jobs[t.ctl->njobs + mrank] = TierJob{r, (int32_t)v};
-      t.ring[(t.ctl->head + mrank) & t.ring_mask] = ring_entry(v, t.clock);
+// Priority-scored, budgeted prefetch (Eq. 17: s = p * r * c), one block,
+// any number of candidates.  For candidate q with matched row r: p =
+// prob[q] (the predicted token's probability; <= 0 and NaN count as 0),
+// r = the matched phrase length (longer phrases are the more specific
+// entries), c = 1 if the row is only in host memory and 0 if it is cached.
+// A row named by several candidates keeps its highest p * len and its first
+// candidate index (both kept in the call-wide row table of the scratch).
+// Cached rows with a positive p * len are referenced: never victims of this
+// prefetch, most recent in order of first candidate.  Rows that are not
+// cached and score above zero are fetched by descending score, then first
+// candidate index, until `budget` rows are fetched or no unreferenced slot
+// is left; the rest are dropped.  Scores are float32 products compared as
+// float32 (as bit patterns: they are never negative).
+//   1. every candidate enters the row table: first index and best score;
+//   2. first candidates: cached rows with a score are stamped referenced and
+//      appended to the recency ring; rows to fetch go to a key list
+//      (~score << 32 | first index, so ascending keys = the fetch order);
+//   3. the budget-th smallest key is found by a radix select (8-bit digits
+//      from the top), the keys at or below it are gathered and sorted in LDS;
+//   4. victims are popped and the rows filled in that order.
+constexpr int kScoredBudgetMax = 1024;
+
+__device__ __forceinline__ uint64_t gh_insert_at(const TierArgs& t, int32_t r, uint32_t q) {
+  const uint64_t tag = (uint64_t)t.clock << 32;
+  const uint64_t want = tag | (uint32_t)r;
+  uint64_t h = gh_home(r, t.hmask);
+  for (;;) {
+    uint64_t old = gh_load(t.hkey + h);
+    while (old != want && (old >> 32) != t.clock) {
+      const uint64_t prev = atomicCAS((unsigned long long*)(t.hkey + h), (unsigned long long)old,
+                                      (unsigned long long)want);
+      old = prev == old ? want : prev;
     }
-    uint32_t c_found;
-    block_count(r >= 0, &c_found);
-    if (threadIdx.x == 0) {
-      t.ctl->head += got;
-      t.ctl->njobs += got;
-      if (got < need) s_stop = 1;
-    }
-    n_found += c_found;
-    n_fill += got;
-    __syncthreads();
+    if (old == want) break;
+    h = (h + 1) & t.hmask;
   }
-  if (threadIdx.x == 0) {
-    TierStats& st = t.ctl->stats;
-    st.prefetch_keys += N;
-    st.prefetch_found += n_found;
-    st.prefetch_filled += n_fill;
-    st.host_bytes += n_fill * t.row_bytes;
-  }
+  atomicMax((unsigned long long*)(t.hpos + h), (unsigned long long)(tag | (uint32_t)~q));
+  return h;
 }
 
-// Priority-scored, budgeted prefetch (Eq. 17: s = p * r * c), single block,
-// at most kScoredMax candidates.  For candidate q with matched row r:
-// p = prob[q] (the predicted token's probability), r = the matched phrase
-// length (longer phrases are the more specific entries), c = 1 if the row is
-// only in host memory and 0 if it is cached (no benefit).  A row named by
-// several candidates keeps its highest score and its first candidate index.
-// Rows with a positive score are fetched in order of score (descending),
-// then first candidate index, until `budget` rows are fetched or no free
-// slot is left; the rest are dropped.  Scores are float32 products, compared
-// as float32.
-constexpr int kScoredMax = 2048;
-constexpr int kScoredHash = 4096;
+__device__ __forceinline__ uint64_t gh_find(const TierArgs& t, int32_t r) {
+  const uint64_t want = ((uint64_t)t.clock << 32) | (uint32_t)r;
+  uint64_t h = gh_home(r, t.hmask);
+  while (gh_load(t.hkey + h) != want) h = (h + 1) & t.hmask;
+  return h;
+}
 
 __global__ __launch_bounds__(kResolveThreads) void k_resolve_prefetch_scored(
     const TierArgs t, uint32_t N, const float* __restrict__ prob, uint32_t budget) {
-  __shared__ int32_t hkey[kScoredHash];
-  __shared__ uint32_t hpos[kScoredHash];
-  __shared__ uint32_t hscore[kScoredHash];
-  __shared__ int32_t qrow[kScoredMax];
-  __shared__ unsigned long long keys[kScoredMax];
+  __shared__ unsigned long long sel[kScoredBudgetMax];
   __shared__ uint32_t vict[kResolveThreads];
-  __shared__ uint32_t s_n, s_found;
-  for (int i = threadIdx.x; i < kScoredHash; i += kResolveThreads) {
-    hkey[i] = -1;
-    hpos[i] = 0xFFFFFFFFu;
-    hscore[i] = 0;
-  }
+  __shared__ uint32_t hist[256];
+  __shared__ uint32_t s_found, s_nref, s_n, s_g, s_bin, s_before;
+  const uint64_t tag = (uint64_t)t.clock << 32;
+  uint64_t* klist = (uint64_t*)t.jobs;  // rows to fetch; becomes the fill list in step 4
   if (threadIdx.x == 0) {
-    s_n = 0;
     s_found = 0;
-    t.ctl->njobs = 0;
+    s_nref = 0;
+    s_n = 0;
+    s_g = 0;
   }
   __syncthreads();
-  for (uint32_t q = threadIdx.x; q < N; q += kResolveThreads) {
-    const int32_t r = t.row_of[q];
-    qrow[q] = r;
-    if (r < 0) continue;
-    atomicAdd(&s_found, 1u);
-    int h = (int)(((uint32_t)r * 2654435761u) >> 20) & (kScoredHash - 1);
-    for (;;) {
-      const int old = atomicCAS(&hkey[h], -1, r);
-      if (old == -1 || old == r) break;
-      h = (h + 1) & (kScoredHash - 1);
+  // 1. Row table: first candidate index and best score per row.
+  for (uint32_t base = 0; base < N; base += kResolveThreads) {
+    const uint32_t q = base + threadIdx.x;
+    const int32_t r = q < N ? t.row_of[q] : -1;
+    if (r >= 0) {
+      const float p = prob[q];
+      const float sc = (p > 0.0f ? p : 0.0f) * (float)t.phase[q];  // NaN and p <= 0 score 0
+      const uint64_t h = gh_insert_at(t, r, q);
+      atomicMax((unsigned long long*)(t.hval + h), (unsigned long long)(tag | __float_as_uint(sc)));
     }
-    atomicMin(&hpos[h], q);
-    const float p = prob[q];
-    const float sc = (p > 0.0f ? p : 0.0f) * (float)t.phase[q];  // NaN and p <= 0 score 0
-    atomicMax(&hscore[h], __float_as_uint(sc));
+    wave_tally(r >= 0, &s_found);
   }
+  __threadfence();  // the row table's atomics have completed before any wave reads it
   __syncthreads();
-  // Rows worth fetching: positive score and not cached.
-  for (int e = threadIdx.x; e < kScoredHash; e += kResolveThreads) {
-    const int32_t r = hkey[e];
-    if (r < 0 || hscore[e] == 0 || t.where[r] >= 0) continue;
-    const uint32_t k = atomicAdd(&s_n, 1u);
-    keys[k] = ((unsigned long long)(~hscore[e]) << 32) | hpos[e];
+  const unsigned long long head0 = t.ctl->head;
+  // 2. References and the key list, in candidate order.
+  for (uint32_t base = 0; base < N; base += kResolveThreads) {
+    const uint32_t q = base + threadIdx.x;
+    const int32_t r = q < N ? t.row_of[q] : -1;
+    bool ref = false, cand = false;
+    int32_t w = -1;
+    uint32_t sc = 0;
+    if (r >= 0) {
+      const uint64_t h = gh_find(t, r);
+      if (gh_load(t.hpos + h) == (tag | (uint32_t)~q)) {
+        sc = (uint32_t)gh_load(t.hval + h);
+        w = t.where[r];
+        ref = sc != 0 && w >= 0;
+        cand = sc != 0 && w < 0;
+      }
+    }
+    if (ref) t.stamp[w] = t.clock;
+    uint32_t nref, ncand;
+    const uint32_t rr = block_count(ref, &nref);
+    const uint32_t rc = block_count(cand, &ncand);
+    if (ref) t.ring[(head0 + s_nref + rr) & t.ring_mask] = ring_entry((uint32_t)w, t.clock);
+    if (cand) klist[s_n + rc] = ((uint64_t)~sc << 32) | q;
+    __threadfence_block();
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      s_nref += nref;
+      s_n += ncand;
+    }
+    __syncthreads();
   }
-  __syncthreads();
-  const uint32_t n = s_n;
+  const uint32_t n = s_n, nref = s_nref;
+  const uint32_t want = n < budget ? n : budget;
+  // 3. The want smallest keys: radix select of the threshold, then gather.
+  uint64_t prefix = 0, pmask = 0;
+  if (want > 0 && want < n) {
+    uint32_t rem = want;  // keys still to take at or below the prefix
+    for (int shift = 56; shift >= 0; shift -= 8) {
+      for (int i = threadIdx.x; i < 256; i += kResolveThreads) hist[i] = 0;
+      __syncthreads();
+      for (uint32_t i = threadIdx.x; i < n; i += kResolveThreads) {
+        const uint64_t k = klist[i];
+        if ((k & pmask) == prefix) atomicAdd(&hist[(k >> shift) & 255], 1u);
+      }
+      __syncthreads();
+      if (threadIdx.x < 64) {
+        // The bin where the running count reaches rem: lane l sums bins
+        // 4l .. 4l+3, then a wave scan.
+        const uint32_t c0 = hist[4 * threadIdx.x], c1 = hist[4 * threadIdx.x + 1],
+                       c2 = hist[4 * threadIdx.x + 2], c3 = hist[4 * threadIdx.x + 3];
+        uint32_t x = c0 + c1 + c2 + c3;
+        for (int d = 1; d < 64; d <<= 1) {
+          const uint32_t y = __shfl_up(x, d, 64);
+          if ((int)threadIdx.x >= d) x += y;
+        }
+        const uint32_t before = x - (c0 + c1 + c2 + c3);
+        if (before < rem && x >= rem) {
+          uint32_t b = 4 * threadIdx.x, acc = before;
+          const uint32_t cs[4] = {c0, c1, c2, c3};
+          int j = 0;
+          while (acc + cs[j] < rem) acc += cs[j++];
+          s_bin = b + j;
+          s_before = acc;
+        }
+      }
+      __syncthreads();
+      const uint32_t bin = s_bin;
+      rem -= s_before;
+      prefix |= (uint64_t)bin << shift;
+      pmask |= 255ull << shift;
+      const bool exact = hist[bin] == rem;  // every key of this prefix is taken
+      __syncthreads();
+      if (exact) break;
+    }
+  }
+  const uint64_t thresh = want == 0 ? 0 : (want < n ? (prefix | ~pmask) : ~0ull);
+  if (want > 0) {
+    for (uint32_t base = 0; base < n; base += kResolveThreads) {
+      const uint32_t i = base + threadIdx.x;
+      const uint64_t k = i < n ? klist[i] : ~0ull;
+      const bool take = i < n && k <= thresh;
+      uint32_t c;
+      const uint32_t rk = block_count(take, &c);
+      if (take) sel[s_g + rk] = k;
+      __syncthreads();
+      if (threadIdx.x == 0) s_g += c;
+      __syncthreads();
+    }
+  }
   uint32_t p2 = 1;
-  while (p2 < n) p2 <<= 1;
-  for (uint32_t i = n + threadIdx.x; i < p2; i += kResolveThreads) keys[i] = ~0ull;
+  while (p2 < want) p2 <<= 1;
+  for (uint32_t i = want + threadIdx.x; i < p2; i += kResolveThreads) sel[i] = ~0ull;
   __syncthreads();
   // Bitonic sort, ascending: highest score first, then lowest candidate index.
   for (uint32_t size = 2; size <= p2; size <<= 1) {
@@ -819,33 +1062,32 @@ __global__ __launch_bounds__(kResolveThreads) void k_resolve_prefetch_scored(
         const uint32_t a = 2 * i - (i & (stride - 1));
         const uint32_t b = a + stride;
         const bool up = (a & size) == 0;
-        const unsigned long long ka = keys[a], kb = keys[b];
+        const unsigned long long ka = sel[a], kb = sel[b];
         if ((ka > kb) == up) {
-          keys[a] = kb;
-          keys[b] = ka;
+          sel[a] = kb;
+          sel[b] = ka;
         }
       }
       __syncthreads();
     }
   }
-  const uint32_t want = n < budget ? n : budget;
+  // 4. Victims and fills (the key list is no longer read: jobs are rewritten).
   const uint32_t got = want ? pop_victims(t, want, vict) : 0;
   if (threadIdx.x < got) {
     const uint32_t v = vict[threadIdx.x];
-    const int32_t r = qrow[(uint32_t)keys[threadIdx.x]];
+    const int32_t r = t.row_of[(uint32_t)sel[threadIdx.x]];
     const int32_t old = t.owner[v];
     if (old >= 0) t.where[old] = -1;
     t.owner[v] = r;
     t.where[r] = (int32_t)v;
     t.stamp[v] = t.clock;
-    t.filled_at[v] = t.clock;
     t.pref[v] = 1;
     t.jobs[threadIdx.x] = TierJob{r, (int32_t)v};
-    t.ring[(t.ctl->head + threadIdx.x) & t.ring_mask] = ring_entry(v, t.clock);
+    t.ring[(head0 + nref + threadIdx.x) & t.ring_mask] = ring_entry(v, t.clock);
   }
   __syncthreads();
   if (threadIdx.x == 0) {
-    t.ctl->head += got;
+    t.ctl->head = head0 + nref + got;
     t.ctl->njobs = got;
     TierStats& st = t.ctl->stats;
     st.prefetch_keys += N;
@@ -969,7 +1211,6 @@ __global__ void k_tier_init(const TierArgs t, uint32_t C, uint32_t prefill) {
   t.ring[i] = ring_entry(slot, 0);
   t.owner[i] = i < prefill ? (int32_t)i : -1;
   t.stamp[i] = 0;
-  t.filled_at[i] = 0;
   t.pref[i] = 0;
   if (i < prefill) t.where[i] = (int32_t)i;
   if (i == 0) {
@@ -980,8 +1221,11 @@ __global__ void k_tier_init(const TierArgs t, uint32_t C, uint32_t prefill) {
 }
 
 // Drops dead entries: live entries move, in order, to `dst` (single block).
+// With `restamp`, every live entry and its slot's stamp restart at clock 0
+// (each slot has exactly one live entry, so order and liveness are kept).
 __global__ __launch_bounds__(kResolveThreads) void k_ring_compact(const TierArgs t, uint64_t* dst,
-                                                                  uint64_t dst_mask) {
+                                                                  uint64_t dst_mask,
+                                                                  uint32_t restamp) {
   __shared__ unsigned long long s_out;
   if (threadIdx.x == 0) s_out = 0;
   __syncthreads();
@@ -993,7 +1237,10 @@ __global__ __launch_bounds__(kResolveThreads) void k_ring_compact(const TierArgs
     const bool live = in && t.stamp[(uint32_t)(e >> 32)] == (uint32_t)e;
     uint32_t n;
     const uint32_t rank = block_count(live, &n);
-    if (live) dst[(s_out + rank) & dst_mask] = e;
+    if (live) {
+      dst[(s_out + rank) & dst_mask] = restamp ? ring_entry((uint32_t)(e >> 32), 0u) : e;
+      if (restamp) t.stamp[(uint32_t)(e >> 32)] = 0;
+    }
     __syncthreads();
     if (threadIdx.x == 0) s_out += n;
     __syncthreads();
@@ -1002,6 +1249,16 @@ __global__ __launch_bounds__(kResolveThreads) void k_ring_compact(const TierArgs
     t.ctl->tail = 0;
     t.ctl->head = s_out;
   }
+}
+
+// Residency of phrase rows: the HBM cache slot of each row (tiered tables),
+// -1 where the row is only in host memory, -2 for ids outside [0, P).
+__global__ void k_residency(const int32_t* __restrict__ where, int64_t P,
+                            const int32_t* __restrict__ rows, int64_t n, int32_t* __restrict__ out) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  const int32_t r = rows[i];
+  out[i] = (r < 0 || (int64_t)r >= P) ? -2 : (where ? where[r] : r);
 }
 
 template <int NCH>
@@ -1028,8 +1285,9 @@ hipError_t launch_tier_init(const TierArgs& t, uint32_t C, uint32_t prefill, hip
 }
 
 hipError_t launch_ring_compact(const TierArgs& t, uint64_t* dst, uint64_t dst_mask,
-                               hipStream_t s) {
-  hipLaunchKernelGGL(k_ring_compact, dim3(1), dim3(kResolveThreads), 0, s, t, dst, dst_mask);
+                               bool restamp, hipStream_t s) {
+  hipLaunchKernelGGL(k_ring_compact, dim3(1), dim3(kResolveThreads), 0, s, t, dst, dst_mask,
+                     restamp ? 1u : 0u);
   return hipGetLastError();
 }
 
@@ -1046,8 +1304,19 @@ hipError_t launch_lookup_resolve_small(const TierArgs& t, hipStream_t s) {
   return hipGetLastError();
 }
 
+uint32_t lookup_resolve_one_block_max() { return kGroup; }
+
 hipError_t launch_resolve_lookup(const TierArgs& t, hipStream_t s) {
-  hipLaunchKernelGGL(k_resolve_lookup, dim3(1), dim3(kResolveThreads), 0, s, t, t.look.T);
+  const uint32_t T = t.look.T;
+  if (T <= (uint32_t)kGroup) {
+    hipLaunchKernelGGL(k_resolve_lookup, dim3(1), dim3(kResolveThreads), 0, s, t, T);
+    return hipGetLastError();
+  }
+  const uint32_t nblk = (T + kMarkThreads - 1) / kMarkThreads;
+  hipLaunchKernelGGL(k_res_mark, dim3(nblk), dim3(kMarkThreads), 0, s, t, T);
+  hipLaunchKernelGGL(k_res_first, dim3(nblk), dim3(kMarkThreads), 0, s, t, T);
+  hipLaunchKernelGGL(k_res_pop, dim3(1), dim3(kResolveThreads), 0, s, t, nblk);
+  hipLaunchKernelGGL(k_res_assign, dim3(nblk), dim3(kMarkThreads), 0, s, t, T);
   return hipGetLastError();
 }
 
@@ -1058,11 +1327,6 @@ hipError_t launch_prefetch_probe(const TierArgs& t, const int32_t* tail, int32_t
   return hipGetLastError();
 }
 
-hipError_t launch_resolve_prefetch(const TierArgs& t, uint32_t N, hipStream_t s) {
-  hipLaunchKernelGGL(k_resolve_prefetch, dim3(1), dim3(kResolveThreads), 0, s, t, N);
-  return hipGetLastError();
-}
-
 hipError_t launch_resolve_prefetch_scored(const TierArgs& t, uint32_t N, const float* prob,
                                          uint32_t budget, hipStream_t s) {
   hipLaunchKernelGGL(k_resolve_prefetch_scored, dim3(1), dim3(kResolveThreads), 0, s, t, N, prob,
@@ -1070,7 +1334,15 @@ hipError_t launch_resolve_prefetch_scored(const TierArgs& t, uint32_t N, const f
   return hipGetLastError();
 }
 
-uint32_t scored_prefetch_max() { return kScoredMax; }
+uint32_t scored_prefetch_budget_max() { return kScoredBudgetMax; }
+
+hipError_t launch_residency(const int32_t* where, int64_t P, const int32_t* rows, int64_t n,
+                            int32_t* out, hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  hipLaunchKernelGGL(k_residency, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, where, P,
+                     rows, n, out);
+  return hipGetLastError();
+}
 
 hipError_t launch_fill(const TierArgs& t, int dtype, int dim, uint32_t max_jobs, hipStream_t s) {
   switch (chunks_of(dtype, dim)) {

@@ -81,6 +81,7 @@ def _load():
                           ctypes.c_int),
         "tfe_get_stats": ([vp, ctypes.POINTER(tfe_stats)], ctypes.c_int),
         "tfe_reset_stats": ([vp], ctypes.c_int),
+        "tfe_residency": ([vp, vp, i64, vp, vp], ctypes.c_int),
         "tfe_last_error": ([], ctypes.c_char_p),
         "tfe_index_capacity": ([i64, ctypes.c_double], i64),
         "tfe_index_build_host": ([vp, vp, i64, i32, i32, i32, vp, i64], ctypes.c_int),
@@ -100,7 +101,8 @@ EXPORTED = ("tfe_table_load", "tfe_table_free", "tfe_lookup_inject", "tfe_lookup
             "tfe_prefetch",
             "tfe_prefetch_scored", "tfe_head_create", "tfe_head_topk", "tfe_head_free",
             "tfe_ngram_top", "tfe_ngram_release",
-            "tfe_get_stats", "tfe_reset_stats", "tfe_last_error", "tfe_index_capacity",
+            "tfe_get_stats", "tfe_reset_stats", "tfe_residency", "tfe_last_error",
+            "tfe_index_capacity",
             "tfe_index_build_host", "tfe_index_probe_host")
 
 
@@ -206,6 +208,10 @@ def tfe_get_stats(table):
 
 def tfe_reset_stats(table):
     return _check(lib.tfe_reset_stats(table))
+
+
+def tfe_residency(table, rows, n, out, stream=None):
+    return _check(lib.tfe_residency(table, addr(rows), n, addr(out), stream_handle(stream)))
 
 
 def tfe_index_capacity(n_phrases, max_load_factor=0.5):

@@ -48,3 +48,41 @@ def test_build_bytes_per_window():
 def test_host_cpu_fields():
     h = bench.host_cpu()
     assert set(h) == {"host_cpu", "host_threads"} and h["host_threads"] >= 1
+
+
+def test_hit_counts_come_from_sets_that_ran():
+    """With fewer warmup calls than rotating sets, the sets the warmup never
+    reached still hold the output buffers' sentinel fill; every count must
+    come from a set's own call (the driver's --warmup 5 with 8 sets)."""
+    n_sets, warmup, rows = 8, 5, 64
+    sentinel = 0xEE
+    hit = [[sentinel] * rows for _ in range(n_sets)]
+    truth = [(7 * k + 3) % rows for k in range(n_sets)]   # hits each set's call writes
+    calls = []
+
+    def run(k):
+        k %= n_sets
+        calls.append(k)
+        hit[k] = [1] * truth[k] + [0] * (rows - truth[k])
+
+    for k in range(warmup):
+        run(k)
+    synced = []
+    counts = bench.counts_after_run(n_sets, run, lambda: synced.append(len(calls)),
+                                    lambda k: sum(hit[k]))
+    assert counts == truth
+    assert sorted(set(calls)) == list(range(n_sets))
+    assert synced == [warmup + n_sets]          # one sync, after every set ran
+    assert all(0 <= c <= rows for c in counts)
+
+
+def test_check_line_rejects_impossible_rates():
+    good = {"config": {"hit_rate": 0.65}, "roofline": {"frac": 0.6},
+            "runs": [{"frac_of_8tbs": 0.7, "hit_rate": 0.35}]}
+    assert bench.check_line(good) is good
+    for bad in ({"config": {"hit_rate": 89.66}}, {"roofline": {"frac": 16.6}},
+                {"runs": [{"frac_of_8tbs": -0.1}]}):
+        with pytest.raises(AssertionError):
+            bench.check_line(bad)
+    # Missing fields (traffic unmeasured, no hit rate) are not an error.
+    assert bench.check_line({"roofline": {"frac": None}})

@@ -307,3 +307,36 @@ def test_vocab_boundary_ids_pack_and_match():
     assert {0, 2, 3, 4} <= set(ln.tolist())
     check_multi(table, gt, ot, tokens, 3, 61, hidden, tfe.TFE_WEIGHT_LENGTH)
     gt.close()
+
+
+def test_resident_hit_count_in_stats(w2):
+    """tfe_get_stats on a resident table: hits equals the oracle's matched
+    positions over a sequence of calls of several sizes (one launch of 16384
+    rows spreads its counts over the table's counters), calls and positions
+    count API calls, and tfe_reset_stats clears them."""
+    table, _, ot = w2
+    gt = H.GpuTable(table)
+    want_hits = want_pos = 0
+    for k, T in enumerate([64, 16384, 1, 1000]):
+        batch = synth.decode_batch(1, T, set_index=50 + k)
+        hit, _ = check(table, gt, ot, batch.tokens, batch.ctx, batch.S, batch.hidden())
+        want_hits += int(hit.sum())
+        want_pos += T
+        st = tfe.tfe_get_stats(gt.handle)
+        assert st["hits"] == want_hits and st["positions"] == want_pos and st["calls"] == k + 1
+    tfe.tfe_reset_stats(gt.handle)
+    st = tfe.tfe_get_stats(gt.handle)
+    assert st["hits"] == 0 and st["positions"] == 0 and st["calls"] == 0
+    # Multi-match calls count positions with any retained phrase.
+    batch = synth.decode_batch(1, 4096, set_index=60)
+    T = 4096
+    tok = torch.from_numpy(batch.tokens).cuda()
+    h = H.to_device(batch.hidden(), table.dtype)
+    mask = torch.zeros(T, dtype=torch.uint8, device="cuda")
+    slots = torch.zeros((T, 2), dtype=torch.int32, device="cuda")
+    out = torch.empty_like(h)
+    tfe.tfe_lookup_inject_multi(gt.handle, tok, T, batch.ctx, batch.S, h, out, mask, slots,
+                                tfe.TFE_WEIGHT_LENGTH, tfe.TFE_GATE_SIGMOID, 1.0, H.cur_stream())
+    hit, _, _ = ot.lookup(batch.tokens, batch.ctx, batch.S)
+    assert tfe.tfe_get_stats(gt.handle)["hits"] == int(hit.sum())
+    gt.close()

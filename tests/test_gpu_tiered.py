@@ -198,14 +198,12 @@ def test_tiny_cache_direct_reads_and_ring_compaction(w2_tables):
 
 @pytest.mark.parametrize("fill", FILLS)
 def test_multi_group_lookup_and_in_place(w2_tables, fill):
-    """9000 positions (resolve groups of 4096, 4096 and 808) with many
-    repeats, in place, against a cache that fits part of them: rows filled by
-    one group and referenced by a later one, victims taken across several
-    ring windows."""
-    from oracle.lru import GROUP
+    """9000 positions (the multi-block resolve: 9 blocks, the last ragged)
+    with many repeats, in place, against a cache that fits part of them:
+    rows repeated far apart within a call, victims taken across several ring
+    windows."""
     table, res, ot = w2_tables
     T = 9000
-    assert GROUP < T < 3 * GROUP
     C, pre = 4000, 1800
     tier = TieredTable(table, C, pre, fill=fill)
     model = LruModel(C, pre, table.dim * 2, fill_rereads=fill == tfe.TFE_FILL_SIDE_STREAM)

@@ -1,0 +1,302 @@
+"""Cache policy of tiered tables on calls of every length, against the
+policy model (oracle/lru.py): statistics after every call and the residency
+of every row (phrase id -> HBM cache slot, or host only), slot for slot.
+
+Calls longer than 4096 positions are resolved over many blocks; the policy
+must not depend on that: every cached row a call uses is referenced before
+any victim is chosen (a row named only at the end of a long call is never
+evicted by a miss at its start)."""
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import synth
+from oracle.lru import LruModel
+from paper_2607_07388_amd import tfe
+
+from . import harness as H
+from .test_gpu_tiered import STAT_KEYS, TieredTable, check_stats
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def w2():
+    table = synth.config2_table()
+    res = H.GpuTable(table)
+    yield table, res, H.oracle_table(table)
+    res.close()
+    H.release_pinned()
+
+
+def windows_for_rows(table, rows):
+    """Decode windows (2 history tokens + 1) whose longest match is exactly
+    the given row (-1: a window of absent tokens, no match)."""
+    w = np.full((len(rows), 3), -1, np.int32)
+    for i, r in enumerate(rows):
+        if r >= 0:
+            n = int(table.lens[r])
+            w[i, 3 - n:] = table.tokens[r, :n]
+    return w
+
+
+def residency(tier, P):
+    rows = torch.arange(P, dtype=torch.int32, device="cuda")
+    out = torch.full((P,), -9, dtype=torch.int32, device="cuda")
+    tfe.tfe_residency(tier.handle, rows, P, out, H.cur_stream())
+    torch.cuda.synchronize()
+    return out.cpu().numpy()
+
+
+def check_residency(tier, model, P):
+    got = residency(tier, P)
+    want = np.full(P, -1, np.int32)
+    for r, s in model.resident().items():
+        want[r] = s
+    bad = np.flatnonzero(got != want)
+    assert bad.size == 0, (bad[:8], got[bad[:8]], want[bad[:8]])
+
+
+def call(tier, res, table, tokens, hidden, inplace=False, stream=None):
+    """One call on the tiered table and one on the resident table; outputs
+    byte-identical; returns the matched rows."""
+    T = tokens.shape[0]
+    tok = torch.from_numpy(np.ascontiguousarray(tokens, np.int32)).cuda()
+    h1 = H.to_device(hidden, synth.BF16)
+    h2 = h1.clone()
+    o1, o2 = H.Outputs(T, 1024, synth.BF16), H.Outputs(T, 1024, synth.BF16)
+    out1 = H.run(res, tok, T, 2, 1, h1, o1, inplace=inplace)
+    out2 = h2 if inplace else o2.out
+    tfe.tfe_lookup_inject(tier.handle, tok, T, 2, 1, h2, out2, o2.hit, o2.slot, o2.len,
+                          tfe.TFE_GATE_SIGMOID, 1.0,
+                          stream.cuda_stream if stream is not None else H.cur_stream())
+    torch.cuda.synchronize()
+    assert torch.equal(o1.slot, o2.slot) and torch.equal(o1.hit, o2.hit)
+    assert torch.equal(out1.view(torch.int16), out2.view(torch.int16))
+    return o2.slot.cpu().numpy()
+
+
+@pytest.mark.parametrize("fill", [tfe.TFE_FILL_INLINE, tfe.TFE_FILL_SIDE_STREAM])
+def test_late_reference_is_not_evicted_in_a_long_call(w2, fill):
+    table, res, ot = w2
+    C = 4
+    tier = TieredTable(table, C, C, fill=fill)      # rows 0..3 cached; least recent: row 3
+    model = LruModel(C, C, 2048, fill_rereads=fill == tfe.TFE_FILL_SIDE_STREAM)
+    T = 5000
+    rows = [100] + [-1] * (T - 2) + [3]
+    tokens = windows_for_rows(table, rows)
+    hidden = synth.normal_range(11, 1, 0, T, 1024, 1.0, synth.BF16)
+    got = call(tier, res, table, tokens, hidden)
+    np.testing.assert_array_equal(got, np.array(rows, np.int32))
+    model.lookup(rows)
+    check_stats(tier, model)
+    check_residency(tier, model, table.n_phrases)
+    assert model.resident() == {0: 0, 1: 1, 3: 3, 100: 2}
+    st = tfe.tfe_get_stats(tier.handle)
+    assert st["cache_hits"] == 1 and st["cache_misses"] == 1
+    tier.close()
+
+
+@pytest.mark.parametrize("fill", [tfe.TFE_FILL_INLINE, tfe.TFE_FILL_SIDE_STREAM])
+def test_long_calls_of_every_shape_follow_the_model(w2, fill):
+    """Calls of 4097 .. 20000 positions (ragged last blocks) drawn from a few
+    hundred rows, so rows repeat within a call and across calls, cached rows
+    recur late, and the cache (300 rows) is smaller than a call's distinct
+    rows: victims, direct host reads and ring compaction all occur; one call
+    in place.  Outputs equal the resident table byte for byte and the
+    oracle's rows; stats and residency equal the model after every call."""
+    table, res, ot = w2
+    C, pre = 300, 120
+    tier = TieredTable(table, C, pre, fill=fill)
+    model = LruModel(C, pre, 2048, fill_rereads=fill == tfe.TFE_FILL_SIDE_STREAM)
+    rng = np.random.default_rng(31 + fill)
+    pool = np.concatenate([np.arange(0, 200), rng.choice(table.n_phrases, 400, replace=False)])
+    for step, T in enumerate([4097, 6000, 9000, 5121, 20000, 4097, 8191]):
+        pick = rng.zipf(1.3, T) % pool.size
+        rows = pool[pick].astype(np.int64)
+        rows[rng.random(T) < 0.2] = -1
+        tokens = windows_for_rows(table, rows)
+        hidden = synth.normal_range(12, step, 0, T, 1024, 1.0, synth.BF16)
+        got = call(tier, res, table, tokens, hidden, inplace=step == 2)
+        _, orow, _ = ot.lookup(tokens, 2, 1)
+        np.testing.assert_array_equal(got, orow)
+        np.testing.assert_array_equal(got, rows.astype(np.int32))
+        model.lookup([int(r) for r in rows])
+        check_stats(tier, model)
+        check_residency(tier, model, table.n_phrases)
+    tier.close()
+
+
+def test_prefetch_then_long_lookup_without_sync(w2):
+    """tfe_prefetch on a side stream, then at once (no synchronisation, no
+    stats read) a lookup of 200 positions on the main stream, which runs the
+    wide probe and the one-block resolve: the lookup must wait for the
+    prefetch before any of its kernels touch the shared scratch, ring or
+    residency.  A 16-row cache makes ring compaction fire along the way."""
+    table, res, ot = w2
+    C, pre, B, K, T = 16, 8, 64, 8, 200
+    tier = TieredTable(table, C, pre)
+    model = LruModel(C, pre, 2048)
+    side = torch.cuda.Stream()
+    rng = np.random.default_rng(99)
+    seqs = synth.zipf_tokens(1, 900, T * 40, 1.1).reshape(T, 40)
+    outs = []
+    for s in range(30):
+        tail = np.ascontiguousarray(seqs[:B, s + 1:s + 3])
+        cand = synth.workloads.candidates(1, B, K, seqs[:B, s + 3], step=300 + s)
+        win = np.concatenate([np.repeat(tail, K, axis=0), cand.reshape(-1, 1)], axis=1)
+        _, crow, _ = ot.lookup(win, 2, 1)
+        window = np.ascontiguousarray(seqs[:, s:s + 3])
+        hidden = synth.normal_range(13, s, 0, T, 1024, 1.0, synth.BF16)
+        tok = torch.from_numpy(window).cuda()
+        h = H.to_device(hidden, synth.BF16)
+        o = H.Outputs(T, 1024, synth.BF16)
+        tail_d, cand_d = torch.from_numpy(tail).cuda(), torch.from_numpy(cand).cuda()
+        torch.cuda.synchronize()
+        tfe.tfe_prefetch(tier.handle, tail_d, 2, cand_d, B, K, side)
+        tfe.tfe_lookup_inject(tier.handle, tok, T, 2, 1, h, o.out, o.hit, o.slot, o.len,
+                              tfe.TFE_GATE_SIGMOID, 1.0, H.cur_stream())
+        outs.append((window, hidden, o, tail_d, cand_d, tok, h))
+        model.prefetch([int(r) for r in crow])
+        _, row, _ = ot.lookup(window, 2, 1)
+        model.lookup([int(r) for r in row])
+    torch.cuda.synchronize()
+    for window, hidden, o, *_ in outs:
+        o1 = H.Outputs(T, 1024, synth.BF16)
+        H.run(res, torch.from_numpy(window).cuda(), T, 2, 1, H.to_device(hidden, synth.BF16), o1)
+        torch.cuda.synchronize()
+        assert torch.equal(o1.slot, o.slot)
+        assert torch.equal(o1.out.view(torch.int16), o.out.view(torch.int16))
+    check_stats(tier, model)
+    check_residency(tier, model, table.n_phrases)
+    tier.close()
+
+
+def test_recency_clock_restart(w2):
+    """The 32-bit recency clock restarts (stamps renormalised, order kept)
+    without changing the policy: a table whose clock starts 20 calls below
+    the wrap runs 40 calls of mixed lengths with prefetches."""
+    table, res, ot = w2
+    C, pre = 64, 32
+    os.environ["TFE_TIER_CLOCK_START"] = str(0xFFFFFFFF - 20)
+    try:
+        tier = TieredTable(table, C, pre)
+    finally:
+        del os.environ["TFE_TIER_CLOCK_START"]
+    model = LruModel(C, pre, 2048)
+    rng = np.random.default_rng(5)
+    pool = np.arange(0, 400)
+    side = torch.cuda.Stream()
+    for step in range(40):
+        T = [64, 300, 5000][step % 3]
+        rows = pool[rng.zipf(1.2, T) % pool.size].astype(np.int64)
+        tokens = windows_for_rows(table, rows)
+        hidden = synth.normal_range(14, step, 0, T, 1024, 1.0, synth.BF16)
+        call(tier, res, table, tokens, hidden)
+        model.lookup([int(r) for r in rows])
+        if step % 4 == 1:
+            cr = pool[rng.zipf(1.2, 64) % pool.size].astype(np.int64)
+            cw = windows_for_rows(table, cr)
+            # Candidate = the window's last token, tail = the two before it:
+            # the candidate's longest match is the row itself.
+            cand = torch.from_numpy(np.ascontiguousarray(cw[:, 2:3])).cuda()
+            tail = torch.from_numpy(np.ascontiguousarray(cw[:, 0:2])).cuda()
+            tfe.tfe_prefetch(tier.handle, tail, 2, cand, 64, 1, side)
+            model.prefetch([int(r) for r in cr])
+        check_stats(tier, model)
+    check_residency(tier, model, table.n_phrases)
+    tier.close()
+
+
+def test_prefetch_keeps_the_cached_rows_it_names(w2):
+    """Candidates whose rows sit in the least recent slots: the prefetch
+    references them (never its own victims) and fills the other rows into
+    the next least recent slots, after lookups through each launch shape."""
+    table, res, ot = w2
+    for pattern in [(64, 300), (64, 64), (5000, 5000)]:
+        C, pre = 64, 32
+        tier = TieredTable(table, C, pre)
+        model = LruModel(C, pre, 2048)
+        rng = np.random.default_rng(5)
+        pool = np.arange(0, 400)
+        for step, T in enumerate(pattern):
+            rows = pool[rng.zipf(1.2, T) % pool.size].astype(np.int64)
+            call(tier, res, table, windows_for_rows(table, rows),
+                 synth.normal_range(14, step, 0, T, 1024, 1.0, synth.BF16))
+            model.lookup([int(r) for r in rows])
+        cr = pool[rng.zipf(1.2, 64) % pool.size].astype(np.int64)
+        cw = windows_for_rows(table, cr)
+        cand = torch.from_numpy(np.ascontiguousarray(cw[:, 2:3])).cuda()
+        tail = torch.from_numpy(np.ascontiguousarray(cw[:, 0:2])).cuda()
+        tfe.tfe_prefetch(tier.handle, tail, 2, cand, 64, 1, torch.cuda.Stream())
+        model.prefetch([int(r) for r in cr])
+        check_stats(tier, model)
+        check_residency(tier, model, table.n_phrases)
+        tier.close()
+
+
+def test_residency_of_resident_table_and_bad_ids(w2):
+    table, res, ot = w2
+    rows = torch.tensor([0, 5, table.n_phrases - 1, -1, table.n_phrases, 1 << 30],
+                        dtype=torch.int32, device="cuda")
+    out = torch.full((6,), -9, dtype=torch.int32, device="cuda")
+    tfe.tfe_residency(res.handle, rows, 6, out, H.cur_stream())
+    torch.cuda.synchronize()
+    assert out.cpu().tolist() == [0, 5, table.n_phrases - 1, -2, -2, -2]
+    tfe.tfe_residency(res.handle, rows, 0, out, H.cur_stream())  # empty query
+    with pytest.raises(tfe.TfeError):
+        tfe.tfe_residency(res.handle, rows, -1, out, H.cur_stream())
+
+
+@pytest.mark.parametrize("budget", [64, 1024])
+def test_head_topk_feeds_scored_prefetch_at_batch64_k128(w2, budget):
+    """The early-exit head's top 128 of a 151936-token vocabulary for 64 rows
+    (Eq. 13, Eq. 14) goes straight into tfe_prefetch_scored (Eq. 17): 8192
+    candidates per call, more candidate rows than the budget (the threshold
+    is found by radix select), cached candidates referenced.  Alternate steps
+    run the plain prefetch of the same 8192 candidates (the multi-block
+    resolve).  Statistics and residency equal the model after every call;
+    outputs equal the resident table."""
+    table, res, ot = w2
+    V, Dh, B, K, steps = synth.V, 1024, 64, 128, 6
+    C, pre = 8192, 4096
+    w = torch.empty((V, Dh), dtype=torch.bfloat16, device="cuda")
+    synth.normal_fill_device(w.data_ptr(), 0, V, Dh, 3, 40, 0.1, synth.BF16, H.cur_stream())
+    torch.cuda.synchronize()
+    head = tfe.tfe_head_create(w, V, Dh, B, K)
+    tier = TieredTable(table, C, pre)
+    model = LruModel(C, pre, 2048)
+    seqs = synth.zipf_tokens(1, 1200 + budget, B * (steps + 3), 1.1).reshape(B, steps + 3)
+    side = torch.cuda.Stream()
+    for s in range(steps):
+        window = np.ascontiguousarray(seqs[:, s:s + 3])
+        hidden = synth.normal_range(15, s, 0, B, 1024, 1.0, synth.BF16)
+        rows = call(tier, res, table, window, hidden)
+        model.lookup([int(r) for r in rows])
+        hd = H.to_device(synth.normal_range(16, s, 0, B, Dh, 1.0, synth.BF16), synth.BF16)
+        ids = torch.full((B, K), -7, dtype=torch.int32, device="cuda")
+        prob = torch.full((B, K), -1.0, dtype=torch.float32, device="cuda")
+        tfe.tfe_head_topk(head, hd, B, K, ids, prob, H.cur_stream())
+        torch.cuda.synchronize()
+        tail = np.ascontiguousarray(seqs[:, s + 1:s + 3])
+        ids_h, prob_h = ids.cpu().numpy(), prob.cpu().numpy()
+        win = np.concatenate([np.repeat(tail, K, axis=0), ids_h.reshape(-1, 1)], axis=1)
+        _, crow, clen = ot.lookup(win, 2, 1)
+        tail_d = torch.from_numpy(tail).cuda()
+        if s % 2 == 0:
+            tfe.tfe_prefetch_scored(tier.handle, tail_d, 2, ids, prob, B, K, budget, side)
+            model.prefetch_scored([int(r) for r in crow], [int(x) for x in clen],
+                                  prob_h.ravel(), budget)
+        else:
+            tfe.tfe_prefetch(tier.handle, tail_d, 2, ids, B, K, side)
+            model.prefetch([int(r) for r in crow])
+        check_stats(tier, model)
+        check_residency(tier, model, table.n_phrases)
+    st = tfe.tfe_get_stats(tier.handle)
+    assert st["prefetch_filled"] > 0
+    if budget == 64:
+        assert st["prefetch_dropped"] > 0
+    tier.close()
+    tfe.tfe_head_free(head)
