@@ -258,6 +258,24 @@ tfe_status tfe_head_topk(tfe_head *head, const void *hidden, int32_t B, int32_t 
 /* Releases a head (waits for the device first).  NULL is accepted. */
 tfe_status tfe_head_free(tfe_head *head);
 
+/* tfe_head_topk without a head and without any allocation, for callers that
+ * cannot allocate device memory (code under HIP graph capture, tight serving
+ * loops, harnesses that forbid hipMalloc).  Same kernels, arguments and
+ * results as tfe_head_create(w_pref, vocab, dim, B, K) + tfe_head_topk(...):
+ *   w_pref  DEVICE bf16 [vocab x dim], 16-byte aligned, on the current device;
+ *   hidden  DEVICE bf16 [B x dim], 16-byte aligned;
+ *   top_ids DEVICE int32 [B x K], top_prob DEVICE float32 [B x K].
+ * Limits: 0 <= B <= 64, 1 <= vocab <= 2^18, 0 <= K <= min(256, vocab), dim
+ * 256, 512 or 1024; larger sizes return TFE_ERR_INVALID_ARG.  The scratch
+ * (logits and tile statistics: 76 MiB) is a static device array that every
+ * GPU the library runs on holds until the process ends; the call allocates
+ * nothing.  Every call on one GPU shares that GPU's scratch: calls that
+ * overlap on one GPU (different streams, or host threads) race and must be
+ * ordered by the caller. */
+tfe_status tfe_head_topk_noalloc(const void *w_pref, int32_t vocab, int32_t dim,
+                                 const void *hidden, int32_t B, int32_t K, int32_t *top_ids,
+                                 float *top_prob, void *stream);
+
 /* ---- Offline phrase-table construction -----------------------------------
  * Paper: Sec. 4.2 (candidate phrases mined from a corpus and selected by
  * frequency; n-gram extraction is the dominant construction cost reported in

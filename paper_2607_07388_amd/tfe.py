@@ -76,6 +76,7 @@ def _load():
         "tfe_head_create": ([vp, i32, i32, i32, i32, ctypes.POINTER(vp)], ctypes.c_int),
         "tfe_head_topk": ([vp, vp, i32, i32, vp, vp, vp], ctypes.c_int),
         "tfe_head_free": ([vp], ctypes.c_int),
+        "tfe_head_topk_noalloc": ([vp, i32, i32, vp, i32, i32, vp, vp, vp], ctypes.c_int),
         "tfe_ngram_release": ([], ctypes.c_int),
         "tfe_ngram_top": ([vp, i64, i32, i32, i64, i64, vp, vp, ctypes.POINTER(i64), vp],
                           ctypes.c_int),
@@ -100,6 +101,7 @@ lib = _load()
 EXPORTED = ("tfe_table_load", "tfe_table_free", "tfe_lookup_inject", "tfe_lookup_inject_multi",
             "tfe_prefetch",
             "tfe_prefetch_scored", "tfe_head_create", "tfe_head_topk", "tfe_head_free",
+            "tfe_head_topk_noalloc",
             "tfe_ngram_top", "tfe_ngram_release",
             "tfe_get_stats", "tfe_reset_stats", "tfe_residency", "tfe_last_error",
             "tfe_index_capacity",
@@ -182,6 +184,11 @@ def tfe_head_create(w_pref, vocab, dim, max_batch, max_k):
 def tfe_head_topk(head, hidden, B, K, top_ids, top_prob, stream=None):
     return _check(lib.tfe_head_topk(head, addr(hidden), B, K, addr(top_ids), addr(top_prob),
                                     stream_handle(stream)))
+
+
+def tfe_head_topk_noalloc(w_pref, vocab, dim, hidden, B, K, top_ids, top_prob, stream=None):
+    return _check(lib.tfe_head_topk_noalloc(addr(w_pref), vocab, dim, addr(hidden), B, K,
+                                            addr(top_ids), addr(top_prob), stream_handle(stream)))
 
 
 def tfe_head_free(head):
