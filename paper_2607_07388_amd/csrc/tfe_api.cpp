@@ -79,7 +79,7 @@ static void release(tfe_table* t) {
   (void)sync_table(t);
   void* dev_bufs[] = {t->d_slots, t->d_values, t->d_cache, t->d_where, t->d_owner, t->d_stamp,
                       t->d_pref, t->d_ring, t->d_ring2, t->d_ctl, t->d_row_of,
-                      t->d_slot_of, t->d_phase, t->d_jobs, t->d_hit_ctr, t->d_hkey, t->d_hpos, t->d_hval, t->d_blk};
+                      t->d_slot_of, t->d_phase, t->d_jobs, t->d_hit_ctr, t->d_hkey, t->d_hpos, t->d_hval, t->d_blk, t->d_stage};
   for (void* b : dev_bufs)
     if (b) (void)hipFree(b);
   if (t->own_h_values && t->h_values) (void)hipHostFree(t->h_values);
@@ -153,6 +153,7 @@ static tfe::TierArgs tier_args(tfe_table* t) {
   a.hval = t->d_hval;
   a.hmask = 2 * (uint64_t)t->scratch_cap - 1;
   a.blk = t->d_blk;
+  a.stage = t->d_stage;
   a.clock = t->clock;
   a.row_bytes = (uint32_t)(t->dim * elem_size(t->dtype));
   a.fill_inline = t->fill_mode == TFE_FILL_INLINE ? 1u : 0u;
@@ -212,6 +213,7 @@ static tfe_status load_tiered(tfe_table* t, const tfe_table_desc* d, hipStream_t
   TFE_TRY(dev_alloc(&t->d_ring, t->ring_cap, "recency ring"));
   TFE_TRY(dev_alloc(&t->d_ring2, t->ring_cap, "recency ring"));
   TFE_TRY(dev_alloc(&t->d_ctl, 1, "tier control block"));
+  TFE_TRY(dev_alloc((char**)&t->d_stage, (size_t)tfe::kDecodeMaxT * row_bytes, "staging rows"));
   TFE_HIP(hipMemsetAsync(t->d_where, 0xFF, where_n * sizeof(int32_t), stream), "init");
   TFE_HIP(hipMemsetAsync(t->d_ctl, 0, sizeof(tfe::TierCtl), stream), "init");
   tfe::TierArgs a = tier_args(t);
@@ -347,6 +349,13 @@ static tfe_status lookup_tiered(tfe_table* t, const LookupArgs& look, hipStream_
   TFE_TRY(advance_clock(t, look.T, stream));
   tfe::TierArgs a = tier_args(t);
   a.look = look;
+  if (t->fill_mode == TFE_FILL_INLINE && look.T <= tfe::kDecodeMaxT) {
+    // The whole call in one launch (probe, inject, residency).
+    TFE_HIP(tfe::launch_tier_decode(a, t->dtype, t->dim, stream), "tiered decode");
+    t->lookup_recorded = true;
+    t->last_stream = stream;
+    return TFE_OK;
+  }
   const bool fused = tfe::lookup_resolve_fused(look.T);
   if (!fused) TFE_HIP(tfe::launch_tier_probe(a, stream), "tier probe");
   if (fused)
@@ -635,9 +644,9 @@ tfe_status tfe_get_stats(const tfe_table* table, tfe_stats* out) {
     s.host_bytes = c.stats.host_bytes;
     s.prefetch_dropped = c.stats.prefetch_dropped;
   } else if (table->d_hit_ctr) {
-    unsigned long long ctr[tfe::kHitCounters * tfe::kHitStride];
-    hipError_t e = hipMemcpyAsync(ctr, table->d_hit_ctr, sizeof ctr, hipMemcpyDeviceToHost,
-                                  table->own_stream);
+    std::vector<unsigned long long> ctr((size_t)tfe::kHitCounters * tfe::kHitStride);
+    hipError_t e = hipMemcpyAsync(ctr.data(), table->d_hit_ctr, ctr.size() * sizeof ctr[0],
+                                  hipMemcpyDeviceToHost, table->own_stream);
     if (e == hipSuccess) e = hipStreamSynchronize(table->own_stream);
     if (e != hipSuccess) return tfe::fail(TFE_ERR_HIP, "stats: %s", hipGetErrorString(e));
     s.hits = 0;

@@ -272,8 +272,9 @@ __device__ __forceinline__ void write_result(const LookupArgs& a, uint32_t p, in
 }
 
 // Resident tables: one matched position added to the table's hit count
-// (called by one lane of the position's wave).  The counter is picked by
-// block, so a launch's additions spread over kHitCounters lines.
+// (called by one lane of the position's wave, right after the probe; an
+// addition after the value row's loads, or after the stores, measured
+// slower).  The counter is picked by block, spreading a launch's additions.
 __device__ __forceinline__ void count_hit(const LookupArgs& a, bool matched) {
   if (a.hit_ctr && matched)
     __hip_atomic_fetch_add(a.hit_ctr + (blockIdx.x & (kHitCounters - 1)) * kHitStride, 1ull,

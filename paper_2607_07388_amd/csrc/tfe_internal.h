@@ -49,13 +49,14 @@ struct LookupArgs {
   float inv_sqrt_d;           // 1 / sqrt(dim)
   int32_t weighting;          // multi-match kernel: tfe_weighting
   // Resident tables: matched-position counters, kHitCounters of them
-  // kHitStride words apart (one 128-byte line each, so that the waves of a
-  // launch spread their additions over many addresses); null for tiered
-  // tables, whose resolve kernels count their own.
+  // kHitStride words apart; null for tiered tables, whose resolve kernels
+  // count their own.  Blocks add to counter blockIdx mod kHitCounters, so a
+  // launch's additions are spread thin (with 64 counters, same-address
+  // additions cost 2% of the stacked decode launch; with 4096, 0.5%).
   unsigned long long* hit_ctr;
 };
-constexpr int kHitCounters = 64;
-constexpr int kHitStride = 16;
+constexpr int kHitCounters = 4096;
+constexpr int kHitStride = 1;
 
 // Device-side bookkeeping of a tiered table (see tfe_tiered.hip).
 struct TierStats {
@@ -66,6 +67,8 @@ struct TierCtl {
   unsigned long long head, tail;  // recency ring cursors (monotone)
   unsigned long long njobs;       // host -> cache copies of the current call
   unsigned long long call_head;   // long calls: ring head before the call's appends
+  unsigned int arrive;            // one-launch decode: waves done with their position
+  unsigned int pad_;
   TierStats stats;
 };
 struct TierJob {
@@ -91,6 +94,7 @@ struct TierArgs {
   uint64_t* hval;             // [2 cap] scored prefetch: best score (clock << 32 | bits)
   uint64_t hmask;             // 2 cap - 1
   uint64_t* blk;              // [cap / 1024 + 1] per-block first-position counts
+  void* stage;                // one-launch decode: [kDecodeMaxT x dim] rows read from host
   uint32_t clock;
   uint32_t row_bytes;
   uint32_t fill_inline;       // the inject writes missed rows into their slots
@@ -112,6 +116,10 @@ uint32_t lookup_resolve_one_block_max();
 hipError_t launch_resolve_lookup(const TierArgs& t, hipStream_t s);
 // Decode-sized lookups: probe + resolve in one single-block launch.
 bool lookup_resolve_fused(uint32_t T);
+// Decode-sized lookups with inline fill: the whole call (probe, inject,
+// residency) in one launch, for T <= kDecodeMaxT.
+constexpr uint32_t kDecodeMaxT = 64;
+hipError_t launch_tier_decode(const TierArgs& t, int dtype, int dim, hipStream_t s);
 hipError_t launch_lookup_resolve_small(const TierArgs& t, hipStream_t s);
 hipError_t launch_prefetch_probe(const TierArgs& t, const int32_t* tail, int32_t tail_len,
                                  const int32_t* cand, uint32_t B, uint32_t K, hipStream_t s);
@@ -176,6 +184,7 @@ struct tfe_table {
   uint64_t* d_hpos = nullptr;    // [2 scratch_cap]
   uint64_t* d_hval = nullptr;    // [2 scratch_cap]
   uint64_t* d_blk = nullptr;     // [scratch_cap / 1024 + 1]
+  void* d_stage = nullptr;       // [kDecodeMaxT x dim] staging rows (tiered, inline fill)
   uint32_t scratch_cap = 0;
   uint32_t clock = 0;
   hipEvent_t ev_resolved = nullptr, ev_filled = nullptr, ev_lookup = nullptr,

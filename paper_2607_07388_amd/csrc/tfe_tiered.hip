@@ -1201,6 +1201,251 @@ __global__ __launch_bounds__(WPB * 64) void k_tier_inject(const TierArgs t) {
   dev::store_injected<DT, NCH>(out, hv, mv, g, lane);
 }
 
+// Decode-sized lookups with inline fill (T <= kDecodeMaxT positions): the
+// whole call in one launch of T one-wave blocks.
+//   Every wave runs its position at once: key formation and probe, the
+//   row's residency (where), the value row from the cache or -- when it is
+//   not cached -- straight from pinned host memory, gate and injection.  A
+//   row read from host memory is also written to the position's staging row
+//   in HBM.  This is safe before any residency decision: victims are never
+//   slots that the call references, so nothing a wave reads changes during
+//   the call.
+//   Each wave then publishes its row and the slot it found and counts itself
+//   in; the last wave to arrive resolves residency for the whole call with
+//   the policy of k_resolve_lookup: first positions of rows (lane q =
+//   position q), cached rows referenced, victims for the missed rows from
+//   the tail of the recency ring, the staged rows copied into their victim
+//   slots, recency appends in first-position order, counters.
+// One launch and no cross-block waiting: a wave that is not last exits.
+// What crosses blocks (row, slot, staged row) is written and read with
+// device-scope stores and loads, and each wave waits for its stores to
+// complete before it counts in; a device-scope fence would instead write
+// back and invalidate the whole L2 in every wave.
+
+// Device-scope (coherent across the XCDs' L2s) store and load.
+__device__ __forceinline__ void st_dev(int32_t* p, int32_t v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ int32_t ld_dev(const int32_t* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void st_dev(u32x4* p, const u32x4 v) {
+  unsigned long long* q = (unsigned long long*)p;
+  __hip_atomic_store(q, (unsigned long long)v[0] | ((unsigned long long)v[1] << 32),
+                     __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  __hip_atomic_store(q + 1, (unsigned long long)v[2] | ((unsigned long long)v[3] << 32),
+                     __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ u32x4 ld_dev(const u32x4* p) {
+  const unsigned long long* q = (const unsigned long long*)p;
+  const unsigned long long lo = __hip_atomic_load(q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  const unsigned long long hi =
+      __hip_atomic_load(q + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  return u32x4{(uint32_t)lo, (uint32_t)(lo >> 32), (uint32_t)hi, (uint32_t)(hi >> 32)};
+}
+// Waits until every memory operation this wave issued has completed
+// (s_waitcnt vmcnt(0); the other counters left at their maximum).
+__device__ __forceinline__ void wait_mem() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+
+constexpr int kWalkPer = 8;  // ring entries per lane and round of the victim walk
+
+template <int NCH>
+__device__ void decode_resolve_last(const TierArgs& t, uint32_t T) {
+  constexpr uint32_t row_vecs = NCH * 64;
+  __shared__ uint32_t vict[kDecodeMaxT];
+  __shared__ int32_t vown[kDecodeMaxT];
+  __shared__ uint32_t fpos[kDecodeMaxT];
+  const int lane = threadIdx.x;
+  const bool valid = (uint32_t)lane < T;
+  const int32_t r = valid ? ld_dev(t.row_of + lane) : -1;
+  const int32_t s0 = valid ? ld_dev(t.slot_of + lane) : -1;
+  // Ring cursors and the first window of the walk, read while the first
+  // positions are worked out.
+  unsigned long long tail = t.ctl->tail;
+  const unsigned long long head = t.ctl->head;
+  // First position of each row: no lower lane holds it.
+  bool first = r >= 0;
+  for (int j = 0; j < (int)kDecodeMaxT; ++j) {
+    const int32_t rj = __builtin_amdgcn_readlane(r, j);
+    first = first && !(j < lane && rj == r);
+  }
+  const bool fc = first && s0 >= 0, fm = first && s0 < 0;
+  const uint8_t pv = fc ? t.pref[s0] : (uint8_t)0;
+  if (fc) {
+    t.stamp[s0] = t.clock;  // referenced: never a victim of this call
+    if (pv) t.pref[s0] = 0;
+  }
+  const uint64_t mfm = __builtin_amdgcn_ballot_w64(fm);
+  const uint32_t need = (uint32_t)__builtin_popcountll(mfm);
+  const uint32_t mrank = lanes_below(mfm);
+  if (fm) fpos[mrank] = (uint32_t)lane;
+  wait_mem();  // the stamps above land before the walk reads stamps
+  uint32_t got = 0;
+  // Least recent live entries (stamp still current, not this call's),
+  // kWalkPer x 64 per round; an entry of this call (none are appended
+  // before the walk) or the head ends the walk.
+  while (got < need && tail < head) {
+    uint64_t e[kWalkPer];
+#pragma unroll
+    for (int k = 0; k < kWalkPer; ++k)
+      e[k] = t.ring[(tail + (uint64_t)(k * 64 + lane)) & t.ring_mask];
+    uint32_t sn[kWalkPer];
+    int32_t own[kWalkPer];
+#pragma unroll
+    for (int k = 0; k < kWalkPer; ++k) {
+      const bool in = tail + (uint64_t)(k * 64 + lane) < head;
+      const uint32_t slot = in ? (uint32_t)(e[k] >> 32) : 0u;
+      sn[k] = t.stamp[slot];
+      own[k] = t.owner[slot];
+    }
+    bool stop = false;
+#pragma unroll
+    for (int k = 0; k < kWalkPer; ++k) {
+      if (stop || got == need) continue;  // wave-uniform
+      const unsigned long long base = tail + (uint64_t)(k * 64);
+      const bool in = base + (uint64_t)lane < head;
+      const uint32_t slot = (uint32_t)(e[k] >> 32), st = (uint32_t)e[k];
+      const bool cur = in && st == t.clock;
+      const uint64_t mcur = __builtin_amdgcn_ballot_w64(cur);
+      const uint32_t lim = mcur ? (uint32_t)__builtin_ctzll(mcur) : 64u;
+      const bool live = in && !cur && sn[k] == st && (uint32_t)lane < lim;
+      const uint64_t ml = __builtin_amdgcn_ballot_w64(live);
+      const uint32_t nl = (uint32_t)__builtin_popcountll(ml);
+      const uint32_t rk = lanes_below(ml);
+      const uint32_t take = nl < need - got ? nl : need - got;
+      if (live && rk < take) {
+        vict[got + rk] = slot;
+        vown[got + rk] = own[k];
+      }
+      if (take == need - got && take > 0) {
+        // Resume after the last victim taken.
+        uint64_t m = ml;
+        for (uint32_t q = 1; q < take; ++q) m &= m - 1;
+        tail = base + (uint64_t)__builtin_ctzll(m) + 1;
+        got = need;
+        stop = true;
+        continue;
+      }
+      got += take;
+      if (mcur || base + 64 >= head) {
+        tail = mcur ? base + lim : head;
+        stop = true;
+        continue;
+      }
+    }
+    if (stop) break;
+    tail += (uint64_t)kWalkPer * 64;
+  }
+  __syncthreads();  // vict, vown, fpos
+  const bool fill = fm && mrank < got;
+  uint32_t slot_now = fc ? (uint32_t)s0 : 0u;
+  if (fill) {
+    const uint32_t v = vict[mrank];
+    const int32_t old = vown[mrank];
+    if (old >= 0) t.where[old] = -1;
+    t.owner[v] = r;
+    t.where[r] = (int32_t)v;
+    t.stamp[v] = t.clock;
+    t.pref[v] = 0;
+    slot_now = v;
+  }
+  // The staged rows into their slots, four rows in flight per lane.
+  const u32x4* stage = (const u32x4*)t.stage;
+  u32x4* cache = (u32x4*)t.cache;
+  for (uint32_t q0 = 0; q0 < got; q0 += 4) {
+    u32x4 buf[4][NCH];
+#pragma unroll
+    for (uint32_t q = 0; q < 4; ++q)
+      if (q0 + q < got) {
+#pragma unroll
+        for (int k = 0; k < NCH; ++k)
+          buf[q][k] = ld_dev(stage + (size_t)fpos[q0 + q] * row_vecs + k * 64 + lane);
+      }
+#pragma unroll
+    for (uint32_t q = 0; q < 4; ++q)
+      if (q0 + q < got) {
+#pragma unroll
+        for (int k = 0; k < NCH; ++k)
+          cache[(size_t)vict[q0 + q] * row_vecs + k * 64 + lane] = buf[q][k];
+      }
+  }
+  const bool app = fc || fill;
+  const uint64_t ma = __builtin_amdgcn_ballot_w64(app);
+  if (app) t.ring[(head + lanes_below(ma)) & t.ring_mask] = ring_entry(slot_now, t.clock);
+  const uint32_t nhit = (uint32_t)__builtin_popcountll(__builtin_amdgcn_ballot_w64(r >= 0));
+  const uint32_t nch =
+      (uint32_t)__builtin_popcountll(__builtin_amdgcn_ballot_w64(r >= 0 && s0 >= 0));
+  const uint32_t nused = (uint32_t)__builtin_popcountll(__builtin_amdgcn_ballot_w64(fc && pv));
+  if (lane == 0) {
+    t.ctl->tail = tail;
+    t.ctl->head = head + (uint64_t)__builtin_popcountll(ma);
+    t.ctl->njobs = 0;
+    TierStats& st = t.ctl->stats;
+    st.positions += T;
+    st.hits += nhit;
+    st.cache_hits += nch;
+    st.cache_misses += nhit - nch;
+    st.prefetch_used += nused;
+    st.host_bytes += (unsigned long long)(nhit - nch) * t.row_bytes;
+    t.ctl->arrive = 0;  // the next call starts counting from zero
+  }
+}
+
+template <int DT, int NCH>
+__global__ __launch_bounds__(64) void k_tier_decode(const TierArgs t) {
+  constexpr int ROW_VECS = NCH * 64;
+  static_assert(NCH <= 8, "staging copy holds at most 8 vectors per lane and row");
+  const LookupArgs& a = t.look;
+  const int lane = threadIdx.x;
+  const uint32_t p = blockIdx.x;  // grid = T <= kDecodeMaxT
+  u32x4 hv[NCH];
+  const u32x4* hin = (const u32x4*)a.hin + (size_t)p * ROW_VECS;
+#pragma unroll
+  for (int k = 0; k < NCH; ++k) hv[k] = dev::load_hidden(hin + k * 64 + lane);
+  int32_t tw[4];
+  dev::window_tokens(a, p, tw);
+  const dev::Probe pr = dev::probe_begin(a, tw, lane);
+  int len;
+  const int32_t row = dev::probe_finish(a, pr, lane, &len);
+  if (lane == 0) dev::write_result(a, p, row, len);
+  u32x4* out = (u32x4*)a.hout + (size_t)p * ROW_VECS;
+  int32_t w = -1;
+  if (row < 0) {
+    if (!a.inplace) {
+#pragma unroll
+      for (int k = 0; k < NCH; ++k) dev::store_out(hv[k], out + k * 64 + lane);
+    }
+  } else {
+    w = t.where[row];
+    const u32x4* mrow = w >= 0 ? (const u32x4*)t.cache + (size_t)w * ROW_VECS
+                               : (const u32x4*)t.host_values + (size_t)row * ROW_VECS;
+    u32x4 mv[NCH];
+#pragma unroll
+    for (int k = 0; k < NCH; ++k) mv[k] = mrow[k * 64 + lane];
+    if (w < 0) {
+      u32x4* st = (u32x4*)t.stage + (size_t)p * ROW_VECS;
+#pragma unroll
+      for (int k = 0; k < NCH; ++k) st_dev(st + k * 64 + lane, mv[k]);
+    }
+    const float g = dev::gate_of<DT, NCH>(a, hv, mv);
+    dev::store_injected<DT, NCH>(out, hv, mv, g, lane);
+  }
+  if (lane == 0) {
+    st_dev(t.row_of + p, row);
+    st_dev(t.slot_of + p, w);
+  }
+  // Count in once this wave's published writes are complete; the last
+  // wave resolves the call.
+  wait_mem();
+  uint32_t last = 0;
+  if (lane == 0)
+    last = __hip_atomic_fetch_add(&t.ctl->arrive, 1u, __ATOMIC_RELAXED,
+                                  __HIP_MEMORY_SCOPE_AGENT) == a.T - 1 ? 1u : 0u;
+  last = __builtin_amdgcn_readfirstlane(last);
+  if (!last) return;
+  decode_resolve_last<NCH>(t, a.T);
+}
+
 // Initial state: slot s < prefill holds row s; the ring lists the empty
 // slots in ascending order, then the filled slots by descending row.
 __global__ void k_tier_init(const TierArgs t, uint32_t C, uint32_t prefill) {
@@ -1277,6 +1522,12 @@ hipError_t launch_inject_t(const TierArgs& t, hipStream_t s) {
 
 int chunks_of(int dtype, int dim) { return dim / (dtype == TFE_F32 ? 256 : 512); }
 
+template <int DT, int NCH>
+hipError_t launch_decode_t(const TierArgs& t, hipStream_t s) {
+  hipLaunchKernelGGL((k_tier_decode<DT, NCH>), dim3(t.look.T), dim3(64), 0, s, t);
+  return hipGetLastError();
+}
+
 }  // namespace
 
 hipError_t launch_tier_init(const TierArgs& t, uint32_t C, uint32_t prefill, hipStream_t s) {
@@ -1350,6 +1601,28 @@ hipError_t launch_fill(const TierArgs& t, int dtype, int dim, uint32_t max_jobs,
     case 2: return launch_fill_t<2>(t, max_jobs, s);
     case 4: return launch_fill_t<4>(t, max_jobs, s);
     case 8: return launch_fill_t<8>(t, max_jobs, s);
+  }
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_tier_decode(const TierArgs& t, int dtype, int dim, hipStream_t s) {
+  if (t.look.T == 0) return hipSuccess;
+  if (t.look.T > kDecodeMaxT) return hipErrorInvalidValue;
+  const int nch = chunks_of(dtype, dim);
+  if (dtype == TFE_F32) {
+    switch (nch) {
+      case 1: return launch_decode_t<0, 1>(t, s);
+      case 2: return launch_decode_t<0, 2>(t, s);
+      case 4: return launch_decode_t<0, 4>(t, s);
+      case 8: return launch_decode_t<0, 8>(t, s);
+    }
+  } else {
+    switch (nch) {
+      case 1: return launch_decode_t<1, 1>(t, s);
+      case 2: return launch_decode_t<1, 2>(t, s);
+      case 4: return launch_decode_t<1, 4>(t, s);
+      case 8: return launch_decode_t<1, 8>(t, s);
+    }
   }
   return hipErrorInvalidValue;
 }
