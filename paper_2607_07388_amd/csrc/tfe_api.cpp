@@ -79,7 +79,7 @@ static void release(tfe_table* t) {
   (void)sync_table(t);
   void* dev_bufs[] = {t->d_slots, t->d_values, t->d_cache, t->d_where, t->d_owner, t->d_stamp,
                       t->d_pref, t->d_ring, t->d_ring2, t->d_ctl, t->d_row_of,
-                      t->d_slot_of, t->d_phase, t->d_jobs, t->d_hit_ctr, t->d_hkey, t->d_hpos, t->d_hval, t->d_blk, t->d_stage};
+                      t->d_slot_of, t->d_phase, t->d_jobs, t->d_hit_ctr, t->d_hkey, t->d_hpos, t->d_hval, t->d_blk, t->d_spare};
   for (void* b : dev_bufs)
     if (b) (void)hipFree(b);
   if (t->own_h_values && t->h_values) (void)hipHostFree(t->h_values);
@@ -153,7 +153,7 @@ static tfe::TierArgs tier_args(tfe_table* t) {
   a.hval = t->d_hval;
   a.hmask = 2 * (uint64_t)t->scratch_cap - 1;
   a.blk = t->d_blk;
-  a.stage = t->d_stage;
+  a.spare = t->d_spare;
   a.clock = t->clock;
   a.row_bytes = (uint32_t)(t->dim * elem_size(t->dtype));
   a.fill_inline = t->fill_mode == TFE_FILL_INLINE ? 1u : 0u;
@@ -202,18 +202,23 @@ static tfe_status load_tiered(tfe_table* t, const tfe_table_desc* d, hipStream_t
     TFE_HIP(hipHostGetDevicePointer(&dp, t->h_values, 0), "hipHostGetDevicePointer");
     t->h_values_dev = dp;
   }
-  TFE_TRY(dev_alloc((char**)&t->d_cache, (size_t)C * row_bytes, "HBM cache"));
+  // Physical cache slots: C rows of the cache plus kDecodeMaxT spare slots
+  // that the one-launch decode writes missed rows into and swaps with its
+  // victims (never in the recency order, never mapped by a row).
+  const size_t slots = (size_t)C + tfe::kDecodeMaxT;
+  TFE_TRY(dev_alloc((char**)&t->d_cache, slots * row_bytes, "HBM cache"));
   // At least one entry: the resolve kernels read entry 0 unconditionally.
   const size_t where_n = P > 0 ? (size_t)P : 1;
   TFE_TRY(dev_alloc(&t->d_where, where_n, "residency map"));
-  TFE_TRY(dev_alloc(&t->d_owner, (size_t)C, "slot owners"));
-  TFE_TRY(dev_alloc(&t->d_stamp, (size_t)C, "slot stamps"));
-  TFE_TRY(dev_alloc(&t->d_pref, (size_t)C, "prefetch flags"));
+  TFE_TRY(dev_alloc(&t->d_owner, slots, "slot owners"));
+  TFE_TRY(dev_alloc(&t->d_stamp, slots, "slot stamps"));
+  TFE_TRY(dev_alloc(&t->d_pref, slots, "prefetch flags"));
+  TFE_TRY(dev_alloc(&t->d_spare, (size_t)tfe::kDecodeMaxT, "spare slots"));
   t->ring_cap = pow2_at_least((uint64_t)C * 4 < 4096 ? 4096 : (uint64_t)C * 4);
   TFE_TRY(dev_alloc(&t->d_ring, t->ring_cap, "recency ring"));
   TFE_TRY(dev_alloc(&t->d_ring2, t->ring_cap, "recency ring"));
   TFE_TRY(dev_alloc(&t->d_ctl, 1, "tier control block"));
-  TFE_TRY(dev_alloc((char**)&t->d_stage, (size_t)tfe::kDecodeMaxT * row_bytes, "staging rows"));
+
   TFE_HIP(hipMemsetAsync(t->d_where, 0xFF, where_n * sizeof(int32_t), stream), "init");
   TFE_HIP(hipMemsetAsync(t->d_ctl, 0, sizeof(tfe::TierCtl), stream), "init");
   tfe::TierArgs a = tier_args(t);
@@ -424,7 +429,8 @@ static tfe_status load(const tfe_table_desc* d, hipStream_t stream, tfe_table** 
   double lf = d->max_load_factor == 0.0 ? 0.5 : d->max_load_factor;
   if (!(lf > 0.0 && lf <= 0.9)) return fail(TFE_ERR_INVALID_ARG, "max_load_factor not in (0, 0.9]");
   if (d->hbm_cache_rows < 0) return fail(TFE_ERR_INVALID_ARG, "hbm_cache_rows < 0");
-  if (d->hbm_cache_rows > 0x7FFFFFFFll) return fail(TFE_ERR_UNSUPPORTED, "hbm_cache_rows above 2^31 - 1");
+  if (d->hbm_cache_rows > (1ll << 30) - 1024)
+    return fail(TFE_ERR_UNSUPPORTED, "hbm_cache_rows above 2^30 - 1024");
   if (d->prefill_rows < 0 || d->prefill_rows > d->hbm_cache_rows ||
       d->prefill_rows > d->n_phrases)
     return fail(TFE_ERR_INVALID_ARG, "prefill_rows outside [0, min(hbm_cache_rows, n_phrases)]");

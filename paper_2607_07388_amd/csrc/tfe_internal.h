@@ -79,8 +79,8 @@ struct TierArgs {
   const void* host_values;    // device address of the pinned host rows [P x dim]
   void* cache;                // HBM cache [C x dim]
   int32_t* where;             // [P]  slot or -1
-  int32_t* owner;             // [C]  row or -1
-  uint32_t* stamp;            // [C]  clock of the last reference
+  int32_t* owner;             // [C + kDecodeMaxT]  row or -1 (physical slots)
+  uint32_t* stamp;            // [C + kDecodeMaxT]  clock of the last reference
   uint8_t* pref;              // [C]  filled by a prefetch and not used yet
   uint64_t* ring;             // recency ring of (slot << 32 | stamp)
   uint64_t ring_mask;
@@ -94,7 +94,8 @@ struct TierArgs {
   uint64_t* hval;             // [2 cap] scored prefetch: best score (clock << 32 | bits)
   uint64_t hmask;             // 2 cap - 1
   uint64_t* blk;              // [cap / 1024 + 1] per-block first-position counts
-  void* stage;                // one-launch decode: [kDecodeMaxT x dim] rows read from host
+  int32_t* spare;             // one-launch decode: [kDecodeMaxT] spare cache slot of each
+                              // position (slots C .. C + kDecodeMaxT - 1 at load)
   uint32_t clock;
   uint32_t row_bytes;
   uint32_t fill_inline;       // the inject writes missed rows into their slots
@@ -184,7 +185,7 @@ struct tfe_table {
   uint64_t* d_hpos = nullptr;    // [2 scratch_cap]
   uint64_t* d_hval = nullptr;    // [2 scratch_cap]
   uint64_t* d_blk = nullptr;     // [scratch_cap / 1024 + 1]
-  void* d_stage = nullptr;       // [kDecodeMaxT x dim] staging rows (tiered, inline fill)
+  int32_t* d_spare = nullptr;    // [kDecodeMaxT] spare slots of the one-launch decode
   uint32_t scratch_cap = 0;
   uint32_t clock = 0;
   hipEvent_t ev_resolved = nullptr, ev_filled = nullptr, ev_lookup = nullptr,

@@ -1206,21 +1206,23 @@ __global__ __launch_bounds__(WPB * 64) void k_tier_inject(const TierArgs t) {
 //   Every wave runs its position at once: key formation and probe, the
 //   row's residency (where), the value row from the cache or -- when it is
 //   not cached -- straight from pinned host memory, gate and injection.  A
-//   row read from host memory is also written to the position's staging row
-//   in HBM.  This is safe before any residency decision: victims are never
-//   slots that the call references, so nothing a wave reads changes during
-//   the call.
-//   Each wave then publishes its row and the slot it found and counts itself
-//   in; the last wave to arrive resolves residency for the whole call with
-//   the policy of k_resolve_lookup: first positions of rows (lane q =
-//   position q), cached rows referenced, victims for the missed rows from
-//   the tail of the recency ring, the staged rows copied into their victim
-//   slots, recency appends in first-position order, counters.
+//   row read from host memory is also written into the position's spare
+//   slot: the cache has kDecodeMaxT physical slots beyond its C rows that
+//   no row maps to and the recency order does not hold.  This is safe
+//   before any residency decision: victims are never slots that the call
+//   references, so nothing a wave reads changes during the call.
+//   Each wave publishes its row and slot and counts itself in; the last
+//   wave to arrive resolves residency for the whole call with the policy of
+//   k_resolve_lookup: first positions of rows (lane q = position q), cached
+//   rows referenced, victims for the missed rows from the tail of the
+//   recency ring, recency appends in first-position order, counters.  A
+//   filled row takes over its position's spare slot and the victim slot
+//   becomes the new spare, so no row is copied.
 // One launch and no cross-block waiting: a wave that is not last exits.
-// What crosses blocks (row, slot, staged row) is written and read with
-// device-scope stores and loads, and each wave waits for its stores to
-// complete before it counts in; a device-scope fence would instead write
-// back and invalidate the whole L2 in every wave.
+// What crosses blocks (row, slot) is written and read with device-scope
+// stores and loads, and each wave waits for its stores to complete before
+// it counts in; a device-scope fence would instead write back and
+// invalidate the whole L2 in every wave.
 
 // Device-scope (coherent across the XCDs' L2s) store and load.
 __device__ __forceinline__ void st_dev(int32_t* p, int32_t v) {
@@ -1229,40 +1231,71 @@ __device__ __forceinline__ void st_dev(int32_t* p, int32_t v) {
 __device__ __forceinline__ int32_t ld_dev(const int32_t* p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
-__device__ __forceinline__ void st_dev(u32x4* p, const u32x4 v) {
-  unsigned long long* q = (unsigned long long*)p;
-  __hip_atomic_store(q, (unsigned long long)v[0] | ((unsigned long long)v[1] << 32),
-                     __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  __hip_atomic_store(q + 1, (unsigned long long)v[2] | ((unsigned long long)v[3] << 32),
-                     __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ u32x4 ld_dev(const u32x4* p) {
-  const unsigned long long* q = (const unsigned long long*)p;
-  const unsigned long long lo = __hip_atomic_load(q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  const unsigned long long hi =
-      __hip_atomic_load(q + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  return u32x4{(uint32_t)lo, (uint32_t)(lo >> 32), (uint32_t)hi, (uint32_t)(hi >> 32)};
-}
 // Waits until every memory operation this wave issued has completed
 // (s_waitcnt vmcnt(0); the other counters left at their maximum).
 __device__ __forceinline__ void wait_mem() { __builtin_amdgcn_s_waitcnt(0x0F70); }
 
 constexpr int kWalkPer = 8;  // ring entries per lane and round of the victim walk
 
+// The first window of the victim walk: kWalkPer x 64 ring entries from the
+// tail, with their slots' stamps and owners.  Every wave of the decode
+// launch reads it while its own probe is in flight (the ring, stamps and
+// owners do not change until the last wave writes them), so the last wave
+// starts its walk with the window in registers.
+struct WalkWindow {
+  unsigned long long tail, head;
+  uint64_t e[kWalkPer];
+  uint32_t sn[kWalkPer];
+  int32_t own[kWalkPer];
+};
+
+__device__ __forceinline__ void walk_load_entries(const TierArgs& t, WalkWindow& w) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int k = 0; k < kWalkPer; ++k)
+    w.e[k] = t.ring[(w.tail + (uint64_t)(k * 64 + lane)) & t.ring_mask];
+}
+
+__device__ __forceinline__ void walk_load_slots(const TierArgs& t, WalkWindow& w) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int k = 0; k < kWalkPer; ++k) {
+    const bool in = w.tail + (uint64_t)(k * 64 + lane) < w.head;
+    const uint32_t slot = in ? (uint32_t)(w.e[k] >> 32) : 0u;
+    w.sn[k] = t.stamp[slot];
+    w.own[k] = t.owner[slot];
+  }
+}
+
+constexpr int kRefSet = 128;  // referenced-slot set of a decode call (LDS)
+
+__device__ __forceinline__ bool rset_has(const int32_t* rset, uint32_t slot) {
+  for (int q = (int)slot_hash(slot);; q = (q + 1) & (kRefSet - 1)) {
+    const int32_t v = rset[q];
+    if (v == -1) return false;
+    if ((uint32_t)v == slot) return true;
+  }
+}
+
+// Published slot word of a decode position: the cache slot (< 2^30) with
+// bit 30 set when the slot was filled by a prefetch and not used yet; -1
+// when the row is not cached (or there is no row).
+constexpr int32_t kSlotPref = 0x40000000;
+
 template <int NCH>
-__device__ void decode_resolve_last(const TierArgs& t, uint32_t T) {
-  constexpr uint32_t row_vecs = NCH * 64;
+__device__ void decode_resolve_last(const TierArgs& t, uint32_t T, WalkWindow& w) {
   __shared__ uint32_t vict[kDecodeMaxT];
   __shared__ int32_t vown[kDecodeMaxT];
-  __shared__ uint32_t fpos[kDecodeMaxT];
+  __shared__ int32_t rset[kRefSet];
   const int lane = threadIdx.x;
   const bool valid = (uint32_t)lane < T;
   const int32_t r = valid ? ld_dev(t.row_of + lane) : -1;
-  const int32_t s0 = valid ? ld_dev(t.slot_of + lane) : -1;
-  // Ring cursors and the first window of the walk, read while the first
-  // positions are worked out.
-  unsigned long long tail = t.ctl->tail;
-  const unsigned long long head = t.ctl->head;
+  const int32_t sw = valid ? ld_dev(t.slot_of + lane) : -1;
+  const int32_t sp = t.spare[lane];
+  const int32_t s0 = sw >= 0 ? (sw & ~kSlotPref) : -1;
+  const bool pv = sw >= 0 && (sw & kSlotPref) != 0;
+  rset[lane] = -1;
+  rset[lane + 64] = -1;
   // First position of each row: no lower lane holds it.
   bool first = r >= 0;
   for (int j = 0; j < (int)kDecodeMaxT; ++j) {
@@ -1270,52 +1303,48 @@ __device__ void decode_resolve_last(const TierArgs& t, uint32_t T) {
     first = first && !(j < lane && rj == r);
   }
   const bool fc = first && s0 >= 0, fm = first && s0 < 0;
-  const uint8_t pv = fc ? t.pref[s0] : (uint8_t)0;
-  if (fc) {
-    t.stamp[s0] = t.clock;  // referenced: never a victim of this call
-    if (pv) t.pref[s0] = 0;
+  __syncthreads();
+  if (fc) {  // referenced: never a victim of this call
+    int q = (int)slot_hash((uint32_t)s0);
+    while (atomicCAS(&rset[q], -1, s0) != -1) q = (q + 1) & (kRefSet - 1);
   }
   const uint64_t mfm = __builtin_amdgcn_ballot_w64(fm);
   const uint32_t need = (uint32_t)__builtin_popcountll(mfm);
   const uint32_t mrank = lanes_below(mfm);
-  if (fm) fpos[mrank] = (uint32_t)lane;
-  wait_mem();  // the stamps above land before the walk reads stamps
+  __syncthreads();  // rset
+  unsigned long long tail = w.tail;
+  const unsigned long long head = w.head;
   uint32_t got = 0;
-  // Least recent live entries (stamp still current, not this call's),
-  // kWalkPer x 64 per round; an entry of this call (none are appended
-  // before the walk) or the head ends the walk.
+  bool fresh = false;  // window w holds the entries from `tail`
+  // Least recent live entries (stamp still current, not referenced by this
+  // call, not this call's), kWalkPer x 64 per round; an entry of this call
+  // or the head ends the walk.
   while (got < need && tail < head) {
-    uint64_t e[kWalkPer];
-#pragma unroll
-    for (int k = 0; k < kWalkPer; ++k)
-      e[k] = t.ring[(tail + (uint64_t)(k * 64 + lane)) & t.ring_mask];
-    uint32_t sn[kWalkPer];
-    int32_t own[kWalkPer];
-#pragma unroll
-    for (int k = 0; k < kWalkPer; ++k) {
-      const bool in = tail + (uint64_t)(k * 64 + lane) < head;
-      const uint32_t slot = in ? (uint32_t)(e[k] >> 32) : 0u;
-      sn[k] = t.stamp[slot];
-      own[k] = t.owner[slot];
+    if (fresh) {
+      w.tail = tail;
+      walk_load_entries(t, w);
+      walk_load_slots(t, w);
     }
+    fresh = true;
     bool stop = false;
 #pragma unroll
     for (int k = 0; k < kWalkPer; ++k) {
       if (stop || got == need) continue;  // wave-uniform
       const unsigned long long base = tail + (uint64_t)(k * 64);
       const bool in = base + (uint64_t)lane < head;
-      const uint32_t slot = (uint32_t)(e[k] >> 32), st = (uint32_t)e[k];
+      const uint32_t slot = (uint32_t)(w.e[k] >> 32), st = (uint32_t)w.e[k];
       const bool cur = in && st == t.clock;
       const uint64_t mcur = __builtin_amdgcn_ballot_w64(cur);
       const uint32_t lim = mcur ? (uint32_t)__builtin_ctzll(mcur) : 64u;
-      const bool live = in && !cur && sn[k] == st && (uint32_t)lane < lim;
+      const bool live = in && !cur && w.sn[k] == st && (uint32_t)lane < lim &&
+                        !rset_has(rset, slot);
       const uint64_t ml = __builtin_amdgcn_ballot_w64(live);
       const uint32_t nl = (uint32_t)__builtin_popcountll(ml);
       const uint32_t rk = lanes_below(ml);
       const uint32_t take = nl < need - got ? nl : need - got;
       if (live && rk < take) {
         vict[got + rk] = slot;
-        vown[got + rk] = own[k];
+        vown[got + rk] = w.own[k];
       }
       if (take == need - got && take > 0) {
         // Resume after the last victim taken.
@@ -1336,38 +1365,27 @@ __device__ void decode_resolve_last(const TierArgs& t, uint32_t T) {
     if (stop) break;
     tail += (uint64_t)kWalkPer * 64;
   }
-  __syncthreads();  // vict, vown, fpos
+  __syncthreads();  // vict, vown
+  // A filled row keeps the spare slot its position's wave wrote it into; the
+  // victim's row leaves the cache and the victim slot becomes that
+  // position's spare.  No row data moves.
   const bool fill = fm && mrank < got;
   uint32_t slot_now = fc ? (uint32_t)s0 : 0u;
+  if (fc) {
+    t.stamp[s0] = t.clock;
+    if (pv) t.pref[s0] = 0;
+  }
   if (fill) {
     const uint32_t v = vict[mrank];
     const int32_t old = vown[mrank];
     if (old >= 0) t.where[old] = -1;
-    t.owner[v] = r;
-    t.where[r] = (int32_t)v;
-    t.stamp[v] = t.clock;
-    t.pref[v] = 0;
-    slot_now = v;
-  }
-  // The staged rows into their slots, four rows in flight per lane.
-  const u32x4* stage = (const u32x4*)t.stage;
-  u32x4* cache = (u32x4*)t.cache;
-  for (uint32_t q0 = 0; q0 < got; q0 += 4) {
-    u32x4 buf[4][NCH];
-#pragma unroll
-    for (uint32_t q = 0; q < 4; ++q)
-      if (q0 + q < got) {
-#pragma unroll
-        for (int k = 0; k < NCH; ++k)
-          buf[q][k] = ld_dev(stage + (size_t)fpos[q0 + q] * row_vecs + k * 64 + lane);
-      }
-#pragma unroll
-    for (uint32_t q = 0; q < 4; ++q)
-      if (q0 + q < got) {
-#pragma unroll
-        for (int k = 0; k < NCH; ++k)
-          cache[(size_t)vict[q0 + q] * row_vecs + k * 64 + lane] = buf[q][k];
-      }
+    t.owner[v] = -1;
+    t.spare[lane] = (int32_t)v;
+    t.owner[sp] = r;
+    t.where[r] = sp;
+    t.stamp[sp] = t.clock;
+    t.pref[sp] = 0;
+    slot_now = (uint32_t)sp;
   }
   const bool app = fc || fill;
   const uint64_t ma = __builtin_amdgcn_ballot_w64(app);
@@ -1391,10 +1409,25 @@ __device__ void decode_resolve_last(const TierArgs& t, uint32_t T) {
   }
 }
 
+// Publishes this wave's row and slot word, waits for its writes, and counts
+// in; true for the last wave of the call.
+__device__ __forceinline__ bool decode_arrive(const TierArgs& t, uint32_t p, int32_t row,
+                                              int32_t sw) {
+  if (threadIdx.x == 0) {
+    st_dev(t.row_of + p, row);
+    st_dev(t.slot_of + p, sw);
+  }
+  wait_mem();
+  uint32_t last = 0;
+  if (threadIdx.x == 0)
+    last = __hip_atomic_fetch_add(&t.ctl->arrive, 1u, __ATOMIC_RELAXED,
+                                  __HIP_MEMORY_SCOPE_AGENT) == t.look.T - 1 ? 1u : 0u;
+  return __builtin_amdgcn_readfirstlane(last) != 0;
+}
+
 template <int DT, int NCH>
 __global__ __launch_bounds__(64) void k_tier_decode(const TierArgs t) {
   constexpr int ROW_VECS = NCH * 64;
-  static_assert(NCH <= 8, "staging copy holds at most 8 vectors per lane and row");
   const LookupArgs& a = t.look;
   const int lane = threadIdx.x;
   const uint32_t p = blockIdx.x;  // grid = T <= kDecodeMaxT
@@ -1405,51 +1438,59 @@ __global__ __launch_bounds__(64) void k_tier_decode(const TierArgs t) {
   int32_t tw[4];
   dev::window_tokens(a, p, tw);
   const dev::Probe pr = dev::probe_begin(a, tw, lane);
+  WalkWindow win;
+  win.tail = t.ctl->tail;
+  win.head = t.ctl->head;
+  walk_load_entries(t, win);
+  const int32_t sp = t.spare[p];
   int len;
   const int32_t row = dev::probe_finish(a, pr, lane, &len);
   if (lane == 0) dev::write_result(a, p, row, len);
+  const int32_t w = row >= 0 ? t.where[row] : -1;
+  walk_load_slots(t, win);
   u32x4* out = (u32x4*)a.hout + (size_t)p * ROW_VECS;
-  int32_t w = -1;
   if (row < 0) {
+    if (decode_arrive(t, p, row, -1)) decode_resolve_last<NCH>(t, a.T, win);
     if (!a.inplace) {
 #pragma unroll
       for (int k = 0; k < NCH; ++k) dev::store_out(hv[k], out + k * 64 + lane);
     }
-  } else {
-    w = t.where[row];
-    const u32x4* mrow = w >= 0 ? (const u32x4*)t.cache + (size_t)w * ROW_VECS
-                               : (const u32x4*)t.host_values + (size_t)row * ROW_VECS;
-    u32x4 mv[NCH];
+    return;
+  }
+  u32x4 mv[NCH];
+  if (w >= 0) {
+    // Cached: count in first (with the slot's prefetched flag), then read
+    // the row; the last wave never writes a slot this call uses.
+    const int32_t sw = t.pref[w] ? (w | kSlotPref) : w;
+    if (decode_arrive(t, p, row, sw)) decode_resolve_last<NCH>(t, a.T, win);
+    const u32x4* mrow = (const u32x4*)t.cache + (size_t)w * ROW_VECS;
 #pragma unroll
     for (int k = 0; k < NCH; ++k) mv[k] = mrow[k * 64 + lane];
-    if (w < 0) {
-      u32x4* st = (u32x4*)t.stage + (size_t)p * ROW_VECS;
+  } else {
+    // Host only: the row is read once, written into this position's spare
+    // slot (which no row maps to, so no wave reads it), and injected.
+    const u32x4* mrow = (const u32x4*)t.host_values + (size_t)row * ROW_VECS;
 #pragma unroll
-      for (int k = 0; k < NCH; ++k) st_dev(st + k * 64 + lane, mv[k]);
-    }
-    const float g = dev::gate_of<DT, NCH>(a, hv, mv);
-    dev::store_injected<DT, NCH>(out, hv, mv, g, lane);
+    for (int k = 0; k < NCH; ++k) mv[k] = mrow[k * 64 + lane];
+    u32x4* dst = (u32x4*)t.cache + (size_t)sp * ROW_VECS;
+#pragma unroll
+    for (int k = 0; k < NCH; ++k) dst[k * 64 + lane] = mv[k];
+    if (decode_arrive(t, p, row, -1)) decode_resolve_last<NCH>(t, a.T, win);
   }
-  if (lane == 0) {
-    st_dev(t.row_of + p, row);
-    st_dev(t.slot_of + p, w);
-  }
-  // Count in once this wave's published writes are complete; the last
-  // wave resolves the call.
-  wait_mem();
-  uint32_t last = 0;
-  if (lane == 0)
-    last = __hip_atomic_fetch_add(&t.ctl->arrive, 1u, __ATOMIC_RELAXED,
-                                  __HIP_MEMORY_SCOPE_AGENT) == a.T - 1 ? 1u : 0u;
-  last = __builtin_amdgcn_readfirstlane(last);
-  if (!last) return;
-  decode_resolve_last<NCH>(t, a.T);
+  const float g = dev::gate_of<DT, NCH>(a, hv, mv);
+  dev::store_injected<DT, NCH>(out, hv, mv, g, lane);
 }
 
 // Initial state: slot s < prefill holds row s; the ring lists the empty
 // slots in ascending order, then the filled slots by descending row.
 __global__ void k_tier_init(const TierArgs t, uint32_t C, uint32_t prefill) {
   const uint32_t i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= C && i < C + kDecodeMaxT) {  // spare slots: no row, not in the ring
+    t.owner[i] = -1;
+    t.stamp[i] = 0;
+    t.pref[i] = 0;
+    t.spare[i - C] = (int32_t)i;
+  }
   if (i >= C) return;
   const uint32_t empty = C - prefill;
   const uint32_t slot = i < empty ? prefill + i : prefill - 1 - (i - empty);
@@ -1531,7 +1572,8 @@ hipError_t launch_decode_t(const TierArgs& t, hipStream_t s) {
 }  // namespace
 
 hipError_t launch_tier_init(const TierArgs& t, uint32_t C, uint32_t prefill, hipStream_t s) {
-  hipLaunchKernelGGL(k_tier_init, dim3((C + 255) / 256), dim3(256), 0, s, t, C, prefill);
+  hipLaunchKernelGGL(k_tier_init, dim3((C + kDecodeMaxT + 255) / 256), dim3(256), 0, s, t, C,
+                     prefill);
   return hipGetLastError();
 }
 
