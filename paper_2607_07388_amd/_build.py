@@ -35,7 +35,9 @@ def build(verbose=False):
         if verbose and out.strip():
             print(out)
         objs.append(obj)
-    cmd = ["hipcc", "--offload-arch=gfx950", "-shared", "-fPIC", "-pthread", "-o", SO + ".tmp"] + objs
+    # -z defs: a symbol left undefined fails the link here, not the load on the GPU machine.
+    cmd = ["hipcc", "--offload-arch=gfx950", "-shared", "-fPIC", "-pthread", "-Wl,-z,defs",
+           "-o", SO + ".tmp"] + objs
     r = subprocess.run(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True)
     if r.returncode != 0:
         raise RuntimeError("libtfe link failed:\n" + r.stdout)

@@ -66,6 +66,14 @@ static tfe_status sync_table(const tfe_table* ct) {
   }
   if (t->prefetch_pending && t->ev_prefetch)
     TFE_HIP(hipEventSynchronize(t->ev_prefetch), "wait for the prefetch");
+  if (t->pf_counted_pending && t->ev_prefetch) {
+    hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+    TFE_HIP(hipStreamIsCapturing(t->pf_stream, &cs), "hipStreamIsCapturing");
+    if (cs == hipStreamCaptureStatusNone) {
+      TFE_HIP(hipEventRecord(t->ev_prefetch, t->pf_stream), "record");
+      TFE_HIP(hipEventSynchronize(t->ev_prefetch), "wait for the prefetch");
+    }
+  }
   if (t->own_stream) TFE_HIP(hipStreamSynchronize(t->own_stream), "wait for the table stream");
   return TFE_OK;
 }
@@ -79,7 +87,8 @@ static void release(tfe_table* t) {
   (void)sync_table(t);
   void* dev_bufs[] = {t->d_slots, t->d_values, t->d_cache, t->d_where, t->d_owner, t->d_stamp,
                       t->d_pref, t->d_ring, t->d_ring2, t->d_ctl, t->d_row_of,
-                      t->d_slot_of, t->d_phase, t->d_jobs, t->d_hit_ctr, t->d_hkey, t->d_hpos, t->d_hval, t->d_blk, t->d_spare};
+                      t->d_slot_of, t->d_phase, t->d_jobs, t->d_hit_ctr, t->d_hkey, t->d_hpos, t->d_hval, t->d_blk, t->d_spare, t->d_pf_row_of,
+                      t->d_pf_slot_of, t->d_pf_phase, t->d_pf_jobs};
   for (void* b : dev_bufs)
     if (b) (void)hipFree(b);
   if (t->own_h_values && t->h_values) (void)hipHostFree(t->h_values);
@@ -163,6 +172,18 @@ static tfe::TierArgs tier_args(tfe_table* t) {
   a.look.n_max = t->n_max;
   a.look.vocab = t->vocab;
   return a;
+}
+
+// Orders the kernels enqueued next on `s` after the counted work submitted
+// so far -- every one-launch decode wave (lk) and every one-block prefetch's
+// copy blocks (pf) -- with one waiting wave.
+static tfe_status order_after_counted(tfe_table* t, hipStream_t s, bool lk, bool pf) {
+  tfe::TierArgs a = tier_args(t);
+  a.wait_lk = lk ? t->waves_issued : 0;
+  a.wait_pf = pf ? t->fills_issued : 0;
+  if (!a.wait_lk && !a.wait_pf) return TFE_OK;
+  TFE_HIP(tfe::launch_tier_wait(a, s), "ordering wait");
+  return TFE_OK;
 }
 
 static uint64_t pow2_at_least(uint64_t n) {
@@ -269,15 +290,40 @@ static tfe_status ensure_scratch(tfe_table* t, uint32_t n) {
   return TFE_OK;
 }
 
+// Grows the prefetches' own per-call scratch to n entries, after the
+// table's pending work that may still use the old buffers.
+static tfe_status ensure_pf_scratch(tfe_table* t, uint64_t n) {
+  if (n <= t->pf_cap) return TFE_OK;
+  TFE_TRY(sync_table(t));
+  void* olds[] = {t->d_pf_row_of, t->d_pf_slot_of, t->d_pf_phase, t->d_pf_jobs};
+  for (void* b : olds)
+    if (b) (void)hipFree(b);
+  t->d_pf_row_of = t->d_pf_slot_of = nullptr;
+  t->d_pf_phase = nullptr;
+  t->d_pf_jobs = nullptr;
+  t->pf_cap = 0;
+  const uint64_t cap = pow2_at_least(n < 1024 ? 1024 : n);
+  TFE_TRY(dev_alloc(&t->d_pf_row_of, cap, "prefetch scratch"));
+  TFE_TRY(dev_alloc(&t->d_pf_slot_of, cap, "prefetch scratch"));
+  TFE_TRY(dev_alloc(&t->d_pf_phase, cap, "prefetch scratch"));
+  TFE_TRY(dev_alloc(&t->d_pf_jobs, cap, "prefetch scratch"));
+  t->pf_cap = (uint32_t)cap;
+  return TFE_OK;
+}
+
 // Before a call that appends at most `appends` recency entries: drops the
 // dead entries when the ring could overflow (every slot keeps exactly one
 // live entry, so afterwards the ring holds cache_rows entries), growing the
 // ring if even that would not leave room.
-static tfe_status reserve_ring(tfe_table* t, uint64_t appends, hipStream_t stream) {
+// `lk`, `pf`: counted work that the kernels of this call on `stream` still
+// have to follow (a compaction launched here waits for it first).
+static tfe_status reserve_ring(tfe_table* t, uint64_t appends, hipStream_t stream, bool lk,
+                               bool pf) {
   if (t->ring_bound + appends <= t->ring_cap) {
     t->ring_bound += appends;
     return TFE_OK;
   }
+  TFE_TRY(order_after_counted(t, stream, lk, pf));
   const uint64_t need = (uint64_t)t->cache_rows + appends;
   tfe::TierArgs a = tier_args(t);
   if (need > t->ring_cap) {
@@ -310,8 +356,10 @@ static tfe_status reserve_ring(tfe_table* t, uint64_t appends, hipStream_t strea
 // table hold 32-bit clocks; before the clock would wrap, every live recency
 // entry and slot stamp restart at 0 (order kept) and the row table is
 // cleared, so clocks 1, 2, ... can be used again.
-static tfe_status advance_clock(tfe_table* t, uint64_t appends, hipStream_t stream) {
+static tfe_status advance_clock(tfe_table* t, uint64_t appends, hipStream_t stream, bool lk,
+                                bool pf) {
   if (t->clock == 0xFFFFFFFFu) {
+    TFE_TRY(order_after_counted(t, stream, lk, pf));
     tfe::TierArgs a = tier_args(t);
     TFE_HIP(tfe::launch_ring_compact(a, t->d_ring2, t->ring_cap - 1, true, stream),
             "clock restart");
@@ -350,17 +398,30 @@ static tfe_status lookup_tiered(tfe_table* t, const LookupArgs& look, hipStream_
     t->prefetch_pending = false;
   }
   if (t->fill_recorded) TFE_HIP(hipStreamWaitEvent(stream, t->ev_filled, 0), "wait fill");
-  TFE_TRY(reserve_ring(t, look.T, stream));
-  TFE_TRY(advance_clock(t, look.T, stream));
+  // A one-block prefetch on another stream is followed without HIP events:
+  // the one-launch decode waits for its copy blocks itself; any other
+  // kernel of this call is preceded by a waiting wave.
+  const bool pf = t->pf_counted_pending && stream != t->pf_stream;
+  const bool decode = t->fill_mode == TFE_FILL_INLINE && look.T <= tfe::kDecodeMaxT;
+  if (pf && !decode) TFE_TRY(order_after_counted(t, stream, false, true));
+  const bool pf_kernel = pf && decode;  // still to be awaited by the decode kernel
+  TFE_TRY(reserve_ring(t, look.T, stream, false, pf_kernel));
+  TFE_TRY(advance_clock(t, look.T, stream, false, pf_kernel));
+  t->pf_counted_pending = false;  // everything after this call follows it
   tfe::TierArgs a = tier_args(t);
   a.look = look;
-  if (t->fill_mode == TFE_FILL_INLINE && look.T <= tfe::kDecodeMaxT) {
+  if (decode) {
     // The whole call in one launch (probe, inject, residency).
+    a.wait_pf = pf_kernel ? t->fills_issued : 0;
+    a.count_lookup = 1;
     TFE_HIP(tfe::launch_tier_decode(a, t->dtype, t->dim, stream), "tiered decode");
+    t->waves_issued += look.T;
+    t->last_lookup_counted = true;
     t->lookup_recorded = true;
     t->last_stream = stream;
     return TFE_OK;
   }
+  t->last_lookup_counted = false;
   const bool fused = tfe::lookup_resolve_fused(look.T);
   if (!fused) TFE_HIP(tfe::launch_tier_probe(a, stream), "tier probe");
   if (fused)
@@ -391,18 +452,53 @@ static tfe_status prefetch_tiered(tfe_table* t, const int32_t* tail, int32_t tai
   if (N > 0x7FFFFFFFull) return fail(TFE_ERR_UNSUPPORTED, "B * K above 2^31 - 1");
   TFE_TRY(check_device(t));
   TFE_TRY(refuse_capture(side, "a prefetch"));
+  const bool one_block = N <= tfe::prefetch_fused_max();
+  // The one-block prefetch keeps one probe result per (candidate, length)
+  // in its scratch; the scored resolution uses the call-wide row table of
+  // the lookups' scratch (never run by two calls at once).
+  TFE_TRY(ensure_pf_scratch(t, one_block ? N * (uint64_t)(t->n_max - t->n_min + 1) : N));
   TFE_TRY(ensure_scratch(t, (uint32_t)N));
-  // After the table's last lookup (all work submitted to its stream so far),
-  // its cache fill, and any earlier prefetch.
-  if (t->lookup_recorded) {
+  // After the table's last lookup, its cache fill, and any earlier
+  // prefetch.  A one-launch decode lookup and a one-block prefetch are
+  // followed on the device (counters in the control block) instead of with
+  // HIP events; the other kernels use events.
+  const bool other_stream = t->lookup_recorded && side != t->last_stream;
+  const bool lk = one_block && other_stream && t->last_lookup_counted;
+  if (other_stream && !lk) {
     TFE_HIP(hipEventRecord(t->ev_lookup, t->last_stream), "record");
     TFE_HIP(hipStreamWaitEvent(side, t->ev_lookup, 0), "wait lookup");
   }
   if (t->fill_recorded) TFE_HIP(hipStreamWaitEvent(side, t->ev_filled, 0), "wait fill");
   if (t->prefetch_pending) TFE_HIP(hipStreamWaitEvent(side, t->ev_prefetch, 0), "wait prefetch");
-  TFE_TRY(reserve_ring(t, N, side));
-  TFE_TRY(advance_clock(t, N, side));
+  t->prefetch_pending = false;
+  // A counted prefetch on another stream shares this one's scratch: this
+  // whole call (its probe too) waits for it.
+  const bool pf = t->pf_counted_pending && side != t->pf_stream;
+  if (pf) TFE_TRY(order_after_counted(t, side, false, true));
+  if (!one_block) TFE_TRY(order_after_counted(t, side, lk, false));
+  TFE_TRY(reserve_ring(t, N, side, lk, false));
+  TFE_TRY(advance_clock(t, N, side, lk, false));
   tfe::TierArgs a = tier_args(t);
+  a.prefetch = 1;
+  a.row_of = t->d_pf_row_of;
+  a.slot_of = t->d_pf_slot_of;
+  a.phase = t->d_pf_phase;
+  a.jobs = t->d_pf_jobs;
+  if (one_block) {
+    // The probe runs before this wait: it touches only the index, the
+    // candidates and the prefetch scratch.
+    a.wait_lk = lk ? t->waves_issued : 0;
+    TFE_HIP(tfe::launch_prefetch_fused(a, tail, tail_len, cand, (uint32_t)B, (uint32_t)K, prob,
+                                       (uint32_t)budget, side),
+            "prefetch");
+    a.wait_lk = a.wait_pf = 0;
+    a.count_fill = 1;
+    TFE_HIP(tfe::launch_fill(a, t->dtype, t->dim, (uint32_t)N, side), "prefetch fill");
+    t->fills_issued += tfe::fill_blocks((uint32_t)N);
+    t->pf_counted_pending = true;
+    t->pf_stream = side;
+    return TFE_OK;
+  }
   TFE_HIP(tfe::launch_prefetch_probe(a, tail, tail_len, cand, (uint32_t)B, (uint32_t)K, side),
           "prefetch probe");
   if (prob) {
@@ -411,12 +507,12 @@ static tfe_status prefetch_tiered(tfe_table* t, const int32_t* tail, int32_t tai
   } else {
     // The candidates are referenced like a lookup's positions.
     a.look.T = (uint32_t)N;
-    a.prefetch = 1;
     TFE_HIP(tfe::launch_resolve_lookup(a, side), "prefetch resolve");
   }
   TFE_HIP(tfe::launch_fill(a, t->dtype, t->dim, (uint32_t)N, side), "prefetch fill");
   TFE_HIP(hipEventRecord(t->ev_prefetch, side), "record");
   t->prefetch_pending = true;
+  t->pf_counted_pending = false;  // this prefetch follows the counted ones
   return TFE_OK;
 }
 
@@ -649,6 +745,9 @@ tfe_status tfe_get_stats(const tfe_table* table, tfe_stats* out) {
     s.prefetch_used = c.stats.prefetch_used;
     s.host_bytes = c.stats.host_bytes;
     s.prefetch_dropped = c.stats.prefetch_dropped;
+    if (c.wait_timeouts)
+      return tfe::fail(TFE_ERR_HIP, "%u device-side ordering waits hit their bound",
+                       c.wait_timeouts);
   } else if (table->d_hit_ctr) {
     std::vector<unsigned long long> ctr((size_t)tfe::kHitCounters * tfe::kHitStride);
     hipError_t e = hipMemcpyAsync(ctr.data(), table->d_hit_ctr, ctr.size() * sizeof ctr[0],
@@ -702,6 +801,10 @@ tfe_status tfe_residency(const tfe_table* table, const int32_t* rows, int64_t n,
     if (t->prefetch_pending) {
       const hipError_t e = hipStreamWaitEvent(s, t->ev_prefetch, 0);
       if (e != hipSuccess) return tfe::fail(TFE_ERR_HIP, "residency: %s", hipGetErrorString(e));
+    }
+    if (t->pf_counted_pending && s != t->pf_stream) {
+      st = tfe::order_after_counted(t, s, false, true);
+      if (st != TFE_OK) return st;
     }
   }
   const hipError_t e = tfe::launch_residency(t->cache_rows > 0 ? t->d_where : nullptr,

@@ -211,6 +211,44 @@ __device__ __forceinline__ int32_t probe_finish(const LookupArgs& a, const Probe
   return __builtin_amdgcn_readlane(w.myrow, sel);
 }
 
+// Exact-match probe of one key by one thread (no cross-lane work): the
+// key's home bucket is read whole (8 slots of 16 bytes, all in flight), then
+// the following buckets while the key is neither found nor ruled out by an
+// empty slot.  Returns the row, or -1 when the key is absent.  Used where one
+// thread handles a whole window (the single-block prefetch).
+__device__ __forceinline__ int32_t probe_key_thread(const LookupArgs& a, uint64_t key,
+                                                    uint32_t ext) {
+  uint64_t b = tfe_hash(key, ext) & a.bucket_mask;
+  for (uint64_t it = 0; it <= a.bucket_mask; ++it) {
+    u32x4 sl[TFE_SLOTS_PER_BUCKET];
+    const u32x4* bp = (const u32x4*)(a.slots + b * TFE_SLOTS_PER_BUCKET);
+#pragma unroll
+    for (int i = 0; i < TFE_SLOTS_PER_BUCKET; ++i) sl[i] = bp[i];
+    bool empty = false;
+    int32_t row = -1;
+#pragma unroll
+    for (int i = 0; i < TFE_SLOTS_PER_BUCKET; ++i) {
+      const uint64_t sk = (uint64_t)sl[i][0] | ((uint64_t)sl[i][1] << 32);
+      if (sk == key && sl[i][2] == ext) row = (int32_t)sl[i][3];
+      empty = empty || sk == TFE_EMPTY_KEY;
+    }
+    if (row >= 0 || empty) return row;
+    b = (b + 1) & a.bucket_mask;
+  }
+  return -1;
+}
+
+// The key and extension word of the n-gram of window t (newest first) and
+// whether the window holds n valid tokens.
+__device__ __forceinline__ bool window_key(const LookupArgs& a, const int32_t* t, int n,
+                                           uint64_t* key, uint32_t* ext) {
+  const bool ok = tok_ok(t[0], a.vocab) && tok_ok(t[1], a.vocab) &&
+                  (n < 3 || tok_ok(t[2], a.vocab)) && (n < 4 || tok_ok(t[3], a.vocab));
+  *key = tfe_key(n, (uint32_t)t[0], (uint32_t)t[1], n >= 3 ? (uint32_t)t[2] : 0u);
+  *ext = n == 4 ? (uint32_t)t[3] : 0u;
+  return ok;
+}
+
 // Gate of Eq. 5 from this lane's partial sums of h.h, m.m and h.m.
 __device__ __forceinline__ float gate_finish(const LookupArgs& a, float shh, float smm,
                                              float shm) {

@@ -68,7 +68,10 @@ struct TierCtl {
   unsigned long long njobs;       // host -> cache copies of the current call
   unsigned long long call_head;   // long calls: ring head before the call's appends
   unsigned int arrive;            // one-launch decode: waves done with their position
-  unsigned int pad_;
+  unsigned int wait_timeouts;     // device-side ordering waits that hit their bound
+  // Device-side ordering of decode lookups and prefetches (no HIP events):
+  unsigned long long lk_done;     // decode waves done with the shared state (monotone)
+  unsigned long long pf_done;     // prefetch copy blocks done (monotone)
   TierStats stats;
 };
 struct TierJob {
@@ -101,6 +104,11 @@ struct TierArgs {
   uint32_t fill_inline;       // the inject writes missed rows into their slots
   uint32_t prefetch;          // resolve kernels: the call is a prefetch (fills are marked
                               // prefetched; prefetch counters instead of lookup counters)
+  // Device-side ordering: wait until ctl->lk_done >= wait_lk and ctl->pf_done
+  // >= wait_pf before touching the shared state (0: no wait); count_* make
+  // the decode waves and the copy blocks count themselves in when done.
+  unsigned long long wait_lk, wait_pf;
+  uint32_t count_lookup, count_fill;
 };
 
 // Phase bit of a position whose inject writes its row into slot_of (inline
@@ -127,10 +135,22 @@ hipError_t launch_prefetch_probe(const TierArgs& t, const int32_t* tail, int32_t
 hipError_t launch_resolve_prefetch_scored(const TierArgs& t, uint32_t N, const float* prob,
                                          uint32_t budget, hipStream_t s);
 uint32_t scored_prefetch_budget_max();
+// Prefetches of at most prefetch_fused_max() candidates run as one
+// single-block launch (probe, residency, copies).
+uint32_t prefetch_fused_max();
+hipError_t launch_prefetch_fused(const TierArgs& t, const int32_t* tail, int32_t tail_len,
+                                 const int32_t* cand, uint32_t B, uint32_t K, const float* prob,
+                                 uint32_t budget, hipStream_t s);
 // out[i] = where[rows[i]] (where = null: rows[i]); -2 outside [0, P).
 hipError_t launch_residency(const int32_t* where, int64_t P, const int32_t* rows, int64_t n,
                             int32_t* out, hipStream_t s);
 hipError_t launch_fill(const TierArgs& t, int dtype, int dim, uint32_t max_jobs, hipStream_t s);
+// Blocks of one fill launch (each counts itself into ctl->pf_done when
+// t.count_fill is set).
+uint32_t fill_blocks(uint32_t max_jobs);
+// One wave that waits for ctl->lk_done >= t.wait_lk and ctl->pf_done >=
+// t.wait_pf: orders the following kernels of its stream after them.
+hipError_t launch_tier_wait(const TierArgs& t, hipStream_t s);
 hipError_t launch_tier_inject(const TierArgs& t, int dtype, int dim, hipStream_t s);
 
 // Launches the fused resident-table kernel; returns the launch error.
@@ -186,11 +206,27 @@ struct tfe_table {
   uint64_t* d_hval = nullptr;    // [2 scratch_cap]
   uint64_t* d_blk = nullptr;     // [scratch_cap / 1024 + 1]
   int32_t* d_spare = nullptr;    // [kDecodeMaxT] spare slots of the one-launch decode
+  // Per-call scratch of prefetches, apart from the lookups' (a prefetch's
+  // probe runs while a decode lookup on another stream may still use its
+  // own): matched row, matched length / phase, slot, fill list.
+  int32_t* d_pf_row_of = nullptr;
+  int32_t* d_pf_slot_of = nullptr;
+  uint8_t* d_pf_phase = nullptr;
+  tfe::TierJob* d_pf_jobs = nullptr;
+  uint32_t pf_cap = 0;
   uint32_t scratch_cap = 0;
   uint32_t clock = 0;
   hipEvent_t ev_resolved = nullptr, ev_filled = nullptr, ev_lookup = nullptr,
              ev_prefetch = nullptr;
   bool lookup_recorded = false, prefetch_pending = false, fill_recorded = false;
   hipStream_t last_stream = nullptr;   // stream of the last lookup (lookup_recorded)
+  // Device-side ordering of one-launch decode lookups and one-block
+  // prefetches: totals submitted, compared by the kernels with ctl->lk_done
+  // and ctl->pf_done.
+  uint64_t waves_issued = 0;     // decode waves submitted
+  uint64_t fills_issued = 0;     // counted prefetch copy blocks submitted
+  bool last_lookup_counted = false;  // the last lookup was a counted decode
+  bool pf_counted_pending = false;   // a counted prefetch may still run
+  hipStream_t pf_stream = nullptr;   // stream of the last counted prefetch
 };
 #endif

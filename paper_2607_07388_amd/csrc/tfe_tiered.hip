@@ -67,6 +67,53 @@ __device__ __forceinline__ uint64_t ring_entry(uint32_t slot, uint32_t stamp) {
   return ((uint64_t)slot << 32) | stamp;
 }
 
+// Device-scope (coherent across the XCDs' L2s) store and load.
+__device__ __forceinline__ void st_dev(int32_t* p, int32_t v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ int32_t ld_dev(const int32_t* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+// Waits until every memory operation this wave issued has completed
+// (s_waitcnt vmcnt(0); the other counters left at their maximum).
+__device__ __forceinline__ void wait_mem() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+
+// Device-side ordering between a one-launch decode lookup and a one-block
+// prefetch on different streams, instead of HIP events (whose record and
+// cross-stream wait cost about 20 us of host time per prefetch here).  A
+// waiter only ever waits for work that the host submitted before it, so
+// the waits end; each is bounded all the same (kWaitLimit sleeps, about a
+// second), and a wait that hits the bound is counted in ctl->wait_timeouts
+// (tfe_get_stats then reports an error).
+constexpr uint32_t kWaitLimit = 1u << 22;
+
+// One thread: waits until *ctr >= want.
+__device__ __forceinline__ void wait_at_least(TierCtl* ctl, unsigned long long* ctr,
+                                              unsigned long long want) {
+  uint32_t n = 0;
+  while (__hip_atomic_load(ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < want) {
+    __builtin_amdgcn_s_sleep(8);
+    if (++n == kWaitLimit) {
+      atomicAdd(&ctl->wait_timeouts, 1u);
+      break;
+    }
+  }
+}
+
+// Called by every thread of a block: the block's thread 0 waits for
+// ctl->lk_done >= t.wait_lk and ctl->pf_done >= t.wait_pf, then every wave
+// drops its stale cache lines (agent-scope acquire) before reading state
+// that the awaited kernels wrote.
+__device__ __forceinline__ void wait_ordered_block(const TierArgs& t) {
+  if (!t.wait_lk && !t.wait_pf) return;  // block-uniform
+  if (threadIdx.x == 0) {
+    if (t.wait_lk) wait_at_least(t.ctl, &t.ctl->lk_done, t.wait_lk);
+    if (t.wait_pf) wait_at_least(t.ctl, &t.ctl->pf_done, t.wait_pf);
+  }
+  __syncthreads();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+}
+
 // Takes up to `need` least-recent slots not referenced in this call (stamp
 // below the call's clock) from the tail of the ring into vict[0..got).
 // Dead entries passed on the way are dropped.  Returns got (block-uniform).
@@ -337,7 +384,9 @@ constexpr int kGroupItems = 4;
 constexpr int kGroup = kGroupItems * kResolveThreads;
 constexpr int kGroupHash = 2 * kGroup;
 
-__global__ __launch_bounds__(kResolveThreads) void k_resolve_lookup(const TierArgs t, uint32_t T) {
+// Returns the number of rows filled (block-uniform); the fill list is
+// jobs[0 .. filled).
+__device__ uint32_t resolve_one_block(const TierArgs& t, uint32_t T) {
   constexpr int N = kGroupItems;
   __shared__ int32_t hkey[kGroupHash];
   __shared__ uint32_t hpos[kGroupHash];
@@ -471,6 +520,11 @@ __global__ __launch_bounds__(kResolveThreads) void k_resolve_lookup(const TierAr
       st.host_bytes += (unsigned long long)((t.fill_inline ? 0u : got) + s_cnt[3]) * t.row_bytes;
     }
   }
+  return got;
+}
+
+__global__ __launch_bounds__(kResolveThreads) void k_resolve_lookup(const TierArgs t, uint32_t T) {
+  (void)resolve_one_block(t, T);
 }
 
 // ---- Resolution of calls longer than kGroup positions, over many blocks.
@@ -933,8 +987,10 @@ __device__ __forceinline__ uint64_t gh_find(const TierArgs& t, int32_t r) {
   return h;
 }
 
-__global__ __launch_bounds__(kResolveThreads) void k_resolve_prefetch_scored(
-    const TierArgs t, uint32_t N, const float* __restrict__ prob, uint32_t budget) {
+// Returns the number of rows filled (block-uniform); the fill list is
+// jobs[0 .. filled).
+__device__ uint32_t resolve_scored(const TierArgs& t, uint32_t N, const float* __restrict__ prob,
+                                   uint32_t budget) {
   __shared__ unsigned long long sel[kScoredBudgetMax];
   __shared__ uint32_t vict[kResolveThreads];
   __shared__ uint32_t hist[256];
@@ -1096,23 +1152,105 @@ __global__ __launch_bounds__(kResolveThreads) void k_resolve_prefetch_scored(
     st.prefetch_dropped += n - got;
     st.host_bytes += (unsigned long long)got * t.row_bytes;
   }
+  return got;
 }
+
+__global__ __launch_bounds__(kResolveThreads) void k_resolve_prefetch_scored(
+    const TierArgs t, uint32_t N, const float* __restrict__ prob, uint32_t budget) {
+  (void)resolve_scored(t, N, prob, budget);
+}
+
+// ---- Prefetch of up to kPrefetchFusedMax candidates in two launches: one
+// block runs the probe of every candidate window and the residency
+// resolution (the lookup policy for tfe_prefetch, the scored policy for
+// tfe_prefetch_scored); then k_fill copies the chosen rows from pinned host
+// memory into their slots over many compute units (one compute unit's
+// outstanding host reads would make the copies several times slower).
+constexpr uint32_t kPrefetchFusedMax = kGroup;
+
+// Longest match of every candidate window (the row the next lookup selects
+// if that candidate is the next token).  Thread items are (candidate,
+// length) pairs, longest first, each probed by one thread reading whole
+// buckets, so that the bucket reads of up to 1024 items are in flight at
+// once.  Writes row_of[q] and phase[q] = matched length; uses slot_of as
+// scratch for the N * L item results.
+__device__ void prefetch_probe_block(const TierArgs& t, const int32_t* __restrict__ tail,
+                                     int32_t tail_len, const int32_t* __restrict__ cand,
+                                     uint32_t B, uint32_t K) {
+  const LookupArgs& a = t.look;
+  const uint32_t N = B * K;
+  const uint32_t L = (uint32_t)(a.n_max - a.n_min + 1);
+  int32_t* item_row = t.slot_of;
+  for (uint32_t i = threadIdx.x; i < N * L; i += kResolveThreads) {
+    const uint32_t q = i / L, l = i - q * L;
+    const uint32_t b = q / K;
+    int32_t tw[4];
+    tw[0] = cand[q];
+    for (int j = 1; j < 4; ++j)
+      tw[j] = tail_len - j >= 0 ? tail[(size_t)b * tail_len + (tail_len - j)] : -1;
+    uint64_t key;
+    uint32_t ext;
+    const bool ok = dev::window_key(a, tw, a.n_max - (int)l, &key, &ext);
+    item_row[i] = ok ? dev::probe_key_thread(a, key, ext) : -1;
+  }
+  __syncthreads();
+  for (uint32_t q = threadIdx.x; q < N; q += kResolveThreads) {
+    int32_t row = -1;
+    int len = 0;
+    for (uint32_t l = 0; l < L; ++l) {
+      const int32_t r = item_row[q * L + l];
+      if (r >= 0) {
+        row = r;
+        len = a.n_max - (int)l;
+        break;
+      }
+    }
+    t.row_of[q] = row;
+    t.phase[q] = (uint8_t)len;
+  }
+  __syncthreads();
+}
+
+template <bool SCORED>
+__global__ __launch_bounds__(kResolveThreads) void k_prefetch_fused(
+    const TierArgs t, const int32_t* __restrict__ tail, int32_t tail_len,
+    const int32_t* __restrict__ cand, uint32_t B, uint32_t K, const float* __restrict__ prob,
+    uint32_t budget) {
+  // The probe reads only the index and the candidates: it runs before the
+  // wait for the lookups that share the residency state.
+  prefetch_probe_block(t, tail, tail_len, cand, B, K);
+  wait_ordered_block(t);
+  if (SCORED)
+    (void)resolve_scored(t, B * K, prob, budget);
+  else
+    (void)resolve_one_block(t, B * K);
+}
+
+__global__ void k_tier_wait(const TierArgs t) { wait_ordered_block(t); }
 
 // Host row -> cache slot copies of the current fill list, one wave per job,
 // reading the pinned host rows directly over PCIe (zero-copy).
+// With t.count_fill each block then counts into ctl->pf_done once its
+// copies have reached memory (a lookup on another stream waits for it).
 template <int NCH>
 __global__ __launch_bounds__(256) void k_fill(const TierArgs t, uint32_t max_jobs) {
   const int lane = threadIdx.x & 63;
   const uint32_t j = blockIdx.x * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  if (j >= max_jobs || j >= t.ctl->njobs) return;
-  const TierJob job = t.jobs[j];
-  const u32x4* src = (const u32x4*)t.host_values + (size_t)job.row * (NCH * 64);
-  u32x4* dst = (u32x4*)t.cache + (size_t)job.slot * (NCH * 64);
-  u32x4 v[NCH];
+  if (j < max_jobs && j < t.ctl->njobs) {
+    const TierJob job = t.jobs[j];
+    const u32x4* src = (const u32x4*)t.host_values + (size_t)job.row * (NCH * 64);
+    u32x4* dst = (u32x4*)t.cache + (size_t)job.slot * (NCH * 64);
+    u32x4 v[NCH];
 #pragma unroll
-  for (int k = 0; k < NCH; ++k) v[k] = __builtin_nontemporal_load(src + k * 64 + lane);
+    for (int k = 0; k < NCH; ++k) v[k] = __builtin_nontemporal_load(src + k * 64 + lane);
 #pragma unroll
-  for (int k = 0; k < NCH; ++k) dst[k * 64 + lane] = v[k];
+    for (int k = 0; k < NCH; ++k) dst[k * 64 + lane] = v[k];
+  }
+  if (!t.count_fill) return;
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+  __syncthreads();
+  if (threadIdx.x == 0)
+    __hip_atomic_fetch_add(&t.ctl->pf_done, 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 // Probe of a tiered lookup: the resident kernel's key formation and probe,
@@ -1223,17 +1361,6 @@ __global__ __launch_bounds__(WPB * 64) void k_tier_inject(const TierArgs t) {
 // stores and loads, and each wave waits for its stores to complete before
 // it counts in; a device-scope fence would instead write back and
 // invalidate the whole L2 in every wave.
-
-// Device-scope (coherent across the XCDs' L2s) store and load.
-__device__ __forceinline__ void st_dev(int32_t* p, int32_t v) {
-  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ int32_t ld_dev(const int32_t* p) {
-  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-// Waits until every memory operation this wave issued has completed
-// (s_waitcnt vmcnt(0); the other counters left at their maximum).
-__device__ __forceinline__ void wait_mem() { __builtin_amdgcn_s_waitcnt(0x0F70); }
 
 constexpr int kWalkPer = 8;  // ring entries per lane and round of the victim walk
 
@@ -1407,6 +1534,9 @@ __device__ void decode_resolve_last(const TierArgs& t, uint32_t T, WalkWindow& w
     st.host_bytes += (unsigned long long)(nhit - nch) * t.row_bytes;
     t.ctl->arrive = 0;  // the next call starts counting from zero
   }
+  // The residency writes above reach memory before this wave counts as
+  // done (a prefetch on another stream reads them).
+  if (t.count_lookup) __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
 }
 
 // Publishes this wave's row and slot word, waits for its writes, and counts
@@ -1425,6 +1555,14 @@ __device__ __forceinline__ bool decode_arrive(const TierArgs& t, uint32_t p, int
   return __builtin_amdgcn_readfirstlane(last) != 0;
 }
 
+// A decode wave is done with the shared state (its row read, and for the
+// last wave its residency writes released): it counts into ctl->lk_done,
+// which a prefetch on another stream waits for.
+__device__ __forceinline__ void decode_done(const TierArgs& t) {
+  if (t.count_lookup && threadIdx.x == 0)
+    __hip_atomic_fetch_add(&t.ctl->lk_done, 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
 template <int DT, int NCH>
 __global__ __launch_bounds__(64) void k_tier_decode(const TierArgs t) {
   constexpr int ROW_VECS = NCH * 64;
@@ -1438,6 +1576,7 @@ __global__ __launch_bounds__(64) void k_tier_decode(const TierArgs t) {
   int32_t tw[4];
   dev::window_tokens(a, p, tw);
   const dev::Probe pr = dev::probe_begin(a, tw, lane);
+  wait_ordered_block(t);  // a prefetch on another stream, before any residency read
   WalkWindow win;
   win.tail = t.ctl->tail;
   win.head = t.ctl->head;
@@ -1451,6 +1590,7 @@ __global__ __launch_bounds__(64) void k_tier_decode(const TierArgs t) {
   u32x4* out = (u32x4*)a.hout + (size_t)p * ROW_VECS;
   if (row < 0) {
     if (decode_arrive(t, p, row, -1)) decode_resolve_last<NCH>(t, a.T, win);
+    decode_done(t);
     if (!a.inplace) {
 #pragma unroll
       for (int k = 0; k < NCH; ++k) dev::store_out(hv[k], out + k * 64 + lane);
@@ -1466,6 +1606,8 @@ __global__ __launch_bounds__(64) void k_tier_decode(const TierArgs t) {
     const u32x4* mrow = (const u32x4*)t.cache + (size_t)w * ROW_VECS;
 #pragma unroll
     for (int k = 0; k < NCH; ++k) mv[k] = mrow[k * 64 + lane];
+    if (t.count_lookup) wait_mem();  // the row is read before this wave counts as done
+    decode_done(t);
   } else {
     // Host only: the row is read once, written into this position's spare
     // slot (which no row maps to, so no wave reads it), and injected.
@@ -1476,6 +1618,7 @@ __global__ __launch_bounds__(64) void k_tier_decode(const TierArgs t) {
 #pragma unroll
     for (int k = 0; k < NCH; ++k) dst[k * 64 + lane] = mv[k];
     if (decode_arrive(t, p, row, -1)) decode_resolve_last<NCH>(t, a.T, win);
+    decode_done(t);
   }
   const float g = dev::gate_of<DT, NCH>(a, hv, mv);
   dev::store_injected<DT, NCH>(out, hv, mv, g, lane);
@@ -1628,6 +1771,28 @@ hipError_t launch_resolve_prefetch_scored(const TierArgs& t, uint32_t N, const f
 }
 
 uint32_t scored_prefetch_budget_max() { return kScoredBudgetMax; }
+
+uint32_t prefetch_fused_max() { return kPrefetchFusedMax; }
+
+hipError_t launch_prefetch_fused(const TierArgs& t, const int32_t* tail, int32_t tail_len,
+                                 const int32_t* cand, uint32_t B, uint32_t K, const float* prob,
+                                 uint32_t budget, hipStream_t s) {
+  if (B * K > kPrefetchFusedMax) return hipErrorInvalidValue;
+  if (prob)
+    hipLaunchKernelGGL(k_prefetch_fused<true>, dim3(1), dim3(kResolveThreads), 0, s, t, tail,
+                       tail_len, cand, B, K, prob, budget);
+  else
+    hipLaunchKernelGGL(k_prefetch_fused<false>, dim3(1), dim3(kResolveThreads), 0, s, t, tail,
+                       tail_len, cand, B, K, prob, budget);
+  return hipGetLastError();
+}
+
+hipError_t launch_tier_wait(const TierArgs& t, hipStream_t s) {
+  hipLaunchKernelGGL(k_tier_wait, dim3(1), dim3(64), 0, s, t);
+  return hipGetLastError();
+}
+
+uint32_t fill_blocks(uint32_t max_jobs) { return (max_jobs + 3) / 4; }
 
 hipError_t launch_residency(const int32_t* where, int64_t P, const int32_t* rows, int64_t n,
                             int32_t* out, hipStream_t s) {

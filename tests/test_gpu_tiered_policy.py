@@ -307,3 +307,64 @@ def test_head_topk_feeds_scored_prefetch_at_batch64_k128(w2, budget):
         assert st["prefetch_dropped"] > 0
     tier.close()
     tfe.tfe_head_free(head)
+
+
+@pytest.mark.parametrize("scored", [False, True])
+def test_decode_and_prefetch_overlapping_without_sync(w2, scored):
+    """Decode steps on the main stream and a prefetch of 8 candidates per
+    row on a side stream after each, 300 steps enqueued without any
+    synchronisation, so that each prefetch's probe overlaps the decode
+    before it and the next decode waits for the prefetch on the device.  A
+    2048-row cache makes victims and ring compactions frequent.  Every
+    step's output equals the resident table's; statistics and residency
+    equal the model at the end."""
+    table, res, ot = w2
+    C, pre, B, K, steps = 2048, 1024, 64, 8, 300
+    tier = TieredTable(table, C, pre)
+    model = LruModel(C, pre, 2048)
+    seqs = synth.zipf_tokens(1, 1300 + scored, B * (steps + 3), 1.1).reshape(B, steps + 3)
+    seqs_d = torch.from_numpy(seqs).cuda()
+    wins = [seqs_d[:, s:s + 3].contiguous() for s in range(steps)]
+    tails = [seqs_d[:, s + 1:s + 3].contiguous() for s in range(steps)]
+    cands = np.stack([synth.workloads.candidates(1, B, K, seqs[:, s + 3], step=500 + s)
+                      for s in range(steps)])
+    cands_d = torch.from_numpy(cands).cuda()
+    prob = torch.from_numpy(np.tile((np.float32(0.5) ** np.arange(K)).astype(np.float32),
+                                    (B, 1))).cuda()
+    hid = H.to_device(synth.normal_range(17, 0, 0, B * steps, 1024, 1.0, synth.BF16), synth.BF16)
+    out = torch.empty((steps, B, 1024), dtype=torch.bfloat16, device="cuda")
+    slots = torch.full((steps, B), -7, dtype=torch.int32, device="cuda")
+    hit = torch.zeros((steps, B), dtype=torch.uint8, device="cuda")
+    side = torch.cuda.Stream()
+    torch.cuda.synchronize()
+    for s in range(steps):
+        tfe.tfe_lookup_inject(tier.handle, wins[s], B, 2, 1, hid[s * B:(s + 1) * B], out[s],
+                              hit[s], slots[s], None, tfe.TFE_GATE_SIGMOID, 1.0, H.cur_stream())
+        if scored:
+            tfe.tfe_prefetch_scored(tier.handle, tails[s], 2, cands_d[s], prob, B, K, 48, side)
+        else:
+            tfe.tfe_prefetch(tier.handle, tails[s], 2, cands_d[s], B, K, side)
+    torch.cuda.synchronize()
+    # The same steps on the resident table.
+    o_res = H.Outputs(B * steps, 1024, synth.BF16)
+    win_all = np.ascontiguousarray(np.concatenate([seqs[:, s:s + 3] for s in range(steps)]))
+    H.run(res, torch.from_numpy(win_all).cuda(), B * steps, 2, 1, hid, o_res)
+    torch.cuda.synchronize()
+    assert torch.equal(o_res.slot, slots.view(-1))
+    assert torch.equal(o_res.out.view(torch.int16), out.view(-1, 1024).view(torch.int16))
+    # The model, call by call.
+    pk = (np.float32(0.5) ** np.arange(K)).astype(np.float32)
+    for s in range(steps):
+        _, row, _ = ot.lookup(np.ascontiguousarray(seqs[:, s:s + 3]), 2, 1)
+        model.lookup([int(r) for r in row])
+        win = np.concatenate([np.repeat(seqs[:, s + 1:s + 3], K, axis=0),
+                              cands[s].reshape(-1, 1)], axis=1)
+        _, crow, clen = ot.lookup(win, 2, 1)
+        if scored:
+            model.prefetch_scored([int(r) for r in crow], [int(x) for x in clen],
+                                  np.tile(pk, B), 48)
+        else:
+            model.prefetch([int(r) for r in crow])
+    check_stats(tier, model)
+    check_residency(tier, model, table.n_phrases)
+    tier.close()
