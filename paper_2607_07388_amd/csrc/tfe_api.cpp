@@ -175,11 +175,11 @@ static tfe::TierArgs tier_args(tfe_table* t) {
 }
 
 // Orders the kernels enqueued next on `s` after the counted work submitted
-// so far -- every one-launch decode wave (lk) and every one-block prefetch's
+// so far -- every one-launch decode call (lk) and every one-block prefetch's
 // copy blocks (pf) -- with one waiting wave.
 static tfe_status order_after_counted(tfe_table* t, hipStream_t s, bool lk, bool pf) {
   tfe::TierArgs a = tier_args(t);
-  a.wait_lk = lk ? t->waves_issued : 0;
+  a.wait_lk = lk ? t->decodes_issued : 0;
   a.wait_pf = pf ? t->fills_issued : 0;
   if (!a.wait_lk && !a.wait_pf) return TFE_OK;
   TFE_HIP(tfe::launch_tier_wait(a, s), "ordering wait");
@@ -413,10 +413,12 @@ static tfe_status lookup_tiered(tfe_table* t, const LookupArgs& look, hipStream_
   if (decode) {
     // The whole call in one launch (probe, inject, residency).
     a.wait_pf = pf_kernel ? t->fills_issued : 0;
-    a.count_lookup = 1;
+    // Counting (a release of the residency writes and one addition) is only
+    // needed once prefetches follow decodes on this table.
+    a.count_lookup = t->counting ? 1u : 0u;
     TFE_HIP(tfe::launch_tier_decode(a, t->dtype, t->dim, stream), "tiered decode");
-    t->waves_issued += look.T;
-    t->last_lookup_counted = true;
+    if (t->counting) t->decodes_issued += 1;
+    t->last_lookup_counted = t->counting;
     t->lookup_recorded = true;
     t->last_stream = stream;
     return TFE_OK;
@@ -453,6 +455,7 @@ static tfe_status prefetch_tiered(tfe_table* t, const int32_t* tail, int32_t tai
   TFE_TRY(check_device(t));
   TFE_TRY(refuse_capture(side, "a prefetch"));
   const bool one_block = N <= tfe::prefetch_fused_max();
+  t->counting = true;  // later decodes count themselves for the prefetches
   // The one-block prefetch keeps one probe result per (candidate, length)
   // in its scratch; the scored resolution uses the call-wide row table of
   // the lookups' scratch (never run by two calls at once).
@@ -487,7 +490,7 @@ static tfe_status prefetch_tiered(tfe_table* t, const int32_t* tail, int32_t tai
   if (one_block) {
     // The probe runs before this wait: it touches only the index, the
     // candidates and the prefetch scratch.
-    a.wait_lk = lk ? t->waves_issued : 0;
+    a.wait_lk = lk ? t->decodes_issued : 0;
     TFE_HIP(tfe::launch_prefetch_fused(a, tail, tail_len, cand, (uint32_t)B, (uint32_t)K, prob,
                                        (uint32_t)budget, side),
             "prefetch");

@@ -70,7 +70,7 @@ struct TierCtl {
   unsigned int arrive;            // one-launch decode: waves done with their position
   unsigned int wait_timeouts;     // device-side ordering waits that hit their bound
   // Device-side ordering of decode lookups and prefetches (no HIP events):
-  unsigned long long lk_done;     // decode waves done with the shared state (monotone)
+  unsigned long long lk_done;     // decode calls done with the shared state (monotone)
   unsigned long long pf_done;     // prefetch copy blocks done (monotone)
   TierStats stats;
 };
@@ -106,7 +106,7 @@ struct TierArgs {
                               // prefetched; prefetch counters instead of lookup counters)
   // Device-side ordering: wait until ctl->lk_done >= wait_lk and ctl->pf_done
   // >= wait_pf before touching the shared state (0: no wait); count_* make
-  // the decode waves and the copy blocks count themselves in when done.
+  // a decode call and the copy blocks count themselves in when done.
   unsigned long long wait_lk, wait_pf;
   uint32_t count_lookup, count_fill;
 };
@@ -223,9 +223,10 @@ struct tfe_table {
   // Device-side ordering of one-launch decode lookups and one-block
   // prefetches: totals submitted, compared by the kernels with ctl->lk_done
   // and ctl->pf_done.
-  uint64_t waves_issued = 0;     // decode waves submitted
+  uint64_t decodes_issued = 0;   // one-launch decode calls submitted
   uint64_t fills_issued = 0;     // counted prefetch copy blocks submitted
   bool last_lookup_counted = false;  // the last lookup was a counted decode
+  bool counting = false;             // decodes count themselves (from the first prefetch on)
   bool pf_counted_pending = false;   // a counted prefetch may still run
   hipStream_t pf_stream = nullptr;   // stream of the last counted prefetch
 };

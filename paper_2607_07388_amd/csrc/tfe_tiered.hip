@@ -989,21 +989,48 @@ __device__ __forceinline__ uint64_t gh_find(const TierArgs& t, int32_t r) {
 
 // Returns the number of rows filled (block-uniform); the fill list is
 // jobs[0 .. filled).
+// LDS: the row table of calls of at most kScoredLdsMax candidates (the
+// one-block prefetch) lives in LDS, with the key list; larger calls use the
+// call-wide table in the scratch (fewer LDS bytes, atomics through L2).
+constexpr uint32_t kScoredLdsMax = kGroup;
+constexpr int kScoredLdsHash = 2 * kScoredLdsMax;
+
+template <bool LDS>
 __device__ uint32_t resolve_scored(const TierArgs& t, uint32_t N, const float* __restrict__ prob,
                                    uint32_t budget) {
   __shared__ unsigned long long sel[kScoredBudgetMax];
   __shared__ uint32_t vict[kResolveThreads];
   __shared__ uint32_t hist[256];
   __shared__ uint32_t s_found, s_nref, s_n, s_g, s_bin, s_before;
+  // LDS row table: row, first candidate index (minimum), best score bits
+  // (maximum); and the key list.
+  __shared__ int32_t lkey[LDS ? kScoredLdsHash : 1];
+  __shared__ uint32_t lpos[LDS ? kScoredLdsHash : 1];
+  __shared__ uint32_t lsc[LDS ? kScoredLdsHash : 1];
+  __shared__ unsigned long long lklist[LDS ? kScoredLdsMax : 1];
   const uint64_t tag = (uint64_t)t.clock << 32;
-  uint64_t* klist = (uint64_t*)t.jobs;  // rows to fetch; becomes the fill list in step 4
+  // Rows to fetch; in the scratch version it becomes the fill list in step 4.
+  uint64_t* klist = LDS ? (uint64_t*)lklist : (uint64_t*)t.jobs;
   if (threadIdx.x == 0) {
     s_found = 0;
     s_nref = 0;
     s_n = 0;
     s_g = 0;
   }
+  if (LDS) {
+    for (int i = threadIdx.x; i < kScoredLdsHash; i += kResolveThreads) {
+      lkey[i] = -1;
+      lpos[i] = 0xFFFFFFFFu;
+      lsc[i] = 0;
+    }
+  }
   __syncthreads();
+  constexpr int lshift = 32 - __builtin_ctz(kScoredLdsHash);
+  auto lfind = [&](int32_t r) {
+    int h = (int)(((uint32_t)r * 2654435761u) >> lshift);
+    while (lkey[h] != r) h = (h + 1) & (kScoredLdsHash - 1);
+    return h;
+  };
   // 1. Row table: first candidate index and best score per row.
   for (uint32_t base = 0; base < N; base += kResolveThreads) {
     const uint32_t q = base + threadIdx.x;
@@ -1011,12 +1038,24 @@ __device__ uint32_t resolve_scored(const TierArgs& t, uint32_t N, const float* _
     if (r >= 0) {
       const float p = prob[q];
       const float sc = (p > 0.0f ? p : 0.0f) * (float)t.phase[q];  // NaN and p <= 0 score 0
-      const uint64_t h = gh_insert_at(t, r, q);
-      atomicMax((unsigned long long*)(t.hval + h), (unsigned long long)(tag | __float_as_uint(sc)));
+      if (LDS) {
+        int h = (int)(((uint32_t)r * 2654435761u) >> lshift);
+        for (;;) {
+          const int old = atomicCAS(&lkey[h], -1, r);
+          if (old == -1 || old == r) break;
+          h = (h + 1) & (kScoredLdsHash - 1);
+        }
+        atomicMin(&lpos[h], q);
+        atomicMax(&lsc[h], __float_as_uint(sc));
+      } else {
+        const uint64_t h = gh_insert_at(t, r, q);
+        atomicMax((unsigned long long*)(t.hval + h),
+                  (unsigned long long)(tag | __float_as_uint(sc)));
+      }
     }
     wave_tally(r >= 0, &s_found);
   }
-  __threadfence();  // the row table's atomics have completed before any wave reads it
+  if (!LDS) __threadfence();  // the row table's atomics have completed before any wave reads it
   __syncthreads();
   const unsigned long long head0 = t.ctl->head;
   // 2. References and the key list, in candidate order.
@@ -1027,9 +1066,17 @@ __device__ uint32_t resolve_scored(const TierArgs& t, uint32_t N, const float* _
     int32_t w = -1;
     uint32_t sc = 0;
     if (r >= 0) {
-      const uint64_t h = gh_find(t, r);
-      if (gh_load(t.hpos + h) == (tag | (uint32_t)~q)) {
-        sc = (uint32_t)gh_load(t.hval + h);
+      bool first;
+      if (LDS) {
+        const int h = lfind(r);
+        first = lpos[h] == q;
+        sc = lsc[h];
+      } else {
+        const uint64_t h = gh_find(t, r);
+        first = gh_load(t.hpos + h) == (tag | (uint32_t)~q);
+        if (first) sc = (uint32_t)gh_load(t.hval + h);
+      }
+      if (first) {
         w = t.where[r];
         ref = sc != 0 && w >= 0;
         cand = sc != 0 && w < 0;
@@ -1157,7 +1204,7 @@ __device__ uint32_t resolve_scored(const TierArgs& t, uint32_t N, const float* _
 
 __global__ __launch_bounds__(kResolveThreads) void k_resolve_prefetch_scored(
     const TierArgs t, uint32_t N, const float* __restrict__ prob, uint32_t budget) {
-  (void)resolve_scored(t, N, prob, budget);
+  (void)resolve_scored<false>(t, N, prob, budget);
 }
 
 // ---- Prefetch of up to kPrefetchFusedMax candidates in two launches: one
@@ -1221,7 +1268,7 @@ __global__ __launch_bounds__(kResolveThreads) void k_prefetch_fused(
   prefetch_probe_block(t, tail, tail_len, cand, B, K);
   wait_ordered_block(t);
   if (SCORED)
-    (void)resolve_scored(t, B * K, prob, budget);
+    (void)resolve_scored<true>(t, B * K, prob, budget);
   else
     (void)resolve_one_block(t, B * K);
 }
@@ -1349,7 +1396,8 @@ __global__ __launch_bounds__(WPB * 64) void k_tier_inject(const TierArgs t) {
 //   no row maps to and the recency order does not hold.  This is safe
 //   before any residency decision: victims are never slots that the call
 //   references, so nothing a wave reads changes during the call.
-//   Each wave publishes its row and slot and counts itself in; the last
+//   Each wave publishes its row and slot and counts itself in (a wave that
+//   reads a cached row reads it first); the last
 //   wave to arrive resolves residency for the whole call with the policy of
 //   k_resolve_lookup: first positions of rows (lane q = position q), cached
 //   rows referenced, victims for the missed rows from the tail of the
@@ -1534,9 +1582,15 @@ __device__ void decode_resolve_last(const TierArgs& t, uint32_t T, WalkWindow& w
     st.host_bytes += (unsigned long long)(nhit - nch) * t.row_bytes;
     t.ctl->arrive = 0;  // the next call starts counting from zero
   }
-  // The residency writes above reach memory before this wave counts as
-  // done (a prefetch on another stream reads them).
-  if (t.count_lookup) __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+  // Every wave of the call has read what it needed before counting in, so
+  // the call is done with the shared state once the residency writes above
+  // reach memory: it counts into ctl->lk_done, which a prefetch on another
+  // stream waits for.
+  if (t.count_lookup) {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+    if (lane == 0)
+      __hip_atomic_fetch_add(&t.ctl->lk_done, 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
 }
 
 // Publishes this wave's row and slot word, waits for its writes, and counts
@@ -1553,14 +1607,6 @@ __device__ __forceinline__ bool decode_arrive(const TierArgs& t, uint32_t p, int
     last = __hip_atomic_fetch_add(&t.ctl->arrive, 1u, __ATOMIC_RELAXED,
                                   __HIP_MEMORY_SCOPE_AGENT) == t.look.T - 1 ? 1u : 0u;
   return __builtin_amdgcn_readfirstlane(last) != 0;
-}
-
-// A decode wave is done with the shared state (its row read, and for the
-// last wave its residency writes released): it counts into ctl->lk_done,
-// which a prefetch on another stream waits for.
-__device__ __forceinline__ void decode_done(const TierArgs& t) {
-  if (t.count_lookup && threadIdx.x == 0)
-    __hip_atomic_fetch_add(&t.ctl->lk_done, 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 template <int DT, int NCH>
@@ -1590,7 +1636,6 @@ __global__ __launch_bounds__(64) void k_tier_decode(const TierArgs t) {
   u32x4* out = (u32x4*)a.hout + (size_t)p * ROW_VECS;
   if (row < 0) {
     if (decode_arrive(t, p, row, -1)) decode_resolve_last<NCH>(t, a.T, win);
-    decode_done(t);
     if (!a.inplace) {
 #pragma unroll
       for (int k = 0; k < NCH; ++k) dev::store_out(hv[k], out + k * 64 + lane);
@@ -1599,15 +1644,14 @@ __global__ __launch_bounds__(64) void k_tier_decode(const TierArgs t) {
   }
   u32x4 mv[NCH];
   if (w >= 0) {
-    // Cached: count in first (with the slot's prefetched flag), then read
-    // the row; the last wave never writes a slot this call uses.
+    // Cached: the row is read before this wave counts in (with the slot's
+    // prefetched flag), so once the last wave has arrived no wave of the
+    // call reads the cache any more.
     const int32_t sw = t.pref[w] ? (w | kSlotPref) : w;
-    if (decode_arrive(t, p, row, sw)) decode_resolve_last<NCH>(t, a.T, win);
     const u32x4* mrow = (const u32x4*)t.cache + (size_t)w * ROW_VECS;
 #pragma unroll
     for (int k = 0; k < NCH; ++k) mv[k] = mrow[k * 64 + lane];
-    if (t.count_lookup) wait_mem();  // the row is read before this wave counts as done
-    decode_done(t);
+    if (decode_arrive(t, p, row, sw)) decode_resolve_last<NCH>(t, a.T, win);
   } else {
     // Host only: the row is read once, written into this position's spare
     // slot (which no row maps to, so no wave reads it), and injected.
@@ -1618,7 +1662,6 @@ __global__ __launch_bounds__(64) void k_tier_decode(const TierArgs t) {
 #pragma unroll
     for (int k = 0; k < NCH; ++k) dst[k * 64 + lane] = mv[k];
     if (decode_arrive(t, p, row, -1)) decode_resolve_last<NCH>(t, a.T, win);
-    decode_done(t);
   }
   const float g = dev::gate_of<DT, NCH>(a, hv, mv);
   dev::store_injected<DT, NCH>(out, hv, mv, g, lane);
