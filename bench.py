@@ -65,8 +65,8 @@ HBM_PEAK_GBPS = 8000.0
 # profiles/k_lookup_inject_bf16_d1024_decode_stacked16384.md.  Reported only
 # while the kernel sources still hash to the profiled version.
 PROFILED_TRAFFIC = {
-    "sources_sha256": "85e96ab3378fbbc70b437c2db574c88a0a23360f5bb9d24b5668690f5556743f",
-    "bytes_per_launch": 93388276,
+    "sources_sha256": "4fece8a7d469ff90d4cf9bddfb427eed004d59f96cac15bc45f4826f406b2d78",
+    "bytes_per_launch": 93801562,
 }
 KERNEL_SOURCES = ("paper_2607_07388_amd/csrc/tfe_lookup.hip",
                   "paper_2607_07388_amd/csrc/tfe_device.h",
@@ -76,8 +76,8 @@ KERNEL_SOURCES = ("paper_2607_07388_amd/csrc/tfe_lookup.hip",
 # The same for the multi-match kernel in the same 16384-row launch, from the
 # passes in profiles/k_lookup_inject_multi_bf16_d1024_decode_stacked16384.md.
 PROFILED_TRAFFIC_MULTI = {
-    "sources_sha256": "d3c3784baa6b25ccf44ae283ae97ac1f6a44818186dc69958aaca186a3c7a113",
-    "bytes_per_launch": 98456716,
+    "sources_sha256": "ced797b78d255db95b6544bf97d341421fb20e2f6f63030710ecac13e1354c45",
+    "bytes_per_launch": 98836857,
 }
 MULTI_SOURCES = ("paper_2607_07388_amd/csrc/tfe_multi.hip",
                  "paper_2607_07388_amd/csrc/tfe_device.h",

@@ -26,6 +26,14 @@
  *   - Argument errors are detected on the host before anything is enqueued and
  *     return a negative status; tfe_last_error() then describes the problem.
  *     A failed HIP call returns TFE_ERR_HIP.  No C++ exception crosses the ABI.
+ *   - A failed allocation returns TFE_ERR_OOM and leaks nothing: a failed
+ *     load or head creation returns no handle and holds no memory; a lookup
+ *     or prefetch that fails leaves the table usable, and its results and
+ *     statistics as if the call had not been made (a scratch buffer grown
+ *     before the failure stays with the table, as a successful call's
+ *     would).  For tests of these paths, TFE_FAIL_ALLOC=k in the environment
+ *     makes the k-th device, pinned-host or host allocation of every library
+ *     call fail (the count restarts at each call).
  *   - A table handle is not thread-safe: calls on one handle must be issued
  *     from one host thread at a time.
  *   - HIP graph capture: lookups on resident tables (tfe_lookup_inject,
@@ -113,7 +121,7 @@ typedef struct {
 } tfe_table_desc;
 
 typedef struct {
-  uint64_t calls;            /* tfe_lookup_inject calls */
+  uint64_t calls;            /* tfe_lookup_inject(_multi) calls that returned TFE_OK */
   uint64_t positions;        /* injected positions looked up */
   uint64_t hits;             /* positions with a match (multi-match: any length) */
   uint64_t cache_hits;       /* tiered: matched rows found in the HBM cache */
@@ -334,6 +342,12 @@ tfe_status tfe_residency(const tfe_table *table, const int32_t *rows, int64_t n,
 
 /* Message describing the last error returned on this host thread ("" if none). */
 const char *tfe_last_error(void);
+
+/* Device and pinned host bytes the library holds right now, over every
+ * table, head and construction buffer of the process (either pointer may be
+ * NULL, not both).  Returns to its earlier value once what was loaded or
+ * created since is freed (and tfe_ngram_release has run).  No GPU needed. */
+tfe_status tfe_memory_held(int64_t *device_bytes, int64_t *pinned_bytes);
 
 /* ---- Host-only index utilities (no GPU needed) ----------------------------
  * The index is an open-addressing table of 16-byte slots grouped in buckets

@@ -26,9 +26,12 @@ _lib = None
 def lib():
     global _lib
     if _lib is None:
-        if not os.path.exists(_build.SO):
+        # ORACLE_SO names another build of the same sources (the sanitizer
+        # tests load an instrumented one).
+        so = os.environ.get("ORACLE_SO") or _build.SO
+        if not os.path.exists(so):
             _build.build()
-        L = ctypes.CDLL(_build.SO)
+        L = ctypes.CDLL(so)
         vp, i64 = ctypes.c_void_p, ctypes.c_int64
         L.oracle_table_new.argtypes = [vp, vp, i64, ctypes.c_int, ctypes.c_int, ctypes.c_int,
                                        ctypes.POINTER(ctypes.c_int)]

@@ -16,17 +16,43 @@
 
 namespace tfe {
 
-static thread_local char g_err[512] = "";
-
-tfe_status fail(tfe_status st, const char* fmt, ...) {
-  va_list ap;
-  va_start(ap, fmt);
-  vsnprintf(g_err, sizeof g_err, fmt, ap);
-  va_end(ap);
-  return st;
+hipError_t dev_malloc(void** p, size_t n) {
+  *p = nullptr;
+  if (alloc_fails()) return hipErrorOutOfMemory;
+  const hipError_t e = hipMalloc(p, n);
+  if (e != hipSuccess) {
+    *p = nullptr;
+    (void)hipGetLastError();
+    return e;
+  }
+  note_alloc(*p, n, false);
+  return hipSuccess;
 }
 
-void clear_error() { g_err[0] = 0; }
+void dev_free(void* p) {
+  if (!p) return;
+  note_free(p);
+  (void)hipFree(p);
+}
+
+hipError_t pinned_malloc(void** p, size_t n) {
+  *p = nullptr;
+  if (alloc_fails()) return hipErrorOutOfMemory;
+  const hipError_t e = hipHostMalloc(p, n, hipHostMallocDefault);
+  if (e != hipSuccess) {
+    *p = nullptr;
+    (void)hipGetLastError();
+    return e;
+  }
+  note_alloc(*p, n, true);
+  return hipSuccess;
+}
+
+void pinned_free(void* p) {
+  if (!p) return;
+  note_free(p);
+  (void)hipHostFree(p);
+}
 
 tfe_status refuse_capture(hipStream_t stream, const char* what) {
   hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
@@ -90,8 +116,8 @@ static void release(tfe_table* t) {
                       t->d_slot_of, t->d_phase, t->d_jobs, t->d_hit_ctr, t->d_hkey, t->d_hpos, t->d_hval, t->d_blk, t->d_spare, t->d_pf_row_of,
                       t->d_pf_slot_of, t->d_pf_phase, t->d_pf_jobs};
   for (void* b : dev_bufs)
-    if (b) (void)hipFree(b);
-  if (t->own_h_values && t->h_values) (void)hipHostFree(t->h_values);
+    dev_free(b);
+  if (t->own_h_values && t->h_values) pinned_free(t->h_values);
   if (t->own_stream) (void)hipStreamDestroy(t->own_stream);
   hipEvent_t evs[] = {t->ev_resolved, t->ev_filled, t->ev_lookup, t->ev_prefetch};
   for (hipEvent_t e : evs)
@@ -111,7 +137,7 @@ static tfe_status check_device(const tfe_table* t) {
 
 static tfe_status load_resident(tfe_table* t, const tfe_table_desc* d, hipStream_t stream) {
   const size_t ctr_bytes = (size_t)kHitCounters * kHitStride * sizeof(unsigned long long);
-  if (hipMalloc((void**)&t->d_hit_ctr, ctr_bytes) != hipSuccess) {
+  if (dev_malloc((void**)&t->d_hit_ctr, ctr_bytes) != hipSuccess) {
     t->d_hit_ctr = nullptr;
     return fail(TFE_ERR_OOM, "hit counters (%zu bytes)", ctr_bytes);
   }
@@ -119,7 +145,7 @@ static tfe_status load_resident(tfe_table* t, const tfe_table_desc* d, hipStream
   TFE_HIP(hipStreamSynchronize(stream), "hit counters");
   if (d->n_phrases == 0) return TFE_OK;
   const size_t vbytes = (size_t)d->n_phrases * d->dim * elem_size(d->dtype);
-  if (hipMalloc(&t->d_values, vbytes) != hipSuccess)
+  if (dev_malloc(&t->d_values, vbytes) != hipSuccess)
     return fail(TFE_ERR_OOM, "device values (%zu bytes)", vbytes);
   TFE_HIP(hipMemcpyAsync(t->d_values, d->values, vbytes,
                          d->values_on_device ? hipMemcpyDeviceToDevice : hipMemcpyHostToDevice,
@@ -131,7 +157,7 @@ static tfe_status load_resident(tfe_table* t, const tfe_table_desc* d, hipStream
 
 template <class T>
 static tfe_status dev_alloc(T** p, size_t n, const char* what) {
-  if (hipMalloc((void**)p, n * sizeof(T) + (n == 0)) != hipSuccess)
+  if (dev_malloc((void**)p, n * sizeof(T) + (n == 0)) != hipSuccess)
     return fail(TFE_ERR_OOM, "%s (%zu bytes)", what, n * sizeof(T));
   return TFE_OK;
 }
@@ -209,7 +235,7 @@ static tfe_status load_tiered(tfe_table* t, const tfe_table_desc* d, hipStream_t
       return fail(TFE_ERR_INVALID_ARG, "adopted values are not pinned host memory (hipHostMalloc)");
     t->h_values = const_cast<void*>(d->values);
   } else if (P > 0) {
-    if (hipHostMalloc(&t->h_values, (size_t)P * row_bytes, hipHostMallocDefault) != hipSuccess) {
+    if (pinned_malloc(&t->h_values, (size_t)P * row_bytes) != hipSuccess) {
       t->h_values = nullptr;
       return fail(TFE_ERR_OOM, "pinned host values (%zu bytes)", (size_t)P * row_bytes);
     }
@@ -257,29 +283,45 @@ static tfe_status load_tiered(tfe_table* t, const tfe_table_desc* d, hipStream_t
   return TFE_OK;
 }
 
-// Grows the per-call scratch (rows, slots, phases, fill jobs) to n entries,
-// after the table's pending work that may still use the old buffers.
+// Grows the per-call scratch (rows, slots, phases, fill jobs, the call-wide
+// row table) to n entries.  The new buffers are allocated first: if one
+// fails, the others are returned and the table keeps its old scratch.  The
+// old buffers are freed after the table's pending work that may still use
+// them.
 static tfe_status ensure_scratch(tfe_table* t, uint32_t n) {
   if (n <= t->scratch_cap) return TFE_OK;
-  TFE_TRY(sync_table(t));
+  const uint64_t cap = pow2_at_least(n < 1024 ? 1024 : n);
+  int32_t *row_of = nullptr, *slot_of = nullptr;
+  uint8_t* phase = nullptr;
+  tfe::TierJob* jobs = nullptr;
+  uint64_t *hkey = nullptr, *hpos = nullptr, *hval = nullptr;
+  uint64_t* blk = nullptr;
+  tfe_status st = TFE_OK;
+  if ((st = dev_alloc(&row_of, cap, "scratch")) == TFE_OK &&
+      (st = dev_alloc(&slot_of, cap, "scratch")) == TFE_OK &&
+      (st = dev_alloc(&phase, cap, "scratch")) == TFE_OK &&
+      (st = dev_alloc(&jobs, cap, "scratch")) == TFE_OK &&
+      (st = dev_alloc(&hkey, 2 * cap, "scratch")) == TFE_OK &&
+      (st = dev_alloc(&hpos, 2 * cap, "scratch")) == TFE_OK &&
+      (st = dev_alloc(&hval, 2 * cap, "scratch")) == TFE_OK)
+    st = dev_alloc(&blk, cap / 1024 + 1, "scratch");
+  void* fresh[] = {row_of, slot_of, phase, jobs, hkey, hpos, hval, blk};
+  if (st == TFE_OK) st = sync_table(t);
+  if (st != TFE_OK) {
+    for (void* b : fresh) dev_free(b);
+    return st;
+  }
   void* olds[] = {t->d_row_of, t->d_slot_of, t->d_phase, t->d_jobs, t->d_hkey, t->d_hpos,
                   t->d_hval, t->d_blk};
-  for (void* b : olds)
-    if (b) (void)hipFree(b);
-  t->d_row_of = t->d_slot_of = nullptr;
-  t->d_phase = nullptr;
-  t->d_jobs = nullptr;
-  t->d_hkey = t->d_hpos = t->d_hval = t->d_blk = nullptr;
-  t->scratch_cap = 0;
-  const uint64_t cap = pow2_at_least(n < 1024 ? 1024 : n);
-  TFE_TRY(dev_alloc(&t->d_row_of, cap, "scratch"));
-  TFE_TRY(dev_alloc(&t->d_slot_of, cap, "scratch"));
-  TFE_TRY(dev_alloc(&t->d_phase, cap, "scratch"));
-  TFE_TRY(dev_alloc(&t->d_jobs, cap, "scratch"));
-  TFE_TRY(dev_alloc(&t->d_hkey, 2 * cap, "scratch"));
-  TFE_TRY(dev_alloc(&t->d_hpos, 2 * cap, "scratch"));
-  TFE_TRY(dev_alloc(&t->d_hval, 2 * cap, "scratch"));
-  TFE_TRY(dev_alloc(&t->d_blk, cap / 1024 + 1, "scratch"));
+  for (void* b : olds) dev_free(b);
+  t->d_row_of = row_of;
+  t->d_slot_of = slot_of;
+  t->d_phase = phase;
+  t->d_jobs = jobs;
+  t->d_hkey = hkey;
+  t->d_hpos = hpos;
+  t->d_hval = hval;
+  t->d_blk = blk;
   // Clock 0 tags every entry of the call-wide row table as empty (calls use
   // clocks from 1).
   TFE_HIP(hipMemsetAsync(t->d_hkey, 0, 2 * cap * sizeof(uint64_t), t->own_stream), "scratch");
@@ -290,23 +332,30 @@ static tfe_status ensure_scratch(tfe_table* t, uint32_t n) {
   return TFE_OK;
 }
 
-// Grows the prefetches' own per-call scratch to n entries, after the
-// table's pending work that may still use the old buffers.
+// Grows the prefetches' own per-call scratch to n entries, in the same way.
 static tfe_status ensure_pf_scratch(tfe_table* t, uint64_t n) {
   if (n <= t->pf_cap) return TFE_OK;
-  TFE_TRY(sync_table(t));
-  void* olds[] = {t->d_pf_row_of, t->d_pf_slot_of, t->d_pf_phase, t->d_pf_jobs};
-  for (void* b : olds)
-    if (b) (void)hipFree(b);
-  t->d_pf_row_of = t->d_pf_slot_of = nullptr;
-  t->d_pf_phase = nullptr;
-  t->d_pf_jobs = nullptr;
-  t->pf_cap = 0;
   const uint64_t cap = pow2_at_least(n < 1024 ? 1024 : n);
-  TFE_TRY(dev_alloc(&t->d_pf_row_of, cap, "prefetch scratch"));
-  TFE_TRY(dev_alloc(&t->d_pf_slot_of, cap, "prefetch scratch"));
-  TFE_TRY(dev_alloc(&t->d_pf_phase, cap, "prefetch scratch"));
-  TFE_TRY(dev_alloc(&t->d_pf_jobs, cap, "prefetch scratch"));
+  int32_t *row_of = nullptr, *slot_of = nullptr;
+  uint8_t* phase = nullptr;
+  tfe::TierJob* jobs = nullptr;
+  tfe_status st = TFE_OK;
+  if ((st = dev_alloc(&row_of, cap, "prefetch scratch")) == TFE_OK &&
+      (st = dev_alloc(&slot_of, cap, "prefetch scratch")) == TFE_OK &&
+      (st = dev_alloc(&phase, cap, "prefetch scratch")) == TFE_OK)
+    st = dev_alloc(&jobs, cap, "prefetch scratch");
+  void* fresh[] = {row_of, slot_of, phase, jobs};
+  if (st == TFE_OK) st = sync_table(t);
+  if (st != TFE_OK) {
+    for (void* b : fresh) dev_free(b);
+    return st;
+  }
+  void* olds[] = {t->d_pf_row_of, t->d_pf_slot_of, t->d_pf_phase, t->d_pf_jobs};
+  for (void* b : olds) dev_free(b);
+  t->d_pf_row_of = row_of;
+  t->d_pf_slot_of = slot_of;
+  t->d_pf_phase = phase;
+  t->d_pf_jobs = jobs;
   t->pf_cap = (uint32_t)cap;
   return TFE_OK;
 }
@@ -331,13 +380,13 @@ static tfe_status reserve_ring(tfe_table* t, uint64_t appends, hipStream_t strea
     uint64_t *r1 = nullptr, *r2 = nullptr;
     TFE_TRY(dev_alloc(&r1, cap, "recency ring"));
     if (dev_alloc(&r2, cap, "recency ring") != TFE_OK) {
-      (void)hipFree(r1);
+      dev_free(r1);
       return TFE_ERR_OOM;
     }
     TFE_HIP(tfe::launch_ring_compact(a, r1, cap - 1, false, stream), "ring compaction");
     TFE_HIP(hipStreamSynchronize(stream), "ring regrow");
-    (void)hipFree(t->d_ring);
-    (void)hipFree(t->d_ring2);
+    dev_free(t->d_ring);
+    dev_free(t->d_ring2);
     t->d_ring = r1;
     t->d_ring2 = r2;
     t->ring_cap = cap;
@@ -393,10 +442,8 @@ static tfe_status lookup_tiered(tfe_table* t, const LookupArgs& look, hipStream_
   // the same per-call scratch (matched rows, fill list), the recency ring
   // and the residency state as everything below, so every kernel of this
   // call -- ring compaction and the probe included -- waits for them.
-  if (t->prefetch_pending) {
-    TFE_HIP(hipStreamWaitEvent(stream, t->ev_prefetch, 0), "wait prefetch");
-    t->prefetch_pending = false;
-  }
+  // (The pending flag is cleared once this call has been enqueued.)
+  if (t->prefetch_pending) TFE_HIP(hipStreamWaitEvent(stream, t->ev_prefetch, 0), "wait prefetch");
   if (t->fill_recorded) TFE_HIP(hipStreamWaitEvent(stream, t->ev_filled, 0), "wait fill");
   // A one-block prefetch on another stream is followed without HIP events:
   // the one-launch decode waits for its copy blocks itself; any other
@@ -407,7 +454,9 @@ static tfe_status lookup_tiered(tfe_table* t, const LookupArgs& look, hipStream_
   const bool pf_kernel = pf && decode;  // still to be awaited by the decode kernel
   TFE_TRY(reserve_ring(t, look.T, stream, false, pf_kernel));
   TFE_TRY(advance_clock(t, look.T, stream, false, pf_kernel));
-  t->pf_counted_pending = false;  // everything after this call follows it
+  // Everything after this call follows it, and through it the prefetches.
+  t->pf_counted_pending = false;
+  t->prefetch_pending = false;
   tfe::TierArgs a = tier_args(t);
   a.look = look;
   if (decode) {
@@ -455,12 +504,12 @@ static tfe_status prefetch_tiered(tfe_table* t, const int32_t* tail, int32_t tai
   TFE_TRY(check_device(t));
   TFE_TRY(refuse_capture(side, "a prefetch"));
   const bool one_block = N <= tfe::prefetch_fused_max();
-  t->counting = true;  // later decodes count themselves for the prefetches
   // The one-block prefetch keeps one probe result per (candidate, length)
   // in its scratch; the scored resolution uses the call-wide row table of
   // the lookups' scratch (never run by two calls at once).
   TFE_TRY(ensure_pf_scratch(t, one_block ? N * (uint64_t)(t->n_max - t->n_min + 1) : N));
   TFE_TRY(ensure_scratch(t, (uint32_t)N));
+  t->counting = true;  // later decodes count themselves for the prefetches
   // After the table's last lookup, its cache fill, and any earlier
   // prefetch.  A one-launch decode lookup and a one-block prefetch are
   // followed on the device (counters in the control block) instead of with
@@ -472,8 +521,9 @@ static tfe_status prefetch_tiered(tfe_table* t, const int32_t* tail, int32_t tai
     TFE_HIP(hipStreamWaitEvent(side, t->ev_lookup, 0), "wait lookup");
   }
   if (t->fill_recorded) TFE_HIP(hipStreamWaitEvent(side, t->ev_filled, 0), "wait fill");
+  // (The pending flag is cleared once this call has been enqueued: if it
+  // fails on the way, later calls still wait for the earlier prefetch.)
   if (t->prefetch_pending) TFE_HIP(hipStreamWaitEvent(side, t->ev_prefetch, 0), "wait prefetch");
-  t->prefetch_pending = false;
   // A counted prefetch on another stream shares this one's scratch: this
   // whole call (its probe too) waits for it.
   const bool pf = t->pf_counted_pending && side != t->pf_stream;
@@ -498,6 +548,7 @@ static tfe_status prefetch_tiered(tfe_table* t, const int32_t* tail, int32_t tai
     a.count_fill = 1;
     TFE_HIP(tfe::launch_fill(a, t->dtype, t->dim, (uint32_t)N, side), "prefetch fill");
     t->fills_issued += tfe::fill_blocks((uint32_t)N);
+    t->prefetch_pending = false;
     t->pf_counted_pending = true;
     t->pf_stream = side;
     return TFE_OK;
@@ -545,6 +596,7 @@ static tfe_status load(const tfe_table_desc* d, hipStream_t stream, tfe_table** 
   const int64_t cap = index_capacity(d->n_phrases, lf);
   std::vector<tfe_slot> slots;
   try {
+    if (alloc_fails()) throw std::bad_alloc();
     slots.resize((size_t)cap);
   } catch (const std::bad_alloc&) {
     return fail(TFE_ERR_OOM, "host index of %lld slots", (long long)cap);
@@ -552,7 +604,7 @@ static tfe_status load(const tfe_table_desc* d, hipStream_t stream, tfe_table** 
   st = build_index(d->phrase_tokens, d->phrase_len, d->n_phrases, d->n_max, slots.data(), cap);
   if (st != TFE_OK) return st;
 
-  tfe_table* t = new (std::nothrow) tfe_table;
+  tfe_table* t = alloc_fails() ? nullptr : new (std::nothrow) tfe_table;
   if (!t) return fail(TFE_ERR_OOM, "table object");
   if (hipGetDevice(&t->device) != hipSuccess ||
       hipDeviceGetAttribute(&t->cus, hipDeviceAttributeMultiprocessorCount, t->device) !=
@@ -579,7 +631,7 @@ static tfe_status load(const tfe_table_desc* d, hipStream_t stream, tfe_table** 
   }
 
   const size_t slot_bytes = (size_t)cap * sizeof(tfe_slot);
-  if (hipMalloc((void**)&t->d_slots, slot_bytes) != hipSuccess) {
+  if (dev_malloc((void**)&t->d_slots, slot_bytes) != hipSuccess) {
     release(t);
     return fail(TFE_ERR_OOM, "device index (%zu bytes)", slot_bytes);
   }
@@ -618,7 +670,6 @@ static tfe_status lookup_inject(tfe_table* t, const int32_t* tokens, int32_t B, 
   // tiered table live on the host and change with every call: a replayed
   // graph would reuse them.  Refused before anything is counted.
   if (t->cache_rows > 0) TFE_TRY(refuse_capture(stream, "a lookup on a tiered table"));
-  t->stats.calls++;
   if (T == 0) return TFE_OK;
   if (!tokens || !hin || !hout || !hit || !slot)
     return fail(TFE_ERR_INVALID_ARG, "null tokens, hidden, mask or slot_ids");
@@ -669,12 +720,12 @@ static tfe_status lookup_inject(tfe_table* t, const int32_t* tokens, int32_t B, 
 extern "C" {
 
 tfe_status tfe_table_load(const tfe_table_desc* desc, void* stream, tfe_table** out) {
-  tfe::clear_error();
+  tfe::begin_call();
   return tfe::load(desc, (hipStream_t)stream, out);
 }
 
 tfe_status tfe_table_free(tfe_table* table) {
-  tfe::clear_error();
+  tfe::begin_call();
   tfe::release(table);
   return TFE_OK;
 }
@@ -683,24 +734,30 @@ tfe_status tfe_lookup_inject(tfe_table* table, const int32_t* tokens, int32_t B,
                              int32_t S, const void* hidden_in, void* hidden_out,
                              uint8_t* hit_mask, int32_t* slot_ids, uint8_t* match_len,
                              int32_t gate, float scale, void* stream) {
-  tfe::clear_error();
-  return tfe::lookup_inject(table, tokens, B, ctx, S, hidden_in, hidden_out, hit_mask, slot_ids,
-                            match_len, gate, scale, (hipStream_t)stream);
+  tfe::begin_call();
+  const tfe_status st = tfe::lookup_inject(table, tokens, B, ctx, S, hidden_in, hidden_out,
+                                           hit_mask, slot_ids, match_len, gate, scale,
+                                           (hipStream_t)stream);
+  if (st == TFE_OK) table->stats.calls++;
+  return st;
 }
 
 tfe_status tfe_lookup_inject_multi(tfe_table* table, const int32_t* tokens, int32_t B,
                                    int32_t ctx, int32_t S, const void* hidden_in,
                                    void* hidden_out, uint8_t* match_mask, int32_t* slot_ids,
                                    int32_t weighting, int32_t gate, float scale, void* stream) {
-  tfe::clear_error();
+  tfe::begin_call();
   if (weighting < 0) return tfe::fail(TFE_ERR_INVALID_ARG, "bad weighting");
-  return tfe::lookup_inject(table, tokens, B, ctx, S, hidden_in, hidden_out, match_mask,
-                            slot_ids, nullptr, gate, scale, (hipStream_t)stream, weighting);
+  const tfe_status st = tfe::lookup_inject(table, tokens, B, ctx, S, hidden_in, hidden_out,
+                                           match_mask, slot_ids, nullptr, gate, scale,
+                                           (hipStream_t)stream, weighting);
+  if (st == TFE_OK) table->stats.calls++;
+  return st;
 }
 
 tfe_status tfe_prefetch(tfe_table* table, const int32_t* tail, int32_t tail_len,
                         const int32_t* candidates, int32_t B, int32_t K, void* side_stream) {
-  tfe::clear_error();
+  tfe::begin_call();
   if (!table) return tfe::fail(TFE_ERR_INVALID_ARG, "null table");
   if (tail_len < 0 || B < 0 || K < 0) return tfe::fail(TFE_ERR_INVALID_ARG, "negative size");
   if ((int64_t)B * K > 0 && (!candidates || (tail_len > 0 && !tail)))
@@ -713,7 +770,7 @@ tfe_status tfe_prefetch(tfe_table* table, const int32_t* tail, int32_t tail_len,
 tfe_status tfe_prefetch_scored(tfe_table* table, const int32_t* tail, int32_t tail_len,
                                const int32_t* candidates, const float* cand_prob, int32_t B,
                                int32_t K, int32_t budget, void* side_stream) {
-  tfe::clear_error();
+  tfe::begin_call();
   if (!table) return tfe::fail(TFE_ERR_INVALID_ARG, "null table");
   if (tail_len < 0 || B < 0 || K < 0) return tfe::fail(TFE_ERR_INVALID_ARG, "negative size");
   if (budget < 0 || budget > (int32_t)tfe::scored_prefetch_budget_max())
@@ -727,7 +784,7 @@ tfe_status tfe_prefetch_scored(tfe_table* table, const int32_t* tail, int32_t ta
 }
 
 tfe_status tfe_get_stats(const tfe_table* table, tfe_stats* out) {
-  tfe::clear_error();
+  tfe::begin_call();
   if (!table || !out) return tfe::fail(TFE_ERR_INVALID_ARG, "null table or out");
   tfe_status st = tfe::sync_table(table);
   if (st != TFE_OK) return st;
@@ -765,7 +822,7 @@ tfe_status tfe_get_stats(const tfe_table* table, tfe_stats* out) {
 }
 
 tfe_status tfe_reset_stats(tfe_table* table) {
-  tfe::clear_error();
+  tfe::begin_call();
   if (!table) return tfe::fail(TFE_ERR_INVALID_ARG, "null table");
   tfe_status st = tfe::sync_table(table);
   if (st != TFE_OK) return st;
@@ -785,7 +842,7 @@ tfe_status tfe_reset_stats(tfe_table* table) {
 
 tfe_status tfe_residency(const tfe_table* table, const int32_t* rows, int64_t n, int32_t* out,
                          void* stream) {
-  tfe::clear_error();
+  tfe::begin_call();
   if (!table) return tfe::fail(TFE_ERR_INVALID_ARG, "null table");
   if (n < 0 || n > 0x7FFFFFFF00ll) return tfe::fail(TFE_ERR_INVALID_ARG, "bad n");
   if (n > 0 && (!rows || !out)) return tfe::fail(TFE_ERR_INVALID_ARG, "null rows or out");
@@ -816,6 +873,5 @@ tfe_status tfe_residency(const tfe_table* table, const int32_t* rows, int64_t n,
   return TFE_OK;
 }
 
-const char* tfe_last_error(void) { return tfe::g_err; }
 
 }  // extern "C"

@@ -825,7 +825,7 @@ void* cache_get(int device, size_t bytes) {
   }
   for (size_t i = 0; i < g_cache.size();) {
     if (!g_cache[i].used && g_cache[i].device == device) {
-      (void)hipFree(g_cache[i].p);
+      dev_free(g_cache[i].p);
       g_cache[i] = g_cache.back();
       g_cache.pop_back();
     } else {
@@ -834,10 +834,7 @@ void* cache_get(int device, size_t bytes) {
   }
   const size_t rounded = (bytes + kGrain - 1) / kGrain * kGrain;
   void* p = nullptr;
-  if (hipMalloc(&p, rounded) != hipSuccess) {
-    (void)hipGetLastError();
-    return nullptr;
-  }
+  if (dev_malloc(&p, rounded) != hipSuccess) return nullptr;
   g_cache.push_back(CachedBuf{p, rounded, device, true});
   return p;
 }
@@ -1028,14 +1025,14 @@ tfe_status ngram_top(const int32_t* tokens, int64_t N, int32_t vocab, int32_t n,
 }  // namespace tfe
 
 extern "C" tfe_status tfe_ngram_release(void) {
-  tfe::clear_error();
+  tfe::begin_call();
   std::lock_guard<std::mutex> lock(tfe::g_cache_mu);
   int cur = 0;
   (void)hipGetDevice(&cur);
   for (size_t i = 0; i < tfe::g_cache.size();) {
     if (!tfe::g_cache[i].used) {
       (void)hipSetDevice(tfe::g_cache[i].device);
-      (void)hipFree(tfe::g_cache[i].p);
+      tfe::dev_free(tfe::g_cache[i].p);
       tfe::g_cache[i] = tfe::g_cache.back();
       tfe::g_cache.pop_back();
     } else {
@@ -1049,7 +1046,7 @@ extern "C" tfe_status tfe_ngram_release(void) {
 extern "C" tfe_status tfe_ngram_top(const int32_t* tokens, int64_t n_tokens, int32_t vocab,
                                     int32_t n, int64_t skip, int64_t top, int32_t* out_tuples,
                                     int64_t* out_counts, int64_t* written, void* stream) {
-  tfe::clear_error();
+  tfe::begin_call();
   return tfe::ngram_top(tokens, n_tokens, vocab, n, skip, top, out_tuples, out_counts, written,
                         (hipStream_t)stream);
 }

@@ -19,6 +19,10 @@ struct tfe_head {
   float* d_logits = nullptr;  // [rows x tiles x 16]
   uint64_t* d_tkey = nullptr; // [rows x tiles rounded up to 16]
   float* d_tsum = nullptr;    // [rows x tiles rounded up to 16]
+  // Recorded after every top-K call made outside graph capture; freeing the
+  // head waits for it (and for nothing else on the device).
+  hipEvent_t ev_last = nullptr;
+  bool recorded = false;
 };
 
 namespace tfe {
@@ -39,10 +43,10 @@ void release(tfe_head* h) {
   int cur = 0;
   (void)hipGetDevice(&cur);
   (void)hipSetDevice(h->device);
-  (void)hipDeviceSynchronize();
+  if (h->recorded) (void)hipEventSynchronize(h->ev_last);
   void* bufs[] = {h->d_logits, h->d_tkey, h->d_tsum};
-  for (void* b : bufs)
-    if (b) (void)hipFree(b);
+  for (void* b : bufs) dev_free(b);
+  if (h->ev_last) (void)hipEventDestroy(h->ev_last);
   (void)hipSetDevice(cur);
   delete h;
 }
@@ -67,7 +71,7 @@ tfe_status create(const void* w, int32_t vocab, int32_t dim, int32_t max_batch, 
     (void)hipGetLastError();
     return fail(TFE_ERR_INVALID_ARG, "projection is not device memory");
   }
-  tfe_head* h = new (std::nothrow) tfe_head;
+  tfe_head* h = alloc_fails() ? nullptr : new (std::nothrow) tfe_head;
   if (!h) return fail(TFE_ERR_OOM, "head");
   tfe_status st = TFE_OK;
   do {
@@ -97,11 +101,15 @@ tfe_status create(const void* w, int32_t vocab, int32_t dim, int32_t max_batch, 
     h->max_k = (uint32_t)max_k;
     const size_t nb = ((size_t)h->max_batch + 63) / 64 * 64, nt = (h->V + 31) / 32 * 2;
     const size_t nt16 = (nt + 15) / 16 * 16;
-    if (hipMalloc(&h->d_logits, nb * nt * 16 * sizeof(float)) != hipSuccess ||
-        hipMalloc(&h->d_tkey, nb * nt16 * sizeof(uint64_t)) != hipSuccess ||
-        hipMalloc(&h->d_tsum, nb * nt16 * sizeof(float)) != hipSuccess) {
-      (void)hipGetLastError();
+    if (dev_malloc((void**)&h->d_logits, nb * nt * 16 * sizeof(float)) != hipSuccess ||
+        dev_malloc((void**)&h->d_tkey, nb * nt16 * sizeof(uint64_t)) != hipSuccess ||
+        dev_malloc((void**)&h->d_tsum, nb * nt16 * sizeof(float)) != hipSuccess) {
       st = fail(TFE_ERR_OOM, "head scratch for %u rows", h->max_batch);
+      break;
+    }
+    if (hipEventCreateWithFlags(&h->ev_last, hipEventDisableTiming) != hipSuccess) {
+      h->ev_last = nullptr;
+      st = fail(TFE_ERR_HIP, "head event");
       break;
     }
   } while (0);
@@ -143,6 +151,12 @@ tfe_status topk(tfe_head* h, const void* hidden, int32_t B, int32_t K, int32_t* 
   a.K = (uint32_t)K;
   HEAD_HIP(launch_head_logits(a, (uint32_t)h->cus, stream), "head logits launch");
   HEAD_HIP(launch_head_rows(a, stream), "head top-K launch");
+  hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+  HEAD_HIP(hipStreamIsCapturing(stream, &cs), "hipStreamIsCapturing");
+  if (cs == hipStreamCaptureStatusNone) {
+    HEAD_HIP(hipEventRecord(h->ev_last, stream), "record");
+    h->recorded = true;
+  }
   return TFE_OK;
 }
 
@@ -153,18 +167,18 @@ extern "C" {
 
 tfe_status tfe_head_create(const void* w_pref, int32_t vocab, int32_t dim, int32_t max_batch,
                            int32_t max_k, tfe_head** out) {
-  tfe::clear_error();
+  tfe::begin_call();
   return tfe::create(w_pref, vocab, dim, max_batch, max_k, out);
 }
 
 tfe_status tfe_head_topk(tfe_head* head, const void* hidden, int32_t B, int32_t K,
                          int32_t* top_ids, float* top_prob, void* stream) {
-  tfe::clear_error();
+  tfe::begin_call();
   return tfe::topk(head, hidden, B, K, top_ids, top_prob, (hipStream_t)stream);
 }
 
 tfe_status tfe_head_free(tfe_head* head) {
-  tfe::clear_error();
+  tfe::begin_call();
   tfe::release(head);
   return TFE_OK;
 }

@@ -128,7 +128,7 @@ tfe_status topk_noalloc(const void* w, int32_t vocab, int32_t dim, const void* h
 extern "C" tfe_status tfe_head_topk_noalloc(const void* w_pref, int32_t vocab, int32_t dim,
                                             const void* hidden, int32_t B, int32_t K,
                                             int32_t* top_ids, float* top_prob, void* stream) {
-  tfe::clear_error();
+  tfe::begin_call();
   return tfe::topk_noalloc(w_pref, vocab, dim, hidden, B, K, top_ids, top_prob,
                            (hipStream_t)stream);
 }

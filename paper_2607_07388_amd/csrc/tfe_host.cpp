@@ -1,9 +1,16 @@
-// Host side of the phrase index: validation, capacity, build and a host probe.
+// Host side of libtfe: the error message, the allocation-failure hook and
+// the held-memory count, and the phrase index (validation, capacity, build
+// and a host probe).  Nothing here calls the HIP runtime.
+#include <stdarg.h>
 #include <stdint.h>
+#include <stdio.h>
+#include <stdlib.h>
 #include <string.h>
 
 #include <atomic>
+#include <mutex>
 #include <thread>
+#include <unordered_map>
 #include <vector>
 
 #include "../../include/tfe.h"
@@ -11,6 +18,69 @@
 #include "tfe_internal.h"
 
 namespace tfe {
+
+static thread_local char g_err[512] = "";
+// Allocations made so far by the current library call on this thread.
+static thread_local int64_t g_allocs_in_call = 0;
+
+tfe_status fail(tfe_status st, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof g_err, fmt, ap);
+  va_end(ap);
+  return st;
+}
+
+void clear_error() {
+  g_err[0] = 0;
+  g_allocs_in_call = 0;
+}
+
+const char* last_error() { return g_err; }
+
+bool alloc_fails() {
+  const int64_t k = ++g_allocs_in_call;
+  const char* s = getenv("TFE_FAIL_ALLOC");
+  if (!s || !*s) return false;
+  return strtoll(s, nullptr, 10) == k;
+}
+
+namespace {
+struct Held {
+  std::mutex mu;
+  std::unordered_map<const void*, std::pair<size_t, bool>> live;  // size, pinned
+  int64_t bytes[2] = {0, 0};                                      // device, pinned
+};
+Held& held() {
+  static Held* h = new Held;  // never destroyed: tables may outlive static teardown
+  return *h;
+}
+}  // namespace
+
+void note_alloc(const void* p, size_t n, bool pinned) {
+  if (!p) return;
+  Held& h = held();
+  std::lock_guard<std::mutex> g(h.mu);
+  h.live[p] = {n, pinned};
+  h.bytes[pinned] += (int64_t)n;
+}
+
+void note_free(const void* p) {
+  if (!p) return;
+  Held& h = held();
+  std::lock_guard<std::mutex> g(h.mu);
+  auto it = h.live.find(p);
+  if (it == h.live.end()) return;
+  h.bytes[it->second.second] -= (int64_t)it->second.first;
+  h.live.erase(it);
+}
+
+void memory_held(int64_t* device_bytes, int64_t* pinned_bytes) {
+  Held& h = held();
+  std::lock_guard<std::mutex> g(h.mu);
+  if (device_bytes) *device_bytes = h.bytes[0];
+  if (pinned_bytes) *pinned_bytes = h.bytes[1];
+}
 
 int64_t index_capacity(int64_t n, double lf) {
   if (lf <= 0.0) lf = 0.5;
@@ -157,6 +227,15 @@ tfe_status build_index(const int32_t* tokens, const uint8_t* lens, int64_t P, in
 }  // namespace tfe
 
 extern "C" {
+
+const char* tfe_last_error(void) { return tfe::last_error(); }
+
+tfe_status tfe_memory_held(int64_t* device_bytes, int64_t* pinned_bytes) {
+  tfe::clear_error();
+  if (!device_bytes && !pinned_bytes) return tfe::fail(TFE_ERR_INVALID_ARG, "no output");
+  tfe::memory_held(device_bytes, pinned_bytes);
+  return TFE_OK;
+}
 
 int64_t tfe_index_capacity(int64_t n_phrases, double max_load_factor) {
   if (n_phrases < 0 || max_load_factor < 0.0 || max_load_factor > 0.9) return -1;

@@ -14,11 +14,19 @@ namespace tfe {
 
 // Thread-local error message; fail() formats it and returns the status.
 tfe_status fail(tfe_status st, const char* fmt, ...);
-// TFE_ERR_UNSUPPORTED if `stream` is being captured into a graph (for calls
-// that keep per-call host state or synchronise), TFE_ERR_HIP if the query
-// fails, else TFE_OK.
-tfe_status refuse_capture(hipStream_t stream, const char* what);
+// Clears the message; every C-ABI call starts with it, which also restarts
+// the call's allocation count.
 void clear_error();
+const char* last_error();
+
+// Allocation-failure hook: with TFE_FAIL_ALLOC=k in the environment, the
+// k-th allocation of a library call (counted from its clear_error) fails as
+// if memory had run out.  Every allocation asks this first.
+bool alloc_fails();
+// Device and pinned-host bytes the library holds, across all tables.
+void note_alloc(const void* p, size_t n, bool pinned);
+void note_free(const void* p);
+void memory_held(int64_t* device_bytes, int64_t* pinned_bytes);
 
 int64_t index_capacity(int64_t n, double lf);
 tfe_status validate_phrases(const int32_t* tokens, const uint8_t* lens, int64_t P, int n_min,
@@ -27,6 +35,27 @@ tfe_status build_index(const int32_t* tokens, const uint8_t* lens, int64_t P, in
                        tfe_slot* slots, int64_t cap);
 
 #if defined(__HIPCC__) || defined(__HIP_PLATFORM_AMD__)
+
+// TFE_ERR_UNSUPPORTED if `stream` is being captured into a graph (for calls
+// that keep per-call host state or synchronise), TFE_ERR_HIP if the query
+// fails, else TFE_OK.
+tfe_status refuse_capture(hipStream_t stream, const char* what);
+
+// Starts a C-ABI call that uses the HIP runtime: clears the message and the
+// call's allocation count, and discards an error status that HIP calls made
+// outside the library left on this thread (launches are checked with
+// hipGetLastError, which would report it as theirs).
+inline void begin_call() {
+  clear_error();
+  (void)hipGetLastError();
+}
+
+// The library's only ways to get and give back device and pinned host
+// memory: they honour the failure hook and keep the held-memory count.
+hipError_t dev_malloc(void** p, size_t n);
+void dev_free(void* p);
+hipError_t pinned_malloc(void** p, size_t n);
+void pinned_free(void* p);
 
 // Per-call arguments of the lookup + inject kernels.
 struct LookupArgs {

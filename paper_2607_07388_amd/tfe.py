@@ -59,10 +59,31 @@ class TfeError(RuntimeError):
         self.status = status
 
 
+def hip_runtimes():
+    """Distinct HIP runtime libraries mapped into this process."""
+    with open("/proc/self/maps") as f:
+        return sorted({ln.split()[-1] for ln in f if "libamdhip64" in ln and "/" in ln})
+
+
+def share_torch_hip_runtime():
+    """Makes the next HIP-linked library use torch's HIP runtime, if torch
+    is installed.  torch ships its own copy of the runtime under the same
+    soname as the system one; loaded first, it satisfies the library's
+    dependency.  Loaded second, it would be a second runtime in the process,
+    and one of the two then sees no device."""
+    try:
+        import torch  # noqa: F401
+    except ImportError:
+        pass
+
+
 def _load():
     if not os.path.exists(_build.SO):
         _build.build()
+    share_torch_hip_runtime()
     L = ctypes.CDLL(_build.SO)
+    if len(hip_runtimes()) > 1:
+        raise ImportError("more than one HIP runtime in this process: %s" % hip_runtimes())
     vp, i32, i64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
     sig = {
         "tfe_table_load": ([ctypes.POINTER(tfe_table_desc), vp, ctypes.POINTER(vp)], ctypes.c_int),
@@ -84,6 +105,7 @@ def _load():
         "tfe_reset_stats": ([vp], ctypes.c_int),
         "tfe_residency": ([vp, vp, i64, vp, vp], ctypes.c_int),
         "tfe_last_error": ([], ctypes.c_char_p),
+        "tfe_memory_held": ([ctypes.POINTER(i64), ctypes.POINTER(i64)], ctypes.c_int),
         "tfe_index_capacity": ([i64, ctypes.c_double], i64),
         "tfe_index_build_host": ([vp, vp, i64, i32, i32, i32, vp, i64], ctypes.c_int),
         "tfe_index_probe_host": ([vp, i64, vp, i32, ctypes.POINTER(i32), ctypes.POINTER(i32),
@@ -104,7 +126,7 @@ EXPORTED = ("tfe_table_load", "tfe_table_free", "tfe_lookup_inject", "tfe_lookup
             "tfe_head_topk_noalloc",
             "tfe_ngram_top", "tfe_ngram_release",
             "tfe_get_stats", "tfe_reset_stats", "tfe_residency", "tfe_last_error",
-            "tfe_index_capacity",
+            "tfe_memory_held", "tfe_index_capacity",
             "tfe_index_build_host", "tfe_index_probe_host")
 
 
@@ -136,6 +158,13 @@ def _check(st):
 
 def tfe_last_error():
     return lib.tfe_last_error().decode()
+
+
+def tfe_memory_held():
+    """(device bytes, pinned host bytes) the library holds right now."""
+    d, p = ctypes.c_int64(), ctypes.c_int64()
+    _check(lib.tfe_memory_held(ctypes.byref(d), ctypes.byref(p)))
+    return d.value, p.value
 
 
 def tfe_table_load(desc, stream=None):

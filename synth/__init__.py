@@ -71,6 +71,13 @@ def host_lib():
 def dev_lib():
     global _dev
     if _dev is None:
+        # One HIP runtime per process: torch's, when it is installed (its
+        # copy has the system runtime's soname and satisfies this library's
+        # dependency only if it is loaded first).
+        try:
+            import torch  # noqa: F401
+        except ImportError:
+            pass
         lib = _load(_build.DEV_SO)
         i64, u64, vp = ctypes.c_int64, ctypes.c_uint64, ctypes.c_void_p
         lib.synth_normal_fill_dev.argtypes = [vp, i64, i64, i64, u64, ctypes.c_float,

@@ -7,7 +7,26 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <stdio.h>
+
 #include "synth_rng.h"
+
+// A launch is checked with hipGetLastError, which also reports a failed HIP
+// call made earlier on this thread by other code: that status is cleared
+// before the launch (and named on stderr, with the launch's own error).
+static void clear_stale_status(const char* what) {
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess)
+    fprintf(stderr, "synth: %s: earlier HIP status %s cleared before the launch\n", what,
+            hipGetErrorName(e));
+}
+
+static int launched(const char* what) {
+  const hipError_t e = hipGetLastError();
+  if (e == hipSuccess) return 0;
+  fprintf(stderr, "synth: %s launch failed: %s\n", what, hipGetErrorName(e));
+  return -2;
+}
 
 // One thread per element of rows [row0, row0 + nrows); out points at row0.
 template <int DT>
@@ -30,13 +49,14 @@ extern "C" int synth_normal_fill_dev(void* out, int64_t row0, int64_t nrows, int
   const int64_t n = nrows * cols;
   int64_t blocks = (n + 255) / 256;
   if (blocks > 1 << 20) blocks = 1 << 20;
+  clear_stale_status("normal fill");
   if (dtype == 0)
     hipLaunchKernelGGL(k_normal_fill<0>, dim3((unsigned)blocks), dim3(256), 0, stream, out, row0,
                        nrows, cols, key, scale);
   else
     hipLaunchKernelGGL(k_normal_fill<1>, dim3((unsigned)blocks), dim3(256), 0, stream, out, row0,
                        nrows, cols, key, scale);
-  return hipGetLastError() == hipSuccess ? 0 : -2;
+  return launched("normal fill");
 }
 
 // Plain device copy (16 bytes per lane, non-temporal), used only as the
@@ -54,9 +74,10 @@ __global__ void k_copy16(const synth_u32x4* __restrict__ src, synth_u32x4* __res
 extern "C" int synth_copy_dev(void* dst, const void* src, int64_t nbytes, int blocks,
                               hipStream_t stream) {
   if (!dst || !src || nbytes <= 0 || (nbytes & 15) || blocks <= 0) return -1;
+  clear_stale_status("copy");
   hipLaunchKernelGGL(k_copy16, dim3((unsigned)blocks), dim3(256), 0, stream, (const synth_u32x4*)src,
                      (synth_u32x4*)dst, nbytes / 16);
-  return hipGetLastError() == hipSuccess ? 0 : -2;
+  return launched("copy");
 }
 
 // Device address of pinned host memory (hipHostMalloc), so that the device
@@ -78,6 +99,7 @@ __global__ void k_spin(uint64_t ticks) {
 
 extern "C" int synth_spin_dev(double us, hipStream_t stream) {
   if (!(us >= 0.0) || us > 1e5) return -1;
+  clear_stale_status("spin");
   hipLaunchKernelGGL(k_spin, dim3(1), dim3(64), 0, stream, (uint64_t)(us * 100.0));
-  return hipGetLastError() == hipSuccess ? 0 : -2;
+  return launched("spin");
 }

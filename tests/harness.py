@@ -54,6 +54,7 @@ class GpuTable:
 
     def __init__(self, table, values_on_device=None, lf=0.5):
         self.table = table
+        self.handle = None
         if values_on_device is None:
             values_on_device = table.n_phrases * table.dim > (1 << 22)
         vals = device_values(table) if values_on_device else table.all_values()

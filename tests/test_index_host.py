@@ -156,3 +156,20 @@ def test_parallel_build_finds_a_planted_duplicate():
             build(toks, lens, 2, 3)
         assert e.value.status == tfe.TFE_ERR_DUPLICATE_KEY
         assert str(min(src, dst)) in tfe.tfe_last_error()
+
+
+def test_one_hip_runtime_whatever_the_import_order():
+    """torch carries its own HIP runtime under the system runtime's soname.
+    Loading libtfe (or the workload generator's device library) before
+    torch must not map a second runtime: with two, one of them sees no
+    device.  Checked in a fresh process, libraries first, torch last."""
+    import subprocess
+    import sys
+    code = ("import sys; sys.path.insert(0, %r)\n"
+            "from paper_2607_07388_amd import tfe\n"
+            "import synth; synth.dev_lib()\n"
+            "import torch\n"
+            "print(len(tfe.hip_runtimes()))\n" % ROOT)
+    r = subprocess.run([sys.executable, "-c", code], stdout=subprocess.PIPE,
+                       stderr=subprocess.PIPE, text=True, timeout=300)
+    assert r.returncode == 0 and r.stdout.strip() == "1", r.stdout + r.stderr
