@@ -1,8 +1,14 @@
 """GPU parity of offline phrase-table construction (Sec. 4.2: candidate
 phrases selected by corpus frequency): tfe_ngram_top through the C ABI
-against the oracle (tuples and counts bit-exact, ties by tuple), and at the
-full workload size against the input generator's independent partitioned
-count (itself pinned to the oracle on smaller streams)."""
+against the oracle (tuples and counts bit-exact, ties by tuple); at the full
+workload size against SHA-256 digests of the oracle's own ranking
+(tests/golden/ngram_top_workload2.json, written by make_ngram_digests.py,
+which calls only the oracle and the stream generator) and against the input
+generator's independent partitioned count."""
+import hashlib
+import json
+import os
+
 import numpy as np
 import pytest
 import torch
@@ -109,12 +115,28 @@ def test_zipf_stream_matches_generator_and_oracle():
         np.testing.assert_array_equal(c, wc)
 
 
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden",
+                      "ngram_top_workload2.json")
+
+
+def sha256(a):
+    return hashlib.sha256(np.ascontiguousarray(a).tobytes()).hexdigest()
+
+
 def test_workload2_stream_full_size():
     """The 2^26-token Zipf(1.1) stream of the 2^20-phrase decode table: top
-    2^19 2-, 3- and 4-grams, against the generator's partitioned count."""
+    2^19 2-, 3- and 4-grams, against the digests of the oracle's ranking and
+    against the generator's partitioned count."""
+    golden = json.load(open(GOLDEN))
     toks = synth.workload2_stream()
+    assert sha256(toks) == golden["stream_sha256"]
     for n in (2, 3, 4):
-        t, c = gpu_top(toks, synth.V, n, 0, 1 << 19)
+        g = golden["n"][str(n)]
+        t, c = gpu_top(toks, synth.V, n, 0, golden["top"])
+        assert c.size == g["ranks"] and int(c.sum()) == g["count_sum"]
+        assert [[r.tolist(), int(k)] for r, k in zip(t[:len(g["head"])], c)] == g["head"]
+        assert sha256(t.astype("<i4")) == g["tuples_sha256"]
+        assert sha256(c.astype("<i8")) == g["counts_sha256"]
         wt, wc = synth.ngram_top(toks, n, 1 << 19)
         np.testing.assert_array_equal(t, wt)
         np.testing.assert_array_equal(c, wc)

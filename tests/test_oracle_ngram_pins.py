@@ -2,8 +2,13 @@
 phrases selected by corpus frequency): a hand-counted stream, a brute-force
 Counter over random streams with invalid tokens and many equal counts, the
 skip/top windows of one ranking, the window-count invariant, and agreement
-with the input generator's independent partitioned implementation."""
+with the input generator's independent partitioned implementation (on small
+streams here, and at the full 2^26-token workload size through the digests
+of the oracle's ranking in tests/golden/ngram_top_workload2.json)."""
 import collections
+import hashlib
+import json
+import os
 
 import numpy as np
 import pytest
@@ -70,3 +75,27 @@ def test_agrees_with_the_generators_partitioned_count(n):
     t, c = oracle.ngram_top(toks, synth.V, n, 100, 3000)
     np.testing.assert_array_equal(t, want_t)
     np.testing.assert_array_equal(c, want_c)
+
+
+def test_generator_matches_oracle_digests_at_full_size():
+    """The stored digests come from the oracle's ranking of the full
+    2^26-token workload-2 stream (tests/golden/make_ngram_digests.py, which
+    calls only the oracle and the generator).  The generator's stream and
+    its partitioned count -- the GPU tests' second reference -- reproduce
+    them; the head ranks are checked in clear against the stream."""
+    golden = json.load(open(os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden",
+                                         "ngram_top_workload2.json")))
+    sha = lambda a: hashlib.sha256(np.ascontiguousarray(a).tobytes()).hexdigest()
+    toks = synth.workload2_stream()
+    assert sha(toks) == golden["stream_sha256"] and toks.size == golden["stream_tokens"]
+    for n in (2, 3, 4):
+        g = golden["n"][str(n)]
+        t, c = synth.ngram_top(toks, n, golden["top"])
+        assert sha(t.astype("<i4")) == g["tuples_sha256"]
+        assert sha(c.astype("<i8")) == g["counts_sha256"]
+        # The most frequent tuple's count, by a direct scan of the stream.
+        head = np.array(g["head"][0][0], np.int32)
+        hits = np.ones(toks.size - n + 1, bool)
+        for j in range(n):
+            hits &= toks[j:toks.size - n + 1 + j] == head[j]
+        assert int(hits.sum()) == g["head"][0][1]
