@@ -52,6 +52,12 @@ import os
 import sys
 import time
 
+# Idle OpenMP workers (torch's CPU thread pool) sleep instead of spinning:
+# spinning workers take the CPU from the host threads that stage a tiered
+# table's pageable rows (measured: 16384-row miss-path calls 5-6 ms instead
+# of 0.6-0.8 ms right after CPU-parallel work).  Set before torch loads.
+os.environ.setdefault("OMP_WAIT_POLICY", "PASSIVE")
+
 import numpy as np
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
@@ -207,6 +213,10 @@ def main():
     ap.add_argument("--tier-steps", type=int, default=2000)
     ap.add_argument("--tier-warmup", type=int, default=100)
     ap.add_argument("--t-hide-us", default="0,100")
+    ap.add_argument("--tier-log2-phrases", type=int, default=26,
+                    help="tiered table size (2^26: 128 GiB of values)")
+    ap.add_argument("--tier-pinned-log2", type=int, default=25,
+                    help="rows kept in pinned host memory (2^25: 64 GiB, this box's pin limit)")
     ap.add_argument("--prefetch-budget", type=int, default=64)
     ap.add_argument("--tier-fill", default="inline,side",
                     help="miss fill modes of the tiered table to run (inline, side)")
@@ -914,17 +924,26 @@ def run_tiered(args):
 
     B, K, C = 64, 8, 4 << 20
     t0 = time.time()
-    table = synth.config5_table()
-    P = table.n_phrases
     log = lambda m: print("# %s (%.1f s)" % (m, time.time() - t0), file=sys.stderr, flush=True)
+    table = synth.config5_table(args.tier_log2_phrases)
+    P = table.n_phrases
     log("table of %d phrases generated" % P)
-    vals = torch.empty((P, D), dtype=torch.bfloat16, pin_memory=True)
+    # The most frequent rows (the table is ordered by count) in pinned host
+    # memory, the rest, if any, in pageable host memory behind the table's
+    # staging queue: one process pins at most 64 GiB here.
+    Pp = min(P, 1 << args.tier_pinned_log2)
+    vals = torch.empty((Pp, D), dtype=torch.bfloat16, pin_memory=True)
     log("pinned %.1f GiB" % (vals.numel() * 2 / 2**30))
     stream = torch.cuda.current_stream()
-    synth.normal_fill_device(synth.host_device_ptr(vals.data_ptr()), 0, P, D, table.seed,
+    synth.normal_fill_device(synth.host_device_ptr(vals.data_ptr()), 0, Pp, D, table.seed,
                              synth.TAG_VALUES, table.sigma, synth.BF16, stream.cuda_stream)
     torch.cuda.synchronize()
+    pageable = None
+    if Pp < P:
+        pageable = H.pageable_values(table, Pp, stream)
+        log("pageable %.1f GiB" % (pageable.nbytes / 2**30))
     log("values drawn into host memory")
+    split = dict(pinned_rows=Pp if Pp < P else 0, pageable_values=pageable)
 
     # Host -> device copy ceiling of this machine (pinned, 1 GiB).
     hb = vals[: (1 << 29) // D]
@@ -966,7 +985,7 @@ def run_tiered(args):
                                    for f in fill_names for p in ("off", "all", "scored")]:
         desc = tfe.make_desc(table.tokens, table.lens, 2, 3, synth.V, vals, D, synth.BF16, 0,
                              0.5, hbm_cache_rows=C, adopt_host_values=1, prefill_rows=C,
-                             miss_fill=fills[fill])
+                             miss_fill=fills[fill], **split)
         handle = tfe.tfe_table_load(desc, stream.cuda_stream)
         log("tiered table loaded (T_hide %g us, fill %s, prefetch %s)" % (t_hide, fill,
                                                                         prefetch))
@@ -1019,7 +1038,7 @@ def run_tiered(args):
         if k == 0:
             desc = tfe.make_desc(table.tokens, table.lens, 2, 3, synth.V, vals, D, synth.BF16, 0,
                                  0.5, hbm_cache_rows=C, adopt_host_values=1, prefill_rows=0,
-                                 miss_fill=fills[fill])
+                                 miss_fill=fills[fill], **split)
             handle = tfe.tfe_table_load(desc, stream.cuda_stream)
             # Untimed call whose windows match nothing (every token -1): it
             # sizes the table's per-call scratch for RB positions and leaves
@@ -1047,8 +1066,10 @@ def run_tiered(args):
         torch.cuda.synchronize()
         st = tfe.tfe_get_stats(handle)
         sec = e0.elapsed_time(e1) * 1e-3
+        rows = ob.slot.cpu().numpy()
         cold.append({"fill": fill, "call": k, "us": sec * 1e6, "hits": st["hits"],
                      "cache_misses": st["cache_misses"], "host_bytes": st["host_bytes"],
+                     "pageable_rows_matched": int((rows >= Pp).sum()),
                      "host_link_gbps": st["host_bytes"] / sec / 1e9})
         print(json.dumps(cold[-1]), file=sys.stderr, flush=True)
         if k == 3:
@@ -1070,8 +1091,10 @@ def run_tiered(args):
         "dtype": "bf16",
         "data": "synthetic",
         "config": {
-            "workload": "tiered: 2^25-phrase 2/3-gram table, 64 GiB bf16 values in pinned host "
-                        "memory, 4M-row HBM cache (LRU), batch-64 decode, 8 candidates per row",
+            "workload": "tiered: 2^%d-phrase 2/3-gram table, %d GiB bf16 values in host memory "
+                        "(%d GiB pinned, the rest pageable behind the staging queue), 4M-row "
+                        "HBM cache (LRU), batch-64 decode, 8 candidates per row"
+                        % (args.tier_log2_phrases, P * D * 2 >> 30, Pp * D * 2 >> 30),
             "h2d_copy_gbps": h2d_gbps,
             "prefetch_budget_scored": args.prefetch_budget,
             "miss_fill": "headline: %s (best no-prefetch, T_hide 0); all modes under 'runs'"

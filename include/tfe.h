@@ -118,6 +118,22 @@ typedef struct {
                                    must come from hipHostMalloc and outlive the table */
   int64_t prefill_rows;         /* tiered: rows [0, prefill_rows) start cached */
   int32_t miss_fill;            /* tiered: tfe_fill_mode (0 = inline); must be 0 or 1 */
+  /* Tiered, when not every row can be pinned (the pinnable host memory of a
+   * process is limited): with 0 < pinned_rows < n_phrases, `values` holds
+   * rows [0, pinned_rows) only (pinned as above), and rows [pinned_rows, P)
+   * stay in the caller's pageable host memory `pageable_values`
+   * (HOST [(P - pinned_rows) x dim], read in place; it must outlive the
+   * table and not change).  A kernel that needs one of those rows has a
+   * host thread of the table copy it into pinned staging memory first (the
+   * staging of rows into GPU-readable memory of Sec. 4.3); results are the
+   * same, only slower for those rows (a few microseconds each).  Order the
+   * rows by expected use (e.g. phrase frequency) so the pinned ones are the
+   * hot ones.  The table's host threads (4) need CPU time while kernels
+   * wait for them: thread pools that spin while idle (OpenMP's default wait
+   * policy; OMP_WAIT_POLICY=PASSIVE avoids it) delay them by milliseconds.
+   * pinned_rows = 0 (or P): every row is pinned; pageable_values is ignored. */
+  int64_t pinned_rows;
+  const void *pageable_values;
 } tfe_table_desc;
 
 typedef struct {

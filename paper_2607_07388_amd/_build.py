@@ -8,7 +8,7 @@ ROOT = os.path.dirname(HERE)
 SO = os.path.join(HERE, "libtfe.so")
 ROCM_INC = os.path.join(os.environ.get("ROCM_PATH", "/opt/rocm"), "include")
 
-SOURCES = ["tfe_api.cpp", "tfe_head_api.cpp", "tfe_host.cpp", "tfe_build.hip", "tfe_head.hip",
+SOURCES = ["tfe_api.cpp", "tfe_head_api.cpp", "tfe_host.cpp", "tfe_stage.cpp", "tfe_build.hip", "tfe_head.hip",
            "tfe_head_noalloc.hip", "tfe_lookup.hip", "tfe_multi.hip", "tfe_tiered.hip"]
 
 HIP_FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-Wall",

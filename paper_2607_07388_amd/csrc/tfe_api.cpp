@@ -35,10 +35,10 @@ void dev_free(void* p) {
   (void)hipFree(p);
 }
 
-hipError_t pinned_malloc(void** p, size_t n) {
+hipError_t pinned_malloc(void** p, size_t n, unsigned flags) {
   *p = nullptr;
   if (alloc_fails()) return hipErrorOutOfMemory;
-  const hipError_t e = hipHostMalloc(p, n, hipHostMallocDefault);
+  const hipError_t e = hipHostMalloc(p, n, flags);
   if (e != hipSuccess) {
     *p = nullptr;
     (void)hipGetLastError();
@@ -76,6 +76,10 @@ static tfe_status hip_fail(hipError_t e, const char* what) {
 
 static size_t elem_size(int dtype) { return dtype == TFE_F32 ? 4 : 2; }
 
+// Host threads that stage pageable rows of one tiered table (each serves
+// about four rows per microsecond).
+constexpr int kStageThreads = 4;
+
 // Waits on the host for the work this table has enqueued -- its last
 // lookup, a pending prefetch, its own stream (uploads, side-stream fills) --
 // and for nothing else on the device.  A lookup still being captured into a
@@ -111,10 +115,11 @@ static void release(tfe_table* t) {
   (void)hipGetDevice(&cur);
   (void)hipSetDevice(t->device);
   (void)sync_table(t);
+  tfe::stager_stop(t->stager);  // after the table's kernels, the only ones that post to it
   void* dev_bufs[] = {t->d_slots, t->d_values, t->d_cache, t->d_where, t->d_owner, t->d_stamp,
                       t->d_pref, t->d_ring, t->d_ring2, t->d_ctl, t->d_row_of,
                       t->d_slot_of, t->d_phase, t->d_jobs, t->d_hit_ctr, t->d_hkey, t->d_hpos, t->d_hval, t->d_blk, t->d_spare, t->d_pf_row_of,
-                      t->d_pf_slot_of, t->d_pf_phase, t->d_pf_jobs};
+                      t->d_pf_slot_of, t->d_pf_phase, t->d_pf_jobs, t->d_stage_ack};
   for (void* b : dev_bufs)
     dev_free(b);
   if (t->own_h_values && t->h_values) pinned_free(t->h_values);
@@ -171,6 +176,12 @@ static tfe_status dev_alloc(T** p, size_t n, const char* what) {
 static tfe::TierArgs tier_args(tfe_table* t) {
   tfe::TierArgs a = {};
   a.host_values = t->h_values_dev;
+  a.pinned_rows = (uint32_t)t->pinned_rows;
+  if (t->stager) {
+    a.stage = tfe::stager_queue(t->stager);
+    a.stage_rows = tfe::stager_rows(t->stager);
+    a.stage_ack = t->d_stage_ack;
+  }
   a.cache = t->d_cache;
   a.where = t->d_where;
   a.owner = t->d_owner;
@@ -224,6 +235,10 @@ static uint64_t pow2_at_least(uint64_t n) {
 static tfe_status load_tiered(tfe_table* t, const tfe_table_desc* d, hipStream_t stream) {
   const int64_t P = d->n_phrases, C = d->hbm_cache_rows;
   const size_t row_bytes = (size_t)d->dim * elem_size(d->dtype);
+  // Rows [0, Ppin) are pinned; rows [Ppin, P) stay in the caller's pageable
+  // memory behind the staging queue.
+  const int64_t Ppin = d->pinned_rows > 0 ? d->pinned_rows : P;
+  t->pinned_rows = Ppin;
   t->cache_rows = C;
   t->prefill_rows = d->prefill_rows;
   t->fill_mode = d->miss_fill;
@@ -235,14 +250,21 @@ static tfe_status load_tiered(tfe_table* t, const tfe_table_desc* d, hipStream_t
       return fail(TFE_ERR_INVALID_ARG, "adopted values are not pinned host memory (hipHostMalloc)");
     t->h_values = const_cast<void*>(d->values);
   } else if (P > 0) {
-    if (pinned_malloc(&t->h_values, (size_t)P * row_bytes) != hipSuccess) {
+    if (pinned_malloc(&t->h_values, (size_t)Ppin * row_bytes) != hipSuccess) {
       t->h_values = nullptr;
-      return fail(TFE_ERR_OOM, "pinned host values (%zu bytes)", (size_t)P * row_bytes);
+      return fail(TFE_ERR_OOM, "pinned host values (%zu bytes)", (size_t)Ppin * row_bytes);
     }
     t->own_h_values = true;
-    TFE_HIP(hipMemcpy(t->h_values, d->values, (size_t)P * row_bytes,
+    TFE_HIP(hipMemcpy(t->h_values, d->values, (size_t)Ppin * row_bytes,
                       d->values_on_device ? hipMemcpyDeviceToHost : hipMemcpyHostToHost),
             "values to pinned host memory");
+  }
+  if (Ppin < P) {
+    TFE_TRY(dev_alloc(&t->d_stage_ack, tfe::kStageSlots, "staging acknowledgements"));
+    TFE_HIP(hipMemsetAsync(t->d_stage_ack, 0, tfe::kStageSlots * sizeof(unsigned long long),
+                           stream),
+            "init");
+    TFE_TRY(tfe::stager_start(d->pageable_values, Ppin, P, row_bytes, kStageThreads, &t->stager));
   }
   if (t->h_values) {
     void* dp = nullptr;
@@ -270,9 +292,15 @@ static tfe_status load_tiered(tfe_table* t, const tfe_table_desc* d, hipStream_t
   TFE_HIP(hipMemsetAsync(t->d_ctl, 0, sizeof(tfe::TierCtl), stream), "init");
   tfe::TierArgs a = tier_args(t);
   TFE_HIP(tfe::launch_tier_init(a, (uint32_t)C, (uint32_t)d->prefill_rows, stream), "init launch");
-  if (d->prefill_rows > 0)
-    TFE_HIP(hipMemcpyAsync(t->d_cache, t->h_values, (size_t)d->prefill_rows * row_bytes,
+  const int64_t pre_pinned = d->prefill_rows < Ppin ? d->prefill_rows : Ppin;
+  if (pre_pinned > 0)
+    TFE_HIP(hipMemcpyAsync(t->d_cache, t->h_values, (size_t)pre_pinned * row_bytes,
                            hipMemcpyHostToDevice, stream),
+            "cache prefill");
+  if (d->prefill_rows > Ppin)  // from pageable memory (a staged copy by the runtime)
+    TFE_HIP(hipMemcpyAsync((char*)t->d_cache + (size_t)Ppin * row_bytes, d->pageable_values,
+                           (size_t)(d->prefill_rows - Ppin) * row_bytes, hipMemcpyHostToDevice,
+                           stream),
             "cache prefill");
   t->ring_bound = (uint64_t)C;
   // Test hook: TFE_TIER_CLOCK_START starts the recency clock elsewhere than
@@ -588,6 +616,12 @@ static tfe_status load(const tfe_table_desc* d, hipStream_t stream, tfe_table** 
     return fail(TFE_ERR_INVALID_ARG, "miss_fill must be TFE_FILL_INLINE or TFE_FILL_SIDE_STREAM");
   if (d->adopt_host_values && (d->hbm_cache_rows == 0 || d->values_on_device))
     return fail(TFE_ERR_INVALID_ARG, "adopt_host_values needs a tiered table and host values");
+  if (d->pinned_rows < 0 || d->pinned_rows > d->n_phrases)
+    return fail(TFE_ERR_INVALID_ARG, "pinned_rows outside [0, n_phrases]");
+  if (d->pinned_rows > 0 && d->pinned_rows < d->n_phrases &&
+      (d->hbm_cache_rows == 0 || d->values_on_device || !d->pageable_values))
+    return fail(TFE_ERR_INVALID_ARG,
+                "pinned_rows < n_phrases needs a tiered table, host values and pageable_values");
   tfe_status st = validate_phrases(d->phrase_tokens, d->phrase_len, d->n_phrases, d->n_min,
                                    d->n_max, d->vocab);
   if (st != TFE_OK) return st;

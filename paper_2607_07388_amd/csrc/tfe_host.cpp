@@ -8,6 +8,7 @@
 #include <string.h>
 
 #include <atomic>
+#include <chrono>
 #include <mutex>
 #include <thread>
 #include <unordered_map>
@@ -73,6 +74,41 @@ void note_free(const void* p) {
   if (it == h.live.end()) return;
   h.bytes[it->second.second] -= (int64_t)it->second.first;
   h.live.erase(it);
+}
+
+// A thread spins while requests keep coming and sleeps briefly once it has
+// been idle for a while; the first request after a quiet period therefore
+// waits up to about a tenth of a millisecond.
+void stage_serve(StageSlot* q, char* rows, const char* pageable, int64_t first_row,
+                 int64_t n_rows, size_t row_bytes, uint64_t first, uint64_t step,
+                 const volatile bool* stop) {
+  using clock = std::chrono::steady_clock;
+  constexpr auto kSpin = std::chrono::milliseconds(2);
+  uint64_t tk = first;
+  auto last = clock::now();
+  while (!__atomic_load_n(stop, __ATOMIC_ACQUIRE)) {
+    StageSlot& slot = q[tk % kStageSlots];
+    const unsigned long long r = __atomic_load_n(&slot.req, __ATOMIC_ACQUIRE);
+    if ((r >> 32) != ((tk + 1) & 0xFFFFFFFFull)) {
+      if (clock::now() - last < kSpin)
+        __builtin_ia32_pause();
+      else
+        std::this_thread::sleep_for(std::chrono::microseconds(20));
+      continue;
+    }
+    const int64_t i = (int64_t)(int32_t)(uint32_t)r - first_row;
+    char* dst = rows + (tk % kStageSlots) * row_bytes;
+    if (i >= 0 && i < n_rows)
+      memcpy(dst, pageable + i * (int64_t)row_bytes, row_bytes);
+    else
+      memset(dst, 0, row_bytes);
+    // The row's stores (memcpy may use non-temporal ones) are visible
+    // before the slot is marked done.
+    std::atomic_thread_fence(std::memory_order_seq_cst);
+    __atomic_store_n(&slot.done, tk + 1, __ATOMIC_RELEASE);
+    tk += step;
+    last = clock::now();
+  }
 }
 
 void memory_held(int64_t* device_bytes, int64_t* pinned_bytes) {

@@ -19,6 +19,33 @@ tfe_status fail(tfe_status st, const char* fmt, ...);
 void clear_error();
 const char* last_error();
 
+// Staging of pageable host rows.  Rows at or beyond a tiered table's pinned
+// rows live in pageable host memory, which the GPU cannot address; a wave
+// that needs one takes a ticket, and slot ticket mod kStageSlots of a queue
+// in coherent pinned host memory carries the request to the table's host
+// threads, which copy the row into the slot's staging row.  A requester
+// posts into a slot only once the slot's previous ticket has been read
+// (acknowledged in a word of its own, which only requesters use), so a
+// staging row is never overwritten while it is read.
+struct StageSlot {
+  unsigned long long req;   // requester: ((ticket + 1) mod 2^32) << 32 | row, one store
+  unsigned long long done;  // host: ticket + 1 once the staging row holds the row
+};
+constexpr uint32_t kStageSlots = 4096;  // requests in flight at most
+
+// The request word of `ticket` for row id `row` (0 never is one).
+TFE_HD unsigned long long stage_request(unsigned long long ticket, int32_t row) {
+  return (((ticket + 1) & 0xFFFFFFFFull) << 32) | (uint32_t)row;
+}
+
+// The serving loop of one host thread: tickets first, first + step, ... in
+// order, until *stop.  Row r >= first_row is copied from
+// pageable + (r - first_row) * row_bytes into rows + slot * row_bytes; other
+// ids (never asked for) read as zeros.
+void stage_serve(StageSlot* q, char* rows, const char* pageable, int64_t first_row,
+                 int64_t n_rows, size_t row_bytes, uint64_t first, uint64_t step,
+                 const volatile bool* stop);
+
 // Allocation-failure hook: with TFE_FAIL_ALLOC=k in the environment, the
 // k-th allocation of a library call (counted from its clear_error) fails as
 // if memory had run out.  Every allocation asks this first.
@@ -54,8 +81,24 @@ inline void begin_call() {
 // memory: they honour the failure hook and keep the held-memory count.
 hipError_t dev_malloc(void** p, size_t n);
 void dev_free(void* p);
-hipError_t pinned_malloc(void** p, size_t n);
+hipError_t pinned_malloc(void** p, size_t n, unsigned flags = hipHostMallocDefault);
 void pinned_free(void* p);
+
+// Host side of the pageable-row staging: a coherent pinned queue of
+// kStageSlots slots and staging rows, served by host threads that copy the
+// requested rows out of the caller's pageable memory.
+struct Stager;
+struct StageSlot;
+// Starts the queue and `threads` host threads for rows [pinned_rows, P) at
+// `pageable` (row_bytes each); *out owns them.
+tfe_status stager_start(const void* pageable, int64_t pinned_rows, int64_t n_phrases,
+                        size_t row_bytes, int threads, Stager** out);
+// Device addresses of the queue and of the staging rows.
+StageSlot* stager_queue(const Stager* s);
+const void* stager_rows(const Stager* s);
+// Stops and joins the threads and frees the queue (the table's work that
+// may still post requests must be finished).
+void stager_stop(Stager* s);
 
 // Per-call arguments of the lookup + inject kernels.
 struct LookupArgs {
@@ -101,8 +144,10 @@ struct TierCtl {
   // Device-side ordering of decode lookups and prefetches (no HIP events):
   unsigned long long lk_done;     // decode calls done with the shared state (monotone)
   unsigned long long pf_done;     // prefetch copy blocks done (monotone)
+  unsigned long long stage_ticket;  // pageable rows: staging requests issued (monotone)
   TierStats stats;
 };
+
 struct TierJob {
   int32_t row, slot;
 };
@@ -138,6 +183,11 @@ struct TierArgs {
   // a decode call and the copy blocks count themselves in when done.
   unsigned long long wait_lk, wait_pf;
   uint32_t count_lookup, count_fill;
+  // Rows [pinned_rows, P) are pageable: read through the staging queue.
+  uint32_t pinned_rows;       // P when every row is pinned
+  StageSlot* stage;           // device address of the queue [kStageSlots]
+  unsigned long long* stage_ack;  // [kStageSlots] device memory: ticket + 1 of the last read
+  const void* stage_rows;     // device address of the staging rows [kStageSlots x dim]
 };
 
 // Phase bit of a position whose inject writes its row into slot_of (inline
@@ -213,9 +263,12 @@ struct tfe_table {
   int64_t cache_rows = 0;
   int64_t prefill_rows = 0;
   int32_t fill_mode = 0;         // tfe_fill_mode
-  void* h_values = nullptr;      // pinned host rows [P x dim]
+  void* h_values = nullptr;      // pinned host rows [pinned_rows x dim]
   const void* h_values_dev = nullptr;
   bool own_h_values = false;
+  int64_t pinned_rows = 0;       // rows [pinned_rows, P) are pageable (caller's memory)
+  tfe::Stager* stager = nullptr;  // queue and host threads of the pageable rows
+  unsigned long long* d_stage_ack = nullptr;  // [kStageSlots] with a stager
   void* d_cache = nullptr;
   int32_t* d_where = nullptr;
   int32_t* d_owner = nullptr;

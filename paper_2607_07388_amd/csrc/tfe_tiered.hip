@@ -114,6 +114,95 @@ __device__ __forceinline__ void wait_ordered_block(const TierArgs& t) {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
 }
 
+// Reads a value row that is not cached.  Rows below t.pinned_rows are read
+// straight from pinned host memory (zero-copy over PCIe; NT: non-temporal).
+// Rows at or beyond it are pageable: the wave's first lane takes a ticket,
+// waits until the ticket's queue slot is free (the slot's previous ticket
+// has been read: its ack word in device memory), posts ticket and row in
+// one word, and waits until a host thread has staged the row; the whole
+// wave then reads the staged row and the first lane frees the slot.  The
+// queue and the staged rows are coherent host memory, written, polled and
+// read with system-scope accesses (sc0 sc1) that bypass the GPU caches; no
+// fence is needed, and none is used: a system-scope acquire would
+// invalidate the whole L2 once per staged row.  The polls back off -- about 0.4 us apart at first,
+// then 1.7, 3.4 and at last 54 us -- so that the thousands of waves of a
+// long call that wait behind each other in the queue do not crowd the host
+// link with reads (polling every few microseconds, 2000 waves read about
+// 40 GB/s and starve both the polls and the zero-copy row reads).
+// The waits are bounded (seconds); one that runs out is counted in
+// ctl->wait_timeouts (tfe_get_stats then reports an error) and the row
+// reads as zeros.  `row` is wave-uniform.
+constexpr uint32_t kStageWaitLimit = 1u << 17;  // polls: seconds at the longest interval
+
+__device__ __forceinline__ bool wait_host_done(TierCtl* ctl, const unsigned long long* p,
+                                               unsigned long long want) {
+  for (uint32_t n = 0; n < kStageWaitLimit; ++n) {
+    if (__hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM) == want) return true;
+    if (n < 4) {
+      __builtin_amdgcn_s_sleep(16);
+    } else if (n < 16) {
+      __builtin_amdgcn_s_sleep(64);
+    } else if (n < 48) {
+      __builtin_amdgcn_s_sleep(127);
+    } else {
+      for (int k = 0; k < 16; ++k) __builtin_amdgcn_s_sleep(127);
+    }
+  }
+  atomicAdd(&ctl->wait_timeouts, 1u);
+  return false;
+}
+
+__device__ __forceinline__ bool wait_slot_free(TierCtl* ctl, const unsigned long long* p,
+                                               unsigned long long want) {
+  for (uint32_t n = 0; n < kStageWaitLimit; ++n) {
+    if (__hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == want) return true;
+    __builtin_amdgcn_s_sleep(64);
+  }
+  atomicAdd(&ctl->wait_timeouts, 1u);
+  return false;
+}
+
+template <int NCH, bool NT>
+__device__ __forceinline__ void read_host_row(const TierArgs& t, int32_t row, u32x4* v,
+                                              int lane) {
+  constexpr int ROW_VECS = NCH * 64;
+  if ((uint32_t)row < t.pinned_rows) {
+    const u32x4* src = (const u32x4*)t.host_values + (size_t)row * ROW_VECS;
+#pragma unroll
+    for (int k = 0; k < NCH; ++k)
+      v[k] = NT ? __builtin_nontemporal_load(src + k * 64 + lane) : src[k * 64 + lane];
+    return;
+  }
+  unsigned long long tk = 0;
+  uint32_t slot = 0, ok = 0;
+  if (lane == 0) {
+    tk = __hip_atomic_fetch_add(&t.ctl->stage_ticket, 1ull, __ATOMIC_RELAXED,
+                                __HIP_MEMORY_SCOPE_AGENT);
+    slot = (uint32_t)(tk % kStageSlots);
+    ok = wait_slot_free(t.ctl, t.stage_ack + slot,
+                        tk >= kStageSlots ? tk + 1 - kStageSlots : 0ull);
+    if (ok) {
+      __hip_atomic_store(&t.stage[slot].req, stage_request(tk, row), __ATOMIC_RELAXED,
+                         __HIP_MEMORY_SCOPE_SYSTEM);
+      ok = wait_host_done(t.ctl, &t.stage[slot].done, tk + 1);
+    }
+  }
+  slot = __builtin_amdgcn_readfirstlane(slot);
+  ok = __builtin_amdgcn_readfirstlane(ok);
+  // Buffer loads with cache policy sc0 | sc1 (= 1 | 16): read from host
+  // memory, past the L2.  The resource covers the slot's staging row.
+  const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)((const u32x4*)t.stage_rows + (size_t)slot * ROW_VECS), (short)0, ROW_VECS * 16,
+      0x00020000);
+#pragma unroll
+  for (int k = 0; k < NCH; ++k)
+    v[k] = ok ? (u32x4)__builtin_amdgcn_raw_buffer_load_b128(rs, (k * 64 + lane) * 16, 0, 17)
+              : u32x4{0u, 0u, 0u, 0u};
+  wait_mem();
+  if (lane == 0 && ok)
+    __hip_atomic_store(t.stage_ack + slot, tk + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
 // Takes up to `need` least-recent slots not referenced in this call (stamp
 // below the call's clock) from the tail of the ring into vict[0..got).
 // Dead entries passed on the way are dropped.  Returns got (block-uniform).
@@ -1285,11 +1374,9 @@ __global__ __launch_bounds__(256) void k_fill(const TierArgs t, uint32_t max_job
   const uint32_t j = blockIdx.x * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   if (j < max_jobs && j < t.ctl->njobs) {
     const TierJob job = t.jobs[j];
-    const u32x4* src = (const u32x4*)t.host_values + (size_t)job.row * (NCH * 64);
     u32x4* dst = (u32x4*)t.cache + (size_t)job.slot * (NCH * 64);
     u32x4 v[NCH];
-#pragma unroll
-    for (int k = 0; k < NCH; ++k) v[k] = __builtin_nontemporal_load(src + k * 64 + lane);
+    read_host_row<NCH, true>(t, __builtin_amdgcn_readfirstlane(job.row), v, lane);
 #pragma unroll
     for (int k = 0; k < NCH; ++k) dst[k * 64 + lane] = v[k];
   }
@@ -1372,11 +1459,14 @@ __global__ __launch_bounds__(WPB * 64) void k_tier_inject(const TierArgs t) {
     }
     return;
   }
-  const u32x4* mrow = ph != 0 ? (const u32x4*)t.host_values + (size_t)t.row_of[p] * ROW_VECS
-                              : (const u32x4*)t.cache + (size_t)t.slot_of[p] * ROW_VECS;
   u32x4 mv[NCH];
+  if (ph != 0) {
+    read_host_row<NCH, false>(t, __builtin_amdgcn_readfirstlane(t.row_of[p]), mv, lane);
+  } else {
+    const u32x4* mrow = (const u32x4*)t.cache + (size_t)t.slot_of[p] * ROW_VECS;
 #pragma unroll
-  for (int k = 0; k < NCH; ++k) mv[k] = mrow[k * 64 + lane];
+    for (int k = 0; k < NCH; ++k) mv[k] = mrow[k * 64 + lane];
+  }
   if (ph_w & kPhaseWrite) {
     u32x4* dst = (u32x4*)t.cache + (size_t)t.slot_of[p] * ROW_VECS;
 #pragma unroll
@@ -1655,9 +1745,7 @@ __global__ __launch_bounds__(64) void k_tier_decode(const TierArgs t) {
   } else {
     // Host only: the row is read once, written into this position's spare
     // slot (which no row maps to, so no wave reads it), and injected.
-    const u32x4* mrow = (const u32x4*)t.host_values + (size_t)row * ROW_VECS;
-#pragma unroll
-    for (int k = 0; k < NCH; ++k) mv[k] = mrow[k * 64 + lane];
+    read_host_row<NCH, false>(t, __builtin_amdgcn_readfirstlane(row), mv, lane);
     u32x4* dst = (u32x4*)t.cache + (size_t)sp * ROW_VECS;
 #pragma unroll
     for (int k = 0; k < NCH; ++k) dst[k * 64 + lane] = mv[k];

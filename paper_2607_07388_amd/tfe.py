@@ -41,6 +41,8 @@ class tfe_table_desc(ctypes.Structure):
         ("adopt_host_values", ctypes.c_int32),
         ("prefill_rows", ctypes.c_int64),
         ("miss_fill", ctypes.c_int32),
+        ("pinned_rows", ctypes.c_int64),
+        ("pageable_values", ctypes.c_void_p),
     ]
 
 
@@ -269,7 +271,7 @@ def tfe_index_probe_host(slots, capacity, tokens, n):
 
 def make_desc(phrase_tokens, phrase_len, n_min, n_max, vocab, values, dim, dtype,
               values_on_device, max_load_factor=0.5, hbm_cache_rows=0, adopt_host_values=0,
-              prefill_rows=0, miss_fill=0):
+              prefill_rows=0, miss_fill=0, pinned_rows=0, pageable_values=None):
     """Fills a tfe_table_desc; the caller keeps the arrays alive until
     tfe_table_load returns (and `values` for the table's life if adopted)."""
     d = tfe_table_desc()
@@ -284,4 +286,6 @@ def make_desc(phrase_tokens, phrase_len, n_min, n_max, vocab, values, dim, dtype
     d.adopt_host_values = adopt_host_values
     d.prefill_rows = prefill_rows
     d.miss_fill = miss_fill
+    d.pinned_rows = pinned_rows
+    d.pageable_values = addr(pageable_values)
     return d

@@ -19,6 +19,8 @@
    that cannot pin 128 GiB.  The HBM cache has 4M rows (8 GiB).
 """
 import functools
+import sys
+import time
 
 import numpy as np
 
@@ -97,11 +99,20 @@ def workload3_stream():
 
 
 def _freq_table(seed, s, stream_len, per_n, stop=None):
+    # Builds over 2^28 tokens take minutes: each finished stage is reported.
+    loud = stream_len >= 1 << 28
+    t0 = time.time()
     stream = corpus_stream(seed, s, stream_len)
+    if loud:
+        print("# synth: %d-token stream (%.0f s)" % (stream_len, time.time() - t0),
+              file=sys.stderr, flush=True)
     parts = []
     for j, (n, want) in enumerate(per_n):
         skip = 0 if stop is None else stop[j]
         parts.append(ngram_top(stream, n, want, skip=skip))
+        if loud:
+            print("# synth: top %d %d-grams (%.0f s)" % (want, n, time.time() - t0),
+                  file=sys.stderr, flush=True)
     del stream
     n_max = max(n for n, _ in per_n)
     toks, lens, _ = stack_tables(parts, n_max)

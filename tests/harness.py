@@ -35,6 +35,23 @@ def device_values(table):
     return v
 
 
+def pageable_values(table, first, stream=None, chunk=1 << 19):
+    """Value rows [first, P) of `table` (bf16) in ordinary pageable host
+    memory, drawn on the device chunk by chunk and copied down."""
+    stream = stream or torch.cuda.current_stream()
+    P, D = table.n_phrases, table.dim
+    host = np.empty((P - first, D), np.int16)
+    ht = torch.from_numpy(host)
+    dbuf = torch.empty((min(chunk, P - first), D), dtype=torch.bfloat16, device="cuda")
+    for r0 in range(first, P, chunk):
+        n = min(chunk, P - r0)
+        synth.normal_fill_device(dbuf.data_ptr(), r0, n, D, table.seed, synth.TAG_VALUES,
+                                 table.sigma, synth.BF16, stream.cuda_stream)
+        ht[r0 - first:r0 - first + n].copy_(dbuf[:n].view(torch.int16))
+    torch.cuda.synchronize()
+    return host
+
+
 def to_device(a, dtype):
     """Host array (float32, or uint16 bf16 patterns) -> device tensor."""
     if dtype == synth.BF16:

@@ -213,12 +213,77 @@ static void hook_and_held_memory() {
   CHECK(tfe_memory_held(&d1, nullptr) == TFE_OK && d1 == 0);
 }
 
+// The staging queue of pageable rows (StageSlot, stage_serve) with emulated
+// requesters following the kernels' protocol: take a ticket, wait until the
+// slot's previous ticket is acknowledged, post the row and then the ticket,
+// wait for done, check the staged row against the pageable one, acknowledge.
+// More requests than slots, several requesters and two serving threads.
+static void staging_protocol() {
+  const int64_t first_row = 1000, n_rows = 20000;
+  const size_t row_bytes = 256;
+  std::vector<char> pageable((size_t)n_rows * row_bytes);
+  for (size_t i = 0; i < pageable.size(); ++i) pageable[i] = (char)((i * 131u) >> 3);
+  std::vector<tfe::StageSlot> q(tfe::kStageSlots);
+  memset(q.data(), 0, q.size() * sizeof(tfe::StageSlot));
+  std::vector<char> rows((size_t)tfe::kStageSlots * row_bytes);
+  volatile bool stop = false;
+  const int servers = 2;
+  std::vector<std::thread> serve;
+  for (int i = 0; i < servers; ++i)
+    serve.emplace_back(tfe::stage_serve, q.data(), rows.data(), pageable.data(), first_row,
+                       n_rows, row_bytes, (uint64_t)i, (uint64_t)servers, &stop);
+  std::vector<unsigned long long> ack(tfe::kStageSlots, 0);  // device memory on the GPU
+  unsigned long long ticket = 0;
+  const int requesters = 8, per = 7500;  // 60000 requests: the queue wraps 14 times
+  std::vector<int> bad(requesters, 0);
+  std::vector<std::thread> req;
+  for (int w = 0; w < requesters; ++w)
+    req.emplace_back([&, w] {
+      uint64_t x = 0x9E3779B97F4A7C15ull * (w + 1);
+      for (int r = 0; r < per; ++r) {
+        x ^= x << 13;
+        x ^= x >> 7;
+        x ^= x << 17;
+        const int32_t row = (int32_t)(first_row + (int64_t)(x % (uint64_t)n_rows));
+        const unsigned long long tk = __atomic_fetch_add(&ticket, 1ull, __ATOMIC_RELAXED);
+        const size_t k = tk % tfe::kStageSlots;
+        tfe::StageSlot& sl = q[k];
+        const unsigned long long prev = tk >= tfe::kStageSlots ? tk + 1 - tfe::kStageSlots : 0;
+        while (__atomic_load_n(&ack[k], __ATOMIC_ACQUIRE) != prev) std::this_thread::yield();
+        __atomic_store_n(&sl.req, tfe::stage_request(tk, row), __ATOMIC_RELEASE);
+        while (__atomic_load_n(&sl.done, __ATOMIC_ACQUIRE) != tk + 1) std::this_thread::yield();
+        const char* got = rows.data() + k * row_bytes;
+        const char* want = pageable.data() + (size_t)(row - first_row) * row_bytes;
+        if (memcmp(got, want, row_bytes) != 0) ++bad[(size_t)w];
+        __atomic_store_n(&ack[k], tk + 1, __ATOMIC_RELEASE);
+      }
+    });
+  for (auto& t : req) t.join();
+  __atomic_store_n(&stop, true, __ATOMIC_RELEASE);
+  for (auto& t : serve) t.join();
+  for (int w = 0; w < requesters; ++w) CHECK(bad[(size_t)w] == 0);
+  CHECK(ticket == (unsigned long long)requesters * per);
+  // A row id outside the pageable range (never asked for by the kernels)
+  // is staged as zeros.
+  memset(q.data(), 0, q.size() * sizeof(tfe::StageSlot));
+  memset(rows.data(), 0x5A, row_bytes);
+  stop = false;
+  std::thread one(tfe::stage_serve, q.data(), rows.data(), pageable.data(), first_row, n_rows,
+                  row_bytes, (uint64_t)0, (uint64_t)1, &stop);
+  __atomic_store_n(&q[0].req, tfe::stage_request(0, (int32_t)(first_row - 1)), __ATOMIC_RELEASE);
+  while (__atomic_load_n(&q[0].done, __ATOMIC_ACQUIRE) != 1ull) std::this_thread::yield();
+  for (size_t i = 0; i < row_bytes; ++i) CHECK(rows[i] == 0);
+  __atomic_store_n(&stop, true, __ATOMIC_RELEASE);
+  one.join();
+}
+
 int main() {
   validation_errors();
   build_and_probe_all(1 << 20);
   build_and_probe_all(5);
   duplicates();
   hook_and_held_memory();
+  staging_protocol();
   printf("ok\n");
   return 0;
 }

@@ -101,28 +101,37 @@ def test_every_allocation_of_a_resident_load(w2):
     assert tfe.tfe_memory_held() == base
 
 
-@pytest.mark.parametrize("adopt", [False, True])
-def test_every_allocation_of_a_tiered_load(w2, adopt):
+@pytest.mark.parametrize("adopt,split", [(False, False), (True, False), (False, True)])
+def test_every_allocation_of_a_tiered_load(w2, adopt, split):
+    """split: the upper half of the rows stays in pageable memory behind the
+    staging queue (its acknowledgement words, state and pinned queue)."""
     table, _ = w2
+    P = table.n_phrases
+    Pp = P // 2 if split else P
     pinned = pinned_values(table) if adopt else None
     host = None if adopt else table.all_values()
+    pageable = np.ascontiguousarray(host[Pp:]) if split else None
     base = tfe.tfe_memory_held()
 
     def load():
         desc = tfe.make_desc(table.tokens, table.lens, table.n_min, table.n_max, table.vocab,
-                             pinned if adopt else host, table.dim, table.dtype, 0, 0.5,
+                             pinned if adopt else host[:Pp], table.dim, table.dtype, 0, 0.5,
                              hbm_cache_rows=4096, adopt_host_values=int(adopt),
-                             prefill_rows=1024)
+                             prefill_rows=1024, pinned_rows=Pp if split else 0,
+                             pageable_values=pageable)
         return tfe.tfe_table_load(desc, H.cur_stream())
 
     h, msgs = fail_every_allocation(load)
     want = ["host index", "table object", "device index"] + ([] if adopt else ["pinned host values"])
+    if split:
+        want += ["staging acknowledgements", "staging state", "staging queue", "staging queue"]
     want += ["HBM cache", "residency map", "slot owners", "slot stamps", "prefetch flags",
              "spare slots", "recency ring", "recency ring", "tier control block"]
     assert names(msgs) == want
     d, p = tfe.tfe_memory_held()
     esz = 2 if table.dtype == synth.BF16 else 4
-    assert d > base[0] and p == base[1] + (0 if adopt else table.n_phrases * table.dim * esz)
+    staging = 4096 * 16 + 4096 * table.dim * esz if split else 0
+    assert d > base[0] and p == base[1] + (0 if adopt else Pp * table.dim * esz) + staging
     tfe.tfe_table_free(h)
     assert tfe.tfe_memory_held() == base
     del pinned
