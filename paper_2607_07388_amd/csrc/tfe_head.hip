@@ -57,10 +57,9 @@ __device__ __forceinline__ uint32_t f2key(float f) {
 __device__ __forceinline__ float key2f(uint32_t k) {
   return __uint_as_float((k & 0x80000000u) ? (k & 0x7FFFFFFFu) : ~k);
 }
-// 64-bit unsigned max / min (the generic max/min overloads can resolve to
+// 64-bit unsigned max (the generic max/min overloads can resolve to
 // floating point for mixed integer types, which would round the keys).
 __device__ __forceinline__ uint64_t umax64(uint64_t x, uint64_t y) { return x > y ? x : y; }
-__device__ __forceinline__ uint64_t umin64(uint64_t x, uint64_t y) { return x < y ? x : y; }
 // (logit, token) -> 64-bit key: higher logit first, then lower token id.
 // Keys are distinct, and 0 is below every real key.
 __device__ __forceinline__ uint64_t tkey64(float l, uint32_t id) {
@@ -463,7 +462,10 @@ __global__ __launch_bounds__(kRowThreads) void k_head_rows(const HeadArgs a) {
     }
   }
   // Candidate tiles: the keys whose masked bits reach the prefix (at most
-  // max(K, kStopCand) of them); every answer logit is at or above the prefix.
+  // max(K, kStopCand) of them, the keys being distinct); every answer logit
+  // is at or above the prefix.  The list is cut at its capacity all the same,
+  // so that statistics that were never written (equal keys) cannot make the
+  // block write past it.
   uint32_t mine = 0;
 #pragma unroll
   for (int i = 0; i < kRowTiles; ++i)
@@ -473,8 +475,12 @@ __global__ __launch_bounds__(kRowThreads) void k_head_rows(const HeadArgs a) {
 #pragma unroll
   for (int i = 0; i < kRowTiles; ++i) {
     const uint32_t t = tid + i * kRowThreads;
-    if (t < NT && (key[i] & mask) >= prefix) s_tiles[off++] = t;
+    if (t < NT && (key[i] & mask) >= prefix) {
+      if (off < (uint32_t)kHeadMaxK) s_tiles[off] = t;
+      ++off;
+    }
   }
+  ntile = min(ntile, (uint32_t)kHeadMaxK);
   // (With all tiles taken, every logit is a candidate.)
   const uint64_t tau = take == NT ? 0 : (common | prefix);
   __syncthreads();
