@@ -1187,80 +1187,95 @@ __device__ uint32_t resolve_scored(const TierArgs& t, uint32_t N, const float* _
   }
   const uint32_t n = s_n, nref = s_nref;
   const uint32_t want = n < budget ? n : budget;
-  // 3. The want smallest keys: radix select of the threshold, then gather.
-  uint64_t prefix = 0, pmask = 0;
-  if (want > 0 && want < n) {
-    uint32_t rem = want;  // keys still to take at or below the prefix
-    for (int shift = 56; shift >= 0; shift -= 8) {
-      for (int i = threadIdx.x; i < 256; i += kResolveThreads) hist[i] = 0;
-      __syncthreads();
-      for (uint32_t i = threadIdx.x; i < n; i += kResolveThreads) {
-        const uint64_t k = klist[i];
-        if ((k & pmask) == prefix) atomicAdd(&hist[(k >> shift) & 255], 1u);
-      }
-      __syncthreads();
-      if (threadIdx.x < 64) {
-        // The bin where the running count reaches rem: lane l sums bins
-        // 4l .. 4l+3, then a wave scan.
-        const uint32_t c0 = hist[4 * threadIdx.x], c1 = hist[4 * threadIdx.x + 1],
-                       c2 = hist[4 * threadIdx.x + 2], c3 = hist[4 * threadIdx.x + 3];
-        uint32_t x = c0 + c1 + c2 + c3;
-        for (int d = 1; d < 64; d <<= 1) {
-          const uint32_t y = __shfl_up(x, d, 64);
-          if ((int)threadIdx.x >= d) x += y;
-        }
-        const uint32_t before = x - (c0 + c1 + c2 + c3);
-        if (before < rem && x >= rem) {
-          uint32_t b = 4 * threadIdx.x, acc = before;
-          const uint32_t cs[4] = {c0, c1, c2, c3};
-          int j = 0;
-          while (acc + cs[j] < rem) acc += cs[j++];
-          s_bin = b + j;
-          s_before = acc;
-        }
-      }
-      __syncthreads();
-      const uint32_t bin = s_bin;
-      rem -= s_before;
-      prefix |= (uint64_t)bin << shift;
-      pmask |= 255ull << shift;
-      const bool exact = hist[bin] == rem;  // every key of this prefix is taken
-      __syncthreads();
-      if (exact) break;
+  // 3. The want smallest keys, in ascending order, into sel.  Keys are
+  // distinct (they end in the candidate index).  Up to one key per thread:
+  // each thread counts the smaller keys and a key of rank below want goes
+  // to sel[rank] (a few hundred broadcast reads instead of select passes
+  // and a sort, each a series of barriers).  More keys: a radix select of
+  // the threshold, a gather and a bitonic sort.
+  if (n <= (uint32_t)kResolveThreads) {
+    if (want > 0 && threadIdx.x < n) {
+      const uint64_t k = klist[threadIdx.x];
+      uint32_t rank = 0;
+      for (uint32_t u = 0; u < n; ++u) rank += klist[u] < k ? 1u : 0u;
+      if (rank < want) sel[rank] = k;
     }
-  }
-  const uint64_t thresh = want == 0 ? 0 : (want < n ? (prefix | ~pmask) : ~0ull);
-  if (want > 0) {
-    for (uint32_t base = 0; base < n; base += kResolveThreads) {
-      const uint32_t i = base + threadIdx.x;
-      const uint64_t k = i < n ? klist[i] : ~0ull;
-      const bool take = i < n && k <= thresh;
-      uint32_t c;
-      const uint32_t rk = block_count(take, &c);
-      if (take) sel[s_g + rk] = k;
-      __syncthreads();
-      if (threadIdx.x == 0) s_g += c;
-      __syncthreads();
-    }
-  }
-  uint32_t p2 = 1;
-  while (p2 < want) p2 <<= 1;
-  for (uint32_t i = want + threadIdx.x; i < p2; i += kResolveThreads) sel[i] = ~0ull;
-  __syncthreads();
-  // Bitonic sort, ascending: highest score first, then lowest candidate index.
-  for (uint32_t size = 2; size <= p2; size <<= 1) {
-    for (uint32_t stride = size >> 1; stride > 0; stride >>= 1) {
-      for (uint32_t i = threadIdx.x; i < p2 / 2; i += kResolveThreads) {
-        const uint32_t a = 2 * i - (i & (stride - 1));
-        const uint32_t b = a + stride;
-        const bool up = (a & size) == 0;
-        const unsigned long long ka = sel[a], kb = sel[b];
-        if ((ka > kb) == up) {
-          sel[a] = kb;
-          sel[b] = ka;
+    __syncthreads();
+  } else {
+    uint64_t prefix = 0, pmask = 0;
+    if (want > 0 && want < n) {
+      uint32_t rem = want;  // keys still to take at or below the prefix
+      for (int shift = 56; shift >= 0; shift -= 8) {
+        for (int i = threadIdx.x; i < 256; i += kResolveThreads) hist[i] = 0;
+        __syncthreads();
+        for (uint32_t i = threadIdx.x; i < n; i += kResolveThreads) {
+          const uint64_t k = klist[i];
+          if ((k & pmask) == prefix) atomicAdd(&hist[(k >> shift) & 255], 1u);
         }
+        __syncthreads();
+        if (threadIdx.x < 64) {
+          // The bin where the running count reaches rem: lane l sums bins
+          // 4l .. 4l+3, then a wave scan.
+          const uint32_t c0 = hist[4 * threadIdx.x], c1 = hist[4 * threadIdx.x + 1],
+                         c2 = hist[4 * threadIdx.x + 2], c3 = hist[4 * threadIdx.x + 3];
+          uint32_t x = c0 + c1 + c2 + c3;
+          for (int d = 1; d < 64; d <<= 1) {
+            const uint32_t y = __shfl_up(x, d, 64);
+            if ((int)threadIdx.x >= d) x += y;
+          }
+          const uint32_t before = x - (c0 + c1 + c2 + c3);
+          if (before < rem && x >= rem) {
+            uint32_t b = 4 * threadIdx.x, acc = before;
+            const uint32_t cs[4] = {c0, c1, c2, c3};
+            int j = 0;
+            while (acc + cs[j] < rem) acc += cs[j++];
+            s_bin = b + j;
+            s_before = acc;
+          }
+        }
+        __syncthreads();
+        const uint32_t bin = s_bin;
+        rem -= s_before;
+        prefix |= (uint64_t)bin << shift;
+        pmask |= 255ull << shift;
+        const bool exact = hist[bin] == rem;  // every key of this prefix is taken
+        __syncthreads();
+        if (exact) break;
       }
-      __syncthreads();
+    }
+    const uint64_t thresh = want == 0 ? 0 : (want < n ? (prefix | ~pmask) : ~0ull);
+    if (want > 0) {
+      for (uint32_t base = 0; base < n; base += kResolveThreads) {
+        const uint32_t i = base + threadIdx.x;
+        const uint64_t k = i < n ? klist[i] : ~0ull;
+        const bool take = i < n && k <= thresh;
+        uint32_t c;
+        const uint32_t rk = block_count(take, &c);
+        if (take) sel[s_g + rk] = k;
+        __syncthreads();
+        if (threadIdx.x == 0) s_g += c;
+        __syncthreads();
+      }
+    }
+    uint32_t p2 = 1;
+    while (p2 < want) p2 <<= 1;
+    for (uint32_t i = want + threadIdx.x; i < p2; i += kResolveThreads) sel[i] = ~0ull;
+    __syncthreads();
+    // Bitonic sort, ascending: highest score first, then lowest candidate index.
+    for (uint32_t size = 2; size <= p2; size <<= 1) {
+      for (uint32_t stride = size >> 1; stride > 0; stride >>= 1) {
+        for (uint32_t i = threadIdx.x; i < p2 / 2; i += kResolveThreads) {
+          const uint32_t a = 2 * i - (i & (stride - 1));
+          const uint32_t b = a + stride;
+          const bool up = (a & size) == 0;
+          const unsigned long long ka = sel[a], kb = sel[b];
+          if ((ka > kb) == up) {
+            sel[a] = kb;
+            sel[b] = ka;
+          }
+        }
+        __syncthreads();
+      }
     }
   }
   // 4. Victims and fills (the key list is no longer read: jobs are rewritten).
