@@ -1547,11 +1547,19 @@ __device__ __forceinline__ void walk_load_slots(const TierArgs& t, WalkWindow& w
   }
 }
 
-constexpr int kRefSet = 128;  // referenced-slot set of a decode call (LDS)
+// The keys of a decode call's positions, in an LDS hash: a cached row's
+// slot, or a missed row's id with bit 30 set (slots and rows are below 2^30,
+// so the two never meet).  At most kDecodeMaxT keys in kCallSet entries:
+// every insertion finds a free or equal entry.
+constexpr int kCallSet = 256;
+constexpr int32_t kRowKey = 0x40000000;
 
-__device__ __forceinline__ bool rset_has(const int32_t* rset, uint32_t slot) {
-  for (int q = (int)slot_hash(slot);; q = (q + 1) & (kRefSet - 1)) {
-    const int32_t v = rset[q];
+__device__ __forceinline__ uint32_t key_hash(uint32_t k) { return (k * 2654435761u) >> 24; }
+
+// Whether the call references cache slot `slot`.
+__device__ __forceinline__ bool call_has_slot(const int32_t* ckey, uint32_t slot) {
+  for (int q = (int)key_hash(slot);; q = (q + 1) & (kCallSet - 1)) {
+    const int32_t v = ckey[q];
     if (v == -1) return false;
     if ((uint32_t)v == slot) return true;
   }
@@ -1566,7 +1574,8 @@ template <int NCH>
 __device__ void decode_resolve_last(const TierArgs& t, uint32_t T, WalkWindow& w) {
   __shared__ uint32_t vict[kDecodeMaxT];
   __shared__ int32_t vown[kDecodeMaxT];
-  __shared__ int32_t rset[kRefSet];
+  __shared__ int32_t ckey[kCallSet];
+  __shared__ uint32_t cpos[kCallSet];
   const int lane = threadIdx.x;
   const bool valid = (uint32_t)lane < T;
   const int32_t r = valid ? ld_dev(t.row_of + lane) : -1;
@@ -1574,24 +1583,31 @@ __device__ void decode_resolve_last(const TierArgs& t, uint32_t T, WalkWindow& w
   const int32_t sp = t.spare[lane];
   const int32_t s0 = sw >= 0 ? (sw & ~kSlotPref) : -1;
   const bool pv = sw >= 0 && (sw & kSlotPref) != 0;
-  rset[lane] = -1;
-  rset[lane + 64] = -1;
-  // First position of each row: no lower lane holds it.
-  bool first = r >= 0;
-  for (int j = 0; j < (int)kDecodeMaxT; ++j) {
-    const int32_t rj = __builtin_amdgcn_readlane(r, j);
-    first = first && !(j < lane && rj == r);
+#pragma unroll
+  for (int i = 0; i < kCallSet / 64; ++i) {
+    ckey[lane + 64 * i] = -1;
+    cpos[lane + 64 * i] = kDecodeMaxT;
   }
-  const bool fc = first && s0 >= 0, fm = first && s0 < 0;
   __syncthreads();
-  if (fc) {  // referenced: never a victim of this call
-    int q = (int)slot_hash((uint32_t)s0);
-    while (atomicCAS(&rset[q], -1, s0) != -1) q = (q + 1) & (kRefSet - 1);
+  // First position of each row: the lowest lane with its key.  The cached
+  // slots in the table are the ones this call references, never victims.
+  int h = 0;
+  if (r >= 0) {
+    const int32_t key = s0 >= 0 ? s0 : (r | kRowKey);
+    h = (int)key_hash((uint32_t)key);
+    for (;;) {
+      const int32_t prev = atomicCAS(&ckey[h], -1, key);
+      if (prev == -1 || prev == key) break;
+      h = (h + 1) & (kCallSet - 1);
+    }
+    atomicMin(&cpos[h], (uint32_t)lane);
   }
+  __syncthreads();
+  const bool first = r >= 0 && cpos[h] == (uint32_t)lane;
+  const bool fc = first && s0 >= 0, fm = first && s0 < 0;
   const uint64_t mfm = __builtin_amdgcn_ballot_w64(fm);
   const uint32_t need = (uint32_t)__builtin_popcountll(mfm);
   const uint32_t mrank = lanes_below(mfm);
-  __syncthreads();  // rset
   unsigned long long tail = w.tail;
   const unsigned long long head = w.head;
   uint32_t got = 0;
@@ -1617,7 +1633,7 @@ __device__ void decode_resolve_last(const TierArgs& t, uint32_t T, WalkWindow& w
       const uint64_t mcur = __builtin_amdgcn_ballot_w64(cur);
       const uint32_t lim = mcur ? (uint32_t)__builtin_ctzll(mcur) : 64u;
       const bool live = in && !cur && w.sn[k] == st && (uint32_t)lane < lim &&
-                        !rset_has(rset, slot);
+                        !call_has_slot(ckey, slot);
       const uint64_t ml = __builtin_amdgcn_ballot_w64(live);
       const uint32_t nl = (uint32_t)__builtin_popcountll(ml);
       const uint32_t rk = lanes_below(ml);
@@ -1628,9 +1644,8 @@ __device__ void decode_resolve_last(const TierArgs& t, uint32_t T, WalkWindow& w
       }
       if (take == need - got && take > 0) {
         // Resume after the last victim taken.
-        uint64_t m = ml;
-        for (uint32_t q = 1; q < take; ++q) m &= m - 1;
-        tail = base + (uint64_t)__builtin_ctzll(m) + 1;
+        const uint64_t mlast = __builtin_amdgcn_ballot_w64(live && rk == take - 1);
+        tail = base + (uint64_t)__builtin_ctzll(mlast) + 1;
         got = need;
         stop = true;
         continue;
