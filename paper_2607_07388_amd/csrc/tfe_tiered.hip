@@ -1379,24 +1379,37 @@ __global__ __launch_bounds__(kResolveThreads) void k_prefetch_fused(
 
 __global__ void k_tier_wait(const TierArgs t) { wait_ordered_block(t); }
 
+// A wave's row stored with device scope (cache policy sc1): the stores
+// write through the XCD's L2, so once they have completed (wait_mem) the
+// row is visible to agent-scope readers on every XCD -- without the L2
+// writeback of a release fence, which cost about 7 us per block when the
+// blocks of a fill issued it together.
+template <int NCH>
+__device__ __forceinline__ void st_dev_row(u32x4* dst, const u32x4* v, int lane) {
+  const __amdgpu_buffer_rsrc_t rs =
+      __builtin_amdgcn_make_buffer_rsrc((void*)dst, (short)0, NCH * 64 * 16, 0x00020000);
+#pragma unroll
+  for (int k = 0; k < NCH; ++k)
+    __builtin_amdgcn_raw_buffer_store_b128(v[k], rs, (k * 64 + lane) * 16, 0, 16);
+}
+
 // Host row -> cache slot copies of the current fill list, one wave per job,
 // reading the pinned host rows directly over PCIe (zero-copy).
 // With t.count_fill each block then counts into ctl->pf_done once its
-// copies have reached memory (a lookup on another stream waits for it).
+// copies have completed (a lookup on another stream waits for it and then
+// acquires).
 template <int NCH>
 __global__ __launch_bounds__(256) void k_fill(const TierArgs t, uint32_t max_jobs) {
   const int lane = threadIdx.x & 63;
   const uint32_t j = blockIdx.x * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   if (j < max_jobs && j < t.ctl->njobs) {
     const TierJob job = t.jobs[j];
-    u32x4* dst = (u32x4*)t.cache + (size_t)job.slot * (NCH * 64);
     u32x4 v[NCH];
     read_host_row<NCH, true>(t, __builtin_amdgcn_readfirstlane(job.row), v, lane);
-#pragma unroll
-    for (int k = 0; k < NCH; ++k) dst[k * 64 + lane] = v[k];
+    st_dev_row<NCH>((u32x4*)t.cache + (size_t)job.slot * (NCH * 64), v, lane);
   }
   if (!t.count_fill) return;
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+  wait_mem();
   __syncthreads();
   if (threadIdx.x == 0)
     __hip_atomic_fetch_add(&t.ctl->pf_done, 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -1774,11 +1787,12 @@ __global__ __launch_bounds__(64) void k_tier_decode(const TierArgs t) {
     if (decode_arrive(t, p, row, sw)) decode_resolve_last<NCH>(t, a.T, win);
   } else {
     // Host only: the row is read once, written into this position's spare
-    // slot (which no row maps to, so no wave reads it), and injected.
+    // slot (which no row maps to, so no wave reads it), and injected.  The
+    // copy is a device-scope store that completes before the wave counts
+    // in, so no line of it is left in this XCD's L2 for a later fill of the
+    // same slot (after the call counts in) to be overwritten by.
     read_host_row<NCH, false>(t, __builtin_amdgcn_readfirstlane(row), mv, lane);
-    u32x4* dst = (u32x4*)t.cache + (size_t)sp * ROW_VECS;
-#pragma unroll
-    for (int k = 0; k < NCH; ++k) dst[k * 64 + lane] = mv[k];
+    st_dev_row<NCH>((u32x4*)t.cache + (size_t)sp * ROW_VECS, mv, lane);
     if (decode_arrive(t, p, row, -1)) decode_resolve_last<NCH>(t, a.T, win);
   }
   const float g = dev::gate_of<DT, NCH>(a, hv, mv);
