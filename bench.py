@@ -93,8 +93,8 @@ MULTI_SOURCES = ("paper_2607_07388_amd/csrc/tfe_multi.hip",
 # K = 128): k_head_logits + k_head_rows, from the passes in
 # profiles/k_head_logits_rows_v151936_d1024_b64_k128.md.
 PROFILED_TRAFFIC_HEAD = {
-    "sources_sha256": "a974fe4357de216f1cc8bccb408f007f145b3e7eaf98ff8d07141076c35d223a",
-    "bytes_per_launch": 372542834,
+    "sources_sha256": "f1721f6388df035969b08e57bb4955e283515d7ade4d1a1c77be2b417e23862f",
+    "bytes_per_launch": 372583509,
 }
 HEAD_SOURCES = ("paper_2607_07388_amd/csrc/tfe_head.hip",
                 "paper_2607_07388_amd/csrc/tfe_head.h",
@@ -105,8 +105,8 @@ HEAD_SOURCES = ("paper_2607_07388_amd/csrc/tfe_head.hip",
 # (every kernel of the call summed), from the passes in
 # profiles/tfe_ngram_top_zipf_streams.md.
 PROFILED_TRAFFIC_BUILD = {
-    "sources_sha256": "d60f5eddca08a4e580aeab57e7de74d67e850874b30c5c2478ebf29e1fde6f81",
-    "bytes_per_call": 8900284107,
+    "sources_sha256": "872c29d1ced338c490a937f579b39c901ac8bf1551c4200b56550a20a221c558",
+    "bytes_per_call": 8901000455,
 }
 BUILD_SOURCES = ("paper_2607_07388_amd/csrc/tfe_build.hip",)
 
