@@ -26,6 +26,17 @@ def release_pinned():
         empty()
 
 
+def release_device():
+    """Returns the device memory torch's caching allocator keeps after its
+    tensors died, and the library's idle construction scratch, so that a
+    large device allocation by the library that follows finds the memory."""
+    import gc
+    gc.collect()
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    tfe.tfe_ngram_release()
+
+
 def device_values(table):
     """The table's value rows drawn on the device (bit-identical to the host draw)."""
     v = torch.empty((table.n_phrases, table.dim), dtype=TORCH_DT[table.dtype], device="cuda")
@@ -80,7 +91,10 @@ class GpuTable:
                              vals if table.n_phrases else None, table.dim, table.dtype,
                              values_on_device, lf)
         self.handle = tfe.tfe_table_load(desc, cur_stream())
+        big = values_on_device and table.n_phrases * table.dim * 2 > (1 << 30)
         del vals
+        if big:  # the library holds its own copy now
+            release_device()
 
     def close(self):
         if self.handle:

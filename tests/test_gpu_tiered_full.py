@@ -31,6 +31,13 @@ def test_workload5_full_scale_tiered_equals_resident_and_oracle():
     H.release_pinned()
     held = torch.cuda.host_memory_stats().get("allocated_bytes.current", 0)
     print("# pinned bytes still held by torch: %d" % held, flush=True)
+    # Device memory that earlier tests freed stays reserved by torch's caching
+    # allocator, out of reach of the library's allocations (the two tables
+    # here need about 140 GB of HBM); idle construction scratch goes back too.
+    H.release_device()
+    free, total = torch.cuda.mem_get_info()
+    print("# device memory: %.1f of %.1f GB free; library holds %d bytes"
+          % (free / 1e9, total / 1e9, tfe.tfe_memory_held()[0]), flush=True)
     vals = torch.empty((Pp, D), dtype=torch.bfloat16, pin_memory=True)
     synth.normal_fill_device(synth.host_device_ptr(vals.data_ptr()), 0, Pp, D, table.seed,
                              synth.TAG_VALUES, table.sigma, synth.BF16, H.cur_stream())
