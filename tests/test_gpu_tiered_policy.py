@@ -257,6 +257,76 @@ def test_residency_of_resident_table_and_bad_ids(w2):
         tfe.tfe_residency(res.handle, rows, -1, out, H.cur_stream())
 
 
+def continuations(table, need):
+    """The table's 2-gram phrases grouped by first token: (first, seconds)
+    for the first tokens with at least `need` continuations, most first."""
+    two = np.flatnonzero(table.lens == 2)
+    f, s = table.tokens[two, 0], table.tokens[two, 1]
+    order = np.argsort(f, kind="stable")
+    f, s = f[order], s[order]
+    uniq, start, cnt = np.unique(f, return_index=True, return_counts=True)
+    out = []
+    for i in np.argsort(-cnt, kind="stable"):
+        if cnt[i] < need:
+            break
+        out.append((int(uniq[i]), s[start[i]:start[i] + cnt[i]]))
+    return out
+
+
+@pytest.mark.parametrize("K,many", [(64, True), (80, False), (80, True)])
+def test_scored_prefetch_selection_paths(w2, K, many):
+    """Eq. 17's budgeted selection ranks a call's distinct uncached candidate
+    rows by score: by counting when they number at most one per thread of
+    the resolving block, else by radix select, gather and sort -- in the
+    one-block prefetch (up to 4096 windows: K = 64) and in the global-memory
+    resolution (K = 80: 5120 windows).  Each row's candidates continue its
+    last token with 2-grams the table holds: all K of them (thousands of
+    distinct rows), or 4 of them and absent tokens otherwise (a few
+    hundred), so that each case takes the path it names (asserted from the
+    model's count).  Statistics and residency equal the model after every
+    call; outputs equal the resident table."""
+    table, res, ot = w2
+    B, C, pre, budget, steps = 64, 8192, 4096, 256, 4
+    groups = continuations(table, K)
+    assert len(groups) >= B * steps
+    tier = TieredTable(table, C, pre)
+    model = LruModel(C, pre, 2048)
+    rng = np.random.default_rng(K + int(many))
+    seqs = synth.zipf_tokens(1, 1500 + K, B * (steps + 3), 1.1).reshape(B, steps + 3)
+    # Scores fall with the candidate's rank, in equal pairs (ties).
+    prob = np.tile(((K - np.arange(K)) // 2 + 1).astype(np.float32), (B, 1))
+    prob /= prob.sum(axis=1, keepdims=True)
+    side = torch.cuda.Stream()
+    for s in range(steps):
+        hidden = synth.normal_range(17, s, 0, B, 1024, 1.0, synth.BF16)
+        rows = call(tier, res, table, np.ascontiguousarray(seqs[:, s:s + 3]), hidden)
+        model.lookup([int(r) for r in rows])
+        tail = np.full((B, 2), -1, np.int32)
+        cand = np.full((B, K), -1, np.int32)
+        take = K if many else 4
+        for b in range(B):
+            first, nexts = groups[s * B + b]
+            tail[b, 1] = first
+            cand[b, :take] = rng.choice(nexts, take, replace=False)
+        win = np.concatenate([np.repeat(tail, K, axis=0), cand.reshape(-1, 1)], axis=1)
+        _, crow, clen = ot.lookup(win, 2, 1)
+        cached = set(int(r) for r in model.resident())
+        n = len({int(r) for r in crow if r >= 0 and int(r) not in cached})
+        assert (n > 1024) if many else (0 < n <= 1024), n
+        tfe.tfe_prefetch_scored(tier.handle, torch.from_numpy(tail).cuda(), 2,
+                                torch.from_numpy(cand).cuda(), torch.from_numpy(prob).cuda(),
+                                B, K, budget, side)
+        model.prefetch_scored([int(r) for r in crow], [int(x) for x in clen], prob.ravel(),
+                              budget)
+        check_stats(tier, model)
+        check_residency(tier, model, table.n_phrases)
+    st = tfe.tfe_get_stats(tier.handle)
+    assert st["prefetch_filled"] > 0
+    if many:
+        assert st["prefetch_dropped"] > 0
+    tier.close()
+
+
 @pytest.mark.parametrize("budget", [64, 1024])
 def test_head_topk_feeds_scored_prefetch_at_batch64_k128(w2, budget):
     """The early-exit head's top 128 of a 151936-token vocabulary for 64 rows
