@@ -93,8 +93,8 @@ MULTI_SOURCES = ("paper_2607_07388_amd/csrc/tfe_multi.hip",
 # K = 128): k_head_logits + k_head_rows, from the passes in
 # profiles/k_head_logits_rows_v151936_d1024_b64_k128.md.
 PROFILED_TRAFFIC_HEAD = {
-    "sources_sha256": "f1721f6388df035969b08e57bb4955e283515d7ade4d1a1c77be2b417e23862f",
-    "bytes_per_launch": 372583509,
+    "sources_sha256": "13430fd830728ef3bc77491a784ac98fed71f501f65643be41c0a7a04e916146",
+    "bytes_per_launch": 372138399,
 }
 HEAD_SOURCES = ("paper_2607_07388_amd/csrc/tfe_head.hip",
                 "paper_2607_07388_amd/csrc/tfe_head.h",
