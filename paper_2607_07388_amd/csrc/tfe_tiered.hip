@@ -1561,11 +1561,12 @@ __device__ __forceinline__ void walk_load_slots(const TierArgs& t, WalkWindow& w
 }
 
 // The keys of a decode call's positions, in an LDS hash: a cached row's
-// slot, or a missed row's id with bit 30 set (slots and rows are below 2^30,
-// so the two never meet).  At most kDecodeMaxT keys in kCallSet entries:
-// every insertion finds a free or equal entry.
+// slot (in [0, 2^30)), or the bitwise complement of a missed row's id (in
+// [-2^31 + 1, -1]: rows are below 2^31 - 1), so the two never meet; empty
+// entries hold kCallEmpty, which neither can be.  At most kDecodeMaxT keys
+// in kCallSet entries: every insertion finds a free or equal entry.
 constexpr int kCallSet = 256;
-constexpr int32_t kRowKey = 0x40000000;
+constexpr int32_t kCallEmpty = INT32_MIN;
 
 __device__ __forceinline__ uint32_t key_hash(uint32_t k) { return (k * 2654435761u) >> 24; }
 
@@ -1573,8 +1574,8 @@ __device__ __forceinline__ uint32_t key_hash(uint32_t k) { return (k * 265443576
 __device__ __forceinline__ bool call_has_slot(const int32_t* ckey, uint32_t slot) {
   for (int q = (int)key_hash(slot);; q = (q + 1) & (kCallSet - 1)) {
     const int32_t v = ckey[q];
-    if (v == -1) return false;
-    if ((uint32_t)v == slot) return true;
+    if (v == kCallEmpty) return false;
+    if (v == (int32_t)slot) return true;
   }
 }
 
@@ -1598,7 +1599,7 @@ __device__ void decode_resolve_last(const TierArgs& t, uint32_t T, WalkWindow& w
   const bool pv = sw >= 0 && (sw & kSlotPref) != 0;
 #pragma unroll
   for (int i = 0; i < kCallSet / 64; ++i) {
-    ckey[lane + 64 * i] = -1;
+    ckey[lane + 64 * i] = kCallEmpty;
     cpos[lane + 64 * i] = kDecodeMaxT;
   }
   __syncthreads();
@@ -1606,11 +1607,11 @@ __device__ void decode_resolve_last(const TierArgs& t, uint32_t T, WalkWindow& w
   // slots in the table are the ones this call references, never victims.
   int h = 0;
   if (r >= 0) {
-    const int32_t key = s0 >= 0 ? s0 : (r | kRowKey);
+    const int32_t key = s0 >= 0 ? s0 : ~r;
     h = (int)key_hash((uint32_t)key);
     for (;;) {
-      const int32_t prev = atomicCAS(&ckey[h], -1, key);
-      if (prev == -1 || prev == key) break;
+      const int32_t prev = atomicCAS(&ckey[h], kCallEmpty, key);
+      if (prev == kCallEmpty || prev == key) break;
       h = (h + 1) & (kCallSet - 1);
     }
     atomicMin(&cpos[h], (uint32_t)lane);
