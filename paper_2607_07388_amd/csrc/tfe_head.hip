@@ -104,7 +104,7 @@ __device__ __forceinline__ float col_sum(float x) {
 // of 64), so the logits stores are in bounds and unconditional (columns
 // past B and tokens past V hold junk that nothing reads).
 __device__ __forceinline__ void tile_epilogue(const HeadArgs& a, uint32_t t, int r, int g,
-                                              const f32x4* acc) {
+                                              const f32x4* acc, uint64_t* bm) {
   const uint32_t i0 = t * 16 + 4 * g;
   const size_t tile = (size_t)blockIdx.y * a.tpitch + t;
 #pragma unroll
@@ -120,6 +120,7 @@ __device__ __forceinline__ void tile_epilogue(const HeadArgs& a, uint32_t t, int
     for (int q = 0; q < 4; ++q)
       best = umax64(best, i0 + q < a.V ? tkey64(acc[bt][q], i0 + q) : (uint64_t)0);
     best = col_max64(best);
+    bm[bt] = umax64(bm[bt], best);  // the wave's largest key of column c so far
     const float m = key2f((uint32_t)(best >> 32));
     float sum = 0.f;
 #pragma unroll
@@ -149,7 +150,7 @@ __device__ __forceinline__ void tile_epilogue(const HeadArgs& a, uint32_t t, int
 template <int KS, int TPW, int PC>
 __device__ __forceinline__ void logits_tiles(const HeadArgs& a, uint32_t t, uint32_t t_hi,
                                              const __bf16* hs, __bf16* st, int hoff, int lane,
-                                             int r, int g) {
+                                             int r, int g, uint64_t* bm) {
   constexpr int D = KS * 32;
   constexpr int STRIDE = D + 8;  // staged hidden row pitch (elements)
   constexpr int NCH = D / 64;    // 64-element chunks per W row
@@ -211,7 +212,7 @@ __device__ __forceinline__ void logits_tiles(const HeadArgs& a, uint32_t t, uint
   }
 #pragma unroll
   for (int i = 0; i < TPW; ++i)
-    if (t + (uint32_t)i < t_hi) tile_epilogue(a, t + i, r, g, acc[i]);
+    if (t + (uint32_t)i < t_hi) tile_epilogue(a, t + i, r, g, acc[i], bm);
 }
 
 // Tiles per wave and chunks per pass of the logits kernel: three tiles
@@ -232,6 +233,8 @@ __global__ __launch_bounds__(kLogitWaves * 64) void k_head_logits(const HeadArgs
   __shared__ __attribute__((aligned(16))) __bf16 hs[kCols * STRIDE];
   __shared__ __attribute__((aligned(16))) __bf16 stage[kLogitWaves][16 * SP];
   __shared__ uint32_t s_next, s_next1;
+  __shared__ unsigned long long s_bmax[kCols];  // the block's largest tile key per column
+  if (threadIdx.x < kCols) s_bmax[threadIdx.x] = 0;
   const uint32_t col0 = blockIdx.y * kCols;
   const int ncols = (int)min((uint32_t)kCols, a.B - col0);
   for (int e = threadIdx.x; e < kCols * (D / 8); e += kLogitWaves * 64) {
@@ -259,13 +262,14 @@ __global__ __launch_bounds__(kLogitWaves * 64) void k_head_logits(const HeadArgs
   // from the optimiser keeps their LDS reads inside the loop (hoisted, the
   // whole 128 KB B operand would be held in registers and spill).
   int hoff = r * STRIDE + 8 * g;
+  uint64_t bm[4] = {0, 0, 0, 0};  // column bt * 16 + r (lanes g = 0 hold it)
   for (;;) {
     uint32_t t = 0;
     if (lane == 0) t = atomicAdd(&s_next, (uint32_t)kTileGroup);
     t = __builtin_amdgcn_readfirstlane(t);
     if (t >= t_grp) break;
     asm volatile("" : "+v"(hoff));
-    logits_tiles<KS, kTileGroup, kGroupChunks>(a, t, t_hi, hs, st, hoff, lane, r, g);
+    logits_tiles<KS, kTileGroup, kGroupChunks>(a, t, t_hi, hs, st, hoff, lane, r, g, bm);
   }
   for (;;) {
     uint32_t t = 0;
@@ -273,8 +277,19 @@ __global__ __launch_bounds__(kLogitWaves * 64) void k_head_logits(const HeadArgs
     t = __builtin_amdgcn_readfirstlane(t);
     if (t >= t_hi) break;
     asm volatile("" : "+v"(hoff));
-    logits_tiles<KS, 1, kSingleChunks>(a, t, t_hi, hs, st, hoff, lane, r, g);
+    logits_tiles<KS, 1, kSingleChunks>(a, t, t_hi, hs, st, hoff, lane, r, g, bm);
   }
+  // The block's largest tile key per row (0 for a block without tiles),
+  // from which the top-K kernel certifies a lower bound of each row's K-th
+  // largest logit.
+  if (g == 0) {
+#pragma unroll
+    for (int bt = 0; bt < 4; ++bt)
+      if (bm[bt]) atomicMax(&s_bmax[bt * 16 + r], (unsigned long long)bm[bt]);
+  }
+  __syncthreads();
+  if (threadIdx.x < kCols)
+    a.bmax[((size_t)blockIdx.y * a.nblk + blockIdx.x) * kCols + threadIdx.x] = s_bmax[threadIdx.x];
 }
 
 // Wave-wide reductions and scans with DPP (rows of 16 lanes) and readlane,
@@ -353,16 +368,42 @@ constexpr int kRowThreads = 1024;
 constexpr int kRowTiles = kHeadMaxTiles / kRowThreads;  // tile entries per thread
 constexpr int kRowCand = 16 * kHeadMaxK;                // logits of the candidate tiles
 
+// Appends the tiles whose masked key reaches lo ((key & msk) >= lo) to
+// s_tiles, in no particular order (the ranking does not depend on it): each
+// wave appends its tiles with one LDS atomic.  *s_n counts every such tile;
+// the list is cut at its capacity.
+template <int NI, int NT_>
+__device__ __forceinline__ void list_tiles(const uint64_t (&key)[NI], uint32_t NT, uint64_t msk,
+                                           uint64_t lo, uint32_t* s_tiles, uint32_t* s_n) {
+  const int tid = threadIdx.x, lane = tid & 63;
+  const uint64_t below = (1ull << lane) - 1ull;
+#pragma unroll
+  for (int i = 0; i < NI; ++i) {
+    const uint32_t t = tid + i * NT_;
+    const bool in = t < NT && (key[i] & msk) >= lo;
+    const uint64_t m = __builtin_amdgcn_ballot_w64(in);
+    if (m) {
+      uint32_t base = 0;
+      if (lane == 0) base = atomicAdd(s_n, (uint32_t)__builtin_popcountll(m));
+      base = __builtin_amdgcn_readfirstlane(base);
+      const uint32_t off = base + (uint32_t)__builtin_popcountll(m & below);
+      if (in && off < (uint32_t)kHeadMaxK) s_tiles[off] = t;
+    }
+  }
+}
+
 // Per row: the K most likely tokens and their probabilities from the tile
 // statistics and the logits.
-//   1. M = max logit (S = sum over tiles of tsum * exp(tile max - M) is
-//      formed in step 3, while the candidate logits load).
-//   2. A radix select over the tile-max keys (8-bit digits from the highest
-//      bit in which they differ; one LDS histogram per pass) narrows the
-//      tiles to the bins at and above the one holding the K-th largest key;
-//      it stops when those hold at most 192 tiles (or exactly K).  The K
-//      tiles with the largest maxima are among them and hold every top-K
-//      logit, and every top-K logit is at or above the bins' lower bound.
+//   1. M = max logit, S = sum over tiles of tsum * exp(tile max - M).
+//   2. A lower bound of the K-th largest logit from the logits blocks'
+//      largest keys (one 8-bit histogram of 256 values) usually lists the
+//      candidate tiles in one pass.  Otherwise a radix select over the
+//      tile-max keys (8-bit digits from the highest bit in which they
+//      differ; one LDS histogram per pass) narrows the tiles to the bins at
+//      and above the one holding the K-th largest key; it stops when those
+//      hold at most 192 tiles (or exactly K).  The K tiles with the largest
+//      maxima are among them and hold every top-K logit, and every top-K
+//      logit is at or above the bins' lower bound.
 //   3. The logits of those tiles at or above that bound are ranked in LDS,
 //      by counting when there are at most 1024 of them, else by a bitonic
 //      sort; the first K are the answer.  The tile and logit lists are
@@ -375,13 +416,16 @@ __global__ __launch_bounds__(kRowThreads) void k_head_rows(const HeadArgs a) {
   __shared__ uint32_t s_tiles[kHeadMaxK];
   __shared__ uint32_t s_wave[kRowThreads / 64];
   __shared__ uint32_t s_wmin[kRowThreads / 64];
+  __shared__ uint32_t s_bwmax[kRowThreads / 64], s_bwmin[kRowThreads / 64];
   __shared__ float s_red[kRowThreads / 64];
   __shared__ uint32_t s_bin, s_above, s_cnt, s_ntile, s_nc;
+  __shared__ unsigned long long s_lo;
   const uint32_t b = blockIdx.x;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   if (tid == 0) {
     s_ntile = 0;
     s_nc = 0;
+    s_lo = 0;
   }
   const uint32_t NT = (a.V + 15) >> 4;
   // Statistics of tile t of this row: block t / 16 of the row's 64-row
@@ -391,7 +435,12 @@ __global__ __launch_bounds__(kRowThreads) void k_head_rows(const HeadArgs a) {
   const float* ts = a.tsum + (grp * a.tblocks * 64 + c) * 16;
   auto sidx = [](uint32_t t) { return (size_t)(t >> 4) * 1024 + (t & 15); };
 
-  // Tile keys and sums are loaded together (one round trip).
+  // Tile keys and sums, and the logits blocks' largest keys of this row
+  // (step 2a), are loaded together (one round trip).
+  const uint32_t take = min(a.K, NT);
+  const bool bound = take < NT && a.K <= a.nblk && a.nblk <= (uint32_t)kRowThreads;
+  const uint64_t bmv = bound && (uint32_t)tid < a.nblk
+                           ? a.bmax[(grp * a.nblk + (uint32_t)tid) * 64 + c] : 0;  // 0: none
   uint64_t key[kRowTiles];
   float tsv[kRowTiles];
 #pragma unroll
@@ -414,121 +463,180 @@ __global__ __launch_bounds__(kRowThreads) void k_head_rows(const HeadArgs a) {
   // too; relative error about an ulp per term).
   hmax = wave_max_u32(hmax);
   hmin = ~wave_max_u32(~hmin);
+  uint32_t bhmax = wave_max_u32((uint32_t)(bmv >> 32));
+  uint32_t bhmin = ~wave_max_u32(bmv ? ~(uint32_t)(bmv >> 32) : 0u);
   if (lane == 0) {
     s_wave[wave] = hmax;
     s_wmin[wave] = hmin;
+    s_bwmax[wave] = bhmax;
+    s_bwmin[wave] = bhmin;
   }
   __syncthreads();
-  hmax = 0;
-  hmin = 0xFFFFFFFFu;
+  hmax = bhmax = 0;
+  hmin = bhmin = 0xFFFFFFFFu;
   for (int w = 0; w < kRowThreads / 64; ++w) {
     hmax = max(hmax, s_wave[w]);
     hmin = min(hmin, s_wmin[w]);
+    bhmax = max(bhmax, s_bwmax[w]);
+    bhmin = min(bhmin, s_bwmin[w]);
   }
   const float M = key2f(hmax);
-  // (The sum S is formed in step 3, behind the candidate loads.)
-
-  // 2. The K-th largest tile key (all tiles when there are at most K).
-  const uint32_t take = min(a.K, NT);
-  uint64_t prefix = 0, mask = 0, common = 0;
-  if (take < NT) {
-    // Radix select from the highest bit in which the tile keys differ (the
-    // high words of all keys lie between hmin and hmax, so they agree above
-    // the top bit of hmin ^ hmax), 8 bits per pass.  It stops once the bins
-    // at and above the chosen one hold at most kStopCand tiles: every
-    // answer lies in those tiles, so the K-th largest key itself is not
-    // needed.
-    constexpr uint32_t kStopCand = 192;
-    static_assert(kStopCand <= kHeadMaxK, "candidate tiles must fit s_tiles");
-    const uint32_t dhi = hmin ^ hmax;
-    const int top = dhi ? 63 - __builtin_clz(dhi) : 31;  // highest differing bit (low word: 31)
-    const int shift0 = max(top - 7, 0);
-    // Bits above the first digit, shared by every key (all in the high word).
-    if (shift0 + 8 < 64) common = ((uint64_t)hmax << 32) & ~((1ull << (shift0 + 8)) - 1ull);
-    uint32_t need = take, above = 0;
-    const uint64_t lt = (1ull << lane) - 1ull;
-    for (int shift = shift0;; shift = max(shift - 8, 0)) {
-      if (tid < 256) hist[tid] = 0u;
-      __syncthreads();
-      // The lanes holding the first active lane's digit add their number
-      // with one atomic (the top digits of tile maxima are mostly equal).
+  // Each wave's part of S = sum over tiles of tsum * exp(tile max - M); the
+  // parts are added up after a later barrier (step 3).
+  {
+    float part = 0.f;
 #pragma unroll
-      for (int i = 0; i < kRowTiles; ++i) {
-        if (tid + i * kRowThreads < NT && (key[i] & mask) == prefix) {
-          const uint32_t d = (uint32_t)(key[i] >> shift) & 255u;
-          const uint32_t d0 = __builtin_amdgcn_readfirstlane(d);
-          const uint64_t m = __builtin_amdgcn_ballot_w64(d == d0);
-          if (d != d0) atomicAdd(&hist[d], 1u);
-          else if ((m & lt) == 0) atomicAdd(&hist[d0], (uint32_t)__builtin_popcountll(m));
-        }
+    for (int i = 0; i < kRowTiles; ++i) {
+      const uint32_t t = tid + i * kRowThreads;
+      if (t < NT) part += tsv[i] * __expf(key2f((uint32_t)(key[i] >> 32)) - M);
+    }
+    part = wave_add(part);
+    if (lane == 0) s_red[wave] = part;
+  }
+
+  // 2. Candidate tiles.  Every top-K logit lies in a tile whose largest key
+  // reaches the row's K-th largest logit key, and reaches it itself, so for
+  // any lower bound tau of that key the tiles with a key >= tau hold every
+  // answer, and their logits >= tau include it.
+  uint64_t tau = 0;
+  bool listed = false;
+  // 2a. A certified bound, when K is at most the number of logits blocks:
+  // at least K of the blocks' largest keys reach it, and they are distinct
+  // logit keys, so the row's K-th largest logit key reaches it too.  One
+  // 8-bit histogram of the block maxima (from the highest bit in which they
+  // differ) gives the bin holding their K-th largest; its lower edge is the
+  // bound.  One pass lists the tiles that reach it; if they overflow the
+  // list, the radix select below takes over.
+  if (bound) {
+    const uint32_t dh = bhmin ^ bhmax;
+    const int top = dh ? 63 - __builtin_clz(dh) : 31;
+    const int sh = max(top - 7, 0);
+    const uint64_t cm =
+        sh + 8 < 64 ? ((uint64_t)bhmax << 32) & ~((1ull << (sh + 8)) - 1ull) : 0ull;
+    if (tid < 256) hist[tid] = 0u;
+    __syncthreads();
+    if (bmv) atomicAdd(&hist[(uint32_t)(bmv >> sh) & 255u], 1u);
+    __syncthreads();
+    if (wave == 0) {  // the bin where the count from the top reaches K
+      uint32_t v[4], sum = 0;
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        v[k] = hist[255 - 4 * lane - k];
+        sum += v[k];
       }
-      __syncthreads();
-      // Wave 0 finds the bin holding the need-th largest key: lane l holds
-      // bins 255 - 4 l - k, k = 0..3 (descending order).
-      if (wave == 0) {
-        uint32_t v[4], sum = 0;
+      const uint32_t inc = wave_incl_scan(sum);
+      uint32_t ex = inc - sum;
+      if (ex < a.K && a.K <= inc) {
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
-          v[k] = hist[255 - 4 * lane - k];
-          sum += v[k];
-        }
-        const uint32_t inc = wave_incl_scan(sum);
-        uint32_t ex = inc - sum;
-        if (ex < need && need <= inc) {
-#pragma unroll
-          for (int k = 0; k < 4; ++k) {
-            if (ex < need && need <= ex + v[k]) {
-              s_bin = 255u - 4u * (uint32_t)lane - (uint32_t)k;
-              s_above = ex;
-              s_cnt = v[k];
-            }
-            ex += v[k];
-          }
+          if (ex < a.K && a.K <= ex + v[k])
+            s_lo = cm | ((uint64_t)(255u - 4u * (uint32_t)lane - (uint32_t)k) << sh);
+          ex += v[k];
         }
       }
+    }
+    __syncthreads();
+    const uint64_t lo = s_lo;  // 0: fewer than K blocks with tiles
+    if (lo != 0) {
+      list_tiles<kRowTiles, kRowThreads>(key, NT, ~0ull, lo, s_tiles, &s_ntile);
       __syncthreads();
-      need -= s_above;
-      above += s_above;
-      prefix |= (uint64_t)s_bin << shift;  // bits below the previous digit only
-      mask |= (uint64_t)0xFF << shift;
-      // Every thread has read s_bin / s_above / s_cnt before wave 0 can
-      // write them again (two barriers of the next pass come first).
-      if (s_cnt == need || above + s_cnt <= kStopCand || shift == 0) break;
+      const uint32_t n = s_ntile;
+      __syncthreads();  // every thread has read s_ntile
+      if (n <= (uint32_t)kHeadMaxK) {
+        listed = true;
+        tau = lo;
+      } else if (tid == 0) {
+        s_ntile = 0;  // the radix select's first barrier orders this
+      }
     }
   }
-  // Candidate tiles: the keys whose masked bits reach the prefix (at most
-  // max(K, kStopCand) of them, the keys being distinct); every answer logit
-  // is at or above the prefix.  The list is cut at its capacity all the same,
-  // so that statistics that were never written (equal keys) cannot make the
-  // block write past it.
-  // The list is in no particular order (the ranking below does not depend
-  // on it): each wave appends its tiles with one LDS atomic, instead of a
-  // block-wide scan and its barriers.
-  const uint64_t below = (1ull << lane) - 1ull;
+  if (!listed) {
+    // 2b. The K-th largest tile key (all tiles when there are at most K).
+    uint64_t prefix = 0, mask = 0, common = 0;
+    if (take < NT) {
+      // Radix select from the highest bit in which the tile keys differ (the
+      // high words of all keys lie between hmin and hmax, so they agree above
+      // the top bit of hmin ^ hmax), 8 bits per pass.  It stops once the bins
+      // at and above the chosen one hold at most kStopCand tiles: every
+      // answer lies in those tiles, so the K-th largest key itself is not
+      // needed.
+      constexpr uint32_t kStopCand = 192;
+      static_assert(kStopCand <= kHeadMaxK, "candidate tiles must fit s_tiles");
+      const uint32_t dhi = hmin ^ hmax;
+      const int top = dhi ? 63 - __builtin_clz(dhi) : 31;  // highest differing bit (low word: 31)
+      const int shift0 = max(top - 7, 0);
+      // Bits above the first digit, shared by every key (all in the high word).
+      if (shift0 + 8 < 64) common = ((uint64_t)hmax << 32) & ~((1ull << (shift0 + 8)) - 1ull);
+      uint32_t need = take, above = 0;
+      const uint64_t lt = (1ull << lane) - 1ull;
+      for (int shift = shift0;; shift = max(shift - 8, 0)) {
+        if (tid < 256) hist[tid] = 0u;
+        __syncthreads();
+        // The lanes holding the first active lane's digit add their number
+        // with one atomic (the top digits of tile maxima are mostly equal).
 #pragma unroll
-  for (int i = 0; i < kRowTiles; ++i) {
-    const uint32_t t = tid + i * kRowThreads;
-    const bool in = t < NT && (key[i] & mask) >= prefix;
-    const uint64_t m = __builtin_amdgcn_ballot_w64(in);
-    if (m) {
-      uint32_t base = 0;
-      if (lane == 0) base = atomicAdd(&s_ntile, (uint32_t)__builtin_popcountll(m));
-      base = __builtin_amdgcn_readfirstlane(base);
-      const uint32_t off = base + (uint32_t)__builtin_popcountll(m & below);
-      if (in && off < (uint32_t)kHeadMaxK) s_tiles[off] = t;
+        for (int i = 0; i < kRowTiles; ++i) {
+          if (tid + i * kRowThreads < NT && (key[i] & mask) == prefix) {
+            const uint32_t d = (uint32_t)(key[i] >> shift) & 255u;
+            const uint32_t d0 = __builtin_amdgcn_readfirstlane(d);
+            const uint64_t m = __builtin_amdgcn_ballot_w64(d == d0);
+            if (d != d0) atomicAdd(&hist[d], 1u);
+            else if ((m & lt) == 0) atomicAdd(&hist[d0], (uint32_t)__builtin_popcountll(m));
+          }
+        }
+        __syncthreads();
+        // Wave 0 finds the bin holding the need-th largest key: lane l holds
+        // bins 255 - 4 l - k, k = 0..3 (descending order).
+        if (wave == 0) {
+          uint32_t v[4], sum = 0;
+#pragma unroll
+          for (int k = 0; k < 4; ++k) {
+            v[k] = hist[255 - 4 * lane - k];
+            sum += v[k];
+          }
+          const uint32_t inc = wave_incl_scan(sum);
+          uint32_t ex = inc - sum;
+          if (ex < need && need <= inc) {
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+              if (ex < need && need <= ex + v[k]) {
+                s_bin = 255u - 4u * (uint32_t)lane - (uint32_t)k;
+                s_above = ex;
+                s_cnt = v[k];
+              }
+              ex += v[k];
+            }
+          }
+        }
+        __syncthreads();
+        need -= s_above;
+        above += s_above;
+        prefix |= (uint64_t)s_bin << shift;  // bits below the previous digit only
+        mask |= (uint64_t)0xFF << shift;
+        // Every thread has read s_bin / s_above / s_cnt before wave 0 can
+        // write them again (two barriers of the next pass come first).
+        if (s_cnt == need || above + s_cnt <= kStopCand || shift == 0) break;
+      }
     }
+    // Candidate tiles: the keys whose masked bits reach the prefix (at most
+    // max(K, kStopCand) of them, the keys being distinct); every answer
+    // logit is at or above the prefix.  The list is cut at its capacity all
+    // the same, so that statistics that were never written (equal keys)
+    // cannot make the block write past it.
+    list_tiles<kRowTiles, kRowThreads>(key, NT, mask, prefix, s_tiles, &s_ntile);
+    // (With all tiles taken, every logit is a candidate.)
+    tau = take == NT ? 0 : (common | prefix);
+    __syncthreads();
   }
-  // (With all tiles taken, every logit is a candidate.)
-  const uint64_t tau = take == NT ? 0 : (common | prefix);
-  __syncthreads();
   const uint32_t ntile = min(s_ntile, (uint32_t)kHeadMaxK);
+  const uint64_t below = (1ull << lane) - 1ull;
 
   // 3. Gather the candidate tiles' logits at or above tau, sort, emit.
   const float* lg = a.logits + (grp * a.tpitch * 64 + c) * 16;  // tile t at lg[1024 t]
   // All candidate logits are loaded first (16 per tile, kRowThreads per
   // round; the logits scratch holds whole tiles, so the reads past V stay
-  // in it), the log-sum-exp's sum is formed while they arrive, and the
-  // logits at or above tau are appended, wave by wave, to the candidates.
+  // in it), and the logits at or above tau are appended, wave by wave, to
+  // the candidates.
   constexpr int kRounds = kRowCand / kRowThreads;
   const uint32_t nlog = 16 * ntile;  // <= kRowCand
   float lv[kRounds];
@@ -538,15 +646,6 @@ __global__ __launch_bounds__(kRowThreads) void k_head_rows(const HeadArgs a) {
     lv[j] = 0.f;
     if (e < nlog) lv[j] = lg[1024 * (size_t)s_tiles[e >> 4] + (e & 15)];
   }
-  // The log-sum-exp's sum, while the candidate logits load.
-  float part = 0.f;
-#pragma unroll
-  for (int i = 0; i < kRowTiles; ++i) {
-    const uint32_t t = tid + i * kRowThreads;
-    if (t < NT) part += tsv[i] * __expf(key2f((uint32_t)(key[i] >> 32)) - M);
-  }
-  part = wave_add(part);
-  if (lane == 0) s_red[wave] = part;
 #pragma unroll
   for (int j = 0; j < kRounds; ++j) {
     const uint32_t e = j * kRowThreads + tid;
@@ -600,11 +699,11 @@ __global__ __launch_bounds__(kRowThreads) void k_head_rows(const HeadArgs a) {
 bool head_dim_supported(int D) { return D == 256 || D == 512 || D == 1024; }
 
 uint32_t head_lds_bytes(int D) {
-  return (uint32_t)(kCols * (D + 8) * 2 + kLogitWaves * 16 * 72 * 2 + 4);
+  return (uint32_t)(kCols * (D + 8) * 2 + kLogitWaves * 16 * 72 * 2 + 8 + kCols * 8);
 }
 
-hipError_t launch_head_logits(const HeadArgs& a, uint32_t blocks, hipStream_t s) {
-  const dim3 grid(blocks, (a.B + kCols - 1) / kCols);
+hipError_t launch_head_logits(const HeadArgs& a, hipStream_t s) {
+  const dim3 grid(a.nblk, (a.B + kCols - 1) / kCols);
   switch (a.D) {
     case 256: hipLaunchKernelGGL(k_head_logits<8>, grid, dim3(kLogitWaves * 64), 0, s, a); break;
     case 512: hipLaunchKernelGGL(k_head_logits<16>, grid, dim3(kLogitWaves * 64), 0, s, a); break;

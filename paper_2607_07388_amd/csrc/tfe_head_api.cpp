@@ -19,6 +19,7 @@ struct tfe_head {
   float* d_logits = nullptr;  // [rows x tiles x 16]
   uint64_t* d_tkey = nullptr; // [rows x tiles rounded up to 16]
   float* d_tsum = nullptr;    // [rows x tiles rounded up to 16]
+  uint64_t* d_bmax = nullptr; // [rows x compute units]
   // Recorded after every top-K call made outside graph capture; freeing the
   // head waits for it (and for nothing else on the device).
   hipEvent_t ev_last = nullptr;
@@ -44,7 +45,7 @@ void release(tfe_head* h) {
   (void)hipGetDevice(&cur);
   (void)hipSetDevice(h->device);
   if (h->recorded) (void)hipEventSynchronize(h->ev_last);
-  void* bufs[] = {h->d_logits, h->d_tkey, h->d_tsum};
+  void* bufs[] = {h->d_logits, h->d_tkey, h->d_tsum, h->d_bmax};
   for (void* b : bufs) dev_free(b);
   if (h->ev_last) (void)hipEventDestroy(h->ev_last);
   (void)hipSetDevice(cur);
@@ -103,7 +104,8 @@ tfe_status create(const void* w, int32_t vocab, int32_t dim, int32_t max_batch, 
     const size_t nt16 = (nt + 15) / 16 * 16;
     if (dev_malloc((void**)&h->d_logits, nb * nt * 16 * sizeof(float)) != hipSuccess ||
         dev_malloc((void**)&h->d_tkey, nb * nt16 * sizeof(uint64_t)) != hipSuccess ||
-        dev_malloc((void**)&h->d_tsum, nb * nt16 * sizeof(float)) != hipSuccess) {
+        dev_malloc((void**)&h->d_tsum, nb * nt16 * sizeof(float)) != hipSuccess ||
+        dev_malloc((void**)&h->d_bmax, nb * (size_t)h->cus * sizeof(uint64_t)) != hipSuccess) {
       st = fail(TFE_ERR_OOM, "head scratch for %u rows", h->max_batch);
       break;
     }
@@ -141,6 +143,7 @@ tfe_status topk(tfe_head* h, const void* hidden, int32_t B, int32_t K, int32_t* 
   a.logits = h->d_logits;
   a.tkey = h->d_tkey;
   a.tsum = h->d_tsum;
+  a.bmax = h->d_bmax;
   a.top_ids = ids;
   a.top_prob = prob;
   a.V = h->V;
@@ -149,7 +152,8 @@ tfe_status topk(tfe_head* h, const void* hidden, int32_t B, int32_t K, int32_t* 
   a.D = h->D;
   a.B = (uint32_t)B;
   a.K = (uint32_t)K;
-  HEAD_HIP(launch_head_logits(a, (uint32_t)h->cus, stream), "head logits launch");
+  a.nblk = (uint32_t)h->cus;
+  HEAD_HIP(launch_head_logits(a, stream), "head logits launch");
   HEAD_HIP(launch_head_rows(a, stream), "head top-K launch");
   hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
   HEAD_HIP(hipStreamIsCapturing(stream, &cs), "hipStreamIsCapturing");

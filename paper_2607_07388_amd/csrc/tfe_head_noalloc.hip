@@ -1,9 +1,10 @@
 // Early-exit head top-K without any allocation, for callers that cannot
 // allocate device memory (code under HIP graph capture, serving loops,
 // harnesses that forbid hipMalloc).  Same kernels and results as
-// tfe_head_topk; their scratch (logits and tile statistics of one 64-row
-// group, for vocabularies up to 2^18) is a file-scope device array that
-// each GPU holds until the process ends.
+// tfe_head_topk; their scratch (logits, tile statistics and block maxima of
+// one 64-row group, for vocabularies up to 2^18 and up to kNaMaxBlocks
+// compute units) is a file-scope device array that each GPU holds until the
+// process ends.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -21,7 +22,9 @@ constexpr uint32_t kNaTiles = kHeadMaxTiles;  // 16-token tiles of a 2^18 vocabu
 constexpr size_t kNaLogitBytes = (size_t)kNaRows * kNaTiles * 16 * sizeof(float);  // 64 MiB
 constexpr size_t kNaKeyBytes = (size_t)kNaRows * kNaTiles * sizeof(uint64_t);      // 8 MiB
 constexpr size_t kNaSumBytes = (size_t)kNaRows * kNaTiles * sizeof(float);         // 4 MiB
-constexpr size_t kNaBytes = kNaLogitBytes + kNaKeyBytes + kNaSumBytes;
+constexpr uint32_t kNaMaxBlocks = 1024;       // logits blocks: one per compute unit
+constexpr size_t kNaBmaxBytes = (size_t)kNaRows * kNaMaxBlocks * sizeof(uint64_t); // 512 KiB
+constexpr size_t kNaBytes = kNaLogitBytes + kNaKeyBytes + kNaSumBytes + kNaBmaxBytes;
 constexpr int kNaMaxDevices = 64;
 
 }  // namespace
@@ -97,6 +100,9 @@ tfe_status topk_noalloc(const void* w, int32_t vocab, int32_t dim, const void* h
   NaDevice d;
   tfe_status st = na_device(dev, &d);
   if (st != TFE_OK) return st;
+  if (d.cus < 1 || (uint32_t)d.cus > kNaMaxBlocks)
+    return fail(TFE_ERR_UNSUPPORTED, "%d compute units (the no-allocation scratch holds %u)",
+                d.cus, kNaMaxBlocks);
   if ((uint32_t)d.lds < head_lds_bytes(dim))
     return fail(TFE_ERR_UNSUPPORTED, "dim %d needs %u bytes of LDS per block, device has %d", dim,
                 head_lds_bytes(dim), d.lds);
@@ -106,6 +112,7 @@ tfe_status topk_noalloc(const void* w, int32_t vocab, int32_t dim, const void* h
   a.logits = (float*)d.ptr;
   a.tkey = (uint64_t*)(d.ptr + kNaLogitBytes);
   a.tsum = (float*)(d.ptr + kNaLogitBytes + kNaKeyBytes);
+  a.bmax = (uint64_t*)(d.ptr + kNaLogitBytes + kNaKeyBytes + kNaSumBytes);
   a.top_ids = ids;
   a.top_prob = prob;
   a.V = (uint32_t)vocab;
@@ -114,9 +121,11 @@ tfe_status topk_noalloc(const void* w, int32_t vocab, int32_t dim, const void* h
   a.D = (uint32_t)dim;
   a.B = (uint32_t)B;
   a.K = (uint32_t)K;
+  a.nblk = (uint32_t)d.cus;
   // One 64-row group: logits [tpitch x 64 x 16] <= kNaLogitBytes, statistics
-  // [tblocks x 64 x 16] <= kNaKeyBytes / 8 entries.
-  e = launch_head_logits(a, (uint32_t)d.cus, stream);
+  // [tblocks x 64 x 16] <= kNaKeyBytes / 8 entries, block maxima
+  // [nblk x 64] <= kNaBmaxBytes / 8.
+  e = launch_head_logits(a, stream);
   if (e == hipSuccess) e = launch_head_rows(a, stream);
   if (e != hipSuccess) return fail(TFE_ERR_HIP, "head launch: %s", hipGetErrorString(e));
   return TFE_OK;
