@@ -93,8 +93,8 @@ MULTI_SOURCES = ("paper_2607_07388_amd/csrc/tfe_multi.hip",
 # K = 128): k_head_logits + k_head_rows, from the passes in
 # profiles/k_head_logits_rows_v151936_d1024_b64_k128.md.
 PROFILED_TRAFFIC_HEAD = {
-    "sources_sha256": "dd016e8374777b899396262bda56794b94793f2de1d83b0c8e9782252b7e2528",
-    "bytes_per_launch": 372172536,
+    "sources_sha256": "17623774cbebd67d0ee86b05db7addf13107105ce22724d75e633c81789ddde9",
+    "bytes_per_launch": 373928662,
 }
 HEAD_SOURCES = ("paper_2607_07388_amd/csrc/tfe_head.hip",
                 "paper_2607_07388_amd/csrc/tfe_head.h",
