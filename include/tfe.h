@@ -291,9 +291,10 @@ tfe_status tfe_head_free(tfe_head *head);
  *   top_ids DEVICE int32 [B x K], top_prob DEVICE float32 [B x K].
  * Limits: 0 <= B <= 64, 1 <= vocab <= 2^18, 0 <= K <= min(256, vocab), dim
  * 256, 512 or 1024; larger sizes return TFE_ERR_INVALID_ARG.  The scratch
- * (logits and tile statistics: 76 MiB) is a static device array that every
- * GPU the library runs on holds until the process ends; the call allocates
- * nothing.  Every call on one GPU shares that GPU's scratch: calls that
+ * (logits, tile statistics and the logits blocks' maxima: 76.5 MiB) is a
+ * static device array that every GPU the library runs on holds until the
+ * process ends; the call allocates nothing.  A device with more than 1024
+ * compute units is refused (TFE_ERR_UNSUPPORTED).  Every call on one GPU shares that GPU's scratch: calls that
  * overlap on one GPU (different streams, or host threads) race and must be
  * ordered by the caller. */
 tfe_status tfe_head_topk_noalloc(const void *w_pref, int32_t vocab, int32_t dim,
