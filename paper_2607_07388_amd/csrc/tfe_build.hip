@@ -614,10 +614,23 @@ __global__ __launch_bounds__(1024) void k_run_counts(const uint32_t* ustart, uin
   const uint32_t base = blockIdx.x * (1024u * 16u);
   for (int k = 0; k < 16; ++k) {
     const uint32_t i = base + (uint32_t)k * 1024u + threadIdx.x;
-    if (i < u) {
+    const bool in = i < u;
+    uint32_t bin = 0;
+    if (in) {
       const uint32_t c = (i + 1 < u ? ustart[i + 1] : n) - ustart[i];
       ucount[i] = c;
-      atomicAdd(&h[c < (uint32_t)kSelBins ? c : (uint32_t)kSelBins - 1u], 1u);
+      bin = c < (uint32_t)kSelBins ? c : (uint32_t)kSelBins - 1u;
+    }
+    // Most runs are short, so most lanes share a bin: the lanes holding the
+    // first lane's bin add their number with one atomic (one atomic per
+    // lane put 64-way same-address atomics on the few small-count bins).
+    if (__builtin_amdgcn_ballot_w64(in)) {
+      const uint32_t b0 = __builtin_amdgcn_readfirstlane(bin);
+      const uint64_t m = __builtin_amdgcn_ballot_w64(in && bin == b0);
+      if (in && bin != b0)
+        atomicAdd(&h[bin], 1u);
+      else if (in && (m & ((1ull << (threadIdx.x & 63)) - 1ull)) == 0)
+        atomicAdd(&h[b0], (uint32_t)__builtin_popcountll(m));
     }
   }
   __syncthreads();
