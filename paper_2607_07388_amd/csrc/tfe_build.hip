@@ -711,29 +711,122 @@ __global__ __launch_bounds__(256) void k_sel_pick(uint32_t* hist, uint32_t* stat
 }
 
 // keep[i]: count > c*, or count == c* and among the first `need` such runs.
-__global__ __launch_bounds__(256) void k_sel_eq(const uint32_t* cnt, uint32_t u,
-                                                const uint32_t* state, uint32_t* eq) {
-  const uint32_t i = blockIdx.x * 256 + threadIdx.x;
-  if (i < u) eq[i] = cnt[i] == state[0] ? 1u : 0u;
-}
+// The runs that make ranks [0, R): with c* = state[0] and need = state[2],
+// run i is kept when its count exceeds c*, or equals c* and fewer than
+// `need` runs of count c* come before it.  Kept runs keep their order
+// (rkey = ~count, rval = the run index): the stable sort that ranks them
+// then leaves equal counts in tuple order.  Two launches over the counts:
+// per-block numbers above and at c*, then each block places its kept runs.
 
-__global__ __launch_bounds__(256) void k_sel_keep(const uint32_t* cnt, uint32_t u,
-                                                  const uint32_t* state, const uint32_t* eqrank,
-                                                  uint32_t* keep) {
-  const uint32_t i = blockIdx.x * 256 + threadIdx.x;
-  if (i < u) {
-    const uint32_t c = cnt[i], cstar = state[0];
-    keep[i] = (c > cstar || (c == cstar && eqrank[i] < state[2])) ? 1u : 0u;
+// Per block of kScanBlock runs: how many counts exceed c* and how many
+// equal it.
+__global__ __launch_bounds__(kScanThreads) void k_sel_count(const uint32_t* cnt, uint32_t u,
+                                                            const uint32_t* state,
+                                                            uint32_t* part_gt, uint32_t* part_eq) {
+  __shared__ uint32_t s_gt[kScanThreads / 64], s_eq[kScanThreads / 64];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const uint32_t cstar = state[0];  // >= 1: the R-th largest count
+  const uint64_t base = (uint64_t)blockIdx.x * kScanBlock + (uint64_t)wave * (64 * kScanItems);
+  uint32_t c[kScanItems];
+#pragma unroll
+  for (int k = 0; k < kScanItems; ++k) {
+    const uint64_t i = base + (uint64_t)k * 64 + lane;
+    c[k] = i < u ? cnt[i] : 0u;  // 0: no run
+  }
+  uint32_t g = 0, e = 0;
+#pragma unroll
+  for (int k = 0; k < kScanItems; ++k) {
+    g += (uint32_t)__builtin_popcountll(__builtin_amdgcn_ballot_w64(c[k] > cstar));
+    e += (uint32_t)__builtin_popcountll(__builtin_amdgcn_ballot_w64(c[k] == cstar));
+  }
+  if (lane == 0) {
+    s_gt[wave] = g;
+    s_eq[wave] = e;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint32_t tg = 0, te = 0;
+    for (int w = 0; w < kScanThreads / 64; ++w) {
+      tg += s_gt[w];
+      te += s_eq[w];
+    }
+    part_gt[blockIdx.x] = tg;
+    part_eq[blockIdx.x] = te;
   }
 }
 
-__global__ __launch_bounds__(256) void k_sel_compact(const uint32_t* cnt, uint32_t u,
-                                                     const uint32_t* keep, const uint32_t* pos,
-                                                     uint32_t* rkey, uint64_t* rval) {
-  const uint32_t i = blockIdx.x * 256 + threadIdx.x;
-  if (i < u && keep[i]) {
-    rkey[pos[i]] = ~cnt[i];  // ascending ~count = descending count
-    rval[pos[i]] = i;        // the run; runs are in tuple order
+// Places the block's kept runs.  The runs above c* before the block, and
+// the kept ones at c* (the first `need` of them, in order), are added up
+// from the per-block numbers of the earlier blocks (at most kScanItems per
+// thread, from L2); within the block each wave takes its contiguous
+// kScanItems x 64 runs, ranks the ones at c* and then the kept ones with
+// ballots, and one exchange of wave totals places the waves.  Positions at
+// or past R (none when the selection state is consistent) are not written.
+__global__ __launch_bounds__(kScanThreads) void k_sel_place(const uint32_t* cnt, uint32_t u,
+                                                            const uint32_t* state,
+                                                            const uint32_t* part_gt,
+                                                            const uint32_t* part_eq, uint32_t R,
+                                                            uint32_t* rkey, uint64_t* rval) {
+  __shared__ uint64_t s_sum[kScanThreads / 64];
+  __shared__ uint32_t s_eq[kScanThreads / 64], s_keep[kScanThreads / 64];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const uint32_t cstar = state[0], need = state[2];
+  const uint64_t base = (uint64_t)blockIdx.x * kScanBlock + (uint64_t)wave * (64 * kScanItems);
+  uint32_t c[kScanItems];
+#pragma unroll
+  for (int k = 0; k < kScanItems; ++k) {
+    const uint64_t i = base + (uint64_t)k * 64 + lane;
+    c[k] = i < u ? cnt[i] : 0u;
+  }
+  // Earlier blocks: above c* in the high word, at c* in the low word (each
+  // total is below 2^32).
+  uint64_t b = 0;
+#pragma unroll
+  for (int k = 0; k < kScanItems; ++k) {
+    const uint32_t j = (uint32_t)k * kScanThreads + threadIdx.x;
+    if (j < blockIdx.x) b += ((uint64_t)part_gt[j] << 32) | part_eq[j];
+  }
+  for (int d = 32; d >= 1; d >>= 1) b += __shfl_xor(b, d, 64);
+  if (lane == 0) s_sum[wave] = b;
+  const uint64_t lt = (1ull << lane) - 1ull;
+  uint64_t em[kScanItems];
+  uint32_t e = 0;
+#pragma unroll
+  for (int k = 0; k < kScanItems; ++k) {
+    em[k] = __builtin_amdgcn_ballot_w64(c[k] == cstar);
+    e += (uint32_t)__builtin_popcountll(em[k]);
+  }
+  if (lane == 0) s_eq[wave] = e;
+  __syncthreads();
+  uint64_t before = 0;
+  for (int w = 0; w < kScanThreads / 64; ++w) before += s_sum[w];
+  const uint32_t gt_before = (uint32_t)(before >> 32), eq_before = (uint32_t)before;
+  uint32_t erun = eq_before;
+  for (int w = 0; w < wave; ++w) erun += s_eq[w];
+  uint64_t km[kScanItems];
+  uint32_t kc = 0;
+#pragma unroll
+  for (int k = 0; k < kScanItems; ++k) {
+    const uint32_t er = erun + (uint32_t)__builtin_popcountll(em[k] & lt);
+    const bool keep = c[k] > cstar || (((em[k] >> lane) & 1ull) && er < need);
+    km[k] = __builtin_amdgcn_ballot_w64(keep);
+    kc += (uint32_t)__builtin_popcountll(km[k]);
+    erun += (uint32_t)__builtin_popcountll(em[k]);
+  }
+  if (lane == 0) s_keep[wave] = kc;
+  __syncthreads();
+  uint32_t krun = gt_before + min(need, eq_before);
+  for (int w = 0; w < wave; ++w) krun += s_keep[w];
+#pragma unroll
+  for (int k = 0; k < kScanItems; ++k) {
+    if ((km[k] >> lane) & 1ull) {
+      const uint32_t pos = krun + (uint32_t)__builtin_popcountll(km[k] & lt);
+      if (pos < R) {
+        rkey[pos] = ~c[k];  // ascending ~count = descending count
+        rval[pos] = base + (uint64_t)k * 64 + lane;
+      }
+    }
+    krun += (uint32_t)__builtin_popcountll(km[k]);
   }
 }
 
@@ -975,8 +1068,7 @@ tfe_status ngram_top(const int32_t* tokens, int64_t N, int32_t vocab, int32_t n,
   uint32_t* uhi = wide ? sc.get<uint32_t>(U) : nullptr;
   uint32_t* ustart = sc.get<uint32_t>(U);
   uint32_t* ucnt = sc.get<uint32_t>(U);
-  uint32_t* eq = sc.get<uint32_t>(U);
-  if (!ukey || !ustart || !ucnt || !eq || (wide && !uhi)) return fail(TFE_ERR_OOM, "run arrays");
+  if (!ukey || !ustart || !ucnt || (wide && !uhi)) return fail(TFE_ERR_OOM, "run arrays");
   if (wide)
     hipLaunchKernelGGL(k_runs_write<true>, dim3(nbr), dim3(kScanThreads), 0, s, keys, hi, M, part,
                        ukey, uhi, ustart);
@@ -1006,21 +1098,21 @@ tfe_status ngram_top(const int32_t* tokens, int64_t N, int32_t vocab, int32_t n,
   }
   BUILD_HIP(hipGetLastError(), "select launches");
   // state = {c*, ~0, needed runs with count c*, runs above c*}.
-  hipLaunchKernelGGL(k_sel_eq, dim3(blocks_for(U, 256)), dim3(256), 0, s, ucnt, U, d_small, eq);
-  BUILD_HIP(scan_u32(eq, eq, U, part, s), "tie scan");
-  uint32_t* keep = ustart;  // the run starts are no longer needed
-  hipLaunchKernelGGL(k_sel_keep, dim3(blocks_for(U, 256)), dim3(256), 0, s, ucnt, U, d_small, eq,
-                     keep);
-  uint32_t* pos = eq;
-  BUILD_HIP(scan_u32(keep, pos, U, part, s), "keep scan");
   uint32_t* rkey = sc.get<uint32_t>(R);
   uint32_t* rkey_alt = sc.get<uint32_t>(R);
   uint64_t* rval = sc.get<uint64_t>(R);
   uint64_t* rval_alt = sc.get<uint64_t>(R);
   if (!rkey || !rkey_alt || !rval || !rval_alt) return fail(TFE_ERR_OOM, "rank arrays");
-  hipLaunchKernelGGL(k_sel_compact, dim3(blocks_for(U, 256)), dim3(256), 0, s, ucnt, U, keep,
-                     pos, rkey, rval);
-  BUILD_HIP(hipGetLastError(), "compact launch");
+  // Per-block numbers in the radix histogram buffer (idle until the rank
+  // sort; it holds kBins x ntiles >= 2 x blocks entries).
+  const uint32_t nbs = blocks_for(U, kScanBlock);
+  uint32_t* part_gt = hist;
+  uint32_t* part_eq = hist + nbs;
+  hipLaunchKernelGGL(k_sel_count, dim3(nbs), dim3(kScanThreads), 0, s, ucnt, U, d_small, part_gt,
+                     part_eq);
+  hipLaunchKernelGGL(k_sel_place, dim3(nbs), dim3(kScanThreads), 0, s, ucnt, U, d_small, part_gt,
+                     part_eq, (uint32_t)R, rkey, rval);
+  BUILD_HIP(hipGetLastError(), "selection launches");
   // 5. rank by count (stable: tuple order among equal counts).
   BUILD_HIP((radix_sort<uint32_t, true>(rkey, rkey_alt, rval, rval_alt, R, 32, hist, part, s)),
             "rank sort");
