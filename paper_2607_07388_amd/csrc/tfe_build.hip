@@ -1089,12 +1089,18 @@ tfe_status ngram_top(const int32_t* tokens, int64_t N, int32_t vocab, int32_t n,
   BUILD_HIP(hipMemsetAsync(selh, 0, 256 * sizeof(uint32_t), s), "memset");
   BUILD_HIP(hipMemcpyAsync(d_small, state0, sizeof state0, hipMemcpyHostToDevice, s), "copy");
   hipLaunchKernelGGL(k_sel_small, dim3(1), dim3(1024), 0, s, sel_bins, d_small);
-  // Few blocks: each adds its LDS histogram to the 256 global bins once.
-  const uint32_t sel_blocks = std::min<uint32_t>(blocks_for(U, 256), 512);
-  for (int shift = 24; shift >= 0; shift -= 8) {
-    hipLaunchKernelGGL(k_sel_hist, dim3(sel_blocks), dim3(256), 0, s, ucnt, U, d_small, shift,
-                       selh);
-    hipLaunchKernelGGL(k_sel_pick, dim3(1), dim3(256), 0, s, selh, d_small, shift);
+  // The R largest counts add up to at most M, so the R-th largest is at
+  // most M / R: below kSelBins - 1 the small-count histogram has found it
+  // for certain, and the radix passes (which would return at once, at
+  // about 5 us per launch) are not launched.
+  if (M / R >= (uint64_t)kSelBins - 1) {
+    // Few blocks: each adds its LDS histogram to the 256 global bins once.
+    const uint32_t sel_blocks = std::min<uint32_t>(blocks_for(U, 256), 512);
+    for (int shift = 24; shift >= 0; shift -= 8) {
+      hipLaunchKernelGGL(k_sel_hist, dim3(sel_blocks), dim3(256), 0, s, ucnt, U, d_small, shift,
+                         selh);
+      hipLaunchKernelGGL(k_sel_pick, dim3(1), dim3(256), 0, s, selh, d_small, shift);
+    }
   }
   BUILD_HIP(hipGetLastError(), "select launches");
   // state = {c*, ~0, needed runs with count c*, runs above c*}.
