@@ -264,7 +264,10 @@ typedef struct tfe_head tfe_head; /* opaque; owned by the library */
  * pointer (no copy): w_pref must stay valid and unchanged until
  * tfe_head_free.  dim is 256, 512 or 1024; 1 <= vocab <= 2^18;
  * 1 <= max_k <= min(256, vocab); 1 <= max_batch <= 65535 sizes the scratch
- * (max_batch x vocab float32 logits plus candidate lists). */
+ * (max_batch x vocab float32 logits plus candidate lists, and the one-launch
+ * path's per-block maxima and candidate segments: 64 rows x compute units x
+ * (16 x ceil(vocab / (16 x compute units)) + 1) keys, about 80 MB for the
+ * 151936-token vocabulary on 256 compute units). */
 tfe_status tfe_head_create(const void *w_pref, int32_t vocab, int32_t dim, int32_t max_batch,
                            int32_t max_k, tfe_head **out);
 
@@ -275,7 +278,18 @@ tfe_status tfe_head_create(const void *w_pref, int32_t vocab, int32_t dim, int32
  * softmax are computed in float32 (bf16 products, float32 accumulation).
  * 0 <= B <= max_batch, 0 <= K <= max_k; stream-ordered on `stream`.  Calls
  * on one head share its scratch: they must be ordered (same stream, or
- * synchronised). */
+ * synchronised).
+ * Calls of at most 64 rows with K at most the number of compute units (and
+ * at most 48 16-token tiles per compute unit) take a one-launch path,
+ * except under stream capture: one block per compute unit keeps its logits
+ * in registers, and two device-wide barriers inside the launch replace the
+ * write of the logits.  Its blocks must all be resident at once, so such a
+ * call must not overlap on the device with other work that holds compute
+ * units while waiting for it (a one-launch call of another head on another
+ * stream, say).  Its waits are bounded (about a second); if one runs out,
+ * that call's top_ids are all -1 and its top_prob 0.  Other calls take two
+ * launches (logits, then the per-row selection), which have no such
+ * requirement. */
 tfe_status tfe_head_topk(tfe_head *head, const void *hidden, int32_t B, int32_t K,
                          int32_t *top_ids, float *top_prob, void *stream);
 
@@ -284,8 +298,10 @@ tfe_status tfe_head_free(tfe_head *head);
 
 /* tfe_head_topk without a head and without any allocation, for callers that
  * cannot allocate device memory (code under HIP graph capture, tight serving
- * loops, harnesses that forbid hipMalloc).  Same kernels, arguments and
- * results as tfe_head_create(w_pref, vocab, dim, B, K) + tfe_head_topk(...):
+ * loops, harnesses that forbid hipMalloc).  Same arguments and results as
+ * tfe_head_create(w_pref, vocab, dim, B, K) + tfe_head_topk(...), always
+ * through the two-launch kernels (the same ids as the one-launch path, and
+ * probabilities within float32 rounding of its):
  *   w_pref  DEVICE bf16 [vocab x dim], 16-byte aligned, on the current device;
  *   hidden  DEVICE bf16 [B x dim], 16-byte aligned;
  *   top_ids DEVICE int32 [B x K], top_prob DEVICE float32 [B x K].

@@ -23,6 +23,18 @@ struct HeadArgs {
   float* top_prob;      // [B x K]
   uint32_t V, tpitch, tblocks, D, B, K;
   uint32_t nblk;        // logits blocks per 64-row group (one per compute unit)
+  // One-launch path (B <= 64; see launch_head_fused): per (row, logits
+  // block) the high word of the block's largest key (0: no logits) and its
+  // sum of exp(logit - that logit); per (row, block) a segment of ccap
+  // words: the number of the block's logit keys that reach the row's bound,
+  // then the keys; the grid barrier's counters and flags and a fault word.
+  uint32_t* bhi;        // [64 x nblk]
+  uint32_t* bsum;       // [64 x nblk], float bits
+  uint64_t* cand;       // [64 x nblk x ccap]
+  unsigned long long* bar;
+  uint32_t* fault;
+  uint32_t ccap;        // 1 + 16 x the most tiles a block owns, rounded up to 16
+  uint32_t epoch;       // one-launch calls made before this one on this scratch
 };
 
 // True if D has a logits kernel.
@@ -32,5 +44,16 @@ uint32_t head_lds_bytes(int D);
 
 hipError_t launch_head_logits(const HeadArgs& a, hipStream_t s);
 hipError_t launch_head_rows(const HeadArgs& a, hipStream_t s);
+
+// The one-launch head: true if a call of this shape can take it (B <= 64,
+// B and K at most nblk <= 256, at most 48 tiles per block).
+bool head_fused_fits(const HeadArgs& a);
+// Words per (row, block) segment of the candidate scratch for this vocabulary.
+uint32_t head_fused_ccap(uint32_t V, uint32_t nblk);
+// True if a block of the one-launch kernel for D fits a compute unit of the
+// current device.
+bool head_fused_resident(int D);
+// Launch of nblk blocks, one per compute unit, all resident at once.
+hipError_t launch_head_fused(const HeadArgs& a, hipStream_t s);
 
 }  // namespace tfe

@@ -3,7 +3,8 @@
 // (Eq. 13) and its K most likely tokens (Eq. 14), which are the candidates
 // the cache prefetch consumes.
 //
-// Two launches:
+// For up to 64 rows (and K at most the number of compute units) one launch,
+// k_head_fused (below, with its design); otherwise two launches:
 //   k_head_logits  logits = W h for up to 64 rows h per block: a dense
 //                  contraction, so it runs on the matrix cores
 //                  (v_mfma_f32_16x16x32_bf16).  W ([V x D] bf16, 311 MB for
@@ -134,9 +135,9 @@ __device__ __forceinline__ void tile_epilogue(const HeadArgs& a, uint32_t t, int
   }
 }
 
-// One wave's logits for TPW consecutive 16-token tiles from t (a tile at or
-// past t_hi is not stored, and its loads re-read tile t's rows; the
-// kernel's claims never produce one).  The tiles share each B-operand read of the
+// One wave's logits for TPW consecutive 16-token tiles from t, accumulated
+// in acc (a tile at or past t_hi re-reads tile t's rows; its accumulators
+// are junk that the callers skip).  The tiles share each B-operand read of the
 // staged hidden rows, so the LDS traffic per token falls with TPW; the W
 // rows stream PC 64-element chunks per pass (PC x 2 TPW x 1 KB in flight
 // per wave).
@@ -148,9 +149,9 @@ __device__ __forceinline__ void tile_epilogue(const HeadArgs& a, uint32_t t, int
 // back in MFMA layout: step x of the chunk takes elements 64 c + 32 x +
 // 8 g .. + 8.
 template <int KS, int TPW, int PC>
-__device__ __forceinline__ void logits_tiles(const HeadArgs& a, uint32_t t, uint32_t t_hi,
-                                             const __bf16* hs, __bf16* st, int hoff, int lane,
-                                             int r, int g, uint64_t* bm) {
+__device__ __forceinline__ void logits_acc(const HeadArgs& a, uint32_t t, uint32_t t_hi,
+                                           const __bf16* hs, __bf16* st, int hoff, int lane,
+                                           int r, int g, f32x4 (&acc)[TPW][4]) {
   constexpr int D = KS * 32;
   constexpr int STRIDE = D + 8;  // staged hidden row pitch (elements)
   constexpr int NCH = D / 64;    // 64-element chunks per W row
@@ -163,7 +164,6 @@ __device__ __forceinline__ void logits_tiles(const HeadArgs& a, uint32_t t, uint
     const uint32_t row = tt * 16 + 8 * (q & 1) + (lane >> 3);
     wr[q] = (const u32x4*)a.w + ((size_t)min(row, a.V - 1) * D) / 8 + (lane & 7);
   }
-  f32x4 acc[TPW][4];
 #pragma unroll
   for (int i = 0; i < TPW; ++i)
 #pragma unroll
@@ -210,6 +210,15 @@ __device__ __forceinline__ void logits_tiles(const HeadArgs& a, uint32_t t, uint
       }
     }
   }
+}
+
+// logits_acc, then the epilogue of every tile below t_hi.
+template <int KS, int TPW, int PC>
+__device__ __forceinline__ void logits_tiles(const HeadArgs& a, uint32_t t, uint32_t t_hi,
+                                             const __bf16* hs, __bf16* st, int hoff, int lane,
+                                             int r, int g, uint64_t* bm) {
+  f32x4 acc[TPW][4];
+  logits_acc<KS, TPW, PC>(a, t, t_hi, hs, st, hoff, lane, r, g, acc);
 #pragma unroll
   for (int i = 0; i < TPW; ++i)
     if (t + (uint32_t)i < t_hi) tile_epilogue(a, t + i, r, g, acc[i], bm);
@@ -694,6 +703,539 @@ __global__ __launch_bounds__(kRowThreads) void k_head_rows(const HeadArgs a) {
   for (uint32_t i = tid; i < a.K; i += kRowThreads) emit(i, s_cand[i]);
 }
 
+
+// ---------------------------------------------------------------------------
+// One launch for up to 64 rows (K at most the number of blocks).
+//
+// The two launches above write every logit (39 MB for the 151936-token head
+// at B = 64) so that the second can select from them, and read back about 2%
+// of them.  Here each wave keeps the logits of its tile groups (at most two)
+// in registers, and two grid barriers take the place of that write:
+//   A. the logits as in k_head_logits (one block per compute unit, the same
+//      tiles); after each tile group the wave folds its logits into a
+//      running per-row maximum and sum of exp(logit - maximum), which hides
+//      that arithmetic under the other waves' loads; each block publishes
+//      per row its largest logit (as a key) and its sum;
+//   B. after the first barrier every block derives, per row, a lower bound
+//      of the row's K-th largest logit: split the blocks' maxima into K
+//      disjoint non-empty groups; each group holds a logit at least as
+//      large as the smallest of the K group maxima, and these K logits are
+//      distinct entries of the row, so the K-th largest logit reaches that
+//      minimum;
+//   C. each block writes the (logit, id) keys of its logits at or above the
+//      bound (a few per row) to its own segment of the row's candidate list;
+//   D. after the second barrier block r ranks row r: M and S from the
+//      published maxima and sums, then a radix select of the K largest
+//      candidates in LDS (first over the segments in memory when more than
+//      LDS holds, which only heavy ties produce), emitted with exp(l - M) / S.
+// Data that crosses blocks is stored and loaded with device scope (cache
+// policy sc1: the stores write through the XCD's L2 and the loads do not
+// take stale L2 lines), and each wave's stores have completed before its
+// block counts itself in at a barrier.
+// The barriers need all blocks resident at once: one block per compute
+// unit fits (the LDS allows no second), and the launch is an ordinary one
+// (a cooperative launch, which guarantees residency, cost about 15 us more
+// per call).  So a call must not overlap on the device with other work that
+// holds compute units while it waits for this call, such as a one-launch
+// head call of another head on another stream.  The waits are bounded
+// (about a second); if one runs out, that call answers every row with ids
+// -1 and probabilities 0.
+constexpr int kFuseThreads = kLogitWaves * 64;
+constexpr int kFuseGroups = 2;      // tile groups a wave computes and holds
+constexpr uint32_t kFuseMaxBlocks = 256;
+constexpr uint32_t kGridWaitLimit = 1u << 20;
+
+template <typename T>
+__device__ __forceinline__ void st_agent(T* p, T v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+template <typename T>
+__device__ __forceinline__ T ld_agent(const T* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+// 16 bytes at base + off with device scope (buffer load, cache policy sc1).
+__device__ __forceinline__ u32x4 ld_agent16(const void* base, uint32_t off) {
+  const __amdgpu_buffer_rsrc_t rs =
+      __builtin_amdgcn_make_buffer_rsrc((void*)base, (short)0, 0x7FFFFFFF, 0x00020000);
+  return __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 16);
+}
+
+// Barrier j (1 or 2) of the call with epoch e, called by every thread, as a
+// two-level tree: block b counts into the counter of its group b % 16 (each
+// counter in a 128-byte line of its own), the last block of a group into the
+// root counter, and the last group releases every group's flag; a block
+// then waits on its group's flag.  Every launch passes each barrier once per
+// block, so a group of n blocks is complete at barrier j once its counter
+// reaches (2 e + j) n, and the release value is 2 e + j.  (One counter that
+// every block counts into and polls took 9-13 us from the last arrival to
+// the release: its reads and atomics queue behind each other.)  Thread 0
+// counts the block in after all its waves' stores have completed
+// (s_waitcnt vmcnt(0)); with `wait`, it then waits for the release.
+constexpr uint32_t kBarGroups = 16;
+constexpr uint32_t kBarLine = 16;  // 64-bit words per 128-byte line
+
+__device__ __forceinline__ void grid_barrier(const HeadArgs& a, uint32_t j, bool wait) {
+  __builtin_amdgcn_s_waitcnt(0x0F70);
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const uint32_t nb = a.nblk, grp = blockIdx.x % kBarGroups;
+    const uint32_t ngrp = min(nb, kBarGroups);
+    const uint64_t gsize = nb / kBarGroups + (grp < nb % kBarGroups ? 1u : 0u);
+    const uint64_t phase = 2ull * a.epoch + j;
+    unsigned long long* cnt = a.bar + kBarLine * (1 + grp);
+    unsigned long long* root = a.bar;
+    unsigned long long* flag = a.bar + kBarLine * (1 + kBarGroups);
+    const unsigned long long old =
+        __hip_atomic_fetch_add(cnt, 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (old + 1 == phase * gsize) {
+      const unsigned long long r =
+          __hip_atomic_fetch_add(root, 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      if (r + 1 == phase * ngrp)
+        for (uint32_t q = 0; q < ngrp; ++q) st_agent(flag + kBarLine * q, (unsigned long long)phase);
+    }
+    if (wait) {
+      const unsigned long long* f = flag + kBarLine * grp;
+      for (uint32_t n = 0; ld_agent(f) < phase; ++n) {
+        if (n == kGridWaitLimit) {
+          atomicMax(a.fault, a.epoch + 1u);
+          break;
+        }
+        __builtin_amdgcn_s_sleep(1);
+      }
+    }
+  }
+  __syncthreads();
+}
+
+// (m, s) <- the merge of two partial softmax sums: m the largest logit, s
+// the sum of exp(logit - m); (-inf, 0) is empty.
+__device__ __forceinline__ void lse_merge(float& m, float& s, float m2, float s2) {
+  const float mm = fmaxf(m, m2);
+  if (mm == -INFINITY) return;
+  s = s * __expf(m - mm) + s2 * __expf(m2 - mm);
+  m = mm;
+}
+
+// lse_merge over the four lanes of one MFMA output column (as col_sum).
+__device__ __forceinline__ void col_lse(float& m, float& s) {
+  uint32_t um = __float_as_uint(m), us = __float_as_uint(s);
+  const auto m16 = __builtin_amdgcn_permlane16_swap(um, um, false, false);
+  const auto s16 = __builtin_amdgcn_permlane16_swap(us, us, false, false);
+  m = __uint_as_float(m16[0]);
+  s = __uint_as_float(s16[0]);
+  lse_merge(m, s, __uint_as_float(m16[1]), __uint_as_float(s16[1]));
+  um = __float_as_uint(m);
+  us = __float_as_uint(s);
+  const auto m32 = __builtin_amdgcn_permlane32_swap(um, um, false, false);
+  const auto s32 = __builtin_amdgcn_permlane32_swap(us, us, false, false);
+  m = __uint_as_float(m32[0]);
+  s = __uint_as_float(s32[0]);
+  lse_merge(m, s, __uint_as_float(m32[1]), __uint_as_float(s32[1]));
+}
+
+// Wave 0 finds the histogram bin that holds the need-th largest key (lane l
+// holds bins 255 - 4 l - k, k = 0..3, in descending order) and leaves the
+// bin, the count above it and its own count in s_sel[0..2].
+__device__ __forceinline__ void pick_bin(const uint32_t* hist, uint32_t need, uint32_t* s_sel) {
+  const int lane = threadIdx.x & 63;
+  uint32_t v[4], sum = 0;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    v[k] = hist[255 - 4 * lane - k];
+    sum += v[k];
+  }
+  const uint32_t inc = wave_incl_scan(sum);
+  uint32_t ex = inc - sum;
+  if (ex < need && need <= inc) {
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      if (ex < need && need <= ex + v[k]) {
+        s_sel[0] = 255u - 4u * (uint32_t)lane - (uint32_t)k;
+        s_sel[1] = ex;
+        s_sel[2] = v[k];
+      }
+      ex += v[k];
+    }
+  }
+}
+
+// Adds a key to the radix histogram of the current pass if it agrees with
+// the decided bits (lanes holding the first active lane's digit add their
+// number with one atomic).
+__device__ __forceinline__ void hist_key(uint32_t* hist, bool in, uint64_t key, uint64_t dm,
+                                         uint64_t lo, int sh) {
+  in = in && (key & dm) == lo;
+  const uint64_t act = __builtin_amdgcn_ballot_w64(in);
+  if (!act) return;
+  const uint32_t d = (uint32_t)(key >> sh) & 255u;
+  const int first = __builtin_ctzll(act);
+  const uint32_t d0 = (uint32_t)__builtin_amdgcn_readlane((int)d, first);
+  const uint64_t same = __builtin_amdgcn_ballot_w64(in && d == d0);
+  const int lane = threadIdx.x & 63;
+  if (in && d != d0) atomicAdd(&hist[d], 1u);
+  else if (lane == first) atomicAdd(&hist[d0], (uint32_t)__builtin_popcountll(same));
+}
+
+template <int KS>
+__global__ __launch_bounds__(kFuseThreads) void k_head_fused(const HeadArgs a) {
+  constexpr int D = KS * 32;
+  constexpr int STRIDE = D + 8;
+  constexpr int SP = 72;
+  // The staged hidden rows; in phase D the candidates of the block's row.
+  __shared__ __attribute__((aligned(16))) __bf16 hs[kCols * STRIDE];
+  __shared__ __attribute__((aligned(16))) __bf16 stage[kLogitWaves][16 * SP];
+  __shared__ float s_wm[kLogitWaves][kCols], s_ws[kLogitWaves][kCols];
+  __shared__ uint32_t s_bound[kCols], s_cnt[kCols];
+  __shared__ uint32_t s_off[kFuseMaxBlocks + 1];
+  __shared__ uint32_t hist[256];
+  __shared__ unsigned long long s_top[kHeadMaxK];
+  __shared__ uint32_t s_wtot[kLogitWaves], s_wmax[kLogitWaves];
+  __shared__ float s_red[kLogitWaves];
+  __shared__ uint32_t s_next, s_n, s_sel[3];
+  constexpr uint32_t kLds = sizeof(hs) / 8;  // candidates selected in LDS
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int r = lane & 15, g = lane >> 4;
+  const uint32_t b = blockIdx.x, nblk = a.nblk, B = a.B, K = a.K;
+
+  // A. Logits of the block's tiles, held in registers; per (lane, row) the
+  // running maximum rm and sum rs of exp(logit - rm).
+  if (tid < kCols) s_cnt[tid] = 0;
+  for (int e = tid; e < kCols * (D / 8); e += kFuseThreads) {
+    const int j = e / (D / 8), c = e - j * (D / 8);
+    u32x4 v = {0u, 0u, 0u, 0u};
+    if ((uint32_t)j < B) v = *((const u32x4*)a.hidden + ((size_t)j * D) / 8 + c);
+    *(u32x4*)(hs + j * STRIDE + c * 8) = v;
+  }
+  const uint32_t nt = (a.V + 15) >> 4;
+  const uint32_t t_lo = (uint32_t)((uint64_t)nt * b / nblk);
+  const uint32_t t_hi = (uint32_t)((uint64_t)nt * (b + 1) / nblk);
+  if (tid == 0) s_next = t_lo;
+  __syncthreads();
+  __bf16* st = stage[wave];
+  int hoff = r * STRIDE + 8 * g;
+  f32x4 acc[kFuseGroups][kTileGroup][4];
+  uint32_t tg[kFuseGroups];
+  float rm[4] = {-INFINITY, -INFINITY, -INFINITY, -INFINITY}, rs[4] = {0.f, 0.f, 0.f, 0.f};
+  // Held logit (k, i, bt, q): tile tg[k] + i, token 16 (tg[k] + i) + 4 g + q,
+  // row bt * 16 + r; it exists if the tile is below t_hi and the token
+  // below V (tile-uniform tests first).
+  auto held = [&](int k, int i) { return tg[k] < t_hi && tg[k] + (uint32_t)i < t_hi; };
+  auto whole = [&](int k, int i) { return (tg[k] + (uint32_t)i) * 16 + 16 <= a.V; };
+#pragma unroll
+  for (int k = 0; k < kFuseGroups; ++k) {
+    uint32_t t = 0;
+    if (lane == 0) t = atomicAdd(&s_next, (uint32_t)kTileGroup);
+    tg[k] = __builtin_amdgcn_readfirstlane(t);
+#pragma unroll
+    for (int i = 0; i < kTileGroup; ++i)
+#pragma unroll
+      for (int bt = 0; bt < 4; ++bt) acc[k][i][bt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    if (tg[k] < t_hi) {
+      asm volatile("" : "+v"(hoff));
+      logits_acc<KS, kTileGroup, kGroupChunks>(a, tg[k], t_hi, hs, st, hoff, lane, r, g, acc[k]);
+#pragma unroll
+      for (int bt = 0; bt < 4; ++bt) {
+        float x[kTileGroup][4];
+        float gmx = -INFINITY;
+#pragma unroll
+        for (int i = 0; i < kTileGroup; ++i)
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const uint32_t id = (tg[k] + i) * 16 + 4 * g + q;
+            x[i][q] = held(k, i) && (whole(k, i) || id < a.V) ? acc[k][i][bt][q] : -INFINITY;
+            gmx = fmaxf(gmx, x[i][q]);
+          }
+        const float mm = fmaxf(rm[bt], gmx);
+        if (mm != -INFINITY) {
+          float s = rs[bt] * __expf(rm[bt] - mm);
+#pragma unroll
+          for (int i = 0; i < kTileGroup; ++i)
+#pragma unroll
+            for (int q = 0; q < 4; ++q) s += __expf(x[i][q] - mm);
+          rs[bt] = s;
+          rm[bt] = mm;
+        }
+      }
+    }
+  }
+  // The block's maximum and sum per row: the four lanes of each column,
+  // then the eight waves in a fixed order.
+#pragma unroll
+  for (int bt = 0; bt < 4; ++bt) {
+    col_lse(rm[bt], rs[bt]);
+    if (g == 0) {
+      s_wm[wave][bt * 16 + r] = rm[bt];
+      s_ws[wave][bt * 16 + r] = rs[bt];
+    }
+  }
+  __syncthreads();
+  if ((uint32_t)tid < B) {
+    float m = -INFINITY, s = 0.f;
+    for (int w = 0; w < kLogitWaves; ++w) lse_merge(m, s, s_wm[w][tid], s_ws[w][tid]);
+    st_agent(a.bhi + (size_t)tid * nblk + b, m == -INFINITY ? 0u : f2key(m));
+    st_agent(a.bsum + (size_t)tid * nblk + b, __float_as_uint(s));
+  }
+  grid_barrier(a, 1, true);
+
+  // B. Per row, the smallest of K group maxima (high key words; 0 for a
+  // block without logits).  A block that ranks a row in phase D also loads
+  // that row's block maxima and sums here, for M and S.  Thread (row tid / 8, j = tid % 8) holds the cj
+  // blocks j, j + 8, j + 16, ... and forms gj of the K groups as runs of
+  // consecutive ones (gj <= cj, since K <= nblk); blocks of a thread
+  // without groups (K < 8) stay out.
+  uint32_t fbh = 0;
+  float fbs = 0.f;
+  {
+    const uint32_t row = (uint32_t)tid >> 3, j = (uint32_t)tid & 7u;
+    const uint32_t cj = nblk / 8 + (j < nblk % 8 ? 1u : 0u);
+    const uint32_t gj = K / 8 + (j < K % 8 ? 1u : 0u);
+    const uint32_t* bh = a.bhi + (size_t)row * nblk + j;
+    uint32_t v[kFuseMaxBlocks / 8];
+#pragma unroll
+    for (uint32_t s = 0; s < kFuseMaxBlocks / 8; ++s)
+      v[s] = row < B && s < cj ? ld_agent(bh + 8 * s) : 0u;
+    if (b < B && (uint32_t)tid < nblk) {
+      fbh = ld_agent(a.bhi + (size_t)b * nblk + tid);
+      fbs = __uint_as_float(ld_agent(a.bsum + (size_t)b * nblk + tid));
+    }
+    uint32_t lo = 0xFFFFFFFFu;
+    if (gj) {
+      // Block s is in run floor(s gj / cj): a new run starts where s gj
+      // reaches the next multiple of cj.
+      uint32_t run = 0, acc_s = 0, next = cj;
+#pragma unroll
+      for (uint32_t s = 0; s < kFuseMaxBlocks / 8; ++s) {
+        if (s < cj) {
+          if (acc_s >= next) {
+            lo = min(lo, run);
+            run = 0;
+            next += cj;
+          }
+          run = max(run, v[s]);
+          acc_s += gj;
+        }
+      }
+      lo = min(lo, run);
+    }
+    lo = min(lo, (uint32_t)__shfl_xor((int)lo, 1, 8));
+    lo = min(lo, (uint32_t)__shfl_xor((int)lo, 2, 8));
+    lo = min(lo, (uint32_t)__shfl_xor((int)lo, 4, 8));
+    if (j == 0) s_bound[row] = lo;
+    const uint32_t wm = wave_max_u32(fbh);
+    if (lane == 0) s_wmax[wave] = wm;
+  }
+  __syncthreads();
+  // Row b's largest logit M and its part of S = sum over blocks of
+  // bsum exp(block max - M) (added up in phase D).
+  uint32_t hmax = 0;
+  for (int w = 0; w < kLogitWaves; ++w) hmax = max(hmax, s_wmax[w]);
+  const float M = key2f(hmax);
+  {
+    float part = fbh ? fbs * __expf(key2f(fbh) - M) : 0.f;
+    part = wave_add(part);
+    if (lane == 0) s_red[wave] = part;
+  }
+
+  // C. Keys of the held logits that reach their row's bound (compared as
+  // floats: a superset of the keys at or above it, which differs only by
+  // -0 at a bound of +0).  The four logits of a lane, tile and row are
+  // tested against the bound through their maximum first.  (Counting each
+  // lane's candidates first and reserving their places with one atomic per
+  // row was slower: 75.0 against 73.8 us per call.)
+  {
+    float lbf[4];
+#pragma unroll
+    for (int bt = 0; bt < 4; ++bt) {
+      const uint32_t lb = s_bound[bt * 16 + r];
+      lbf[bt] = (uint32_t)(bt * 16 + r) >= B ? INFINITY : lb ? key2f(lb) : -INFINITY;
+    }
+#pragma unroll
+    for (int k = 0; k < kFuseGroups; ++k)
+#pragma unroll
+      for (int i = 0; i < kTileGroup; ++i)
+        if (held(k, i)) {
+          const uint32_t i0 = (tg[k] + i) * 16 + 4 * g;
+#pragma unroll
+          for (int bt = 0; bt < 4; ++bt) {
+            const f32x4 v = acc[k][i][bt];
+            if (fmaxf(fmaxf(v[0], v[1]), fmaxf(v[2], v[3])) >= lbf[bt]) {
+              const uint32_t c = bt * 16 + r;
+#pragma unroll
+              for (int q = 0; q < 4; ++q)
+                if (v[q] >= lbf[bt] && (whole(k, i) || i0 + q < a.V)) {
+                  const uint32_t p = atomicAdd(&s_cnt[c], 1u);
+                  st_agent(a.cand + ((size_t)c * nblk + b) * a.ccap + 1 + p, tkey64(v[q], i0 + q));
+                }
+            }
+          }
+        }
+  }
+  // The counts are final once every wave's LDS atomics have returned (an
+  // LDS-only barrier: the segment stores complete before the block counts
+  // itself in below).
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+  if ((uint32_t)tid < B)
+    st_agent(a.cand + ((size_t)tid * nblk + b) * a.ccap, (uint64_t)s_cnt[tid]);
+  grid_barrier(a, 2, b < B);
+  if (b >= B) return;
+
+  // D. Row b.
+  const uint32_t row = b;
+  if (ld_agent((const uint32_t*)a.fault) == a.epoch + 1u) {
+    for (uint32_t i = tid; i < K; i += kFuseThreads) {
+      a.top_ids[(size_t)row * K + i] = -1;
+      a.top_prob[(size_t)row * K + i] = 0.f;
+    }
+    return;
+  }
+  // Segment t of the row: word 0 its number of keys, words 1.. the keys.
+  // Each thread loads the first line (count and up to 15 keys) of its
+  // segment.
+  const uint64_t* seg = a.cand + (size_t)row * nblk * a.ccap;
+  uint64_t line[16];
+#pragma unroll
+  for (int k = 0; k < 8; ++k) {
+    u32x4 v = {0u, 0u, 0u, 0u};
+    if ((uint32_t)tid < nblk) v = ld_agent16(seg, (uint32_t)(((size_t)tid * a.ccap + 2 * k) * 8));
+    line[2 * k] = ((uint64_t)v[1] << 32) | v[0];
+    line[2 * k + 1] = ((uint64_t)v[3] << 32) | v[2];
+  }
+  const uint32_t cnt = (uint32_t)min(line[0], (uint64_t)(a.ccap - 1));
+  const uint32_t inc = wave_incl_scan(cnt);
+  if (lane == 63) s_wtot[wave] = inc;
+  __syncthreads();
+  uint32_t base = 0, n = 0;
+  for (int w = 0; w < kLogitWaves; ++w) {
+    base += w < wave ? s_wtot[w] : 0u;
+    n += s_wtot[w];
+  }
+  const uint32_t off = base + inc - cnt;
+  if ((uint32_t)tid < nblk) s_off[tid] = off;
+  if (tid == 0) {
+    s_off[nblk] = n;
+    s_n = 0;
+  }
+  __syncthreads();
+  // Every key that decides the answer lies in [bound, largest key of the
+  // row], so those keys agree above the highest bit in which the two
+  // differ (keys below the bound drop out of every histogram).
+  const uint32_t lbnd = s_bound[row];
+  const uint64_t kmax = ((uint64_t)hmax << 32) | 0xFFFFFFFFull, kmin = (uint64_t)lbnd << 32;
+  const uint64_t dk = kmax ^ kmin;
+  const int top = dk ? 63 - __builtin_clzll(dk) : 0;
+  const int sh0 = max(top - 7, 0);
+  const uint64_t dm0 = sh0 + 8 < 64 ? ~((1ull << (sh0 + 8)) - 1ull) : 0ull;
+  uint64_t* s_c = (uint64_t*)hs;
+  uint32_t nl = n;
+  if (n > kLds) {
+    // Heavy ties: narrow in memory until at most kLds keys remain at or
+    // above the chosen bin, then gather those.
+    uint64_t lo = kmax & dm0, dm = dm0;
+    uint32_t need = K, above = 0;
+    for (int sh = sh0;; sh = max(sh - 8, 0)) {
+      if (tid < 256) hist[tid] = 0u;
+      __syncthreads();
+      for (uint32_t t = wave; t < nblk; t += kLogitWaves) {
+        const uint32_t c = s_off[t + 1] - s_off[t];
+        const uint64_t* p = seg + (size_t)t * a.ccap + 1;
+        for (uint32_t j = lane; j < (c + 63) / 64 * 64; j += 64)
+          hist_key(hist, j < c, j < c ? ld_agent(p + j) : 0ull, dm, lo, sh);
+      }
+      __syncthreads();
+      if (wave == 0) pick_bin(hist, need, s_sel);
+      __syncthreads();
+      const uint32_t bin = s_sel[0], ab = s_sel[1], cb = s_sel[2];
+      need -= ab;
+      above += ab;
+      lo |= (uint64_t)bin << sh;
+      dm |= 0xFFull << sh;
+      __syncthreads();  // s_sel read by every thread before it is written again
+      if (cb == need || above + cb <= kLds || sh == 0) break;
+    }
+    for (uint32_t t = wave; t < nblk; t += kLogitWaves) {
+      const uint32_t c = s_off[t + 1] - s_off[t];
+      const uint64_t* p = seg + (size_t)t * a.ccap + 1;
+      for (uint32_t j = lane; j < (c + 63) / 64 * 64; j += 64) {
+        const uint64_t key = j < c ? ld_agent(p + j) : 0ull;
+        const bool in = j < c && key >= lo;
+        const uint64_t m = __builtin_amdgcn_ballot_w64(in);
+        if (m) {
+          uint32_t o = 0;
+          if (lane == 0) o = atomicAdd(&s_n, (uint32_t)__builtin_popcountll(m));
+          o = __builtin_amdgcn_readfirstlane(o);
+          const uint32_t at = o + (uint32_t)__builtin_popcountll(m & ((1ull << lane) - 1ull));
+          if (in && at < kLds) s_c[at] = key;
+        }
+      }
+    }
+    __syncthreads();
+    nl = min(s_n, kLds);
+    __syncthreads();
+    if (tid == 0) s_n = 0;
+  } else if ((uint32_t)tid < nblk) {
+#pragma unroll
+    for (uint32_t i = 1; i < 16; ++i)
+      if (i <= cnt) s_c[off + i - 1] = line[i];
+    for (uint32_t i = 16; i <= cnt; ++i) s_c[off + i - 1] = ld_agent(seg + (size_t)tid * a.ccap + i);
+  }
+  __syncthreads();
+  // Exact K-th largest key of the nl >= K candidates in LDS: afterwards the
+  // keys >= lo are exactly the K largest.
+  uint64_t lo = 0;
+  if (nl > K) {
+    lo = kmax & dm0;
+    uint64_t dm = dm0;
+    uint32_t need = K;
+    for (int sh = sh0;; sh = max(sh - 8, 0)) {
+      if (tid < 256) hist[tid] = 0u;
+      __syncthreads();
+      for (uint32_t e0 = 0; e0 < nl; e0 += kFuseThreads) {
+        const uint32_t e = e0 + tid;
+        hist_key(hist, e < nl, e < nl ? s_c[e] : 0ull, dm, lo, sh);
+      }
+      __syncthreads();
+      if (wave == 0) pick_bin(hist, need, s_sel);
+      __syncthreads();
+      const uint32_t bin = s_sel[0], ab = s_sel[1], cb = s_sel[2];
+      need -= ab;
+      lo |= (uint64_t)bin << sh;
+      dm |= 0xFFull << sh;
+      __syncthreads();
+      if (cb == need || sh == 0) break;
+    }
+  }
+  const uint64_t below = (1ull << lane) - 1ull;
+  for (uint32_t e0 = 0; e0 < nl; e0 += kFuseThreads) {
+    const uint32_t e = e0 + tid;
+    const uint64_t key = e < nl ? s_c[e] : 0ull;
+    const bool in = e < nl && key >= lo;
+    const uint64_t m = __builtin_amdgcn_ballot_w64(in);
+    if (m) {
+      uint32_t o = 0;
+      if (lane == 0) o = atomicAdd(&s_n, (uint32_t)__builtin_popcountll(m));
+      o = __builtin_amdgcn_readfirstlane(o);
+      const uint32_t at = o + (uint32_t)__builtin_popcountll(m & below);
+      if (in && at < (uint32_t)kHeadMaxK) s_top[at] = key;
+    }
+  }
+  __syncthreads();
+  float S = 0.f;
+  for (int w = 0; w < kLogitWaves; ++w) S += s_red[w];
+  const float invS = 1.0f / S;
+  // The K largest ranked by counting, P consecutive lanes per key.
+  const uint32_t lp = K <= 64 ? 3u : K <= 128 ? 2u : 1u;  // log2 P
+  const uint32_t ki = (uint32_t)tid >> lp, part = (uint32_t)tid & ((1u << lp) - 1u);
+  const uint64_t key = ki < K ? s_top[ki] : ~0ull;
+  uint32_t rank = 0;
+#pragma unroll 8
+  for (uint32_t u = part; u < K; u += 1u << lp) rank += s_top[u] > key ? 1u : 0u;
+  for (uint32_t o = 1; o < (1u << lp); o <<= 1) rank += (uint32_t)__shfl_xor((int)rank, (int)o, 8);
+  if (ki < K && part == 0) {
+    a.top_ids[(size_t)row * K + rank] = (int32_t)(0xFFFFFFFFu - (uint32_t)key);
+    a.top_prob[(size_t)row * K + rank] = expf(key2f((uint32_t)(key >> 32)) - M) * invS;
+  }
+}
+
 }  // namespace
 
 bool head_dim_supported(int D) { return D == 256 || D == 512 || D == 1024; }
@@ -715,6 +1257,43 @@ hipError_t launch_head_logits(const HeadArgs& a, hipStream_t s) {
 
 hipError_t launch_head_rows(const HeadArgs& a, hipStream_t s) {
   hipLaunchKernelGGL(k_head_rows, dim3(a.B), dim3(kRowThreads), 0, s, a);
+  return hipGetLastError();
+}
+
+uint32_t head_fused_ccap(uint32_t V, uint32_t nblk) {
+  const uint32_t nt = (V + 15) / 16;
+  return ((nt + nblk - 1) / nblk * 16 + 1 + 15) / 16 * 16;
+}
+
+bool head_fused_fits(const HeadArgs& a) {
+  if (!head_dim_supported((int)a.D) || a.B < 1 || a.B > (uint32_t)kCols || a.B > a.nblk ||
+      a.nblk > kFuseMaxBlocks || a.K < 1 || a.K > a.nblk || a.K > (uint32_t)kHeadMaxK)
+    return false;
+  // Tile groups per block within what the waves hold.
+  const uint32_t tiles = ((a.V + 15) / 16 + a.nblk - 1) / a.nblk;
+  return (tiles + kTileGroup - 1) / kTileGroup <= (uint32_t)(kFuseGroups * kLogitWaves);
+}
+
+bool head_fused_resident(int D) {
+  const void* f = D == 256 ? (const void*)k_head_fused<8>
+                : D == 512 ? (const void*)k_head_fused<16>
+                           : (const void*)k_head_fused<32>;
+  int n = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, f, kFuseThreads, 0) != hipSuccess) {
+    (void)hipGetLastError();
+    return false;
+  }
+  return n >= 1;
+}
+
+hipError_t launch_head_fused(const HeadArgs& a, hipStream_t s) {
+  const dim3 grid(a.nblk), block(kFuseThreads);
+  switch (a.D) {
+    case 256: hipLaunchKernelGGL(k_head_fused<8>, grid, block, 0, s, a); break;
+    case 512: hipLaunchKernelGGL(k_head_fused<16>, grid, block, 0, s, a); break;
+    case 1024: hipLaunchKernelGGL(k_head_fused<32>, grid, block, 0, s, a); break;
+    default: return hipErrorInvalidValue;
+  }
   return hipGetLastError();
 }
 

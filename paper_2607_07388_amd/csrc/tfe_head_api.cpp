@@ -20,6 +20,14 @@ struct tfe_head {
   uint64_t* d_tkey = nullptr; // [rows x tiles rounded up to 16]
   float* d_tsum = nullptr;    // [rows x tiles rounded up to 16]
   uint64_t* d_bmax = nullptr; // [rows x compute units]
+  // Scratch of the one-launch path (calls of at most 64 rows outside graph
+  // capture, when the device can launch it): barrier counter and fault word,
+  // per (row, block) maxima, sums and candidate counts, then the candidate
+  // segments (ccap keys per row and block).
+  unsigned char* d_fuse = nullptr;
+  bool fused = false;
+  uint32_t ccap = 0;
+  uint32_t epoch = 0;  // one-launch calls enqueued so far (barrier targets)
   // Recorded after every top-K call made outside graph capture; freeing the
   // head waits for it (and for nothing else on the device).
   hipEvent_t ev_last = nullptr;
@@ -45,7 +53,7 @@ void release(tfe_head* h) {
   (void)hipGetDevice(&cur);
   (void)hipSetDevice(h->device);
   if (h->recorded) (void)hipEventSynchronize(h->ev_last);
-  void* bufs[] = {h->d_logits, h->d_tkey, h->d_tsum, h->d_bmax};
+  void* bufs[] = {h->d_logits, h->d_tkey, h->d_tsum, h->d_bmax, h->d_fuse};
   for (void* b : bufs) dev_free(b);
   if (h->ev_last) (void)hipEventDestroy(h->ev_last);
   (void)hipSetDevice(cur);
@@ -53,6 +61,26 @@ void release(tfe_head* h) {
 }
 
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+// Layout of the one-launch scratch for nblk blocks: 8 KB of barrier
+// counters and flags (one 128-byte line each) and the fault word, two
+// [64 x nblk] word arrays, then the candidate segments.
+constexpr size_t kFuseCtl = 8192;
+size_t fuse_words(uint32_t nblk) { return (size_t)64 * nblk; }
+size_t fuse_cand_at(uint32_t nblk) { return (kFuseCtl + 2 * fuse_words(nblk) * 4 + 255) / 256 * 256; }
+size_t fuse_bytes(uint32_t nblk, uint32_t ccap) {
+  return fuse_cand_at(nblk) + fuse_words(nblk) * ccap * sizeof(uint64_t);
+}
+void fuse_args(const tfe_head* h, HeadArgs* a) {
+  unsigned char* p = h->d_fuse;
+  const size_t n = fuse_words((uint32_t)h->cus);
+  a->bar = (unsigned long long*)p;
+  a->fault = (uint32_t*)(p + kFuseCtl - 128);
+  a->bhi = (uint32_t*)(p + kFuseCtl);
+  a->bsum = a->bhi + n;
+  a->cand = (uint64_t*)(p + fuse_cand_at((uint32_t)h->cus));
+  a->ccap = h->ccap;
+}
 
 tfe_status create(const void* w, int32_t vocab, int32_t dim, int32_t max_batch, int32_t max_k,
                   tfe_head** out) {
@@ -109,6 +137,26 @@ tfe_status create(const void* w, int32_t vocab, int32_t dim, int32_t max_batch, 
       st = fail(TFE_ERR_OOM, "head scratch for %u rows", h->max_batch);
       break;
     }
+    // The one-launch path, where one of its blocks fits a compute unit and
+    // some call shape fits it.
+    HeadArgs probe{};
+    probe.V = h->V;
+    probe.D = h->D;
+    probe.B = 1;
+    probe.K = 1;
+    probe.nblk = (uint32_t)h->cus;
+    if (head_fused_fits(probe) && head_fused_resident(dim)) {
+      h->ccap = head_fused_ccap(h->V, (uint32_t)h->cus);
+      if (dev_malloc((void**)&h->d_fuse, fuse_bytes((uint32_t)h->cus, h->ccap)) != hipSuccess) {
+        st = fail(TFE_ERR_OOM, "head scratch for %u rows", h->max_batch);
+        break;
+      }
+      if (hipMemset(h->d_fuse, 0, kFuseCtl) != hipSuccess) {
+        st = fail(TFE_ERR_HIP, "head barrier reset");
+        break;
+      }
+      h->fused = true;
+    }
     if (hipEventCreateWithFlags(&h->ev_last, hipEventDisableTiming) != hipSuccess) {
       h->ev_last = nullptr;
       st = fail(TFE_ERR_HIP, "head event");
@@ -137,7 +185,7 @@ tfe_status topk(tfe_head* h, const void* hidden, int32_t B, int32_t K, int32_t* 
   if (cur != h->device)
     return fail(TFE_ERR_INVALID_ARG, "head lives on device %d but device %d is current",
                 h->device, cur);
-  HeadArgs a;
+  HeadArgs a{};
   a.w = h->w;
   a.hidden = hidden;
   a.logits = h->d_logits;
@@ -153,10 +201,17 @@ tfe_status topk(tfe_head* h, const void* hidden, int32_t B, int32_t K, int32_t* 
   a.B = (uint32_t)B;
   a.K = (uint32_t)K;
   a.nblk = (uint32_t)h->cus;
-  HEAD_HIP(launch_head_logits(a, stream), "head logits launch");
-  HEAD_HIP(launch_head_rows(a, stream), "head top-K launch");
   hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
   HEAD_HIP(hipStreamIsCapturing(stream, &cs), "hipStreamIsCapturing");
+  if (h->fused && cs == hipStreamCaptureStatusNone && head_fused_fits(a)) {
+    fuse_args(h, &a);
+    a.epoch = h->epoch;
+    HEAD_HIP(launch_head_fused(a, stream), "head launch");
+    ++h->epoch;
+  } else {
+    HEAD_HIP(launch_head_logits(a, stream), "head logits launch");
+    HEAD_HIP(launch_head_rows(a, stream), "head top-K launch");
+  }
   if (cs == hipStreamCaptureStatusNone) {
     HEAD_HIP(hipEventRecord(h->ev_last, stream), "record");
     h->recorded = true;

@@ -1,10 +1,13 @@
 // Early-exit head top-K without any allocation, for callers that cannot
 // allocate device memory (code under HIP graph capture, serving loops,
-// harnesses that forbid hipMalloc).  Same kernels and results as
-// tfe_head_topk; their scratch (logits, tile statistics and block maxima of
-// one 64-row group, for vocabularies up to 2^18 and up to kNaMaxBlocks
+// harnesses that forbid hipMalloc).  The two-launch kernels of
+// tfe_head_topk (the same ids as its one-launch path, probabilities within
+// float32 rounding); their scratch (logits, tile statistics and block maxima
+// of one 64-row group, for vocabularies up to 2^18 and up to kNaMaxBlocks
 // compute units) is a file-scope device array that each GPU holds until the
-// process ends.
+// process ends.  (The one-launch path is not used here: its barrier targets
+// come from a per-call count kept on the host, which a captured graph would
+// replay unchanged.)
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -106,7 +109,7 @@ tfe_status topk_noalloc(const void* w, int32_t vocab, int32_t dim, const void* h
   if ((uint32_t)d.lds < head_lds_bytes(dim))
     return fail(TFE_ERR_UNSUPPORTED, "dim %d needs %u bytes of LDS per block, device has %d", dim,
                 head_lds_bytes(dim), d.lds);
-  HeadArgs a;
+  HeadArgs a{};
   a.w = w;
   a.hidden = hidden;
   a.logits = (float*)d.ptr;

@@ -1,0 +1,136 @@
+"""The one-launch head (tfe_head_topk for at most 64 rows and K at most the
+number of compute units: logits held in registers, a bound of each row's
+K-th largest logit from the blocks' maxima, only the logits above it
+written) against the two-launch kernels (tfe_head_topk_noalloc, which
+writes every logit), on the same inputs: ids bit-exact and probabilities
+within 1e-5 relative (the two add the softmax denominator up in different
+orders).  The shapes take every branch of the selection: the usual few
+hundred candidates per row, K = 1 and K = 256, heavy ties (an all-zero
+projection makes every logit a candidate, more than LDS holds, so the
+selection first narrows in memory), the largest logits clustered in a few
+blocks, vocabularies smaller than one tile per block, and every width.
+Many calls in a row on one head, and calls of two heads interleaved on
+one stream, check that the grid barriers' counters stay aligned."""
+import numpy as np
+import pytest
+import torch
+
+import synth
+from paper_2607_07388_amd import tfe
+
+from . import harness as H
+
+pytestmark = pytest.mark.gpu
+
+
+def two_launch(w, V, D, h, B, K):
+    ids = torch.full((B, K), -7, dtype=torch.int32, device="cuda")
+    prob = torch.full((B, K), -1.0, dtype=torch.float32, device="cuda")
+    tfe.tfe_head_topk_noalloc(w, V, D, h, B, K, ids, prob, H.cur_stream())
+    torch.cuda.synchronize()
+    return ids.cpu().numpy(), prob.cpu().numpy()
+
+
+def one_launch(head, h, B, K):
+    ids = torch.full((B, K), -7, dtype=torch.int32, device="cuda")
+    prob = torch.full((B, K), -1.0, dtype=torch.float32, device="cuda")
+    tfe.tfe_head_topk(head, h, B, K, ids, prob, H.cur_stream())
+    torch.cuda.synchronize()
+    return ids.cpu().numpy(), prob.cpu().numpy()
+
+
+def gaussian(seed, V, D, B, scale=0.1):
+    w = torch.empty((V, D), dtype=torch.bfloat16, device="cuda")
+    synth.normal_fill_device(w.data_ptr(), 0, V, D, seed, 40, scale, synth.BF16, H.cur_stream())
+    h = H.to_device(synth.normal_range(seed, 41, 0, B, D, 1.0, synth.BF16), synth.BF16)
+    torch.cuda.synchronize()
+    return w, h
+
+
+def small_ints(seed, V, D, B, lo, hi):
+    rng = np.random.default_rng(seed)
+    w = rng.integers(lo, hi, (V, D)).astype(np.float32)
+    h = rng.integers(lo, hi, (B, D)).astype(np.float32)
+    bits = lambda x: (x.view(np.uint32) >> 16).astype(np.uint16)
+    return H.to_device(bits(w), synth.BF16), H.to_device(bits(h), synth.BF16)
+
+
+def check(w, h, V, D, B, K, calls=1):
+    print("# one launch vs two: V=%d D=%d B=%d K=%d" % (V, D, B, K), flush=True)
+    want_ids, want_prob = two_launch(w, V, D, h, B, K)
+    head = tfe.tfe_head_create(w, V, D, B, K)
+    try:
+        for _ in range(calls):
+            ids, prob = one_launch(head, h, B, K)
+            np.testing.assert_array_equal(ids, want_ids)
+            np.testing.assert_allclose(prob, want_prob, rtol=1e-5, atol=1e-37)
+    finally:
+        tfe.tfe_head_free(head)
+    assert np.all(want_ids >= 0) and np.all(want_ids < V)
+
+
+@pytest.mark.parametrize("V,D,B,K", [
+    (151936, 1024, 64, 128),   # the batch-64 decode step
+    (151936, 1024, 64, 1),
+    (151936, 1024, 64, 256),   # K = the number of blocks
+    (151936, 1024, 1, 64),
+    (151936, 1024, 13, 7),     # fewer groups than the 8 threads of a row
+    (40000, 512, 64, 100),
+    (3001, 256, 5, 17),        # ragged vocabulary
+    (300, 512, 17, 256),       # fewer tiles than blocks: empty blocks
+    (100, 1024, 64, 50),
+])
+def test_gaussian(V, D, B, K):
+    w, h = gaussian(V + K, V, D, B)
+    check(w, h, V, D, B, K)
+
+
+def test_all_logits_equal_narrows_in_memory():
+    V, D, B, K = 151936, 1024, 64, 128
+    w = torch.zeros((V, D), dtype=torch.bfloat16, device="cuda")
+    _, h = gaussian(3, 16, D, B)
+    check(w, h, V, D, B, K)
+
+
+def test_integer_ties():
+    V, D, B = 151936, 256, 64
+    w, h = small_ints(4, V, D, B, 0, 2)
+    check(w, h, V, D, B, 128)
+    w, h = small_ints(5, V, D, B, -2, 3)
+    check(w, h, V, D, B, 256)
+
+
+def test_largest_logits_clustered_in_a_few_blocks():
+    V, D, B, K = 151936, 1024, 64, 256
+    w, h = gaussian(6, V, D, B)
+    w[:2000] *= 10
+    check(w, h, V, D, B, K)
+
+
+def test_many_calls_and_two_heads_interleaved():
+    V, D, B, K = 151936, 1024, 64, 128
+    w1, h1 = gaussian(7, V, D, B)
+    w2, h2 = gaussian(8, V, D, B)
+    want1 = two_launch(w1, V, D, h1, B, K)
+    want2 = two_launch(w2, V, D, h2, B, K)
+    a = tfe.tfe_head_create(w1, V, D, B, K)
+    b = tfe.tfe_head_create(w2, V, D, B, K)
+    try:
+        for i in range(40):
+            for head, h, want in ((a, h1, want1), (b, h2, want2)) if i % 3 else ((b, h2, want2),):
+                ids, prob = one_launch(head, h, B, K)
+                np.testing.assert_array_equal(ids, want[0])
+                np.testing.assert_allclose(prob, want[1], rtol=1e-5, atol=1e-37)
+        # Back to back without synchronising in between.
+        outs = []
+        for _ in range(20):
+            ids = torch.empty((B, K), dtype=torch.int32, device="cuda")
+            prob = torch.empty((B, K), dtype=torch.float32, device="cuda")
+            tfe.tfe_head_topk(a, h1, B, K, ids, prob, H.cur_stream())
+            outs.append((ids, prob))
+        torch.cuda.synchronize()
+        for ids, prob in outs:
+            np.testing.assert_array_equal(ids.cpu().numpy(), want1[0])
+    finally:
+        tfe.tfe_head_free(a)
+        tfe.tfe_head_free(b)

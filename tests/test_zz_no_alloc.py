@@ -1,7 +1,9 @@
 """The no-allocation entry point tfe_head_topk_noalloc (for callers that
 cannot allocate) against tfe_head_topk on the same inputs: two calls in a
 row, the second smaller (fewer rows, a ragged vocabulary, another width),
-ids bit-exact and probabilities equal; sizes beyond its scratch are
+ids bit-exact and probabilities within 1e-5 relative (tfe_head_topk takes
+the one-launch path for these shapes, which adds the softmax denominator up
+per logits block instead of per tile); sizes beyond its scratch are
 refused."""
 import numpy as np
 import pytest
@@ -47,7 +49,7 @@ def test_noalloc_matches_head_topk_on_two_calls():
         want_ids, want_prob = reference(w, V, D, h, B, K)
         got_ids, got_prob = noalloc(w, V, D, h, B, K)
         np.testing.assert_array_equal(got_ids, want_ids)
-        np.testing.assert_array_equal(got_prob, want_prob)
+        np.testing.assert_allclose(got_prob, want_prob, rtol=1e-5, atol=0)
         assert np.all(got_ids >= 0) and np.all(got_ids < V)
 
 
