@@ -90,11 +90,11 @@ MULTI_SOURCES = ("paper_2607_07388_amd/csrc/tfe_multi.hip",
                  "paper_2607_07388_amd/csrc/tfe_index.h")
 
 # The same for one call of the early-exit head (W 151936 x 1024 bf16, 64 rows,
-# K = 128): k_head_logits + k_head_rows, from the passes in
-# profiles/k_head_logits_rows_v151936_d1024_b64_k128.md.
+# K = 128): the one-launch k_head_fused, from the passes in
+# profiles/k_head_fused_v151936_d1024_b64_k128.md.
 PROFILED_TRAFFIC_HEAD = {
-    "sources_sha256": "17623774cbebd67d0ee86b05db7addf13107105ce22724d75e633c81789ddde9",
-    "bytes_per_launch": 373928662,
+    "sources_sha256": "74991b9fe211efa3ffee51ceed6ecd42ccc0b1e37941892f9ac98924a0d1d2b5",
+    "bytes_per_launch": 318788051,
 }
 HEAD_SOURCES = ("paper_2607_07388_amd/csrc/tfe_head.hip",
                 "paper_2607_07388_amd/csrc/tfe_head.h",
@@ -772,7 +772,7 @@ def run_head(args):
                    "k": K},
         "roofline": {
             "bound": "hbm",
-            "kernel": "tfe_head_topk (k_head_logits + k_head_rows)",
+            "kernel": "tfe_head_topk (k_head_fused: one launch)",
             "achieved": nbytes / avg / 1e9,
             "peak": HBM_PEAK_GBPS,
             "unit": "GB/s",

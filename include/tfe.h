@@ -266,8 +266,8 @@ typedef struct tfe_head tfe_head; /* opaque; owned by the library */
  * 1 <= max_k <= min(256, vocab); 1 <= max_batch <= 65535 sizes the scratch
  * (max_batch x vocab float32 logits plus candidate lists, and the one-launch
  * path's per-block maxima and candidate segments: 64 rows x compute units x
- * (16 x ceil(vocab / (16 x compute units)) + 1) keys, about 80 MB for the
- * 151936-token vocabulary on 256 compute units). */
+ * (16 x ceil(vocab / (16 x compute units)) + 1) keys, rounded up to 16,
+ * about 80 MB for the 151936-token vocabulary on 256 compute units). */
 tfe_status tfe_head_create(const void *w_pref, int32_t vocab, int32_t dim, int32_t max_batch,
                            int32_t max_k, tfe_head **out);
 
@@ -279,8 +279,9 @@ tfe_status tfe_head_create(const void *w_pref, int32_t vocab, int32_t dim, int32
  * 0 <= B <= max_batch, 0 <= K <= max_k; stream-ordered on `stream`.  Calls
  * on one head share its scratch: they must be ordered (same stream, or
  * synchronised).
- * Calls of at most 64 rows with K at most the number of compute units (and
- * at most 48 16-token tiles per compute unit) take a one-launch path,
+ * Calls of at most 64 rows with K at most the number of compute units (a
+ * power of two up to 256; at most 48 16-token tiles per compute unit)
+ * take a one-launch path,
  * except under stream capture: one block per compute unit keeps its logits
  * in registers, and two device-wide barriers inside the launch replace the
  * write of the logits.  Its blocks must all be resident at once, so such a

@@ -46,7 +46,8 @@ hipError_t launch_head_logits(const HeadArgs& a, hipStream_t s);
 hipError_t launch_head_rows(const HeadArgs& a, hipStream_t s);
 
 // The one-launch head: true if a call of this shape can take it (B <= 64,
-// B and K at most nblk <= 256, at most 48 tiles per block).
+// B and K at most nblk, nblk a power of two <= 256, at most 48 tiles per
+// block).
 bool head_fused_fits(const HeadArgs& a);
 // Words per (row, block) segment of the candidate scratch for this vocabulary.
 uint32_t head_fused_ccap(uint32_t V, uint32_t nblk);

@@ -712,16 +712,19 @@ __global__ __launch_bounds__(kRowThreads) void k_head_rows(const HeadArgs a) {
 // of them.  Here each wave keeps the logits of its tile groups (at most two)
 // in registers, and two grid barriers take the place of that write:
 //   A. the logits as in k_head_logits (one block per compute unit, the same
-//      tiles); after each tile group the wave folds its logits into a
+//      tiles; claiming the second tile groups device-wide instead, first
+//      come first served, made the call slower, 93.2 against 73.4 us: the
+//      compute units that finish early take too many); after each tile
+//      group the wave folds its logits into a
 //      running per-row maximum and sum of exp(logit - maximum), which hides
 //      that arithmetic under the other waves' loads; each block publishes
 //      per row its largest logit (as a key) and its sum;
 //   B. after the first barrier every block derives, per row, a lower bound
-//      of the row's K-th largest logit: split the blocks' maxima into K
+//      of the row's K-th largest logit: split the blocks into G >= K
 //      disjoint non-empty groups; each group holds a logit at least as
-//      large as the smallest of the K group maxima, and these K logits are
-//      distinct entries of the row, so the K-th largest logit reaches that
-//      minimum;
+//      large as the smallest of the G group maxima, and these G logits are
+//      distinct entries of the row, so the G-th largest logit, and with it
+//      the K-th, reaches that minimum;
 //   C. each block writes the (logit, id) keys of its logits at or above the
 //      bound (a few per row) to its own segment of the row's candidate list;
 //   D. after the second barrier block r ranks row r: M and S from the
@@ -977,50 +980,47 @@ __global__ __launch_bounds__(kFuseThreads) void k_head_fused(const HeadArgs a) {
   }
   grid_barrier(a, 1, true);
 
-  // B. Per row, the smallest of K group maxima (high key words; 0 for a
-  // block without logits).  A block that ranks a row in phase D also loads
-  // that row's block maxima and sums here, for M and S.  Thread (row tid / 8, j = tid % 8) holds the cj
-  // blocks j, j + 8, j + 16, ... and forms gj of the K groups as runs of
-  // consecutive ones (gj <= cj, since K <= nblk); blocks of a thread
-  // without groups (K < 8) stay out.
+  // B. Per row, the smallest of G group maxima (high key words; 0 for a
+  // block without logits), G the least power of two >= K (G >= K groups
+  // bound the G-th largest logit, which is at most the K-th): groups of
+  // nblk / G consecutive blocks, nblk a power of two.  Wave w takes rows
+  // 8 w .. 8 w + 7; lane l loads blocks 4 l .. 4 l + 3 of a row with one
+  // 16-byte load.  A block that ranks a row in phase D also loads that
+  // row's block maxima and sums here, for M and S.
   uint32_t fbh = 0;
   float fbs = 0.f;
   {
-    const uint32_t row = (uint32_t)tid >> 3, j = (uint32_t)tid & 7u;
-    const uint32_t cj = nblk / 8 + (j < nblk % 8 ? 1u : 0u);
-    const uint32_t gj = K / 8 + (j < K % 8 ? 1u : 0u);
-    const uint32_t* bh = a.bhi + (size_t)row * nblk + j;
-    uint32_t v[kFuseMaxBlocks / 8];
+    uint32_t G = 1;
+    while (G < K) G <<= 1;
+    const uint32_t sg = nblk / G;  // blocks per group, a power of two
+    const bool mine = 4u * (uint32_t)lane < nblk;
+    u32x4 v[8];
 #pragma unroll
-    for (uint32_t s = 0; s < kFuseMaxBlocks / 8; ++s)
-      v[s] = row < B && s < cj ? ld_agent(bh + 8 * s) : 0u;
+    for (int q = 0; q < 8; ++q) {
+      const uint32_t row = (uint32_t)wave * 8 + q;
+      v[q] = u32x4{0u, 0u, 0u, 0u};
+      if (row < B && mine) v[q] = ld_agent16(a.bhi, (row * nblk + 4u * (uint32_t)lane) * 4u);
+    }
     if (b < B && (uint32_t)tid < nblk) {
       fbh = ld_agent(a.bhi + (size_t)b * nblk + tid);
       fbs = __uint_as_float(ld_agent(a.bsum + (size_t)b * nblk + tid));
     }
-    uint32_t lo = 0xFFFFFFFFu;
-    if (gj) {
-      // Block s is in run floor(s gj / cj): a new run starts where s gj
-      // reaches the next multiple of cj.
-      uint32_t run = 0, acc_s = 0, next = cj;
 #pragma unroll
-      for (uint32_t s = 0; s < kFuseMaxBlocks / 8; ++s) {
-        if (s < cj) {
-          if (acc_s >= next) {
-            lo = min(lo, run);
-            run = 0;
-            next += cj;
-          }
-          run = max(run, v[s]);
-          acc_s += gj;
-        }
+    for (int q = 0; q < 8; ++q) {
+      const u32x4 x = v[q];
+      const uint32_t a0 = max(x[0], x[1]), a1 = max(x[2], x[3]);
+      uint32_t m;
+      if (sg == 1) {
+        m = min(min(x[0], x[1]), min(x[2], x[3]));
+      } else if (sg == 2) {
+        m = min(a0, a1);
+      } else {  // a group spans sg / 4 aligned lanes
+        m = max(a0, a1);
+        for (uint32_t o = 1; o < sg / 4; o <<= 1) m = max(m, (uint32_t)__shfl_xor((int)m, (int)o));
       }
-      lo = min(lo, run);
+      m = ~wave_max_u32(mine ? ~m : 0u);
+      if (lane == 0) s_bound[wave * 8 + q] = m;
     }
-    lo = min(lo, (uint32_t)__shfl_xor((int)lo, 1, 8));
-    lo = min(lo, (uint32_t)__shfl_xor((int)lo, 2, 8));
-    lo = min(lo, (uint32_t)__shfl_xor((int)lo, 4, 8));
-    if (j == 0) s_bound[row] = lo;
     const uint32_t wm = wave_max_u32(fbh);
     if (lane == 0) s_wmax[wave] = wm;
   }
@@ -1267,7 +1267,8 @@ uint32_t head_fused_ccap(uint32_t V, uint32_t nblk) {
 
 bool head_fused_fits(const HeadArgs& a) {
   if (!head_dim_supported((int)a.D) || a.B < 1 || a.B > (uint32_t)kCols || a.B > a.nblk ||
-      a.nblk > kFuseMaxBlocks || a.K < 1 || a.K > a.nblk || a.K > (uint32_t)kHeadMaxK)
+      a.nblk > kFuseMaxBlocks || (a.nblk & (a.nblk - 1)) != 0 || a.K < 1 || a.K > a.nblk ||
+      a.K > (uint32_t)kHeadMaxK)
     return false;
   // Tile groups per block within what the waves hold.
   const uint32_t tiles = ((a.V + 15) / 16 + a.nblk - 1) / a.nblk;
