@@ -993,6 +993,7 @@ __global__ __launch_bounds__(kFuseThreads) void k_head_fused(const HeadArgs a) {
     uint32_t G = 1;
     while (G < K) G <<= 1;
     const uint32_t sg = nblk / G;  // blocks per group, a power of two
+    const uint32_t om = (4u * K + nblk - 1u) / nblk;
     const bool mine = 4u * (uint32_t)lane < nblk;
     u32x4 v[8];
 #pragma unroll
@@ -1019,6 +1020,18 @@ __global__ __launch_bounds__(kFuseThreads) void k_head_fused(const HeadArgs a) {
         for (uint32_t o = 1; o < sg / 4; o <<= 1) m = max(m, (uint32_t)__shfl_xor((int)m, (int)o));
       }
       m = ~wave_max_u32(mine ? ~m : 0u);
+      // A second bound, the larger one is kept: blocks in groups of four
+      // (one lane); the om largest maxima of a group, om = ceil(4 K / nblk)
+      // <= 4, are distinct logits of the row, (nblk / 4) om >= K of them,
+      // each at least the group's om-th largest.  (Groups of eight, with a
+      // sort across lane pairs, halved the candidates again but cost as
+      // much in this step as they saved later.)
+      if (om == 2u || om == 3u) {
+        const uint32_t lo0 = min(x[0], x[1]), lo1 = min(x[2], x[3]);
+        const uint32_t ms = om == 2u ? max(min(a0, a1), max(lo0, lo1))   // second largest
+                                     : min(max(lo0, lo1), min(a0, a1));  // third largest
+        m = max(m, ~wave_max_u32(mine ? ~ms : 0u));
+      }
       if (lane == 0) s_bound[wave * 8 + q] = m;
     }
     const uint32_t wm = wave_max_u32(fbh);
