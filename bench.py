@@ -93,8 +93,8 @@ MULTI_SOURCES = ("paper_2607_07388_amd/csrc/tfe_multi.hip",
 # K = 128): the one-launch k_head_fused, from the passes in
 # profiles/k_head_fused_v151936_d1024_b64_k128.md.
 PROFILED_TRAFFIC_HEAD = {
-    "sources_sha256": "9aa8e9eb28a5043a0f185cebca348ecace35f93d81cdf258c7a23abd85c59120",
-    "bytes_per_launch": 318454326,
+    "sources_sha256": "09a44c01ed640c3d6a982d8cc2a8e651cb45bd14e27789612c38ec5c42d30f8a",
+    "bytes_per_launch": 318447789,
 }
 HEAD_SOURCES = ("paper_2607_07388_amd/csrc/tfe_head.hip",
                 "paper_2607_07388_amd/csrc/tfe_head.h",

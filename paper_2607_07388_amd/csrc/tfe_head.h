@@ -32,9 +32,9 @@ struct HeadArgs {
   uint32_t* bsum;       // [64 x nblk], float bits
   uint64_t* cand;       // [64 x nblk x ccap]
   unsigned long long* bar;
-  uint32_t* fault;
+  unsigned long long* fault;  // the last faulted call's epoch + 1
   uint32_t ccap;        // 1 + 16 x the most tiles a block owns, rounded up to 16
-  uint32_t epoch;       // one-launch calls made before this one on this scratch
+  uint64_t epoch;       // one-launch calls made before this one on this scratch
 };
 
 // True if D has a logits kernel.

@@ -800,7 +800,7 @@ __device__ __forceinline__ void grid_barrier(const HeadArgs& a, uint32_t j, bool
       const unsigned long long* f = flag + kBarLine * grp;
       for (uint32_t n = 0; ld_agent(f) < phase; ++n) {
         if (n == kGridWaitLimit) {
-          atomicMax(a.fault, a.epoch + 1u);
+          atomicMax(a.fault, (unsigned long long)a.epoch + 1ull);
           break;
         }
         __builtin_amdgcn_s_sleep(1);
@@ -1094,7 +1094,7 @@ __global__ __launch_bounds__(kFuseThreads) void k_head_fused(const HeadArgs a) {
 
   // D. Row b.
   const uint32_t row = b;
-  if (ld_agent((const uint32_t*)a.fault) == a.epoch + 1u) {
+  if (ld_agent((const unsigned long long*)a.fault) == (unsigned long long)a.epoch + 1ull) {
     for (uint32_t i = tid; i < K; i += kFuseThreads) {
       a.top_ids[(size_t)row * K + i] = -1;
       a.top_prob[(size_t)row * K + i] = 0.f;

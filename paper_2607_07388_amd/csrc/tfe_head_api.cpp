@@ -27,7 +27,7 @@ struct tfe_head {
   unsigned char* d_fuse = nullptr;
   bool fused = false;
   uint32_t ccap = 0;
-  uint32_t epoch = 0;  // one-launch calls enqueued so far (barrier targets)
+  uint64_t epoch = 0;  // one-launch calls enqueued so far (barrier targets)
   // Recorded after every top-K call made outside graph capture; freeing the
   // head waits for it (and for nothing else on the device).
   hipEvent_t ev_last = nullptr;
@@ -75,7 +75,7 @@ void fuse_args(const tfe_head* h, HeadArgs* a) {
   unsigned char* p = h->d_fuse;
   const size_t n = fuse_words((uint32_t)h->cus);
   a->bar = (unsigned long long*)p;
-  a->fault = (uint32_t*)(p + kFuseCtl - 128);
+  a->fault = (unsigned long long*)(p + kFuseCtl - 128);
   a->bhi = (uint32_t*)(p + kFuseCtl);
   a->bsum = a->bhi + n;
   a->cand = (uint64_t*)(p + fuse_cand_at((uint32_t)h->cus));
