@@ -35,7 +35,13 @@ struct HeadArgs {
   unsigned long long* fault;  // the last faulted call's epoch + 1
   uint32_t ccap;        // 1 + 16 x the most tiles a block owns, rounded up to 16
   uint64_t epoch;       // one-launch calls made before this one on this scratch
+  uint32_t wait_limit;  // polls before a barrier wait gives up (kHeadWaitLimit)
 };
+
+// Polls of a one-launch barrier before it gives up (about a second).  The
+// environment variable TFE_HEAD_WAIT_LIMIT overrides it per call, so that
+// tests can force the give-up path from the host.
+constexpr uint32_t kHeadWaitLimit = 1u << 20;
 
 // True if D has a logits kernel.
 bool head_dim_supported(int D);

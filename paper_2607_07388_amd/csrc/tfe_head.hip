@@ -746,7 +746,6 @@ __global__ __launch_bounds__(kRowThreads) void k_head_rows(const HeadArgs a) {
 constexpr int kFuseThreads = kLogitWaves * 64;
 constexpr int kFuseGroups = 2;      // tile groups a wave computes and holds
 constexpr uint32_t kFuseMaxBlocks = 256;
-constexpr uint32_t kGridWaitLimit = 1u << 20;
 
 template <typename T>
 __device__ __forceinline__ void st_agent(T* p, T v) {
@@ -799,7 +798,7 @@ __device__ __forceinline__ void grid_barrier(const HeadArgs& a, uint32_t j, bool
     if (wait) {
       const unsigned long long* f = flag + kBarLine * grp;
       for (uint32_t n = 0; ld_agent(f) < phase; ++n) {
-        if (n == kGridWaitLimit) {
+        if (n == a.wait_limit) {
           atomicMax(a.fault, (unsigned long long)a.epoch + 1ull);
           break;
         }

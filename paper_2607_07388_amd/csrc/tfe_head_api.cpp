@@ -1,6 +1,7 @@
 // C ABI of the early-exit prefetch head: create / top-K / free.
 #include <hip/hip_runtime_api.h>
 #include <stdint.h>
+#include <stdlib.h>
 
 #include <new>
 
@@ -206,6 +207,8 @@ tfe_status topk(tfe_head* h, const void* hidden, int32_t B, int32_t K, int32_t* 
   if (h->fused && cs == hipStreamCaptureStatusNone && head_fused_fits(a)) {
     fuse_args(h, &a);
     a.epoch = h->epoch;
+    a.wait_limit = kHeadWaitLimit;
+    if (const char* wl = getenv("TFE_HEAD_WAIT_LIMIT")) a.wait_limit = (uint32_t)strtoul(wl, nullptr, 0);
     HEAD_HIP(launch_head_fused(a, stream), "head launch");
     ++h->epoch;
   } else {

@@ -10,7 +10,9 @@ projection makes every logit a candidate, more than LDS holds, so the
 selection first narrows in memory), the largest logits clustered in a few
 blocks, vocabularies smaller than one tile per block, and every width.
 Many calls in a row on one head, and calls of two heads interleaved on
-one stream, check that the grid barriers' counters stay aligned."""
+one stream, check that the grid barriers' counters stay aligned; a call
+whose barrier waits are forced to give up (TFE_HEAD_WAIT_LIMIT=0) answers
+-1 and leaves the head working."""
 import numpy as np
 import pytest
 import torch
@@ -134,3 +136,28 @@ def test_many_calls_and_two_heads_interleaved():
     finally:
         tfe.tfe_head_free(a)
         tfe.tfe_head_free(b)
+
+
+def test_a_barrier_wait_that_gives_up_fails_only_its_call(monkeypatch):
+    """The one-launch barriers' waits are bounded; TFE_HEAD_WAIT_LIMIT=0
+    makes every wait give up at once (forced from the host: every block
+    still arrives, so no kernel waits forever).  That call answers every row
+    with id -1 and probability 0; the next call on the same head, with the
+    default limit, is correct again (the barrier counters stayed aligned)."""
+    V, D, B, K = 40000, 1024, 64, 64
+    w, h = gaussian(11, V, D, B)
+    want = two_launch(w, V, D, h, B, K)
+    head = tfe.tfe_head_create(w, V, D, B, K)
+    try:
+        ids, prob = one_launch(head, h, B, K)
+        np.testing.assert_array_equal(ids, want[0])
+        monkeypatch.setenv("TFE_HEAD_WAIT_LIMIT", "0")
+        ids, prob = one_launch(head, h, B, K)
+        assert np.all(ids == -1) and np.all(prob == 0)
+        monkeypatch.delenv("TFE_HEAD_WAIT_LIMIT")
+        for _ in range(3):
+            ids, prob = one_launch(head, h, B, K)
+            np.testing.assert_array_equal(ids, want[0])
+            np.testing.assert_allclose(prob, want[1], rtol=1e-5, atol=1e-37)
+    finally:
+        tfe.tfe_head_free(head)
