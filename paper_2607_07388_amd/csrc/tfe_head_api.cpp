@@ -3,6 +3,7 @@
 #include <stdint.h>
 #include <stdlib.h>
 
+#include <mutex>
 #include <new>
 
 #include "../../include/tfe.h"
@@ -48,12 +49,15 @@ tfe_status hip_fail(hipError_t e, const char* what) {
     if (e_ != hipSuccess) return hip_fail(e_, what); \
   } while (0)
 
+void forget_fused(const tfe_head* h);
+
 void release(tfe_head* h) {
   if (!h) return;
   int cur = 0;
   (void)hipGetDevice(&cur);
   (void)hipSetDevice(h->device);
   if (h->recorded) (void)hipEventSynchronize(h->ev_last);
+  forget_fused(h);
   void* bufs[] = {h->d_logits, h->d_tkey, h->d_tsum, h->d_bmax, h->d_fuse};
   for (void* b : bufs) dev_free(b);
   if (h->ev_last) (void)hipEventDestroy(h->ev_last);
@@ -62,6 +66,42 @@ void release(tfe_head* h) {
 }
 
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+// One-launch calls of all heads on a device run one after another: a call
+// on another stream than the previous one waits on the device for that
+// call's event (the head's ev_last, recorded right after each call).  Two of
+// them side by side could each hold part of the compute units with blocks
+// waiting at a grid barrier for blocks of their own that cannot start.
+// Calls on the stream of the previous one are ordered by the stream itself
+// and add nothing.  The stream handle is only compared, never used.
+constexpr int kOrderDevices = 64;
+std::mutex g_fused_mu;
+const tfe_head* g_fused_head[kOrderDevices];
+hipStream_t g_fused_stream[kOrderDevices];
+
+// A head that is released stops being the previous call's head (release
+// has waited for its last call).
+void forget_fused(const tfe_head* h) {
+  std::lock_guard<std::mutex> lock(g_fused_mu);
+  if (h->device >= 0 && h->device < kOrderDevices && g_fused_head[h->device] == h)
+    g_fused_head[h->device] = nullptr;
+}
+
+// Enqueues launch() on `stream` behind the previous one-launch call on the
+// device, then records h->ev_last behind it.
+template <class F>
+tfe_status fused_in_order(tfe_head* h, hipStream_t stream, F launch) {
+  std::lock_guard<std::mutex> lock(g_fused_mu);
+  const tfe_head* prev = g_fused_head[h->device];
+  if (prev && g_fused_stream[h->device] != stream)
+    HEAD_HIP(hipStreamWaitEvent(stream, prev->ev_last, 0), "head ordering wait");
+  HEAD_HIP(launch(), "head launch");
+  HEAD_HIP(hipEventRecord(h->ev_last, stream), "record");
+  h->recorded = true;
+  g_fused_head[h->device] = h;
+  g_fused_stream[h->device] = stream;
+  return TFE_OK;
+}
 
 // Layout of the one-launch scratch for nblk blocks: 8 KB of barrier
 // counters and flags (one 128-byte line each) and the fault word, two
@@ -204,17 +244,21 @@ tfe_status topk(tfe_head* h, const void* hidden, int32_t B, int32_t K, int32_t* 
   a.nblk = (uint32_t)h->cus;
   hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
   HEAD_HIP(hipStreamIsCapturing(stream, &cs), "hipStreamIsCapturing");
-  if (h->fused && cs == hipStreamCaptureStatusNone && head_fused_fits(a)) {
+  if (h->fused && cs == hipStreamCaptureStatusNone && head_fused_fits(a) &&
+      h->device < kOrderDevices) {
     fuse_args(h, &a);
     a.epoch = h->epoch;
     a.wait_limit = kHeadWaitLimit;
     if (const char* wl = getenv("TFE_HEAD_WAIT_LIMIT")) a.wait_limit = (uint32_t)strtoul(wl, nullptr, 0);
-    HEAD_HIP(launch_head_fused(a, stream), "head launch");
-    ++h->epoch;
-  } else {
-    HEAD_HIP(launch_head_logits(a, stream), "head logits launch");
-    HEAD_HIP(launch_head_rows(a, stream), "head top-K launch");
+    // The epoch counts launched calls (the barrier targets), whatever follows.
+    return fused_in_order(h, stream, [&] {
+      const hipError_t e = launch_head_fused(a, stream);
+      if (e == hipSuccess) ++h->epoch;
+      return e;
+    });
   }
+  HEAD_HIP(launch_head_logits(a, stream), "head logits launch");
+  HEAD_HIP(launch_head_rows(a, stream), "head top-K launch");
   if (cs == hipStreamCaptureStatusNone) {
     HEAD_HIP(hipEventRecord(h->ev_last, stream), "record");
     h->recorded = true;

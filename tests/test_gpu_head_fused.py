@@ -10,7 +10,9 @@ projection makes every logit a candidate, more than LDS holds, so the
 selection first narrows in memory), the largest logits clustered in a few
 blocks, vocabularies smaller than one tile per block, and every width.
 Many calls in a row on one head, and calls of two heads interleaved on
-one stream, check that the grid barriers' counters stay aligned; a call
+one stream, check that the grid barriers' counters stay aligned; calls of
+two heads on two streams without synchronisation run one after another; a
+call
 whose barrier waits are forced to give up (TFE_HEAD_WAIT_LIMIT=0) answers
 -1 and leaves the head working."""
 import numpy as np
@@ -133,6 +135,38 @@ def test_many_calls_and_two_heads_interleaved():
         torch.cuda.synchronize()
         for ids, prob in outs:
             np.testing.assert_array_equal(ids.cpu().numpy(), want1[0])
+    finally:
+        tfe.tfe_head_free(a)
+        tfe.tfe_head_free(b)
+
+
+def test_two_heads_on_two_streams_without_sync():
+    """One-launch calls of two heads on two streams, issued alternately with
+    no synchronisation in between: the library runs them one after another
+    on the device (side by side, each could hold compute units with blocks
+    waiting at a barrier for blocks of its own that cannot start, until the
+    bounded waits give up).  Every call matches the two-launch kernels."""
+    V, D, B, K = 151936, 1024, 64, 128
+    print("# two heads, two streams: V=%d D=%d B=%d K=%d" % (V, D, B, K), flush=True)
+    w1, h1 = gaussian(12, V, D, B)
+    w2, h2 = gaussian(13, V, D, B)
+    want1 = two_launch(w1, V, D, h1, B, K)
+    want2 = two_launch(w2, V, D, h2, B, K)
+    a = tfe.tfe_head_create(w1, V, D, B, K)
+    b = tfe.tfe_head_create(w2, V, D, B, K)
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    try:
+        outs = []
+        for _ in range(16):
+            for head, h, st, want in ((a, h1, s1, want1), (b, h2, s2, want2)):
+                ids = torch.empty((B, K), dtype=torch.int32, device="cuda")
+                prob = torch.empty((B, K), dtype=torch.float32, device="cuda")
+                tfe.tfe_head_topk(head, h, B, K, ids, prob, st)
+                outs.append((ids, prob, want))
+        torch.cuda.synchronize()
+        for ids, prob, want in outs:
+            np.testing.assert_array_equal(ids.cpu().numpy(), want[0])
+            np.testing.assert_allclose(prob.cpu().numpy(), want[1], rtol=1e-5, atol=1e-37)
     finally:
         tfe.tfe_head_free(a)
         tfe.tfe_head_free(b)
