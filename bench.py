@@ -93,8 +93,8 @@ MULTI_SOURCES = ("paper_2607_07388_amd/csrc/tfe_multi.hip",
 # K = 128): the one-launch k_head_fused, from the passes in
 # profiles/k_head_fused_v151936_d1024_b64_k128.md.
 PROFILED_TRAFFIC_HEAD = {
-    "sources_sha256": "70f6f2a952f49f8ea870e337d8e2d57cad069b18eb6912fa0af8a4528c527b3e",
-    "bytes_per_launch": 318412834,
+    "sources_sha256": "be789c228281e6d7aa42a8767167bd341ff168fa11757e004ae26ebd3f124ec8",
+    "bytes_per_launch": 318404965,
 }
 HEAD_SOURCES = ("paper_2607_07388_amd/csrc/tfe_head.hip",
                 "paper_2607_07388_amd/csrc/tfe_head.h",
