@@ -438,3 +438,93 @@ def test_decode_and_prefetch_overlapping_without_sync(w2, scored):
     check_stats(tier, model)
     check_residency(tier, model, table.n_phrases)
     tier.close()
+
+
+@pytest.mark.parametrize("fill", [tfe.TFE_FILL_INLINE, tfe.TFE_FILL_SIDE_STREAM])
+def test_random_interleavings_of_every_call_kind(w2, fill):
+    """A seeded random sequence of 400 calls on one tiered table: decode
+    lookups (64 positions, one launch) and long lookups (65 to 6000
+    positions, several kernels) on two streams; plain and scored prefetches
+    of at most 4096 candidates (one block) and of more (several kernels) on
+    any of three streams, scored ones with random budgets; now and then a
+    device synchronisation or a statistics read.  Every input and output
+    buffer is made first; the calls are then enqueued with no other
+    synchronisation.  Calls on one table take effect in the order they are
+    enqueued, whatever their streams, so every lookup's output equals the
+    resident table's byte for byte, and the statistics (at every read and at
+    the end) and the residency of every row equal the policy model fed the
+    same calls in that order.  A 4096-row cache keeps victims and
+    recency-ring compactions frequent."""
+    table, res, ot = w2
+    C, pre, B = 4096, 2048, 64
+    print("# random interleavings, fill mode %d" % fill, flush=True)
+    rng = np.random.default_rng(4242 + fill)
+    kinds = ["decode", "long", "pf", "pf_big", "scored", "scored_big", "sync", "stats"]
+    weights = np.array([30, 12, 14, 5, 14, 5, 6, 4], np.float64)
+    plan = []
+    for i in range(400):
+        kind = kinds[rng.choice(len(kinds), p=weights / weights.sum())]
+        c = {"kind": kind, "stream": int(rng.integers(0, 3))}
+        if kind in ("decode", "long"):
+            T = 64 if kind == "decode" else int(rng.integers(65, 6001))
+            seq = synth.zipf_tokens(51, 100 + i, T + 2, 1.1)
+            win = np.stack([seq[0:T], seq[1:T + 1], seq[2:T + 2]], axis=1).astype(np.int32)
+            c.update(T=T, win=win, stream=int(rng.integers(0, 2)),
+                     tok=torch.from_numpy(win).cuda(),
+                     hid=H.to_device(synth.normal_range(52, i, 0, T, 1024, 1.0, synth.BF16),
+                                     synth.BF16),
+                     out=H.Outputs(T, 1024, synth.BF16))
+        elif kind not in ("sync", "stats"):
+            K = int(rng.integers(1, 65)) if kind in ("pf", "scored") else int(rng.integers(65, 129))
+            tail = synth.zipf_tokens(53, 100 + i, B * 2, 1.1).reshape(B, 2)
+            cand = synth.zipf_tokens(54, 100 + i, B * K, 1.1).reshape(B, K)
+            c.update(K=K, tail=tail, cand=cand,
+                     tail_d=torch.from_numpy(np.ascontiguousarray(tail)).cuda(),
+                     cand_d=torch.from_numpy(np.ascontiguousarray(cand)).cuda())
+            if kind.startswith("scored"):
+                c["prob"] = rng.dirichlet(np.ones(K) * 0.5, B).astype(np.float32)
+                c["prob_d"] = torch.from_numpy(c["prob"]).cuda()
+                c["budget"] = int(rng.integers(8, 1025))
+        plan.append(c)
+    tier = TieredTable(table, C, pre, fill=fill)
+    model = LruModel(C, pre, 2048, fill_rereads=fill == tfe.TFE_FILL_SIDE_STREAM)
+    streams = [torch.cuda.current_stream(), torch.cuda.Stream(), torch.cuda.Stream()]
+    torch.cuda.synchronize()
+    for c in plan:
+        kind, st = c["kind"], streams[c["stream"]]
+        if kind == "sync":
+            torch.cuda.synchronize()
+        elif kind == "stats":
+            check_stats(tier, model)
+        elif kind in ("decode", "long"):
+            o, T = c["out"], c["T"]
+            tfe.tfe_lookup_inject(tier.handle, c["tok"], T, 2, 1, c["hid"], o.out, o.hit, o.slot,
+                                  o.len, tfe.TFE_GATE_SIGMOID, 1.0, st)
+            _, row, _ = ot.lookup(c["win"], 2, 1)
+            model.lookup([int(r) for r in row])
+        else:
+            K = c["K"]
+            win = np.concatenate([np.repeat(c["tail"], K, axis=0), c["cand"].reshape(-1, 1)],
+                                 axis=1)
+            _, crow, clen = ot.lookup(np.ascontiguousarray(win, np.int32), 2, 1)
+            if kind.startswith("scored"):
+                tfe.tfe_prefetch_scored(tier.handle, c["tail_d"], 2, c["cand_d"], c["prob_d"], B,
+                                        K, c["budget"], st)
+                model.prefetch_scored([int(r) for r in crow], [int(x) for x in clen],
+                                      c["prob"].reshape(-1), c["budget"])
+            else:
+                tfe.tfe_prefetch(tier.handle, c["tail_d"], 2, c["cand_d"], B, K, st)
+                model.prefetch([int(r) for r in crow])
+    torch.cuda.synchronize()
+    for c in plan:
+        if c["kind"] not in ("decode", "long"):
+            continue
+        o, T = c["out"], c["T"]
+        o_res = H.Outputs(T, 1024, synth.BF16)
+        H.run(res, c["tok"], T, 2, 1, c["hid"], o_res)
+        torch.cuda.synchronize()
+        assert torch.equal(o_res.slot, o.slot) and torch.equal(o_res.hit, o.hit)
+        assert torch.equal(o_res.out.view(torch.int16), o.out.view(torch.int16))
+    check_stats(tier, model)
+    check_residency(tier, model, table.n_phrases)
+    tier.close()
