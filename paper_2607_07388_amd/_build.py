@@ -35,7 +35,7 @@ def build(verbose=False):
         if verbose and out.strip():
             print(out)
         objs.append(obj)
-    # -z defs: a symbol left undefined fails the link here, not the load on the GPU machine.
+    # -z defs: a symbol left undefined fails the link here, not the library load at run time.
     cmd = ["hipcc", "--offload-arch=gfx950", "-shared", "-fPIC", "-pthread", "-Wl,-z,defs",
            "-o", SO + ".tmp"] + objs
     r = subprocess.run(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True)
