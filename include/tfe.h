@@ -281,14 +281,15 @@ tfe_status tfe_head_create(const void *w_pref, int32_t vocab, int32_t dim, int32
  * synchronised).
  * Calls of at most 64 rows with K at most the number of compute units (a
  * power of two up to 256; at most 48 16-token tiles per compute unit)
- * take a one-launch path,
- * except under stream capture: one block per compute unit keeps its logits
- * in registers, and two device-wide barriers inside the launch replace the
- * write of the logits.  Its blocks must all be resident at once: the
- * library runs the one-launch calls of all heads on a device one after
- * another (each waits on the device for the previous one, whatever its
- * stream), and such a call must not overlap on the device with other work
- * that holds compute units while waiting for it.  Its waits are bounded
+ * take a one-launch path, also under stream capture: one block per
+ * compute unit keeps its logits in registers, and two device-wide barriers
+ * inside the launch replace the write of the logits.  Its blocks must all
+ * be resident at once: the library runs the one-launch calls of all heads
+ * on a device one after another (each waits on the device for the previous
+ * one, whatever its stream; in a captured graph the graph's own order
+ * applies, so two such calls must not sit on parallel branches), and such
+ * a call must not overlap on the device with other work that holds compute
+ * units while waiting for it.  Its waits are bounded
  * (about a second); if one runs out,
  * that call's top_ids are all -1 and its top_prob 0.  Other calls take two
  * launches (logits, then the per-row selection), which have no such

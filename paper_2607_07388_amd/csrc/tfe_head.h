@@ -34,7 +34,8 @@ struct HeadArgs {
   unsigned long long* bar;
   unsigned long long* fault;  // the last faulted call's epoch + 1
   uint32_t ccap;        // 1 + 16 x the most tiles a block owns, rounded up to 16
-  uint64_t epoch;       // one-launch calls made before this one on this scratch
+  unsigned long long* ectl;  // [16 i], i < 16: blocks of earlier one-launch calls
+                             // on this scratch that have left (block b adds to b mod 16)
   uint32_t wait_limit;  // polls before a barrier wait gives up (kHeadWaitLimit)
 };
 

@@ -762,6 +762,28 @@ __device__ __forceinline__ u32x4 ld_agent16(const void* base, uint32_t off) {
   return __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 16);
 }
 
+// The call's epoch (one-launch calls made before it on this scratch) lives
+// in device memory, so that a captured graph replays correctly: every block
+// adds one to counter b mod 16 of ectl (each in a 128-byte line of its own)
+// as it leaves, without waiting for the result, and the next call -- which
+// starts only once this one has ended, its additions included -- takes the
+// sum of the counters over the number of blocks as its epoch.
+constexpr uint32_t kLeaveCtrs = 16;
+
+__device__ __forceinline__ uint64_t call_epoch(const HeadArgs& a) {
+  unsigned long long n = 0;
+#pragma unroll
+  for (uint32_t i = 0; i < kLeaveCtrs; ++i)
+    n += __hip_atomic_load(a.ectl + 16 * i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  return n / a.nblk;
+}
+
+__device__ __forceinline__ void leave_call(const HeadArgs& a) {
+  if (threadIdx.x == 0)
+    (void)__hip_atomic_fetch_add(a.ectl + 16 * (blockIdx.x % kLeaveCtrs), 1ull, __ATOMIC_RELAXED,
+                                 __HIP_MEMORY_SCOPE_AGENT);
+}
+
 // Barrier j (1 or 2) of the call with epoch e, called by every thread, as a
 // two-level tree: block b counts into the counter of its group b % 16 (each
 // counter in a 128-byte line of its own), the last block of a group into the
@@ -776,14 +798,15 @@ __device__ __forceinline__ u32x4 ld_agent16(const void* base, uint32_t off) {
 constexpr uint32_t kBarGroups = 16;
 constexpr uint32_t kBarLine = 16;  // 64-bit words per 128-byte line
 
-__device__ __forceinline__ void grid_barrier(const HeadArgs& a, uint32_t j, bool wait) {
+__device__ __forceinline__ void grid_barrier(const HeadArgs& a, uint64_t epoch, uint32_t j,
+                                             bool wait) {
   __builtin_amdgcn_s_waitcnt(0x0F70);
   __syncthreads();
   if (threadIdx.x == 0) {
     const uint32_t nb = a.nblk, grp = blockIdx.x % kBarGroups;
     const uint32_t ngrp = min(nb, kBarGroups);
     const uint64_t gsize = nb / kBarGroups + (grp < nb % kBarGroups ? 1u : 0u);
-    const uint64_t phase = 2ull * a.epoch + j;
+    const uint64_t phase = 2ull * epoch + j;
     unsigned long long* cnt = a.bar + kBarLine * (1 + grp);
     unsigned long long* root = a.bar;
     unsigned long long* flag = a.bar + kBarLine * (1 + kBarGroups);
@@ -799,7 +822,7 @@ __device__ __forceinline__ void grid_barrier(const HeadArgs& a, uint32_t j, bool
       const unsigned long long* f = flag + kBarLine * grp;
       for (uint32_t n = 0; ld_agent(f) < phase; ++n) {
         if (n == a.wait_limit) {
-          atomicMax(a.fault, (unsigned long long)a.epoch + 1ull);
+          atomicMax(a.fault, (unsigned long long)epoch + 1ull);
           break;
         }
         __builtin_amdgcn_s_sleep(1);
@@ -911,7 +934,13 @@ __global__ __launch_bounds__(kFuseThreads) void k_head_fused(const HeadArgs a) {
   const uint32_t nt = (a.V + 15) >> 4;
   const uint32_t t_lo = (uint32_t)((uint64_t)nt * b / nblk);
   const uint32_t t_hi = (uint32_t)((uint64_t)nt * (b + 1) / nblk);
-  if (tid == 0) s_next = t_lo;
+  // The epoch is read now and first used at the first barrier (thread 0
+  // takes part in both); the other threads get it through LDS there.
+  uint64_t ep = 0;
+  if (tid == 0) {
+    s_next = t_lo;
+    ep = call_epoch(a);
+  }
   __syncthreads();
   __bf16* st = stage[wave];
   int hoff = r * STRIDE + 8 * g;
@@ -977,7 +1006,9 @@ __global__ __launch_bounds__(kFuseThreads) void k_head_fused(const HeadArgs a) {
     st_agent(a.bhi + (size_t)tid * nblk + b, m == -INFINITY ? 0u : f2key(m));
     st_agent(a.bsum + (size_t)tid * nblk + b, __float_as_uint(s));
   }
-  grid_barrier(a, 1, true);
+  if (tid == 0) s_top[0] = ep;  // s_top is next written in phase D
+  grid_barrier(a, ep, 1, true);
+  ep = s_top[0];
 
   // B. Per row, the smallest of G group maxima (high key words; 0 for a
   // block without logits), G the least power of two >= K (G >= K groups
@@ -1088,16 +1119,20 @@ __global__ __launch_bounds__(kFuseThreads) void k_head_fused(const HeadArgs a) {
   asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
   if ((uint32_t)tid < B)
     st_agent(a.cand + ((size_t)tid * nblk + b) * a.ccap, (uint64_t)s_cnt[tid]);
-  grid_barrier(a, 2, b < B);
-  if (b >= B) return;
+  grid_barrier(a, ep, 2, b < B);
+  if (b >= B) {
+    leave_call(a);
+    return;
+  }
 
   // D. Row b.
   const uint32_t row = b;
-  if (ld_agent((const unsigned long long*)a.fault) == (unsigned long long)a.epoch + 1ull) {
+  if (ld_agent((const unsigned long long*)a.fault) == (unsigned long long)ep + 1ull) {
     for (uint32_t i = tid; i < K; i += kFuseThreads) {
       a.top_ids[(size_t)row * K + i] = -1;
       a.top_prob[(size_t)row * K + i] = 0.f;
     }
+    leave_call(a);
     return;
   }
   // Segment t of the row: word 0 its number of keys, words 1.. the keys.
@@ -1246,6 +1281,7 @@ __global__ __launch_bounds__(kFuseThreads) void k_head_fused(const HeadArgs a) {
     a.top_ids[(size_t)row * K + rank] = (int32_t)(0xFFFFFFFFu - (uint32_t)key);
     a.top_prob[(size_t)row * K + rank] = expf(key2f((uint32_t)(key >> 32)) - M) * invS;
   }
+  leave_call(a);
 }
 
 }  // namespace

@@ -22,14 +22,13 @@ struct tfe_head {
   uint64_t* d_tkey = nullptr; // [rows x tiles rounded up to 16]
   float* d_tsum = nullptr;    // [rows x tiles rounded up to 16]
   uint64_t* d_bmax = nullptr; // [rows x compute units]
-  // Scratch of the one-launch path (calls of at most 64 rows outside graph
-  // capture, when the device can launch it): barrier counter and fault word,
+  // Scratch of the one-launch path (calls of at most 64 rows, also under
+  // capture, when the device can launch it): barrier counters, call epoch and fault word,
   // per (row, block) maxima, sums and candidate counts, then the candidate
   // segments (ccap keys per row and block).
   unsigned char* d_fuse = nullptr;
   bool fused = false;
   uint32_t ccap = 0;
-  uint64_t epoch = 0;  // one-launch calls enqueued so far (barrier targets)
   // Recorded after every top-K call made outside graph capture; freeing the
   // head waits for it (and for nothing else on the device).
   hipEvent_t ev_last = nullptr;
@@ -116,6 +115,7 @@ void fuse_args(const tfe_head* h, HeadArgs* a) {
   unsigned char* p = h->d_fuse;
   const size_t n = fuse_words((uint32_t)h->cus);
   a->bar = (unsigned long long*)p;
+  a->ectl = (unsigned long long*)(p + 4352);  // 16 lines after the barrier's 33
   a->fault = (unsigned long long*)(p + kFuseCtl - 128);
   a->bhi = (uint32_t*)(p + kFuseCtl);
   a->bsum = a->bhi + n;
@@ -244,18 +244,17 @@ tfe_status topk(tfe_head* h, const void* hidden, int32_t B, int32_t K, int32_t* 
   a.nblk = (uint32_t)h->cus;
   hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
   HEAD_HIP(hipStreamIsCapturing(stream, &cs), "hipStreamIsCapturing");
-  if (h->fused && cs == hipStreamCaptureStatusNone && head_fused_fits(a) &&
-      h->device < kOrderDevices) {
+  if (h->fused && head_fused_fits(a) && h->device < kOrderDevices) {
     fuse_args(h, &a);
-    a.epoch = h->epoch;
     a.wait_limit = kHeadWaitLimit;
     if (const char* wl = getenv("TFE_HEAD_WAIT_LIMIT")) a.wait_limit = (uint32_t)strtoul(wl, nullptr, 0);
-    // The epoch counts launched calls (the barrier targets), whatever follows.
-    return fused_in_order(h, stream, [&] {
-      const hipError_t e = launch_head_fused(a, stream);
-      if (e == hipSuccess) ++h->epoch;
-      return e;
-    });
+    // Captured: the graph's edges order the call (the call epoch is kept on
+    // the device, so replays stay aligned).
+    if (cs != hipStreamCaptureStatusNone) {
+      HEAD_HIP(launch_head_fused(a, stream), "head launch");
+      return TFE_OK;
+    }
+    return fused_in_order(h, stream, [&] { return launch_head_fused(a, stream); });
   }
   HEAD_HIP(launch_head_logits(a, stream), "head logits launch");
   HEAD_HIP(launch_head_rows(a, stream), "head top-K launch");

@@ -11,7 +11,8 @@ selection first narrows in memory), the largest logits clustered in a few
 blocks, vocabularies smaller than one tile per block, and every width.
 Many calls in a row on one head, and calls of two heads interleaved on
 one stream, check that the grid barriers' counters stay aligned; calls of
-two heads on two streams without synchronisation run one after another; a
+two heads on two streams without synchronisation run one after another;
+calls captured in a HIP graph replay correctly between eager calls; a
 call
 whose barrier waits are forced to give up (TFE_HEAD_WAIT_LIMIT=0) answers
 -1 and leaves the head working."""
@@ -170,6 +171,56 @@ def test_two_heads_on_two_streams_without_sync():
     finally:
         tfe.tfe_head_free(a)
         tfe.tfe_head_free(b)
+
+
+def test_captured_calls_replay_with_eager_calls_between():
+    """One-launch calls captured in a HIP graph (through torch's CUDA-graph
+    API).  The call epoch that the grid barriers count against lives on the
+    device, so graph replays and eager calls of the same head stay aligned
+    in any order: three calls on different inputs are captured, the graph
+    is replayed three times with eager calls of the head and eager fills of
+    the outputs between, and every output equals the two-launch kernels'."""
+    V, D, B, K = 151936, 1024, 64, 128
+    print("# captured one-launch head: V=%d D=%d B=%d K=%d" % (V, D, B, K), flush=True)
+    w, h0 = gaussian(14, V, D, B)
+    hs = [h0] + [H.to_device(synth.normal_range(14, 41 + k, 0, B, D, 1.0, synth.BF16),
+                             synth.BF16) for k in (1, 2)]
+    want = [two_launch(w, V, D, h, B, K) for h in hs]
+    head = tfe.tfe_head_create(w, V, D, B, K)
+    outs = [(torch.empty((B, K), dtype=torch.int32, device="cuda"),
+             torch.empty((B, K), dtype=torch.float32, device="cuda")) for _ in hs]
+
+    def calls():
+        s = torch.cuda.current_stream().cuda_stream
+        for h, (ids, prob) in zip(hs, outs):
+            tfe.tfe_head_topk(head, h, B, K, ids, prob, s)
+
+    try:
+        g = torch.cuda.CUDAGraph()
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            calls()  # warm-up on the capture stream
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        with torch.cuda.graph(g):
+            calls()
+        for rep in range(3):
+            for ids, prob in outs:  # eager work between replays
+                ids.fill_(-7)
+                prob.fill_(-1.0)
+            torch.cuda.synchronize()
+            g.replay()
+            torch.cuda.synchronize()
+            for (ids, prob), wnt in zip(outs, want):
+                np.testing.assert_array_equal(ids.cpu().numpy(), wnt[0])
+                np.testing.assert_allclose(prob.cpu().numpy(), wnt[1], rtol=1e-5, atol=1e-37)
+            ids, prob = one_launch(head, hs[rep], B, K)
+            np.testing.assert_array_equal(ids, want[rep][0])
+            np.testing.assert_allclose(prob, want[rep][1], rtol=1e-5, atol=1e-37)
+        del g
+    finally:
+        tfe.tfe_head_free(head)
 
 
 def test_a_barrier_wait_that_gives_up_fails_only_its_call(monkeypatch):
