@@ -93,8 +93,8 @@ MULTI_SOURCES = ("paper_2607_07388_amd/csrc/tfe_multi.hip",
 # K = 128): the one-launch k_head_fused, from the passes in
 # profiles/k_head_fused_v151936_d1024_b64_k128.md.
 PROFILED_TRAFFIC_HEAD = {
-    "sources_sha256": "be789c228281e6d7aa42a8767167bd341ff168fa11757e004ae26ebd3f124ec8",
-    "bytes_per_launch": 318404965,
+    "sources_sha256": "2ed1ecc3a03165f183f7b4fa9eb2ebc786623ed3eba5af4ceeb37768ebacd491",
+    "bytes_per_launch": 318465431,
 }
 HEAD_SOURCES = ("paper_2607_07388_amd/csrc/tfe_head.hip",
                 "paper_2607_07388_amd/csrc/tfe_head.h",
