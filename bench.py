@@ -750,6 +750,40 @@ def run_head(args):
     torch.cuda.synchronize()
     wall = time.perf_counter() - w0
     avg = e0.elapsed_time(e1) * 1e-3 / args.steps
+    # The same calls captured in a HIP graph (16 per graph, as a model step
+    # that captures its head would run them), timed after the timed region.
+    graph_us = None
+    try:
+        gcalls = 16
+
+        def gloop():
+            cs = torch.cuda.current_stream().cuda_stream
+            for k in range(gcalls):
+                h, ids, prob = sets[k % len(sets)]
+                tfe.tfe_head_topk(head, h, B, K, ids, prob, cs)
+
+        side = torch.cuda.Stream()
+        side.wait_stream(stream)
+        with torch.cuda.stream(side):
+            gloop()
+        stream.wait_stream(side)
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            gloop()
+        graph.replay()
+        torch.cuda.synchronize()
+        reps = max(1, args.steps // gcalls)
+        g0, g1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        g0.record(stream)
+        for _ in range(reps):
+            graph.replay()
+        g1.record(stream)
+        torch.cuda.synchronize()
+        graph_us = g0.elapsed_time(g1) * 1e3 / (reps * gcalls)
+        del graph
+    except RuntimeError as e:  # graphs unavailable: report without them
+        print("# graph replay skipped: %s" % e, file=sys.stderr)
     # Algorithmic bytes of one call: W once, the hidden rows, the outputs.
     nbytes = V * Dh * 2 + B * Dh * 2 + B * K * 8
     flops = 2.0 * V * Dh * B
@@ -785,6 +819,9 @@ def run_head(args):
             "avg_launch_us": avg * 1e6,
             "mfma_tflops": flops / avg / 1e12,
         },
+        "graph_replay_us_per_call": graph_us,
+        "graph_replay_frac_of_8tbs": (nbytes / (graph_us * 1e-6) / 1e9 / HBM_PEAK_GBPS
+                                      if graph_us else None),
     }
     if not args.no_cpu_baseline:
         import oracle
