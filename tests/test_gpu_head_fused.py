@@ -173,20 +173,26 @@ def test_two_heads_on_two_streams_without_sync():
         tfe.tfe_head_free(b)
 
 
-def test_captured_calls_replay_with_eager_calls_between():
-    """One-launch calls captured in a HIP graph (through torch's CUDA-graph
-    API).  The call epoch that the grid barriers count against lives on the
-    device, so graph replays and eager calls of the same head stay aligned
-    in any order: three calls on different inputs are captured, the graph
-    is replayed three times with eager calls of the head and eager fills of
-    the outputs between, and every output equals the two-launch kernels'."""
-    V, D, B, K = 151936, 1024, 64, 128
-    print("# captured one-launch head: V=%d D=%d B=%d K=%d" % (V, D, B, K), flush=True)
+@pytest.mark.parametrize("B,K", [(64, 128), (100, 64)])
+def test_captured_calls_replay_with_eager_calls_between(B, K):
+    """Head calls captured in a HIP graph (through torch's CUDA-graph API):
+    64 rows take the one-launch path, 100 rows the two launches.  The call
+    epoch that the one-launch barriers count against lives on the device, so
+    graph replays and eager calls of the same head stay aligned in any
+    order: three calls on different inputs are captured, the graph is
+    replayed three times with eager calls of the head and eager fills of the
+    outputs between, and every output equals the eager calls' (for 64 rows,
+    whose ids equal the two-launch kernels')."""
+    V, D = 151936, 1024
+    print("# captured head calls: V=%d D=%d B=%d K=%d" % (V, D, B, K), flush=True)
     w, h0 = gaussian(14, V, D, B)
     hs = [h0] + [H.to_device(synth.normal_range(14, 41 + k, 0, B, D, 1.0, synth.BF16),
                              synth.BF16) for k in (1, 2)]
-    want = [two_launch(w, V, D, h, B, K) for h in hs]
     head = tfe.tfe_head_create(w, V, D, B, K)
+    want = [one_launch(head, h, B, K) for h in hs]  # eager calls, the same path
+    if B <= 64:
+        for h, wnt in zip(hs, want):
+            np.testing.assert_array_equal(two_launch(w, V, D, h, B, K)[0], wnt[0])
     outs = [(torch.empty((B, K), dtype=torch.int32, device="cuda"),
              torch.empty((B, K), dtype=torch.float32, device="cuda")) for _ in hs]
 
