@@ -286,8 +286,10 @@ tfe_status tfe_head_create(const void *w_pref, int32_t vocab, int32_t dim, int32
  * inside the launch replace the write of the logits.  Its blocks must all
  * be resident at once: the library runs the one-launch calls of all heads
  * on a device one after another (each waits on the device for the previous
- * one, whatever its stream; in a captured graph the graph's own order
- * applies, so two such calls must not sit on parallel branches), and such
+ * one, whatever its stream; a captured call is ordered only by its graph
+ * and the stream the graph is launched on, so two such calls must not sit
+ * on parallel branches, nor run beside an eager one-launch call of another
+ * head on another stream), and such
  * a call must not overlap on the device with other work that holds compute
  * units while waiting for it.  Its waits are bounded
  * (about a second); if one runs out,
