@@ -299,7 +299,9 @@ tfe_status tfe_head_create(const void *w_pref, int32_t vocab, int32_t dim, int32
 tfe_status tfe_head_topk(tfe_head *head, const void *hidden, int32_t B, int32_t K,
                          int32_t *top_ids, float *top_prob, void *stream);
 
-/* Releases a head (waits for the device first).  NULL is accepted. */
+/* Releases a head (waits for its last call made outside stream capture
+ * first).  A captured graph that holds calls of the head must have finished
+ * running, and must not run again.  NULL is accepted. */
 tfe_status tfe_head_free(tfe_head *head);
 
 /* tfe_head_topk without a head and without any allocation, for callers that
