@@ -161,7 +161,9 @@ typedef struct {
  * pinned memory of the table until tfe_table_free. */
 tfe_status tfe_table_load(const tfe_table_desc *desc, void *stream, tfe_table **out);
 
-/* Releases a table (waits for its pending work first).  NULL is accepted. */
+/* Releases a table (waits for its pending work made outside stream capture
+ * first).  A captured graph that holds lookups of the table must have
+ * finished running, and must not run again.  NULL is accepted. */
 tfe_status tfe_table_free(tfe_table *table);
 
 /* Lookup + inject for B rows of ctx + S tokens.
