@@ -93,8 +93,8 @@ MULTI_SOURCES = ("paper_2607_07388_amd/csrc/tfe_multi.hip",
 # K = 128): the one-launch k_head_fused, from the passes in
 # profiles/k_head_fused_v151936_d1024_b64_k128.md.
 PROFILED_TRAFFIC_HEAD = {
-    "sources_sha256": "2ed1ecc3a03165f183f7b4fa9eb2ebc786623ed3eba5af4ceeb37768ebacd491",
-    "bytes_per_launch": 318465431,
+    "sources_sha256": "7b4673180138ac6e265fddd9bbf2936a9155dbb45a0f719f9ae1d65f7bc524c0",
+    "bytes_per_launch": 318459155,
 }
 HEAD_SOURCES = ("paper_2607_07388_amd/csrc/tfe_head.hip",
                 "paper_2607_07388_amd/csrc/tfe_head.h",

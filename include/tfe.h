@@ -301,6 +301,13 @@ tfe_status tfe_head_create(const void *w_pref, int32_t vocab, int32_t dim, int32
 tfe_status tfe_head_topk(tfe_head *head, const void *hidden, int32_t B, int32_t K,
                          int32_t *top_ids, float *top_prob, void *stream);
 
+/* *call = the number, counted from 1 over the head's one-launch calls, of
+ * the latest one-launch call whose barrier waits gave up (its top_ids all
+ * -1 and its top_prob 0), or 0 if none has.  Waits for the head's last call
+ * made outside stream capture first; calls replayed from a graph count like
+ * the others.  For callers that cannot read every call's ids back. */
+tfe_status tfe_head_last_fault(tfe_head *head, int64_t *call);
+
 /* Releases a head (waits for its last call made outside stream capture
  * first).  A captured graph that holds calls of the head must have finished
  * running, and must not run again.  NULL is accepted. */

@@ -265,6 +265,25 @@ tfe_status topk(tfe_head* h, const void* hidden, int32_t B, int32_t K, int32_t* 
   return TFE_OK;
 }
 
+tfe_status last_fault(tfe_head* h, int64_t* call) {
+  if (!h || !call) return fail(TFE_ERR_INVALID_ARG, "null head or output");
+  *call = 0;
+  if (!h->fused) return TFE_OK;
+  int cur = -1;
+  HEAD_HIP(hipGetDevice(&cur), "hipGetDevice");
+  if (cur != h->device)
+    return fail(TFE_ERR_INVALID_ARG, "head lives on device %d but device %d is current",
+                h->device, cur);
+  if (h->recorded) HEAD_HIP(hipEventSynchronize(h->ev_last), "head wait");
+  // The fault word holds the largest (epoch + 1) of the calls that gave up:
+  // the 1-based number of the latest such call.
+  unsigned long long f = 0;
+  HEAD_HIP(hipMemcpy(&f, h->d_fuse + kFuseCtl - 128, sizeof f, hipMemcpyDeviceToHost),
+           "head fault word");
+  *call = (int64_t)f;
+  return TFE_OK;
+}
+
 }  // namespace
 }  // namespace tfe
 
@@ -280,6 +299,11 @@ tfe_status tfe_head_topk(tfe_head* head, const void* hidden, int32_t B, int32_t 
                          int32_t* top_ids, float* top_prob, void* stream) {
   tfe::begin_call();
   return tfe::topk(head, hidden, B, K, top_ids, top_prob, (hipStream_t)stream);
+}
+
+tfe_status tfe_head_last_fault(tfe_head* head, int64_t* call) {
+  tfe::begin_call();
+  return tfe::last_fault(head, call);
 }
 
 tfe_status tfe_head_free(tfe_head* head) {

@@ -99,6 +99,7 @@ def _load():
         "tfe_head_create": ([vp, i32, i32, i32, i32, ctypes.POINTER(vp)], ctypes.c_int),
         "tfe_head_topk": ([vp, vp, i32, i32, vp, vp, vp], ctypes.c_int),
         "tfe_head_free": ([vp], ctypes.c_int),
+        "tfe_head_last_fault": ([vp, ctypes.POINTER(i64)], ctypes.c_int),
         "tfe_head_topk_noalloc": ([vp, i32, i32, vp, i32, i32, vp, vp, vp], ctypes.c_int),
         "tfe_ngram_release": ([], ctypes.c_int),
         "tfe_ngram_top": ([vp, i64, i32, i32, i64, i64, vp, vp, ctypes.POINTER(i64), vp],
@@ -125,7 +126,7 @@ lib = _load()
 EXPORTED = ("tfe_table_load", "tfe_table_free", "tfe_lookup_inject", "tfe_lookup_inject_multi",
             "tfe_prefetch",
             "tfe_prefetch_scored", "tfe_head_create", "tfe_head_topk", "tfe_head_free",
-            "tfe_head_topk_noalloc",
+            "tfe_head_last_fault", "tfe_head_topk_noalloc",
             "tfe_ngram_top", "tfe_ngram_release",
             "tfe_get_stats", "tfe_reset_stats", "tfe_residency", "tfe_last_error",
             "tfe_memory_held", "tfe_index_capacity",
@@ -224,6 +225,13 @@ def tfe_head_topk_noalloc(w_pref, vocab, dim, hidden, B, K, top_ids, top_prob, s
 
 def tfe_head_free(head):
     return _check(lib.tfe_head_free(head))
+
+
+def tfe_head_last_fault(head):
+    """Number (from 1) of the head's latest one-launch call that gave up, or 0."""
+    n = ctypes.c_int64()
+    _check(lib.tfe_head_last_fault(head, ctypes.byref(n)))
+    return n.value
 
 
 def tfe_ngram_top(tokens, n_tokens, vocab, n, skip, top, out_tuples, out_counts, stream=None):

@@ -233,8 +233,9 @@ def test_a_barrier_wait_that_gives_up_fails_only_its_call(monkeypatch):
     """The one-launch barriers' waits are bounded; TFE_HEAD_WAIT_LIMIT=0
     makes every wait give up at once (forced from the host: every block
     still arrives, so no kernel waits forever).  That call answers every row
-    with id -1 and probability 0; the next call on the same head, with the
-    default limit, is correct again (the barrier counters stayed aligned)."""
+    with id -1 and probability 0, and tfe_head_last_fault names it; the next
+    calls on the same head, with the default limit, are correct again (the
+    barrier counters stayed aligned) and leave the fault record as it was."""
     V, D, B, K = 40000, 1024, 64, 64
     w, h = gaussian(11, V, D, B)
     want = two_launch(w, V, D, h, B, K)
@@ -242,13 +243,16 @@ def test_a_barrier_wait_that_gives_up_fails_only_its_call(monkeypatch):
     try:
         ids, prob = one_launch(head, h, B, K)
         np.testing.assert_array_equal(ids, want[0])
+        assert tfe.tfe_head_last_fault(head) == 0
         monkeypatch.setenv("TFE_HEAD_WAIT_LIMIT", "0")
         ids, prob = one_launch(head, h, B, K)
         assert np.all(ids == -1) and np.all(prob == 0)
+        assert tfe.tfe_head_last_fault(head) == 2  # the second one-launch call
         monkeypatch.delenv("TFE_HEAD_WAIT_LIMIT")
         for _ in range(3):
             ids, prob = one_launch(head, h, B, K)
             np.testing.assert_array_equal(ids, want[0])
             np.testing.assert_allclose(prob, want[1], rtol=1e-5, atol=1e-37)
+        assert tfe.tfe_head_last_fault(head) == 2
     finally:
         tfe.tfe_head_free(head)
